@@ -1,0 +1,16 @@
+"""MI355X (gfx950) hot path of distributed deep Q-learning (arXiv 1508.04186).
+
+Thin Python binding over libdqn.so: the same entry points as the C ABI in
+include/dqn.h (replay_gather, dqn_forward, dqn_td_gradient, ps_apply_update
+and the layout/workspace queries), with torch tensors for device memory and
+streams.  All arithmetic runs in the library's HIP kernels; there is no CPU
+or PyTorch fallback, and loading fails loudly when the library is missing.
+"""
+from .native import (  # noqa: F401
+    DQN_OK, DQN_EINVAL, DQN_EWORKSPACE, DQN_EHIP, DQN_EUNSUPPORTED,
+    PS_SGD, PS_RMSPROP, PS_ADAGRAD, DQN_OP_FORWARD, DQN_OP_TD_GRADIENT,
+    DqnError, Net, NET_SMALL, NET_LARGE, Replay,
+    lib, lib_path, dqn_param_count, dqn_param_offset, dqn_workspace_bytes,
+    replay_gather, dqn_forward, dqn_td_gradient, ps_apply_update, dqn_status_string,
+    workspace,
+)

@@ -1,0 +1,389 @@
+// C ABI of libdqn.so (declared in include/dqn.h): argument checks, the
+// workspace layout and the kernel sequence of each entry point.
+#include <algorithm>
+#include <cmath>
+#include <cstddef>
+
+#include "common.h"
+#include "dqn.h"
+
+using namespace dqn;
+
+namespace {
+
+struct NetInfo {
+    int n_conv;
+    ConvId conv[3];
+    ConvDims d[3];
+    int H, A, flat;
+    int64_t P;
+    int64_t w_off[5], b_off[5];  // conv layers, then fc1, fc2
+};
+
+// Only the two network shapes the kernels are built for are accepted.
+int identify(const dqn_net* net, NetInfo* ni) {
+    if (!net) return DQN_EINVAL;
+    if (net->precision != DQN_FP32) return DQN_EUNSUPPORTED;
+    if (net->in_c != 4 || net->in_h != 84 || net->in_w != 84) return DQN_EUNSUPPORTED;
+    if (net->n_conv == 2 && net->conv_out[0] == 16 && net->conv_k[0] == 8 && net->conv_stride[0] == 4 &&
+        net->conv_out[1] == 32 && net->conv_k[1] == 4 && net->conv_stride[1] == 2 &&
+        net->fc_hidden == 256 && net->n_actions == 6) {
+        ni->n_conv = 2;
+        ni->conv[0] = CONV_S1;
+        ni->conv[1] = CONV_S2;
+        ni->H = 256;
+        ni->A = 6;
+    } else if (net->n_conv == 3 && net->conv_out[0] == 32 && net->conv_k[0] == 8 &&
+               net->conv_stride[0] == 4 && net->conv_out[1] == 64 && net->conv_k[1] == 4 &&
+               net->conv_stride[1] == 2 && net->conv_out[2] == 64 && net->conv_k[2] == 3 &&
+               net->conv_stride[2] == 1 && net->fc_hidden == 512 && net->n_actions == 18) {
+        ni->n_conv = 3;
+        ni->conv[0] = CONV_L1;
+        ni->conv[1] = CONV_L2;
+        ni->conv[2] = CONV_L3;
+        ni->H = 512;
+        ni->A = 18;
+    } else {
+        return DQN_EUNSUPPORTED;
+    }
+    int64_t off = 0;
+    for (int l = 0; l < ni->n_conv; ++l) {
+        ni->d[l] = conv_dims(ni->conv[l]);
+        const ConvDims& c = ni->d[l];
+        ni->w_off[l] = off;
+        off += (int64_t)c.cout * c.cin * c.k * c.k;
+        ni->b_off[l] = off;
+        off += c.cout;
+    }
+    const ConvDims& last = ni->d[ni->n_conv - 1];
+    ni->flat = last.cout * last.oh * last.ow;
+    const int L = ni->n_conv;
+    ni->w_off[L] = off;
+    off += (int64_t)ni->H * ni->flat;
+    ni->b_off[L] = off;
+    off += ni->H;
+    ni->w_off[L + 1] = off;
+    off += (int64_t)ni->A * ni->H;
+    ni->b_off[L + 1] = off;
+    off += ni->A;
+    ni->P = off;
+    return DQN_OK;
+}
+
+inline int64_t act_elems(const ConvDims& c) { return (int64_t)c.cout * c.oh * c.ow; }
+
+// fc1 forward split-K: enough slices that the launch covers the chip.
+void fc1_split(int rows, int H, int K, int* ks, int* kchunk) {
+    const int tiles = ((rows + 63) / 64) * ((H + 63) / 64);
+    int want = std::max(1, 256 / tiles);
+    want = std::min(want, std::max(1, K / 64));
+    int kc = (K + want - 1) / want;
+    kc = (kc + 15) / 16 * 16;
+    *kchunk = kc;
+    *ks = (K + kc - 1) / kc;
+}
+
+struct Carver {
+    size_t off = 0;
+    template <class T>
+    T* take(void* base, int64_t count) {
+        T* p = base ? (T*)((char*)base + off) : nullptr;
+        off += ((size_t)count * sizeof(T) + 255) / 256 * 256;
+        return p;
+    }
+};
+
+struct TdLayout {
+    float* act[3];
+    float* fc1p;
+    float *h1s, *dz1, *delta, *lossj;
+    float* dconv[3];
+    float* wpart[3];
+    float* bpart[3];
+    int chunks[3];
+    int ks, kchunk;
+    size_t bytes;
+};
+
+TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
+    TdLayout t{};
+    Carver cv;
+    const int n2 = 2 * B;
+    for (int l = 0; l < ni.n_conv; ++l) t.act[l] = cv.take<float>(ws, (int64_t)n2 * act_elems(ni.d[l]));
+    fc1_split(n2, ni.H, ni.flat, &t.ks, &t.kchunk);
+    t.fc1p = cv.take<float>(ws, (int64_t)t.ks * n2 * ni.H);
+    t.h1s = cv.take<float>(ws, (int64_t)B * ni.H);
+    t.dz1 = cv.take<float>(ws, (int64_t)B * ni.H);
+    t.delta = cv.take<float>(ws, B);
+    t.lossj = cv.take<float>(ws, B);
+    for (int l = 0; l < ni.n_conv; ++l) t.dconv[l] = cv.take<float>(ws, (int64_t)B * act_elems(ni.d[l]));
+    for (int l = 0; l < ni.n_conv; ++l) {
+        const ConvDims& c = ni.d[l];
+        t.chunks[l] = conv_wgrad_chunks(ni.conv[l], B);
+        t.wpart[l] = cv.take<float>(ws, (int64_t)t.chunks[l] * c.cout * c.cin * c.k * c.k);
+        t.bpart[l] = cv.take<float>(ws, (int64_t)t.chunks[l] * c.cout);
+    }
+    t.bytes = cv.off;
+    return t;
+}
+
+struct FwdLayout {
+    float* act[3];
+    float* fc1p;
+    int ks, kchunk;
+    size_t bytes;
+};
+
+FwdLayout fwd_layout(const NetInfo& ni, int B, void* ws) {
+    FwdLayout f{};
+    Carver cv;
+    for (int l = 0; l < ni.n_conv; ++l) f.act[l] = cv.take<float>(ws, (int64_t)B * act_elems(ni.d[l]));
+    fc1_split(B, ni.H, ni.flat, &f.ks, &f.kchunk);
+    f.fc1p = cv.take<float>(ws, (int64_t)f.ks * B * ni.H);
+    f.bytes = cv.off;
+    return f;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const char* pa = (const char*)a;
+    const char* pb = (const char*)b;
+    return pa < pb + nb && pb < pa + na;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+#define HIP_TRY(expr)                              \
+    do {                                           \
+        if ((expr) != hipSuccess) return DQN_EHIP; \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* dqn_status_string(int status) {
+    switch (status) {
+        case DQN_OK: return "ok";
+        case DQN_EINVAL: return "invalid argument";
+        case DQN_EWORKSPACE: return "workspace too small";
+        case DQN_EHIP: return "HIP launch failed";
+        case DQN_EUNSUPPORTED: return "unsupported network";
+        default: return "unknown status";
+    }
+}
+
+int64_t dqn_param_count(const dqn_net* net) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    return rc != DQN_OK ? rc : ni.P;
+}
+
+int64_t dqn_param_offset(const dqn_net* net, int32_t layer, int32_t is_bias) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (layer < 0 || layer > ni.n_conv + 1) return DQN_EINVAL;
+    return is_bias ? ni.b_off[layer] : ni.w_off[layer];
+}
+
+int64_t dqn_workspace_bytes(const dqn_net* net, int32_t batch, int32_t op) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (batch <= 0) return DQN_EINVAL;
+    if (op == DQN_OP_FORWARD) return (int64_t)fwd_layout(ni, batch, nullptr).bytes;
+    if (op == DQN_OP_TD_GRADIENT) return (int64_t)td_layout(ni, batch, nullptr).bytes;
+    return DQN_EINVAL;
+}
+
+int replay_gather(const dqn_replay* rp, const int64_t* idx, int32_t batch, uint8_t* s_out,
+                  uint8_t* s_next_out, int32_t* a_out, float* r_out, uint8_t* term_out,
+                  void* stream) {
+    if (!rp || !idx || !s_out || batch <= 0) return DQN_EINVAL;
+    if (!rp->frames || rp->c <= 0 || rp->h <= 0 || rp->w <= 0) return DQN_EINVAL;
+    const int64_t rec = (int64_t)rp->c * rp->h * rp->w;
+    if (rec % 16 != 0 || rp->record_stride < rec || rp->record_stride % 16 != 0) return DQN_EINVAL;
+    if (!aligned(rp->frames, 16) || !aligned(s_out, 16) || (s_next_out && !aligned(s_next_out, 16)))
+        return DQN_EINVAL;
+    if (rp->size < (s_next_out ? 2 : 1)) return DQN_EINVAL;
+    if ((a_out && !rp->action) || (r_out && !rp->reward) || (term_out && !rp->terminal))
+        return DQN_EINVAL;
+    if (batch > 65535) return DQN_EINVAL;
+    HIP_TRY(launch_gather(rp->frames, rp->record_stride, rec, rp->action, rp->reward, rp->terminal,
+                          idx, batch, s_out, s_next_out, a_out, r_out, term_out,
+                          (hipStream_t)stream));
+    return DQN_OK;
+}
+
+int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, int32_t batch,
+                float epsilon, const uint64_t* draws, float* q_out, int32_t* action_out, void* ws,
+                size_t ws_bytes, void* stream) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (!theta || !states || batch <= 0 || !ws) return DQN_EINVAL;
+    if (!(epsilon >= 0.f && epsilon <= 1.f)) return DQN_EINVAL;
+    const double te = std::floor((double)epsilon * 4294967296.0);
+    const uint64_t thresh = te >= 4294967296.0 ? 4294967296ull : (uint64_t)te;
+    if (thresh > 0 && !draws) return DQN_EINVAL;
+    if (!aligned(ws, 256) || !aligned(theta, 16) || !aligned(states, 16)) return DQN_EINVAL;
+    FwdLayout f = fwd_layout(ni, batch, nullptr);
+    if (ws_bytes < f.bytes) return DQN_EWORKSPACE;
+    f = fwd_layout(ni, batch, ws);
+    hipStream_t st = (hipStream_t)stream;
+    const float* th = theta;
+    for (int l = 0; l < ni.n_conv; ++l) {
+        const void* in = l == 0 ? (const void*)states : (const void*)f.act[l - 1];
+        const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
+        HIP_TRY(launch_conv_fwd(ni.conv[l], in, in, batch, batch, th + ni.w_off[l], th + ni.b_off[l],
+                                th + ni.w_off[l], th + ni.b_off[l], f.act[l], scale, st));
+    }
+    const int L = ni.n_conv;
+    HIP_TRY(launch_gemm(GEMM_NT, batch, ni.H, ni.flat, f.act[L - 1], ni.flat, th + ni.w_off[L],
+                        ni.flat, f.fc1p, ni.H, f.ks, f.kchunk, (int64_t)batch * ni.H, nullptr, st));
+    HeadFwdArgs h{};
+    h.fc1p = f.fc1p;
+    h.ks = f.ks;
+    h.B = batch;
+    h.b1 = th + ni.b_off[L];
+    h.W2 = th + ni.w_off[L + 1];
+    h.b2 = th + ni.b_off[L + 1];
+    h.thresh = thresh;
+    h.draws = draws;
+    h.q_out = q_out;
+    h.action_out = action_out;
+    HIP_TRY(launch_head_fwd(ni.H, ni.A, h, st));
+    return DQN_OK;
+}
+
+int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_target,
+                    const uint8_t* s, const uint8_t* s_next, const int32_t* action,
+                    const float* reward, const uint8_t* terminal, int32_t batch, float gamma,
+                    float* grad_out, float* loss_out, float* q_out, float* y_out, void* ws,
+                    size_t ws_bytes, void* stream) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (!theta || !s || !s_next || !action || !reward || !terminal || !grad_out || !loss_out || !ws)
+        return DQN_EINVAL;
+    if (batch <= 0 || !std::isfinite(gamma)) return DQN_EINVAL;
+    const float* tt = theta_target ? theta_target : theta;
+    const size_t pbytes = (size_t)ni.P * sizeof(float);
+    if (overlaps(grad_out, pbytes, theta, pbytes) || overlaps(grad_out, pbytes, tt, pbytes))
+        return DQN_EINVAL;
+    if (!aligned(ws, 256) || !aligned(theta, 16) || !aligned(tt, 16) || !aligned(grad_out, 16) ||
+        !aligned(s, 16) || !aligned(s_next, 16))
+        return DQN_EINVAL;
+    TdLayout t = td_layout(ni, batch, nullptr);
+    if (ws_bytes < t.bytes) return DQN_EWORKSPACE;
+    t = td_layout(ni, batch, ws);
+    hipStream_t st = (hipStream_t)stream;
+    const int B = batch, L = ni.n_conv;
+    const float* th = theta;
+
+    // Forward of s under theta (samples 0..B-1) and of s' under theta^-
+    // (samples B..2B-1), one launch per layer.
+    for (int l = 0; l < L; ++l) {
+        const void* in_a = l == 0 ? (const void*)s : (const void*)t.act[l - 1];
+        const void* in_b = l == 0 ? (const void*)s_next
+                                  : (const void*)(t.act[l - 1] + (int64_t)B * act_elems(ni.d[l - 1]));
+        const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
+        HIP_TRY(launch_conv_fwd(ni.conv[l], in_a, in_b, B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
+                                tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], scale, st));
+    }
+    const float* xlast = t.act[L - 1];
+    const int64_t slice = (int64_t)2 * B * ni.H;
+    if (tt == th) {
+        HIP_TRY(launch_gemm(GEMM_NT, 2 * B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
+                            t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, st));
+    } else {
+        HIP_TRY(launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
+                            t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, st));
+        HIP_TRY(launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast + (int64_t)B * ni.flat, ni.flat,
+                            tt + ni.w_off[L], ni.flat, t.fc1p + (int64_t)B * ni.H, ni.H, t.ks,
+                            t.kchunk, slice, nullptr, st));
+    }
+    HeadTdArgs h{};
+    h.fc1p = t.fc1p;
+    h.ks = t.ks;
+    h.B = B;
+    h.b1 = th + ni.b_off[L];
+    h.b1t = tt + ni.b_off[L];
+    h.W2 = th + ni.w_off[L + 1];
+    h.b2 = th + ni.b_off[L + 1];
+    h.W2t = tt + ni.w_off[L + 1];
+    h.b2t = tt + ni.b_off[L + 1];
+    h.action = action;
+    h.reward = reward;
+    h.terminal = terminal;
+    h.gamma = gamma;
+    h.h1s = t.h1s;
+    h.dz1 = t.dz1;
+    h.delta = t.delta;
+    h.lossj = t.lossj;
+    h.q_out = q_out;
+    h.y_out = y_out;
+    HIP_TRY(launch_head_td(ni.H, ni.A, h, st));
+
+    // fc1: weight gradient and the masked gradient of the last conv output.
+    HIP_TRY(launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat,
+                        grad_out + ni.w_off[L], ni.flat, 1, (B + 15) / 16 * 16, 0, nullptr, st));
+    HIP_TRY(launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
+                        t.dconv[L - 1], ni.flat, 1, (ni.H + 15) / 16 * 16, 0, xlast, st));
+    // conv layers, last to first
+    for (int l = L - 1; l >= 0; --l) {
+        const void* in = l == 0 ? (const void*)s : (const void*)t.act[l - 1];
+        const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
+        HIP_TRY(launch_conv_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
+        if (l > 0)
+            HIP_TRY(launch_conv_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],
+                                      t.dconv[l - 1], B, st));
+    }
+    FinalizeArgs fa{};
+    fa.n_conv = L;
+    for (int l = 0; l < L; ++l) {
+        const ConvDims& c = ni.d[l];
+        fa.wpart[l] = t.wpart[l];
+        fa.bpart[l] = t.bpart[l];
+        fa.chunks[l] = t.chunks[l];
+        fa.wcount[l] = c.cout * c.cin * c.k * c.k;
+        fa.cout[l] = c.cout;
+        fa.gw[l] = grad_out + ni.w_off[l];
+        fa.gb[l] = grad_out + ni.b_off[l];
+    }
+    fa.dz1 = t.dz1;
+    fa.h1s = t.h1s;
+    fa.delta = t.delta;
+    fa.lossj = t.lossj;
+    fa.action = action;
+    fa.B = B;
+    fa.H = ni.H;
+    fa.A = ni.A;
+    fa.g_b1 = grad_out + ni.b_off[L];
+    fa.g_W2 = grad_out + ni.w_off[L + 1];
+    fa.g_b2 = grad_out + ni.b_off[L + 1];
+    fa.loss_out = loss_out;
+    HIP_TRY(launch_finalize(fa, st));
+    return DQN_OK;
+}
+
+int ps_apply_update(int32_t rule, const float* theta_in, float* theta_out, float* state,
+                    const float* grad, int64_t n, float lr, float decay, float eps, void* stream) {
+    if (rule != PS_SGD && rule != PS_RMSPROP && rule != PS_ADAGRAD) return DQN_EINVAL;
+    if (!theta_in || !theta_out || !grad || n <= 0) return DQN_EINVAL;
+    if (rule != PS_SGD && !state) return DQN_EINVAL;
+    if (!aligned(theta_in, 16) || !aligned(theta_out, 16) || !aligned(grad, 16) ||
+        (state && !aligned(state, 16)))
+        return DQN_EINVAL;
+    const size_t nb = (size_t)n * sizeof(float);
+    if (theta_out != theta_in && overlaps(theta_out, nb, theta_in, nb)) return DQN_EINVAL;
+    if (overlaps(grad, nb, theta_out, nb) || (state && overlaps(grad, nb, state, nb)) ||
+        (state && overlaps(state, nb, theta_out, nb)))
+        return DQN_EINVAL;
+    if (!std::isfinite(lr) || !std::isfinite(decay) || !std::isfinite(eps)) return DQN_EINVAL;
+    HIP_TRY(launch_apply(rule, theta_in, theta_out, state, grad, n, lr, decay, eps,
+                         (hipStream_t)stream));
+    return DQN_OK;
+}
+
+}  // extern "C"

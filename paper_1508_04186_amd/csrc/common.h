@@ -1,0 +1,118 @@
+// Internal declarations shared by the translation units of libdqn.so.
+// Target: gfx950 (CDNA4), wave64.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dqn {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+// One v_mfma_f32_16x16x4_f32: D[16x16] += A[16x4] * B[4x16] over a wave.
+// Lane l supplies A[l%16][l/16] and B[l/16][l%16]; it holds
+// D[4*(l/16) + r][l%16] in element r of the accumulator.
+__device__ __forceinline__ f4 mfma16x16x4(float a, float b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+    return v;
+}
+
+// The convolution layers the library is built for (valid padding).
+enum ConvId { CONV_S1 = 0, CONV_S2 = 1, CONV_L1 = 2, CONV_L2 = 3, CONV_L3 = 4, CONV_COUNT = 5 };
+
+struct ConvDims {
+    int cin, ih, iw, cout, k, s, oh, ow;
+};
+
+inline ConvDims conv_dims(ConvId id) {
+    switch (id) {
+        case CONV_S1: return {4, 84, 84, 16, 8, 4, 20, 20};
+        case CONV_S2: return {16, 20, 20, 32, 4, 2, 9, 9};
+        case CONV_L1: return {4, 84, 84, 32, 8, 4, 20, 20};
+        case CONV_L2: return {32, 20, 20, 64, 4, 2, 9, 9};
+        default:      return {64, 9, 9, 64, 3, 1, 7, 7};
+    }
+}
+
+// ---- launchers (host side); every one returns hipGetLastError() ----------
+
+// Forward convolution + bias + ReLU for n samples.  Samples j < n_a read
+// in_a[j] and use (w_a, b_a); samples j >= n_a read in_b[j - n_a] and use
+// (w_b, b_b).  Output float [n][cout][oh][ow].  in_scale multiplies the
+// accumulated products before the bias (1/255 for byte input).
+hipError_t launch_conv_fwd(ConvId id, const void* in_a, const void* in_b, int n_a, int n,
+                           const float* w_a, const float* b_a, const float* w_b, const float* b_b,
+                           float* out, float in_scale, hipStream_t st);
+
+// Weight and bias gradient partial sums over sample chunks:
+// wpart [chunks][cout][cin*k*k], bpart [chunks][cout].
+int conv_wgrad_chunks(ConvId id, int batch);
+hipError_t launch_conv_wgrad(ConvId id, const void* in, const float* dz, int batch, float* wpart,
+                             float* bpart, float in_scale, hipStream_t st);
+
+// Input gradient din = (W^T * dz) masked by [h_in > 0], float [n][cin][ih][iw].
+hipError_t launch_conv_dgrad(ConvId id, const float* dz, const float* w, const float* h_in,
+                             float* din, int batch, hipStream_t st);
+
+// C = A * B over fp32 MFMA tiles.  A(m,k) = ta ? A[k*lda+m] : A[m*lda+k];
+// B(k,n) = tb ? B[n*ldb+k] : B[k*ldb+n].  Split-K: slice z covers
+// k in [z*kchunk, min(K,(z+1)*kchunk)) and writes C + z*c_slice.
+// With mask != NULL: C = acc * [mask[m*ldc+n] > 0].
+enum GemmKind { GEMM_NT = 0, GEMM_TN = 1, GEMM_NN = 2 };
+hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
+                       int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
+                       const float* mask, hipStream_t st);
+
+struct HeadTdArgs {
+    const float* fc1p;   // [ks][2B][H] split-K partials of fc1 (rows < B: s, >= B: s')
+    int ks, B;
+    const float *b1, *b1t, *W2, *b2, *W2t, *b2t;
+    const int32_t* action;
+    const float* reward;
+    const uint8_t* terminal;
+    float gamma;
+    float *h1s, *dz1, *delta, *lossj, *q_out, *y_out;
+};
+hipError_t launch_head_td(int H, int A, const HeadTdArgs& a, hipStream_t st);
+
+struct HeadFwdArgs {
+    const float* fc1p;   // [ks][B][H]
+    int ks, B;
+    const float *b1, *W2, *b2;
+    uint64_t thresh;     // explore iff (draw >> 32) < thresh
+    const uint64_t* draws;
+    float* q_out;
+    int32_t* action_out;
+};
+hipError_t launch_head_fwd(int H, int A, const HeadFwdArgs& a, hipStream_t st);
+
+struct FinalizeArgs {
+    int n_conv;
+    const float* wpart[3];
+    const float* bpart[3];
+    int chunks[3];
+    int wcount[3];
+    int cout[3];
+    float* gw[3];
+    float* gb[3];
+    const float *dz1, *h1s, *delta, *lossj;
+    const int32_t* action;
+    int B, H, A;
+    float *g_b1, *g_W2, *g_b2, *loss_out;
+};
+hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t st);
+
+hipError_t launch_gather(const uint8_t* frames, int64_t stride, int64_t rec_bytes,
+                         const uint8_t* act, const int8_t* rew, const uint8_t* term,
+                         const int64_t* idx, int batch, uint8_t* s, uint8_t* sn, int32_t* a,
+                         float* r, uint8_t* t, hipStream_t st);
+
+hipError_t launch_apply(int rule, const float* th_in, float* th_out, float* state, const float* g,
+                        int64_t n, float lr, float decay, float eps, hipStream_t st);
+
+}  // namespace dqn

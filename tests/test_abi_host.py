@@ -1,0 +1,198 @@
+"""Host-side checks of the C ABI: the library loads, exports every function
+that include/dqn.h declares, reports the documented layout, and rejects bad
+arguments with the documented status before enqueueing anything.  No kernel
+is launched here; these run without a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import dqn_inputs as di
+import paper_1508_04186_amd as dq
+from paper_1508_04186_amd import native
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    txt = open(os.path.join(ROOT, "include", "dqn.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(\w+)\s*\(", txt, flags=re.M)))
+
+
+def test_header_declares_the_four_calls():
+    fns = header_functions()
+    for f in ("replay_gather", "dqn_forward", "dqn_td_gradient", "ps_apply_update",
+              "dqn_param_count", "dqn_param_offset", "dqn_workspace_bytes", "dqn_status_string"):
+        assert f in fns
+
+
+def test_library_exports_every_declared_symbol():
+    L = dq.lib()
+    for f in header_functions():
+        assert hasattr(L, f), f
+    # extern "C": no mangled names needed
+    assert isinstance(ctypes.cast(L.dqn_forward, ctypes.c_void_p).value, int)
+
+
+@pytest.mark.parametrize("net,shape", [(dq.NET_SMALL, di.NET_S), (dq.NET_LARGE, di.NET_L)])
+def test_param_layout_matches_documentation(net, shape):
+    assert dq.dqn_param_count(net) == shape.param_count()
+    sl = shape.slices()
+    L = len(net.conv)
+    for l in range(L):
+        assert dq.dqn_param_offset(net, l, False) == sl[f"conv{l+1}.W"][0]
+        assert dq.dqn_param_offset(net, l, True) == sl[f"conv{l+1}.b"][0]
+    assert dq.dqn_param_offset(net, L, False) == sl["fc1.W"][0]
+    assert dq.dqn_param_offset(net, L, True) == sl["fc1.b"][0]
+    assert dq.dqn_param_offset(net, L + 1, False) == sl["fc2.W"][0]
+    assert dq.dqn_param_offset(net, L + 1, True) == sl["fc2.b"][0]
+    with pytest.raises(dq.DqnError) as e:
+        dq.dqn_param_offset(net, L + 2, False)
+    assert e.value.status == dq.DQN_EINVAL
+
+
+def test_documented_offsets_small_net():
+    assert [dq.dqn_param_offset(dq.NET_SMALL, l, b) for l in range(4) for b in (0, 1)] == \
+        [0, 4096, 4112, 12304, 12336, 675888, 676144, 677680]
+    assert dq.dqn_param_count(dq.NET_SMALL) == 677686
+    assert dq.dqn_param_count(dq.NET_LARGE) == 1693362
+
+
+def test_unsupported_networks_and_bad_batch():
+    bad = dq.Net(4, 84, 84, ((16, 8, 4), (32, 4, 2)), 256, 7)
+    with pytest.raises(dq.DqnError) as e:
+        dq.dqn_param_count(bad)
+    assert e.value.status == dq.DQN_EUNSUPPORTED
+    with pytest.raises(dq.DqnError) as e:
+        dq.dqn_workspace_bytes(dq.NET_SMALL, 0, dq.DQN_OP_TD_GRADIENT)
+    assert e.value.status == dq.DQN_EINVAL
+    with pytest.raises(dq.DqnError):
+        dq.dqn_workspace_bytes(dq.NET_SMALL, 4, 7)
+    fp16 = dq.Net(4, 84, 84, ((16, 8, 4), (32, 4, 2)), 256, 6, precision=3)
+    with pytest.raises(dq.DqnError) as e:
+        dq.dqn_param_count(fp16)
+    assert e.value.status == dq.DQN_EUNSUPPORTED
+
+
+def test_workspace_grows_with_batch():
+    for net in (dq.NET_SMALL, dq.NET_LARGE):
+        for op in (dq.DQN_OP_FORWARD, dq.DQN_OP_TD_GRADIENT):
+            a = dq.dqn_workspace_bytes(net, 32, op)
+            b = dq.dqn_workspace_bytes(net, 2048, op)
+            assert 0 < a < b and a % 256 == 0 and b % 256 == 0
+
+
+# Raw C calls with fake (never dereferenced) device addresses: every one of
+# these must fail the host checks, so nothing is launched.  They run only
+# where no GPU is visible, so a missing check can never become a launch on
+# bogus pointers.
+FAKE = 0x7F0000000000
+
+
+def _no_gpu():
+    try:
+        import torch
+        return not torch.cuda.is_available()
+    except Exception:
+        return True
+
+
+fake_ptr_test = pytest.mark.skipif(not _no_gpu(), reason="fake-pointer checks run only without a GPU")
+
+
+def _cnet(net):
+    return ctypes.byref(native._cnet(net))
+
+
+@fake_ptr_test
+def test_td_gradient_argument_errors():
+    L = dq.lib()
+    n = dq.NET_SMALL
+    P = dq.dqn_param_count(n)
+    ws = dq.dqn_workspace_bytes(n, 8, dq.DQN_OP_TD_GRADIENT)
+    args = dict(theta=FAKE, tt=FAKE, s=FAKE + 2**30, sn=FAKE + 2**31, a=FAKE, r=FAKE, t=FAKE, B=8,
+                g=FAKE + 2**33, loss=FAKE, q=None, y=None, ws=FAKE + 2**34, wsb=ws)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return L.dqn_td_gradient(_cnet(n), a["theta"], a["tt"], a["s"], a["sn"], a["a"], a["r"],
+                                 a["t"], a["B"], ctypes.c_float(0.99), a["g"], a["loss"], a["q"],
+                                 a["y"], a["ws"], a["wsb"], None)
+    assert call(theta=None) == dq.DQN_EINVAL
+    assert call(s=None) == dq.DQN_EINVAL
+    assert call(g=None) == dq.DQN_EINVAL
+    assert call(B=0) == dq.DQN_EINVAL
+    assert call(B=-3) == dq.DQN_EINVAL
+    assert call(wsb=ws - 1) == dq.DQN_EWORKSPACE
+    assert call(ws=FAKE + 2**34 + 8) == dq.DQN_EINVAL            # misaligned workspace
+    assert call(g=FAKE + 4 * (P // 2)) == dq.DQN_EINVAL           # grad overlaps theta
+    assert call(g=FAKE, tt=FAKE + 2**33) == dq.DQN_EINVAL         # grad overlaps theta_target
+    bad = dq.Net(4, 84, 84, ((16, 8, 4),), 256, 6)
+    assert L.dqn_td_gradient(_cnet(bad), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8,
+                             ctypes.c_float(0.99), FAKE + 2**33, FAKE, None, None, FAKE, ws,
+                             None) == dq.DQN_EUNSUPPORTED
+
+
+@fake_ptr_test
+def test_forward_argument_errors():
+    L = dq.lib()
+    n = dq.NET_LARGE
+    ws = dq.dqn_workspace_bytes(n, 16, dq.DQN_OP_FORWARD)
+
+    def call(eps=0.0, draws=None, B=16, wsb=ws, theta=FAKE):
+        return L.dqn_forward(_cnet(n), theta, FAKE, B, ctypes.c_float(eps), draws, FAKE, FAKE,
+                             FAKE + 2**34, wsb, None)
+    assert call(eps=0.05, draws=None) == dq.DQN_EINVAL   # exploration needs draws
+    assert call(eps=-0.1, draws=FAKE) == dq.DQN_EINVAL
+    assert call(eps=1.5, draws=FAKE) == dq.DQN_EINVAL
+    assert call(eps=float("nan"), draws=FAKE) == dq.DQN_EINVAL
+    assert call(B=0) == dq.DQN_EINVAL
+    assert call(wsb=ws - 256) == dq.DQN_EWORKSPACE
+    assert call(theta=None) == dq.DQN_EINVAL
+
+
+@fake_ptr_test
+def test_gather_argument_errors():
+    L = dq.lib()
+    rp = native._CReplay()
+    rp.frames, rp.action, rp.reward, rp.terminal = FAKE, FAKE, FAKE, FAKE
+    rp.record_stride, rp.size, rp.c, rp.h, rp.w = 28224, 100, 4, 84, 84
+
+    def call(B=4, s=FAKE + 2**30, sn=FAKE + 2**31, **kw):
+        for k, v in kw.items():
+            setattr(rp, k, v)
+        return L.replay_gather(ctypes.byref(rp), FAKE, B, s, sn, None, None, None, None)
+    assert call(s=None) == dq.DQN_EINVAL
+    assert call(B=0) == dq.DQN_EINVAL
+    assert call(s=FAKE + 2**30 + 4) == dq.DQN_EINVAL          # misaligned output
+    assert call(record_stride=28224 + 8) == dq.DQN_EINVAL     # stride not a multiple of 16
+    assert call(record_stride=1000) == dq.DQN_EINVAL          # stride below record size
+    rp.record_stride = 28224
+    assert call(size=1) == dq.DQN_EINVAL                      # needs two records for s'
+    rp.size = 100
+    assert call(h=83, w=83) == dq.DQN_EINVAL                  # record not a multiple of 16 bytes
+
+
+@fake_ptr_test
+def test_apply_argument_errors():
+    L = dq.lib()
+
+    def call(rule=0, th=FAKE, out=FAKE, st=None, g=FAKE + 2**32, n=1000, lr=0.1):
+        return L.ps_apply_update(rule, th, out, st, g, n, ctypes.c_float(lr), ctypes.c_float(0.9),
+                                 ctypes.c_float(0.0), None)
+    assert call(rule=5) == dq.DQN_EINVAL
+    assert call(rule=1, st=None) == dq.DQN_EINVAL            # RMSProp needs its state
+    assert call(rule=2, st=None) == dq.DQN_EINVAL
+    assert call(n=0) == dq.DQN_EINVAL
+    assert call(g=FAKE + 64) == dq.DQN_EINVAL                # grad overlaps theta_out
+    assert call(out=FAKE + 64) == dq.DQN_EINVAL              # partial overlap of in and out
+    assert call(rule=2, st=FAKE + 2**32 + 16) == dq.DQN_EINVAL  # state overlaps grad
+    assert call(th=FAKE + 2) == dq.DQN_EINVAL                # misaligned
+    assert call(lr=float("inf")) == dq.DQN_EINVAL
+
+
+def test_status_strings():
+    for s in (dq.DQN_OK, dq.DQN_EINVAL, dq.DQN_EWORKSPACE, dq.DQN_EHIP, dq.DQN_EUNSUPPORTED):
+        assert dq.dqn_status_string(s) not in ("", "unknown status")

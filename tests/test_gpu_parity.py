@@ -1,0 +1,289 @@
+"""GPU parity: every entry point of libdqn.so against the CPU oracle on the
+same seeded inputs.  Bit-exact for gathers and action choices (per the rule
+in gpu_util.check_actions); per-tensor relative L2 error <= 1e-4 for float32
+Q values, targets, losses, gradients and parameters."""
+import numpy as np
+import pytest
+
+import dqn_inputs as di
+import oracle
+import paper_1508_04186_amd as dq
+from gpu_util import FP32_TOL, assert_grad_close, check_actions, dev_tensor, host, rel_l2, say
+
+pytestmark = pytest.mark.gpu
+
+NETS = {"small": (dq.NET_SMALL, di.NET_S), "large": (dq.NET_LARGE, di.NET_L)}
+F32 = np.float32
+
+
+@pytest.fixture(scope="module")
+def replay(dev):
+    size = 3000
+    say(f"[setup] host replay size={size} seed=31 -> device")
+    hr = di.host_replay(size, 6, seed=31)
+    rec, a, r, t = di.device_replay(size, 6, seed=31, host=hr)
+    return hr, dq.Replay(rec, a, r, t, size)
+
+
+# ---------------------------------------------------------------------------
+# replay_gather
+
+@pytest.mark.parametrize("batch", [1, 32, 77])
+def test_gather_bit_exact(dev, replay, batch):
+    import torch
+    hr, rp = replay
+    rng = np.random.default_rng(batch)
+    idx = rng.integers(0, rp.size - 1, batch).astype(np.int64)
+    idx[0] = rp.size - 2
+    if batch > 2:
+        idx[1] = 0
+        idx[2] = idx[0]      # duplicate: sampled with replacement
+    say(f"[gather] batch={batch}")
+    s = torch.empty((batch, 4, 84, 84), dtype=torch.uint8, device=dev)
+    sn = torch.empty_like(s)
+    a = torch.empty(batch, dtype=torch.int32, device=dev)
+    r = torch.empty(batch, dtype=torch.float32, device=dev)
+    t = torch.empty(batch, dtype=torch.uint8, device=dev)
+    dq.replay_gather(rp, dev_tensor(idx), s, sn, a, r, t)
+    torch.cuda.synchronize()
+    rs, rsn, ra, rr, rt = oracle.gather_from_host_replay(hr, idx)
+    assert np.array_equal(host(s).reshape(batch, -1), rs)
+    assert np.array_equal(host(sn).reshape(batch, -1), rsn)
+    assert np.array_equal(host(a), ra) and np.array_equal(host(r), rr) and np.array_equal(host(t), rt)
+
+
+def test_gather_states_only_reaches_last_record(dev, replay):
+    import torch
+    hr, rp = replay
+    idx = np.array([rp.size - 1, 5, rp.size - 1], np.int64)
+    say("[gather] states only, last record")
+    s = torch.empty((3, 4, 84, 84), dtype=torch.uint8, device=dev)
+    dq.replay_gather(rp, dev_tensor(idx), s)
+    torch.cuda.synchronize()
+    rs, _, _, _, _ = oracle.gather_from_host_replay(hr, idx, with_next=False)
+    assert np.array_equal(host(s).reshape(3, -1), rs)
+
+
+# ---------------------------------------------------------------------------
+# ps_apply_update
+
+@pytest.mark.parametrize("rule", ["sgd", "rmsprop", "adagrad"])
+@pytest.mark.parametrize("n", [1, 7, 677686])
+def test_apply_matches_oracle(dev, rule, n):
+    import torch
+    rng = np.random.default_rng(n)
+    th = (rng.standard_normal(n) * 0.05).astype(F32)
+    st = None if rule == "sgd" else (np.abs(rng.standard_normal(n)) * 1e-4).astype(F32)
+    if st is not None:
+        st[: max(1, n // 10)] = 0.0           # fresh state, including r = 0 exactly
+    lr, decay, eps = (2.5e-4, 0.9, 0.0) if rule != "adagrad" else (0.01, 0.0, 1e-8)
+    th_d = dev_tensor(th)
+    st_d = None if st is None else dev_tensor(st)
+    out_d = torch.empty_like(th_d)
+    ref_th, ref_st = th, st
+    for step in range(3):
+        g = di.random_gradient(n, 100 * n + step)
+        if rule == "rmsprop" and step == 0:
+            g[: max(1, n // 20)] = 0.0        # r stays 0 -> parameter unchanged
+        say(f"[apply] rule={rule} n={n} step={step} out_of_place={step == 1}")
+        g_d = dev_tensor(g)
+        if step == 1:
+            dq.ps_apply_update(rule, th_d, out_d, st_d, g_d, lr, decay, eps)
+            th_d, out_d = out_d, th_d
+        else:
+            dq.ps_apply_update(rule, th_d, th_d, st_d, g_d, lr, decay, eps)
+        torch.cuda.synchronize()
+        prev = ref_th
+        ref_th, ref_st = oracle.apply_update(rule, ref_th, ref_st, g.astype(np.float64),
+                                             float(F32(lr)), float(F32(decay)), float(F32(eps)))
+        # float32 arithmetic on operands of size |theta| and |step|: the
+        # error bound scales with the operands, not with the (possibly
+        # cancelled) result
+        scale = np.abs(prev).astype(np.float64) + np.abs(ref_th.astype(np.float64) - prev)
+        err = np.abs(host(th_d).astype(np.float64) - ref_th)
+        assert np.all(err <= 1e-6 * scale), f"max err/scale {np.max(err / np.maximum(scale, 1e-30))}"
+        if st is not None:
+            assert np.allclose(host(st_d), ref_st, rtol=1e-6, atol=0)
+
+
+# ---------------------------------------------------------------------------
+# dqn_forward
+
+@pytest.mark.parametrize("name,batch", [("small", 1), ("small", 45), ("large", 3), ("large", 70)])
+def test_forward_q_and_greedy_actions(dev, name, batch):
+    import torch
+    net, shape = NETS[name]
+    th = di.xavier_theta(shape, 40 + batch, bias_scale=0.05)
+    st = di.random_states(batch, 41 + batch)
+    say(f"[forward] net={name} batch={batch} eps=0")
+    q = torch.empty((batch, net.n_actions), dtype=torch.float32, device=dev)
+    act = torch.empty(batch, dtype=torch.int32, device=dev)
+    dq.dqn_forward(net, dev_tensor(th), dev_tensor(st), 0.0, None, q, act)
+    torch.cuda.synchronize()
+    q_ref = oracle.forward_q(shape, th, st)
+    assert rel_l2(host(q), q_ref) <= FP32_TOL
+    act_ref = oracle.select_actions(q_ref, 0.0)
+    check_actions(host(act), host(q), q_ref, act_ref, np.zeros(batch, bool))
+
+
+@pytest.mark.parametrize("name", ["small", "large"])
+def test_forward_epsilon_greedy(dev, name):
+    import torch
+    net, shape = NETS[name]
+    B = 300
+    th = di.xavier_theta(shape, 50, bias_scale=0.05)
+    st = di.random_states(B, 51)
+    draws = di.egreedy_draws(B, 52)
+    eps = F32(0.05)
+    say(f"[forward] net={name} batch={B} eps=0.05")
+    q = torch.empty((B, net.n_actions), dtype=torch.float32, device=dev)
+    act = torch.empty(B, dtype=torch.int32, device=dev)
+    dq.dqn_forward(net, dev_tensor(th), dev_tensor(st), float(eps), dev_tensor(draws), q, act)
+    torch.cuda.synchronize()
+    q_ref = oracle.forward_q(shape, th, st)
+    act_ref = oracle.select_actions(q_ref, float(eps), draws)
+    explore = (draws >> np.uint64(32)) < np.uint64(214748368)
+    assert explore.any() and not explore.all()
+    check_actions(host(act), host(q), q_ref, act_ref, explore)
+    # epsilon = 1: every action is the drawn one
+    say(f"[forward] net={name} batch={B} eps=1")
+    dq.dqn_forward(net, dev_tensor(th), dev_tensor(st), 1.0, dev_tensor(draws), None, act)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(act), oracle.select_actions(q_ref, 1.0, draws))
+
+
+def test_forward_exact_ties_take_action_zero(dev):
+    import torch
+    net, shape = NETS["large"]
+    th = np.zeros(shape.param_count(), F32)
+    st = di.random_states(9, 3)
+    say("[forward] all-zero parameters: exact ties")
+    q = torch.empty((9, net.n_actions), dtype=torch.float32, device=dev)
+    act = torch.full((9,), -1, dtype=torch.int32, device=dev)
+    dq.dqn_forward(net, dev_tensor(th), dev_tensor(st), 0.0, None, q, act)
+    torch.cuda.synchronize()
+    assert np.all(host(q) == 0.0) and np.all(host(act) == 0)
+
+
+# ---------------------------------------------------------------------------
+# dqn_td_gradient
+
+def _td_inputs(shape, B, seed, p_term=0.2, states="uniform", replay=None):
+    if states == "uniform":
+        s = di.random_states(B, seed)
+        sn = di.random_states(B, seed + 1)
+        a, r, t = di.random_transitions(B, shape.n_actions, seed + 2, p_terminal=p_term)
+    else:
+        hr, _ = replay
+        idx = np.random.default_rng(seed).integers(0, hr.size - 1, B)
+        s, sn, a, r, t = oracle.gather_from_host_replay(hr, idx)
+        s = s.reshape(B, 4, 84, 84)
+        sn = sn.reshape(B, 4, 84, 84)
+        a = a % shape.n_actions
+    return s, sn, a.astype(np.int32), r.astype(F32), t.astype(np.uint8)
+
+
+def _run_td(dev, net, th, tt, s, sn, a, r, t, gamma):
+    import torch
+    B = s.shape[0]
+    P = dq.dqn_param_count(net)
+    g = torch.empty(P, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    q = torch.empty((B, net.n_actions), dtype=torch.float32, device=dev)
+    y = torch.empty(B, dtype=torch.float32, device=dev)
+    th_d = dev_tensor(th)
+    tt_d = th_d if tt is None else dev_tensor(tt)
+    dq.dqn_td_gradient(net, th_d, tt_d, dev_tensor(s), dev_tensor(sn), dev_tensor(a), dev_tensor(r),
+                       dev_tensor(t), gamma, g, loss, q, y)
+    torch.cuda.synchronize()
+    return host(g), float(host(loss)[0]), host(q), host(y)
+
+
+TD_CASES = [
+    ("small", 1, "same"), ("small", 3, "same"), ("small", 32, "same"), ("small", 33, "held"),
+    ("large", 2, "same"), ("large", 17, "held"),
+]
+
+
+@pytest.mark.parametrize("name,B,target", TD_CASES)
+def test_td_gradient_matches_oracle(dev, name, B, target):
+    net, shape = NETS[name]
+    th = di.xavier_theta(shape, 60 + B, bias_scale=0.05)
+    tt = None if target == "same" else di.xavier_theta(shape, 61 + B, bias_scale=0.05)
+    s, sn, a, r, t = _td_inputs(shape, B, 62 + B)
+    say(f"[td] net={name} batch={B} target={target}")
+    g, loss, q, y = _run_td(dev, net, th, tt, s, sn, a, r, t, 0.99)
+    ref = oracle.td_gradient(shape, th, tt, s, sn, a, r, t, float(F32(0.99)))
+    assert rel_l2(q, ref["q"]) <= FP32_TOL
+    assert rel_l2(y, ref["y"]) <= FP32_TOL
+    assert abs(loss - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
+    assert_grad_close(shape, g, ref["grad"])
+
+
+def test_td_gradient_on_replay_frames(dev, replay):
+    net, shape = NETS["small"]
+    B = 32
+    th = di.xavier_theta(shape, 70)
+    s, sn, a, r, t = _td_inputs(shape, B, 71, states="replay", replay=replay)
+    say(f"[td] net=small batch={B} replay frames")
+    g, loss, q, y = _run_td(dev, net, th, None, s, sn, a, r, t, 0.99)
+    ref = oracle.td_gradient(shape, th, None, s, sn, a, r, t, float(F32(0.99)))
+    assert abs(loss - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
+    assert_grad_close(shape, g, ref["grad"])
+
+
+def test_td_gradient_deterministic_and_all_terminal(dev):
+    net, shape = NETS["small"]
+    B = 32
+    th = di.xavier_theta(shape, 80, bias_scale=0.05)
+    s, sn, a, r, t = _td_inputs(shape, B, 81)
+    say("[td] determinism, net=small batch=32")
+    g1, l1, _, _ = _run_td(dev, net, th, None, s, sn, a, r, t, 0.99)
+    g2, l2, _, _ = _run_td(dev, net, th, None, s, sn, a, r, t, 0.99)
+    assert np.array_equal(g1, g2) and l1 == l2
+    say("[td] all terminal -> y = r")
+    t1 = np.ones(B, np.uint8)
+    _, _, _, y = _run_td(dev, net, th, None, s, sn, a, r, t1, 0.99)
+    assert np.array_equal(y, r)
+
+
+def test_td_gradient_zero_when_q_equals_target(dev):
+    # fc2.W = 0 and fc2.b = 0.5 everywhere, all terminal with r = 0.5
+    net, shape = NETS["small"]
+    B = 8
+    th = di.xavier_theta(shape, 90)
+    o, shp = shape.slices()["fc2.W"]
+    th[o:o + int(np.prod(shp))] = 0.0
+    o, _ = shape.slices()["fc2.b"]
+    th[o:o + 6] = 0.5
+    s, sn, a, _, _ = _td_inputs(shape, B, 91)
+    r = np.full(B, 0.5, F32)
+    t = np.ones(B, np.uint8)
+    say("[td] zero residual")
+    g, loss, _, _ = _run_td(dev, net, th, None, s, sn, a, r, t, 0.99)
+    assert loss == 0.0 and np.all(g == 0.0)
+
+
+def test_sgd_step_matches_oracle(dev):
+    import torch
+    net, shape = NETS["small"]
+    B = 32
+    th = di.xavier_theta(shape, 100)
+    s, sn, a, r, t = _td_inputs(shape, B, 101)
+    say("[step] td_gradient + SGD, net=small batch=32")
+    P = dq.dqn_param_count(net)
+    th_d = dev_tensor(th)
+    g = torch.empty(P, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    dq.dqn_td_gradient(net, th_d, th_d, dev_tensor(s), dev_tensor(sn), dev_tensor(a), dev_tensor(r),
+                       dev_tensor(t), 0.99, g, loss)
+    dq.ps_apply_update("sgd", th_d, th_d, None, g, 2.5e-4)
+    torch.cuda.synchronize()
+    ref = oracle.td_gradient(shape, th, None, s, sn, a, r, t, float(F32(0.99)))
+    ref_th, _ = oracle.apply_update("sgd", th, None, ref["grad"], float(F32(2.5e-4)))
+    new = host(th_d)
+    assert_grad_close(shape, new, ref_th, what="theta")
+    # each parameter moved by the oracle's step up to one float32 rounding
+    step_ref = ref_th.astype(np.float64) - th
+    err = np.abs(new.astype(np.float64) - ref_th)
+    assert np.all(err <= np.spacing(np.abs(ref_th)) + FP32_TOL * np.abs(step_ref))
