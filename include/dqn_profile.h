@@ -1,0 +1,53 @@
+/*
+ * dqn_profile.h -- measurement hook of libdqn.so.
+ *
+ * Lets a benchmark time one internal kernel of the hot path with HIP events
+ * recorded on the stream that kernel runs on.  Not needed for normal use.
+ *
+ * dqn_profile_attach(kernel, events, n_pairs): from now on, each launch of
+ * `kernel` is bracketed by hipEventRecord(events[2*i]) before and
+ * hipEventRecord(events[2*i+1]) after, for i = 0, 1, ... up to n_pairs - 1;
+ * later launches are not bracketed.  `events` is a host array of hipEvent_t
+ * created by the caller; it must stay valid while attached.  Pass
+ * events = NULL (or n_pairs = 0) to detach.  Returns DQN_OK or DQN_EINVAL.
+ * dqn_profile_used(kernel): number of pairs recorded since the last attach.
+ *
+ * The hook is process-wide state: attach/detach must not race with calls of
+ * the hot-path entry points on other host threads.
+ */
+#ifndef DQN_PROFILE_H
+#define DQN_PROFILE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DQN_K_GATHER = 0,
+    DQN_K_CONV1_FWD = 1,
+    DQN_K_CONV2_FWD = 2,
+    DQN_K_CONV3_FWD = 3,
+    DQN_K_FC1_FWD = 4,
+    DQN_K_HEAD = 5,
+    DQN_K_FC1_WGRAD = 6,
+    DQN_K_FC1_DGRAD = 7,
+    DQN_K_CONV1_WGRAD = 8,
+    DQN_K_CONV2_WGRAD = 9,
+    DQN_K_CONV3_WGRAD = 10,
+    DQN_K_CONV2_DGRAD = 11,
+    DQN_K_CONV3_DGRAD = 12,
+    DQN_K_FINALIZE = 13,
+    DQN_K_APPLY = 14,
+    DQN_K_COUNT = 15
+} dqn_kernel;
+
+int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs);
+int32_t dqn_profile_used(int32_t kernel);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DQN_PROFILE_H */

@@ -55,6 +55,8 @@ def _lib():
         if not os.path.exists(lib_path()):
             build()
         lib = ctypes.CDLL(lib_path())
+        lib.oracle_num_threads.argtypes = []
+        lib.oracle_num_threads.restype = ctypes.c_int
         lib.oracle_param_count.argtypes = [ctypes.POINTER(_Net)]
         lib.oracle_param_count.restype = ctypes.c_int64
         lib.oracle_param_offset.argtypes = [ctypes.POINTER(_Net), ctypes.c_int32, ctypes.c_int32]
@@ -93,6 +95,10 @@ def _ptr(a):
 def _check(rc, what):
     if rc != 0:
         raise RuntimeError(f"{what} failed with status {rc}")
+
+
+def num_threads() -> int:
+    return int(_lib().oracle_num_threads())
 
 
 def param_count(net) -> int:

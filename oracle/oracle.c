@@ -97,6 +97,9 @@ static int make_shapes(const oracle_net* net, shapes_t* sh) {
     return ORACLE_OK;
 }
 
+/* Threads the oracle's parallel loops use. */
+int oracle_num_threads(void) { return omp_get_max_threads(); }
+
 int64_t oracle_param_count(const oracle_net* net) {
     shapes_t sh;
     if (make_shapes(net, &sh) != ORACLE_OK) return -1;

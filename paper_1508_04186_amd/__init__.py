@@ -12,5 +12,5 @@ from .native import (  # noqa: F401
     DqnError, Net, NET_SMALL, NET_LARGE, Replay,
     lib, lib_path, dqn_param_count, dqn_param_offset, dqn_workspace_bytes,
     replay_gather, dqn_forward, dqn_td_gradient, ps_apply_update, dqn_status_string,
-    workspace,
+    workspace, profile_attach, profile_used, KERNEL_NAMES,
 )

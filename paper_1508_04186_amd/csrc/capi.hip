@@ -6,6 +6,7 @@
 
 #include "common.h"
 #include "dqn.h"
+#include "dqn_profile.h"
 
 using namespace dqn;
 
@@ -152,9 +153,34 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-#define HIP_TRY(expr)                              \
-    do {                                           \
-        if ((expr) != hipSuccess) return DQN_EHIP; \
+
+// Measurement hook (dqn_profile.h): event pairs recorded around one kernel.
+struct ProfSlot {
+    hipEvent_t* ev = nullptr;
+    int n = 0;
+    int used = 0;
+};
+ProfSlot g_prof[DQN_K_COUNT];
+
+inline void prof_begin(int k, hipStream_t st) {
+    ProfSlot& p = g_prof[k];
+    if (p.ev && p.used < p.n) (void)hipEventRecord(p.ev[2 * p.used], st);
+}
+inline void prof_end(int k, hipStream_t st) {
+    ProfSlot& p = g_prof[k];
+    if (p.ev && p.used < p.n) {
+        (void)hipEventRecord(p.ev[2 * p.used + 1], st);
+        ++p.used;
+    }
+}
+
+// Launch one kernel of the hot path, bracketed by the profiling events of
+// kernel id `kid` when attached.
+#define RUN(kid, expr)                                  \
+    do {                                                \
+        prof_begin((kid), st);                          \
+        if ((expr) != hipSuccess) return DQN_EHIP;      \
+        prof_end((kid), st);                            \
     } while (0)
 
 }  // namespace
@@ -209,9 +235,10 @@ int replay_gather(const dqn_replay* rp, const int64_t* idx, int32_t batch, uint8
     if ((a_out && !rp->action) || (r_out && !rp->reward) || (term_out && !rp->terminal))
         return DQN_EINVAL;
     if (batch > 65535) return DQN_EINVAL;
-    HIP_TRY(launch_gather(rp->frames, rp->record_stride, rec, rp->action, rp->reward, rp->terminal,
-                          idx, batch, s_out, s_next_out, a_out, r_out, term_out,
-                          (hipStream_t)stream));
+    hipStream_t st = (hipStream_t)stream;
+    RUN(DQN_K_GATHER, launch_gather(rp->frames, rp->record_stride, rec, rp->action, rp->reward,
+                                    rp->terminal, idx, batch, s_out, s_next_out, a_out, r_out,
+                                    term_out, st));
     return DQN_OK;
 }
 
@@ -235,12 +262,14 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
     for (int l = 0; l < ni.n_conv; ++l) {
         const void* in = l == 0 ? (const void*)states : (const void*)f.act[l - 1];
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
-        HIP_TRY(launch_conv_fwd(ni.conv[l], in, in, batch, batch, th + ni.w_off[l], th + ni.b_off[l],
-                                th + ni.w_off[l], th + ni.b_off[l], f.act[l], scale, st));
+        RUN(DQN_K_CONV1_FWD + l,
+            launch_conv_fwd(ni.conv[l], in, in, batch, batch, th + ni.w_off[l], th + ni.b_off[l],
+                            th + ni.w_off[l], th + ni.b_off[l], f.act[l], scale, st));
     }
     const int L = ni.n_conv;
-    HIP_TRY(launch_gemm(GEMM_NT, batch, ni.H, ni.flat, f.act[L - 1], ni.flat, th + ni.w_off[L],
-                        ni.flat, f.fc1p, ni.H, f.ks, f.kchunk, (int64_t)batch * ni.H, nullptr, st));
+    RUN(DQN_K_FC1_FWD,
+        launch_gemm(GEMM_NT, batch, ni.H, ni.flat, f.act[L - 1], ni.flat, th + ni.w_off[L], ni.flat,
+                    f.fc1p, ni.H, f.ks, f.kchunk, (int64_t)batch * ni.H, nullptr, st));
     HeadFwdArgs h{};
     h.fc1p = f.fc1p;
     h.ks = f.ks;
@@ -252,7 +281,7 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
     h.draws = draws;
     h.q_out = q_out;
     h.action_out = action_out;
-    HIP_TRY(launch_head_fwd(ni.H, ni.A, h, st));
+    RUN(DQN_K_HEAD, launch_head_fwd(ni.H, ni.A, h, st));
     return DQN_OK;
 }
 
@@ -288,20 +317,24 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
         const void* in_b = l == 0 ? (const void*)s_next
                                   : (const void*)(t.act[l - 1] + (int64_t)B * act_elems(ni.d[l - 1]));
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
-        HIP_TRY(launch_conv_fwd(ni.conv[l], in_a, in_b, B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
-                                tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], scale, st));
+        RUN(DQN_K_CONV1_FWD + l,
+            launch_conv_fwd(ni.conv[l], in_a, in_b, B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
+                            tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], scale, st));
     }
     const float* xlast = t.act[L - 1];
     const int64_t slice = (int64_t)2 * B * ni.H;
     if (tt == th) {
-        HIP_TRY(launch_gemm(GEMM_NT, 2 * B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
-                            t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, st));
+        RUN(DQN_K_FC1_FWD,
+            launch_gemm(GEMM_NT, 2 * B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
+                        t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, st));
     } else {
-        HIP_TRY(launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
-                            t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, st));
-        HIP_TRY(launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast + (int64_t)B * ni.flat, ni.flat,
-                            tt + ni.w_off[L], ni.flat, t.fc1p + (int64_t)B * ni.H, ni.H, t.ks,
-                            t.kchunk, slice, nullptr, st));
+        RUN(DQN_K_FC1_FWD,
+            launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
+                        t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, st));
+        RUN(DQN_K_FC1_FWD,
+            launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast + (int64_t)B * ni.flat, ni.flat,
+                        tt + ni.w_off[L], ni.flat, t.fc1p + (int64_t)B * ni.H, ni.H, t.ks,
+                        t.kchunk, slice, nullptr, st));
     }
     HeadTdArgs h{};
     h.fc1p = t.fc1p;
@@ -323,21 +356,25 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
     h.lossj = t.lossj;
     h.q_out = q_out;
     h.y_out = y_out;
-    HIP_TRY(launch_head_td(ni.H, ni.A, h, st));
+    RUN(DQN_K_HEAD, launch_head_td(ni.H, ni.A, h, st));
 
     // fc1: weight gradient and the masked gradient of the last conv output.
-    HIP_TRY(launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat,
-                        grad_out + ni.w_off[L], ni.flat, 1, (B + 15) / 16 * 16, 0, nullptr, st));
-    HIP_TRY(launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
-                        t.dconv[L - 1], ni.flat, 1, (ni.H + 15) / 16 * 16, 0, xlast, st));
+    RUN(DQN_K_FC1_WGRAD,
+        launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat, grad_out + ni.w_off[L],
+                    ni.flat, 1, (B + 15) / 16 * 16, 0, nullptr, st));
+    RUN(DQN_K_FC1_DGRAD,
+        launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
+                    t.dconv[L - 1], ni.flat, 1, (ni.H + 15) / 16 * 16, 0, xlast, st));
     // conv layers, last to first
     for (int l = L - 1; l >= 0; --l) {
         const void* in = l == 0 ? (const void*)s : (const void*)t.act[l - 1];
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
-        HIP_TRY(launch_conv_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
+        RUN(DQN_K_CONV1_WGRAD + l,
+            launch_conv_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
         if (l > 0)
-            HIP_TRY(launch_conv_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],
-                                      t.dconv[l - 1], B, st));
+            RUN(DQN_K_CONV2_DGRAD + (l - 1),
+                launch_conv_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],
+                                  t.dconv[l - 1], B, st));
     }
     FinalizeArgs fa{};
     fa.n_conv = L;
@@ -363,7 +400,7 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
     fa.g_W2 = grad_out + ni.w_off[L + 1];
     fa.g_b2 = grad_out + ni.b_off[L + 1];
     fa.loss_out = loss_out;
-    HIP_TRY(launch_finalize(fa, st));
+    RUN(DQN_K_FINALIZE, launch_finalize(fa, st));
     return DQN_OK;
 }
 
@@ -381,9 +418,23 @@ int ps_apply_update(int32_t rule, const float* theta_in, float* theta_out, float
         (state && overlaps(state, nb, theta_out, nb)))
         return DQN_EINVAL;
     if (!std::isfinite(lr) || !std::isfinite(decay) || !std::isfinite(eps)) return DQN_EINVAL;
-    HIP_TRY(launch_apply(rule, theta_in, theta_out, state, grad, n, lr, decay, eps,
-                         (hipStream_t)stream));
+    hipStream_t st = (hipStream_t)stream;
+    RUN(DQN_K_APPLY, launch_apply(rule, theta_in, theta_out, state, grad, n, lr, decay, eps, st));
     return DQN_OK;
+}
+
+int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs) {
+    if (kernel < 0 || kernel >= DQN_K_COUNT || n_pairs < 0) return DQN_EINVAL;
+    ProfSlot& p = g_prof[kernel];
+    p.ev = (events && n_pairs > 0) ? (hipEvent_t*)events : nullptr;
+    p.n = p.ev ? n_pairs : 0;
+    p.used = 0;
+    return DQN_OK;
+}
+
+int32_t dqn_profile_used(int32_t kernel) {
+    if (kernel < 0 || kernel >= DQN_K_COUNT) return DQN_EINVAL;
+    return g_prof[kernel].used;
 }
 
 }  // extern "C"

@@ -77,6 +77,10 @@ def lib():
     """The loaded libdqn.so.  Raises if it has not been built."""
     global _LIB
     if _LIB is None:
+        # torch ships its own HIP runtime under the same SONAME; importing it
+        # first makes libdqn.so bind to that one, so there is a single HIP
+        # runtime (and one set of streams) in the process.
+        import torch  # noqa: F401
         path = lib_path()
         if not os.path.exists(path):
             raise RuntimeError(f"libdqn.so not found at {path}; build it with "
@@ -101,6 +105,10 @@ def lib():
             getattr(L, f).restype = ctypes.c_int
         L.dqn_status_string.argtypes = [ctypes.c_int]
         L.dqn_status_string.restype = ctypes.c_char_p
+        L.dqn_profile_attach.argtypes = [ctypes.c_int32, _P, ctypes.c_int32]
+        L.dqn_profile_attach.restype = ctypes.c_int
+        L.dqn_profile_used.argtypes = [ctypes.c_int32]
+        L.dqn_profile_used.restype = ctypes.c_int32
         _LIB = L
     return _LIB
 
@@ -258,3 +266,32 @@ def ps_apply_update(rule, theta_in, theta_out, state, grad, lr, decay=0.9, eps=0
                                _ptr(state, torch.float32, "state"), _ptr(grad, torch.float32, "grad"),
                                n, float(lr), float(decay), float(eps), _stream(stream))
     _check(rc, "ps_apply_update")
+
+
+# ----------------------------------------------------------------------------
+# Measurement hook (include/dqn_profile.h)
+
+K_GATHER, K_CONV1_FWD, K_CONV2_FWD, K_CONV3_FWD, K_FC1_FWD, K_HEAD, K_FC1_WGRAD, K_FC1_DGRAD, \
+    K_CONV1_WGRAD, K_CONV2_WGRAD, K_CONV3_WGRAD, K_CONV2_DGRAD, K_CONV3_DGRAD, K_FINALIZE, \
+    K_APPLY = range(15)
+KERNEL_NAMES = ["gather", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head", "fc1_wgrad",
+                "fc1_dgrad", "conv1_wgrad", "conv2_wgrad", "conv3_wgrad", "conv2_dgrad",
+                "conv3_dgrad", "finalize", "apply"]
+_ATTACHED = {}
+
+
+def profile_attach(kernel: int, events) -> None:
+    """Bracket the next len(events)//2 launches of `kernel` with the given
+    hipEvent_t handles (ints), pairwise.  events=None detaches."""
+    if events is None or len(events) < 2:
+        rc = lib().dqn_profile_attach(kernel, None, 0)
+        _ATTACHED.pop(kernel, None)
+    else:
+        arr = (ctypes.c_void_p * len(events))(*events)
+        _ATTACHED[kernel] = arr
+        rc = lib().dqn_profile_attach(kernel, ctypes.cast(arr, ctypes.c_void_p), len(events) // 2)
+    _check(rc, "dqn_profile_attach")
+
+
+def profile_used(kernel: int) -> int:
+    return int(lib().dqn_profile_used(kernel))

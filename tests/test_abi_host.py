@@ -15,14 +15,16 @@ from paper_1508_04186_amd import native
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def header_functions():
-    txt = open(os.path.join(ROOT, "include", "dqn.h")).read()
+def header_functions(names=None):
+    inc = os.path.join(ROOT, "include")
+    names = names or sorted(f for f in os.listdir(inc) if f.endswith(".h"))
+    txt = "".join(open(os.path.join(inc, f)).read() for f in names)
     txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(\w+)\s*\(", txt, flags=re.M)))
 
 
 def test_header_declares_the_four_calls():
-    fns = header_functions()
+    fns = header_functions(["dqn.h"])
     for f in ("replay_gather", "dqn_forward", "dqn_td_gradient", "ps_apply_update",
               "dqn_param_count", "dqn_param_offset", "dqn_workspace_bytes", "dqn_status_string"):
         assert f in fns

@@ -81,6 +81,9 @@ def test_apply_matches_oracle(dev, rule, n):
     st_d = None if st is None else dev_tensor(st)
     out_d = torch.empty_like(th_d)
     ref_th, ref_st = th, st
+    # float32 rounding error accumulates with the size of every operand seen
+    # so far: |theta_0| plus the magnitude of each step taken
+    scale = np.abs(th).astype(np.float64)
     for step in range(3):
         g = di.random_gradient(n, 100 * n + step)
         if rule == "rmsprop" and step == 0:
@@ -96,10 +99,7 @@ def test_apply_matches_oracle(dev, rule, n):
         prev = ref_th
         ref_th, ref_st = oracle.apply_update(rule, ref_th, ref_st, g.astype(np.float64),
                                              float(F32(lr)), float(F32(decay)), float(F32(eps)))
-        # float32 arithmetic on operands of size |theta| and |step|: the
-        # error bound scales with the operands, not with the (possibly
-        # cancelled) result
-        scale = np.abs(prev).astype(np.float64) + np.abs(ref_th.astype(np.float64) - prev)
+        scale = scale + np.abs(ref_th.astype(np.float64) - prev)
         err = np.abs(host(th_d).astype(np.float64) - ref_th)
         assert np.all(err <= 1e-6 * scale), f"max err/scale {np.max(err / np.maximum(scale, 1e-30))}"
         if st is not None:
