@@ -79,7 +79,7 @@ void fc1_split(int rows, int H, int K, int* ks, int* kchunk) {
     int want = std::max(1, 256 / tiles);
     want = std::min(want, std::max(1, K / 64));
     int kc = (K + want - 1) / want;
-    kc = (kc + 15) / 16 * 16;
+    kc = (kc + 31) / 32 * 32;  // whole k-steps of the GEMM kernel
     *kchunk = kc;
     *ks = (K + kc - 1) / kc;
 }
@@ -361,10 +361,10 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
     // fc1: weight gradient and the masked gradient of the last conv output.
     RUN(DQN_K_FC1_WGRAD,
         launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat, grad_out + ni.w_off[L],
-                    ni.flat, 1, (B + 15) / 16 * 16, 0, nullptr, st));
+                    ni.flat, 1, (B + 31) / 32 * 32, 0, nullptr, st));
     RUN(DQN_K_FC1_DGRAD,
         launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
-                    t.dconv[L - 1], ni.flat, 1, (ni.H + 15) / 16 * 16, 0, xlast, st));
+                    t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, st));
     // conv layers, last to first
     for (int l = L - 1; l >= 0; --l) {
         const void* in = l == 0 ? (const void*)s : (const void*)t.act[l - 1];

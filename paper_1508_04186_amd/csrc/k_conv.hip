@@ -1,8 +1,11 @@
 // Convolution layers of the Q-network (Sec. III.A): forward with fused
 // bias + ReLU, weight/bias gradient, and input gradient with the ReLU mask of
 // the layer below fused in.  All three are implicit GEMMs on fp32 MFMA
-// (v_mfma_f32_16x16x4_f32) with LDS-staged operands.  Activations are NCHW
-// float32; the network input is bytes.
+// (v_mfma_f32_16x16x4_f32) with every operand staged in LDS: a workgroup
+// copies its weights once (padded so the 16 lanes of an MFMA row and the 4
+// lane groups fall in distinct banks) and the input rows it needs (16-byte
+// loads where aligned), then runs its MFMA loop from LDS only.
+// Activations are NCHW float32; the network input is bytes.
 #include "common.h"
 
 namespace dqn {
@@ -10,29 +13,75 @@ namespace {
 
 constexpr int WG = 256;  // 4 waves
 
+// Copy `words` 32-bit words from global to LDS; 16-byte accesses when both
+// sides are 16-byte aligned and the length is a multiple of four words.
+__device__ __forceinline__ void stage_words(uint32_t* __restrict__ dst, const uint32_t* __restrict__ src,
+                                            int words) {
+    if ((((uintptr_t)src | (uintptr_t)dst) & 15) == 0 && (words & 3) == 0) {
+        const f4* s4 = (const f4*)src;
+        f4* d4 = (f4*)dst;
+        for (int e = threadIdx.x; e < words / 4; e += WG) d4[e] = s4[e];
+    } else {
+        for (int e = threadIdx.x; e < words; e += WG) dst[e] = src[e];
+    }
+}
+
+// LDS row strides for a weight block [o][c][k*k]: c stride = 16 mod 64,
+// o stride = 1 mod 64, so lane (li, g) -> bank li + 16 g is conflict-free.
+template <int CIN, int K>
+struct WLayout {
+    static constexpr int KK = K * K;
+    static constexpr int RC = ((KK + 47) / 64) * 64 + 16;   // >= KK, = 16 mod 64
+    static constexpr int RO = ((CIN * RC) / 64) * 64 + 65;  // > CIN*RC, = 1 mod 64
+};
+
+// Stage weight rows o in [o0, o0+CO) of W[COUT][CIN][K][K] into the padded
+// LDS layout.
+template <int CIN, int K, int CO>
+__device__ __forceinline__ void stage_weights(float* __restrict__ sw, const float* __restrict__ W, int o0) {
+    using L = WLayout<CIN, K>;
+    constexpr int NW = CIN * K * K;
+    const float* src = W + (size_t)o0 * NW;
+    for (int e = threadIdx.x; e < CO * NW; e += WG) {
+        const int o = e / NW, r = e - o * NW;
+        const int c = r / L::KK, k = r - c * L::KK;
+        sw[o * L::RO + c * L::RC + k] = src[e];
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Forward.  GEMM view per sample: M = output pixels (oh*ow), N = cout,
-// K = cin*k*k.  A workgroup takes one sample and a run of 16-pixel M-tiles;
-// it stages the input rows those pixels read into LDS (all channels) and each
-// wave computes whole M-tiles across all N-tiles.  Contraction order: lane
-// group g = lane/16 takes channel 4*cb + g; MFMA steps walk (cb, ky, kx), so a
-// lane reads k consecutive input columns per (c, ky).
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
+// K = cin*k*k.  A workgroup owns a run of 16-pixel M-tiles, a block of CO
+// output channels and a run of samples; it stages the weights once and, per
+// sample, the input rows its pixels read.  Each wave computes whole M-tiles
+// across the CO/16 N-tiles.  Contraction order: lane group g = lane/16 takes
+// channel 4*cb + g; MFMA steps walk (cb, ky, kx).
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int CO>
 __global__ __launch_bounds__(WG) void conv_fwd_kernel(
-    const void* __restrict__ in_a, const void* __restrict__ in_b, int n_a,
+    const void* __restrict__ in_a, const void* __restrict__ in_b, int n_a, int n_total,
     const float* __restrict__ w_a, const float* __restrict__ bias_a,
     const float* __restrict__ w_b, const float* __restrict__ bias_b,
-    float* __restrict__ out, int mt_per_wg, float in_scale) {
+    float* __restrict__ out, int mt_per_wg, int spw, int in_rows_max, float in_scale) {
+    using L = WLayout<CIN, K>;
     constexpr int P = OH * OW;
     constexpr int MT = (P + 15) / 16;
-    constexpr int NT = COUT / 16;
+    constexpr int NT = CO / 16;
     constexpr int CB = CIN / 4;
     constexpr int ESZ = U8 ? 1 : 4;
+    constexpr int COB = COUT / CO;
     extern __shared__ __align__(16) unsigned char smem[];
+    float* sw = (float*)smem;                                       // [CO][RO]
+    unsigned char* sin = smem + ((CO * L::RO * 4 + 15) / 16) * 16;  // [CIN][rows][IW]
 
     const int groups = (MT + mt_per_wg - 1) / mt_per_wg;
-    const int n = blockIdx.x / groups;
-    const int grp = blockIdx.x - n * groups;
+    int b = blockIdx.x;
+    const int grp = b % groups;
+    b /= groups;
+    const int cob = b % COB;
+    b /= COB;
+    const int n0 = b * spw;
+    const int n1 = min(n_total, n0 + spw);
+    const int o0 = cob * CO;
     const int mt0 = grp * mt_per_wg;
     const int mt1 = min(MT, mt0 + mt_per_wg);
     const int p0 = mt0 * 16;
@@ -42,24 +91,261 @@ __global__ __launch_bounds__(WG) void conv_fwd_kernel(
     const int iy0 = oy0 * S;
     const int rows = (oy1 - oy0) * S + K;
 
-    const bool second = n >= n_a;
-    const int ns = second ? n - n_a : n;
-    const unsigned char* src = (const unsigned char*)(second ? in_b : in_a) +
-                               (size_t)ns * CIN * IH * IW * ESZ;
-    const float* W = second ? w_b : w_a;
-    const float* bias = second ? bias_b : bias_a;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int li = lane & 15;
+    const int g = lane >> 4;
 
-    // Stage rows [iy0, iy0+rows) of every channel, as 32-bit words.
-    {
-        const int words_per_ch = rows * IW * ESZ / 4;
-        const int total = CIN * words_per_ch;
-        const uint32_t* s32 = (const uint32_t*)src;
-        uint32_t* d32 = (uint32_t*)smem;
-        for (int e = threadIdx.x; e < total; e += WG) {
-            int c = e / words_per_ch;
-            int r = e - c * words_per_ch;
-            d32[e] = s32[(c * IH * IW + iy0 * IW) * ESZ / 4 + r];
+    int staged_w = -1;  // which weight set is in LDS: 0 = a, 1 = b
+    for (int n = n0; n < n1; ++n) {
+        const int second = n >= n_a ? 1 : 0;
+        const int ns = second ? n - n_a : n;
+        const unsigned char* src = (const unsigned char*)(second ? in_b : in_a) +
+                                   (size_t)ns * CIN * IH * IW * ESZ;
+        __syncthreads();  // previous sample's reads are done
+        if (staged_w != second) {
+            stage_weights<CIN, K, CO>(sw, second ? w_b : w_a, o0);
+            staged_w = second;
         }
+        {
+            const int words_per_ch = rows * IW * ESZ / 4;
+            const int row_words = in_rows_max * IW * ESZ / 4;
+            for (int c = 0; c < CIN; ++c)
+                stage_words((uint32_t*)sin + c * row_words,
+                            (const uint32_t*)(src + ((size_t)c * IH * IW + iy0 * IW) * ESZ), words_per_ch);
+        }
+        __syncthreads();
+        const float* bias = second ? bias_b : bias_a;
+        const int row_elems = in_rows_max * IW;
+
+        for (int mt = mt0 + wave; mt < mt1; mt += 4) {
+            const int p = mt * 16 + li;
+            const int pc = p < P ? p : P - 1;
+            const int oy = pc / OW, ox = pc - (pc / OW) * OW;
+            const float amask = p < P ? 1.f : 0.f;
+            f4 acc[NT];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
+            for (int cb = 0; cb < CB; ++cb) {
+                const int c = cb * 4 + g;
+#pragma unroll
+                for (int ky = 0; ky < K; ++ky) {
+                    float a[K];
+                    const int row = S * oy + ky - iy0;
+                    if constexpr (U8) {
+                        const unsigned char* base = sin + c * row_elems + row * IW + S * ox;
+#pragma unroll
+                        for (int q = 0; q < K / 4; ++q) {
+                            const uint32_t wv = *(const uint32_t*)(base + 4 * q);
+                            a[4 * q + 0] = (float)(wv & 0xffu) * amask;
+                            a[4 * q + 1] = (float)((wv >> 8) & 0xffu) * amask;
+                            a[4 * q + 2] = (float)((wv >> 16) & 0xffu) * amask;
+                            a[4 * q + 3] = (float)(wv >> 24) * amask;
+                        }
+                    } else {
+                        const float* base = (const float*)sin + c * row_elems + row * IW + S * ox;
+#pragma unroll
+                        for (int kx = 0; kx < K; ++kx) a[kx] = base[kx] * amask;
+                    }
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+                        const float* wp = sw + (t * 16 + li) * L::RO + c * L::RC + ky * K;
+#pragma unroll
+                        for (int kx = 0; kx < K; ++kx) acc[t] = mfma16x16x4(a[kx], wp[kx], acc[t]);
+                    }
+                }
+            }
+            // Epilogue: lane holds pixels mt*16 + 4g + r of channel o0 + t*16 + li.
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int o = o0 + t * 16 + li;
+                const float bo = bias[o];
+                float* dst = out + ((size_t)n * COUT + o) * P;
+                const int pb = mt * 16 + 4 * g;
+                float v[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[t][r] * in_scale + bo, 0.f);
+                if constexpr (P % 4 == 0) {
+                    if (pb < P) *(f4*)(dst + pb) = f4{v[0], v[1], v[2], v[3]};
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (pb + r < P) dst[pb + r] = v[r];
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Weight gradient.  GEMM view: M = cout, N = cin*k*k (the W layout), the
+// contraction runs over every output pixel of every sample.  A workgroup
+// owns (a chunk of samples, a block of output rows, 4 N-tiles); per sample it
+// stages the input rows and the dz rows of its block, then accumulates in
+// registers.  Partial sums per (chunk, row block) are written without atomics
+// and reduced later in a fixed order.
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
+__global__ __launch_bounds__(WG) void conv_wgrad_kernel(
+    const void* __restrict__ in, const float* __restrict__ dz, int batch, int spc, int rows_per_blk,
+    int in_rows_max, int pix_pad, float* __restrict__ wpart, float* __restrict__ bpart,
+    float in_scale) {
+    constexpr int P = OH * OW;
+    constexpr int NCOL = CIN * K * K;
+    constexpr int NTT = NCOL / 16;
+    constexpr int GROUPS = NTT / 4;
+    constexpr int MT = COUT / 16;
+    constexpr int ESZ = U8 ? 1 : 4;
+    const int RB = (OH + rows_per_blk - 1) / rows_per_blk;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int in_bytes = ((CIN * in_rows_max * IW * ESZ + 15) / 16) * 16;
+    unsigned char* s_in = smem;
+    float* s_dz = (float*)(smem + in_bytes);          // [COUT][pix_pad]
+    int* s_pix = (int*)(s_dz + COUT * pix_pad);       // [pix_pad]
+
+    int b = blockIdx.x;
+    const int grp = b % GROUPS;
+    b /= GROUPS;
+    const int rb = b % RB;
+    const int chunk = b / RB;
+    const int j0 = chunk * spc;
+    const int j1 = min(batch, j0 + spc);
+    const int oy0 = rb * rows_per_blk;
+    const int oy1 = min(OH, oy0 + rows_per_blk);      // exclusive
+    const int pbeg = oy0 * OW;
+    const int npix = (oy1 - oy0) * OW;
+    const int iy0 = oy0 * S;
+    const int rows = (oy1 - 1 - oy0) * S + K;
+    const int row_elems = in_rows_max * IW;
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int li = lane & 15;
+    const int g = lane >> 4;
+
+    for (int q = threadIdx.x; q < pix_pad; q += WG) {
+        const int p = pbeg + q;
+        const int oy = p / OW, ox = p - (p / OW) * OW;
+        s_pix[q] = q < npix ? (S * (oy - oy0) * IW + S * ox) : 0;
+    }
+    const int col = (grp * 4 + wave) * 16 + li;
+    const int kc = col / (K * K);
+    const int kyy = (col / K) % K;
+    const int kxx = col % K;
+    const int koff = kc * row_elems + kyy * IW + kxx;
+
+    f4 acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = f4{0.f, 0.f, 0.f, 0.f};
+    float bacc = 0.f;
+
+    for (int j = j0; j < j1; ++j) {
+        __syncthreads();
+        {
+            const unsigned char* src = (const unsigned char*)in + (size_t)j * CIN * IH * IW * ESZ;
+            const int words_per_ch = rows * IW * ESZ / 4;
+            for (int c = 0; c < CIN; ++c)
+                stage_words((uint32_t*)s_in + c * (row_elems * ESZ / 4),
+                            (const uint32_t*)(src + ((size_t)c * IH * IW + iy0 * IW) * ESZ), words_per_ch);
+            const float* dzj = dz + (size_t)j * COUT * P + pbeg;
+            for (int e = threadIdx.x; e < COUT * pix_pad; e += WG) {
+                const int o = e / pix_pad, q = e - o * pix_pad;
+                s_dz[e] = q < npix ? dzj[(size_t)o * P + q] : 0.f;
+            }
+        }
+        __syncthreads();
+        if (grp == 0 && threadIdx.x < COUT) {
+            const float* row = s_dz + threadIdx.x * pix_pad;
+            float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+            for (int q = 0; q < pix_pad; q += 4) {
+                s0 += row[q];
+                s1 += row[q + 1];
+                s2 += row[q + 2];
+                s3 += row[q + 3];
+            }
+            bacc += (s0 + s1) + (s2 + s3);
+        }
+        for (int st = 0; st < pix_pad / 4; ++st) {
+            const int q = st * 4 + g;
+            float bv;
+            if constexpr (U8) bv = (float)s_in[koff + s_pix[q]];
+            else bv = ((const float*)s_in)[koff + s_pix[q]];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) acc[m] = mfma16x16x4(s_dz[(m * 16 + li) * pix_pad + q], bv, acc[m]);
+        }
+    }
+    // D[4g + r][li] of tile m: o = m*16 + 4g + r, weight column col.
+    const int slot = chunk * RB + rb;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int o = m * 16 + 4 * g + r;
+            wpart[((size_t)slot * COUT + o) * NCOL + col] = acc[m][r] * in_scale;
+        }
+    if (grp == 0 && threadIdx.x < COUT) bpart[(size_t)slot * COUT + threadIdx.x] = bacc;
+}
+
+// ---------------------------------------------------------------------------
+// Input gradient (transposed convolution), split into stride phases so no
+// MFMA multiplies a structural zero: input pixel (S*qy + py, S*qx + px)
+// receives W[o][c][py + S*ty][px + S*tx] * dz[o][qy - ty][qx - tx] for taps
+// ty, tx < K/S.  GEMM view per (sample, phase): M = phase pixels, N = cin,
+// contraction over (o, ty, tx).  dz is staged in LDS with a zero border, and
+// the phase's weight taps for a block of CI input channels as [tap][o][c].
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int CI>
+__global__ __launch_bounds__(WG) void conv_dgrad_kernel(
+    const float* __restrict__ dz, const float* __restrict__ W, const float* __restrict__ h_in,
+    float* __restrict__ din, int mt_per_wg) {
+    static_assert(K % S == 0, "phase decomposition needs k divisible by stride");
+    constexpr int T = K / S;
+    constexpr int TT = T * T;
+    constexpr int QHM = (IH + S - 1) / S;
+    constexpr int QWM = (IW + S - 1) / S;
+    constexpr int PH = QHM + T - 1;
+    constexpr int PW = QWM + T - 1;
+    constexpr int NT = CI / 16;
+    constexpr int OB = COUT / 4;
+    constexpr int CIB = CIN / CI;
+    constexpr int RCW = CI + 1;   // LDS row stride of the [tap][o][c] weight slice
+    constexpr int MTM = (QHM * QWM + 15) / 16;
+    extern __shared__ __align__(16) unsigned char smem[];
+    float* s_dz = (float*)smem;                 // [COUT][PH][PW]
+    float* s_w = s_dz + COUT * PH * PW;         // [TT][COUT][RCW]
+
+    const int groups = (MTM + mt_per_wg - 1) / mt_per_wg;
+    int b = blockIdx.x;
+    const int grp = b % groups;
+    b /= groups;
+    const int cib = b % CIB;
+    b /= CIB;
+    const int ph = b % (S * S);
+    const int n = b / (S * S);
+    const int py = ph / S, px = ph - (ph / S) * S;
+    const int QH = (IH - py + S - 1) / S;
+    const int QW = (IW - px + S - 1) / S;
+    const int QP = QH * QW;
+    const int MTq = (QP + 15) / 16;
+    const int mt0 = grp * mt_per_wg;
+    const int mt1 = min(MTq, mt0 + mt_per_wg);
+    if (mt0 >= mt1) return;  // uniform across the workgroup
+    const int c0 = cib * CI;
+
+    const float* dzn = dz + (size_t)n * COUT * OH * OW;
+    for (int e = threadIdx.x; e < COUT * PH * PW; e += WG) {
+        const int o = e / (PH * PW);
+        const int r = e - o * (PH * PW);
+        const int yy = r / PW, xx = r - (r / PW) * PW;
+        const int y = yy - (T - 1), x = xx - (T - 1);
+        s_dz[e] = (y >= 0 && y < OH && x >= 0 && x < OW) ? dzn[(o * OH + y) * OW + x] : 0.f;
+    }
+    for (int e = threadIdx.x; e < TT * COUT * CI; e += WG) {
+        const int c = e % CI;
+        const int r = e / CI;
+        const int o = r % COUT;
+        const int tap = r / COUT;
+        const int ty = tap / T, tx = tap - (tap / T) * T;
+        s_w[(tap * COUT + o) * RCW + c] =
+            W[(((size_t)o * CIN + c0 + c) * K + py + S * ty) * K + px + S * tx];
     }
     __syncthreads();
 
@@ -69,217 +355,6 @@ __global__ __launch_bounds__(WG) void conv_fwd_kernel(
     const int g = lane >> 4;
 
     for (int mt = mt0 + wave; mt < mt1; mt += 4) {
-        const int p = mt * 16 + li;
-        const int pc = p < P ? p : P - 1;
-        const int oy = pc / OW, ox = pc - (pc / OW) * OW;
-        const float amask = p < P ? 1.f : 0.f;
-        f4 acc[NT];
-#pragma unroll
-        for (int t = 0; t < NT; ++t) acc[t] = f4{0.f, 0.f, 0.f, 0.f};
-
-        for (int cb = 0; cb < CB; ++cb) {
-            const int c = cb * 4 + g;
-#pragma unroll
-            for (int ky = 0; ky < K; ++ky) {
-                float a[K];
-                const int row = S * oy + ky - iy0;
-                if constexpr (U8) {
-                    const unsigned char* base = smem + (c * rows + row) * IW + S * ox;
-#pragma unroll
-                    for (int q = 0; q < K / 4; ++q) {
-                        uint32_t wv = *(const uint32_t*)(base + 4 * q);
-                        a[4 * q + 0] = (float)(wv & 0xffu) * amask;
-                        a[4 * q + 1] = (float)((wv >> 8) & 0xffu) * amask;
-                        a[4 * q + 2] = (float)((wv >> 16) & 0xffu) * amask;
-                        a[4 * q + 3] = (float)(wv >> 24) * amask;
-                    }
-                } else {
-                    const float* base = (const float*)smem + (c * rows + row) * IW + S * ox;
-#pragma unroll
-                    for (int kx = 0; kx < K; ++kx) a[kx] = base[kx] * amask;
-                }
-#pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const float* wp = W + (((t * 16 + li) * CIN + c) * K + ky) * K;
-                    float b[K];
-#pragma unroll
-                    for (int kx = 0; kx < K; ++kx) b[kx] = __ldg(wp + kx);
-#pragma unroll
-                    for (int kx = 0; kx < K; ++kx) acc[t] = mfma16x16x4(a[kx], b[kx], acc[t]);
-                }
-            }
-        }
-        // Epilogue: lane holds pixels mt*16 + 4g + r of channel t*16 + li.
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int o = t * 16 + li;
-            const float bo = bias[o];
-            float* dst = out + ((size_t)n * COUT + o) * P;
-            const int pb = mt * 16 + 4 * g;
-            float v[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[t][r] * in_scale + bo, 0.f);
-            if constexpr (P % 4 == 0) {
-                if (pb < P) *(f4*)(dst + pb) = f4{v[0], v[1], v[2], v[3]};
-            } else {
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    if (pb + r < P) dst[pb + r] = v[r];
-            }
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Weight gradient.  GEMM view: M = cout, N = cin*k*k (the W layout), the
-// contraction runs over every output pixel of every sample.  A workgroup owns
-// a chunk of samples and 4*NTW N-tiles; per sample it stages the input and
-// dz into LDS and accumulates in registers.  Partial sums per chunk are
-// written without atomics and reduced later in a fixed order.
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int NTW>
-__global__ __launch_bounds__(WG) void conv_wgrad_kernel(
-    const void* __restrict__ in, const float* __restrict__ dz, int batch, int spc,
-    float* __restrict__ wpart, float* __restrict__ bpart, float in_scale) {
-    constexpr int P = OH * OW;
-    constexpr int PP = (P + 3) / 4 * 4;
-    constexpr int NCOL = CIN * K * K;
-    constexpr int NTT = NCOL / 16;
-    constexpr int GROUPS = NTT / (4 * NTW);
-    constexpr int MT = COUT / 16;
-    constexpr int ESZ = U8 ? 1 : 4;
-    constexpr int IN_BYTES = CIN * IH * IW * ESZ;
-    constexpr int IN_BYTES_PAD = (IN_BYTES + 15) / 16 * 16;
-    extern __shared__ __align__(16) unsigned char smem[];
-    unsigned char* s_in = smem;
-    float* s_dz = (float*)(smem + IN_BYTES_PAD);       // [COUT][PP]
-    int* s_pix = (int*)(s_dz + COUT * PP);              // [PP]
-
-    const int chunk = blockIdx.x / GROUPS;
-    const int grp = blockIdx.x - chunk * GROUPS;
-    const int j0 = chunk * spc;
-    const int j1 = min(batch, j0 + spc);
-
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int li = lane & 15;
-    const int g = lane >> 4;
-
-    for (int p = threadIdx.x; p < PP; p += WG) {
-        int oy = p / OW, ox = p - (p / OW) * OW;
-        s_pix[p] = p < P ? (S * oy * IW + S * ox) : 0;
-    }
-    int koff[NTW];
-#pragma unroll
-    for (int u = 0; u < NTW; ++u) {
-        const int col = (grp * 4 * NTW + wave + 4 * u) * 16 + li;
-        const int c = col / (K * K);
-        const int ky = (col / K) % K;
-        const int kx = col % K;
-        koff[u] = c * IH * IW + ky * IW + kx;
-    }
-
-    f4 acc[MT][NTW];
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int u = 0; u < NTW; ++u) acc[m][u] = f4{0.f, 0.f, 0.f, 0.f};
-    float bacc = 0.f;
-
-    for (int j = j0; j < j1; ++j) {
-        __syncthreads();
-        {
-            const uint32_t* s32 = (const uint32_t*)((const unsigned char*)in + (size_t)j * IN_BYTES);
-            uint32_t* d32 = (uint32_t*)s_in;
-            for (int e = threadIdx.x; e < IN_BYTES / 4; e += WG) d32[e] = s32[e];
-            const float* dzj = dz + (size_t)j * COUT * P;
-            for (int e = threadIdx.x; e < COUT * PP; e += WG) {
-                int o = e / PP, p = e - (e / PP) * PP;
-                s_dz[e] = p < P ? dzj[o * P + p] : 0.f;
-            }
-        }
-        __syncthreads();
-        if (grp == 0 && threadIdx.x < COUT) {
-            const float* row = s_dz + threadIdx.x * PP;
-            float s = 0.f;
-            for (int p = 0; p < P; ++p) s += row[p];
-            bacc += s;
-        }
-        for (int st = 0; st < PP / 4; ++st) {
-            const int p = st * 4 + g;
-            const int po = s_pix[p];
-            float a[MT], b[NTW];
-#pragma unroll
-            for (int m = 0; m < MT; ++m) a[m] = s_dz[(m * 16 + li) * PP + p];
-#pragma unroll
-            for (int u = 0; u < NTW; ++u) {
-                if constexpr (U8) b[u] = (float)s_in[koff[u] + po];
-                else b[u] = ((const float*)s_in)[koff[u] + po];
-            }
-#pragma unroll
-            for (int m = 0; m < MT; ++m)
-#pragma unroll
-                for (int u = 0; u < NTW; ++u) acc[m][u] = mfma16x16x4(a[m], b[u], acc[m][u]);
-        }
-    }
-    // D[4g + r][li] of tile (m, u): o = m*16 + 4g + r, col = tile col + li.
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int u = 0; u < NTW; ++u) {
-            const int col = (grp * 4 * NTW + wave + 4 * u) * 16 + li;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int o = m * 16 + 4 * g + r;
-                wpart[((size_t)chunk * COUT + o) * NCOL + col] = acc[m][u][r] * in_scale;
-            }
-        }
-    if (grp == 0 && threadIdx.x < COUT) bpart[(size_t)chunk * COUT + threadIdx.x] = bacc;
-}
-
-// ---------------------------------------------------------------------------
-// Input gradient (transposed convolution), split into stride phases so no
-// MFMA multiplies a structural zero: input pixel (S*qy + py, S*qx + px)
-// receives W[o][c][py + S*ty][px + S*tx] * dz[o][qy - ty][qx - tx] for taps
-// ty, tx < K/S.  GEMM view per (sample, phase): M = phase pixels, N = cin,
-// contraction over (o, ty, tx).  dz is staged in LDS with a zero border.
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW>
-__global__ __launch_bounds__(WG) void conv_dgrad_kernel(
-    const float* __restrict__ dz, const float* __restrict__ W, const float* __restrict__ h_in,
-    float* __restrict__ din) {
-    static_assert(K % S == 0, "phase decomposition needs k divisible by stride");
-    constexpr int T = K / S;
-    constexpr int QHM = (IH + S - 1) / S;
-    constexpr int QWM = (IW + S - 1) / S;
-    constexpr int PH = QHM + T - 1;
-    constexpr int PW = QWM + T - 1;
-    constexpr int NT = CIN / 16;
-    constexpr int OB = COUT / 4;
-    __shared__ float s_dz[COUT * PH * PW];
-
-    const int n = blockIdx.x / (S * S);
-    const int ph = blockIdx.x - n * (S * S);
-    const int py = ph / S, px = ph - (ph / S) * S;
-    const int QH = (IH - py + S - 1) / S;
-    const int QW = (IW - px + S - 1) / S;
-    const int QP = QH * QW;
-    const int MTq = (QP + 15) / 16;
-
-    const float* dzn = dz + (size_t)n * COUT * OH * OW;
-    for (int e = threadIdx.x; e < COUT * PH * PW; e += WG) {
-        int o = e / (PH * PW);
-        int r = e - o * (PH * PW);
-        int yy = r / PW, xx = r - (r / PW) * PW;
-        int y = yy - (T - 1), x = xx - (T - 1);
-        s_dz[e] = (y >= 0 && y < OH && x >= 0 && x < OW) ? dzn[(o * OH + y) * OW + x] : 0.f;
-    }
-    __syncthreads();
-
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int li = lane & 15;
-    const int g = lane >> 4;
-
-    for (int mt = wave; mt < MTq; mt += 4) {
         const int q = mt * 16 + li;
         const int qc = q < QP ? q : QP - 1;
         const int qy = qc / QW, qx = qc - (qc / QW) * QW;
@@ -294,17 +369,14 @@ __global__ __launch_bounds__(WG) void conv_dgrad_kernel(
 #pragma unroll
                 for (int tx = 0; tx < T; ++tx) {
                     const float a = s_dz[(o * PH + qy - ty + T - 1) * PW + qx - tx + T - 1] * amask;
-                    const int ky = py + S * ty, kx = px + S * tx;
+                    const float* wrow = s_w + ((ty * T + tx) * COUT + o) * RCW;
 #pragma unroll
-                    for (int t = 0; t < NT; ++t) {
-                        const float b = __ldg(W + (((size_t)o * CIN + t * 16 + li) * K + ky) * K + kx);
-                        acc[t] = mfma16x16x4(a, b, acc[t]);
-                    }
+                    for (int t = 0; t < NT; ++t) acc[t] = mfma16x16x4(a, wrow[t * 16 + li], acc[t]);
                 }
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            const int c = t * 16 + li;
+            const int c = c0 + t * 16 + li;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int qq = mt * 16 + 4 * g + r;
@@ -319,78 +391,125 @@ __global__ __launch_bounds__(WG) void conv_dgrad_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Host-side launch shapes.
 
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
+template <class Kern>
+bool allow_lds(Kern kern, size_t bytes) {
+    // Raise the dynamic LDS limit once per kernel to the largest size used.
+    static size_t granted = 0;
+    if (bytes <= granted) return true;
+    if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) !=
+        hipSuccess)
+        return false;
+    granted = bytes;
+    return true;
+}
+
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int CO>
 hipError_t fwd_launch(const void* in_a, const void* in_b, int n_a, int n, const float* w_a,
                       const float* b_a, const float* w_b, const float* b_b, float* out,
                       float in_scale, hipStream_t st) {
+    using L = WLayout<CIN, K>;
     constexpr int P = OH * OW;
     constexpr int MT = (P + 15) / 16;
     constexpr int ESZ = U8 ? 1 : 4;
-    // Small batches: one M-tile per wave for parallelism; large batches: a
-    // longer run of tiles per workgroup to amortise the input staging.
-    int mt_per_wg = ((long)n * MT >= 4L * 4096) ? MT : 4;
+    constexpr int COB = COUT / CO;
+    // Small batches: one M-tile per wave and one sample per workgroup, for
+    // parallelism; large batches: whole samples and several per workgroup,
+    // so the weight staging is amortised.
+    const long tiles = (long)n * MT * COB;
+    int mt_per_wg, spw;
+    if (tiles >= 8L * 1024 * 4) {
+        mt_per_wg = MT;
+        spw = 4;
+    } else if (tiles >= 2L * 1024 * 4) {
+        mt_per_wg = MT;
+        spw = 1;
+    } else {
+        mt_per_wg = 4;
+        spw = 1;
+    }
     if (mt_per_wg > MT) mt_per_wg = MT;
     const int groups = (MT + mt_per_wg - 1) / mt_per_wg;
     int max_rows = 0;
     for (int gi = 0; gi < groups; ++gi) {
-        int p0 = gi * mt_per_wg * 16;
-        int p1 = std::min(P, (gi + 1) * mt_per_wg * 16);
-        int rows = ((p1 - 1) / OW - p0 / OW) * S + K;
-        max_rows = std::max(max_rows, rows);
+        const int p0 = gi * mt_per_wg * 16;
+        const int p1 = std::min(P, (gi + 1) * mt_per_wg * 16);
+        max_rows = std::max(max_rows, ((p1 - 1) / OW - p0 / OW) * S + K);
     }
-    size_t lds = (size_t)CIN * max_rows * IW * ESZ;
-    lds = (lds + 15) / 16 * 16;
-    auto kern = conv_fwd_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8>;
-    if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds) != hipSuccess)
-        return hipErrorInvalidValue;
-    hipLaunchKernelGGL((conv_fwd_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8>),
-                       dim3((unsigned)(n * groups)), dim3(WG), lds, st, in_a, in_b, n_a, w_a, b_a,
-                       w_b, b_b, out, mt_per_wg, in_scale);
+    // keep each channel's staged rows 16-byte aligned
+    while ((max_rows * IW * ESZ) % 16 != 0) ++max_rows;
+    const size_t w_bytes = ((size_t)CO * L::RO * 4 + 15) / 16 * 16;
+    const size_t lds = w_bytes + (size_t)CIN * max_rows * IW * ESZ;
+    auto kern = conv_fwd_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8, CO>;
+    if (!allow_lds(kern, lds)) return hipErrorInvalidValue;
+    const int nblk = (n + spw - 1) / spw;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(nblk * COB * groups)), dim3(WG), lds, st, in_a, in_b, n_a,
+                       n, w_a, b_a, w_b, b_b, out, mt_per_wg, spw, max_rows, in_scale);
     return hipGetLastError();
+}
+
+// wgrad launch shape: (chunks, row blocks); partial slots = chunks * row blocks.
+struct WgradShape {
+    int chunks, spc, rows_per_blk, rb;
+};
+
+WgradShape wgrad_shape(int batch, int groups, int oh) {
+    WgradShape w;
+    // Row blocks only when the batch alone cannot fill the chip.
+    int rb = 1;
+    if ((long)batch * groups < 512) {
+        rb = (int)std::min<long>(oh, (512 + (long)batch * groups - 1) / ((long)batch * groups));
+    }
+    w.rows_per_blk = (oh + rb - 1) / rb;
+    w.rb = (oh + w.rows_per_blk - 1) / w.rows_per_blk;
+    int c = (1024 + groups * w.rb - 1) / (groups * w.rb);
+    c = std::max(1, std::min(c, batch));
+    w.spc = (batch + c - 1) / c;
+    w.chunks = (batch + w.spc - 1) / w.spc;
+    return w;
 }
 
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW>
 constexpr int wgrad_groups() {
-    return (CIN * K * K / 16) / 4;  // NTW = 1
-}
-
-int target_chunks(int batch, int groups) {
-    int c = (1024 + groups - 1) / groups;
-    if (c > batch) c = batch;
-    if (c < 1) c = 1;
-    // chunk = ceil(batch / c) samples; recompute the chunk count from it
-    int spc = (batch + c - 1) / c;
-    return (batch + spc - 1) / spc;
+    return (CIN * K * K / 16) / 4;
 }
 
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
 hipError_t wgrad_launch(const void* in, const float* dz, int batch, float* wpart, float* bpart,
                         float in_scale, hipStream_t st) {
     constexpr int GROUPS = wgrad_groups<CIN, IH, IW, COUT, K, S, OH, OW>();
-    constexpr int P = OH * OW;
-    constexpr int PP = (P + 3) / 4 * 4;
     constexpr int ESZ = U8 ? 1 : 4;
-    constexpr int IN_BYTES_PAD = (CIN * IH * IW * ESZ + 15) / 16 * 16;
-    const int chunks = target_chunks(batch, GROUPS);
-    const int spc = (batch + chunks - 1) / chunks;
-    size_t lds = IN_BYTES_PAD + (size_t)COUT * PP * 4 + PP * 4;
-    auto kern = conv_wgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8, 1>;
-    if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds) != hipSuccess)
-        return hipErrorInvalidValue;
-    hipLaunchKernelGGL((conv_wgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8, 1>),
-                       dim3((unsigned)(chunks * GROUPS)), dim3(WG), lds, st, in, dz, batch, spc,
-                       wpart, bpart, in_scale);
+    const WgradShape w = wgrad_shape(batch, GROUPS, OH);
+    int in_rows_max = (w.rows_per_blk - 1) * S + K;
+    while ((in_rows_max * IW * ESZ) % 16 != 0) ++in_rows_max;
+    const int pix_pad = (w.rows_per_blk * OW + 3) / 4 * 4;
+    const size_t in_bytes = ((size_t)CIN * in_rows_max * IW * ESZ + 15) / 16 * 16;
+    const size_t lds = in_bytes + (size_t)COUT * pix_pad * 4 + (size_t)pix_pad * 4;
+    auto kern = conv_wgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8>;
+    if (!allow_lds(kern, lds)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(w.chunks * w.rb * GROUPS)), dim3(WG), lds, st, in, dz,
+                       batch, w.spc, w.rows_per_blk, in_rows_max, pix_pad, wpart, bpart, in_scale);
     return hipGetLastError();
 }
 
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW>
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int CI>
 hipError_t dgrad_launch(const float* dz, const float* w, const float* h_in, float* din, int batch,
                         hipStream_t st) {
-    hipLaunchKernelGGL((conv_dgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW>),
-                       dim3((unsigned)(batch * S * S)), dim3(WG), 0, st, dz, w, h_in, din);
+    constexpr int QP = ((IH + S - 1) / S) * ((IW + S - 1) / S);
+    constexpr int MTM = (QP + 15) / 16;
+    constexpr int CIB = CIN / CI;
+    constexpr int T = K / S;
+    constexpr int PH = (IH + S - 1) / S + T - 1;
+    constexpr int PW = (IW + S - 1) / S + T - 1;
+    const long wgs = (long)batch * S * S * CIB;
+    const int mt_per_wg = wgs >= 1024 ? MTM : 4;
+    const int groups = (MTM + mt_per_wg - 1) / mt_per_wg;
+    const size_t lds = ((size_t)COUT * PH * PW + (size_t)T * T * COUT * (CI + 1)) * 4;
+    auto kern = conv_dgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, CI>;
+    if (!allow_lds(kern, lds)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(wgs * groups)), dim3(WG), lds, st, dz, w, h_in, din,
+                       mt_per_wg);
     return hipGetLastError();
 }
 
@@ -400,24 +519,26 @@ hipError_t launch_conv_fwd(ConvId id, const void* in_a, const void* in_b, int n_
                            const float* w_a, const float* b_a, const float* w_b, const float* b_b,
                            float* out, float in_scale, hipStream_t st) {
     switch (id) {
-        case CONV_S1: return fwd_launch<4, 84, 84, 16, 8, 4, 20, 20, true>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
-        case CONV_S2: return fwd_launch<16, 20, 20, 32, 4, 2, 9, 9, false>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
-        case CONV_L1: return fwd_launch<4, 84, 84, 32, 8, 4, 20, 20, true>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
-        case CONV_L2: return fwd_launch<32, 20, 20, 64, 4, 2, 9, 9, false>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
-        case CONV_L3: return fwd_launch<64, 9, 9, 64, 3, 1, 7, 7, false>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
+        case CONV_S1: return fwd_launch<4, 84, 84, 16, 8, 4, 20, 20, true, 16>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
+        case CONV_S2: return fwd_launch<16, 20, 20, 32, 4, 2, 9, 9, false, 32>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
+        case CONV_L1: return fwd_launch<4, 84, 84, 32, 8, 4, 20, 20, true, 32>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
+        case CONV_L2: return fwd_launch<32, 20, 20, 64, 4, 2, 9, 9, false, 32>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
+        case CONV_L3: return fwd_launch<64, 9, 9, 64, 3, 1, 7, 7, false, 16>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
         default: return hipErrorInvalidValue;
     }
 }
 
 int conv_wgrad_chunks(ConvId id, int batch) {
+    WgradShape w;
     switch (id) {
-        case CONV_S1: return target_chunks(batch, wgrad_groups<4, 84, 84, 16, 8, 4, 20, 20>());
-        case CONV_S2: return target_chunks(batch, wgrad_groups<16, 20, 20, 32, 4, 2, 9, 9>());
-        case CONV_L1: return target_chunks(batch, wgrad_groups<4, 84, 84, 32, 8, 4, 20, 20>());
-        case CONV_L2: return target_chunks(batch, wgrad_groups<32, 20, 20, 64, 4, 2, 9, 9>());
-        case CONV_L3: return target_chunks(batch, wgrad_groups<64, 9, 9, 64, 3, 1, 7, 7>());
+        case CONV_S1: w = wgrad_shape(batch, wgrad_groups<4, 84, 84, 16, 8, 4, 20, 20>(), 20); break;
+        case CONV_S2: w = wgrad_shape(batch, wgrad_groups<16, 20, 20, 32, 4, 2, 9, 9>(), 9); break;
+        case CONV_L1: w = wgrad_shape(batch, wgrad_groups<4, 84, 84, 32, 8, 4, 20, 20>(), 20); break;
+        case CONV_L2: w = wgrad_shape(batch, wgrad_groups<32, 20, 20, 64, 4, 2, 9, 9>(), 9); break;
+        case CONV_L3: w = wgrad_shape(batch, wgrad_groups<64, 9, 9, 64, 3, 1, 7, 7>(), 7); break;
         default: return -1;
     }
+    return w.chunks * w.rb;
 }
 
 hipError_t launch_conv_wgrad(ConvId id, const void* in, const float* dz, int batch, float* wpart,
@@ -435,9 +556,9 @@ hipError_t launch_conv_wgrad(ConvId id, const void* in, const float* dz, int bat
 hipError_t launch_conv_dgrad(ConvId id, const float* dz, const float* w, const float* h_in,
                              float* din, int batch, hipStream_t st) {
     switch (id) {
-        case CONV_S2: return dgrad_launch<16, 20, 20, 32, 4, 2, 9, 9>(dz, w, h_in, din, batch, st);
-        case CONV_L2: return dgrad_launch<32, 20, 20, 64, 4, 2, 9, 9>(dz, w, h_in, din, batch, st);
-        case CONV_L3: return dgrad_launch<64, 9, 9, 64, 3, 1, 7, 7>(dz, w, h_in, din, batch, st);
+        case CONV_S2: return dgrad_launch<16, 20, 20, 32, 4, 2, 9, 9, 16>(dz, w, h_in, din, batch, st);
+        case CONV_L2: return dgrad_launch<32, 20, 20, 64, 4, 2, 9, 9, 16>(dz, w, h_in, din, batch, st);
+        case CONV_L3: return dgrad_launch<64, 9, 9, 64, 3, 1, 7, 7, 16>(dz, w, h_in, din, batch, st);
         default: return hipErrorInvalidValue;
     }
 }

@@ -1,25 +1,30 @@
 // Fully connected layer contractions on fp32 MFMA: fc1 forward (split-K,
 // partial sums), fc1 weight gradient, and fc1 input gradient with the ReLU
-// mask of the last conv layer fused in.  64x64 output tiles, k-steps of 16
-// staged through LDS; four waves each own a 32x32 quadrant (2x2 MFMA tiles).
+// mask of the last conv layer fused in.  BMxBN output tiles (32 or 64 each),
+// k-steps of 32 staged through LDS with the next step's global loads issued
+// before the current step's MFMAs; four waves in a 2x2 arrangement.
 #include "common.h"
 
 namespace dqn {
 namespace {
 
-constexpr int BM = 64, BN = 64, BK = 16, LDP = BM + 4;
+constexpr int BK = 32;
 
 // TA: A(m,k) = A[k*lda + m] else A[m*lda + k].
 // TB: B(k,n) = B[n*ldb + k] else B[k*ldb + n].
-template <bool TA, bool TB, bool MASK>
+template <int BM, int BN, bool TA, bool TB, bool MASK>
 __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K,
                                                    const float* __restrict__ A, int lda,
                                                    const float* __restrict__ Bm, int ldb,
                                                    float* __restrict__ C, int ldc, int kchunk,
                                                    int64_t c_slice,
                                                    const float* __restrict__ mask) {
-    __shared__ __align__(16) float As[BK][LDP];
-    __shared__ __align__(16) float Bs[BK][LDP];
+    constexpr int TM = BM / 32, TN = BN / 32;     // MFMA tiles per wave
+    constexpr int LDA = BM + 4, LDB = BN + 4;
+    constexpr int AV = BM * BK / 4 / 256;         // float4 loads per thread per k-step
+    constexpr int BV = BN * BK / 4 / 256;
+    __shared__ __align__(16) float As[BK][LDA];
+    __shared__ __align__(16) float Bs[BK][LDB];
     const int m0 = blockIdx.x * BM;
     const int n0 = blockIdx.y * BN;
     const int z = blockIdx.z;
@@ -28,66 +33,95 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K,
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
-    const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+    const int wm = (wave >> 1) * (BM / 2), wn = (wave & 1) * (BN / 2);
 
-    f4 acc[2][2];
+    f4 ra[AV], rb[BV];
+    auto load = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+        for (int v = 0; v < AV; ++v) {
+            const int e = t + 256 * v;
+            f4 x = f4{0.f, 0.f, 0.f, 0.f};
+            if constexpr (!TA) {  // rows of A, 4 consecutive k
+                const int row = e / (BK / 4), kq = (e % (BK / 4)) * 4;
+                if (m0 + row < M && k0 + kq < kend) x = *(const f4*)(A + (size_t)(m0 + row) * lda + k0 + kq);
+            } else {              // k rows, 4 consecutive m
+                const int kr = e / (BM / 4), mq = (e % (BM / 4)) * 4;
+                if (k0 + kr < kend && m0 + mq < M) x = *(const f4*)(A + (size_t)(k0 + kr) * lda + m0 + mq);
+            }
+            ra[v] = x;
+        }
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int v = 0; v < BV; ++v) {
+            const int e = t + 256 * v;
+            f4 x = f4{0.f, 0.f, 0.f, 0.f};
+            if constexpr (!TB) {  // k rows, 4 consecutive n
+                const int kr = e / (BN / 4), nq = (e % (BN / 4)) * 4;
+                if (k0 + kr < kend && n0 + nq < N) x = *(const f4*)(Bm + (size_t)(k0 + kr) * ldb + n0 + nq);
+            } else {              // columns n, 4 consecutive k
+                const int col = e / (BK / 4), kq = (e % (BK / 4)) * 4;
+                if (n0 + col < N && k0 + kq < kend) x = *(const f4*)(Bm + (size_t)(n0 + col) * ldb + k0 + kq);
+            }
+            rb[v] = x;
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int v = 0; v < AV; ++v) {
+            const int e = t + 256 * v;
+            if constexpr (!TA) {
+                const int row = e / (BK / 4), kq = (e % (BK / 4)) * 4;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) As[kq + q][row] = ra[v][q];
+            } else {
+                const int kr = e / (BM / 4), mq = (e % (BM / 4)) * 4;
+                *(f4*)&As[kr][mq] = ra[v];
+            }
+        }
+#pragma unroll
+        for (int v = 0; v < BV; ++v) {
+            const int e = t + 256 * v;
+            if constexpr (!TB) {
+                const int kr = e / (BN / 4), nq = (e % (BN / 4)) * 4;
+                *(f4*)&Bs[kr][nq] = rb[v];
+            } else {
+                const int col = e / (BK / 4), kq = (e % (BK / 4)) * 4;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) Bs[kq + q][col] = rb[v][q];
+            }
+        }
+    };
 
+    f4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    if (kbeg < kend) load(kbeg);
     for (int k0 = kbeg; k0 < kend; k0 += BK) {
-        // ---- A tile -> As[k][m]
-        if constexpr (!TA) {
-            const int row = t >> 2, kq = (t & 3) * 4;
-            f4 v = f4{0.f, 0.f, 0.f, 0.f};
-            if (m0 + row < M && k0 + kq < kend) v = *(const f4*)(A + (size_t)(m0 + row) * lda + k0 + kq);
-            As[kq + 0][row] = v[0];
-            As[kq + 1][row] = v[1];
-            As[kq + 2][row] = v[2];
-            As[kq + 3][row] = v[3];
-        } else {
-            const int kr = t >> 4, mq = (t & 15) * 4;
-            f4 v = f4{0.f, 0.f, 0.f, 0.f};
-            if (k0 + kr < kend && m0 + mq < M) v = *(const f4*)(A + (size_t)(k0 + kr) * lda + m0 + mq);
-            *(f4*)&As[kr][mq] = v;
-        }
-        // ---- B tile -> Bs[k][n]
-        if constexpr (!TB) {
-            const int kr = t >> 4, nq = (t & 15) * 4;
-            f4 v = f4{0.f, 0.f, 0.f, 0.f};
-            if (k0 + kr < kend && n0 + nq < N) v = *(const f4*)(Bm + (size_t)(k0 + kr) * ldb + n0 + nq);
-            *(f4*)&Bs[kr][nq] = v;
-        } else {
-            const int col = t >> 2, kq = (t & 3) * 4;
-            f4 v = f4{0.f, 0.f, 0.f, 0.f};
-            if (n0 + col < N && k0 + kq < kend) v = *(const f4*)(Bm + (size_t)(n0 + col) * ldb + k0 + kq);
-            Bs[kq + 0][col] = v[0];
-            Bs[kq + 1][col] = v[1];
-            Bs[kq + 2][col] = v[2];
-            Bs[kq + 3][col] = v[3];
-        }
+        store();
         __syncthreads();
+        if (k0 + BK < kend) load(k0 + BK);   // in flight during the MFMAs below
 #pragma unroll
         for (int kk = 0; kk < BK / 4; ++kk) {
-            float a[2], b[2];
+            float a[TM], b[TN];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) a[i] = As[kk * 4 + g][wm + i * 16 + li];
+            for (int i = 0; i < TM; ++i) a[i] = As[kk * 4 + g][wm + i * 16 + li];
 #pragma unroll
-            for (int j = 0; j < 2; ++j) b[j] = Bs[kk * 4 + g][wn + j * 16 + li];
+            for (int j = 0; j < TN; ++j) b[j] = Bs[kk * 4 + g][wn + j * 16 + li];
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j) acc[i][j] = mfma16x16x4(a[i], b[j], acc[i][j]);
+                for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x4(a[i], b[j], acc[i][j]);
         }
         __syncthreads();
     }
 
     float* Cz = C + (size_t)z * c_slice;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < TN; ++j) {
             const int n = n0 + wn + j * 16 + li;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -101,29 +135,51 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K,
         }
 }
 
+template <int BM, int BN, bool TA, bool TB, bool MASK>
+void launch_tile(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
+                 int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
+                 hipStream_t st) {
+    dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((N + BN - 1) / BN), (unsigned)kslices);
+    hipLaunchKernelGGL((gemm_kernel<BM, BN, TA, TB, MASK>), grid, dim3(256), 0, st, M, N, K, A, lda,
+                       B, ldb, C, ldc, kchunk, c_slice, mask);
+}
+
+template <bool TA, bool TB, bool MASK>
+void launch_shape(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
+                  int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
+                  hipStream_t st) {
+    // Narrow tiles when the output is small, so more workgroups run.
+    const bool small_m = M <= 32;
+    const long tiles64 = (long)((M + 63) / 64) * ((N + 63) / 64) * kslices;
+    const bool small_n = tiles64 < 128 && N > 32;
+    if (small_m && small_n)
+        launch_tile<32, 32, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+    else if (small_m)
+        launch_tile<32, 64, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+    else if (small_n)
+        launch_tile<64, 32, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+    else
+        launch_tile<64, 64, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+}
+
 }  // namespace
 
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
                        const float* mask, hipStream_t st) {
-    dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((N + BN - 1) / BN), (unsigned)kslices);
-    dim3 block(256);
+    if (kchunk % BK != 0) return hipErrorInvalidValue;
     switch (kind) {
         case GEMM_NT:
-            hipLaunchKernelGGL((gemm_kernel<false, true, false>), grid, block, 0, st, M, N, K, A,
-                               lda, B, ldb, C, ldc, kchunk, c_slice, (const float*)nullptr);
+            launch_shape<false, true, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
             break;
         case GEMM_TN:
-            hipLaunchKernelGGL((gemm_kernel<true, false, false>), grid, block, 0, st, M, N, K, A,
-                               lda, B, ldb, C, ldc, kchunk, c_slice, (const float*)nullptr);
+            launch_shape<true, false, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
             break;
         case GEMM_NN:
             if (mask)
-                hipLaunchKernelGGL((gemm_kernel<false, false, true>), grid, block, 0, st, M, N, K,
-                                   A, lda, B, ldb, C, ldc, kchunk, c_slice, mask);
+                launch_shape<false, false, true>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
             else
-                hipLaunchKernelGGL((gemm_kernel<false, false, false>), grid, block, 0, st, M, N, K,
-                                   A, lda, B, ldb, C, ldc, kchunk, c_slice, (const float*)nullptr);
+                launch_shape<false, false, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
             break;
         default:
             return hipErrorInvalidValue;

@@ -1,6 +1,7 @@
-// Output head of the Q-network and the TD step of Alg. 1, one wave per
-// sample: reduce the fc1 split-K partials, add the bias and apply ReLU, run
-// the linear output layer, then either
+// Output head of the Q-network and the TD step of Alg. 1, one workgroup per
+// sample: reduce the fc1 split-K partials (one hidden unit per thread), add
+// the bias and apply ReLU, run the linear output layer with a block
+// reduction, then either
 //   (td)  form y = r (terminal) or r + gamma * max_a' Q(s', a'; theta^-),
 //         the residual delta = (Q(s, a) - y) / B, the per-sample loss term
 //         and the fc1 pre-activation gradient delta * W2[a, :] * [z1 > 0];
@@ -13,169 +14,189 @@
 namespace dqn {
 namespace {
 
+constexpr int HT = 256;  // threads per head workgroup
+
+// Sum of n strided values in a fixed association (four interleaved partial
+// sums), so independent loads are in flight together.
+__device__ __forceinline__ float sum_strided(const float* __restrict__ x, int n, int64_t stride) {
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    int c = 0;
+    for (; c + 4 <= n; c += 4) {
+        s0 += x[(int64_t)c * stride];
+        s1 += x[(int64_t)(c + 1) * stride];
+        s2 += x[(int64_t)(c + 2) * stride];
+        s3 += x[(int64_t)(c + 3) * stride];
+    }
+    for (; c < n; ++c) s0 += x[(int64_t)c * stride];
+    return (s0 + s1) + (s2 + s3);
+}
+
+// Block-wide sums of NV per-thread values; every thread gets the results.
+// Wave sums first, then the four wave results in wave order.
+template <int NV>
+__device__ __forceinline__ void block_sums(float (&v)[NV], float* red /* [4][NV] */) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        float s = wave_sum(v[k]);
+        if (lane == 0) red[wave * NV + k] = s;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < NV; ++k) v[k] = (red[k] + red[NV + k]) + (red[2 * NV + k] + red[3 * NV + k]);
+}
+
 template <int H, int A>
-__global__ __launch_bounds__(256) void head_td_kernel(HeadTdArgs p) {
-    constexpr int E = H / 64;
-    const int lane = threadIdx.x & 63;
-    const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (j >= p.B) return;
+__global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
+    constexpr int E = H / HT;
+    __shared__ float red[4 * 2 * A];
+    const int j = blockIdx.x;
     const int B = p.B;
-    float zs[E], hs[E], hn[E];
+    const int64_t slice = (int64_t)2 * B * H;
+    float zs[E], hs[E], v[2 * A];
+#pragma unroll
+    for (int k = 0; k < 2 * A; ++k) v[k] = 0.f;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const int h = lane + 64 * e;
-        float a = 0.f, b = 0.f;
-        for (int z = 0; z < p.ks; ++z) {
-            a += p.fc1p[((size_t)z * 2 * B + j) * H + h];
-            b += p.fc1p[((size_t)z * 2 * B + B + j) * H + h];
-        }
+        const int h = threadIdx.x + HT * e;
+        const float a = sum_strided(p.fc1p + (int64_t)j * H + h, p.ks, slice);
+        const float b = sum_strided(p.fc1p + (int64_t)(B + j) * H + h, p.ks, slice);
         zs[e] = a + p.b1[h];
         hs[e] = fmaxf(zs[e], 0.f);
-        hn[e] = fmaxf(b + p.b1t[h], 0.f);
-    }
-    float q[A], qn[A];
+        const float hn = fmaxf(b + p.b1t[h], 0.f);
 #pragma unroll
-    for (int k = 0; k < A; ++k) {
-        float a = 0.f, b = 0.f;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            const int h = lane + 64 * e;
-            a = fmaf(p.W2[k * H + h], hs[e], a);
-            b = fmaf(p.W2t[k * H + h], hn[e], b);
+        for (int k = 0; k < A; ++k) {
+            v[k] = fmaf(p.W2[k * H + h], hs[e], v[k]);
+            v[A + k] = fmaf(p.W2t[k * H + h], hn, v[A + k]);
         }
-        q[k] = wave_sum(a) + p.b2[k];
-        qn[k] = wave_sum(b) + p.b2t[k];
     }
-    float m = qn[0];
+    block_sums<2 * A>(v, red);
+    float m = v[A] + p.b2t[0];
 #pragma unroll
-    for (int k = 1; k < A; ++k) m = fmaxf(m, qn[k]);
+    for (int k = 1; k < A; ++k) m = fmaxf(m, v[A + k] + p.b2t[k]);
     // An action outside [0, A) is clamped so it can never index outside W2.
     const int act = min(max(p.action[j], 0), A - 1);
     const float r = p.reward[j];
     const float y = p.terminal[j] ? r : fmaf(p.gamma, m, r);
-    float qa = q[0];
+    float qa = v[0] + p.b2[0];
 #pragma unroll
-    for (int k = 1; k < A; ++k) qa = (k == act) ? q[k] : qa;
+    for (int k = 1; k < A; ++k) qa = (k == act) ? v[k] + p.b2[k] : qa;
     const float diff = qa - y;
     const float delta = diff / (float)B;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const int h = lane + 64 * e;
-        p.h1s[(size_t)j * H + h] = hs[e];
-        p.dz1[(size_t)j * H + h] = zs[e] > 0.f ? delta * p.W2[act * H + h] : 0.f;
+        const int h = threadIdx.x + HT * e;
+        p.h1s[(int64_t)j * H + h] = hs[e];
+        p.dz1[(int64_t)j * H + h] = zs[e] > 0.f ? delta * p.W2[act * H + h] : 0.f;
     }
-    if (lane == 0) {
+    if (threadIdx.x == 0) {
         p.delta[j] = delta;
         p.lossj[j] = 0.5f * diff * diff / (float)B;
         if (p.y_out) p.y_out[j] = y;
     }
-    if (p.q_out && lane < A) {
-        float v = q[0];
+    if (p.q_out && threadIdx.x < A) {
+        float q = v[0];
 #pragma unroll
-        for (int k = 1; k < A; ++k) v = (k == lane) ? q[k] : v;
-        p.q_out[(size_t)j * A + lane] = v;
+        for (int k = 1; k < A; ++k) q = (k == (int)threadIdx.x) ? v[k] : q;
+        p.q_out[(int64_t)j * A + threadIdx.x] = q + p.b2[threadIdx.x];
     }
 }
 
 template <int H, int A>
-__global__ __launch_bounds__(256) void head_fwd_kernel(HeadFwdArgs p) {
-    constexpr int E = H / 64;
-    const int lane = threadIdx.x & 63;
-    const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (j >= p.B) return;
-    float hs[E];
+__global__ __launch_bounds__(HT) void head_fwd_kernel(HeadFwdArgs p) {
+    constexpr int E = H / HT;
+    __shared__ float red[4 * A];
+    const int j = blockIdx.x;
+    const int64_t slice = (int64_t)p.B * H;
+    float v[A];
+#pragma unroll
+    for (int k = 0; k < A; ++k) v[k] = 0.f;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const int h = lane + 64 * e;
-        float a = 0.f;
-        for (int z = 0; z < p.ks; ++z) a += p.fc1p[((size_t)z * p.B + j) * H + h];
-        hs[e] = fmaxf(a + p.b1[h], 0.f);
+        const int h = threadIdx.x + HT * e;
+        const float hs = fmaxf(sum_strided(p.fc1p + (int64_t)j * H + h, p.ks, slice) + p.b1[h], 0.f);
+#pragma unroll
+        for (int k = 0; k < A; ++k) v[k] = fmaf(p.W2[k * H + h], hs, v[k]);
     }
+    block_sums<A>(v, red);
     float q[A];
 #pragma unroll
-    for (int k = 0; k < A; ++k) {
-        float a = 0.f;
-#pragma unroll
-        for (int e = 0; e < E; ++e) a = fmaf(p.W2[k * H + lane + 64 * e], hs[e], a);
-        q[k] = wave_sum(a) + p.b2[k];
-    }
+    for (int k = 0; k < A; ++k) q[k] = v[k] + p.b2[k];
     int best = 0;
     float bq = q[0];
 #pragma unroll
     for (int k = 1; k < A; ++k)
-        if (q[k] > bq) { bq = q[k]; best = k; }
+        if (q[k] > bq) {
+            bq = q[k];
+            best = k;
+        }
     if (p.thresh > 0) {
         const uint64_t w = p.draws[j];
         if ((w >> 32) < p.thresh) best = (int)(((w & 0xffffffffull) * (uint64_t)A) >> 32);
     }
-    if (lane == 0 && p.action_out) p.action_out[j] = best;
-    if (p.q_out && lane < A) {
-        float v = q[0];
+    if (threadIdx.x == 0 && p.action_out) p.action_out[j] = best;
+    if (p.q_out && threadIdx.x < A) {
+        float o = q[0];
 #pragma unroll
-        for (int k = 1; k < A; ++k) v = (k == lane) ? q[k] : v;
-        p.q_out[(size_t)j * A + lane] = v;
+        for (int k = 1; k < A; ++k) o = (k == (int)threadIdx.x) ? q[k] : o;
+        p.q_out[(int64_t)j * A + threadIdx.x] = o;
     }
 }
 
-// One thread per output value; each sums its terms in a fixed order.
+// One thread per output value; each sums its terms in a fixed association.
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
     int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     for (int l = 0; l < a.n_conv; ++l) {
         if (i < a.wcount[l]) {
-            float s = 0.f;
-            for (int c = 0; c < a.chunks[l]; ++c) s += a.wpart[l][(size_t)c * a.wcount[l] + i];
-            a.gw[l][i] = s;
+            a.gw[l][i] = sum_strided(a.wpart[l] + i, a.chunks[l], a.wcount[l]);
             return;
         }
         i -= a.wcount[l];
         if (i < a.cout[l]) {
-            float s = 0.f;
-            for (int c = 0; c < a.chunks[l]; ++c) s += a.bpart[l][(size_t)c * a.cout[l] + i];
-            a.gb[l][i] = s;
+            a.gb[l][i] = sum_strided(a.bpart[l] + i, a.chunks[l], a.cout[l]);
             return;
         }
         i -= a.cout[l];
     }
     if (i < a.H) {
-        float s = 0.f;
-        for (int j = 0; j < a.B; ++j) s += a.dz1[(size_t)j * a.H + i];
-        a.g_b1[i] = s;
+        a.g_b1[i] = sum_strided(a.dz1 + i, a.B, a.H);
         return;
     }
     i -= a.H;
     if (i < (int64_t)a.A * a.H) {
         const int k = (int)(i / a.H), h = (int)(i - (int64_t)k * a.H);
-        float s = 0.f;
-        for (int j = 0; j < a.B; ++j)
-            if (a.action[j] == k) s = fmaf(a.delta[j], a.h1s[(size_t)j * a.H + h], s);
-        a.g_W2[i] = s;
+        float s0 = 0.f, s1 = 0.f;
+        int j = 0;
+        for (; j + 2 <= a.B; j += 2) {
+            const float t0 = a.delta[j] * a.h1s[(int64_t)j * a.H + h];
+            const float t1 = a.delta[j + 1] * a.h1s[(int64_t)(j + 1) * a.H + h];
+            s0 += a.action[j] == k ? t0 : 0.f;
+            s1 += a.action[j + 1] == k ? t1 : 0.f;
+        }
+        if (j < a.B) s0 += a.action[j] == k ? a.delta[j] * a.h1s[(int64_t)j * a.H + h] : 0.f;
+        a.g_W2[i] = s0 + s1;
         return;
     }
     i -= (int64_t)a.A * a.H;
     if (i < a.A) {
         float s = 0.f;
-        for (int j = 0; j < a.B; ++j)
-            if (a.action[j] == (int)i) s += a.delta[j];
+        for (int j = 0; j < a.B; ++j) s += a.action[j] == (int)i ? a.delta[j] : 0.f;
         a.g_b2[i] = s;
         return;
     }
     i -= a.A;
-    if (i == 0) {
-        float s = 0.f;
-        for (int j = 0; j < a.B; ++j) s += a.lossj[j];
-        a.loss_out[0] = s;
-    }
+    if (i == 0) a.loss_out[0] = sum_strided(a.lossj, a.B, 1);
 }
 
 template <int H, int A>
 hipError_t td_launch(const HeadTdArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL((head_td_kernel<H, A>), dim3((unsigned)((a.B + 3) / 4)), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((head_td_kernel<H, A>), dim3((unsigned)a.B), dim3(HT), 0, st, a);
     return hipGetLastError();
 }
 
 template <int H, int A>
 hipError_t fwd_launch(const HeadFwdArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL((head_fwd_kernel<H, A>), dim3((unsigned)((a.B + 3) / 4)), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((head_fwd_kernel<H, A>), dim3((unsigned)a.B), dim3(HT), 0, st, a);
     return hipGetLastError();
 }
 
