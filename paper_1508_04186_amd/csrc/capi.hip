@@ -75,9 +75,10 @@ inline int64_t act_elems(const ConvDims& c) { return (int64_t)c.cout * c.oh * c.
 
 // fc1 forward split-K: enough slices that the launch covers the chip.
 void fc1_split(int rows, int H, int K, int* ks, int* kchunk) {
+    // Few enough slices that the head's reduction stays short.
     const int tiles = ((rows + 63) / 64) * ((H + 63) / 64);
-    int want = std::max(1, 256 / tiles);
-    want = std::min(want, std::max(1, K / 64));
+    int want = std::max(1, 128 / tiles);
+    want = std::min(want, 16);
     int kc = (K + want - 1) / want;
     kc = (kc + 31) / 32 * 32;  // whole k-steps of the GEMM kernel
     *kchunk = kc;

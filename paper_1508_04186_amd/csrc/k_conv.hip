@@ -13,16 +13,58 @@ namespace {
 
 constexpr int WG = 256;  // 4 waves
 
-// Copy `words` 32-bit words from global to LDS; 16-byte accesses when both
-// sides are 16-byte aligned and the length is a multiple of four words.
-__device__ __forceinline__ void stage_words(uint32_t* __restrict__ dst, const uint32_t* __restrict__ src,
-                                            int words) {
-    if ((((uintptr_t)src | (uintptr_t)dst) & 15) == 0 && (words & 3) == 0) {
-        const f4* s4 = (const f4*)src;
-        f4* d4 = (f4*)dst;
-        for (int e = threadIdx.x; e < words / 4; e += WG) d4[e] = s4[e];
+// Stage CH rows of `bytes` bytes each from global (row c at src + c*sstride)
+// into LDS (row c at dst + c*dstride).  16-byte accesses when every address
+// is 16-byte aligned, else 4-byte; each thread issues up to U loads before
+// its first LDS store, so the copies of all rows are in flight together.
+template <int U = 8>
+__device__ __forceinline__ void stage_rows(unsigned char* __restrict__ dst, int dstride,
+                                           const unsigned char* __restrict__ src, int64_t sstride,
+                                           int ch, int bytes) {
+    const bool v16 = ((((uintptr_t)src | (uintptr_t)dst | (uintptr_t)sstride | (uintptr_t)dstride |
+                        (uintptr_t)bytes) & 15) == 0);
+    if (v16) {
+        const int per = bytes / 16, n = ch * per;
+        for (int base = threadIdx.x; base < n; base += U * WG) {
+            f4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int i = base + u * WG;
+                if (i < n) {
+                    const int c = i / per, r = i - c * per;
+                    v[u] = *(const f4*)(src + c * sstride + 16 * r);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int i = base + u * WG;
+                if (i < n) {
+                    const int c = i / per, r = i - c * per;
+                    *(f4*)(dst + c * dstride + 16 * r) = v[u];
+                }
+            }
+        }
     } else {
-        for (int e = threadIdx.x; e < words; e += WG) dst[e] = src[e];
+        const int per = bytes / 4, n = ch * per;
+        for (int base = threadIdx.x; base < n; base += U * WG) {
+            uint32_t v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int i = base + u * WG;
+                if (i < n) {
+                    const int c = i / per, r = i - c * per;
+                    v[u] = *(const uint32_t*)(src + c * sstride + 4 * r);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int i = base + u * WG;
+                if (i < n) {
+                    const int c = i / per, r = i - c * per;
+                    *(uint32_t*)(dst + c * dstride + 4 * r) = v[u];
+                }
+            }
+        }
     }
 }
 
@@ -41,11 +83,24 @@ template <int CIN, int K, int CO>
 __device__ __forceinline__ void stage_weights(float* __restrict__ sw, const float* __restrict__ W, int o0) {
     using L = WLayout<CIN, K>;
     constexpr int NW = CIN * K * K;
+    constexpr int U = 8;
     const float* src = W + (size_t)o0 * NW;
-    for (int e = threadIdx.x; e < CO * NW; e += WG) {
-        const int o = e / NW, r = e - o * NW;
-        const int c = r / L::KK, k = r - c * L::KK;
-        sw[o * L::RO + c * L::RC + k] = src[e];
+    for (int base = threadIdx.x; base < CO * NW; base += U * WG) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = base + u * WG;
+            if (e < CO * NW) v[u] = src[e];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = base + u * WG;
+            if (e < CO * NW) {
+                const int o = e / NW, r = e - o * NW;
+                const int c = r / L::KK, k = r - c * L::KK;
+                sw[o * L::RO + c * L::RC + k] = v[u];
+            }
+        }
     }
 }
 
@@ -107,13 +162,8 @@ __global__ __launch_bounds__(WG) void conv_fwd_kernel(
             stage_weights<CIN, K, CO>(sw, second ? w_b : w_a, o0);
             staged_w = second;
         }
-        {
-            const int words_per_ch = rows * IW * ESZ / 4;
-            const int row_words = in_rows_max * IW * ESZ / 4;
-            for (int c = 0; c < CIN; ++c)
-                stage_words((uint32_t*)sin + c * row_words,
-                            (const uint32_t*)(src + ((size_t)c * IH * IW + iy0 * IW) * ESZ), words_per_ch);
-        }
+        stage_rows(sin, in_rows_max * IW * ESZ, src + (size_t)iy0 * IW * ESZ, (int64_t)IH * IW * ESZ,
+                   CIN, rows * IW * ESZ);
         __syncthreads();
         const float* bias = second ? bias_b : bias_a;
         const int row_elems = in_rows_max * IW;
@@ -242,14 +292,23 @@ __global__ __launch_bounds__(WG) void conv_wgrad_kernel(
         __syncthreads();
         {
             const unsigned char* src = (const unsigned char*)in + (size_t)j * CIN * IH * IW * ESZ;
-            const int words_per_ch = rows * IW * ESZ / 4;
-            for (int c = 0; c < CIN; ++c)
-                stage_words((uint32_t*)s_in + c * (row_elems * ESZ / 4),
-                            (const uint32_t*)(src + ((size_t)c * IH * IW + iy0 * IW) * ESZ), words_per_ch);
+            stage_rows(s_in, row_elems * ESZ, src + (size_t)iy0 * IW * ESZ, (int64_t)IH * IW * ESZ, CIN,
+                       rows * IW * ESZ);
             const float* dzj = dz + (size_t)j * COUT * P + pbeg;
-            for (int e = threadIdx.x; e < COUT * pix_pad; e += WG) {
-                const int o = e / pix_pad, q = e - o * pix_pad;
-                s_dz[e] = q < npix ? dzj[(size_t)o * P + q] : 0.f;
+            constexpr int U = 8;
+            for (int base = threadIdx.x; base < COUT * pix_pad; base += U * WG) {
+                float v[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int e = base + u * WG;
+                    const int o = e / pix_pad, q = e - o * pix_pad;
+                    v[u] = (e < COUT * pix_pad && q < npix) ? dzj[(size_t)o * P + q] : 0.f;
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int e = base + u * WG;
+                    if (e < COUT * pix_pad) s_dz[e] = v[u];
+                }
             }
         }
         __syncthreads();
@@ -331,21 +390,47 @@ __global__ __launch_bounds__(WG) void conv_dgrad_kernel(
     const int c0 = cib * CI;
 
     const float* dzn = dz + (size_t)n * COUT * OH * OW;
-    for (int e = threadIdx.x; e < COUT * PH * PW; e += WG) {
-        const int o = e / (PH * PW);
-        const int r = e - o * (PH * PW);
-        const int yy = r / PW, xx = r - (r / PW) * PW;
-        const int y = yy - (T - 1), x = xx - (T - 1);
-        s_dz[e] = (y >= 0 && y < OH && x >= 0 && x < OW) ? dzn[(o * OH + y) * OW + x] : 0.f;
+    constexpr int U = 8;
+    for (int base = threadIdx.x; base < COUT * PH * PW; base += U * WG) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = base + u * WG;
+            const int o = e / (PH * PW);
+            const int r = e - o * (PH * PW);
+            const int yy = r / PW, xx = r - (r / PW) * PW;
+            const int y = yy - (T - 1), x = xx - (T - 1);
+            v[u] = (e < COUT * PH * PW && y >= 0 && y < OH && x >= 0 && x < OW)
+                       ? dzn[(o * OH + y) * OW + x] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = base + u * WG;
+            if (e < COUT * PH * PW) s_dz[e] = v[u];
+        }
     }
-    for (int e = threadIdx.x; e < TT * COUT * CI; e += WG) {
-        const int c = e % CI;
-        const int r = e / CI;
-        const int o = r % COUT;
-        const int tap = r / COUT;
-        const int ty = tap / T, tx = tap - (tap / T) * T;
-        s_w[(tap * COUT + o) * RCW + c] =
-            W[(((size_t)o * CIN + c0 + c) * K + py + S * ty) * K + px + S * tx];
+    for (int base = threadIdx.x; base < TT * COUT * CI; base += U * WG) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = base + u * WG;
+            const int c = e % CI;
+            const int r = e / CI;
+            const int o = r % COUT;
+            const int tap = r / COUT;
+            const int ty = tap / T, tx = tap - (tap / T) * T;
+            v[u] = e < TT * COUT * CI ? W[(((size_t)o * CIN + c0 + c) * K + py + S * ty) * K + px + S * tx]
+                                       : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = base + u * WG;
+            if (e < TT * COUT * CI) {
+                const int c = e % CI;
+                const int r = e / CI;
+                s_w[r * RCW + c] = v[u];
+            }
+        }
     }
     __syncthreads();
 

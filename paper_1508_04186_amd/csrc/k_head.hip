@@ -16,19 +16,20 @@ namespace {
 
 constexpr int HT = 256;  // threads per head workgroup
 
-// Sum of n strided values in a fixed association (four interleaved partial
-// sums), so independent loads are in flight together.
+// Sum of n strided values in a fixed association (element u of each group
+// of 16 goes to partial sum u % 4), with 16 independent loads in flight.
 __device__ __forceinline__ float sum_strided(const float* __restrict__ x, int n, int64_t stride) {
-    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
     int c = 0;
-    for (; c + 4 <= n; c += 4) {
-        s0 += x[(int64_t)c * stride];
-        s1 += x[(int64_t)(c + 1) * stride];
-        s2 += x[(int64_t)(c + 2) * stride];
-        s3 += x[(int64_t)(c + 3) * stride];
+    for (; c + 16 <= n; c += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = x[(int64_t)(c + u) * stride];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) s[u & 3] += v[u];
     }
-    for (; c < n; ++c) s0 += x[(int64_t)c * stride];
-    return (s0 + s1) + (s2 + s3);
+    for (; c < n; ++c) s[0] += x[(int64_t)c * stride];
+    return (s[0] + s[1]) + (s[2] + s[3]);
 }
 
 // Block-wide sums of NV per-thread values; every thread gets the results.
