@@ -6,6 +6,9 @@
 // lane groups fall in distinct banks) and the input rows it needs (16-byte
 // loads where aligned), then runs its MFMA loop from LDS only.
 // Activations are NCHW float32; the network input is bytes.
+#include <mutex>
+#include <unordered_map>
+
 #include "common.h"
 
 namespace dqn {
@@ -17,7 +20,7 @@ constexpr int WG = 256;  // 4 waves
 // into LDS (row c at dst + c*dstride).  16-byte accesses when every address
 // is 16-byte aligned, else 4-byte; each thread issues up to U loads before
 // its first LDS store, so the copies of all rows are in flight together.
-template <int U = 8>
+template <int U = 16>
 __device__ __forceinline__ void stage_rows(unsigned char* __restrict__ dst, int dstride,
                                            const unsigned char* __restrict__ src, int64_t sstride,
                                            int ch, int bytes) {
@@ -78,13 +81,41 @@ struct WLayout {
 };
 
 // Stage weight rows o in [o0, o0+CO) of W[COUT][CIN][K][K] into the padded
-// LDS layout.
+// LDS layout, reading 16 bytes at a time (the block is contiguous and k*k is
+// a multiple of 4, or the scalar path is taken), 16 loads in flight.
 template <int CIN, int K, int CO>
 __device__ __forceinline__ void stage_weights(float* __restrict__ sw, const float* __restrict__ W, int o0) {
     using L = WLayout<CIN, K>;
     constexpr int NW = CIN * K * K;
-    constexpr int U = 8;
+    constexpr int U = 16;
     const float* src = W + (size_t)o0 * NW;
+    if constexpr (L::KK % 4 == 0) {
+        if (((uintptr_t)src & 15) == 0) {
+            constexpr int NV = CO * NW / 4;
+            for (int base = threadIdx.x; base < NV; base += U * WG) {
+                f4 v[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int e = base + u * WG;
+                    if (e < NV) v[u] = ((const f4*)src)[e];
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int e = (base + u * WG) * 4;
+                    if (e < CO * NW) {
+                        const int o = e / NW, r = e - o * NW;
+                        const int c = r / L::KK, k = r - c * L::KK;
+                        float* d = sw + o * L::RO + c * L::RC + k;
+                        d[0] = v[u][0];
+                        d[1] = v[u][1];
+                        d[2] = v[u][2];
+                        d[3] = v[u][3];
+                    }
+                }
+            }
+            return;
+        }
+    }
     for (int base = threadIdx.x; base < CO * NW; base += U * WG) {
         float v[U];
 #pragma unroll
@@ -478,15 +509,17 @@ __global__ __launch_bounds__(WG) void conv_dgrad_kernel(
 // ---------------------------------------------------------------------------
 // Host-side launch shapes.
 
-template <class Kern>
-bool allow_lds(Kern kern, size_t bytes) {
-    // Raise the dynamic LDS limit once per kernel to the largest size used.
-    static size_t granted = 0;
-    if (bytes <= granted) return true;
-    if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) !=
-        hipSuccess)
+// Raise a kernel's dynamic LDS limit to the largest size it is launched
+// with (once per kernel and size; thread-safe).
+bool allow_lds(const void* kern, size_t bytes) {
+    static std::mutex mu;
+    static std::unordered_map<const void*, size_t> granted;
+    std::lock_guard<std::mutex> lock(mu);
+    size_t& g = granted[kern];
+    if (bytes <= g) return true;
+    if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) != hipSuccess)
         return false;
-    granted = bytes;
+    g = bytes;
     return true;
 }
 
@@ -527,7 +560,7 @@ hipError_t fwd_launch(const void* in_a, const void* in_b, int n_a, int n, const 
     const size_t w_bytes = ((size_t)CO * L::RO * 4 + 15) / 16 * 16;
     const size_t lds = w_bytes + (size_t)CIN * max_rows * IW * ESZ;
     auto kern = conv_fwd_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8, CO>;
-    if (!allow_lds(kern, lds)) return hipErrorInvalidValue;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
     const int nblk = (n + spw - 1) / spw;
     hipLaunchKernelGGL(kern, dim3((unsigned)(nblk * COB * groups)), dim3(WG), lds, st, in_a, in_b, n_a,
                        n, w_a, b_a, w_b, b_b, out, mt_per_wg, spw, max_rows, in_scale);
@@ -572,7 +605,7 @@ hipError_t wgrad_launch(const void* in, const float* dz, int batch, float* wpart
     const size_t in_bytes = ((size_t)CIN * in_rows_max * IW * ESZ + 15) / 16 * 16;
     const size_t lds = in_bytes + (size_t)COUT * pix_pad * 4 + (size_t)pix_pad * 4;
     auto kern = conv_wgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8>;
-    if (!allow_lds(kern, lds)) return hipErrorInvalidValue;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(kern, dim3((unsigned)(w.chunks * w.rb * GROUPS)), dim3(WG), lds, st, in, dz,
                        batch, w.spc, w.rows_per_blk, in_rows_max, pix_pad, wpart, bpart, in_scale);
     return hipGetLastError();
@@ -592,7 +625,7 @@ hipError_t dgrad_launch(const float* dz, const float* w, const float* h_in, floa
     const int groups = (MTM + mt_per_wg - 1) / mt_per_wg;
     const size_t lds = ((size_t)COUT * PH * PW + (size_t)T * T * COUT * (CI + 1)) * 4;
     auto kern = conv_dgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, CI>;
-    if (!allow_lds(kern, lds)) return hipErrorInvalidValue;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(kern, dim3((unsigned)(wgs * groups)), dim3(WG), lds, st, dz, w, h_in, din,
                        mt_per_wg);
     return hipGetLastError();

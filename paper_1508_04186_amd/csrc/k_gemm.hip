@@ -1,18 +1,18 @@
 // Fully connected layer contractions on fp32 MFMA: fc1 forward (split-K,
 // partial sums), fc1 weight gradient, and fc1 input gradient with the ReLU
 // mask of the last conv layer fused in.  BMxBN output tiles (32 or 64 each),
-// k-steps of 32 staged through LDS with the next step's global loads issued
-// before the current step's MFMAs; four waves in a 2x2 arrangement.
+// k-steps of BK (32, or 128 for long contractions so that fewer dependent
+// global round trips are needed) staged through LDS, with the next step's
+// global loads issued before the current step's MFMAs; four waves in a 2x2
+// arrangement.
 #include "common.h"
 
 namespace dqn {
 namespace {
 
-constexpr int BK = 32;
-
 // TA: A(m,k) = A[k*lda + m] else A[m*lda + k].
 // TB: B(k,n) = B[n*ldb + k] else B[k*ldb + n].
-template <int BM, int BN, bool TA, bool TB, bool MASK>
+template <int BM, int BN, int BK, bool TA, bool TB, bool MASK>
 __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K,
                                                    const float* __restrict__ A, int lda,
                                                    const float* __restrict__ Bm, int ldb,
@@ -23,8 +23,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K,
     constexpr int LDA = BM + 4, LDB = BN + 4;
     constexpr int AV = BM * BK / 4 / 256;         // float4 loads per thread per k-step
     constexpr int BV = BN * BK / 4 / 256;
-    __shared__ __align__(16) float As[BK][LDA];
-    __shared__ __align__(16) float Bs[BK][LDB];
+    extern __shared__ __align__(16) float smem[];
+    float (*As)[LDA] = (float (*)[LDA])smem;              // [BK][LDA]
+    float (*Bs)[LDB] = (float (*)[LDB])(smem + BK * LDA); // [BK][LDB]
     const int m0 = blockIdx.x * BM;
     const int n0 = blockIdx.y * BN;
     const int z = blockIdx.z;
@@ -135,31 +136,50 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K,
         }
 }
 
-template <int BM, int BN, bool TA, bool TB, bool MASK>
-void launch_tile(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
+template <int BM, int BN, int BK, bool TA, bool TB, bool MASK>
+hipError_t launch_tile(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
                  int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
                  hipStream_t st) {
+    constexpr size_t lds = (size_t)BK * ((BM + 4) + (BN + 4)) * 4;
+    auto kern = gemm_kernel<BM, BN, BK, TA, TB, MASK>;
+    static bool granted = false;
+    if (!granted) {
+        if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+            hipSuccess)
+            return hipErrorInvalidValue;
+        granted = true;
+    }
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((N + BN - 1) / BN), (unsigned)kslices);
-    hipLaunchKernelGGL((gemm_kernel<BM, BN, TA, TB, MASK>), grid, dim3(256), 0, st, M, N, K, A, lda,
-                       B, ldb, C, ldc, kchunk, c_slice, mask);
+    hipLaunchKernelGGL(kern, grid, dim3(256), lds, st, M, N, K, A, lda, B, ldb, C, ldc, kchunk, c_slice,
+                       mask);
+    return hipGetLastError();
 }
 
-template <bool TA, bool TB, bool MASK>
-void launch_shape(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
-                  int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
-                  hipStream_t st) {
+template <int BK, bool TA, bool TB, bool MASK>
+hipError_t launch_bk(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
+               int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask, hipStream_t st) {
     // Narrow tiles when the output is small, so more workgroups run.
     const bool small_m = M <= 32;
     const long tiles64 = (long)((M + 63) / 64) * ((N + 63) / 64) * kslices;
     const bool small_n = tiles64 < 128 && N > 32;
     if (small_m && small_n)
-        launch_tile<32, 32, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+        return launch_tile<32, 32, BK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
     else if (small_m)
-        launch_tile<32, 64, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+        return launch_tile<32, 64, BK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
     else if (small_n)
-        launch_tile<64, 32, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+        return launch_tile<64, 32, BK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
     else
-        launch_tile<64, 64, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+        return launch_tile<64, 64, BK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+}
+
+template <bool TA, bool TB, bool MASK>
+hipError_t launch_shape(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
+                  int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
+                  hipStream_t st) {
+    if (kchunk >= 128)
+        return launch_bk<128, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+    else
+        return launch_bk<32, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
 }
 
 }  // namespace
@@ -167,24 +187,20 @@ void launch_shape(int M, int N, int K, const float* A, int lda, const float* B, 
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
                        const float* mask, hipStream_t st) {
-    if (kchunk % BK != 0) return hipErrorInvalidValue;
+    if (kchunk % 32 != 0) return hipErrorInvalidValue;
     switch (kind) {
         case GEMM_NT:
-            launch_shape<false, true, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
-            break;
+            return launch_shape<false, true, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
         case GEMM_TN:
-            launch_shape<true, false, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
-            break;
+            return launch_shape<true, false, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
         case GEMM_NN:
             if (mask)
-                launch_shape<false, false, true>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+                return launch_shape<false, false, true>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
             else
-                launch_shape<false, false, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
-            break;
+                return launch_shape<false, false, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
         default:
             return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 }  // namespace dqn

@@ -17,19 +17,38 @@ namespace {
 constexpr int HT = 256;  // threads per head workgroup
 
 // Sum of n strided values in a fixed association (element u of each group
-// of 16 goes to partial sum u % 4), with 16 independent loads in flight.
+// of 16 goes to partial sum u % 4; missing tail elements count as +0), with
+// 16 independent loads in flight.
 __device__ __forceinline__ float sum_strided(const float* __restrict__ x, int n, int64_t stride) {
     float s[4] = {0.f, 0.f, 0.f, 0.f};
-    int c = 0;
-    for (; c + 16 <= n; c += 16) {
+    for (int c = 0; c < n; c += 16) {
         float v[16];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = x[(int64_t)(c + u) * stride];
+        for (int u = 0; u < 16; ++u) v[u] = (c + u < n) ? x[(int64_t)(c + u) * stride] : 0.f;
 #pragma unroll
         for (int u = 0; u < 16; ++u) s[u & 3] += v[u];
     }
-    for (; c < n; ++c) s[0] += x[(int64_t)c * stride];
     return (s[0] + s[1]) + (s[2] + s[3]);
+}
+
+// The same sum split over the 8 lanes of an aligned lane group: lane q of the
+// group takes terms c = 16*(8*i + q) + u, and the group combines its lanes'
+// sums in a fixed butterfly order.  Every lane of the group gets the result.
+__device__ __forceinline__ float sum_strided_x8(const float* __restrict__ x, int n, int64_t stride) {
+    const int q = threadIdx.x & 7;
+    float s[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int c = 16 * q; c < n; c += 128) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = (c + u < n) ? x[(int64_t)(c + u) * stride] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) s[u & 3] += v[u];
+    }
+    float t = (s[0] + s[1]) + (s[2] + s[3]);
+    t += __shfl_xor(t, 1, 64);
+    t += __shfl_xor(t, 2, 64);
+    t += __shfl_xor(t, 4, 64);
+    return t;
 }
 
 // Block-wide sums of NV per-thread values; every thread gets the results.
@@ -144,49 +163,67 @@ __global__ __launch_bounds__(HT) void head_fwd_kernel(HeadFwdArgs p) {
     }
 }
 
-// One thread per output value; each sums its terms in a fixed association.
+// Eight lanes per output value; each output's terms are summed in a fixed
+// association.  Segments: conv weight and bias gradients (partial sums over
+// wgrad chunks), fc1 bias (over samples), fc2 weight and bias (over the
+// samples that took each action), and the loss.
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
-    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3;
+    const bool lead = (threadIdx.x & 7) == 0;
     for (int l = 0; l < a.n_conv; ++l) {
         if (i < a.wcount[l]) {
-            a.gw[l][i] = sum_strided(a.wpart[l] + i, a.chunks[l], a.wcount[l]);
+            const float v = sum_strided_x8(a.wpart[l] + i, a.chunks[l], a.wcount[l]);
+            if (lead) a.gw[l][i] = v;
             return;
         }
         i -= a.wcount[l];
         if (i < a.cout[l]) {
-            a.gb[l][i] = sum_strided(a.bpart[l] + i, a.chunks[l], a.cout[l]);
+            const float v = sum_strided_x8(a.bpart[l] + i, a.chunks[l], a.cout[l]);
+            if (lead) a.gb[l][i] = v;
             return;
         }
         i -= a.cout[l];
     }
     if (i < a.H) {
-        a.g_b1[i] = sum_strided(a.dz1 + i, a.B, a.H);
+        const float v = sum_strided_x8(a.dz1 + i, a.B, a.H);
+        if (lead) a.g_b1[i] = v;
         return;
     }
     i -= a.H;
     if (i < (int64_t)a.A * a.H) {
         const int k = (int)(i / a.H), h = (int)(i - (int64_t)k * a.H);
+        const int q = threadIdx.x & 7;
         float s0 = 0.f, s1 = 0.f;
-        int j = 0;
-        for (; j + 2 <= a.B; j += 2) {
-            const float t0 = a.delta[j] * a.h1s[(int64_t)j * a.H + h];
-            const float t1 = a.delta[j + 1] * a.h1s[(int64_t)(j + 1) * a.H + h];
-            s0 += a.action[j] == k ? t0 : 0.f;
-            s1 += a.action[j + 1] == k ? t1 : 0.f;
+        for (int j = q; j < a.B; j += 16) {
+            const float t0 = a.action[j] == k ? a.delta[j] * a.h1s[(int64_t)j * a.H + h] : 0.f;
+            const float t1 = (j + 8 < a.B && a.action[j + 8] == k)
+                                 ? a.delta[j + 8] * a.h1s[(int64_t)(j + 8) * a.H + h] : 0.f;
+            s0 += t0;
+            s1 += t1;
         }
-        if (j < a.B) s0 += a.action[j] == k ? a.delta[j] * a.h1s[(int64_t)j * a.H + h] : 0.f;
-        a.g_W2[i] = s0 + s1;
+        float t = s0 + s1;
+        t += __shfl_xor(t, 1, 64);
+        t += __shfl_xor(t, 2, 64);
+        t += __shfl_xor(t, 4, 64);
+        if (lead) a.g_W2[i] = t;
         return;
     }
     i -= (int64_t)a.A * a.H;
     if (i < a.A) {
+        const int q = threadIdx.x & 7;
         float s = 0.f;
-        for (int j = 0; j < a.B; ++j) s += a.action[j] == (int)i ? a.delta[j] : 0.f;
-        a.g_b2[i] = s;
+        for (int j = q; j < a.B; j += 8) s += a.action[j] == (int)i ? a.delta[j] : 0.f;
+        s += __shfl_xor(s, 1, 64);
+        s += __shfl_xor(s, 2, 64);
+        s += __shfl_xor(s, 4, 64);
+        if (lead) a.g_b2[i] = s;
         return;
     }
     i -= a.A;
-    if (i == 0) a.loss_out[0] = sum_strided(a.lossj, a.B, 1);
+    if (i == 0) {
+        const float v = sum_strided_x8(a.lossj, a.B, 1);
+        if (lead) a.loss_out[0] = v;
+    }
 }
 
 template <int H, int A>
@@ -218,7 +255,7 @@ hipError_t launch_head_fwd(int H, int A, const HeadFwdArgs& a, hipStream_t st) {
 hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t st) {
     int64_t total = a.H + (int64_t)a.A * a.H + a.A + 1;
     for (int l = 0; l < a.n_conv; ++l) total += a.wcount[l] + a.cout[l];
-    hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)((total * 8 + 255) / 256)), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
