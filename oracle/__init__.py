@@ -65,13 +65,15 @@ def _lib():
                                              _P, _P, _P, _P, ctypes.c_int64, ctypes.c_int64,
                                              _P, _P, _P, _P, _P]
         lib.oracle_forward_q.argtypes = [ctypes.POINTER(_Net), _P, _P, ctypes.c_int64, _P]
+        lib.oracle_relu_margins.argtypes = [ctypes.POINTER(_Net), _P, _P, ctypes.c_int64, _P]
         lib.oracle_select_actions.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_double,
                                               _P, _P]
         lib.oracle_td_gradient.argtypes = [ctypes.POINTER(_Net), _P, _P, _P, _P, _P, _P, _P,
                                            ctypes.c_int64, ctypes.c_double, _P, _P, _P, _P, _P]
         lib.oracle_apply_update.argtypes = [ctypes.c_int32, _P, _P, _P, _P, ctypes.c_int64,
                                             ctypes.c_double, ctypes.c_double, ctypes.c_double]
-        for f in ("oracle_replay_gather", "oracle_forward_q", "oracle_select_actions",
+        for f in ("oracle_replay_gather", "oracle_forward_q", "oracle_relu_margins",
+                  "oracle_select_actions",
                   "oracle_td_gradient", "oracle_apply_update"):
             getattr(lib, f).restype = ctypes.c_int
         _LIB = lib
@@ -144,6 +146,18 @@ def forward_q(net, theta, states) -> np.ndarray:
     _check(_lib().oracle_forward_q(ctypes.byref(_net(net)), th.ctypes.data, st.ctypes.data, B,
                                    q.ctypes.data), "oracle_forward_q")
     return q
+
+
+def relu_margins(net, theta, states) -> np.ndarray:
+    """Per-sample smallest normalized ReLU margin |z| / (|b| + sum |w x|) of
+    Q(state; theta) over every conv and hidden fc unit (float64)."""
+    th = np.ascontiguousarray(theta, dtype=np.float64)
+    st = np.ascontiguousarray(states, dtype=np.uint8)
+    B = st.shape[0]
+    m = np.empty(B, np.float64)
+    _check(_lib().oracle_relu_margins(ctypes.byref(_net(net)), th.ctypes.data, st.ctypes.data, B,
+                                      m.ctypes.data), "oracle_relu_margins")
+    return m
 
 
 def select_actions(q, epsilon, draws=None) -> np.ndarray:

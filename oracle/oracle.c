@@ -228,6 +228,89 @@ static void forward_one(const oracle_net* net, const shapes_t* sh, const double*
 }
 
 /* ------------------------------------------------------------------------ */
+/* How close each sample's forward pass comes to a ReLU kink.  For every ReLU
+ * unit u (conv layers and the hidden fc layer) with pre-activation
+ * z_u = b_u + sum_k w_uk x_k, the normalized margin is
+ * |z_u| / (|b_u| + sum_k |w_uk x_k|): the distance to the kink in units of
+ * the magnitude of the terms summed, which is the scale of any rounding
+ * error in z_u.  Where it is below the working precision the ReLU derivative
+ * is not decided by the arithmetic, and two correct implementations may
+ * differ there.  Used by the tests to tell unique gradients from
+ * precision-ambiguous ones. */
+
+static double margin_of(double z, double den) {
+    return den > 0.0 ? fabs(z) / den : (z == 0.0 ? 0.0 : INFINITY);
+}
+
+static void margin_one(const oracle_net* net, const shapes_t* sh, const double* th,
+                       const uint8_t* state, acts_t* a, double* out) {
+    double m = INFINITY;
+    int64_t n_in = (int64_t)sh->c[0] * sh->h[0] * sh->w[0];
+    for (int64_t i = 0; i < n_in; ++i) a->act[0][i] = (double)state[i] / 255.0;
+    for (int l = 0; l < net->n_conv; ++l) {
+        const double* W = th + sh->w_off[l];
+        const double* b = th + sh->b_off[l];
+        const int C = sh->c[l], H = sh->h[l], Wd = sh->w[l], O = sh->c[l + 1];
+        const int k = net->conv_k[l], s = net->conv_stride[l], OH = sh->h[l + 1], OW = sh->w[l + 1];
+        for (int o = 0; o < O; ++o)
+            for (int y = 0; y < OH; ++y)
+                for (int x = 0; x < OW; ++x) {
+                    double z = b[o], den = fabs(b[o]);
+                    for (int c = 0; c < C; ++c)
+                        for (int ky = 0; ky < k; ++ky)
+                            for (int kx = 0; kx < k; ++kx) {
+                                double t = W[((o * C + c) * k + ky) * k + kx] *
+                                           a->act[l][(c * H + s * y + ky) * Wd + s * x + kx];
+                                z += t;
+                                den += fabs(t);
+                            }
+                    double mu = margin_of(z, den);
+                    if (mu < m) m = mu;
+                    a->act[l + 1][(o * OH + y) * OW + x] = relu(z);
+                }
+    }
+    int L = net->n_conv;
+    const double* W1 = th + sh->w_off[L];
+    const double* b1 = th + sh->b_off[L];
+    for (int h = 0; h < net->fc_hidden; ++h) {
+        double z = b1[h], den = fabs(b1[h]);
+        for (int64_t i = 0; i < sh->flat; ++i) {
+            double t = W1[(int64_t)h * sh->flat + i] * a->act[L][i];
+            z += t;
+            den += fabs(t);
+        }
+        double mu = margin_of(z, den);
+        if (mu < m) m = mu;
+    }
+    *out = m;
+}
+
+/* margin_out[j] = smallest normalized ReLU margin of Q(states[j]; theta). */
+int oracle_relu_margins(const oracle_net* net, const double* theta, const uint8_t* states,
+                        int64_t batch, double* margin_out) {
+    shapes_t sh;
+    if (make_shapes(net, &sh) != ORACLE_OK || !theta || !states || !margin_out || batch < 0)
+        return ORACLE_EINVAL;
+    int64_t in_bytes = (int64_t)sh.c[0] * sh.h[0] * sh.w[0];
+    int err = ORACLE_OK;
+    #pragma omp parallel
+    {
+        acts_t a;
+        int e = acts_alloc(net, &sh, &a);
+        if (e != ORACLE_OK) {
+            #pragma omp atomic write
+            err = e;
+        } else {
+            #pragma omp for schedule(static)
+            for (int64_t j = 0; j < batch; ++j)
+                margin_one(net, &sh, theta, states + j * in_bytes, &a, margin_out + j);
+        }
+        acts_free(net, &a);
+    }
+    return err;
+}
+
+/* ------------------------------------------------------------------------ */
 
 /* Minibatch gather from a replay memory (Sec. III.C, Alg. 1).  Record i
  * starts at frames + i * record_stride and holds rec_bytes bytes (the

@@ -70,3 +70,18 @@ def check_actions(act_gpu, q_gpu, q_ref, act_ref, explore_mask, tol=FP32_TOL):
         chosen = q_ref[rows, act_gpu[rows]]
         assert np.all(chosen >= q_ref[rows].max(axis=1) - band[rows]), "near-tie action not near max"
     return int(near.sum())
+
+
+# Normalized ReLU margin below which float32 rounding may decide a ReLU
+# derivative differently from the float64 oracle (the derivative at a
+# pre-activation within rounding of zero is not fixed by the arithmetic).
+# float32 errors in a pre-activation are ~1e-7 of the magnitude of its
+# terms; 1e-6 leaves a factor of ten.
+MARGIN_MIN = 1e-6
+
+
+def split_by_margin(net_shape, theta, states):
+    """Boolean mask: True where the oracle's smallest normalized ReLU margin of
+    Q(state; theta) is at least MARGIN_MIN (the gradient is then unique)."""
+    import oracle
+    return oracle.relu_margins(net_shape, theta, states) >= MARGIN_MIN

@@ -442,3 +442,55 @@ def test_frames_are_pure_function_of_index():
     assert whole.max() >= 192 and np.median(whole) <= 8
     # rectangles move within a segment and are redrawn at segment boundaries
     assert not np.array_equal(whole[10], whole[11])
+
+
+# ---------------------------------------------------------------------------
+# Normalized ReLU margins (used to tell unique gradients from ones that the
+# working precision does not decide).
+
+def np_margins(net, theta, states):
+    th = np.asarray(theta, np.float64)
+    sl = net.slices()
+    B = states.shape[0]
+    x = states.astype(np.float64) / 255.0
+    m = np.full(B, np.inf)
+    for i, (cin, ih, iw, cout, k, s, oh, ow) in enumerate(net.conv_dims()):
+        o, shp = sl[f"conv{i+1}.W"]
+        Wt = th[o:o + np.prod(shp)].reshape(cout, -1)
+        ob, bs = sl[f"conv{i+1}.b"]
+        b = th[ob:ob + bs[0]]
+        win = np.lib.stride_tricks.sliding_window_view(x, (k, k), axis=(2, 3))[:, :, ::s, ::s][:, :, :oh, :ow]
+        cols = win.transpose(0, 2, 3, 1, 4, 5).reshape(B, oh * ow, -1)
+        z = cols @ Wt.T + b
+        den = np.abs(cols) @ np.abs(Wt).T + np.abs(b)
+        m = np.minimum(m, (np.abs(z) / den).reshape(B, -1).min(axis=1))
+        x = np.maximum(z, 0).transpose(0, 2, 1).reshape(B, cout, oh, ow)
+    flat = x.reshape(B, -1)
+    o, shp = sl["fc1.W"]; W1 = th[o:o + np.prod(shp)].reshape(shp)
+    o, shp = sl["fc1.b"]; b1 = th[o:o + shp[0]]
+    z = flat @ W1.T + b1
+    den = np.abs(flat) @ np.abs(W1).T + np.abs(b1)
+    return np.minimum(m, (np.abs(z) / den).min(axis=1))
+
+
+@pytest.mark.parametrize("net", TINY_NETS, ids=lambda n: str(n.conv))
+def test_relu_margins_match_independent_formulation(net):
+    th = di.xavier_theta(net, 31, bias_scale=0.1)
+    st = di.random_states(5, 32, net.in_c, net.in_h, net.in_w)
+    assert np.allclose(oracle.relu_margins(net, th, st), np_margins(net, th, st), rtol=1e-10, atol=0)
+
+
+def test_relu_margin_hand_worked():
+    # conv 1@1x1/1 with weight 1 and bias -x0 puts pixel 0 exactly on the
+    # kink (margin 0); the other pixels have margin |x - x0| / (|x| + x0).
+    net = di.tiny_net(1, 2, 2, ((1, 1, 1),), 1, 1)
+    st = np.array([[[[51, 102], [153, 255]]]], np.uint8)
+    x0 = 51 / 255.0
+    th = np.zeros(net.param_count())
+    sl = net.slices()
+    th[sl["conv1.W"][0]] = 1.0
+    th[sl["conv1.b"][0]] = -x0
+    th[sl["fc1.b"][0]] = 1.0           # fc1 unit: z = 1, margin 1
+    assert oracle.relu_margins(net, th, st)[0] == 0.0
+    th[sl["conv1.b"][0]] = -0.5 * x0   # now the smallest is pixel 0: (x0/2) / (1.5 x0) = 1/3
+    assert np.isclose(oracle.relu_margins(net, th, st)[0], 1.0 / 3.0, rtol=1e-15)
