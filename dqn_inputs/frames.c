@@ -6,7 +6,8 @@
  * screens (Sec. III.A, Sec. V.A): a dark background with uniform noise in
  * 0..8 and one to four bright rectangles (2..4 rows by 4..16 columns,
  * brightness 192..255) that move with a constant velocity in {-2..2}^2 and
- * bounce off the borders.  The frame stream is cut into segments of 100
+ * bounce off the borders.  Noise takes 16 hash bits per pixel, four pixels
+ * per hash.  The frame stream is cut into segments of 100
  * frames; each segment draws fresh rectangles.
  *
  * Every byte is a pure function of (seed, frame index t, y, x), so any frame
@@ -75,22 +76,22 @@ static int segment_rects(uint64_t seed, int64_t t, rect_t* out) {
 }
 
 static void one_frame(uint64_t seed, int64_t t, uint8_t* dst) {
+    /* background noise for every pixel, then the rectangles on top (the
+     * brightest one wins where they overlap) */
+    uint64_t quad0 = (uint64_t)t * (uint64_t)(FRAME_H * FRAME_W / 4);
+    for (int q = 0; q < FRAME_H * FRAME_W / 4; ++q) {
+        uint64_t h = synth_hash(seed, STREAM_NOISE, quad0 + (uint64_t)q);
+        for (int k = 0; k < 4; ++k)   /* 16 bits per pixel -> uniform 0..8 */
+            dst[4 * q + k] = (uint8_t)((((h >> (16 * k)) & 0xffffu) * 9u) >> 16);
+    }
     rect_t rc[4];
     int n = segment_rects(seed, t, rc);
-    uint64_t pix0 = (uint64_t)t * (uint64_t)(FRAME_H * FRAME_W);
-    for (int y = 0; y < FRAME_H; ++y) {
-        for (int x = 0; x < FRAME_W; ++x) {
-            int v = -1;
-            for (int r = 0; r < n; ++r) {
-                if (y >= rc[r].y && y < rc[r].y + rc[r].h &&
-                    x >= rc[r].x && x < rc[r].x + rc[r].w && rc[r].bright > v)
-                    v = rc[r].bright;
+    for (int r = 0; r < n; ++r)
+        for (int y = rc[r].y; y < rc[r].y + rc[r].h; ++y)
+            for (int x = rc[r].x; x < rc[r].x + rc[r].w; ++x) {
+                uint8_t* d = dst + y * FRAME_W + x;
+                if (*d < 192 || *d < rc[r].bright) *d = (uint8_t)rc[r].bright;
             }
-            if (v < 0)
-                v = (int)bounded(synth_hash(seed, STREAM_NOISE, pix0 + (uint64_t)(y * FRAME_W + x)), 9);
-            dst[y * FRAME_W + x] = (uint8_t)v;
-        }
-    }
 }
 
 /* Writes frames t0 .. t0+count-1, each 84*84 bytes, back to back into out. */

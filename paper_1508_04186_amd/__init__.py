@@ -2,8 +2,9 @@
 
 Thin Python binding over libdqn.so: the same entry points as the C ABI in
 include/dqn.h (replay_gather, dqn_forward, dqn_td_gradient, ps_apply_update
-and the layout/workspace queries), with torch tensors for device memory and
-streams.  All arithmetic runs in the library's HIP kernels; there is no CPU
+and the layout/workspace queries) and include/dqn_train.h (the worker and
+parameter-server loops dqn_train_steps and dqn_train_replicas), with torch
+tensors for device memory and streams.  All arithmetic runs in the library's HIP kernels; there is no CPU
 or PyTorch fallback, and loading fails loudly when the library is missing.
 """
 from .native import (  # noqa: F401
@@ -13,4 +14,6 @@ from .native import (  # noqa: F401
     lib, lib_path, dqn_param_count, dqn_param_offset, dqn_workspace_bytes,
     replay_gather, dqn_forward, dqn_td_gradient, ps_apply_update, dqn_status_string,
     workspace, profile_attach, profile_used, KERNEL_NAMES,
+    dqn_train_workspace_bytes, dqn_train_ring_stride, dqn_train_steps, dqn_train_replicas,
+    HipStreams,
 )

@@ -112,6 +112,8 @@ hipError_t launch_gather(const uint8_t* frames, int64_t stride, int64_t rec_byte
                          const int64_t* idx, int batch, uint8_t* s, uint8_t* sn, int32_t* a,
                          float* r, uint8_t* t, hipStream_t st);
 
+hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t st);
+
 hipError_t launch_apply(int rule, const float* th_in, float* th_out, float* state, const float* g,
                         int64_t n, float lr, float decay, float eps, hipStream_t st);
 

@@ -52,7 +52,26 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ th
     }
 }
 
+// Target-network refresh: dst <- src over n floats (a kernel rather than a
+// runtime copy, so it records as an ordinary node under graph capture).
+__global__ __launch_bounds__(256) void copy_kernel(const float* __restrict__ src,
+                                                   float* __restrict__ dst, int64_t n) {
+    const int64_t n4 = n / 4;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += stride)
+        ((f4*)dst)[i] = ((const f4*)src)[i];
+    if (blockIdx.x == 0 && threadIdx.x < (n & 3)) dst[n4 * 4 + threadIdx.x] = src[n4 * 4 + threadIdx.x];
+}
+
 }  // namespace
+
+hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t st) {
+    int64_t blocks = (n / 4 + 255) / 256;
+    if (blocks < 1) blocks = 1;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(copy_kernel, dim3((unsigned)blocks), dim3(256), 0, st, src, dst, n);
+    return hipGetLastError();
+}
 
 hipError_t launch_apply(int rule, const float* th_in, float* th_out, float* state, const float* g,
                         int64_t n, float lr, float decay, float eps, hipStream_t st) {

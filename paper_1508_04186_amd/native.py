@@ -105,6 +105,21 @@ def lib():
             getattr(L, f).restype = ctypes.c_int
         L.dqn_status_string.argtypes = [ctypes.c_int]
         L.dqn_status_string.restype = ctypes.c_char_p
+        L.dqn_train_ring_stride.argtypes = [ctypes.POINTER(_CNet)]
+        L.dqn_train_ring_stride.restype = ctypes.c_int64
+        L.dqn_train_workspace_bytes.argtypes = [ctypes.POINTER(_CNet), ctypes.c_int32, ctypes.c_int32]
+        L.dqn_train_workspace_bytes.restype = ctypes.c_int64
+        L.dqn_train_steps.argtypes = [ctypes.POINTER(_CNet), _P, _P, _P, ctypes.c_int32,
+                                      ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                      ctypes.POINTER(_CReplay), _P, ctypes.c_int32, ctypes.c_int64,
+                                      ctypes.c_int64, ctypes.c_int64, _P, _P, ctypes.c_size_t, _P]
+        L.dqn_train_steps.restype = ctypes.c_int
+        L.dqn_train_replicas.argtypes = [ctypes.POINTER(_CNet), _P, _P, ctypes.c_int32,
+                                         ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                         ctypes.c_float, ctypes.POINTER(_CReplay), _P,
+                                         ctypes.c_int32, ctypes.c_int64, ctypes.c_int32,
+                                         ctypes.c_int32, _P, _P, ctypes.c_size_t, _P]
+        L.dqn_train_replicas.restype = ctypes.c_int
         L.dqn_profile_attach.argtypes = [ctypes.c_int32, _P, ctypes.c_int32]
         L.dqn_profile_attach.restype = ctypes.c_int
         L.dqn_profile_used.argtypes = [ctypes.c_int32]
@@ -179,6 +194,20 @@ def workspace(net, batch: int, op: int, device="cuda"):
     """A device workspace tensor large enough for (net, batch, op)."""
     import torch
     return torch.empty(dqn_workspace_bytes(net, batch, op), dtype=torch.uint8, device=device)
+
+
+def _creplay(replay: Replay) -> _CReplay:
+    import torch
+    rp = _CReplay()
+    rp.frames = _ptr(replay.frames, torch.uint8, "replay.frames")
+    rp.action = _ptr(replay.action, torch.uint8, "replay.action")
+    rp.reward = _ptr(replay.reward, torch.int8, "replay.reward")
+    rp.terminal = _ptr(replay.terminal, torch.uint8, "replay.terminal")
+    rec = replay.c * replay.h * replay.w
+    rp.record_stride = replay.record_stride if replay.record_stride is not None else rec
+    rp.size = replay.size
+    rp.c, rp.h, rp.w = replay.c, replay.h, replay.w
+    return rp
 
 
 def replay_gather(replay: Replay, idx, s_out, s_next_out=None, a_out=None, r_out=None,
@@ -266,6 +295,110 @@ def ps_apply_update(rule, theta_in, theta_out, state, grad, lr, decay=0.9, eps=0
                                _ptr(state, torch.float32, "state"), _ptr(grad, torch.float32, "grad"),
                                n, float(lr), float(decay), float(eps), _stream(stream))
     _check(rc, "ps_apply_update")
+
+
+# ----------------------------------------------------------------------------
+# Worker and parameter-server loops (include/dqn_train.h)
+
+class HipStreams:
+    """n distinct HIP streams at the default priority (torch's stream pool may
+    hand out the same stream twice).  They synchronize with the legacy
+    default stream like torch's own; release them with close()."""
+
+    def __init__(self, n: int):
+        import torch
+        path = os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so")
+        self._hip = ctypes.CDLL(path if os.path.exists(path) else "libamdhip64.so")
+        self._hip.hipStreamCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self._hip.hipStreamCreate.restype = ctypes.c_int
+        self._hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+        self._hip.hipStreamDestroy.restype = ctypes.c_int
+        torch.cuda.init()
+        self.handles = []
+        for _ in range(n):
+            h = ctypes.c_void_p()
+            if self._hip.hipStreamCreate(ctypes.byref(h)) != 0:
+                self.close()
+                raise RuntimeError("hipStreamCreate failed")
+            self.handles.append(h.value)
+
+    def close(self):
+        for h in self.handles:
+            self._hip.hipStreamDestroy(h)
+        self.handles = []
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def dqn_train_ring_stride(net) -> int:
+    v = lib().dqn_train_ring_stride(ctypes.byref(_cnet(net)))
+    _check(0 if v >= 0 else v, "dqn_train_ring_stride")
+    return int(v)
+
+
+def dqn_train_workspace_bytes(net, batch: int, replicas: int = 1) -> int:
+    v = lib().dqn_train_workspace_bytes(ctypes.byref(_cnet(net)), batch, replicas)
+    _check(0 if v >= 0 else v, "dqn_train_workspace_bytes")
+    return int(v)
+
+
+def dqn_train_steps(net, theta, theta_target, opt_state, rule, lr, decay, eps, gamma, replay, idx,
+                    step0=0, target_period=0, losses_out=None, ws=None, stream=None):
+    """idx: device int64 [n_steps][batch]."""
+    import torch
+    rule = _RULES.get(rule, rule)
+    n_steps, batch = idx.shape
+    P = dqn_param_count(net)
+    if ws is None:
+        ws = torch.empty(dqn_train_workspace_bytes(net, batch, 1), dtype=torch.uint8,
+                         device=theta.device)
+    for name, t, n in (("theta", theta, P), ("theta_target", theta_target, P),
+                       ("opt_state", opt_state, P), ("losses_out", losses_out, n_steps)):
+        if t is not None and t.numel() < n:
+            raise ValueError(f"{name} too small")
+    rc = lib().dqn_train_steps(ctypes.byref(_cnet(net)), _ptr(theta, torch.float32, "theta"),
+                               _ptr(theta_target, torch.float32, "theta_target"),
+                               _ptr(opt_state, torch.float32, "opt_state"), int(rule), float(lr),
+                               float(decay), float(eps), float(gamma), ctypes.byref(_creplay(replay)),
+                               _ptr(idx, torch.int64, "idx"), batch, n_steps, int(step0),
+                               int(target_period), _ptr(losses_out, torch.float32, "losses_out"),
+                               _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream))
+    _check(rc, "dqn_train_steps")
+
+
+def dqn_train_replicas(net, theta_ring, opt_state, rule, lr, decay, eps, gamma, replay, idx,
+                       replicas, staleness, streams, losses_out=None, ws=None):
+    """theta_ring: device float [staleness+1][dqn_train_ring_stride(net)]
+    (slot 0 = initial parameters);
+    streams: replicas + 1 distinct streams (HipStreams handles or
+    torch.cuda.Stream objects): the replica streams, then the server stream.
+    idx: device int64 [n_updates][batch]."""
+    import torch
+    rule = _RULES.get(rule, rule)
+    n_updates, batch = idx.shape
+    if theta_ring.numel() < (staleness + 1) * dqn_train_ring_stride(net):
+        raise ValueError("theta_ring too small")
+    if len(streams) != replicas + 1:
+        raise ValueError("need replicas + 1 streams")
+    if ws is None:
+        ws = torch.empty(dqn_train_workspace_bytes(net, batch, replicas), dtype=torch.uint8,
+                         device=theta_ring.device)
+    if losses_out is not None and losses_out.numel() < n_updates:
+        raise ValueError("losses_out too small")
+    arr = (ctypes.c_void_p * (replicas + 1))(*[_stream(s) for s in streams])
+    rc = lib().dqn_train_replicas(ctypes.byref(_cnet(net)), _ptr(theta_ring, torch.float32, "theta_ring"),
+                                  _ptr(opt_state, torch.float32, "opt_state"), int(rule), float(lr),
+                                  float(decay), float(eps), float(gamma),
+                                  ctypes.byref(_creplay(replay)), _ptr(idx, torch.int64, "idx"),
+                                  batch, n_updates, replicas, staleness,
+                                  _ptr(losses_out, torch.float32, "losses_out"),
+                                  _ptr(ws, torch.uint8, "ws"), ws.numel(),
+                                  ctypes.cast(arr, ctypes.c_void_p))
+    _check(rc, "dqn_train_replicas")
 
 
 # ----------------------------------------------------------------------------
