@@ -1,26 +1,41 @@
 #!/usr/bin/env python3
 """Throughput of the DQN TD-gradient + parameter-server update hot path on one
-MI355X (arXiv 1508.04186, Alg. 1 and Alg. 2 with one worker).
+MI355X (arXiv 1508.04186, Alg. 1 and Alg. 2), on seeded synthetic inputs.
 
-Workload (one "step" = one pass of the whole hot path over one minibatch):
-  replay_gather   32 transitions drawn uniformly (seeded index stream) from a
-                  replay memory of 100,000 synthetic uint8 4x84x84 transitions
-                  held in device memory;
-  dqn_td_gradient targets from theta^- = theta, loss and full gradient of the
-                  small Q-network (conv 16@8x8/4, conv 32@4x4/2, fc 256, fc 6);
-  ps_apply_update plain gradient-descent step, lr 2.5e-4.
-2,000 sequential steps are timed (after warmup) between HIP events on the
-stream the work runs on.  Inputs are resident in device memory before timing.
+Configurations (--config; the default line is config 1):
+  0   small Q-network (conv 16@8x8/4, conv 32@4x4/2, fc 256, fc 6), one
+      batch of 32 uniform random states: TD gradient + SGD step, repeated.
+  1   small Q-network, 100,000-transition replay in device memory, 2,000
+      sequential steps of gather (batch 32) -> TD gradient -> SGD.
+  2   small Q-network, 16 worker replicas on 16 streams + a server stream
+      applying AdaGrad (lr 0.01, eps 1e-8) in order, gradients at most 4
+      versions stale, 5,000 updates, 100,000-transition replay.
+  3   large Q-network (conv 32@8x8/4, 64@4x4/2, 64@3x3/1, fc 512, fc 18),
+      batch 256, 1,000,000-transition replay (28 GB), target network
+      refreshed every 1,000 steps, SGD.
+  4a  large Q-network, epsilon-greedy forward pass (eps 0.05) over 8,192
+      states gathered from the 1,000,000-transition replay.
+  4b  large Q-network, TD gradient + SGD at batch 2,048 from that replay.
+
+A step is one pass of the whole hot path over one batch (config 2: one
+update; config 4a: one forward pass over 8,192 states).  Inputs are resident
+in device memory before the timed region; the timed region is bracketed by
+device synchronizations and HIP events on the work's stream(s).
 
 The JSON line adds:
-  roofline      the dominant kernel (largest time per step, chosen by a short
-                event-bracketed breakdown pass before timing): algorithmic
-                FLOP per launch / its average launch time, measured with HIP
-                event pairs around every launch inside the timed region;
-  cpu_baseline  the CPU oracle (fp64, direct loops) timed on this host on the
-                first steps of the same run;
-  breakdown     per-kernel average times (us) from the breakdown pass, and the
-                paper's T (gradient) and tau (server update) times.
+  roofline      the dominant kernel (largest time per step, from an
+                event-bracketed breakdown pass before timing): its
+                algorithmic FLOP (or bytes) per launch divided by its average
+                launch time, measured with HIP event pairs around every
+                launch of that kernel inside the timed region, less the
+                average time of an empty event pair on the same stream;
+                `traffic` is the HBM bytes per launch from the committed
+                rocprofv3 PMC summary (profiles/) while the kernel's source
+                is unchanged;
+  cpu_baseline  the CPU oracle (fp64, direct loops) timed on this host on a
+                bounded sample of the same workload;
+  breakdown     per-kernel average times (us) and the paper's T (worker
+                gradient time) and tau (server update time).
 """
 from __future__ import annotations
 
@@ -40,6 +55,11 @@ if ROOT not in sys.path:
 METRIC = "DQN TD-gradient+update steps/sec (transitions/sec); % MFMA peak and HBM GB/s"
 PEAK_FP32_MFMA = 157.3e12   # MI355X dense fp32 matrix FLOP/s
 PEAK_HBM = 8.0e12           # MI355X HBM3E bytes/s
+F32 = np.float32
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 class HipEvents:
@@ -48,9 +68,7 @@ class HipEvents:
     def __init__(self):
         import torch
         path = os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so")
-        if not os.path.exists(path):
-            path = "libamdhip64.so"
-        L = ctypes.CDLL(path)
+        L = ctypes.CDLL(path if os.path.exists(path) else "libamdhip64.so")
         L.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
         L.hipEventCreate.restype = ctypes.c_int
         L.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
@@ -80,38 +98,159 @@ class HipEvents:
             self.L.hipEventDestroy(e)
 
 
-def kernel_work(shape, B):
-    """Algorithmic work per launch of each kernel for one TD step at batch B
-    (theta^- = theta, so s and s' share one forward launch of 2B samples).
-    Returns {name: (flop, bytes)}: MACs x 2 of the dense contractions; bytes
-    for the memory-bound kernels."""
+def kernel_work(shape, B, forward_only=False):
+    """Algorithmic work per launch of each kernel: {name: (flop, bytes)}.
+    FLOP = 2 x multiply-adds of the dense contractions; bytes for the
+    memory-bound kernels.  A TD step runs the forward on 2B samples (s under
+    theta, s' under theta^-) in one launch per layer; dgrad and wgrad run on
+    B samples."""
     dims = shape.conv_dims()
     H, A, F = shape.fc_hidden, shape.n_actions, shape.flat()
     P = shape.param_count()
     rec = shape.in_c * shape.in_h * shape.in_w
+    nf = B if forward_only else 2 * B
     w = {}
     for l, (cin, ih, iw, cout, k, s, oh, ow) in enumerate(dims):
         macs = oh * ow * cout * cin * k * k
-        w[f"conv{l+1}_fwd"] = (2 * (2 * B) * macs, 0)
-        w[f"conv{l+1}_wgrad"] = (2 * B * macs, 0)
-        if l > 0:
-            w[f"conv{l+1}_dgrad"] = (2 * B * macs, 0)
-    w["fc1_fwd"] = (2 * (2 * B) * H * F, 0)
-    w["fc1_wgrad"] = (2 * B * H * F, 0)
-    w["fc1_dgrad"] = (2 * B * H * F, 0)
-    w["head"] = (2 * (2 * B) * A * H + 2 * B * H, 0)
-    w["gather"] = (0, 4 * B * rec)             # read s and s', write both
-    w["apply"] = (0, 12 * P)                   # SGD: read theta and g, write theta
-    w["finalize"] = (0, 0)
+        w[f"conv{l+1}_fwd"] = (2 * nf * macs, 0)
+        if not forward_only:
+            w[f"conv{l+1}_wgrad"] = (2 * B * macs, 0)
+            if l > 0:
+                w[f"conv{l+1}_dgrad"] = (2 * B * macs, 0)
+    w["fc1_fwd"] = (2 * nf * H * F, 0)
+    w["head"] = (2 * nf * A * H, 0)
+    if forward_only:
+        w["gather"] = (0, 2 * B * rec)          # read s, write s
+    else:
+        w["fc1_wgrad"] = (2 * B * H * F, 0)
+        w["fc1_dgrad"] = (2 * B * H * F, 0)
+        w["gather"] = (0, 4 * B * rec)          # read s and s', write both
+        w["apply"] = (0, 12 * P)                # SGD: read theta and g, write theta
+        w["finalize"] = (0, 0)
     return w
+
+
+# Kernels whose roofline is reported (dense contractions and the
+# memory-bound gather); the head and finalize are latency-bound reductions.
+ROOFLINE_KERNELS = ("conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "fc1_wgrad", "fc1_dgrad",
+                    "conv1_wgrad", "conv2_wgrad", "conv3_wgrad", "conv2_dgrad", "conv3_dgrad",
+                    "gather", "apply")
+
+
+class Profiler:
+    """Event-bracketed timing of the library's kernels via dqn_profile.h."""
+
+    def __init__(self, hip):
+        import paper_1508_04186_amd as dq
+        self.dq, self.hip = dq, hip
+
+    def breakdown(self, run, n, kernels):
+        dq = self.dq
+        evs = {}
+        for name in kernels:
+            kid = dq.KERNEL_NAMES.index(name)
+            evs[kid] = self.hip.create(2 * n * 2)
+            dq.profile_attach(kid, evs[kid])
+        run()
+        import torch
+        torch.cuda.synchronize()
+        out = {}
+        for kid, ev in evs.items():
+            used = dq.profile_used(kid)
+            dq.profile_attach(kid, None)
+            if used:
+                out[dq.KERNEL_NAMES[kid]] = (1e3 * sum(self.hip.ms(ev[2 * j], ev[2 * j + 1])
+                                                       for j in range(used)) / used, used)
+            self.hip.destroy(ev)
+        return out
+
+    def attach(self, name, launches):
+        kid = self.dq.KERNEL_NAMES.index(name)
+        ev = self.hip.create(2 * launches)
+        self.dq.profile_attach(kid, ev)
+        return kid, ev
+
+    def collect(self, kid, ev):
+        used = self.dq.profile_used(kid)
+        self.dq.profile_attach(kid, None)
+        us = 1e3 * sum(self.hip.ms(ev[2 * j], ev[2 * j + 1]) for j in range(used)) / max(used, 1)
+        self.hip.destroy(ev)
+        return us, used
+
+    def empty_pair_us(self, n=200):
+        """Average time between two events recorded back to back on the
+        current stream: the bracket overhead inside every event pair."""
+        import torch
+        stream = torch.cuda.current_stream().cuda_stream
+        ev = self.hip.create(2 * n)
+        rec = self.hip.L.hipEventRecord
+        rec.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        rec.restype = ctypes.c_int
+        torch.cuda.synchronize()
+        for j in range(n):
+            rec(ev[2 * j], stream)
+            rec(ev[2 * j + 1], stream)
+        torch.cuda.synchronize()
+        us = 1e3 * sum(self.hip.ms(ev[2 * j], ev[2 * j + 1]) for j in range(n)) / n
+        self.hip.destroy(ev)
+        return us
+
+
+def measured_traffic(config, name):
+    """HBM bytes per launch of kernel role `name` under `config`, from the
+    committed rocprofv3 PMC summaries (profiles/*_traffic.md lines
+    'traffic|config|role|read|write|source|sha256-16'), or None when no
+    summary exists or the kernel's source changed since it was measured."""
+    import glob
+    import hashlib
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_traffic.md"))):
+        for line in open(path):
+            f = line.strip().split("|")
+            if len(f) == 7 and f[0] == "traffic" and f[1] == f"config {config}" and f[2] == name:
+                src = os.path.join(ROOT, "paper_1508_04186_amd", "csrc", f[5])
+                if not os.path.exists(src):
+                    return None
+                sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+                return int(f[3]) + int(f[4]) if sha == f[6] else None
+    return None
+
+
+def roofline(work, name, avg_us, launches, per_step_launches, raw_us=None, config=None):
+    flop, byts = work[name]
+    if flop > 0:
+        achieved, peak, unit, bound = flop / (avg_us * 1e-6) / 1e12, PEAK_FP32_MFMA / 1e12, "TFLOP/s", "mfma"
+    else:
+        achieved, peak, unit, bound = byts / (avg_us * 1e-6) / 1e9, PEAK_HBM / 1e9, "GB/s", "hbm"
+    out = {"kernel": name, "bound": bound, "achieved": round(achieved, 4), "peak": peak,
+           "unit": unit, "frac": round(achieved / peak, 6),
+           "traffic": measured_traffic(config, name) if config is not None else None,
+           "per_launch": {"flop": flop, "bytes": byts, "avg_us": round(avg_us, 3),
+                          "launches": launches, "launches_per_step": per_step_launches}}
+    if raw_us is not None:
+        out["per_launch"]["event_pair_us"] = round(raw_us, 3)
+        out["per_launch"]["event_overhead_us"] = round(raw_us - avg_us, 3)
+    return out
+
+
+def time_region(stream_sync, fn):
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    fn()
+    stream_sync()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1)
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--breakdown-steps", type=int, default=100)
+    ap.add_argument("--config", default="1", choices=["0", "1", "2", "3", "4a", "4b"])
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default per config)")
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--breakdown-steps", type=int, default=50)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall time budget of the CPU-oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -122,42 +261,262 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(one worker and its parameter server on one device); run with --gpus 1.",
-              file=sys.stderr)
+        print("bench.py measures one GPU only: this build has no multi-GPU path (workers and "
+              "their parameter server run on one device); run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch
-    import dqn_inputs as di
-    import paper_1508_04186_amd as dq
-
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
-    dev = torch.device("cuda:0")
     torch.cuda.init()
+    out = {"0": bench_single, "1": bench_sequential, "2": bench_replicas, "3": bench_large,
+           "4a": bench_forward, "4b": bench_large}[args.config](args)
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib * 2**20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.calib_copy_mib} MiB done")
+    print(json.dumps(out), flush=True)
+
+
+def base_record(K, W, ms, unit="steps/s"):
+    return {"metric": METRIC, "value": round(K / (ms / 1e3), 2), "unit": unit, "n_gpus": 1,
+            "steps": K, "warmup": W, "ms_per_step": round(ms / K, 5), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic"}
+
+
+# ---------------------------------------------------------------------------
+# configs 0 and 1
+
+def _small_setup(dev):
+    import dqn_inputs as di
+    import paper_1508_04186_amd as dq
+    return dq.NET_SMALL, di.NET_S
+
+
+def bench_single(args):
+    import torch
+    import dqn_inputs as di
+    import oracle
+    import paper_1508_04186_amd as dq
+    dev = torch.device("cuda:0")
     hip = HipEvents()
+    prof = Profiler(hip)
+    net, shape = _small_setup(dev)
+    B, SEED, LR, GAMMA = 32, 1000, 2.5e-4, 0.99
+    K = args.steps or 2000
+    W = args.warmup if args.warmup is not None else 50
+    s_h = di.random_states(B, SEED)
+    sn_h = di.random_states(B, SEED + 1)
+    a_h, r_h, t_h = di.random_transitions(B, shape.n_actions, SEED + 2)
+    th0 = di.xavier_theta(shape, SEED)
+    d = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+    s, sn, a, r, t = d(s_h), d(sn_h), d(a_h), d(r_h), d(t_h)
+    theta = d(th0)
+    P = dq.dqn_param_count(net)
+    g = torch.empty(P, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    ws = dq.workspace(net, B, dq.DQN_OP_TD_GRADIENT, dev)
 
-    net, shape = dq.NET_SMALL, di.NET_S
+    def steps(n):
+        for _ in range(n):
+            dq.dqn_td_gradient(net, theta, theta, s, sn, a, r, t, GAMMA, g, loss, ws=ws)
+            dq.ps_apply_update(dq.PS_SGD, theta, theta, None, g, LR)
+
+    steps(W)
+    work = kernel_work(shape, B)
+    work.pop("gather")
+    saved = theta.clone()
+    bd = prof.breakdown(lambda: steps(args.breakdown_steps), args.breakdown_steps, list(work))
+    theta.copy_(saved)
+    dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
+    kid, ev = prof.attach(dom, K * 4)
+    ms = time_region(torch.cuda.synchronize, lambda: steps(K))
+    raw_us, used = prof.collect(kid, ev)
+    dom_us = raw_us - prof.empty_pair_us()
+    rec = base_record(K, W, ms)
+    rec["config"] = {"workload": "config 0: small Q-network, one batch of 32 uniform random "
+                                 "states, TD gradient + SGD step (lr 2.5e-4) repeated",
+                     "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "batch": B, "update": "sgd",
+                     "gamma": GAMMA, "target": "theta"}
+    rec["transitions_per_s"] = round(rec["value"] * B, 1)
+    rec["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us, "0")
+    rec["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()}}
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle steps for about {args.cpu_seconds:.0f}s")
+        th = th0.copy()
+        n, c0 = 0, time.perf_counter()
+        while True:
+            res = oracle.td_gradient(shape, th, None, s_h, sn_h, a_h, r_h, t_h, float(F32(GAMMA)))
+            th, _ = oracle.apply_update("sgd", th, None, res["grad"], float(F32(LR)))
+            n += 1
+            el = time.perf_counter() - c0
+            if el >= args.cpu_seconds:
+                break
+        rec["cpu_baseline"] = {"value": round(n / el, 3), "unit": "steps/s",
+                               "cores": oracle.num_threads(), "kind": "oracle",
+                               "sample": f"{n} repetitions of the same step (fp64 TD gradient + "
+                                         f"SGD), {el:.1f}s wall"}
+    return rec
+
+
+def bench_sequential(args):
+    import torch
+    import dqn_inputs as di
+    import oracle
+    import paper_1508_04186_amd as dq
+    dev = torch.device("cuda:0")
+    hip = HipEvents()
+    prof = Profiler(hip)
+    net, shape = _small_setup(dev)
     B, SIZE, SEED, LR, GAMMA = 32, 100_000, 1001, 2.5e-4, 0.99
-    K, W = args.steps, args.warmup
+    K = args.steps or 2000
+    W = args.warmup if args.warmup is not None else 50
     total = K + W
-
-    def log(msg):
-        print(f"[bench] {msg}", file=sys.stderr, flush=True)
-
     t0 = time.time()
     log(f"replay: generating {SIZE} transitions (seed {SEED})")
     hr = di.host_replay(SIZE, shape.n_actions, SEED)
     rec, ra, rr, rt = di.device_replay(SIZE, shape.n_actions, SEED, device=dev, host=hr)
     rp = dq.Replay(rec, ra, rr, rt, SIZE)
     log(f"replay ready in {time.time() - t0:.1f}s ({rec.numel() / 2**30:.2f} GiB on device)")
-
-    theta0 = di.xavier_theta(shape, SEED)
-    idx_host = di.index_stream(max(total, 1), B, SIZE, SEED)
+    th0 = di.xavier_theta(shape, SEED)
+    idx_host = di.index_stream(total, B, SIZE, SEED)
     idx = torch.from_numpy(idx_host).to(dev)
-    theta = torch.from_numpy(theta0).to(dev)
+    theta = torch.from_numpy(th0).to(dev)
+    losses = torch.empty(total, dtype=torch.float32, device=dev)
+    ws = torch.empty(dq.dqn_train_workspace_bytes(net, B, 1), dtype=torch.uint8, device=dev)
+
+    def run(lo, hi):
+        dq.dqn_train_steps(net, theta, None, None, dq.PS_SGD, LR, 0.9, 0.0, GAMMA, rp, idx[lo:hi],
+                           step0=lo, losses_out=losses[lo:hi], ws=ws)
+
+    run(0, W)
+    torch.cuda.synchronize()
+    work = kernel_work(shape, B)
+    saved = theta.clone()
+    nb = min(args.breakdown_steps, K)
+    bd = prof.breakdown(lambda: run(W, W + nb), nb, list(work))
+    theta.copy_(saved)
+    dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
+    kid, ev = prof.attach(dom, K * 4)
+    ms = time_region(torch.cuda.synchronize, lambda: run(W, total))
+    raw_us, used = prof.collect(kid, ev)
+    dom_us = raw_us - prof.empty_pair_us()
+    final_loss = float(losses[total - 1].item())
+    log(f"timed {K} steps in {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
+
+    # the paper's T (worker gradient) and tau (server update), timed separately
+    s = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
+    sn = torch.empty_like(s)
+    a = torch.empty(B, dtype=torch.int32, device=dev)
+    r = torch.empty(B, dtype=torch.float32, device=dev)
+    t = torch.empty(B, dtype=torch.uint8, device=dev)
+    g = torch.empty(dq.dqn_param_count(net), dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    tws = dq.workspace(net, B, dq.DQN_OP_TD_GRADIENT, dev)
+
+    def grad_only(n):
+        for i in range(n):
+            dq.replay_gather(rp, idx[i], s, sn, a, r, t)
+            dq.dqn_td_gradient(net, theta, theta, s, sn, a, r, t, GAMMA, g, loss, ws=tws)
+
+    th_copy = theta.clone()
+
+    def update_only(n):
+        for _ in range(n):
+            dq.ps_apply_update(dq.PS_SGD, th_copy, th_copy, None, g, LR)
+    T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(200)) / 200
+    tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(200)) / 200
+
+    rec_ = base_record(K, W, ms)
+    rec_["config"] = {
+        "workload": "config 1: small Q-network, batch 32, 100,000-transition device replay, "
+                    "2,000 sequential gather + TD-gradient + SGD steps",
+        "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "batch": B, "replay_transitions": SIZE,
+        "update": "sgd", "lr": LR, "gamma": GAMMA, "target": "theta",
+        "parallelism": "one worker + server on one GPU"}
+    rec_["transitions_per_s"] = round(rec_["value"] * B, 1)
+    rec_["step_tflops"] = round(sum(v[0] for v in work.values()) * rec_["value"] / 1e12, 4)
+    rec_["final_loss"] = final_loss
+    rec_["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us, "1")
+    rec_["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
+                         "T_us": round(T_us, 2), "tau_us": round(tau_us, 2),
+                         "T_over_tau": round(T_us / tau_us, 2)}
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle steps for about {args.cpu_seconds:.0f}s")
+        th = th0.copy()
+        n, c0 = 0, time.perf_counter()
+        while True:
+            si, sni, ai, ri, ti = oracle.gather_from_host_replay(hr, idx_host[n])
+            res = oracle.td_gradient(shape, th, None, si, sni, ai, ri, ti, float(F32(GAMMA)))
+            th, _ = oracle.apply_update("sgd", th, None, res["grad"], float(F32(LR)))
+            n += 1
+            el = time.perf_counter() - c0
+            if el >= args.cpu_seconds or n >= total:
+                break
+        rec_["cpu_baseline"] = {
+            "value": round(n / el, 3), "unit": "steps/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"first {n} steps of the same run (batch 32, same replay and index stream), "
+                      f"gather + fp64 TD gradient + SGD, {el:.1f}s wall"}
+    return rec_
+
+
+# ---------------------------------------------------------------------------
+# config 2
+
+def bench_replicas(args):
+    import torch
+    import dqn_inputs as di
+    import oracle
+    import paper_1508_04186_amd as dq
+    dev = torch.device("cuda:0")
+    net, shape = _small_setup(dev)
+    B, SIZE, SEED, LR, EPS, GAMMA, R, S = 32, 100_000, 1002, 0.01, 1e-8, 0.99, 16, 4
+    U = args.steps or 5000
+    W = args.warmup if args.warmup is not None else 100
+    log(f"replay: generating {SIZE} transitions (seed {SEED})")
+    hr = di.host_replay(SIZE, shape.n_actions, SEED)
+    rec, ra, rr, rt = di.device_replay(SIZE, shape.n_actions, SEED, device=dev, host=hr)
+    rp = dq.Replay(rec, ra, rr, rt, SIZE)
+    th0 = di.xavier_theta(shape, SEED)
+    idx_host = di.index_stream(U, B, SIZE, SEED)
+    idx = torch.from_numpy(idx_host).to(dev)
     P = dq.dqn_param_count(net)
+    RS = dq.dqn_train_ring_stride(net)
+    ring = torch.empty((S + 1) * RS, dtype=torch.float32, device=dev)
+    G = torch.zeros(P, dtype=torch.float32, device=dev)
+    losses = torch.empty(U, dtype=torch.float32, device=dev)
+    ws = torch.empty(dq.dqn_train_workspace_bytes(net, B, R), dtype=torch.uint8, device=dev)
+    hs = dq.HipStreams(R + 1)
+
+    def run(n):
+        ring[:P].copy_(torch.from_numpy(th0).to(dev))
+        G.zero_()
+        torch.cuda.synchronize()
+        dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA, rp, idx[:n], R, S,
+                              hs.handles, losses_out=losses[:n], ws=ws)
+
+    run(W)
+    torch.cuda.synchronize()
+    # timed: all U updates from the initial parameters (the setup copies
+    # above are outside the region)
+    ring[:P].copy_(torch.from_numpy(th0).to(dev))
+    G.zero_()
+    e0 = time.perf_counter()
+    ms = time_region(torch.cuda.synchronize,
+                     lambda: dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA,
+                                                   rp, idx, R, S, hs.handles, losses_out=losses,
+                                                   ws=ws))
+    host_s = time.perf_counter() - e0
+    final_loss = float(losses[U - 1].item())
+    hs.close()
+    log(f"timed {U} updates in {ms:.1f} ms (host enqueue+wait {host_s * 1e3:.1f} ms)")
+    # T and tau (paper Sec. IV.D.1): one worker gradient, one server update
     s = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
     sn = torch.empty_like(s)
     a = torch.empty(B, dtype=torch.int32, device=dev)
@@ -165,152 +524,213 @@ def main():
     t = torch.empty(B, dtype=torch.uint8, device=dev)
     g = torch.empty(P, dtype=torch.float32, device=dev)
     loss = torch.empty(1, dtype=torch.float32, device=dev)
-    ws = dq.workspace(net, B, dq.DQN_OP_TD_GRADIENT, dev)
-    stream = torch.cuda.current_stream()
+    tws = dq.workspace(net, B, dq.DQN_OP_TD_GRADIENT, dev)
+    th = ring[:P].clone()
 
-    def step(i):
-        dq.replay_gather(rp, idx[i], s, sn, a, r, t, stream=stream)
-        dq.dqn_td_gradient(net, theta, theta, s, sn, a, r, t, GAMMA, g, loss, ws=ws, stream=stream)
-        dq.ps_apply_update(dq.PS_SGD, theta, theta, None, g, LR, stream=stream)
+    def grad_only(n):
+        for i in range(n):
+            dq.replay_gather(rp, idx[i], s, sn, a, r, t)
+            dq.dqn_td_gradient(net, th, th, s, sn, a, r, t, GAMMA, g, loss, ws=tws)
 
-    # ---- warmup (also the first W steps of the run)
-    for i in range(W):
-        step(i)
-    torch.cuda.synchronize()
-
-    # ---- breakdown pass on a copy of the state: per-kernel event pairs
-    work = kernel_work(shape, B)
-    names = dq.KERNEL_NAMES
-    nb = args.breakdown_steps
-    theta_save = theta.clone()
-    ev_all = {}
-    for kid, name in enumerate(names):
-        if name in work:
-            ev_all[kid] = hip.create(2 * nb)
-            dq.profile_attach(kid, ev_all[kid])
-    for i in range(nb):
-        step(W + (i % max(K, 1)))
-    torch.cuda.synchronize()
-    per_kernel = {}
-    for kid, evs in ev_all.items():
-        used = dq.profile_used(kid)
-        dq.profile_attach(kid, None)
-        if used:
-            per_kernel[names[kid]] = 1e3 * sum(hip.ms(evs[2 * j], evs[2 * j + 1]) for j in range(used)) / used
-        hip.destroy(evs)
-    theta.copy_(theta_save)
-    torch.cuda.synchronize()
-    dominant = max((k for k in per_kernel if work[k][0] > 0), key=lambda k: per_kernel[k])
-    dom_id = names.index(dominant)
-    log("breakdown (us/launch): " + ", ".join(f"{k} {v:.1f}" for k, v in per_kernel.items()))
-
-    # ---- timed region: K steps, events around every launch of the dominant kernel
-    dom_ev = hip.create(2 * K)
-    dq.profile_attach(dom_id, dom_ev)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for i in range(K):
-        step(W + i)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
-    used = dq.profile_used(dom_id)
-    dq.profile_attach(dom_id, None)
-    dom_us = 1e3 * sum(hip.ms(dom_ev[2 * j], dom_ev[2 * j + 1]) for j in range(used)) / max(used, 1)
-    hip.destroy(dom_ev)
-    final_loss = float(loss.item())
-    log(f"timed {K} steps in {ms:.1f} ms; dominant kernel {dominant} {dom_us:.2f} us/launch")
-
-    # ---- the paper's T (worker gradient) and tau (server update), separately
-    def time_calls(fn, n):
-        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        a0.record(stream)
+    def update_only(n):
         for _ in range(n):
-            fn()
-        a1.record(stream)
-        torch.cuda.synchronize()
-        return 1e3 * a0.elapsed_time(a1) / n
-    th_copy = theta.clone()
-    T_us = time_calls(lambda: (dq.replay_gather(rp, idx[0], s, sn, a, r, t, stream=stream),
-                               dq.dqn_td_gradient(net, theta, theta, s, sn, a, r, t, GAMMA, g, loss,
-                                                  ws=ws, stream=stream)), 200)
-    tau_us = time_calls(lambda: dq.ps_apply_update(dq.PS_SGD, th_copy, th_copy, None, g, LR,
-                                                   stream=stream), 200)
+            dq.ps_apply_update(dq.PS_ADAGRAD, th, th, G, g, LR, 0.0, EPS)
+    T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(200)) / 200
+    tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(200)) / 200
 
-    if args.calib_copy_mib > 0:
-        n = args.calib_copy_mib * 2**20
-        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"calibration copy of {args.calib_copy_mib} MiB done")
-
-    steps_per_s = K / (ms / 1e3)
-    flop, byts = work[dominant]
-    roof = {
-        "kernel": dominant,
-        "bound": "mfma" if flop > 0 else "hbm",
-        "achieved": (flop / (dom_us * 1e-6) / 1e12) if flop > 0 else (byts / (dom_us * 1e-6) / 1e9),
-        "peak": PEAK_FP32_MFMA / 1e12 if flop > 0 else PEAK_HBM / 1e9,
-        "unit": "TFLOP/s" if flop > 0 else "GB/s",
-        "traffic": None,
-        "per_launch": {"flop": flop, "bytes": byts, "avg_us": round(dom_us, 3), "launches": used},
-    }
-    roof["frac"] = roof["achieved"] / roof["peak"]
-
-    out = {
-        "metric": METRIC,
-        "value": round(steps_per_s, 2),
-        "unit": "steps/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": W,
-        "ms_per_step": round(ms / K, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
-        "config": {
-            "workload": "small Q-network, batch 32, 100,000-transition device replay, "
-                        "2,000 sequential TD-gradient + SGD steps",
-            "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "batch": B,
-            "replay_transitions": SIZE, "update": "sgd", "lr": LR, "gamma": GAMMA,
-            "target": "theta", "parallelism": "single worker + server on one GPU",
-        },
-        "transitions_per_s": round(steps_per_s * B, 1),
-        "step_tflops": round(sum(v[0] for v in work.values()) * steps_per_s / 1e12, 4),
-        "final_loss": final_loss,
-        "roofline": roof,
-        "breakdown": {"us_per_launch": {k: round(v, 2) for k, v in per_kernel.items()},
-                      "T_us": round(T_us, 2), "tau_us": round(tau_us, 2),
-                      "T_over_tau": round(T_us / tau_us, 2)},
-    }
-
+    out = base_record(U, W, ms)
+    out["config"] = {
+        "workload": "config 2: 16 small-Q-network worker replicas on 16 streams + server stream, "
+                    "AdaGrad (lr 0.01, eps 1e-8), staleness <= 4, 5,000 updates of batch 32, "
+                    "100,000-transition device replay",
+        "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "batch": B, "replicas": R, "staleness": S,
+        "replay_transitions": SIZE, "update": "adagrad", "lr": LR, "gamma": GAMMA,
+        "parallelism": "16 replicas + 1 server on one GPU (streams)"}
+    out["transitions_per_s"] = round(out["value"] * B, 1)
+    out["final_loss"] = final_loss
+    out["roofline"] = None
+    out["breakdown"] = {"T_us": round(T_us, 2), "tau_us": round(tau_us, 2),
+                        "T_over_tau": round(T_us / tau_us, 2),
+                        "server_bound_updates_per_s": round(1e6 / tau_us, 1)}
     if not args.no_cpu_baseline:
-        import oracle
-        log(f"cpu baseline: oracle steps for about {args.cpu_seconds:.0f}s")
-        th = theta0.copy()
-        n_done = 0
+        log(f"cpu baseline: oracle stale-schedule updates for about {args.cpu_seconds:.0f}s")
+        n_try = 8
         c0 = time.perf_counter()
+        oracle.stale_replica_training(shape, th0, hr, idx_host[:n_try], float(F32(GAMMA)),
+                                      float(F32(LR)), S, rule="adagrad", eps=float(F32(EPS)))
+        per = (time.perf_counter() - c0) / n_try
+        n = max(1, min(U, int(args.cpu_seconds / per)))
+        c0 = time.perf_counter()
+        oracle.stale_replica_training(shape, th0, hr, idx_host[:n], float(F32(GAMMA)),
+                                      float(F32(LR)), S, rule="adagrad", eps=float(F32(EPS)))
+        el = time.perf_counter() - c0
+        out["cpu_baseline"] = {"value": round(n / el, 3), "unit": "steps/s",
+                               "cores": oracle.num_threads(), "kind": "oracle",
+                               "sample": f"first {n} updates of the same schedule, {el:.1f}s wall"}
+    return out
+
+
+# ---------------------------------------------------------------------------
+# configs 3, 4a and 4b (large network, 1,000,000-transition replay)
+
+def _large_replay(dev, size, seed):
+    import dqn_inputs as di
+    import paper_1508_04186_amd as dq
+    t0 = time.time()
+    log(f"replay: generating {size} transitions (seed {seed}) into device memory")
+    rec, ra, rr, rt = di.device_replay(size, di.NET_L.n_actions, seed, device=dev)
+    log(f"replay ready in {time.time() - t0:.1f}s ({rec.numel() / 2**30:.2f} GiB on device)")
+    return dq.Replay(rec, ra, rr, rt, size)
+
+
+def bench_large(args):
+    import torch
+    import dqn_inputs as di
+    import oracle
+    import paper_1508_04186_amd as dq
+    dev = torch.device("cuda:0")
+    hip = HipEvents()
+    prof = Profiler(hip)
+    net, shape = dq.NET_LARGE, di.NET_L
+    SIZE, SEED, LR, GAMMA = 1_000_000, 1003, 2.5e-4, 0.99
+    if args.config == "3":
+        B, C = 256, 1000
+        K = args.steps or 3000
+        W = args.warmup if args.warmup is not None else 20
+    else:
+        B, C = 2048, 0
+        K = args.steps or 100
+        W = args.warmup if args.warmup is not None else 5
+    total = K + W
+    rp = _large_replay(dev, SIZE, SEED)
+    th0 = di.xavier_theta(shape, SEED)
+    idx_host = di.index_stream(total, B, SIZE, SEED)
+    idx = torch.from_numpy(idx_host).to(dev)
+    theta = torch.from_numpy(th0).to(dev)
+    tgt = torch.empty_like(theta) if C else None
+    losses = torch.empty(total, dtype=torch.float32, device=dev)
+    ws = torch.empty(dq.dqn_train_workspace_bytes(net, B, 1), dtype=torch.uint8, device=dev)
+
+    def run(lo, hi):
+        dq.dqn_train_steps(net, theta, tgt, None, dq.PS_SGD, LR, 0.9, 0.0, GAMMA, rp, idx[lo:hi],
+                           step0=lo, target_period=C, losses_out=losses[lo:hi], ws=ws)
+
+    run(0, W)
+    torch.cuda.synchronize()
+    work = kernel_work(shape, B)
+    saved = theta.clone()
+    saved_t = None if tgt is None else tgt.clone()
+    nb = min(args.breakdown_steps, K, 20)
+    bd = prof.breakdown(lambda: run(W, W + nb), nb, list(work))
+    theta.copy_(saved)
+    if tgt is not None:
+        tgt.copy_(saved_t)
+    dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
+    kid, ev = prof.attach(dom, K * 4)
+    ms = time_region(torch.cuda.synchronize, lambda: run(W, total))
+    raw_us, used = prof.collect(kid, ev)
+    dom_us = raw_us - prof.empty_pair_us()
+    final_loss = float(losses[total - 1].item())
+    log(f"timed {K} steps in {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
+    out = base_record(K, W, ms)
+    name = "config 3" if args.config == "3" else "config 4b"
+    out["config"] = {
+        "workload": f"{name}: large Q-network, batch {B}, 1,000,000-transition device replay, "
+                    f"{K} sequential gather + TD-gradient + SGD steps"
+                    + (f", target network refreshed every {C} steps" if C else ""),
+        "net": "conv32@8x8/4-conv64@4x4/2-conv64@3x3/1-fc512-fc18", "batch": B,
+        "replay_transitions": SIZE, "update": "sgd", "lr": LR, "gamma": GAMMA,
+        "target": f"refresh every {C}" if C else "theta"}
+    out["transitions_per_s"] = round(out["value"] * B, 1)
+    out["step_tflops"] = round(sum(v[0] for v in work.values()) * out["value"] / 1e12, 4)
+    out["final_loss"] = final_loss
+    out["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us, args.config)
+    out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
+                        "per_layer_tflops": {k: round(work[k][0] / (v[0] * 1e-6) / 1e12, 3)
+                                             for k, v in bd.items() if work[k][0] > 0}}
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle steps for about {args.cpu_seconds:.0f}s")
+        th = th0.copy()
+        n, c0 = 0, time.perf_counter()
         while True:
-            si, sni, ai, ri, ti = oracle.gather_from_host_replay(hr, idx_host[n_done])
-            res = oracle.td_gradient(shape, th, None, si, sni, ai, ri, ti, float(np.float32(GAMMA)))
-            th, _ = oracle.apply_update("sgd", th, None, res["grad"], float(np.float32(LR)))
-            n_done += 1
+            s, sn, a, r, t = di.transitions_at(SEED, idx_host[n], shape.n_actions, SIZE)
+            res = oracle.td_gradient(shape, th, None, s, sn, a, r, t, float(F32(GAMMA)))
+            th, _ = oracle.apply_update("sgd", th, None, res["grad"], float(F32(LR)))
+            n += 1
             el = time.perf_counter() - c0
-            if el >= args.cpu_seconds or n_done >= total:
+            if el >= args.cpu_seconds or n >= total:
                 break
-        out["cpu_baseline"] = {
-            "value": round(n_done / el, 3), "unit": "steps/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"first {n_done} steps of the same run (batch 32, same replay and index "
-                      f"stream), gather + fp64 TD gradient + SGD, {el:.1f}s wall",
-        }
-    print(json.dumps(out), flush=True)
+        out["cpu_baseline"] = {"value": round(n / el, 4), "unit": "steps/s",
+                               "cores": oracle.num_threads(), "kind": "oracle",
+                               "sample": f"first {n} step(s) of the same run (batch {B}), fp64 TD "
+                                         f"gradient + SGD, {el:.1f}s wall"}
+    return out
+
+
+def bench_forward(args):
+    import torch
+    import dqn_inputs as di
+    import oracle
+    import paper_1508_04186_amd as dq
+    dev = torch.device("cuda:0")
+    hip = HipEvents()
+    prof = Profiler(hip)
+    net, shape = dq.NET_LARGE, di.NET_L
+    SIZE, SEED, B, EPS = 1_000_000, 1004, 8192, F32(0.05)
+    K = args.steps or 200
+    W = args.warmup if args.warmup is not None else 10
+    rp = _large_replay(dev, SIZE, SEED)
+    th0 = di.xavier_theta(shape, SEED)
+    rng = np.random.default_rng(SEED)
+    idx_host = rng.integers(0, SIZE, size=(K + W, B), dtype=np.int64)
+    idx = torch.from_numpy(idx_host).to(dev)
+    draws = torch.from_numpy(di.egreedy_draws(B, SEED)).to(dev)
+    theta = torch.from_numpy(th0).to(dev)
+    st = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
+    q = torch.empty((B, net.n_actions), dtype=torch.float32, device=dev)
+    act = torch.empty(B, dtype=torch.int32, device=dev)
+    ws = dq.workspace(net, B, dq.DQN_OP_FORWARD, dev)
+
+    def run(lo, hi):
+        for i in range(lo, hi):
+            dq.replay_gather(rp, idx[i], st)
+            dq.dqn_forward(net, theta, st, float(EPS), draws, q, act, ws=ws)
+
+    run(0, W)
+    torch.cuda.synchronize()
+    work = kernel_work(shape, B, forward_only=True)
+    nb = min(args.breakdown_steps, K, 20)
+    bd = prof.breakdown(lambda: run(W, W + nb), nb, list(work))
+    dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
+    kid, ev = prof.attach(dom, K * 4)
+    ms = time_region(torch.cuda.synchronize, lambda: run(W, K + W))
+    raw_us, used = prof.collect(kid, ev)
+    dom_us = raw_us - prof.empty_pair_us()
+    log(f"timed {K} forward passes in {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
+    out = base_record(K, W, ms)
+    out["config"] = {
+        "workload": "config 4a: large Q-network, epsilon-greedy (eps 0.05) forward pass over 8,192 "
+                    "states gathered from a 1,000,000-transition device replay",
+        "net": "conv32@8x8/4-conv64@4x4/2-conv64@3x3/1-fc512-fc18", "batch": B,
+        "replay_transitions": SIZE, "epsilon": float(EPS)}
+    out["states_per_s"] = round(out["value"] * B, 1)
+    out["step_tflops"] = round(sum(v[0] for v in work.values()) * out["value"] / 1e12, 4)
+    out["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us, "4a")
+    out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
+                        "per_layer_tflops": {k: round(work[k][0] / (v[0] * 1e-6) / 1e12, 3)
+                                             for k, v in bd.items() if work[k][0] > 0}}
+    if not args.no_cpu_baseline:
+        n = 512
+        s, _, _, _, _ = di.transitions_at(SEED, idx_host[0][:n], shape.n_actions, SIZE)
+        c0 = time.perf_counter()
+        qr = oracle.forward_q(shape, th0, s)
+        oracle.select_actions(qr, float(EPS), di.egreedy_draws(B, SEED)[:n])
+        el = time.perf_counter() - c0
+        out["cpu_baseline"] = {"value": round(n / el / B, 5), "unit": "steps/s",
+                               "cores": oracle.num_threads(), "kind": "oracle",
+                               "sample": f"fp64 forward + epsilon-greedy choice on {n} of the "
+                                         f"8,192 states ({el:.1f}s wall), scaled to 8,192"}
+    return out
 
 
 if __name__ == "__main__":

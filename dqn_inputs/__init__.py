@@ -268,3 +268,21 @@ def device_replay(size: int, n_actions: int, seed: int, device="cuda", c: int = 
     torch.cuda.synchronize()
     return (rec, torch.from_numpy(a).to(device), torch.from_numpy(r).to(device),
             torch.from_numpy(t).to(device))
+
+
+def transitions_at(seed: int, idx, n_actions: int, size: int, c: int = 4):
+    """The transitions idx of the seeded replay of `size` records (the same
+    bytes device_replay(size, n_actions, seed) holds), regenerated from the
+    frame stream without materializing the whole replay.
+    Returns (s, s_next uint8 [B][c][84][84], a int32, r float32, term uint8)."""
+    idx = np.asarray(idx, dtype=np.int64)
+    B = idx.shape[0]
+    s = np.empty((B, c, FRAME_H, FRAME_W), np.uint8)
+    sn = np.empty_like(s)
+    buf = np.empty((c + 1, FRAME_H, FRAME_W), np.uint8)
+    for j, i in enumerate(idx):
+        frames(seed, int(i), c + 1, buf)
+        s[j] = buf[:c]
+        sn[j] = buf[1:]
+    a, r, t = side_arrays(size, n_actions, seed)
+    return s, sn, a[idx].astype(np.int32), r[idx].astype(np.float32), t[idx].astype(np.uint8)

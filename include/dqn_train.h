@@ -70,7 +70,11 @@ int64_t dqn_train_ring_stride(const dqn_net* net);
  * opt_state: server's optimizer state, device float [p] (NULL for PS_SGD).
  * streams: host array of replicas + 1 hipStream_t (as void*): the replica
  * streams, then the server stream.  All must be distinct.  On return every
- * update is enqueued; the caller synchronizes the server stream.
+ * update is enqueued; the caller synchronizes the server stream.  The call
+ * creates replicas + staleness + 2 HIP events for the cross-stream
+ * dependencies and releases them before returning (no device memory is
+ * allocated).  Inputs written on other streams must be complete before the
+ * call (the replica streams do not wait for the caller's stream).
  * replicas must exceed staleness (a replica's gradient buffer is reused only
  * after the server consumed it).  idx: device int64 [n_updates][batch];
  * losses_out: device float [n_updates] or NULL.

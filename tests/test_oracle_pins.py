@@ -494,3 +494,12 @@ def test_relu_margin_hand_worked():
     assert oracle.relu_margins(net, th, st)[0] == 0.0
     th[sl["conv1.b"][0]] = -0.5 * x0   # now the smallest is pixel 0: (x0/2) / (1.5 x0) = 1/3
     assert np.isclose(oracle.relu_margins(net, th, st)[0], 1.0 / 3.0, rtol=1e-15)
+
+
+def test_transitions_at_regenerates_replay_records():
+    hr = di.host_replay(500, 18, 9)
+    idx = np.array([0, 7, 250, 497])
+    s, sn, a, r, t = di.transitions_at(9, idx, 18, 500)
+    rs, rsn, ra, rr, rt = oracle.gather_from_host_replay(hr, idx)
+    assert np.array_equal(s.reshape(4, -1), rs) and np.array_equal(sn.reshape(4, -1), rsn)
+    assert np.array_equal(a, ra) and np.array_equal(r, rr) and np.array_equal(t, rt)
