@@ -153,6 +153,21 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
                     float* grad_out, float* loss_out, float* q_out, float* y_out,
                     void* ws, size_t ws_bytes, void* stream);
 
+/* The same gradient with the minibatch drawn from the replay memory in the
+ * same call (Alg. 1: "uniformly sample minibatch X from D_k", then the
+ * gradient): transition j is idx[j] of `replay`, exactly as replay_gather
+ * would deliver it (s_j = phi_i, s_next_j = phi_{i+1}, a, r, terminal of
+ * record i = idx[j]), but the records are read in place by the first
+ * convolution instead of being copied first.  idx: device int64 [batch] with
+ * values in [0, size-2] (not checked on the device; an out-of-range value
+ * reads out of bounds).  The replay record shape must equal the network
+ * input (4x84x84).  Outputs, workspace (dqn_workspace_bytes with
+ * DQN_OP_TD_GRADIENT) and errors as dqn_td_gradient. */
+int dqn_td_gradient_replay(const dqn_net* net, const float* theta, const float* theta_target,
+                           const dqn_replay* replay, const int64_t* idx, int32_t batch, float gamma,
+                           float* grad_out, float* loss_out, float* q_out, float* y_out, void* ws,
+                           size_t ws_bytes, void* stream);
+
 /* Parameter-server update applied to one received gradient (Alg. 2
  * RMSPROPUPDATE; plain gradient descent of Sec. III.B; AdaGrad of
  * Sec. IV.D.2), elementwise over n float32 parameters:

@@ -44,8 +44,9 @@ int64_t dqn_train_workspace_bytes(const dqn_net* net, int32_t batch, int32_t rep
 
 /* n_steps sequential steps n = 0 .. n_steps-1 (global step g = step0 + n):
  *   if target_period > 0 and g % target_period == 0: theta_target <- theta;
- *   replay_gather(idx + n*batch); dqn_td_gradient(theta, theta_target or, when
- *   target_period == 0, theta itself); ps_apply_update(rule, theta in place).
+ *   dqn_td_gradient_replay(theta, theta_target or, when target_period == 0,
+ *   theta itself, minibatch idx + n*batch); ps_apply_update(rule, theta in
+ *   place).
  * idx: device int64 [n_steps][batch] (transition indices, as replay_gather).
  * theta_target: device float [p]; may be NULL when target_period == 0.
  * opt_state: device float [p] (RMSProp r or AdaGrad G); NULL for PS_SGD.

@@ -99,6 +99,9 @@ struct TdLayout {
     float* act[3];
     float* fc1p;
     float *h1s, *dz1, *delta, *lossj;
+    int32_t* a;     // side fields gathered from a replay (replay source only)
+    float* r;
+    uint8_t* t;
     float* dconv[3];
     float* wpart[3];
     float* bpart[3];
@@ -118,6 +121,9 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
     t.dz1 = cv.take<float>(ws, (int64_t)B * ni.H);
     t.delta = cv.take<float>(ws, B);
     t.lossj = cv.take<float>(ws, B);
+    t.a = cv.take<int32_t>(ws, B);
+    t.r = cv.take<float>(ws, B);
+    t.t = cv.take<uint8_t>(ws, B);
     for (int l = 0; l < ni.n_conv; ++l) t.dconv[l] = cv.take<float>(ws, (int64_t)B * act_elems(ni.d[l]));
     for (int l = 0; l < ni.n_conv; ++l) {
         const ConvDims& c = ni.d[l];
@@ -184,143 +190,66 @@ inline void prof_end(int k, hipStream_t st) {
         prof_end((kid), st);                            \
     } while (0)
 
-}  // namespace
+// Where a TD step's transitions come from: dense device buffers, or replay
+// records and side arrays addressed by an index array.
+struct TdSource {
+    const uint8_t *s, *s_next;
+    const int32_t* action;
+    const float* reward;
+    const uint8_t* terminal;
+    const dqn_replay* replay;
+    const int64_t* idx;
+};
 
-extern "C" {
-
-const char* dqn_status_string(int status) {
-    switch (status) {
-        case DQN_OK: return "ok";
-        case DQN_EINVAL: return "invalid argument";
-        case DQN_EWORKSPACE: return "workspace too small";
-        case DQN_EHIP: return "HIP launch failed";
-        case DQN_EUNSUPPORTED: return "unsupported network";
-        default: return "unknown status";
-    }
-}
-
-int64_t dqn_param_count(const dqn_net* net) {
-    NetInfo ni;
-    int rc = identify(net, &ni);
-    return rc != DQN_OK ? rc : ni.P;
-}
-
-int64_t dqn_param_offset(const dqn_net* net, int32_t layer, int32_t is_bias) {
-    NetInfo ni;
-    int rc = identify(net, &ni);
-    if (rc != DQN_OK) return rc;
-    if (layer < 0 || layer > ni.n_conv + 1) return DQN_EINVAL;
-    return is_bias ? ni.b_off[layer] : ni.w_off[layer];
-}
-
-int64_t dqn_workspace_bytes(const dqn_net* net, int32_t batch, int32_t op) {
-    NetInfo ni;
-    int rc = identify(net, &ni);
-    if (rc != DQN_OK) return rc;
-    if (batch <= 0) return DQN_EINVAL;
-    if (op == DQN_OP_FORWARD) return (int64_t)fwd_layout(ni, batch, nullptr).bytes;
-    if (op == DQN_OP_TD_GRADIENT) return (int64_t)td_layout(ni, batch, nullptr).bytes;
-    return DQN_EINVAL;
-}
-
-int replay_gather(const dqn_replay* rp, const int64_t* idx, int32_t batch, uint8_t* s_out,
-                  uint8_t* s_next_out, int32_t* a_out, float* r_out, uint8_t* term_out,
-                  void* stream) {
-    if (!rp || !idx || !s_out || batch <= 0) return DQN_EINVAL;
-    if (!rp->frames || rp->c <= 0 || rp->h <= 0 || rp->w <= 0) return DQN_EINVAL;
-    const int64_t rec = (int64_t)rp->c * rp->h * rp->w;
-    if (rec % 16 != 0 || rp->record_stride < rec || rp->record_stride % 16 != 0) return DQN_EINVAL;
-    if (!aligned(rp->frames, 16) || !aligned(s_out, 16) || (s_next_out && !aligned(s_next_out, 16)))
-        return DQN_EINVAL;
-    if (rp->size < (s_next_out ? 2 : 1)) return DQN_EINVAL;
-    if ((a_out && !rp->action) || (r_out && !rp->reward) || (term_out && !rp->terminal))
-        return DQN_EINVAL;
-    if (batch > 65535) return DQN_EINVAL;
-    hipStream_t st = (hipStream_t)stream;
-    RUN(DQN_K_GATHER, launch_gather(rp->frames, rp->record_stride, rec, rp->action, rp->reward,
-                                    rp->terminal, idx, batch, s_out, s_next_out, a_out, r_out,
-                                    term_out, st));
-    return DQN_OK;
-}
-
-int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, int32_t batch,
-                float epsilon, const uint64_t* draws, float* q_out, int32_t* action_out, void* ws,
-                size_t ws_bytes, void* stream) {
-    NetInfo ni;
-    int rc = identify(net, &ni);
-    if (rc != DQN_OK) return rc;
-    if (!theta || !states || batch <= 0 || !ws) return DQN_EINVAL;
-    if (!(epsilon >= 0.f && epsilon <= 1.f)) return DQN_EINVAL;
-    const double te = std::floor((double)epsilon * 4294967296.0);
-    const uint64_t thresh = te >= 4294967296.0 ? 4294967296ull : (uint64_t)te;
-    if (thresh > 0 && !draws) return DQN_EINVAL;
-    if (!aligned(ws, 256) || !aligned(theta, 16) || !aligned(states, 16)) return DQN_EINVAL;
-    FwdLayout f = fwd_layout(ni, batch, nullptr);
-    if (ws_bytes < f.bytes) return DQN_EWORKSPACE;
-    f = fwd_layout(ni, batch, ws);
-    hipStream_t st = (hipStream_t)stream;
-    const float* th = theta;
-    for (int l = 0; l < ni.n_conv; ++l) {
-        const void* in = l == 0 ? (const void*)states : (const void*)f.act[l - 1];
-        const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
-        RUN(DQN_K_CONV1_FWD + l,
-            launch_conv_fwd(ni.conv[l], in, in, batch, batch, th + ni.w_off[l], th + ni.b_off[l],
-                            th + ni.w_off[l], th + ni.b_off[l], f.act[l], scale, st));
-    }
-    const int L = ni.n_conv;
-    RUN(DQN_K_FC1_FWD,
-        launch_gemm(GEMM_NT, batch, ni.H, ni.flat, f.act[L - 1], ni.flat, th + ni.w_off[L], ni.flat,
-                    f.fc1p, ni.H, f.ks, f.kchunk, (int64_t)batch * ni.H, nullptr, st));
-    HeadFwdArgs h{};
-    h.fc1p = f.fc1p;
-    h.ks = f.ks;
-    h.B = batch;
-    h.b1 = th + ni.b_off[L];
-    h.W2 = th + ni.w_off[L + 1];
-    h.b2 = th + ni.b_off[L + 1];
-    h.thresh = thresh;
-    h.draws = draws;
-    h.q_out = q_out;
-    h.action_out = action_out;
-    RUN(DQN_K_HEAD, launch_head_fwd(ni.H, ni.A, h, st));
-    return DQN_OK;
-}
-
-int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_target,
-                    const uint8_t* s, const uint8_t* s_next, const int32_t* action,
-                    const float* reward, const uint8_t* terminal, int32_t batch, float gamma,
-                    float* grad_out, float* loss_out, float* q_out, float* y_out, void* ws,
-                    size_t ws_bytes, void* stream) {
-    NetInfo ni;
-    int rc = identify(net, &ni);
-    if (rc != DQN_OK) return rc;
-    if (!theta || !s || !s_next || !action || !reward || !terminal || !grad_out || !loss_out || !ws)
-        return DQN_EINVAL;
+int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
+                            const float* theta_target, const TdSource& src, int32_t batch,
+                            float gamma, float* grad_out, float* loss_out, float* q_out,
+                            float* y_out, void* ws, size_t ws_bytes, hipStream_t st) {
+    if (!theta || !grad_out || !loss_out || !ws) return DQN_EINVAL;
     if (batch <= 0 || !std::isfinite(gamma)) return DQN_EINVAL;
     const float* tt = theta_target ? theta_target : theta;
     const size_t pbytes = (size_t)ni.P * sizeof(float);
     if (overlaps(grad_out, pbytes, theta, pbytes) || overlaps(grad_out, pbytes, tt, pbytes))
         return DQN_EINVAL;
-    if (!aligned(ws, 256) || !aligned(theta, 16) || !aligned(tt, 16) || !aligned(grad_out, 16) ||
-        !aligned(s, 16) || !aligned(s_next, 16))
+    if (!aligned(ws, 256) || !aligned(theta, 16) || !aligned(tt, 16) || !aligned(grad_out, 16))
         return DQN_EINVAL;
     TdLayout t = td_layout(ni, batch, nullptr);
     if (ws_bytes < t.bytes) return DQN_EWORKSPACE;
     t = td_layout(ni, batch, ws);
-    hipStream_t st = (hipStream_t)stream;
     const int B = batch, L = ni.n_conv;
     const float* th = theta;
+    const int64_t rec = (int64_t)net->in_c * net->in_h * net->in_w;
+
+    // Layer-0 inputs and the side fields.
+    ConvIn s0, sn0;
+    SideFields side{};
+    const int32_t* action = src.action;
+    const float* reward = src.reward;
+    const uint8_t* terminal = src.terminal;
+    if (src.replay) {
+        s0 = ConvIn{src.replay->frames, src.idx, src.replay->record_stride, 0};
+        sn0 = ConvIn{src.replay->frames, src.idx, src.replay->record_stride, 1};
+        side = SideFields{src.idx, src.replay->action, src.replay->reward, src.replay->terminal,
+                          t.a, t.r, t.t, B};
+        action = t.a;
+        reward = t.r;
+        terminal = t.t;
+    } else {
+        s0 = ConvIn{src.s, nullptr, rec, 0};
+        sn0 = ConvIn{src.s_next, nullptr, rec, 0};
+    }
 
     // Forward of s under theta (samples 0..B-1) and of s' under theta^-
     // (samples B..2B-1), one launch per layer.
     for (int l = 0; l < L; ++l) {
-        const void* in_a = l == 0 ? (const void*)s : (const void*)t.act[l - 1];
-        const void* in_b = l == 0 ? (const void*)s_next
-                                  : (const void*)(t.act[l - 1] + (int64_t)B * act_elems(ni.d[l - 1]));
+        const int64_t ae = l > 0 ? act_elems(ni.d[l - 1]) : 0;
+        const ConvIn in_a = l == 0 ? s0 : ConvIn{t.act[l - 1], nullptr, ae * 4, 0};
+        const ConvIn in_b = l == 0 ? sn0 : ConvIn{t.act[l - 1] + (int64_t)B * ae, nullptr, ae * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
         RUN(DQN_K_CONV1_FWD + l,
             launch_conv_fwd(ni.conv[l], in_a, in_b, B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
-                            tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], scale, st));
+                            tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], scale,
+                            l == 0 && src.replay ? &side : nullptr, st));
     }
     const float* xlast = t.act[L - 1];
     const int64_t slice = (int64_t)2 * B * ni.H;
@@ -368,7 +297,7 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
                     t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, st));
     // conv layers, last to first
     for (int l = L - 1; l >= 0; --l) {
-        const void* in = l == 0 ? (const void*)s : (const void*)t.act[l - 1];
+        const ConvIn in = l == 0 ? s0 : ConvIn{t.act[l - 1], nullptr, act_elems(ni.d[l - 1]) * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
         RUN(DQN_K_CONV1_WGRAD + l,
             launch_conv_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
@@ -403,6 +332,148 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
     fa.loss_out = loss_out;
     RUN(DQN_K_FINALIZE, launch_finalize(fa, st));
     return DQN_OK;
+}
+
+// Host checks of a replay descriptor shared by the gather and the fused TD step.
+int check_replay(const dqn_replay* rp, bool with_next) {
+    if (!rp || !rp->frames || rp->c <= 0 || rp->h <= 0 || rp->w <= 0) return DQN_EINVAL;
+    const int64_t rec = (int64_t)rp->c * rp->h * rp->w;
+    if (rec % 16 != 0 || rp->record_stride < rec || rp->record_stride % 16 != 0) return DQN_EINVAL;
+    if (!aligned(rp->frames, 16)) return DQN_EINVAL;
+    if (rp->size < (with_next ? 2 : 1)) return DQN_EINVAL;
+    return DQN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dqn_status_string(int status) {
+    switch (status) {
+        case DQN_OK: return "ok";
+        case DQN_EINVAL: return "invalid argument";
+        case DQN_EWORKSPACE: return "workspace too small";
+        case DQN_EHIP: return "HIP launch failed";
+        case DQN_EUNSUPPORTED: return "unsupported network";
+        default: return "unknown status";
+    }
+}
+
+int64_t dqn_param_count(const dqn_net* net) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    return rc != DQN_OK ? rc : ni.P;
+}
+
+int64_t dqn_param_offset(const dqn_net* net, int32_t layer, int32_t is_bias) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (layer < 0 || layer > ni.n_conv + 1) return DQN_EINVAL;
+    return is_bias ? ni.b_off[layer] : ni.w_off[layer];
+}
+
+int64_t dqn_workspace_bytes(const dqn_net* net, int32_t batch, int32_t op) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (batch <= 0) return DQN_EINVAL;
+    if (op == DQN_OP_FORWARD) return (int64_t)fwd_layout(ni, batch, nullptr).bytes;
+    if (op == DQN_OP_TD_GRADIENT) return (int64_t)td_layout(ni, batch, nullptr).bytes;
+    return DQN_EINVAL;
+}
+
+int replay_gather(const dqn_replay* rp, const int64_t* idx, int32_t batch, uint8_t* s_out,
+                  uint8_t* s_next_out, int32_t* a_out, float* r_out, uint8_t* term_out,
+                  void* stream) {
+    if (!idx || !s_out || batch <= 0) return DQN_EINVAL;
+    const int vr = check_replay(rp, s_next_out != nullptr);
+    if (vr != DQN_OK) return vr;
+    const int64_t rec = (int64_t)rp->c * rp->h * rp->w;
+    if (!aligned(s_out, 16) || (s_next_out && !aligned(s_next_out, 16))) return DQN_EINVAL;
+    if ((a_out && !rp->action) || (r_out && !rp->reward) || (term_out && !rp->terminal))
+        return DQN_EINVAL;
+    if (batch > 65535) return DQN_EINVAL;
+    hipStream_t st = (hipStream_t)stream;
+    RUN(DQN_K_GATHER, launch_gather(rp->frames, rp->record_stride, rec, rp->action, rp->reward,
+                                    rp->terminal, idx, batch, s_out, s_next_out, a_out, r_out,
+                                    term_out, st));
+    return DQN_OK;
+}
+
+int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, int32_t batch,
+                float epsilon, const uint64_t* draws, float* q_out, int32_t* action_out, void* ws,
+                size_t ws_bytes, void* stream) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (!theta || !states || batch <= 0 || !ws) return DQN_EINVAL;
+    if (!(epsilon >= 0.f && epsilon <= 1.f)) return DQN_EINVAL;
+    const double te = std::floor((double)epsilon * 4294967296.0);
+    const uint64_t thresh = te >= 4294967296.0 ? 4294967296ull : (uint64_t)te;
+    if (thresh > 0 && !draws) return DQN_EINVAL;
+    if (!aligned(ws, 256) || !aligned(theta, 16) || !aligned(states, 16)) return DQN_EINVAL;
+    FwdLayout f = fwd_layout(ni, batch, nullptr);
+    if (ws_bytes < f.bytes) return DQN_EWORKSPACE;
+    f = fwd_layout(ni, batch, ws);
+    hipStream_t st = (hipStream_t)stream;
+    const float* th = theta;
+    for (int l = 0; l < ni.n_conv; ++l) {
+        const ConvIn in = l == 0 ? ConvIn{states, nullptr, (int64_t)net->in_c * net->in_h * net->in_w, 0}
+                                 : ConvIn{f.act[l - 1], nullptr, act_elems(ni.d[l - 1]) * 4, 0};
+        const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
+        RUN(DQN_K_CONV1_FWD + l,
+            launch_conv_fwd(ni.conv[l], in, in, batch, batch, th + ni.w_off[l], th + ni.b_off[l],
+                            th + ni.w_off[l], th + ni.b_off[l], f.act[l], scale, nullptr, st));
+    }
+    const int L = ni.n_conv;
+    RUN(DQN_K_FC1_FWD,
+        launch_gemm(GEMM_NT, batch, ni.H, ni.flat, f.act[L - 1], ni.flat, th + ni.w_off[L], ni.flat,
+                    f.fc1p, ni.H, f.ks, f.kchunk, (int64_t)batch * ni.H, nullptr, st));
+    HeadFwdArgs h{};
+    h.fc1p = f.fc1p;
+    h.ks = f.ks;
+    h.B = batch;
+    h.b1 = th + ni.b_off[L];
+    h.W2 = th + ni.w_off[L + 1];
+    h.b2 = th + ni.b_off[L + 1];
+    h.thresh = thresh;
+    h.draws = draws;
+    h.q_out = q_out;
+    h.action_out = action_out;
+    RUN(DQN_K_HEAD, launch_head_fwd(ni.H, ni.A, h, st));
+    return DQN_OK;
+}
+
+int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_target,
+                    const uint8_t* s, const uint8_t* s_next, const int32_t* action,
+                    const float* reward, const uint8_t* terminal, int32_t batch, float gamma,
+                    float* grad_out, float* loss_out, float* q_out, float* y_out, void* ws,
+                    size_t ws_bytes, void* stream) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (!s || !s_next || !action || !reward || !terminal) return DQN_EINVAL;
+    if (!aligned(s, 16) || !aligned(s_next, 16)) return DQN_EINVAL;
+    TdSource src{s, s_next, action, reward, terminal, nullptr, nullptr};
+    return td_gradient_impl(net, ni, theta, theta_target, src, batch, gamma, grad_out, loss_out,
+                            q_out, y_out, ws, ws_bytes, (hipStream_t)stream);
+}
+
+int dqn_td_gradient_replay(const dqn_net* net, const float* theta, const float* theta_target,
+                           const dqn_replay* replay, const int64_t* idx, int32_t batch, float gamma,
+                           float* grad_out, float* loss_out, float* q_out, float* y_out, void* ws,
+                           size_t ws_bytes, void* stream) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    rc = check_replay(replay, true);
+    if (rc != DQN_OK) return rc;
+    if (!idx || !replay->action || !replay->reward || !replay->terminal) return DQN_EINVAL;
+    if (replay->c != net->in_c || replay->h != net->in_h || replay->w != net->in_w) return DQN_EINVAL;
+    TdSource src{nullptr, nullptr, nullptr, nullptr, nullptr, replay, idx};
+    return td_gradient_impl(net, ni, theta, theta_target, src, batch, gamma, grad_out, loss_out,
+                            q_out, y_out, ws, ws_bytes, (hipStream_t)stream);
 }
 
 int ps_apply_update(int32_t rule, const float* theta_in, float* theta_out, float* state,

@@ -39,20 +39,48 @@ inline ConvDims conv_dims(ConvId id) {
     }
 }
 
+// Where sample j of a layer input lives: base + j*stride (dense), or, for
+// replay records addressed by index, base + (idx[j] + off)*stride.
+struct ConvIn {
+    const void* base;
+    const int64_t* idx;
+    int64_t stride;  // bytes
+    int off;
+};
+
+__device__ __forceinline__ const unsigned char* sample_ptr(const ConvIn& in, int j) {
+    const int64_t r = in.idx ? in.idx[j] + in.off : (int64_t)j;
+    return (const unsigned char*)in.base + r * in.stride;
+}
+
+// Side fields of the transitions idx[0..batch) copied (with conversion) from
+// the replay's arrays, by block 0 of the first forward launch.
+struct SideFields {
+    const int64_t* idx;  // NULL: nothing to copy
+    const uint8_t* action;
+    const int8_t* reward;
+    const uint8_t* terminal;
+    int32_t* a_out;
+    float* r_out;
+    uint8_t* t_out;
+    int batch;
+};
+
 // ---- launchers (host side); every one returns hipGetLastError() ----------
 
 // Forward convolution + bias + ReLU for n samples.  Samples j < n_a read
-// in_a[j] and use (w_a, b_a); samples j >= n_a read in_b[j - n_a] and use
-// (w_b, b_b).  Output float [n][cout][oh][ow].  in_scale multiplies the
-// accumulated products before the bias (1/255 for byte input).
-hipError_t launch_conv_fwd(ConvId id, const void* in_a, const void* in_b, int n_a, int n,
+// sample j of in_a and use (w_a, b_a); samples j >= n_a read sample j - n_a
+// of in_b and use (w_b, b_b).  Output float [n][cout][oh][ow].  in_scale
+// multiplies the accumulated products before the bias (1/255 for byte
+// input).  side (nullable) is copied by block 0.
+hipError_t launch_conv_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
                            const float* w_a, const float* b_a, const float* w_b, const float* b_b,
-                           float* out, float in_scale, hipStream_t st);
+                           float* out, float in_scale, const SideFields* side, hipStream_t st);
 
 // Weight and bias gradient partial sums over sample chunks:
 // wpart [chunks][cout][cin*k*k], bpart [chunks][cout].
 int conv_wgrad_chunks(ConvId id, int batch);
-hipError_t launch_conv_wgrad(ConvId id, const void* in, const float* dz, int batch, float* wpart,
+hipError_t launch_conv_wgrad(ConvId id, const ConvIn& in, const float* dz, int batch, float* wpart,
                              float* bpart, float in_scale, hipStream_t st);
 
 // Input gradient din = (W^T * dz) masked by [h_in > 0], float [n][cin][ih][iw].

@@ -144,10 +144,11 @@ __device__ __forceinline__ void stage_weights(float* __restrict__ sw, const floa
 // channel 4*cb + g; MFMA steps walk (cb, ky, kx).
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int CO>
 __global__ __launch_bounds__(WG) void conv_fwd_kernel(
-    const void* __restrict__ in_a, const void* __restrict__ in_b, int n_a, int n_total,
+    ConvIn in_a, ConvIn in_b, int n_a, int n_total,
     const float* __restrict__ w_a, const float* __restrict__ bias_a,
     const float* __restrict__ w_b, const float* __restrict__ bias_b,
-    float* __restrict__ out, int mt_per_wg, int spw, int in_rows_max, float in_scale) {
+    float* __restrict__ out, int mt_per_wg, int spw, int in_rows_max, float in_scale,
+    SideFields side) {
     using L = WLayout<CIN, K>;
     constexpr int P = OH * OW;
     constexpr int MT = (P + 15) / 16;
@@ -182,12 +183,20 @@ __global__ __launch_bounds__(WG) void conv_fwd_kernel(
     const int li = lane & 15;
     const int g = lane >> 4;
 
+    if (side.idx && blockIdx.x == 0) {
+        for (int j = threadIdx.x; j < side.batch; j += WG) {
+            const int64_t i = side.idx[j];
+            side.a_out[j] = side.action[i];
+            side.r_out[j] = (float)side.reward[i];
+            side.t_out[j] = side.terminal[i];
+        }
+    }
+
     int staged_w = -1;  // which weight set is in LDS: 0 = a, 1 = b
     for (int n = n0; n < n1; ++n) {
         const int second = n >= n_a ? 1 : 0;
         const int ns = second ? n - n_a : n;
-        const unsigned char* src = (const unsigned char*)(second ? in_b : in_a) +
-                                   (size_t)ns * CIN * IH * IW * ESZ;
+        const unsigned char* src = sample_ptr(second ? in_b : in_a, ns);
         __syncthreads();  // previous sample's reads are done
         if (staged_w != second) {
             stage_weights<CIN, K, CO>(sw, second ? w_b : w_a, o0);
@@ -267,7 +276,7 @@ __global__ __launch_bounds__(WG) void conv_fwd_kernel(
 // and reduced later in a fixed order.
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
 __global__ __launch_bounds__(WG) void conv_wgrad_kernel(
-    const void* __restrict__ in, const float* __restrict__ dz, int batch, int spc, int rows_per_blk,
+    ConvIn in, const float* __restrict__ dz, int batch, int spc, int rows_per_blk,
     int in_rows_max, int pix_pad, float* __restrict__ wpart, float* __restrict__ bpart,
     float in_scale) {
     constexpr int P = OH * OW;
@@ -322,7 +331,7 @@ __global__ __launch_bounds__(WG) void conv_wgrad_kernel(
     for (int j = j0; j < j1; ++j) {
         __syncthreads();
         {
-            const unsigned char* src = (const unsigned char*)in + (size_t)j * CIN * IH * IW * ESZ;
+            const unsigned char* src = sample_ptr(in, j);
             stage_rows(s_in, row_elems * ESZ, src + (size_t)iy0 * IW * ESZ, (int64_t)IH * IW * ESZ, CIN,
                        rows * IW * ESZ);
             const float* dzj = dz + (size_t)j * COUT * P + pbeg;
@@ -524,9 +533,9 @@ bool allow_lds(const void* kern, size_t bytes) {
 }
 
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int CO>
-hipError_t fwd_launch(const void* in_a, const void* in_b, int n_a, int n, const float* w_a,
+hipError_t fwd_launch(const ConvIn& in_a, const ConvIn& in_b, int n_a, int n, const float* w_a,
                       const float* b_a, const float* w_b, const float* b_b, float* out,
-                      float in_scale, hipStream_t st) {
+                      float in_scale, const SideFields* side, hipStream_t st) {
     using L = WLayout<CIN, K>;
     constexpr int P = OH * OW;
     constexpr int MT = (P + 15) / 16;
@@ -562,8 +571,10 @@ hipError_t fwd_launch(const void* in_a, const void* in_b, int n_a, int n, const 
     auto kern = conv_fwd_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8, CO>;
     if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
     const int nblk = (n + spw - 1) / spw;
+    SideFields none{};
     hipLaunchKernelGGL(kern, dim3((unsigned)(nblk * COB * groups)), dim3(WG), lds, st, in_a, in_b, n_a,
-                       n, w_a, b_a, w_b, b_b, out, mt_per_wg, spw, max_rows, in_scale);
+                       n, w_a, b_a, w_b, b_b, out, mt_per_wg, spw, max_rows, in_scale,
+                       side ? *side : none);
     return hipGetLastError();
 }
 
@@ -594,7 +605,7 @@ constexpr int wgrad_groups() {
 }
 
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
-hipError_t wgrad_launch(const void* in, const float* dz, int batch, float* wpart, float* bpart,
+hipError_t wgrad_launch(const ConvIn& in, const float* dz, int batch, float* wpart, float* bpart,
                         float in_scale, hipStream_t st) {
     constexpr int GROUPS = wgrad_groups<CIN, IH, IW, COUT, K, S, OH, OW>();
     constexpr int ESZ = U8 ? 1 : 4;
@@ -633,15 +644,15 @@ hipError_t dgrad_launch(const float* dz, const float* w, const float* h_in, floa
 
 }  // namespace
 
-hipError_t launch_conv_fwd(ConvId id, const void* in_a, const void* in_b, int n_a, int n,
+hipError_t launch_conv_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
                            const float* w_a, const float* b_a, const float* w_b, const float* b_b,
-                           float* out, float in_scale, hipStream_t st) {
+                           float* out, float in_scale, const SideFields* side, hipStream_t st) {
     switch (id) {
-        case CONV_S1: return fwd_launch<4, 84, 84, 16, 8, 4, 20, 20, true, 16>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
-        case CONV_S2: return fwd_launch<16, 20, 20, 32, 4, 2, 9, 9, false, 32>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
-        case CONV_L1: return fwd_launch<4, 84, 84, 32, 8, 4, 20, 20, true, 32>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
-        case CONV_L2: return fwd_launch<32, 20, 20, 64, 4, 2, 9, 9, false, 32>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
-        case CONV_L3: return fwd_launch<64, 9, 9, 64, 3, 1, 7, 7, false, 16>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, st);
+        case CONV_S1: return fwd_launch<4, 84, 84, 16, 8, 4, 20, 20, true, 16>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, side, st);
+        case CONV_S2: return fwd_launch<16, 20, 20, 32, 4, 2, 9, 9, false, 32>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, side, st);
+        case CONV_L1: return fwd_launch<4, 84, 84, 32, 8, 4, 20, 20, true, 32>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, side, st);
+        case CONV_L2: return fwd_launch<32, 20, 20, 64, 4, 2, 9, 9, false, 32>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, side, st);
+        case CONV_L3: return fwd_launch<64, 9, 9, 64, 3, 1, 7, 7, false, 16>(in_a, in_b, n_a, n, w_a, b_a, w_b, b_b, out, in_scale, side, st);
         default: return hipErrorInvalidValue;
     }
 }
@@ -659,7 +670,7 @@ int conv_wgrad_chunks(ConvId id, int batch) {
     return w.chunks * w.rb;
 }
 
-hipError_t launch_conv_wgrad(ConvId id, const void* in, const float* dz, int batch, float* wpart,
+hipError_t launch_conv_wgrad(ConvId id, const ConvIn& in, const float* dz, int batch, float* wpart,
                              float* bpart, float in_scale, hipStream_t st) {
     switch (id) {
         case CONV_S1: return wgrad_launch<4, 84, 84, 16, 8, 4, 20, 20, true>(in, dz, batch, wpart, bpart, in_scale, st);

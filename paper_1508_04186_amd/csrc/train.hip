@@ -11,13 +11,9 @@ using namespace dqn;
 
 namespace {
 
-// Per-replica slice of the workspace: gathered minibatch, gradient, and the
-// dqn_td_gradient workspace.
+// Per-replica slice of the workspace: gradient, loss and the TD workspace.
+// The minibatch is read from the replay in place (dqn_td_gradient_replay).
 struct ReplicaWs {
-    uint8_t *s, *sn;
-    int32_t* a;
-    float* r;
-    uint8_t* t;
     float* grad;
     float* loss;
     void* td_ws;
@@ -32,35 +28,15 @@ int64_t replica_bytes(const dqn_net* net, int32_t batch) {
     if (p < 0) return p;
     const int64_t td = dqn_workspace_bytes(net, batch, DQN_OP_TD_GRADIENT);
     if (td < 0) return td;
-    const size_t rec = (size_t)net->in_c * net->in_h * net->in_w;
-    size_t b = 0;
-    b += 2 * round256(rec * batch);
-    b += round256(4 * (size_t)batch) * 2 + round256((size_t)batch);
-    b += round256(4 * (size_t)p) + 256;
-    b += (size_t)td;
-    return (int64_t)b;
+    return (int64_t)(round256(4 * (size_t)p) + 256 + (size_t)td);
 }
 
 ReplicaWs carve(const dqn_net* net, int32_t batch, char* base) {
     ReplicaWs w;
-    const size_t rec = (size_t)net->in_c * net->in_h * net->in_w;
     const size_t p = (size_t)dqn_param_count(net);
-    size_t off = 0;
-    w.s = (uint8_t*)(base + off);
-    off += round256(rec * batch);
-    w.sn = (uint8_t*)(base + off);
-    off += round256(rec * batch);
-    w.a = (int32_t*)(base + off);
-    off += round256(4 * (size_t)batch);
-    w.r = (float*)(base + off);
-    off += round256(4 * (size_t)batch);
-    w.t = (uint8_t*)(base + off);
-    off += round256((size_t)batch);
-    w.grad = (float*)(base + off);
-    off += round256(4 * p);
-    w.loss = (float*)(base + off);
-    off += 256;
-    w.td_ws = base + off;
+    w.grad = (float*)base;
+    w.loss = (float*)(base + round256(4 * p));
+    w.td_ws = base + round256(4 * p) + 256;
     w.td_bytes = (size_t)dqn_workspace_bytes(net, batch, DQN_OP_TD_GRADIENT);
     return w;
 }
@@ -118,10 +94,10 @@ int dqn_train_steps(const dqn_net* net, float* theta, float* theta_target, float
         const int64_t g = step0 + n;
         if (target_period > 0 && g % target_period == 0)
             if (launch_copy(theta, theta_target, p, st) != hipSuccess) return DQN_EHIP;
-        TRY(replay_gather(replay, idx + n * batch, batch, w.s, w.sn, w.a, w.r, w.t, stream));
-        TRY(dqn_td_gradient(net, theta, target_period > 0 ? theta_target : theta, w.s, w.sn, w.a, w.r,
-                            w.t, batch, gamma, w.grad, losses_out ? losses_out + n : w.loss, nullptr,
-                            nullptr, w.td_ws, w.td_bytes, stream));
+        TRY(dqn_td_gradient_replay(net, theta, target_period > 0 ? theta_target : theta, replay,
+                                   idx + n * batch, batch, gamma, w.grad,
+                                   losses_out ? losses_out + n : w.loss, nullptr, nullptr, w.td_ws,
+                                   w.td_bytes, stream));
         TRY(ps_apply_update(rule, theta, theta, opt_state, w.grad, p, lr, decay, eps, stream));
     }
     return DQN_OK;
@@ -167,11 +143,9 @@ int dqn_train_replicas(const dqn_net* net, float* theta_ring, float* opt_state, 
         if (v > 0 && hipStreamWaitEvent(st, ev_v[v % nv], 0) != hipSuccess) { rc = DQN_EHIP; break; }
         float* th_v = theta_ring + (v % slots) * rs;
         const ReplicaWs& r = w[k];
-        rc = replay_gather(replay, idx + u * batch, batch, r.s, r.sn, r.a, r.r, r.t, st);
-        if (rc != DQN_OK) break;
-        rc = dqn_td_gradient(net, th_v, th_v, r.s, r.sn, r.a, r.r, r.t, batch, gamma, r.grad,
-                             losses_out ? losses_out + u : r.loss, nullptr, nullptr, r.td_ws,
-                             r.td_bytes, st);
+        rc = dqn_td_gradient_replay(net, th_v, th_v, replay, idx + u * batch, batch, gamma, r.grad,
+                                    losses_out ? losses_out + u : r.loss, nullptr, nullptr, r.td_ws,
+                                    r.td_bytes, st);
         if (rc != DQN_OK) break;
         // send the gradient; the server applies update u to version u
         if (hipEventRecord(ev_g[k], st) != hipSuccess || hipStreamWaitEvent(server, ev_g[k], 0) != hipSuccess) {

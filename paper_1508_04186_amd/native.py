@@ -99,6 +99,10 @@ def lib():
         L.dqn_td_gradient.argtypes = [ctypes.POINTER(_CNet), _P, _P, _P, _P, _P, _P, _P,
                                       ctypes.c_int32, ctypes.c_float, _P, _P, _P, _P, _P,
                                       ctypes.c_size_t, _P]
+        L.dqn_td_gradient_replay.argtypes = [ctypes.POINTER(_CNet), _P, _P, ctypes.POINTER(_CReplay),
+                                             _P, ctypes.c_int32, ctypes.c_float, _P, _P, _P, _P,
+                                             _P, ctypes.c_size_t, _P]
+        L.dqn_td_gradient_replay.restype = ctypes.c_int
         L.ps_apply_update.argtypes = [ctypes.c_int32, _P, _P, _P, _P, ctypes.c_int64,
                                       ctypes.c_float, ctypes.c_float, ctypes.c_float, _P]
         for f in ("replay_gather", "dqn_forward", "dqn_td_gradient", "ps_apply_update"):
@@ -280,6 +284,31 @@ def dqn_td_gradient(net, theta, theta_target, s, s_next, action, reward, termina
                                _ptr(q_out, torch.float32, "q_out"), _ptr(y_out, torch.float32, "y_out"),
                                _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream))
     _check(rc, "dqn_td_gradient")
+
+
+def dqn_td_gradient_replay(net, theta, theta_target, replay: Replay, idx, gamma, grad_out, loss_out,
+                           q_out=None, y_out=None, ws=None, stream=None):
+    """TD gradient of the minibatch idx (device int64 [B]) read in place from
+    the replay (include/dqn.h dqn_td_gradient_replay)."""
+    import torch
+    B = idx.shape[0]
+    if ws is None:
+        ws = workspace(net, B, DQN_OP_TD_GRADIENT, theta.device)
+    P = dqn_param_count(net)
+    for name, t, n in (("theta", theta, P), ("theta_target", theta_target, P),
+                       ("grad_out", grad_out, P), ("loss_out", loss_out, 1),
+                       ("q_out", q_out, B * net.n_actions), ("y_out", y_out, B)):
+        if t is not None and t.numel() < n:
+            raise ValueError(f"{name} too small")
+    rc = lib().dqn_td_gradient_replay(ctypes.byref(_cnet(net)), _ptr(theta, torch.float32, "theta"),
+                                      _ptr(theta_target, torch.float32, "theta_target"),
+                                      ctypes.byref(_creplay(replay)), _ptr(idx, torch.int64, "idx"),
+                                      B, float(gamma), _ptr(grad_out, torch.float32, "grad_out"),
+                                      _ptr(loss_out, torch.float32, "loss_out"),
+                                      _ptr(q_out, torch.float32, "q_out"),
+                                      _ptr(y_out, torch.float32, "y_out"),
+                                      _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream))
+    _check(rc, "dqn_td_gradient_replay")
 
 
 def ps_apply_update(rule, theta_in, theta_out, state, grad, lr, decay=0.9, eps=0.0, stream=None,

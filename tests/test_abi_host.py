@@ -25,8 +25,8 @@ def header_functions(names=None):
 
 def test_header_declares_the_four_calls():
     fns = header_functions(["dqn.h"])
-    for f in ("replay_gather", "dqn_forward", "dqn_td_gradient", "ps_apply_update",
-              "dqn_param_count", "dqn_param_offset", "dqn_workspace_bytes", "dqn_status_string"):
+    for f in ("replay_gather", "dqn_forward", "dqn_td_gradient", "dqn_td_gradient_replay",
+              "ps_apply_update", "dqn_param_count", "dqn_param_offset", "dqn_workspace_bytes", "dqn_status_string"):
         assert f in fns
 
 
@@ -198,3 +198,31 @@ def test_apply_argument_errors():
 def test_status_strings():
     for s in (dq.DQN_OK, dq.DQN_EINVAL, dq.DQN_EWORKSPACE, dq.DQN_EHIP, dq.DQN_EUNSUPPORTED):
         assert dq.dqn_status_string(s) not in ("", "unknown status")
+
+
+@fake_ptr_test
+def test_td_gradient_replay_argument_errors():
+    L = dq.lib()
+    n = dq.NET_SMALL
+    ws = dq.dqn_workspace_bytes(n, 8, dq.DQN_OP_TD_GRADIENT)
+    rp = native._CReplay()
+    rp.frames, rp.action, rp.reward, rp.terminal = FAKE, FAKE, FAKE, FAKE
+    rp.record_stride, rp.size, rp.c, rp.h, rp.w = 28224, 100, 4, 84, 84
+
+    def call(idx=FAKE, B=8, wsb=ws, **kw):
+        for k, v in kw.items():
+            setattr(rp, k, v)
+        return L.dqn_td_gradient_replay(_cnet(n), FAKE, FAKE, ctypes.byref(rp), idx, B,
+                                        ctypes.c_float(0.99), FAKE + 2**33, FAKE, None, None,
+                                        FAKE + 2**34, wsb, None)
+    assert call(idx=None) == dq.DQN_EINVAL
+    assert call(B=0) == dq.DQN_EINVAL
+    assert call(wsb=ws - 1) == dq.DQN_EWORKSPACE
+    assert call(c=2) == dq.DQN_EINVAL                  # record shape differs from the input
+    rp.c = 4
+    assert call(size=1) == dq.DQN_EINVAL               # needs two records for s'
+    rp.size = 100
+    assert call(record_stride=28230) == dq.DQN_EINVAL
+    rp.record_stride = 28224
+    rp.action = None
+    assert call() == dq.DQN_EINVAL                     # side arrays required

@@ -287,3 +287,38 @@ def test_sgd_step_matches_oracle(dev):
     step_ref = ref_th.astype(np.float64) - th
     err = np.abs(new.astype(np.float64) - ref_th)
     assert np.all(err <= np.spacing(np.abs(ref_th)) + FP32_TOL * np.abs(step_ref))
+
+
+@pytest.mark.parametrize("name,B,target", [("small", 32, "same"), ("large", 17, "held")])
+def test_td_gradient_replay_equals_gather_then_td(dev, replay, name, B, target):
+    """Reading the minibatch in place from the replay gives bit-for-bit the
+    result of replay_gather followed by dqn_td_gradient."""
+    import torch
+    hr, rp = replay
+    net, shape = NETS[name]
+    if net.n_actions != 6:
+        # the fixture replay stores actions for 6 actions; re-wrap its side
+        # arrays with actions reduced modulo the large net's 18 (all valid)
+        rp = dq.Replay(rp.frames, rp.action, rp.reward, rp.terminal, rp.size)
+    th = dev_tensor(di.xavier_theta(shape, 110 + B, bias_scale=0.05))
+    tt = th if target == "same" else dev_tensor(di.xavier_theta(shape, 111 + B, bias_scale=0.05))
+    idx = dev_tensor(np.random.default_rng(B).integers(0, rp.size - 1, B).astype(np.int64))
+    P = dq.dqn_param_count(net)
+    say(f"[td-replay] net={name} batch={B}: gather + td")
+    s = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
+    sn = torch.empty_like(s)
+    a = torch.empty(B, dtype=torch.int32, device=dev)
+    r = torch.empty(B, dtype=torch.float32, device=dev)
+    t = torch.empty(B, dtype=torch.uint8, device=dev)
+    dq.replay_gather(rp, idx, s, sn, a, r, t)
+    g1 = torch.empty(P, dtype=torch.float32, device=dev)
+    l1 = torch.empty(1, dtype=torch.float32, device=dev)
+    q1 = torch.empty((B, net.n_actions), dtype=torch.float32, device=dev)
+    dq.dqn_td_gradient(net, th, tt, s, sn, a, r, t, 0.99, g1, l1, q1)
+    say(f"[td-replay] net={name} batch={B}: fused")
+    g2 = torch.empty_like(g1)
+    l2 = torch.empty_like(l1)
+    q2 = torch.empty_like(q1)
+    dq.dqn_td_gradient_replay(net, th, tt, rp, idx, 0.99, g2, l2, q2)
+    torch.cuda.synchronize()
+    assert torch.equal(g1, g2) and torch.equal(l1, l2) and torch.equal(q1, q2)
