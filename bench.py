@@ -124,6 +124,10 @@ def kernel_work(shape, B, forward_only=False):
     else:
         w["fc1_wgrad"] = (2 * B * H * F, 0)
         w["fc1_dgrad"] = (2 * B * H * F, 0)
+        # paired launches (weight + input gradient of one layer)
+        w["fc1_bwd"] = (4 * B * H * F, 0)
+        for l in range(1, len(dims)):
+            w[f"conv{l+1}_bwd"] = (w[f"conv{l+1}_wgrad"][0] + w[f"conv{l+1}_dgrad"][0], 0)
         w["gather"] = (0, 4 * B * rec)          # read s and s', write both
         w["apply"] = (0, 12 * P)                # SGD: read theta and g, write theta
         w["finalize"] = (0, 0)
@@ -134,7 +138,7 @@ def kernel_work(shape, B, forward_only=False):
 # memory-bound gather); the head and finalize are latency-bound reductions.
 ROOFLINE_KERNELS = ("conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "fc1_wgrad", "fc1_dgrad",
                     "conv1_wgrad", "conv2_wgrad", "conv3_wgrad", "conv2_dgrad", "conv3_dgrad",
-                    "gather", "apply")
+                    "fc1_bwd", "conv2_bwd", "conv3_bwd", "gather", "apply")
 
 
 class Profiler:

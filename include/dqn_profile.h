@@ -40,7 +40,10 @@ typedef enum {
     DQN_K_CONV3_DGRAD = 12,
     DQN_K_FINALIZE = 13,
     DQN_K_APPLY = 14,
-    DQN_K_COUNT = 15
+    DQN_K_FC1_BWD = 15,     /* fc1 weight + input gradient in one launch (small batch) */
+    DQN_K_CONV2_BWD = 16,   /* conv2 weight + input gradient in one launch (small batch) */
+    DQN_K_CONV3_BWD = 17,   /* conv3 weight + input gradient in one launch (small batch) */
+    DQN_K_COUNT = 18
 } dqn_kernel;
 
 int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs);

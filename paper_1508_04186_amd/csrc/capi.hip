@@ -73,6 +73,10 @@ int identify(const dqn_net* net, NetInfo* ni) {
 
 inline int64_t act_elems(const ConvDims& c) { return (int64_t)c.cout * c.oh * c.ow; }
 
+// Largest batch whose backward kernels are launched in pairs (above it each
+// kernel alone fills the chip and keeps its own occupancy).
+constexpr int kPairMaxBatch = 256;
+
 // fc1 forward split-K: enough slices that the launch covers the chip.
 void fc1_split(int rows, int H, int K, int* ks, int* kchunk) {
     // Few enough slices that the head's reduction stays short.
@@ -288,17 +292,31 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     h.y_out = y_out;
     RUN(DQN_K_HEAD, launch_head_td(ni.H, ni.A, h, st));
 
-    // fc1: weight gradient and the masked gradient of the last conv output.
-    RUN(DQN_K_FC1_WGRAD,
-        launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat, grad_out + ni.w_off[L],
-                    ni.flat, 1, (B + 31) / 32 * 32, 0, nullptr, st));
-    RUN(DQN_K_FC1_DGRAD,
-        launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
-                    t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, st));
-    // conv layers, last to first
+    // fc1: weight gradient and the masked gradient of the last conv output;
+    // then the conv layers, last to first.  At small batch each layer's two
+    // independent backward kernels share one launch.
+    const bool paired = B <= kPairMaxBatch;
+    if (paired) {
+        RUN(DQN_K_FC1_BWD,
+            launch_gemm_wgrad_dgrad(ni.H, ni.flat, B, t.dz1, xlast, grad_out + ni.w_off[L],
+                                    th + ni.w_off[L], t.dconv[L - 1], st));
+    } else {
+        RUN(DQN_K_FC1_WGRAD,
+            launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat,
+                        grad_out + ni.w_off[L], ni.flat, 1, (B + 31) / 32 * 32, 0, nullptr, st));
+        RUN(DQN_K_FC1_DGRAD,
+            launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
+                        t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, st));
+    }
     for (int l = L - 1; l >= 0; --l) {
         const ConvIn in = l == 0 ? s0 : ConvIn{t.act[l - 1], nullptr, act_elems(ni.d[l - 1]) * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
+        if (l > 0 && paired) {
+            RUN(DQN_K_CONV2_BWD + (l - 1),
+                launch_conv_bwd(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l],
+                                th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], st));
+            continue;
+        }
         RUN(DQN_K_CONV1_WGRAD + l,
             launch_conv_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
         if (l > 0)

@@ -83,6 +83,12 @@ int conv_wgrad_chunks(ConvId id, int batch);
 hipError_t launch_conv_wgrad(ConvId id, const ConvIn& in, const float* dz, int batch, float* wpart,
                              float* bpart, float in_scale, hipStream_t st);
 
+// Weight gradient (as launch_conv_wgrad, fp32 input) and input gradient (as
+// launch_conv_dgrad) of one layer from the same dz, in a single launch.
+hipError_t launch_conv_bwd(ConvId id, const ConvIn& in, const float* dz, int batch, float* wpart,
+                           float* bpart, const float* w, const float* h_in, float* din,
+                           hipStream_t st);
+
 // Input gradient din = (W^T * dz) masked by [h_in > 0], float [n][cin][ih][iw].
 hipError_t launch_conv_dgrad(ConvId id, const float* dz, const float* w, const float* h_in,
                              float* din, int batch, hipStream_t st);
@@ -95,6 +101,12 @@ enum GemmKind { GEMM_NT = 0, GEMM_TN = 1, GEMM_NN = 2 };
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
                        const float* mask, hipStream_t st);
+
+// fc1 backward for batch B: dW [H][F] = dz1^T x (x = first B rows of the last
+// conv output) and dx [B][F] = (dz1 W) masked by [x > 0], as one launch where
+// possible.
+hipError_t launch_gemm_wgrad_dgrad(int H, int F, int B, const float* dz1, const float* x,
+                                   float* dW, const float* W, float* dx, hipStream_t st);
 
 struct HeadTdArgs {
     const float* fc1p;   // [ks][2B][H] split-K partials of fc1 (rows < B: s, >= B: s')

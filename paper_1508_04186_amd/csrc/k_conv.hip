@@ -274,11 +274,24 @@ __global__ __launch_bounds__(WG) void conv_fwd_kernel(
 // stages the input rows and the dz rows of its block, then accumulates in
 // registers.  Partial sums per (chunk, row block) are written without atomics
 // and reduced later in a fixed order.
+struct WgradParams {
+    ConvIn in;
+    const float* dz;
+    int batch, spc, rows_per_blk, in_rows_max, pix_pad;
+    float* wpart;
+    float* bpart;
+    float in_scale;
+};
+
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
-__global__ __launch_bounds__(WG) void conv_wgrad_kernel(
-    ConvIn in, const float* __restrict__ dz, int batch, int spc, int rows_per_blk,
-    int in_rows_max, int pix_pad, float* __restrict__ wpart, float* __restrict__ bpart,
-    float in_scale) {
+__device__ __forceinline__ void conv_wgrad_body(const WgradParams& p, int bid, unsigned char* smem) {
+    const ConvIn& in = p.in;
+    const float* __restrict__ dz = p.dz;
+    const int batch = p.batch, spc = p.spc, rows_per_blk = p.rows_per_blk;
+    const int in_rows_max = p.in_rows_max, pix_pad = p.pix_pad;
+    float* __restrict__ wpart = p.wpart;
+    float* __restrict__ bpart = p.bpart;
+    const float in_scale = p.in_scale;
     constexpr int P = OH * OW;
     constexpr int NCOL = CIN * K * K;
     constexpr int NTT = NCOL / 16;
@@ -286,13 +299,12 @@ __global__ __launch_bounds__(WG) void conv_wgrad_kernel(
     constexpr int MT = COUT / 16;
     constexpr int ESZ = U8 ? 1 : 4;
     const int RB = (OH + rows_per_blk - 1) / rows_per_blk;
-    extern __shared__ __align__(16) unsigned char smem[];
     const int in_bytes = ((CIN * in_rows_max * IW * ESZ + 15) / 16) * 16;
     unsigned char* s_in = smem;
     float* s_dz = (float*)(smem + in_bytes);          // [COUT][pix_pad]
     int* s_pix = (int*)(s_dz + COUT * pix_pad);       // [pix_pad]
 
-    int b = blockIdx.x;
+    int b = bid;
     const int grp = b % GROUPS;
     b /= GROUPS;
     const int rb = b % RB;
@@ -384,6 +396,12 @@ __global__ __launch_bounds__(WG) void conv_wgrad_kernel(
     if (grp == 0 && threadIdx.x < COUT) bpart[(size_t)slot * COUT + threadIdx.x] = bacc;
 }
 
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
+__global__ __launch_bounds__(WG) void conv_wgrad_kernel(WgradParams p) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    conv_wgrad_body<CIN, IH, IW, COUT, K, S, OH, OW, U8>(p, blockIdx.x, smem);
+}
+
 // ---------------------------------------------------------------------------
 // Input gradient (transposed convolution), split into stride phases so no
 // MFMA multiplies a structural zero: input pixel (S*qy + py, S*qx + px)
@@ -391,10 +409,21 @@ __global__ __launch_bounds__(WG) void conv_wgrad_kernel(
 // ty, tx < K/S.  GEMM view per (sample, phase): M = phase pixels, N = cin,
 // contraction over (o, ty, tx).  dz is staged in LDS with a zero border, and
 // the phase's weight taps for a block of CI input channels as [tap][o][c].
+struct DgradParams {
+    const float* dz;
+    const float* W;
+    const float* h_in;
+    float* din;
+    int mt_per_wg;
+};
+
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int CI>
-__global__ __launch_bounds__(WG) void conv_dgrad_kernel(
-    const float* __restrict__ dz, const float* __restrict__ W, const float* __restrict__ h_in,
-    float* __restrict__ din, int mt_per_wg) {
+__device__ __forceinline__ void conv_dgrad_body(const DgradParams& p, int bid, unsigned char* smem) {
+    const float* __restrict__ dz = p.dz;
+    const float* __restrict__ W = p.W;
+    const float* __restrict__ h_in = p.h_in;
+    float* __restrict__ din = p.din;
+    const int mt_per_wg = p.mt_per_wg;
     static_assert(K % S == 0, "phase decomposition needs k divisible by stride");
     constexpr int T = K / S;
     constexpr int TT = T * T;
@@ -407,12 +436,11 @@ __global__ __launch_bounds__(WG) void conv_dgrad_kernel(
     constexpr int CIB = CIN / CI;
     constexpr int RCW = CI + 1;   // LDS row stride of the [tap][o][c] weight slice
     constexpr int MTM = (QHM * QWM + 15) / 16;
-    extern __shared__ __align__(16) unsigned char smem[];
     float* s_dz = (float*)smem;                 // [COUT][PH][PW]
     float* s_w = s_dz + COUT * PH * PW;         // [TT][COUT][RCW]
 
     const int groups = (MTM + mt_per_wg - 1) / mt_per_wg;
-    int b = blockIdx.x;
+    int b = bid;
     const int grp = b % groups;
     b /= groups;
     const int cib = b % CIB;
@@ -515,6 +543,25 @@ __global__ __launch_bounds__(WG) void conv_dgrad_kernel(
     }
 }
 
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int CI>
+__global__ __launch_bounds__(WG) void conv_dgrad_kernel(DgradParams p) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    conv_dgrad_body<CIN, IH, IW, COUT, K, S, OH, OW, CI>(p, blockIdx.x, smem);
+}
+
+// Weight gradient and input gradient of one layer in a single launch: both
+// read the same dz and are independent, so at small batch one launch keeps
+// more of the chip busy than two in sequence.  Blocks [0, n_w) run the
+// weight gradient, the rest the input gradient.
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int CI>
+__global__ __launch_bounds__(WG) void conv_bwd_kernel(WgradParams w, DgradParams d, int n_w) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    if ((int)blockIdx.x < n_w)
+        conv_wgrad_body<CIN, IH, IW, COUT, K, S, OH, OW, false>(w, blockIdx.x, smem);
+    else
+        conv_dgrad_body<CIN, IH, IW, COUT, K, S, OH, OW, CI>(d, blockIdx.x - n_w, smem);
+}
+
 // ---------------------------------------------------------------------------
 // Host-side launch shapes.
 
@@ -604,9 +651,10 @@ constexpr int wgrad_groups() {
     return (CIN * K * K / 16) / 4;
 }
 
+// Launch parameters of a layer's weight gradient for `batch` samples.
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
-hipError_t wgrad_launch(const ConvIn& in, const float* dz, int batch, float* wpart, float* bpart,
-                        float in_scale, hipStream_t st) {
+WgradParams wgrad_params(const ConvIn& in, const float* dz, int batch, float* wpart, float* bpart,
+                         float in_scale, int* blocks, size_t* lds) {
     constexpr int GROUPS = wgrad_groups<CIN, IH, IW, COUT, K, S, OH, OW>();
     constexpr int ESZ = U8 ? 1 : 4;
     const WgradShape w = wgrad_shape(batch, GROUPS, OH);
@@ -614,17 +662,16 @@ hipError_t wgrad_launch(const ConvIn& in, const float* dz, int batch, float* wpa
     while ((in_rows_max * IW * ESZ) % 16 != 0) ++in_rows_max;
     const int pix_pad = (w.rows_per_blk * OW + 3) / 4 * 4;
     const size_t in_bytes = ((size_t)CIN * in_rows_max * IW * ESZ + 15) / 16 * 16;
-    const size_t lds = in_bytes + (size_t)COUT * pix_pad * 4 + (size_t)pix_pad * 4;
-    auto kern = conv_wgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8>;
-    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(w.chunks * w.rb * GROUPS)), dim3(WG), lds, st, in, dz,
-                       batch, w.spc, w.rows_per_blk, in_rows_max, pix_pad, wpart, bpart, in_scale);
-    return hipGetLastError();
+    *lds = in_bytes + (size_t)COUT * pix_pad * 4 + (size_t)pix_pad * 4;
+    *blocks = w.chunks * w.rb * GROUPS;
+    return WgradParams{in, dz, batch, w.spc, w.rows_per_blk, in_rows_max, pix_pad, wpart, bpart,
+                       in_scale};
 }
 
+// Launch parameters of a layer's input gradient for `batch` samples.
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int CI>
-hipError_t dgrad_launch(const float* dz, const float* w, const float* h_in, float* din, int batch,
-                        hipStream_t st) {
+DgradParams dgrad_params(const float* dz, const float* w, const float* h_in, float* din, int batch,
+                         int* blocks, size_t* lds) {
     constexpr int QP = ((IH + S - 1) / S) * ((IW + S - 1) / S);
     constexpr int MTM = (QP + 15) / 16;
     constexpr int CIB = CIN / CI;
@@ -634,11 +681,50 @@ hipError_t dgrad_launch(const float* dz, const float* w, const float* h_in, floa
     const long wgs = (long)batch * S * S * CIB;
     const int mt_per_wg = wgs >= 1024 ? MTM : 4;
     const int groups = (MTM + mt_per_wg - 1) / mt_per_wg;
-    const size_t lds = ((size_t)COUT * PH * PW + (size_t)T * T * COUT * (CI + 1)) * 4;
+    *lds = ((size_t)COUT * PH * PW + (size_t)T * T * COUT * (CI + 1)) * 4;
+    *blocks = (int)(wgs * groups);
+    return DgradParams{dz, w, h_in, din, mt_per_wg};
+}
+
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8>
+hipError_t wgrad_launch(const ConvIn& in, const float* dz, int batch, float* wpart, float* bpart,
+                        float in_scale, hipStream_t st) {
+    int blocks;
+    size_t lds;
+    const WgradParams p = wgrad_params<CIN, IH, IW, COUT, K, S, OH, OW, U8>(in, dz, batch, wpart, bpart,
+                                                                         in_scale, &blocks, &lds);
+    auto kern = conv_wgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8>;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(WG), lds, st, p);
+    return hipGetLastError();
+}
+
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int CI>
+hipError_t dgrad_launch(const float* dz, const float* w, const float* h_in, float* din, int batch,
+                        hipStream_t st) {
+    int blocks;
+    size_t lds;
+    const DgradParams p = dgrad_params<CIN, IH, IW, COUT, K, S, OH, OW, CI>(dz, w, h_in, din, batch,
+                                                                         &blocks, &lds);
     auto kern = conv_dgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, CI>;
     if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(wgs * groups)), dim3(WG), lds, st, dz, w, h_in, din,
-                       mt_per_wg);
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(WG), lds, st, p);
+    return hipGetLastError();
+}
+
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int CI>
+hipError_t bwd_launch(const ConvIn& in, const float* dz, int batch, float* wpart, float* bpart,
+                      const float* w, const float* h_in, float* din, hipStream_t st) {
+    int bw, bd;
+    size_t lw, ld;
+    const WgradParams pw = wgrad_params<CIN, IH, IW, COUT, K, S, OH, OW, false>(in, dz, batch, wpart,
+                                                                             bpart, 1.f, &bw, &lw);
+    const DgradParams pd = dgrad_params<CIN, IH, IW, COUT, K, S, OH, OW, CI>(dz, w, h_in, din, batch,
+                                                                          &bd, &ld);
+    const size_t lds = std::max(lw, ld);
+    auto kern = conv_bwd_kernel<CIN, IH, IW, COUT, K, S, OH, OW, CI>;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(bw + bd)), dim3(WG), lds, st, pw, pd, bw);
     return hipGetLastError();
 }
 
@@ -688,6 +774,21 @@ hipError_t launch_conv_dgrad(ConvId id, const float* dz, const float* w, const f
         case CONV_S2: return dgrad_launch<16, 20, 20, 32, 4, 2, 9, 9, 16>(dz, w, h_in, din, batch, st);
         case CONV_L2: return dgrad_launch<32, 20, 20, 64, 4, 2, 9, 9, 16>(dz, w, h_in, din, batch, st);
         case CONV_L3: return dgrad_launch<64, 9, 9, 64, 3, 1, 7, 7, 16>(dz, w, h_in, din, batch, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace dqn
+
+namespace dqn {
+
+hipError_t launch_conv_bwd(ConvId id, const ConvIn& in, const float* dz, int batch, float* wpart,
+                           float* bpart, const float* w, const float* h_in, float* din,
+                           hipStream_t st) {
+    switch (id) {
+        case CONV_S2: return bwd_launch<16, 20, 20, 32, 4, 2, 9, 9, 16>(in, dz, batch, wpart, bpart, w, h_in, din, st);
+        case CONV_L2: return bwd_launch<32, 20, 20, 64, 4, 2, 9, 9, 16>(in, dz, batch, wpart, bpart, w, h_in, din, st);
+        case CONV_L3: return bwd_launch<64, 9, 9, 64, 3, 1, 7, 7, 16>(in, dz, batch, wpart, bpart, w, h_in, din, st);
         default: return hipErrorInvalidValue;
     }
 }

@@ -433,12 +433,9 @@ def dqn_train_replicas(net, theta_ring, opt_state, rule, lr, decay, eps, gamma, 
 # ----------------------------------------------------------------------------
 # Measurement hook (include/dqn_profile.h)
 
-K_GATHER, K_CONV1_FWD, K_CONV2_FWD, K_CONV3_FWD, K_FC1_FWD, K_HEAD, K_FC1_WGRAD, K_FC1_DGRAD, \
-    K_CONV1_WGRAD, K_CONV2_WGRAD, K_CONV3_WGRAD, K_CONV2_DGRAD, K_CONV3_DGRAD, K_FINALIZE, \
-    K_APPLY = range(15)
 KERNEL_NAMES = ["gather", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head", "fc1_wgrad",
                 "fc1_dgrad", "conv1_wgrad", "conv2_wgrad", "conv3_wgrad", "conv2_dgrad",
-                "conv3_dgrad", "finalize", "apply"]
+                "conv3_dgrad", "finalize", "apply", "fc1_bwd", "conv2_bwd", "conv3_bwd"]
 _ATTACHED = {}
 
 

@@ -296,10 +296,7 @@ def test_td_gradient_replay_equals_gather_then_td(dev, replay, name, B, target):
     import torch
     hr, rp = replay
     net, shape = NETS[name]
-    if net.n_actions != 6:
-        # the fixture replay stores actions for 6 actions; re-wrap its side
-        # arrays with actions reduced modulo the large net's 18 (all valid)
-        rp = dq.Replay(rp.frames, rp.action, rp.reward, rp.terminal, rp.size)
+    # the fixture's actions lie in 0..5, valid for both networks
     th = dev_tensor(di.xavier_theta(shape, 110 + B, bias_scale=0.05))
     tt = th if target == "same" else dev_tensor(di.xavier_theta(shape, 111 + B, bias_scale=0.05))
     idx = dev_tensor(np.random.default_rng(B).integers(0, rp.size - 1, B).astype(np.int64))
