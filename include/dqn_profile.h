@@ -4,12 +4,14 @@
  * Lets a benchmark time one internal kernel of the hot path with HIP events
  * recorded on the stream that kernel runs on.  Not needed for normal use.
  *
- * dqn_profile_attach(kernel, events, n_pairs): from now on, each launch of
- * `kernel` is bracketed by hipEventRecord(events[2*i]) before and
+ * dqn_profile_attach(kernel, events, n_pairs, stride): from now on, every
+ * stride-th launch of `kernel` (launches 0, stride, 2*stride, ... counted
+ * from the attach) is bracketed by hipEventRecord(events[2*i]) before and
  * hipEventRecord(events[2*i+1]) after, for i = 0, 1, ... up to n_pairs - 1;
  * later launches are not bracketed.  `events` is a host array of hipEvent_t
  * created by the caller; it must stay valid while attached.  Pass
- * events = NULL (or n_pairs = 0) to detach.  Returns DQN_OK or DQN_EINVAL.
+ * events = NULL (or n_pairs = 0) to detach.  stride >= 1.  Returns DQN_OK or
+ * DQN_EINVAL.
  * dqn_profile_used(kernel): number of pairs recorded since the last attach.
  *
  * The hook is process-wide state: attach/detach must not race with calls of
@@ -43,10 +45,11 @@ typedef enum {
     DQN_K_FC1_BWD = 15,     /* fc1 weight + input gradient in one launch (small batch) */
     DQN_K_CONV2_BWD = 16,   /* conv2 weight + input gradient in one launch (small batch) */
     DQN_K_CONV3_BWD = 17,   /* conv3 weight + input gradient in one launch (small batch) */
-    DQN_K_COUNT = 18
+    DQN_K_FINALIZE_APPLY = 18, /* finalize with the update applied (dqn_train_steps) */
+    DQN_K_COUNT = 19
 } dqn_kernel;
 
-int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs);
+int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs, int32_t stride);
 int32_t dqn_profile_used(int32_t kernel);
 
 #ifdef __cplusplus

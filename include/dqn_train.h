@@ -47,6 +47,9 @@ int64_t dqn_train_workspace_bytes(const dqn_net* net, int32_t batch, int32_t rep
  *   dqn_td_gradient_replay(theta, theta_target or, when target_period == 0,
  *   theta itself, minibatch idx + n*batch); ps_apply_update(rule, theta in
  *   place).
+ * The update is applied by the last kernel of each step rather than by a
+ * separate pass; theta, opt_state and the losses are bit-identical to those
+ * of the two calls above.
  * idx: device int64 [n_steps][batch] (transition indices, as replay_gather).
  * theta_target: device float [p]; may be NULL when target_period == 0.
  * opt_state: device float [p] (RMSProp r or AdaGrad G); NULL for PS_SGD.

@@ -75,20 +75,9 @@ inline int64_t act_elems(const ConvDims& c) { return (int64_t)c.cout * c.oh * c.
 
 // Largest batch whose backward kernels are launched in pairs (above it each
 // kernel alone fills the chip and keeps its own occupancy).
-constexpr int kPairMaxBatch = 256;
+constexpr int kPairMaxBatch = 64;
 
 // fc1 forward split-K: enough slices that the launch covers the chip.
-void fc1_split(int rows, int H, int K, int* ks, int* kchunk) {
-    // Few enough slices that the head's reduction stays short.
-    const int tiles = ((rows + 63) / 64) * ((H + 63) / 64);
-    int want = std::max(1, 128 / tiles);
-    want = std::min(want, 16);
-    int kc = (K + want - 1) / want;
-    kc = (kc + 31) / 32 * 32;  // whole k-steps of the GEMM kernel
-    *kchunk = kc;
-    *ks = (K + kc - 1) / kc;
-}
-
 struct Carver {
     size_t off = 0;
     template <class T>
@@ -119,7 +108,7 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
     Carver cv;
     const int n2 = 2 * B;
     for (int l = 0; l < ni.n_conv; ++l) t.act[l] = cv.take<float>(ws, (int64_t)n2 * act_elems(ni.d[l]));
-    fc1_split(n2, ni.H, ni.flat, &t.ks, &t.kchunk);
+    gemm_fwd_split(n2, ni.H, ni.flat, &t.ks, &t.kchunk);
     t.fc1p = cv.take<float>(ws, (int64_t)t.ks * n2 * ni.H);
     t.h1s = cv.take<float>(ws, (int64_t)B * ni.H);
     t.dz1 = cv.take<float>(ws, (int64_t)B * ni.H);
@@ -150,7 +139,7 @@ FwdLayout fwd_layout(const NetInfo& ni, int B, void* ws) {
     FwdLayout f{};
     Carver cv;
     for (int l = 0; l < ni.n_conv; ++l) f.act[l] = cv.take<float>(ws, (int64_t)B * act_elems(ni.d[l]));
-    fc1_split(B, ni.H, ni.flat, &f.ks, &f.kchunk);
+    gemm_fwd_split(B, ni.H, ni.flat, &f.ks, &f.kchunk);
     f.fc1p = cv.take<float>(ws, (int64_t)f.ks * B * ni.H);
     f.bytes = cv.off;
     return f;
@@ -170,18 +159,26 @@ struct ProfSlot {
     hipEvent_t* ev = nullptr;
     int n = 0;
     int used = 0;
+    int stride = 1;
+    int64_t seen = 0;  // launches since the attach
+    bool open = false;
 };
 ProfSlot g_prof[DQN_K_COUNT];
 
 inline void prof_begin(int k, hipStream_t st) {
     ProfSlot& p = g_prof[k];
-    if (p.ev && p.used < p.n) (void)hipEventRecord(p.ev[2 * p.used], st);
+    if (p.ev && p.used < p.n && p.seen % p.stride == 0) {
+        (void)hipEventRecord(p.ev[2 * p.used], st);
+        p.open = true;
+    }
+    ++p.seen;
 }
 inline void prof_end(int k, hipStream_t st) {
     ProfSlot& p = g_prof[k];
-    if (p.ev && p.used < p.n) {
+    if (p.open) {
         (void)hipEventRecord(p.ev[2 * p.used + 1], st);
         ++p.used;
+        p.open = false;
     }
 }
 
@@ -208,7 +205,8 @@ struct TdSource {
 int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
                             const float* theta_target, const TdSource& src, int32_t batch,
                             float gamma, float* grad_out, float* loss_out, float* q_out,
-                            float* y_out, void* ws, size_t ws_bytes, hipStream_t st) {
+                            float* y_out, void* ws, size_t ws_bytes, hipStream_t st,
+                            const PsUpdate* upd = nullptr) {
     if (!theta || !grad_out || !loss_out || !ws) return DQN_EINVAL;
     if (batch <= 0 || !std::isfinite(gamma)) return DQN_EINVAL;
     const float* tt = theta_target ? theta_target : theta;
@@ -348,7 +346,13 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     fa.g_W2 = grad_out + ni.w_off[L + 1];
     fa.g_b2 = grad_out + ni.b_off[L + 1];
     fa.loss_out = loss_out;
-    RUN(DQN_K_FINALIZE, launch_finalize(fa, st));
+    fa.grad_base = grad_out;
+    fa.fc1w_off = ni.w_off[L];
+    fa.fc1w_count = (int64_t)ni.H * ni.flat;
+    if (upd)
+        RUN(DQN_K_FINALIZE_APPLY, launch_finalize(fa, upd, st));
+    else
+        RUN(DQN_K_FINALIZE, launch_finalize(fa, nullptr, st));
     return DQN_OK;
 }
 
@@ -363,6 +367,33 @@ int check_replay(const dqn_replay* rp, bool with_next) {
 }
 
 }  // namespace
+
+
+namespace dqn {
+
+int td_step_replay(const dqn_net* net, const float* theta_target, const dqn_replay* replay,
+                   const int64_t* idx, int32_t batch, float gamma, float* grad_ws, float* loss_out,
+                   const PsUpdate& upd, void* ws, size_t ws_bytes, hipStream_t st) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    rc = check_replay(replay, true);
+    if (rc != DQN_OK) return rc;
+    if (!idx || !replay->action || !replay->reward || !replay->terminal) return DQN_EINVAL;
+    if (replay->c != net->in_c || replay->h != net->in_h || replay->w != net->in_w) return DQN_EINVAL;
+    if (upd.rule != PS_SGD && upd.rule != PS_RMSPROP && upd.rule != PS_ADAGRAD) return DQN_EINVAL;
+    if (!upd.theta || (upd.rule != PS_SGD && !upd.state)) return DQN_EINVAL;
+    if (upd.state && !aligned(upd.state, 16)) return DQN_EINVAL;
+    if (!std::isfinite(upd.lr) || !std::isfinite(upd.decay) || !std::isfinite(upd.eps)) return DQN_EINVAL;
+    const size_t pb = (size_t)ni.P * sizeof(float);
+    if (upd.state && (overlaps(upd.state, pb, upd.theta, pb) || (grad_ws && overlaps(upd.state, pb, grad_ws, pb))))
+        return DQN_EINVAL;
+    TdSource src{nullptr, nullptr, nullptr, nullptr, nullptr, replay, idx};
+    return td_gradient_impl(net, ni, upd.theta, theta_target, src, batch, gamma, grad_ws, loss_out,
+                            nullptr, nullptr, ws, ws_bytes, st, &upd);
+}
+
+}  // namespace dqn
 
 extern "C" {
 
@@ -513,12 +544,15 @@ int ps_apply_update(int32_t rule, const float* theta_in, float* theta_out, float
     return DQN_OK;
 }
 
-int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs) {
-    if (kernel < 0 || kernel >= DQN_K_COUNT || n_pairs < 0) return DQN_EINVAL;
+int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs, int32_t stride) {
+    if (kernel < 0 || kernel >= DQN_K_COUNT || n_pairs < 0 || stride < 1) return DQN_EINVAL;
     ProfSlot& p = g_prof[kernel];
     p.ev = (events && n_pairs > 0) ? (hipEvent_t*)events : nullptr;
     p.n = p.ev ? n_pairs : 0;
     p.used = 0;
+    p.stride = stride;
+    p.seen = 0;
+    p.open = false;
     return DQN_OK;
 }
 

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "dqn.h"
+
 namespace dqn {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
@@ -14,6 +16,26 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 // D[4*(l/16) + r][l%16] in element r of the accumulator.
 __device__ __forceinline__ f4 mfma16x16x4(float a, float b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Parameter-server update of one parameter theta with gradient g and
+// optimizer state st: RULE 0 gradient descent (Sec. III.B), 1 RMSProp (Alg. 2
+// RMSPROPUPDATE: r <- decay*r + (1-decay)*g^2, theta <- theta - lr*g/sqrt(r),
+// skipped while r == 0), 2 AdaGrad (G <- G + g^2, theta <- theta -
+// lr*g/(sqrt(G) + eps)).  Every kernel that updates parameters calls this, so
+// fused and standalone updates round identically.
+template <int RULE>
+__device__ __forceinline__ void ps_update(float& th, float& st, float g, float lr, float decay,
+                                          float eps) {
+    if constexpr (RULE == 0) {
+        th = fmaf(-lr, g, th);
+    } else if constexpr (RULE == 1) {
+        st = fmaf(decay, st, (1.f - decay) * (g * g));
+        if (st > 0.f) th = th - lr * g / sqrtf(st);
+    } else {
+        st = fmaf(g, g, st);
+        th = th - lr * g / (sqrtf(st) + eps);
+    }
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -68,6 +90,10 @@ struct SideFields {
 
 // ---- launchers (host side); every one returns hipGetLastError() ----------
 
+// Raise a kernel's dynamic LDS limit to `bytes` if it is below (once per
+// kernel and size; thread-safe).  False if the runtime refuses.
+bool allow_lds(const void* kern, size_t bytes);
+
 // Forward convolution + bias + ReLU for n samples.  Samples j < n_a read
 // sample j of in_a and use (w_a, b_a); samples j >= n_a read sample j - n_a
 // of in_b and use (w_b, b_b).  Output float [n][cout][oh][ow].  in_scale
@@ -96,8 +122,13 @@ hipError_t launch_conv_dgrad(ConvId id, const float* dz, const float* w, const f
 // C = A * B over fp32 MFMA tiles.  A(m,k) = ta ? A[k*lda+m] : A[m*lda+k];
 // B(k,n) = tb ? B[n*ldb+k] : B[k*ldb+n].  Split-K: slice z covers
 // k in [z*kchunk, min(K,(z+1)*kchunk)) and writes C + z*c_slice.
-// With mask != NULL: C = acc * [mask[m*ldc+n] > 0].
+// GEMM_NN (the fc1 input gradient) requires mask: C = acc * [mask[m*ldc+n] > 0].
+// kchunk must be a multiple of 32.
 enum GemmKind { GEMM_NT = 0, GEMM_TN = 1, GEMM_NN = 2 };
+
+// k-slicing of the fc1 forward GEMM for `rows` output rows: ks slices of
+// kchunk (a multiple of 64, the last one possibly shorter).
+void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk);
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
                        const float* mask, hipStream_t st);
@@ -144,8 +175,24 @@ struct FinalizeArgs {
     const int32_t* action;
     int B, H, A;
     float *g_b1, *g_W2, *g_b2, *loss_out;
+    // Gradient vector the gw/gb/g_* pointers point into, and the range of it
+    // (the fc1 weights) that an earlier kernel wrote in full.
+    const float* grad_base;
+    int64_t fc1w_off, fc1w_count;
 };
-hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t st);
+
+// A parameter-server update fused into the last kernel of a TD step.
+struct PsUpdate {
+    int rule;        // 0 SGD, 1 RMSProp, 2 AdaGrad (ps_update)
+    float* theta;    // updated in place
+    float* state;    // RMSProp r / AdaGrad G; unused for SGD
+    float lr, decay, eps;
+};
+
+// Reduce the partial sums into the gradient (upd == NULL), or apply the
+// update to every parameter instead of storing the reduced gradient; the fc1
+// weight range is then read from grad_base.  The loss is stored either way.
+hipError_t launch_finalize(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st);
 
 hipError_t launch_gather(const uint8_t* frames, int64_t stride, int64_t rec_bytes,
                          const uint8_t* act, const int8_t* rew, const uint8_t* term,
@@ -156,5 +203,14 @@ hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t st);
 
 hipError_t launch_apply(int rule, const float* th_in, float* th_out, float* state, const float* g,
                         int64_t n, float lr, float decay, float eps, hipStream_t st);
+
+// One sequential training step from replay records: the TD gradient of
+// dqn_td_gradient_replay with the update `upd` applied by its last kernel
+// (theta == upd.theta, updated in place).  grad_ws holds the fc1 weight
+// gradient in between.  Host checks as dqn_td_gradient_replay and
+// ps_apply_update; returns a dqn_status.
+int td_step_replay(const dqn_net* net, const float* theta_target, const dqn_replay* replay,
+                   const int64_t* idx, int32_t batch, float gamma, float* grad_ws, float* loss_out,
+                   const PsUpdate& upd, void* ws, size_t ws_bytes, hipStream_t st);
 
 }  // namespace dqn

@@ -6,8 +6,6 @@
 // lane groups fall in distinct banks) and the input rows it needs (16-byte
 // loads where aligned), then runs its MFMA loop from LDS only.
 // Activations are NCHW float32; the network input is bytes.
-#include <mutex>
-#include <unordered_map>
 
 #include "common.h"
 
@@ -564,20 +562,6 @@ __global__ __launch_bounds__(WG) void conv_bwd_kernel(WgradParams w, DgradParams
 
 // ---------------------------------------------------------------------------
 // Host-side launch shapes.
-
-// Raise a kernel's dynamic LDS limit to the largest size it is launched
-// with (once per kernel and size; thread-safe).
-bool allow_lds(const void* kern, size_t bytes) {
-    static std::mutex mu;
-    static std::unordered_map<const void*, size_t> granted;
-    std::lock_guard<std::mutex> lock(mu);
-    size_t& g = granted[kern];
-    if (bytes <= g) return true;
-    if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) != hipSuccess)
-        return false;
-    g = bytes;
-    return true;
-}
 
 template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int CO>
 hipError_t fwd_launch(const ConvIn& in_a, const ConvIn& in_b, int n_a, int n, const float* w_a,

@@ -5,6 +5,8 @@
 // global round trips are needed) staged through LDS, with the next step's
 // global loads issued before the current step's MFMAs; four waves in a 2x2
 // arrangement.
+#include <algorithm>
+
 #include "common.h"
 
 namespace dqn {
@@ -25,8 +27,27 @@ struct GemmParams {
 // TA: A(m,k) = A[k*lda + m] else A[m*lda + k].
 // TB: B(k,n) = B[n*ldb + k] else B[k*ldb + n].
 // One BMxBN output tile (bx, by) of k-slice bz.
+//
+// Each operand is staged in LDS in its global orientation, so global loads
+// and LDS stores are both 16-byte vectors with no transposition:
+//   k-contiguous operand (A without TA, B with TB): [mn][BK + 4]
+//   mn-contiguous operand (A with TA, B without TB): [BK][MN + 16]
+// The MFMA loop reads, per lane (li = lane % 16, g = lane / 16), element
+// (mn0 + li, 4*kk + g).  With a row stride of 4 (mod 64) floats in the first
+// layout and 16 (mod 64) in the second, the 64 lanes of one read hit 64
+// distinct banks.
+template <int BM, int BN, int BK, bool TA, bool TB>
+struct GemmSmem {
+    static constexpr int RA = TA ? BM + 16 : BK + 4;   // row stride of A's stage
+    static constexpr int RB = TB ? BK + 4 : BN + 16;
+    static constexpr int NA = TA ? BK * RA : BM * RA;  // floats
+    static constexpr int NB = TB ? BN * RB : BK * RB;
+    static constexpr size_t bytes = (size_t)(NA + NB) * 4;
+};
+
 template <int BM, int BN, int BK, bool TA, bool TB, bool MASK>
 __device__ __forceinline__ void gemm_body(const GemmParams& p, int bx, int by, int bz, float* smem) {
+    using SM = GemmSmem<BM, BN, BK, TA, TB>;
     const int M = p.M, N = p.N, K = p.K, lda = p.lda, ldb = p.ldb, ldc = p.ldc, kchunk = p.kchunk;
     const float* __restrict__ A = p.A;
     const float* __restrict__ Bm = p.B;
@@ -34,11 +55,11 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, int bx, int by, i
     const float* __restrict__ mask = p.mask;
     const int64_t c_slice = p.c_slice;
     constexpr int TM = BM / 32, TN = BN / 32;     // MFMA tiles per wave
-    constexpr int LDA = BM + 4, LDB = BN + 4;
-    constexpr int AV = BM * BK / 4 / 256;         // float4 loads per thread per k-step
+    constexpr int AV = BM * BK / 4 / 256;         // float4 loads per thread per stage
     constexpr int BV = BN * BK / 4 / 256;
-    float (*As)[LDA] = (float (*)[LDA])smem;              // [BK][LDA]
-    float (*Bs)[LDB] = (float (*)[LDB])(smem + BK * LDA); // [BK][LDB]
+    static_assert(AV >= 1 && BV >= 1, "tile too small for 256 threads");
+    float* As = smem;
+    float* Bs = smem + SM::NA;
     const int m0 = bx * BM;
     const int n0 = by * BN;
     const int z = bz;
@@ -84,11 +105,10 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, int bx, int by, i
             const int e = t + 256 * v;
             if constexpr (!TA) {
                 const int row = e / (BK / 4), kq = (e % (BK / 4)) * 4;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) As[kq + q][row] = ra[v][q];
+                *(f4*)&As[row * SM::RA + kq] = ra[v];
             } else {
                 const int kr = e / (BM / 4), mq = (e % (BM / 4)) * 4;
-                *(f4*)&As[kr][mq] = ra[v];
+                *(f4*)&As[kr * SM::RA + mq] = ra[v];
             }
         }
 #pragma unroll
@@ -96,14 +116,16 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, int bx, int by, i
             const int e = t + 256 * v;
             if constexpr (!TB) {
                 const int kr = e / (BN / 4), nq = (e % (BN / 4)) * 4;
-                *(f4*)&Bs[kr][nq] = rb[v];
+                *(f4*)&Bs[kr * SM::RB + nq] = rb[v];
             } else {
                 const int col = e / (BK / 4), kq = (e % (BK / 4)) * 4;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) Bs[kq + q][col] = rb[v][q];
+                *(f4*)&Bs[col * SM::RB + kq] = rb[v];
             }
         }
     };
+    // Element (mn, k) of each stage.
+    auto a_at = [&](int m, int k) { return TA ? As[k * SM::RA + m] : As[m * SM::RA + k]; };
+    auto b_at = [&](int k, int n) { return TB ? Bs[n * SM::RB + k] : Bs[k * SM::RB + n]; };
 
     f4 acc[TM][TN];
 #pragma unroll
@@ -120,9 +142,9 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, int bx, int by, i
         for (int kk = 0; kk < BK / 4; ++kk) {
             float a[TM], b[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = As[kk * 4 + g][wm + i * 16 + li];
+            for (int i = 0; i < TM; ++i) a[i] = a_at(wm + i * 16 + li, kk * 4 + g);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) b[j] = Bs[kk * 4 + g][wn + j * 16 + li];
+            for (int j = 0; j < TN; ++j) b[j] = b_at(kk * 4 + g, wn + j * 16 + li);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -173,77 +195,69 @@ __global__ __launch_bounds__(256) void gemm_pair_kernel(GemmParams p1, int g1x, 
 
 template <int BM, int BN, int BK, bool TA, bool TB, bool MASK>
 hipError_t launch_tile(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
-                 int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
-                 hipStream_t st) {
-    constexpr size_t lds = (size_t)BK * ((BM + 4) + (BN + 4)) * 4;
+                       int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
+                       hipStream_t st) {
+    if (kchunk % BK != 0) return hipErrorInvalidValue;
+    constexpr size_t lds = GemmSmem<BM, BN, BK, TA, TB>::bytes;
     auto kern = gemm_kernel<BM, BN, BK, TA, TB, MASK>;
-    static bool granted = false;
-    if (!granted) {
-        if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-            hipSuccess)
-            return hipErrorInvalidValue;
-        granted = true;
-    }
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((N + BN - 1) / BN), (unsigned)kslices);
     const GemmParams p{M, N, K, A, lda, B, ldb, C, ldc, kchunk, c_slice, mask};
     hipLaunchKernelGGL(kern, grid, dim3(256), lds, st, p);
     return hipGetLastError();
 }
 
-template <int BK, bool TA, bool TB, bool MASK>
-hipError_t launch_bk(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
-               int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask, hipStream_t st) {
-    // Narrow tiles when the output is small, so more workgroups run.
-    const bool small_m = M <= 32;
-    const long tiles64 = (long)((M + 63) / 64) * ((N + 63) / 64) * kslices;
-    const bool small_n = tiles64 < 128 && N > 32;
-    if (small_m && small_n)
-        return launch_tile<32, 32, BK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
-    else if (small_m)
-        return launch_tile<32, 64, BK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
-    else if (small_n)
-        return launch_tile<64, 32, BK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
-    else
-        return launch_tile<64, 64, BK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
-}
-
-template <bool TA, bool TB, bool MASK>
-hipError_t launch_shape(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
-                  int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
-                  hipStream_t st) {
-    if (kchunk >= 128)
-        return launch_bk<128, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
-    else
-        return launch_bk<32, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
-}
-
-// Tile configuration the single launches pick for a shape.
+// Tile shapes, from a sweep of dependent back-to-back launches over the fc
+// shapes of both networks (batch 32 to 4096):
+//   forward (NT, split-K): 32x32 up to 64 rows, 64x32 up to 1023 rows, 64x64
+//     beyond; k-stages of 64 when the slices are long (kchunk >= 256);
+//   weight gradient (TN): 32x32, k-stages of 32;
+//   input gradient (NN, masked): 32x32, k-stages of 64 up to 64 rows.
 struct TileCfg {
     int bm, bn, bk;
 };
 
-TileCfg pick_tile(int M, int N, int kslices, int kchunk) {
-    const bool small_m = M <= 32;
-    const long tiles64 = (long)((M + 63) / 64) * ((N + 63) / 64) * kslices;
-    const bool small_n = tiles64 < 128 && N > 32;
-    return TileCfg{small_m ? 32 : 64, small_n ? 32 : 64, kchunk >= 128 ? 128 : 32};
+TileCfg fwd_tile(int M, int kchunk) {
+    return TileCfg{M <= 64 ? 32 : 64, M >= 1024 ? 64 : 32, (kchunk >= 256 && kchunk % 64 == 0) ? 64 : 32};
 }
 
-template <int BM1, int BN1, int BK1, int BM2, int BN2, int BK2>
-hipError_t pair_tn_nnmask(const GemmParams& w, const GemmParams& d, hipStream_t st) {
-    auto kern = gemm_pair_kernel<BM1, BN1, BK1, true, false, false, BM2, BN2, BK2, false, false, true>;
-    constexpr size_t l1 = (size_t)BK1 * ((BM1 + 4) + (BN1 + 4)) * 4;
-    constexpr size_t l2 = (size_t)BK2 * ((BM2 + 4) + (BN2 + 4)) * 4;
-    constexpr size_t lds = l1 > l2 ? l1 : l2;
-    static bool granted = false;
-    if (!granted) {
-        if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-            hipSuccess)
-            return hipErrorInvalidValue;
-        granted = true;
+TileCfg dgrad_tile(int M, int kchunk) { return TileCfg{32, 32, (M <= 64 && kchunk % 64 == 0) ? 64 : 32}; }
+
+template <bool TA, bool TB, bool MASK>
+hipError_t launch_cfg(TileCfg c, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
+                      float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
+                      hipStream_t st) {
+#define DQN_TILE(TBM, TBN, TBK)                                                                     \
+    if (c.bm == TBM && c.bn == TBN && c.bk == TBK)                                                  \
+        return launch_tile<TBM, TBN, TBK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices,     \
+                                                        kchunk, c_slice, mask, st);
+    if constexpr (!TA && TB) {  // forward
+        DQN_TILE(32, 32, 32)
+        DQN_TILE(32, 32, 64)
+        DQN_TILE(64, 32, 32)
+        DQN_TILE(64, 32, 64)
+        DQN_TILE(64, 64, 32)
+        DQN_TILE(64, 64, 64)
+    } else if constexpr (TA && !TB) {  // weight gradient
+        DQN_TILE(32, 32, 32)
+    } else {  // input gradient
+        DQN_TILE(32, 32, 32)
+        DQN_TILE(32, 32, 64)
     }
-    const int g1x = (w.M + BM1 - 1) / BM1, g1y = (w.N + BN1 - 1) / BN1;
-    const int g2x = (d.M + BM2 - 1) / BM2, g2y = (d.N + BN2 - 1) / BN2;
+#undef DQN_TILE
+    return hipErrorInvalidValue;
+}
+
+template <int BK2>
+hipError_t pair_tn_nnmask(const GemmParams& w, const GemmParams& d, hipStream_t st) {
+    constexpr int BM = 32, BN = 32, BK1 = 32;
+    auto kern = gemm_pair_kernel<BM, BN, BK1, true, false, false, BM, BN, BK2, false, false, true>;
+    constexpr size_t l1 = GemmSmem<BM, BN, BK1, true, false>::bytes;
+    constexpr size_t l2 = GemmSmem<BM, BN, BK2, false, false>::bytes;
+    constexpr size_t lds = l1 > l2 ? l1 : l2;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+    const int g1x = (w.M + BM - 1) / BM, g1y = (w.N + BN - 1) / BN;
+    const int g2x = (d.M + BM - 1) / BM, g2y = (d.N + BN - 1) / BN;
     const int n1 = g1x * g1y, n2 = g2x * g2y;
     hipLaunchKernelGGL(kern, dim3((unsigned)(n1 + n2)), dim3(256), lds, st, w, g1x, g1y, d, g2x, g2y, n1);
     return hipGetLastError();
@@ -251,24 +265,28 @@ hipError_t pair_tn_nnmask(const GemmParams& w, const GemmParams& d, hipStream_t 
 
 }  // namespace
 
+void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk) {
+    // Enough k-slices that the launch has several hundred workgroups; the
+    // head kernel sums the slices.  Past 256 output tiles the launch fills
+    // the chip without splitting, and every slice would cost the head a
+    // read of rows x N partial sums.
+    const TileCfg c = fwd_tile(rows, 64);
+    const long tiles = (long)((rows + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn);
+    const int whole = (K + 63) / 64 * 64;
+    const int kc = std::min(tiles <= 32 ? 64 : tiles <= 256 ? 256 : whole, whole);
+    *kchunk = kc;
+    *ks = (K + kc - 1) / kc;
+}
+
 // The fc1 weight gradient (TN, one k-slice) and the masked fc1 input gradient
-// (NN, one k-slice) in one launch when their tile configurations are one of
-// the instantiated pairs; otherwise two launches.
+// (NN, one k-slice) in one launch.
 hipError_t launch_gemm_wgrad_dgrad(int H, int F, int B, const float* dz1, const float* x,
                                    float* dW, const float* W, float* dx, hipStream_t st) {
     const int kw = (B + 31) / 32 * 32, kd = (H + 31) / 32 * 32;
     const GemmParams w{H, F, B, dz1, H, x, F, dW, F, kw, 0, nullptr};
     const GemmParams d{B, F, H, dz1, H, W, F, dx, F, kd, 0, x};
-    const TileCfg cw = pick_tile(H, F, 1, kw), cd = pick_tile(B, F, 1, kd);
-    if (cw.bm == 64 && cw.bn == 64 && cd.bk == 128) {
-        if (cw.bk == 32 && cd.bm == 32 && cd.bn == 32) return pair_tn_nnmask<64, 64, 32, 32, 32, 128>(w, d, st);
-        if (cw.bk == 32 && cd.bm == 64 && cd.bn == 32) return pair_tn_nnmask<64, 64, 32, 64, 32, 128>(w, d, st);
-        if (cw.bk == 128 && cd.bm == 64 && cd.bn == 32) return pair_tn_nnmask<64, 64, 128, 64, 32, 128>(w, d, st);
-        if (cw.bk == 128 && cd.bm == 64 && cd.bn == 64) return pair_tn_nnmask<64, 64, 128, 64, 64, 128>(w, d, st);
-    }
-    hipError_t e = launch_gemm(GEMM_TN, H, F, B, dz1, H, x, F, dW, F, 1, kw, 0, nullptr, st);
-    if (e != hipSuccess) return e;
-    return launch_gemm(GEMM_NN, B, F, H, dz1, H, W, F, dx, F, 1, kd, 0, x, st);
+    if (dgrad_tile(B, kd).bk == 64) return pair_tn_nnmask<64>(w, d, st);
+    return pair_tn_nnmask<32>(w, d, st);
 }
 
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
@@ -277,14 +295,15 @@ hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int l
     if (kchunk % 32 != 0) return hipErrorInvalidValue;
     switch (kind) {
         case GEMM_NT:
-            return launch_shape<false, true, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
+            return launch_cfg<false, true, false>(fwd_tile(M, kchunk), M, N, K, A, lda, B, ldb, C, ldc,
+                                                  kslices, kchunk, c_slice, nullptr, st);
         case GEMM_TN:
-            return launch_shape<true, false, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
+            return launch_cfg<true, false, false>(TileCfg{32, 32, 32}, M, N, K, A, lda, B, ldb, C, ldc,
+                                                  kslices, kchunk, c_slice, nullptr, st);
         case GEMM_NN:
-            if (mask)
-                return launch_shape<false, false, true>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
-            else
-                return launch_shape<false, false, false>(M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, nullptr, st);
+            if (!mask) return hipErrorInvalidValue;
+            return launch_cfg<false, false, true>(dgrad_tile(M, kchunk), M, N, K, A, lda, B, ldb, C,
+                                                  ldc, kslices, kchunk, c_slice, mask, st);
         default:
             return hipErrorInvalidValue;
     }

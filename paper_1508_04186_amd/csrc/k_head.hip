@@ -1,7 +1,6 @@
 // Output head of the Q-network and the TD step of Alg. 1, one workgroup per
-// sample: reduce the fc1 split-K partials (one hidden unit per thread), add
-// the bias and apply ReLU, run the linear output layer with a block
-// reduction, then either
+// sample: reduce the fc1 split-K partials, add the bias and apply ReLU, run
+// the linear output layer with a block reduction, then either
 //   (td)  form y = r (terminal) or r + gamma * max_a' Q(s', a'; theta^-),
 //         the residual delta = (Q(s, a) - y) / B, the per-sample loss term
 //         and the fc1 pre-activation gradient delta * W2[a, :] * [z1 > 0];
@@ -16,23 +15,9 @@ namespace {
 
 constexpr int HT = 256;  // threads per head workgroup
 
-// Sum of n strided values in a fixed association (element u of each group
-// of 16 goes to partial sum u % 4; missing tail elements count as +0), with
-// 16 independent loads in flight.
-__device__ __forceinline__ float sum_strided(const float* __restrict__ x, int n, int64_t stride) {
-    float s[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < n; c += 16) {
-        float v[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = (c + u < n) ? x[(int64_t)(c + u) * stride] : 0.f;
-#pragma unroll
-        for (int u = 0; u < 16; ++u) s[u & 3] += v[u];
-    }
-    return (s[0] + s[1]) + (s[2] + s[3]);
-}
-
-// The same sum split over the 8 lanes of an aligned lane group: lane q of the
-// group takes terms c = 16*(8*i + q) + u, and the group combines its lanes'
+// Sum of n strided values split over the 8 lanes of an aligned lane group:
+// lane q of the group takes terms c = 16*(8*i + q) + u into partial sum
+// u % 4 (missing tail terms count as +0), and the group combines its lanes'
 // sums in a fixed butterfly order.  Every lane of the group gets the result.
 __device__ __forceinline__ float sum_strided_x8(const float* __restrict__ x, int n, int64_t stride) {
     const int q = threadIdx.x & 7;
@@ -66,9 +51,57 @@ __device__ __forceinline__ void block_sums(float (&v)[NV], float* red /* [4][NV]
     for (int k = 0; k < NV; ++k) v[k] = (red[k] + red[NV + k]) + (red[2 * NV + k] + red[3 * NV + k]);
 }
 
+// Sum of the ks split-K slices of NR rows of the fc1 partial sums
+// (row r at fc1p + rows[r]*H, slice z at + z*slice).  Thread t adds, for the
+// four hidden units 4q..4q+3 (q = t mod H/4), the slices congruent to
+// t / (H/4) modulo G = 1024/H in increasing order, with up to 12 slices per
+// row in flight; the G group sums are then added in group order through LDS.
+// Thread t receives hidden units t + 256e in out[r][e].
+template <int H, int NR>
+__device__ __forceinline__ void reduce_slices(const float* __restrict__ fc1p, const int64_t (&rows)[NR],
+                                              int ks, int64_t slice, float* red /* [NR][G][H] */,
+                                              float (&out)[NR][H / HT]) {
+    constexpr int Q = H / 4, G = HT / Q, U = 12;
+    static_assert(HT % Q == 0, "hidden width must divide 1024");
+    const int q = threadIdx.x % Q, sg = threadIdx.x / Q;
+    f4 acc[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) acc[r] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int z0 = sg; z0 < ks; z0 += U * G) {
+        f4 v[NR][U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int z = z0 + u * G;
+#pragma unroll
+            for (int r = 0; r < NR; ++r)
+                v[r][u] = z < ks ? *(const f4*)(fc1p + (int64_t)z * slice + rows[r] * H + 4 * q)
+                                 : f4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int r = 0; r < NR; ++r) acc[r] += v[r][u];
+    }
+#pragma unroll
+    for (int r = 0; r < NR; ++r) *(f4*)&red[(r * G + sg) * H + 4 * q] = acc[r];
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < H / HT; ++e) {
+        const int h = threadIdx.x + HT * e;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            float x = red[(r * G) * H + h];
+#pragma unroll
+            for (int k = 1; k < G; ++k) x += red[(r * G + k) * H + h];
+            out[r][e] = x;
+        }
+    }
+}
+
 template <int H, int A>
 __global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
     constexpr int E = H / HT;
+    __shared__ __align__(16) float sred[2 * 1024];
     __shared__ float red[4 * 2 * A];
     const int j = blockIdx.x;
     const int B = p.B;
@@ -76,11 +109,14 @@ __global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
     float zs[E], hs[E], v[2 * A];
 #pragma unroll
     for (int k = 0; k < 2 * A; ++k) v[k] = 0.f;
+    float sums[2][E];
+    const int64_t rows[2] = {j, B + j};
+    reduce_slices<H, 2>(p.fc1p, rows, p.ks, slice, sred, sums);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
         const int h = threadIdx.x + HT * e;
-        const float a = sum_strided(p.fc1p + (int64_t)j * H + h, p.ks, slice);
-        const float b = sum_strided(p.fc1p + (int64_t)(B + j) * H + h, p.ks, slice);
+        const float a = sums[0][e];
+        const float b = sums[1][e];
         zs[e] = a + p.b1[h];
         hs[e] = fmaxf(zs[e], 0.f);
         const float hn = fmaxf(b + p.b1t[h], 0.f);
@@ -125,16 +161,20 @@ __global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
 template <int H, int A>
 __global__ __launch_bounds__(HT) void head_fwd_kernel(HeadFwdArgs p) {
     constexpr int E = H / HT;
+    __shared__ __align__(16) float sred[1024];
     __shared__ float red[4 * A];
     const int j = blockIdx.x;
     const int64_t slice = (int64_t)p.B * H;
     float v[A];
 #pragma unroll
     for (int k = 0; k < A; ++k) v[k] = 0.f;
+    float sums[1][E];
+    const int64_t rows[1] = {j};
+    reduce_slices<H, 1>(p.fc1p, rows, p.ks, slice, sred, sums);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
         const int h = threadIdx.x + HT * e;
-        const float hs = fmaxf(sum_strided(p.fc1p + (int64_t)j * H + h, p.ks, slice) + p.b1[h], 0.f);
+        const float hs = fmaxf(sums[0][e] + p.b1[h], 0.f);
 #pragma unroll
         for (int k = 0; k < A; ++k) v[k] = fmaf(p.W2[k * H + h], hs, v[k]);
     }
@@ -167,26 +207,69 @@ __global__ __launch_bounds__(HT) void head_fwd_kernel(HeadFwdArgs p) {
 // association.  Segments: conv weight and bias gradients (partial sums over
 // wgrad chunks), fc1 bias (over samples), fc2 weight and bias (over the
 // samples that took each action), and the loss.
-__global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
+//
+// MODE < 0 stores the gradient; MODE = 0, 1, 2 applies update rule MODE to
+// each parameter instead (fused parameter-server update), and the blocks
+// from n_fin on update the fc1 weights from the gradient stored there.
+template <int MODE>
+__device__ __forceinline__ void emit(const FinalizeArgs& a, const PsUpdate& u, float* dst, float v) {
+    if constexpr (MODE < 0) {
+        *dst = v;
+    } else {
+        const int64_t off = dst - a.grad_base;
+        float th = u.theta[off], sv = MODE != 0 ? u.state[off] : 0.f;
+        ps_update<MODE>(th, sv, v, u.lr, u.decay, u.eps);
+        u.theta[off] = th;
+        if constexpr (MODE != 0) u.state[off] = sv;
+    }
+}
+
+template <int MODE>
+__device__ __forceinline__ void apply_fc1w(const FinalizeArgs& a, const PsUpdate& u, int64_t i4) {
+    if (i4 >= a.fc1w_count / 4) return;
+    const int64_t off = a.fc1w_off + 4 * i4;
+    f4 th = *(const f4*)(u.theta + off);
+    const f4 gv = *(const f4*)(a.grad_base + off);
+    f4 sv = f4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (MODE != 0) sv = *(const f4*)(u.state + off);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        float t = th[r], s = sv[r];
+        ps_update<MODE>(t, s, gv[r], u.lr, u.decay, u.eps);
+        th[r] = t;
+        sv[r] = s;
+    }
+    *(f4*)(u.theta + off) = th;
+    if constexpr (MODE != 0) *(f4*)(u.state + off) = sv;
+}
+
+template <int MODE>
+__global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a, PsUpdate u, int n_fin) {
+    if constexpr (MODE >= 0) {
+        if ((int)blockIdx.x >= n_fin) {
+            apply_fc1w<MODE>(a, u, (int64_t)(blockIdx.x - n_fin) * 256 + threadIdx.x);
+            return;
+        }
+    }
     int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3;
     const bool lead = (threadIdx.x & 7) == 0;
     for (int l = 0; l < a.n_conv; ++l) {
         if (i < a.wcount[l]) {
             const float v = sum_strided_x8(a.wpart[l] + i, a.chunks[l], a.wcount[l]);
-            if (lead) a.gw[l][i] = v;
+            if (lead) emit<MODE>(a, u, a.gw[l] + i, v);
             return;
         }
         i -= a.wcount[l];
         if (i < a.cout[l]) {
             const float v = sum_strided_x8(a.bpart[l] + i, a.chunks[l], a.cout[l]);
-            if (lead) a.gb[l][i] = v;
+            if (lead) emit<MODE>(a, u, a.gb[l] + i, v);
             return;
         }
         i -= a.cout[l];
     }
     if (i < a.H) {
         const float v = sum_strided_x8(a.dz1 + i, a.B, a.H);
-        if (lead) a.g_b1[i] = v;
+        if (lead) emit<MODE>(a, u, a.g_b1 + i, v);
         return;
     }
     i -= a.H;
@@ -205,7 +288,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
         t += __shfl_xor(t, 1, 64);
         t += __shfl_xor(t, 2, 64);
         t += __shfl_xor(t, 4, 64);
-        if (lead) a.g_W2[i] = t;
+        if (lead) emit<MODE>(a, u, a.g_W2 + i, t);
         return;
     }
     i -= (int64_t)a.A * a.H;
@@ -216,7 +299,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a) {
         s += __shfl_xor(s, 1, 64);
         s += __shfl_xor(s, 2, 64);
         s += __shfl_xor(s, 4, 64);
-        if (lead) a.g_b2[i] = s;
+        if (lead) emit<MODE>(a, u, a.g_b2 + i, s);
         return;
     }
     i -= a.A;
@@ -252,10 +335,23 @@ hipError_t launch_head_fwd(int H, int A, const HeadFwdArgs& a, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_finalize(const FinalizeArgs& a, hipStream_t st) {
+hipError_t launch_finalize(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
     int64_t total = a.H + (int64_t)a.A * a.H + a.A + 1;
     for (int l = 0; l < a.n_conv; ++l) total += a.wcount[l] + a.cout[l];
-    hipLaunchKernelGGL(finalize_kernel, dim3((unsigned)((total * 8 + 255) / 256)), dim3(256), 0, st, a);
+    const int n_fin = (int)((total * 8 + 255) / 256);
+    if (!upd) {
+        hipLaunchKernelGGL(finalize_kernel<-1>, dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{},
+                           n_fin);
+        return hipGetLastError();
+    }
+    if (a.fc1w_off % 4 != 0 || a.fc1w_count % 4 != 0 || !a.grad_base) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(n_fin + (a.fc1w_count / 4 + 255) / 256));
+    switch (upd->rule) {
+        case 0: hipLaunchKernelGGL(finalize_kernel<0>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 1: hipLaunchKernelGGL(finalize_kernel<1>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 2: hipLaunchKernelGGL(finalize_kernel<2>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

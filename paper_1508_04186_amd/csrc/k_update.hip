@@ -7,20 +7,6 @@ namespace dqn {
 namespace {
 
 template <int RULE>
-__device__ __forceinline__ void update_one(float& th, float& st, float g, float lr, float decay,
-                                           float eps) {
-    if constexpr (RULE == 0) {
-        th = fmaf(-lr, g, th);
-    } else if constexpr (RULE == 1) {
-        st = fmaf(decay, st, (1.f - decay) * (g * g));
-        if (st > 0.f) th = th - lr * g / sqrtf(st);
-    } else {
-        st = fmaf(g, g, st);
-        th = th - lr * g / (sqrtf(st) + eps);
-    }
-}
-
-template <int RULE>
 __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ th_in,
                                                     float* th_out, float* state,
                                                     const float* __restrict__ g, int64_t n,
@@ -35,7 +21,7 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ th
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             float t = th[r], sv = s[r];
-            update_one<RULE>(t, sv, gv[r], lr, decay, eps);
+            ps_update<RULE>(t, sv, gv[r], lr, decay, eps);
             th[r] = t;
             s[r] = sv;
         }
@@ -46,7 +32,7 @@ __global__ __launch_bounds__(256) void apply_kernel(const float* __restrict__ th
     if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
         const int64_t i = n4 * 4 + threadIdx.x;
         float t = th_in[i], sv = RULE != 0 ? state[i] : 0.f;
-        update_one<RULE>(t, sv, g[i], lr, decay, eps);
+        ps_update<RULE>(t, sv, g[i], lr, decay, eps);
         th_out[i] = t;
         if constexpr (RULE != 0) state[i] = sv;
     }

@@ -90,15 +90,16 @@ int dqn_train_steps(const dqn_net* net, float* theta, float* theta_target, float
     }
     const ReplicaWs w = carve(net, batch, (char*)ws);
     hipStream_t st = (hipStream_t)stream;
+    // The update is applied by the step's last kernel (same arithmetic as
+    // ps_apply_update on the stored gradient).
+    const PsUpdate upd{rule, theta, opt_state, lr, decay, eps};
     for (int64_t n = 0; n < n_steps; ++n) {
         const int64_t g = step0 + n;
         if (target_period > 0 && g % target_period == 0)
             if (launch_copy(theta, theta_target, p, st) != hipSuccess) return DQN_EHIP;
-        TRY(dqn_td_gradient_replay(net, theta, target_period > 0 ? theta_target : theta, replay,
-                                   idx + n * batch, batch, gamma, w.grad,
-                                   losses_out ? losses_out + n : w.loss, nullptr, nullptr, w.td_ws,
-                                   w.td_bytes, stream));
-        TRY(ps_apply_update(rule, theta, theta, opt_state, w.grad, p, lr, decay, eps, stream));
+        TRY(td_step_replay(net, target_period > 0 ? theta_target : theta, replay, idx + n * batch,
+                           batch, gamma, w.grad, losses_out ? losses_out + n : w.loss, upd, w.td_ws,
+                           w.td_bytes, st));
     }
     return DQN_OK;
 }

@@ -124,7 +124,7 @@ def lib():
                                          ctypes.c_int32, ctypes.c_int64, ctypes.c_int32,
                                          ctypes.c_int32, _P, _P, ctypes.c_size_t, _P]
         L.dqn_train_replicas.restype = ctypes.c_int
-        L.dqn_profile_attach.argtypes = [ctypes.c_int32, _P, ctypes.c_int32]
+        L.dqn_profile_attach.argtypes = [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32]
         L.dqn_profile_attach.restype = ctypes.c_int
         L.dqn_profile_used.argtypes = [ctypes.c_int32]
         L.dqn_profile_used.restype = ctypes.c_int32
@@ -435,20 +435,23 @@ def dqn_train_replicas(net, theta_ring, opt_state, rule, lr, decay, eps, gamma, 
 
 KERNEL_NAMES = ["gather", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head", "fc1_wgrad",
                 "fc1_dgrad", "conv1_wgrad", "conv2_wgrad", "conv3_wgrad", "conv2_dgrad",
-                "conv3_dgrad", "finalize", "apply", "fc1_bwd", "conv2_bwd", "conv3_bwd"]
+                "conv3_dgrad", "finalize", "apply", "fc1_bwd", "conv2_bwd", "conv3_bwd",
+                "finalize_apply"]
 _ATTACHED = {}
 
 
-def profile_attach(kernel: int, events) -> None:
-    """Bracket the next len(events)//2 launches of `kernel` with the given
-    hipEvent_t handles (ints), pairwise.  events=None detaches."""
+def profile_attach(kernel: int, events, stride: int = 1) -> None:
+    """Bracket every stride-th launch of `kernel`, up to len(events)//2 of
+    them, with the given hipEvent_t handles (ints), pairwise.  events=None
+    detaches."""
     if events is None or len(events) < 2:
-        rc = lib().dqn_profile_attach(kernel, None, 0)
+        rc = lib().dqn_profile_attach(kernel, None, 0, 1)
         _ATTACHED.pop(kernel, None)
     else:
         arr = (ctypes.c_void_p * len(events))(*events)
         _ATTACHED[kernel] = arr
-        rc = lib().dqn_profile_attach(kernel, ctypes.cast(arr, ctypes.c_void_p), len(events) // 2)
+        rc = lib().dqn_profile_attach(kernel, ctypes.cast(arr, ctypes.c_void_p), len(events) // 2,
+                                      int(stride))
     _check(rc, "dqn_profile_attach")
 
 
