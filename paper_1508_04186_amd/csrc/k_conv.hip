@@ -341,24 +341,35 @@ __device__ __forceinline__ void conv_wgrad_body(const WgradParams& p, int bid, u
     for (int j = j0; j < j1; ++j) {
         __syncthreads();
         {
-            const unsigned char* src = sample_ptr(in, j);
-            stage_rows(s_in, row_elems * ESZ, src + (size_t)iy0 * IW * ESZ, (int64_t)IH * IW * ESZ, CIN,
-                       rows * IW * ESZ);
+            // The first U dz values per thread are loaded before the input
+            // rows are staged, so both sets of loads are in flight together.
             const float* dzj = dz + (size_t)j * COUT * P + pbeg;
             constexpr int U = 8;
-            for (int base = threadIdx.x; base < COUT * pix_pad; base += U * WG) {
-                float v[U];
+            auto dz_load = [&](int base, float (&v)[U]) {
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const int e = base + u * WG;
                     const int o = e / pix_pad, q = e - o * pix_pad;
                     v[u] = (e < COUT * pix_pad && q < npix) ? dzj[(size_t)o * P + q] : 0.f;
                 }
+            };
+            auto dz_store = [&](int base, const float (&v)[U]) {
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const int e = base + u * WG;
                     if (e < COUT * pix_pad) s_dz[e] = v[u];
                 }
+            };
+            float v0[U];
+            dz_load(threadIdx.x, v0);
+            const unsigned char* src = sample_ptr(in, j);
+            stage_rows<8>(s_in, row_elems * ESZ, src + (size_t)iy0 * IW * ESZ, (int64_t)IH * IW * ESZ, CIN,
+                          rows * IW * ESZ);
+            dz_store(threadIdx.x, v0);
+            for (int base = threadIdx.x + U * WG; base < COUT * pix_pad; base += U * WG) {
+                float v[U];
+                dz_load(base, v);
+                dz_store(base, v);
             }
         }
         __syncthreads();
@@ -455,12 +466,36 @@ __device__ __forceinline__ void conv_dgrad_body(const DgradParams& p, int bid, u
     if (mt0 >= mt1) return;  // uniform across the workgroup
     const int c0 = cib * CI;
 
+    // The first UW weight-tap values per thread are loaded before dz is
+    // staged, so both sets of loads are in flight together.
     const float* dzn = dz + (size_t)n * COUT * OH * OW;
-    constexpr int U = 8;
-    for (int base = threadIdx.x; base < COUT * PH * PW; base += U * WG) {
-        float v[U];
+    constexpr int NWT = TT * COUT * CI;
+    constexpr int UW = 8, UD = 16;
+    auto w_load = [&](int base, float (&v)[UW]) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
+        for (int u = 0; u < UW; ++u) {
+            const int e = base + u * WG;
+            const int c = e % CI;
+            const int r = e / CI;
+            const int o = r % COUT;
+            const int tap = r / COUT;
+            const int ty = tap / T, tx = tap - (tap / T) * T;
+            v[u] = e < NWT ? W[(((size_t)o * CIN + c0 + c) * K + py + S * ty) * K + px + S * tx] : 0.f;
+        }
+    };
+    auto w_store = [&](int base, const float (&v)[UW]) {
+#pragma unroll
+        for (int u = 0; u < UW; ++u) {
+            const int e = base + u * WG;
+            if (e < NWT) s_w[(e / CI) * RCW + e % CI] = v[u];
+        }
+    };
+    float wv0[UW];
+    w_load(threadIdx.x, wv0);
+    for (int base = threadIdx.x; base < COUT * PH * PW; base += UD * WG) {
+        float v[UD];
+#pragma unroll
+        for (int u = 0; u < UD; ++u) {
             const int e = base + u * WG;
             const int o = e / (PH * PW);
             const int r = e - o * (PH * PW);
@@ -470,33 +505,16 @@ __device__ __forceinline__ void conv_dgrad_body(const DgradParams& p, int bid, u
                        ? dzn[(o * OH + y) * OW + x] : 0.f;
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
+        for (int u = 0; u < UD; ++u) {
             const int e = base + u * WG;
             if (e < COUT * PH * PW) s_dz[e] = v[u];
         }
     }
-    for (int base = threadIdx.x; base < TT * COUT * CI; base += U * WG) {
-        float v[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int e = base + u * WG;
-            const int c = e % CI;
-            const int r = e / CI;
-            const int o = r % COUT;
-            const int tap = r / COUT;
-            const int ty = tap / T, tx = tap - (tap / T) * T;
-            v[u] = e < TT * COUT * CI ? W[(((size_t)o * CIN + c0 + c) * K + py + S * ty) * K + px + S * tx]
-                                       : 0.f;
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int e = base + u * WG;
-            if (e < TT * COUT * CI) {
-                const int c = e % CI;
-                const int r = e / CI;
-                s_w[r * RCW + c] = v[u];
-            }
-        }
+    w_store(threadIdx.x, wv0);
+    for (int base = threadIdx.x + UW * WG; base < NWT; base += UW * WG) {
+        float v[UW];
+        w_load(base, v);
+        w_store(base, v);
     }
     __syncthreads();
 

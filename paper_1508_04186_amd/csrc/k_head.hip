@@ -106,6 +106,24 @@ __global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
     const int j = blockIdx.x;
     const int B = p.B;
     const int64_t slice = (int64_t)2 * B * H;
+    // Everything else this workgroup reads is loaded before the slice
+    // reduction, so that all of it is in flight together.  An action outside
+    // [0, A) is clamped so it can never select a row outside W2.
+    const int act = min(max(p.action[j], 0), A - 1);
+    const float r = p.reward[j];
+    const bool term = p.terminal[j] != 0;
+    float b1v[E], b1tv[E], w2[A][E], w2t[A][E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int h = threadIdx.x + HT * e;
+        b1v[e] = p.b1[h];
+        b1tv[e] = p.b1t[h];
+#pragma unroll
+        for (int k = 0; k < A; ++k) {
+            w2[k][e] = p.W2[k * H + h];
+            w2t[k][e] = p.W2t[k * H + h];
+        }
+    }
     float zs[E], hs[E], v[2 * A];
 #pragma unroll
     for (int k = 0; k < 2 * A; ++k) v[k] = 0.f;
@@ -114,26 +132,20 @@ __global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
     reduce_slices<H, 2>(p.fc1p, rows, p.ks, slice, sred, sums);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        const int h = threadIdx.x + HT * e;
-        const float a = sums[0][e];
-        const float b = sums[1][e];
-        zs[e] = a + p.b1[h];
+        zs[e] = sums[0][e] + b1v[e];
         hs[e] = fmaxf(zs[e], 0.f);
-        const float hn = fmaxf(b + p.b1t[h], 0.f);
+        const float hn = fmaxf(sums[1][e] + b1tv[e], 0.f);
 #pragma unroll
         for (int k = 0; k < A; ++k) {
-            v[k] = fmaf(p.W2[k * H + h], hs[e], v[k]);
-            v[A + k] = fmaf(p.W2t[k * H + h], hn, v[A + k]);
+            v[k] = fmaf(w2[k][e], hs[e], v[k]);
+            v[A + k] = fmaf(w2t[k][e], hn, v[A + k]);
         }
     }
     block_sums<2 * A>(v, red);
     float m = v[A] + p.b2t[0];
 #pragma unroll
     for (int k = 1; k < A; ++k) m = fmaxf(m, v[A + k] + p.b2t[k]);
-    // An action outside [0, A) is clamped so it can never index outside W2.
-    const int act = min(max(p.action[j], 0), A - 1);
-    const float r = p.reward[j];
-    const float y = p.terminal[j] ? r : fmaf(p.gamma, m, r);
+    const float y = term ? r : fmaf(p.gamma, m, r);
     float qa = v[0] + p.b2[0];
 #pragma unroll
     for (int k = 1; k < A; ++k) qa = (k == act) ? v[k] + p.b2[k] : qa;
@@ -142,8 +154,11 @@ __global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
 #pragma unroll
     for (int e = 0; e < E; ++e) {
         const int h = threadIdx.x + HT * e;
+        float wa = w2[0][e];
+#pragma unroll
+        for (int k = 1; k < A; ++k) wa = (k == act) ? w2[k][e] : wa;
         p.h1s[(int64_t)j * H + h] = hs[e];
-        p.dz1[(int64_t)j * H + h] = zs[e] > 0.f ? delta * p.W2[act * H + h] : 0.f;
+        p.dz1[(int64_t)j * H + h] = zs[e] > 0.f ? delta * wa : 0.f;
     }
     if (threadIdx.x == 0) {
         p.delta[j] = delta;
