@@ -122,6 +122,10 @@ def kernel_work(shape, B, forward_only=False):
             w[f"conv{l+1}_wgrad"] = (2 * B * macs, 0)
             if l > 0:
                 w[f"conv{l+1}_dgrad"] = (2 * B * macs, 0)
+    if len(dims) == 2:   # fused conv1 + conv2 launches of the small network
+        w["conv12_fwd"] = (w["conv1_fwd"][0] + w["conv2_fwd"][0], 0)
+        if not forward_only:
+            w["conv12_bwd"] = (w["conv1_wgrad"][0] + w["conv2_wgrad"][0] + w["conv2_dgrad"][0], 0)
     w["fc1_fwd"] = (2 * nf * H * F, 0)
     w["head"] = (2 * nf * A * H, 0)
     if forward_only:
@@ -142,7 +146,7 @@ def kernel_work(shape, B, forward_only=False):
 
 # Kernels whose roofline is reported (dense contractions and the
 # memory-bound gather); the head and finalize are latency-bound reductions.
-ROOFLINE_KERNELS = ("conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "fc1_wgrad", "fc1_dgrad",
+ROOFLINE_KERNELS = ("conv1_fwd", "conv2_fwd", "conv3_fwd", "conv12_fwd", "conv12_bwd", "fc1_fwd", "fc1_wgrad", "fc1_dgrad",
                     "conv1_wgrad", "conv2_wgrad", "conv3_wgrad", "conv2_dgrad", "conv3_dgrad",
                     "fc1_bwd", "conv2_bwd", "conv3_bwd", "gather", "apply", "finalize_apply")
 

@@ -13,6 +13,10 @@
  * events = NULL (or n_pairs = 0) to detach.  stride >= 1.  Returns DQN_OK or
  * DQN_EINVAL.
  * dqn_profile_used(kernel): number of pairs recorded since the last attach.
+ * dqn_profile_set_fusion(enabled): with 0, the small network's conv layers
+ * run as one launch per layer and pass instead of the fused two-layer
+ * launches (DQN_K_CONV12_FWD / DQN_K_CONV12_BWD), so that the two can be
+ * compared; 1 (the default) restores them.  Returns DQN_OK.
  *
  * The hook is process-wide state: attach/detach must not race with calls of
  * the hot-path entry points on other host threads.
@@ -46,11 +50,14 @@ typedef enum {
     DQN_K_CONV2_BWD = 16,   /* conv2 weight + input gradient in one launch (small batch) */
     DQN_K_CONV3_BWD = 17,   /* conv3 weight + input gradient in one launch (small batch) */
     DQN_K_FINALIZE_APPLY = 18, /* finalize with the update applied (dqn_train_steps) */
-    DQN_K_COUNT = 19
+    DQN_K_CONV12_FWD = 19,  /* both conv layers of the small network */
+    DQN_K_CONV12_BWD = 20,  /* conv2 weight + input gradient and conv1 weight gradient, small network */
+    DQN_K_COUNT = 21
 } dqn_kernel;
 
 int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs, int32_t stride);
 int32_t dqn_profile_used(int32_t kernel);
+int dqn_profile_set_fusion(int32_t enabled);
 
 #ifdef __cplusplus
 }

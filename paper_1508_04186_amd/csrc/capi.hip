@@ -76,6 +76,11 @@ inline int64_t act_elems(const ConvDims& c) { return (int64_t)c.cout * c.oh * c.
 // Largest batch whose backward kernels are launched in pairs (above it each
 // kernel alone fills the chip and keeps its own occupancy).
 constexpr int kPairMaxBatch = 64;
+// Samples per forward launch up to which the small network's two conv layers
+// run as one fused launch (measured faster at every batch up to 1024
+// samples per launch, and by 2x at 64).
+constexpr int kFuseMaxRows = 1 << 20;
+bool g_fusion = true;  // dqn_profile_set_fusion
 
 // fc1 forward split-K: enough slices that the launch covers the chip.
 struct Carver {
@@ -121,8 +126,13 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
     for (int l = 0; l < ni.n_conv; ++l) {
         const ConvDims& c = ni.d[l];
         t.chunks[l] = conv_wgrad_chunks(ni.conv[l], B);
-        t.wpart[l] = cv.take<float>(ws, (int64_t)t.chunks[l] * c.cout * c.cin * c.k * c.k);
-        t.bpart[l] = cv.take<float>(ws, (int64_t)t.chunks[l] * c.cout);
+        // The fused small-network backward writes conv1's partial sums per
+        // (sample, band) instead: room for whichever count is larger.
+        int64_t slots = t.chunks[l];
+        if (l == 0 && ni.n_conv == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]))
+            slots = std::max<int64_t>(slots, conv_s12_bwd_slots(B));
+        t.wpart[l] = cv.take<float>(ws, slots * c.cout * c.cin * c.k * c.k);
+        t.bpart[l] = cv.take<float>(ws, slots * c.cout);
     }
     t.bytes = cv.off;
     return t;
@@ -242,8 +252,16 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     }
 
     // Forward of s under theta (samples 0..B-1) and of s' under theta^-
-    // (samples B..2B-1), one launch per layer.
-    for (int l = 0; l < L; ++l) {
+    // (samples B..2B-1): one launch per layer, or both conv layers of the
+    // small network in one launch at small batch.
+    const bool fused_fwd = g_fusion && L == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
+                           2 * B <= kFuseMaxRows && conv_s12_fwd_aligned(s0) && conv_s12_fwd_aligned(sn0);
+    if (fused_fwd)
+        RUN(DQN_K_CONV12_FWD,
+            launch_conv_s12_fwd(s0, sn0, B, 2 * B, th + ni.w_off[0], th + ni.b_off[0], th + ni.w_off[1],
+                                th + ni.b_off[1], tt + ni.w_off[0], tt + ni.b_off[0], tt + ni.w_off[1],
+                                tt + ni.b_off[1], t.act[0], t.act[1], src.replay ? &side : nullptr, st));
+    for (int l = 0; l < L && !fused_fwd; ++l) {
         const int64_t ae = l > 0 ? act_elems(ni.d[l - 1]) : 0;
         const ConvIn in_a = l == 0 ? s0 : ConvIn{t.act[l - 1], nullptr, ae * 4, 0};
         const ConvIn in_b = l == 0 ? sn0 : ConvIn{t.act[l - 1] + (int64_t)B * ae, nullptr, ae * 4, 0};
@@ -306,7 +324,19 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
                         t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, st));
     }
-    for (int l = L - 1; l >= 0; --l) {
+    // The small network's conv layers in one launch: conv2's weight gradient,
+    // and conv2's input gradient with conv1's weight gradient per (sample,
+    // band of conv1 rows).
+    const bool fused_bwd = g_fusion && L == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
+                           B <= kFuseMaxRows && conv_s12_fwd_aligned(s0);
+    int chunks0 = t.chunks[0];
+    if (fused_bwd) {
+        RUN(DQN_K_CONV12_BWD,
+            launch_conv_s12_bwd(s0, t.act[0], t.dconv[1], th + ni.w_off[1], B, t.wpart[1], t.bpart[1],
+                                t.wpart[0], t.bpart[0], st));
+        chunks0 = conv_s12_bwd_slots(B);
+    }
+    for (int l = L - 1; l >= 0 && !fused_bwd; --l) {
         const ConvIn in = l == 0 ? s0 : ConvIn{t.act[l - 1], nullptr, act_elems(ni.d[l - 1]) * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
         if (l > 0 && paired) {
@@ -328,7 +358,7 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
         const ConvDims& c = ni.d[l];
         fa.wpart[l] = t.wpart[l];
         fa.bpart[l] = t.bpart[l];
-        fa.chunks[l] = t.chunks[l];
+        fa.chunks[l] = l == 0 ? chunks0 : t.chunks[l];
         fa.wcount[l] = c.cout * c.cin * c.k * c.k;
         fa.cout[l] = c.cout;
         fa.gw[l] = grad_out + ni.w_off[l];
@@ -467,8 +497,16 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
     f = fwd_layout(ni, batch, ws);
     hipStream_t st = (hipStream_t)stream;
     const float* th = theta;
-    for (int l = 0; l < ni.n_conv; ++l) {
-        const ConvIn in = l == 0 ? ConvIn{states, nullptr, (int64_t)net->in_c * net->in_h * net->in_w, 0}
+    const ConvIn in0{states, nullptr, (int64_t)net->in_c * net->in_h * net->in_w, 0};
+    const bool fused_fwd = g_fusion && ni.n_conv == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
+                           batch <= kFuseMaxRows && conv_s12_fwd_aligned(in0);
+    if (fused_fwd)
+        RUN(DQN_K_CONV12_FWD,
+            launch_conv_s12_fwd(in0, in0, batch, batch, th + ni.w_off[0], th + ni.b_off[0],
+                                th + ni.w_off[1], th + ni.b_off[1], th + ni.w_off[0], th + ni.b_off[0],
+                                th + ni.w_off[1], th + ni.b_off[1], f.act[0], f.act[1], nullptr, st));
+    for (int l = 0; l < ni.n_conv && !fused_fwd; ++l) {
+        const ConvIn in = l == 0 ? in0
                                  : ConvIn{f.act[l - 1], nullptr, act_elems(ni.d[l - 1]) * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
         RUN(DQN_K_CONV1_FWD + l,
@@ -553,6 +591,11 @@ int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs, int32_t s
     p.stride = stride;
     p.seen = 0;
     p.open = false;
+    return DQN_OK;
+}
+
+int dqn_profile_set_fusion(int32_t enabled) {
+    g_fusion = enabled != 0;
     return DQN_OK;
 }
 

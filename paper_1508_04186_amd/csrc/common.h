@@ -103,6 +103,31 @@ hipError_t launch_conv_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b, in
                            const float* w_a, const float* b_a, const float* w_b, const float* b_b,
                            float* out, float in_scale, const SideFields* side, hipStream_t st);
 
+// Both convolution layers of the small network (CONV_S1 then CONV_S2, bias +
+// ReLU each) in one launch; sample roles, inputs and weights as
+// launch_conv_fwd.  Writes act1 [n][16][20][20] and act2 [n][32][9][9].
+// Requires 16-byte aligned weight blocks, input bases and record strides
+// (conv_s12_fwd_aligned).
+bool conv_s12_fwd_supported(ConvId c1, ConvId c2);
+bool conv_s12_fwd_aligned(const ConvIn& in);
+hipError_t launch_conv_s12_fwd(const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
+                               const float* w1_a, const float* b1_a, const float* w2_a,
+                               const float* b2_a, const float* w1_b, const float* b1_b,
+                               const float* w2_b, const float* b2_b, float* act1, float* act2,
+                               const SideFields* side, hipStream_t st);
+
+// The small network's backward below the fc layers in one launch: conv2's
+// weight/bias partial sums (as launch_conv_wgrad for CONV_S2: wpart2,
+// bpart2 with conv_wgrad_chunks(CONV_S2, batch) slots), and, per sample and
+// band of conv1 rows, conv2's input gradient masked by [act1 > 0] and
+// conv1's weight/bias partial sums over those rows into
+// conv_s12_bwd_slots(batch) slots of wpart1 [slots][16][256], bpart1
+// [slots][16].  in: the network input (bytes), 16-byte aligned.
+int conv_s12_bwd_slots(int batch);
+hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float* dz2, const float* w2,
+                               int batch, float* wpart2, float* bpart2, float* wpart1, float* bpart1,
+                               hipStream_t st);
+
 // Weight and bias gradient partial sums over sample chunks:
 // wpart [chunks][cout][cin*k*k], bpart [chunks][cout].
 int conv_wgrad_chunks(ConvId id, int batch);

@@ -1,0 +1,540 @@
+// The two convolution layers of the small Q-network (Sec. III.A: 16 filters
+// 8x8 stride 4 on the 4x84x84 byte input, then 32 filters 4x4 stride 2, each
+// with ReLU) in one launch, for small batches where the layers are latency
+// bound.  A workgroup owns one sample and a band of three conv2 output rows:
+// it stages the 36 input rows the band needs, both layers' weights and
+// biases (all loads in flight together), computes the 8 conv1 rows the band
+// reads into LDS, writes the conv1 rows it owns, then computes its conv2
+// rows.  Bands overlap by two conv1 rows, which are computed twice and
+// written once.
+//
+// conv1 runs on bf16 MFMA (v_mfma_f32_16x16x32_bf16) without loss of fp32
+// accuracy: the input bytes are exact in bf16, each fp32 weight w is split
+// exactly into three bf16 terms w = hi + mid + lo (8 significand bits each),
+// and each byte x term product is exact in fp32, so the three MFMAs per
+// k-step accumulate the same products an fp32 contraction would, in fp32.
+// conv2 runs on fp32 MFMA with the contraction order of the per-layer kernel.
+//
+// The backward counterpart runs, in one launch, the conv2 weight gradient
+// (the per-layer body) and, per (sample, band of conv1 rows), the conv2 input
+// gradient for those rows with conv1's ReLU mask applied, kept in LDS, and
+// the conv1 weight and bias partial sums over those rows (bands of 4 conv1
+// rows here: the backward per row is heavier than the forward's).
+#include <initializer_list>
+
+#include "conv_body.h"
+
+namespace dqn {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// Small-network geometry.
+constexpr int C0 = 4, H0 = 84;                   // input channels, side
+constexpr int C1 = 16, K1 = 8, S1 = 4, H1 = 20;  // conv1
+constexpr int C2 = 32, K2 = 4, S2 = 2, H2 = 9;   // conv2
+constexpr int R2 = 3;                            // conv2 rows per band
+constexpr int NBAND = H2 / R2;
+constexpr int R1 = (R2 - 1) * S2 + K2;           // conv1 rows per band (8)
+constexpr int R0 = (R1 - 1) * S1 + K1;           // input rows per band (36)
+constexpr int KW1 = C0 * K1 * K1;                // conv1 contraction length (256)
+constexpr int RS1 = KW1 + 8;                     // bf16 row stride of a split conv1 weight row
+constexpr int A1C = R1 * H1 + 16;                // float stride between conv1 channels in LDS
+constexpr int KK2 = K2 * K2;
+constexpr int RC2 = 16;                          // conv2 weight LDS layout: [o][c][ky*kx]
+constexpr int RO2 = (C1 * RC2 / 64) * 64 + 65;  // = 1 mod 64: conflict-free B reads
+static_assert(H2 % R2 == 0, "bands must tile the conv2 rows");
+static_assert(R1 * H1 % 16 == 0, "conv1 band must be whole M-tiles");
+
+// LDS carve (bytes).
+constexpr int OFF_IN = 0;                                  // bf16 [C0][R0][H0]
+constexpr int OFF_W1 = OFF_IN + C0 * R0 * H0 * 2;          // bf16 [3][C1][RS1]
+constexpr int OFF_A1 = OFF_W1 + 3 * C1 * RS1 * 2;          // f32 [C1][A1C]
+constexpr int OFF_W2 = OFF_A1 + C1 * A1C * 4;              // f32 [C2][RO2]
+constexpr int OFF_B = OFF_W2 + C2 * RO2 * 4;               // f32 b1[C1], b2[C2]
+constexpr int LDS_BYTES = OFF_B + (C1 + C2) * 4;
+static_assert(OFF_W1 % 16 == 0 && OFF_A1 % 16 == 0 && OFF_W2 % 16 == 0 && OFF_B % 16 == 0, "alignment");
+
+__device__ __forceinline__ f4 mfma16x16x32bf16(bf16x8 a, bf16x8 b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Exact split of an fp32 value into three bf16 terms, w = hi + mid + lo: each
+// remainder is exactly representable in fp32, and after two terms at most 8
+// significand bits remain.
+__device__ __forceinline__ void split3(float w, __bf16& hi, __bf16& mid, __bf16& lo) {
+    hi = (__bf16)w;
+    const float r1 = w - (float)hi;
+    mid = (__bf16)r1;
+    lo = (__bf16)(r1 - (float)mid);
+}
+
+struct FusedFwdParams {
+    ConvIn in_a, in_b;
+    int n_a, n;
+    const float *w1_a, *b1_a, *w2_a, *b2_a;  // samples < n_a
+    const float *w1_b, *b1_b, *w2_b, *b2_b;  // samples >= n_a
+    float* act1;                             // [n][C1][H1][H1]
+    float* act2;                             // [n][C2][H2][H2]
+    SideFields side;
+};
+
+__global__ __launch_bounds__(WG) void conv_s12_fwd_kernel(FusedFwdParams p) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    __bf16* s_in = (__bf16*)(smem + OFF_IN);
+    __bf16* s_w1 = (__bf16*)(smem + OFF_W1);
+    float* s_a1 = (float*)(smem + OFF_A1);
+    float* s_w2 = (float*)(smem + OFF_W2);
+    float* s_b = (float*)(smem + OFF_B);
+
+    const int band = blockIdx.x % NBAND;
+    const int n = blockIdx.x / NBAND;
+    const bool second = n >= p.n_a;
+    const unsigned char* src = sample_ptr(second ? p.in_b : p.in_a, second ? n - p.n_a : n);
+    const float* w1 = second ? p.w1_b : p.w1_a;
+    const float* w2 = second ? p.w2_b : p.w2_a;
+    const float* b1 = second ? p.b1_b : p.b1_a;
+    const float* b2 = second ? p.b2_b : p.b2_a;
+    const int t = threadIdx.x;
+
+    if (p.side.idx && blockIdx.x == 0) {
+        for (int j = t; j < p.side.batch; j += WG) {
+            const int64_t i = p.side.idx[j];
+            p.side.a_out[j] = p.side.action[i];
+            p.side.r_out[j] = (float)p.side.reward[i];
+            p.side.t_out[j] = p.side.terminal[i];
+        }
+    }
+
+    // ---- staging: every global load of the workgroup is issued before the
+    // first LDS store.  Input rows [band*R2*S2*S1, +R0) of each channel are
+    // contiguous (R0*H0 bytes, 16-byte aligned); weights are contiguous.
+    constexpr int IN_V = C0 * R0 * H0 / 16;    // 16-byte units of input
+    constexpr int IN_PER = (IN_V + WG - 1) / WG;
+    constexpr int W1_V = C1 * KW1 / 4;
+    constexpr int W1_PER = W1_V / WG;
+    constexpr int W2_V = C2 * C1 * KK2 / 4;
+    constexpr int W2_PER = W2_V / WG;
+    static_assert((C0 * R0 * H0) % 16 == 0 && (R0 * H0) % 16 == 0, "input rows must be whole 16-byte units");
+    static_assert(W1_V % WG == 0 && W2_V % WG == 0, "weights must split evenly over the workgroup");
+    const int iy0 = band * R2 * S2 * S1;
+    f4 vin[IN_PER], vw1[W1_PER], vw2[W2_PER];
+#pragma unroll
+    for (int u = 0; u < IN_PER; ++u) {
+        const int e = t + u * WG;
+        if (e < IN_V) {
+            const int c = e / (R0 * H0 / 16), r = e - c * (R0 * H0 / 16);
+            vin[u] = *(const f4*)(src + (size_t)c * H0 * H0 + (size_t)iy0 * H0 + 16 * r);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < W1_PER; ++u) vw1[u] = ((const f4*)w1)[t + u * WG];
+#pragma unroll
+    for (int u = 0; u < W2_PER; ++u) vw2[u] = ((const f4*)w2)[t + u * WG];
+    float bias = 0.f;
+    if (t < C1) bias = b1[t];
+    else if (t < C1 + C2) bias = b2[t - C1];
+
+    // input bytes -> bf16 (exact), same [c][row][x] order
+#pragma unroll
+    for (int u = 0; u < IN_PER; ++u) {
+        const int e = t + u * WG;
+        if (e < IN_V) {
+            union { f4 v; unsigned char b[16]; } q;
+            q.v = vin[u];
+            bf16x8 lo8, hi8;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                lo8[i] = (__bf16)(float)q.b[i];
+                hi8[i] = (__bf16)(float)q.b[8 + i];
+            }
+            *(bf16x8*)(s_in + 16 * e) = lo8;
+            *(bf16x8*)(s_in + 16 * e + 8) = hi8;
+        }
+    }
+    // conv1 weights -> three bf16 planes [part][o][k]
+#pragma unroll
+    for (int u = 0; u < W1_PER; ++u) {
+        const int e = t + u * WG;
+        const int o = (4 * e) / KW1, k = (4 * e) % KW1;
+        bf16x4 h, m, l;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            __bf16 hi, mid, lo;
+            split3(vw1[u][i], hi, mid, lo);
+            h[i] = hi;
+            m[i] = mid;
+            l[i] = lo;
+        }
+        *(bf16x4*)(s_w1 + (0 * C1 + o) * RS1 + k) = h;
+        *(bf16x4*)(s_w1 + (1 * C1 + o) * RS1 + k) = m;
+        *(bf16x4*)(s_w1 + (2 * C1 + o) * RS1 + k) = l;
+    }
+    // conv2 weights -> padded [o][c][ky*kx]
+#pragma unroll
+    for (int u = 0; u < W2_PER; ++u) {
+        const int e = t + u * WG;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int f = 4 * e + i;
+            const int o = f / (C1 * KK2), r = f - o * (C1 * KK2);
+            const int c = r / KK2, k = r - c * KK2;
+            s_w2[o * RO2 + c * RC2 + k] = vw2[u][i];
+        }
+    }
+    if (t < C1 + C2) s_b[t] = bias;
+    __syncthreads();
+
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+
+    // ---- conv1: band-local pixels 16*mt + li (row = p / H1, x = p % H1),
+    // contraction k = c*64 + ky*8 + kx; k-step kb covers c = kb/2 and
+    // ky = 4*(kb%2) + g, kx = 0..7 in lane group g.
+    const int y1 = band * R2 * S2;             // first conv1 row of the band
+    const int own0 = band == 0 ? 0 : y1 + (K2 - S2);
+    const int own1 = band == NBAND - 1 ? H1 : y1 + R2 * S2 + (K2 - S2);
+    constexpr int MT1 = R1 * H1 / 16;
+    float* a1g = p.act1 + (size_t)n * C1 * H1 * H1;
+    for (int mt = wave; mt < MT1; mt += 4) {
+        const int pa = mt * 16 + li;
+        const int ra = pa / H1, xa = pa - ra * H1;
+        f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KW1 / 32; ++kb) {
+            const int c = kb >> 1, ky = (kb & 1) * 4 + g;
+            const __bf16* ap = s_in + (c * R0 + S1 * ra + ky) * H0 + S1 * xa;
+            bf16x8 a;
+            const bf16x4 a0 = *(const bf16x4*)ap;
+            const bf16x4 a1 = *(const bf16x4*)(ap + 4);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                a[i] = a0[i];
+                a[4 + i] = a1[i];
+            }
+#pragma unroll
+            for (int part = 0; part < 3; ++part) {
+                const bf16x8 b = *(const bf16x8*)(s_w1 + (part * C1 + li) * RS1 + kb * 32 + 8 * g);
+                acc = mfma16x16x32bf16(a, b, acc);
+            }
+        }
+        // lane holds pixels 16*mt + 4g + r (one row: H1 is a multiple of 4)
+        // of channel o = li
+        const int pb = mt * 16 + 4 * g;
+        const int rb = pb / H1, xb = pb - rb * H1;
+        const float bo = s_b[li];
+        constexpr float inv255 = (float)(1.0 / 255.0);
+        f4 v;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[r] * inv255 + bo, 0.f);
+        *(f4*)(s_a1 + li * A1C + rb * H1 + xb) = v;
+        const int yg = y1 + rb;
+        if (yg >= own0 && yg < own1) *(f4*)(a1g + ((size_t)li * H1 + yg) * H1 + xb) = v;
+    }
+    __syncthreads();
+
+    // ---- conv2: wave w takes M-tile w/2 (band-local pixels) and N-tile w%2;
+    // lane group g takes channel 4*cb + g; steps walk (cb, ky, kx).
+    {
+        constexpr int P2 = R2 * H2;
+        const int mt = wave >> 1, nt = wave & 1;
+        const int pp = mt * 16 + li;
+        const int pc = pp < P2 ? pp : P2 - 1;
+        const int oy = pc / H2, ox = pc - (pc / H2) * H2;
+        const float amask = pp < P2 ? 1.f : 0.f;
+        f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int cb = 0; cb < C1 / 4; ++cb) {
+            const int c = cb * 4 + g;
+#pragma unroll
+            for (int ky = 0; ky < K2; ++ky) {
+                const float* ar = s_a1 + c * A1C + (S2 * oy + ky) * H1 + S2 * ox;
+                const float* wp = s_w2 + (nt * 16 + li) * RO2 + c * RC2 + ky * K2;
+#pragma unroll
+                for (int kx = 0; kx < K2; ++kx) acc = mfma16x16x4(ar[kx] * amask, wp[kx], acc);
+            }
+        }
+        const int o = nt * 16 + li;
+        const float bo = s_b[C1 + o];
+        float* a2 = p.act2 + ((size_t)n * C2 + o) * H2 * H2 + band * R2 * H2;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int q = mt * 16 + 4 * g + r;
+            if (q < P2) a2[q] = fmaxf(acc[r] + bo, 0.f);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Backward: bands of NRMAX conv1 rows (a partition of the 20 rows; even row
+// counts and band starts keep every stride phase aligned to the band).
+constexpr int NRMAX = 4;                 // conv1 rows per backward band
+constexpr int NBB = H1 / NRMAX;          // backward bands per sample
+static_assert(H1 % NRMAX == 0 && NRMAX % 2 == 0, "backward bands must tile the conv1 rows in pairs");
+constexpr int T2 = K2 / S2;              // taps per stride phase and axis (2)
+constexpr int NZR = NRMAX / 2 + 1;       // staged conv2-gradient rows
+constexpr int NZC = H2 + 2;              // staged conv2-gradient columns (zero border)
+constexpr int RCW = C1 + 1;              // row stride of the [tap][o][c] conv2 weight slice
+constexpr int LD1 = NRMAX * H1 + 4;      // row stride of the conv1 gradient tile (= 36 mod 64)
+constexpr int RIN = (NRMAX - 1) * S1 + K1;  // staged input rows per channel
+
+constexpr int BOFF_DZ = 0;                                  // f32 [C2][NZR][NZC]
+constexpr int BOFF_W = BOFF_DZ + C2 * NZR * NZC * 4;        // f32 [KK2][C2][RCW]
+constexpr int BOFF_MASK = BOFF_W + KK2 * C2 * RCW * 4;      // f32 [C1][NRMAX*H1]
+constexpr int BOFF_D1 = BOFF_MASK + C1 * NRMAX * H1 * 4;    // f32 [C1][LD1]
+constexpr int BOFF_IN = BOFF_D1 + C1 * LD1 * 4;             // u8 [C0][RIN][H0]
+constexpr int BOFF_POFF = BOFF_IN + C0 * RIN * H0;          // int [NRMAX*H1]
+constexpr int B_LDS = BOFF_POFF + NRMAX * H1 * 4;
+static_assert(BOFF_MASK % 16 == 0 && BOFF_IN % 16 == 0 && BOFF_POFF % 16 == 0, "alignment");
+
+struct S1BwdParams {
+    ConvIn in;            // network input of the B samples (bytes)
+    const float* dz2;     // gradient at conv2's pre-activation [B][C2][H2][H2]
+    const float* w2;      // conv2 weights [C2][C1][K2][K2]
+    const float* act1;    // conv1 output [B][C1][H1][H1] (its ReLU mask)
+    float* wpart1;        // conv1 weight partial sums [B*NBB][C1][KW1]
+    float* bpart1;        // conv1 bias partial sums [B*NBB][C1]
+    float in_scale;
+};
+
+// One (sample j, band) of the conv1 side of the backward pass.
+__device__ __forceinline__ void s1_bwd_body(const S1BwdParams& p, int bid, unsigned char* smem) {
+    float* s_dz = (float*)(smem + BOFF_DZ);
+    float* s_w = (float*)(smem + BOFF_W);
+    float* s_mask = (float*)(smem + BOFF_MASK);
+    float* s_d1 = (float*)(smem + BOFF_D1);
+    unsigned char* s_in = smem + BOFF_IN;
+    int* s_poff = (int*)(smem + BOFF_POFF);
+
+    const int band = bid % NBB;
+    const int j = bid / NBB;
+    const int y0 = band * NRMAX, y1 = y0 + NRMAX;
+    const int nr = NRMAX;                    // owned rows
+    const int npx = nr * H1;
+    const int oyb = y0 / 2 - 1;              // conv2-gradient row of staged row 0
+    const int t = threadIdx.x;
+
+    // ---- staging, all loads in flight before the first LDS store
+    constexpr int NDZ = C2 * NZR * NZC;
+    constexpr int UDZ = (NDZ + WG - 1) / WG;
+    constexpr int W2V = C2 * C1 * KK2 / 4;
+    constexpr int UW = W2V / WG;
+    constexpr int MV = C1 * NRMAX * H1 / 4;  // 16-byte units of the mask rows, at most
+    constexpr int UM = (MV + WG - 1) / WG;
+    constexpr int IV = C0 * RIN * H0 / 16;   // 16-byte units of the input rows, at most
+    constexpr int UI = (IV + WG - 1) / WG;
+    static_assert(W2V % WG == 0, "conv2 weights must split evenly");
+    const float* dzj = p.dz2 + (size_t)j * C2 * H2 * H2;
+    float vdz[UDZ];
+#pragma unroll
+    for (int u = 0; u < UDZ; ++u) {
+        const int e = t + u * WG;
+        const int o = e / (NZR * NZC), r = e - o * (NZR * NZC);
+        const int oy = oyb + r / NZC, ox = r % NZC - 1;
+        vdz[u] = (e < NDZ && oy >= 0 && oy < H2 && ox >= 0 && ox < H2) ? dzj[(o * H2 + oy) * H2 + ox] : 0.f;
+    }
+    f4 vw[UW];
+#pragma unroll
+    for (int u = 0; u < UW; ++u) vw[u] = ((const f4*)p.w2)[t + u * WG];
+    const int mv = C1 * nr * H1 / 4;
+    const float* a1j = p.act1 + (size_t)j * C1 * H1 * H1 + y0 * H1;
+    f4 vm[UM];
+#pragma unroll
+    for (int u = 0; u < UM; ++u) {
+        const int e = t + u * WG;
+        if (e < mv) {
+            const int c = e / (nr * H1 / 4), r = e - c * (nr * H1 / 4);
+            vm[u] = *(const f4*)(a1j + (size_t)c * H1 * H1 + 4 * r);
+        }
+    }
+    const int rin = (nr - 1) * S1 + K1;      // input rows for the owned conv1 rows
+    const int iv = C0 * rin * H0 / 16;
+    const unsigned char* src = sample_ptr(p.in, j) + (size_t)S1 * y0 * H0;
+    f4 vi[UI];
+#pragma unroll
+    for (int u = 0; u < UI; ++u) {
+        const int e = t + u * WG;
+        if (e < iv) {
+            const int c = e / (rin * H0 / 16), r = e - c * (rin * H0 / 16);
+            vi[u] = *(const f4*)(src + (size_t)c * H0 * H0 + 16 * r);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < UDZ; ++u) {
+        const int e = t + u * WG;
+        if (e < NDZ) s_dz[e] = vdz[u];
+    }
+#pragma unroll
+    for (int u = 0; u < UW; ++u) {
+        const int e = t + u * WG;  // W2[o][c][ky][kx..kx+3], kx = 0
+        const int o = e / (C1 * K2), r = e - o * (C1 * K2);
+        const int c = r / K2, ky = r - c * K2;
+#pragma unroll
+        for (int kx = 0; kx < K2; ++kx) s_w[((ky * K2 + kx) * C2 + o) * RCW + c] = vw[u][kx];
+    }
+#pragma unroll
+    for (int u = 0; u < UM; ++u) {
+        const int e = t + u * WG;
+        if (e < mv) {
+            const int c = e / (nr * H1 / 4), r = e - c * (nr * H1 / 4);
+            *(f4*)(s_mask + c * NRMAX * H1 + 4 * r) = vm[u];
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < UI; ++u) {
+        const int e = t + u * WG;
+        if (e < iv) {
+            const int c = e / (rin * H0 / 16), r = e - c * (rin * H0 / 16);
+            *(f4*)(s_in + c * RIN * H0 + 16 * r) = vi[u];
+        }
+    }
+    for (int q = t; q < npx; q += WG) {
+        const int y = q / H1, x = q - (q / H1) * H1;
+        s_poff[q] = S1 * y * H0 + S1 * x;
+    }
+    __syncthreads();
+
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+
+    // ---- conv1 input gradient by stride phase (py, px): owned pixels
+    // (y0 + py + 2*qr, px + 2*qc) receive W2[o][c][py+2ty][px+2tx] *
+    // dz2[o][y/2 - ty][qc - tx]; contraction over (o, ty, tx), lane group g
+    // taking o = 4*ob + g.  M = phase pixels, N = the 16 conv1 channels.
+    {
+        const int nrp = nr / 2;
+        const int pp = nrp * (H1 / 2);         // pixels per phase
+        const int mtp = (pp + 15) / 16;
+        for (int tt = wave; tt < 4 * mtp; tt += 4) {
+            const int ph = tt / mtp, mt = tt - ph * mtp;
+            const int py = ph >> 1, px = ph & 1;
+            const int q = mt * 16 + li;
+            const int qv = q < pp ? q : pp - 1;
+            const int qr = qv / (H1 / 2), qc = qv - qr * (H1 / 2);
+            const float amask = q < pp ? 1.f : 0.f;
+            f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ob = 0; ob < C2 / 4; ++ob) {
+                const int o = ob * 4 + g;
+#pragma unroll
+                for (int ty = 0; ty < T2; ++ty)
+#pragma unroll
+                    for (int tx = 0; tx < T2; ++tx) {
+                        const float a = s_dz[(o * NZR + qr - ty + 1) * NZC + qc - tx + 1] * amask;
+                        const int tap = (py + S2 * ty) * K2 + px + S2 * tx;
+                        acc = mfma16x16x4(a, s_w[(tap * C2 + o) * RCW + li], acc);
+                    }
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int qq = mt * 16 + 4 * g + r;
+                if (qq < pp) {
+                    const int lp = (py + 2 * (qq / (H1 / 2))) * H1 + px + 2 * (qq % (H1 / 2));
+                    s_d1[li * LD1 + lp] = s_mask[li * NRMAX * H1 + lp] > 0.f ? acc[r] : 0.f;
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- conv1 weight gradient over the owned pixels: M = 16 output
+    // channels, N = 256 weight columns (c, ky, kx), contraction over pixels
+    // (lane group g takes pixel 4*st + g).  Wave w owns N-tiles w + 4i.
+    const int slot = j * NBB + band;
+    {
+        constexpr int NTW = KW1 / 16 / 4;      // N-tiles per wave
+        int koff[NTW];
+#pragma unroll
+        for (int i = 0; i < NTW; ++i) {
+            const int col = (wave + 4 * i) * 16 + li;
+            const int c = col / (K1 * K1), ky = (col / K1) % K1, kx = col % K1;
+            koff[i] = c * RIN * H0 + ky * H0 + kx;
+        }
+        f4 acc[NTW];
+#pragma unroll
+        for (int i = 0; i < NTW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+        for (int st = 0; st < npx / 4; ++st) {
+            const int lp = 4 * st + g;
+            const float a = s_d1[li * LD1 + lp];
+            const int po = s_poff[lp];
+#pragma unroll
+            for (int i = 0; i < NTW; ++i) acc[i] = mfma16x16x4(a, (float)s_in[koff[i] + po], acc[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < NTW; ++i) {
+            const int col = (wave + 4 * i) * 16 + li;
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                p.wpart1[((size_t)slot * C1 + 4 * g + r) * KW1 + col] = acc[i][r] * p.in_scale;
+        }
+    }
+    if (t < C1) {
+        const float* row = s_d1 + t * LD1;
+        float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+        for (int q = 0; q < npx; q += 4) {
+            s0 += row[q];
+            s1 += row[q + 1];
+            s2 += row[q + 2];
+            s3 += row[q + 3];
+        }
+        p.bpart1[(size_t)slot * C1 + t] = (s0 + s1) + (s2 + s3);
+    }
+}
+
+// Blocks [0, n_b) run the conv1 side (the longer per-block work, so it is
+// dispatched first), the rest conv2's weight gradient.
+__global__ __launch_bounds__(WG) void conv_s12_bwd_kernel(WgradParams w, S1BwdParams b, int n_b) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    if ((int)blockIdx.x < n_b)
+        s1_bwd_body(b, blockIdx.x, smem);
+    else
+        conv_wgrad_body<C1, H1, H1, C2, K2, S2, H2, H2, false>(w, blockIdx.x - n_b, smem);
+}
+
+}  // namespace
+
+bool conv_s12_fwd_supported(ConvId c1, ConvId c2) { return c1 == CONV_S1 && c2 == CONV_S2; }
+
+bool conv_s12_fwd_aligned(const ConvIn& in) {
+    return ((uintptr_t)in.base & 15) == 0 && (in.stride & 15) == 0;
+}
+
+hipError_t launch_conv_s12_fwd(const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
+                               const float* w1_a, const float* b1_a, const float* w2_a,
+                               const float* b2_a, const float* w1_b, const float* b1_b,
+                               const float* w2_b, const float* b2_b, float* act1, float* act2,
+                               const SideFields* side, hipStream_t st) {
+    if (n <= 0 || !conv_s12_fwd_aligned(in_a) || !conv_s12_fwd_aligned(in_b)) return hipErrorInvalidValue;
+    for (const float* w : {w1_a, w2_a, w1_b, w2_b})
+        if (((uintptr_t)w & 15) != 0) return hipErrorInvalidValue;
+    auto kern = conv_s12_fwd_kernel;
+    if (!allow_lds((const void*)kern, LDS_BYTES)) return hipErrorInvalidValue;
+    FusedFwdParams p{in_a, in_b, n_a, n, w1_a, b1_a, w2_a, b2_a, w1_b, b1_b, w2_b, b2_b,
+                     act1, act2, side ? *side : SideFields{}};
+    hipLaunchKernelGGL(kern, dim3((unsigned)(n * NBAND)), dim3(WG), LDS_BYTES, st, p);
+    return hipGetLastError();
+}
+
+int conv_s12_bwd_slots(int batch) { return batch * NBB; }
+
+hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float* dz2, const float* w2,
+                               int batch, float* wpart2, float* bpart2, float* wpart1, float* bpart1,
+                               hipStream_t st) {
+    if (batch <= 0 || !conv_s12_fwd_aligned(in) || ((uintptr_t)w2 & 15) != 0 || ((uintptr_t)act1 & 15) != 0)
+        return hipErrorInvalidValue;
+    int n_w;
+    size_t lw;
+    const ConvIn in2{act1, nullptr, (int64_t)C1 * H1 * H1 * 4, 0};
+    const WgradParams wp = wgrad_params<C1, H1, H1, C2, K2, S2, H2, H2, false>(in2, dz2, batch, wpart2, bpart2,
+                                                                               1.f, &n_w, &lw);
+    const S1BwdParams bp{in, dz2, w2, act1, wpart1, bpart1, (float)(1.0 / 255.0)};
+    const size_t lds = std::max(lw, (size_t)B_LDS);
+    auto kern = conv_s12_bwd_kernel;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(n_w + batch * NBB)), dim3(WG), lds, st, wp, bp, batch * NBB);
+    return hipGetLastError();
+}
+
+}  // namespace dqn

@@ -126,6 +126,8 @@ def lib():
         L.dqn_train_replicas.restype = ctypes.c_int
         L.dqn_profile_attach.argtypes = [ctypes.c_int32, _P, ctypes.c_int32, ctypes.c_int32]
         L.dqn_profile_attach.restype = ctypes.c_int
+        L.dqn_profile_set_fusion.argtypes = [ctypes.c_int32]
+        L.dqn_profile_set_fusion.restype = ctypes.c_int
         L.dqn_profile_used.argtypes = [ctypes.c_int32]
         L.dqn_profile_used.restype = ctypes.c_int32
         _LIB = L
@@ -436,7 +438,7 @@ def dqn_train_replicas(net, theta_ring, opt_state, rule, lr, decay, eps, gamma, 
 KERNEL_NAMES = ["gather", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head", "fc1_wgrad",
                 "fc1_dgrad", "conv1_wgrad", "conv2_wgrad", "conv3_wgrad", "conv2_dgrad",
                 "conv3_dgrad", "finalize", "apply", "fc1_bwd", "conv2_bwd", "conv3_bwd",
-                "finalize_apply"]
+                "finalize_apply", "conv12_fwd", "conv12_bwd"]
 _ATTACHED = {}
 
 
@@ -453,6 +455,12 @@ def profile_attach(kernel: int, events, stride: int = 1) -> None:
         rc = lib().dqn_profile_attach(kernel, ctypes.cast(arr, ctypes.c_void_p), len(events) // 2,
                                       int(stride))
     _check(rc, "dqn_profile_attach")
+
+
+def profile_set_fusion(enabled: bool) -> None:
+    """Enable (default) or disable the fused two-layer conv launches of the
+    small network (include/dqn_profile.h dqn_profile_set_fusion)."""
+    _check(lib().dqn_profile_set_fusion(1 if enabled else 0), "dqn_profile_set_fusion")
 
 
 def profile_used(kernel: int) -> int:

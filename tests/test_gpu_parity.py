@@ -220,6 +220,36 @@ def test_td_gradient_matches_oracle(dev, name, B, target):
     assert_grad_close(shape, g, ref["grad"])
 
 
+@pytest.mark.parametrize("B,target", [(32, "same"), (33, "held"), (100, "held")])
+def test_td_gradient_fused_and_per_layer_conv_paths(dev, B, target):
+    """The small network's conv layers run as fused two-layer launches by
+    default and as one launch per layer and pass with fusion switched off;
+    both paths agree with the oracle, also for the greedy actions and Q of
+    dqn_forward."""
+    import torch
+    net, shape = NETS["small"]
+    th = di.xavier_theta(shape, 64 + B, bias_scale=0.05)
+    tt = None if target == "same" else di.xavier_theta(shape, 65 + B, bias_scale=0.05)
+    s, sn, a, r, t = _td_inputs(shape, B, 66 + B)
+    ref = oracle.td_gradient(shape, th, tt, s, sn, a, r, t, float(F32(0.99)))
+    fref = oracle.forward_q(shape, th, s)
+    try:
+        for fused in (True, False):
+            dq.profile_set_fusion(fused)
+            say(f"[td] small batch={B} target={target} fused={fused}")
+            g, loss, q, y = _run_td(dev, net, th, tt, s, sn, a, r, t, 0.99)
+            assert rel_l2(q, ref["q"]) <= FP32_TOL
+            assert rel_l2(y, ref["y"]) <= FP32_TOL
+            assert abs(loss - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
+            assert_grad_close(shape, g, ref["grad"])
+            qf = torch.empty((B, net.n_actions), dtype=torch.float32, device=dev)
+            dq.dqn_forward(net, dev_tensor(th), dev_tensor(s), q_out=qf)
+            torch.cuda.synchronize()
+            assert rel_l2(host(qf), fref) <= FP32_TOL
+    finally:
+        dq.profile_set_fusion(True)
+
+
 def test_td_gradient_on_replay_frames(dev, replay):
     net, shape = NETS["small"]
     B = 32
