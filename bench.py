@@ -28,8 +28,11 @@ The JSON line adds:
                 algorithmic FLOP (or bytes) per launch divided by its average
                 launch time, measured with HIP event pairs around the launches
                 of that kernel inside the timed region (every launch for the
-                large-batch configs, every tenth for configs 0 and 1), less
-                the average time of an empty event pair on the same stream;
+                large-batch configs, every tenth for configs 0 to 2), less
+                what a pair adds around a one-element fill kernel compared
+                with that kernel's per-launch time in a dependent chain (so
+                the figure includes the kernel's dispatch and drain, as a
+                rocprofv3 kernel duration does);
                 `traffic` is the HBM bytes per launch from the committed
                 rocprofv3 PMC summary (profiles/) while the kernel's source
                 is unchanged;
@@ -103,7 +106,7 @@ class HipEvents:
             self.L.hipEventDestroy(e)
 
 
-def kernel_work(shape, B, forward_only=False):
+def kernel_work(shape, B, forward_only=False, rule="sgd"):
     """Algorithmic work per launch of each kernel: {name: (flop, bytes)}.
     FLOP = 2 x multiply-adds of the dense contractions; bytes for the
     memory-bound kernels.  A TD step runs the forward on 2B samples (s under
@@ -138,9 +141,12 @@ def kernel_work(shape, B, forward_only=False):
         for l in range(1, len(dims)):
             w[f"conv{l+1}_bwd"] = (w[f"conv{l+1}_wgrad"][0] + w[f"conv{l+1}_dgrad"][0], 0)
         w["gather"] = (0, 4 * B * rec)          # read s and s', write both
-        w["apply"] = (0, 12 * P)                # SGD: read theta and g, write theta
+        # SGD reads theta and g and writes theta; RMSProp and AdaGrad also
+        # read and write their state
+        ub = 12 * P if rule == "sgd" else 20 * P
+        w["apply"] = (0, ub)
         w["finalize"] = (0, 0)
-        w["finalize_apply"] = (0, 12 * P)       # as apply, with the reductions fused
+        w["finalize_apply"] = (0, ub)           # as apply, with the reductions fused
     return w
 
 
@@ -157,6 +163,13 @@ class Profiler:
     def __init__(self, hip):
         import paper_1508_04186_amd as dq
         self.dq, self.hip = dq, hip
+        self._overhead = None
+
+    def overhead(self):
+        """Event-bracket overhead in microseconds (measured once)."""
+        if self._overhead is None:
+            self._overhead = self.empty_pair_us()
+        return self._overhead
 
     def breakdown(self, run, n, kernels):
         dq = self.dq
@@ -173,8 +186,8 @@ class Profiler:
             used = dq.profile_used(kid)
             dq.profile_attach(kid, None)
             if used:
-                out[dq.KERNEL_NAMES[kid]] = (1e3 * sum(self.hip.ms(ev[2 * j], ev[2 * j + 1])
-                                                       for j in range(used)) / used, used)
+                raw = 1e3 * sum(self.hip.ms(ev[2 * j], ev[2 * j + 1]) for j in range(used)) / used
+                out[dq.KERNEL_NAMES[kid]] = (raw - self.overhead(), used)
             self.hip.destroy(ev)
         return out
 
@@ -192,22 +205,30 @@ class Profiler:
         return us, used
 
     def empty_pair_us(self, n=200):
-        """Average time between two events recorded back to back on the
-        current stream: the bracket overhead inside every event pair."""
+        """What an event pair adds to the time of the launch it brackets: the
+        mean bracketed time of a one-element fill kernel, less that kernel's
+        per-launch time in a chain of n dependent launches (which, like a
+        rocprofv3 kernel duration, includes its dispatch and drain).  Both
+        are measured here on the current stream."""
         import torch
         stream = torch.cuda.current_stream().cuda_stream
-        ev = self.hip.create(2 * n)
+        x = torch.zeros(1, device="cuda")
         rec = self.hip.L.hipEventRecord
         rec.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         rec.restype = ctypes.c_int
+        for _ in range(20):
+            x.fill_(1.0)
+        chain_ms = time_region(torch.cuda.synchronize, lambda: [x.fill_(1.0) for _ in range(n)])
+        ev = self.hip.create(2 * n)
         torch.cuda.synchronize()
         for j in range(n):
             rec(ev[2 * j], stream)
+            x.fill_(1.0)
             rec(ev[2 * j + 1], stream)
         torch.cuda.synchronize()
         us = 1e3 * sum(self.hip.ms(ev[2 * j], ev[2 * j + 1]) for j in range(n)) / n
         self.hip.destroy(ev)
-        return us
+        return us - 1e3 * chain_ms / n
 
 
 def measured_traffic(config, name):
@@ -221,11 +242,13 @@ def measured_traffic(config, name):
         for line in open(path):
             f = line.strip().split("|")
             if len(f) == 7 and f[0] == "traffic" and f[1] == f"config {config}" and f[2] == name:
-                src = os.path.join(ROOT, "paper_1508_04186_amd", "csrc", f[5])
-                if not os.path.exists(src):
-                    return None
-                sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-                return int(f[3]) + int(f[4]) if sha == f[6] else None
+                h = hashlib.sha256()
+                for part in f[5].split("+"):
+                    src = os.path.join(ROOT, "paper_1508_04186_amd", "csrc", part)
+                    if not os.path.exists(src):
+                        return None
+                    h.update(open(src, "rb").read())
+                return int(f[3]) + int(f[4]) if h.hexdigest()[:16] == f[6] else None
     return None
 
 
@@ -351,7 +374,7 @@ def bench_single(args):
     kid, ev = prof.attach(dom, K * 4 // SAMPLE_STRIDE + 4, SAMPLE_STRIDE)
     ms = time_region(torch.cuda.synchronize, lambda: steps(K))
     raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.empty_pair_us()
+    dom_us = raw_us - prof.overhead()
     rec = base_record(K, W, ms)
     rec["config"] = {"workload": "config 0: small Q-network, one batch of 32 uniform random "
                                  "states, TD gradient + SGD step (lr 2.5e-4) repeated",
@@ -419,7 +442,7 @@ def bench_sequential(args):
     kid, ev = prof.attach(dom, K * 4 // SAMPLE_STRIDE + 4, SAMPLE_STRIDE)
     ms = time_region(torch.cuda.synchronize, lambda: run(W, total))
     raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.empty_pair_us()
+    dom_us = raw_us - prof.overhead()
     final_loss = float(losses[total - 1].item())
     log(f"timed {K} steps in {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
 
@@ -517,16 +540,25 @@ def bench_replicas(args):
 
     run(W)
     torch.cuda.synchronize()
+    hip = HipEvents()
+    prof = Profiler(hip)
+    work = kernel_work(shape, B, rule="adagrad")
+    nb = min(args.breakdown_steps, U)
+    bd = prof.breakdown(lambda: run(nb), nb, list(work))
+    dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
     # timed: all U updates from the initial parameters (the setup copies
     # above are outside the region)
     ring[:P].copy_(torch.from_numpy(th0).to(dev))
     G.zero_()
+    kid, ev = prof.attach(dom, U * 4 // SAMPLE_STRIDE + 4, SAMPLE_STRIDE)
     e0 = time.perf_counter()
     ms = time_region(torch.cuda.synchronize,
                      lambda: dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA,
                                                    rp, idx, R, S, hs.handles, losses_out=losses,
                                                    ws=ws))
     host_s = time.perf_counter() - e0
+    raw_us, used = prof.collect(kid, ev)
+    dom_us = raw_us - prof.overhead()
     final_loss = float(losses[U - 1].item())
     hs.close()
     log(f"timed {U} updates in {ms:.1f} ms (host enqueue+wait {host_s * 1e3:.1f} ms)")
@@ -562,8 +594,12 @@ def bench_replicas(args):
         "parallelism": "16 replicas + 1 server on one GPU (streams)"}
     out["transitions_per_s"] = round(out["value"] * B, 1)
     out["final_loss"] = final_loss
-    out["roofline"] = None
-    out["breakdown"] = {"T_us": round(T_us, 2), "tau_us": round(tau_us, 2),
+    out["roofline"] = roofline(work, dom, dom_us, used, 1, raw_us, "2")
+    out["roofline"]["note"] = ("kernels of up to five updates run concurrently on the replica "
+                               "streams, so the event-bracketed launch time includes sharing "
+                               "the GPU with them")
+    out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
+                        "T_us": round(T_us, 2), "tau_us": round(tau_us, 2),
                         "T_over_tau": round(T_us / tau_us, 2),
                         "server_bound_updates_per_s": round(1e6 / tau_us, 1)}
     if not args.no_cpu_baseline:
@@ -643,7 +679,7 @@ def bench_large(args):
     kid, ev = prof.attach(dom, K * 4)
     ms = time_region(torch.cuda.synchronize, lambda: run(W, total))
     raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.empty_pair_us()
+    dom_us = raw_us - prof.overhead()
     final_loss = float(losses[total - 1].item())
     log(f"timed {K} steps in {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
     out = base_record(K, W, ms)
@@ -719,7 +755,7 @@ def bench_forward(args):
     kid, ev = prof.attach(dom, K * 4)
     ms = time_region(torch.cuda.synchronize, lambda: run(W, K + W))
     raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.empty_pair_us()
+    dom_us = raw_us - prof.overhead()
     log(f"timed {K} forward passes in {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
     out = base_record(K, W, ms)
     out["config"] = {
