@@ -191,78 +191,150 @@ __global__ __launch_bounds__(WG) void conv_s12_fwd_kernel(FusedFwdParams p) {
 
     // ---- conv1: band-local pixels 16*mt + li (row = p / H1, x = p % H1),
     // contraction k = c*64 + ky*8 + kx; k-step kb covers c = kb/2 and
-    // ky = 4*(kb%2) + g, kx = 0..7 in lane group g.
+    // ky = 4*(kb%2) + g, kx = 0..7 in lane group g.  Wave w owns M-tiles
+    // w, w+4, w+8 (below MT1) and runs them together, so their accumulator
+    // chains are independent and share the B operands.
     const int y1 = band * R2 * S2;             // first conv1 row of the band
     const int own0 = band == 0 ? 0 : y1 + (K2 - S2);
     const int own1 = band == NBAND - 1 ? H1 : y1 + R2 * S2 + (K2 - S2);
     constexpr int MT1 = R1 * H1 / 16;
+    constexpr int TPW = (MT1 + 3) / 4;         // M-tiles per wave, at most
     float* a1g = p.act1 + (size_t)n * C1 * H1 * H1;
-    for (int mt = wave; mt < MT1; mt += 4) {
-        const int pa = mt * 16 + li;
-        const int ra = pa / H1, xa = pa - ra * H1;
-        f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+    {
+        // Every wave runs TPW tiles; a wave with fewer repeats its last one
+        // and discards the copy, so the loop has no per-tile branches.
+        const int ntile = (MT1 - wave + 3) / 4;  // this wave's tiles (uniform)
+        int abase[TPW];
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) {
+            const int mt = wave + 4 * min(i, ntile - 1);
+            const int pa = mt * 16 + li;
+            const int ra = pa / H1, xa = pa - ra * H1;
+            abase[i] = S1 * ra * H0 + S1 * xa;
+        }
+        f4 acc[TPW];
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        // operands of k-step kb; the next step's are loaded before this
+        // step's MFMAs issue
+        auto load_a = [&](int kb, bf16x8 (&a)[TPW]) {
+            const int c = kb >> 1, ky = (kb & 1) * 4 + g;
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) {
+                const __bf16* ap = s_in + (c * R0 + ky) * H0 + abase[i];
+                const bf16x4 a0 = *(const bf16x4*)ap;
+                const bf16x4 a1 = *(const bf16x4*)(ap + 4);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    a[i][q] = a0[q];
+                    a[i][4 + q] = a1[q];
+                }
+            }
+        };
+        auto load_b = [&](int kb, bf16x8 (&b)[3]) {
+#pragma unroll
+            for (int part = 0; part < 3; ++part)
+                b[part] = *(const bf16x8*)(s_w1 + (part * C1 + li) * RS1 + kb * 32 + 8 * g);
+        };
+        bf16x8 a[2][TPW], b[2][3];
+        load_a(0, a[0]);
+        load_b(0, b[0]);
 #pragma unroll
         for (int kb = 0; kb < KW1 / 32; ++kb) {
-            const int c = kb >> 1, ky = (kb & 1) * 4 + g;
-            const __bf16* ap = s_in + (c * R0 + S1 * ra + ky) * H0 + S1 * xa;
-            bf16x8 a;
-            const bf16x4 a0 = *(const bf16x4*)ap;
-            const bf16x4 a1 = *(const bf16x4*)(ap + 4);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                a[i] = a0[i];
-                a[4 + i] = a1[i];
+            const int cur = kb & 1;
+            if (kb + 1 < KW1 / 32) {
+                load_a(kb + 1, a[cur ^ 1]);
+                load_b(kb + 1, b[cur ^ 1]);
             }
 #pragma unroll
-            for (int part = 0; part < 3; ++part) {
-                const bf16x8 b = *(const bf16x8*)(s_w1 + (part * C1 + li) * RS1 + kb * 32 + 8 * g);
-                acc = mfma16x16x32bf16(a, b, acc);
-            }
+            for (int part = 0; part < 3; ++part)
+#pragma unroll
+                for (int i = 0; i < TPW; ++i) acc[i] = mfma16x16x32bf16(a[cur][i], b[cur][part], acc[i]);
         }
         // lane holds pixels 16*mt + 4g + r (one row: H1 is a multiple of 4)
         // of channel o = li
-        const int pb = mt * 16 + 4 * g;
-        const int rb = pb / H1, xb = pb - rb * H1;
         const float bo = s_b[li];
         constexpr float inv255 = (float)(1.0 / 255.0);
-        f4 v;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[r] * inv255 + bo, 0.f);
-        *(f4*)(s_a1 + li * A1C + rb * H1 + xb) = v;
-        const int yg = y1 + rb;
-        if (yg >= own0 && yg < own1) *(f4*)(a1g + ((size_t)li * H1 + yg) * H1 + xb) = v;
+        for (int i = 0; i < TPW; ++i) {
+            if (i < ntile) {
+                const int pb = (wave + 4 * i) * 16 + 4 * g;
+                const int rb = pb / H1, xb = pb - rb * H1;
+                f4 v;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[i][r] * inv255 + bo, 0.f);
+                *(f4*)(s_a1 + li * A1C + rb * H1 + xb) = v;
+                const int yg = y1 + rb;
+                if (yg >= own0 && yg < own1) *(f4*)(a1g + ((size_t)li * H1 + yg) * H1 + xb) = v;
+            }
+        }
     }
     __syncthreads();
 
-    // ---- conv2: wave w takes M-tile w/2 (band-local pixels) and N-tile w%2;
-    // lane group g takes channel 4*cb + g; steps walk (cb, ky, kx).
+    // ---- conv2: wave w takes input channels 4w..4w+3 (lane group g takes
+    // channel 4w + g) for both M-tiles (band-local pixels) and both N-tiles,
+    // four independent accumulators; steps walk (ky, kx).  The four waves'
+    // partial sums are then added in wave order through LDS (the input tile
+    // is no longer needed).
     {
         constexpr int P2 = R2 * H2;
-        const int mt = wave >> 1, nt = wave & 1;
-        const int pp = mt * 16 + li;
-        const int pc = pp < P2 ? pp : P2 - 1;
-        const int oy = pc / H2, ox = pc - (pc / H2) * H2;
-        const float amask = pp < P2 ? 1.f : 0.f;
-        f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+        constexpr int MT2 = (P2 + 15) / 16, NT2 = C2 / 16;
+        static_assert(C1 / 4 == 4, "one channel block per wave");
+        static_assert(MT2 * NT2 * 4 * 64 * 4 * 4 <= C0 * R0 * H0 * 2, "partials must fit the input tile");
+        int arow[MT2];
+        float amask[MT2];
 #pragma unroll
-        for (int cb = 0; cb < C1 / 4; ++cb) {
-            const int c = cb * 4 + g;
+        for (int m = 0; m < MT2; ++m) {
+            const int pp = m * 16 + li;
+            const int pc = pp < P2 ? pp : P2 - 1;
+            const int oy = pc / H2, ox = pc - (pc / H2) * H2;
+            arow[m] = S2 * oy * H1 + S2 * ox;
+            amask[m] = pp < P2 ? 1.f : 0.f;
+        }
+        const int c = wave * 4 + g;
+        f4 acc[MT2][NT2];
 #pragma unroll
-            for (int ky = 0; ky < K2; ++ky) {
-                const float* ar = s_a1 + c * A1C + (S2 * oy + ky) * H1 + S2 * ox;
-                const float* wp = s_w2 + (nt * 16 + li) * RO2 + c * RC2 + ky * K2;
+        for (int m = 0; m < MT2; ++m)
 #pragma unroll
-                for (int kx = 0; kx < K2; ++kx) acc = mfma16x16x4(ar[kx] * amask, wp[kx], acc);
+            for (int nt = 0; nt < NT2; ++nt) acc[m][nt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ky = 0; ky < K2; ++ky) {
+#pragma unroll
+            for (int kx = 0; kx < K2; ++kx) {
+                float a[MT2], b[NT2];
+#pragma unroll
+                for (int m = 0; m < MT2; ++m) a[m] = s_a1[c * A1C + arow[m] + ky * H1 + kx] * amask[m];
+#pragma unroll
+                for (int nt = 0; nt < NT2; ++nt) b[nt] = s_w2[(nt * 16 + li) * RO2 + c * RC2 + ky * K2 + kx];
+#pragma unroll
+                for (int m = 0; m < MT2; ++m)
+#pragma unroll
+                    for (int nt = 0; nt < NT2; ++nt) acc[m][nt] = mfma16x16x4(a[m], b[nt], acc[m][nt]);
             }
         }
-        const int o = nt * 16 + li;
-        const float bo = s_b[C1 + o];
-        float* a2 = p.act2 + ((size_t)n * C2 + o) * H2 * H2 + band * R2 * H2;
+        f4* part = (f4*)(smem + OFF_IN);  // [wave][m][nt][lane]
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int q = mt * 16 + 4 * g + r;
-            if (q < P2) a2[q] = fmaxf(acc[r] + bo, 0.f);
+        for (int m = 0; m < MT2; ++m)
+#pragma unroll
+            for (int nt = 0; nt < NT2; ++nt) part[((wave * MT2 + m) * NT2 + nt) * 64 + lane] = acc[m][nt];
+        __syncthreads();
+        // thread t finishes (m, nt) tile t / 64 for lane t % 64
+        {
+            const int tile = t >> 6, ln = t & 63;
+            const int m = tile / NT2, nt = tile - m * NT2;
+            f4 sum = part[((0 * MT2 + m) * NT2 + nt) * 64 + ln];
+#pragma unroll
+            for (int w = 1; w < 4; ++w) sum += part[((w * MT2 + m) * NT2 + nt) * 64 + ln];
+            const int o = nt * 16 + (ln & 15);
+            const float bo = s_b[C1 + o];
+            float* a2 = p.act2 + ((size_t)n * C2 + o) * H2 * H2 + band * R2 * H2;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int q = m * 16 + 4 * (ln >> 4) + r;
+                if (q < P2) a2[q] = fmaxf(sum[r] + bo, 0.f);
+            }
         }
+        static_assert(MT2 * NT2 * 64 == WG, "one thread per output lane of the band");
     }
 }
 
@@ -402,39 +474,58 @@ __device__ __forceinline__ void s1_bwd_body(const S1BwdParams& p, int bid, unsig
     // (y0 + py + 2*qr, px + 2*qc) receive W2[o][c][py+2ty][px+2tx] *
     // dz2[o][y/2 - ty][qc - tx]; contraction over (o, ty, tx), lane group g
     // taking o = 4*ob + g.  M = phase pixels, N = the 16 conv1 channels.
+    // Tiles (phase, M-tile) tt = wave + 4i are run together by wave `wave`,
+    // so their accumulator chains are independent.
     {
-        const int nrp = nr / 2;
-        const int pp = nrp * (H1 / 2);         // pixels per phase
-        const int mtp = (pp + 15) / 16;
-        for (int tt = wave; tt < 4 * mtp; tt += 4) {
-            const int ph = tt / mtp, mt = tt - ph * mtp;
-            const int py = ph >> 1, px = ph & 1;
+        constexpr int NRP = NRMAX / 2;
+        constexpr int PP = NRP * (H1 / 2);      // pixels per phase
+        constexpr int MTP = (PP + 15) / 16;
+        constexpr int TW = MTP;                 // tiles per wave (4 phases x MTP / 4 waves)
+        int zoff[TW], py[TW], px[TW];
+        float amask[TW];
+#pragma unroll
+        for (int i = 0; i < TW; ++i) {
+            const int tt = wave + 4 * i;
+            const int ph = tt / MTP, mt = tt - ph * MTP;
+            py[i] = ph >> 1;
+            px[i] = ph & 1;
             const int q = mt * 16 + li;
-            const int qv = q < pp ? q : pp - 1;
+            const int qv = q < PP ? q : PP - 1;
             const int qr = qv / (H1 / 2), qc = qv - qr * (H1 / 2);
-            const float amask = q < pp ? 1.f : 0.f;
-            f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+            zoff[i] = (qr + 1) * NZC + qc + 1;
+            amask[i] = q < PP ? 1.f : 0.f;
+        }
+        f4 acc[TW];
 #pragma unroll
-            for (int ob = 0; ob < C2 / 4; ++ob) {
-                const int o = ob * 4 + g;
+        for (int i = 0; i < TW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ty = 0; ty < T2; ++ty)
+        for (int ob = 0; ob < C2 / 4; ++ob) {
+            const int o = ob * 4 + g;
 #pragma unroll
-                    for (int tx = 0; tx < T2; ++tx) {
-                        const float a = s_dz[(o * NZR + qr - ty + 1) * NZC + qc - tx + 1] * amask;
-                        const int tap = (py + S2 * ty) * K2 + px + S2 * tx;
-                        acc = mfma16x16x4(a, s_w[(tap * C2 + o) * RCW + li], acc);
+            for (int ty = 0; ty < T2; ++ty)
+#pragma unroll
+                for (int tx = 0; tx < T2; ++tx)
+#pragma unroll
+                    for (int i = 0; i < TW; ++i) {
+                        const float a = s_dz[o * NZR * NZC + zoff[i] - ty * NZC - tx] * amask[i];
+                        const int tap = (py[i] + S2 * ty) * K2 + px[i] + S2 * tx;
+                        acc[i] = mfma16x16x4(a, s_w[(tap * C2 + o) * RCW + li], acc[i]);
                     }
-            }
+        }
+#pragma unroll
+        for (int i = 0; i < TW; ++i) {
+            const int tt = wave + 4 * i;
+            const int mt = tt - (tt / MTP) * MTP;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int qq = mt * 16 + 4 * g + r;
-                if (qq < pp) {
-                    const int lp = (py + 2 * (qq / (H1 / 2))) * H1 + px + 2 * (qq % (H1 / 2));
-                    s_d1[li * LD1 + lp] = s_mask[li * NRMAX * H1 + lp] > 0.f ? acc[r] : 0.f;
+                if (qq < PP) {
+                    const int lp = (py[i] + 2 * (qq / (H1 / 2))) * H1 + px[i] + 2 * (qq % (H1 / 2));
+                    s_d1[li * LD1 + lp] = s_mask[li * NRMAX * H1 + lp] > 0.f ? acc[i][r] : 0.f;
                 }
             }
         }
+        static_assert(4 * MTP % 4 == 0, "phase tiles split evenly over the waves");
     }
     __syncthreads();
 
