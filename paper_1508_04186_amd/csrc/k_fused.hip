@@ -356,9 +356,8 @@ constexpr int BOFF_W = BOFF_DZ + C2 * NZR * NZC * 4;        // f32 [KK2][C2][RCW
 constexpr int BOFF_MASK = BOFF_W + KK2 * C2 * RCW * 4;      // f32 [C1][NRMAX*H1]
 constexpr int BOFF_D1 = BOFF_MASK + C1 * NRMAX * H1 * 4;    // f32 [C1][LD1]
 constexpr int BOFF_IN = BOFF_D1 + C1 * LD1 * 4;             // u8 [C0][RIN][H0]
-constexpr int BOFF_POFF = BOFF_IN + C0 * RIN * H0;          // int [NRMAX*H1]
-constexpr int B_LDS = BOFF_POFF + NRMAX * H1 * 4;
-static_assert(BOFF_MASK % 16 == 0 && BOFF_IN % 16 == 0 && BOFF_POFF % 16 == 0, "alignment");
+constexpr int B_LDS = BOFF_IN + C0 * RIN * H0;
+static_assert(BOFF_MASK % 16 == 0 && BOFF_IN % 16 == 0, "alignment");
 
 struct S1BwdParams {
     ConvIn in;            // network input of the B samples (bytes)
@@ -377,7 +376,6 @@ __device__ __forceinline__ void s1_bwd_body(const S1BwdParams& p, int bid, unsig
     float* s_mask = (float*)(smem + BOFF_MASK);
     float* s_d1 = (float*)(smem + BOFF_D1);
     unsigned char* s_in = smem + BOFF_IN;
-    int* s_poff = (int*)(smem + BOFF_POFF);
 
     const int band = bid % NBB;
     const int j = bid / NBB;
@@ -461,10 +459,6 @@ __device__ __forceinline__ void s1_bwd_body(const S1BwdParams& p, int bid, unsig
             *(f4*)(s_in + c * RIN * H0 + 16 * r) = vi[u];
         }
     }
-    for (int q = t; q < npx; q += WG) {
-        const int y = q / H1, x = q - (q / H1) * H1;
-        s_poff[q] = S1 * y * H0 + S1 * x;
-    }
     __syncthreads();
 
     const int lane = t & 63, wave = t >> 6;
@@ -498,19 +492,45 @@ __device__ __forceinline__ void s1_bwd_body(const S1BwdParams& p, int bid, unsig
         f4 acc[TW];
 #pragma unroll
         for (int i = 0; i < TW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        // Per (tile, tap) base addresses, fixed for the loop: inside it, the
+        // output-channel step ob only adds compile-time offsets (the LDS
+        // reads' immediate offsets).
+        constexpr int NTAP = T2 * T2;
+        int zb[TW][NTAP], wb[TW][NTAP];
 #pragma unroll
-        for (int ob = 0; ob < C2 / 4; ++ob) {
-            const int o = ob * 4 + g;
+        for (int i = 0; i < TW; ++i)
 #pragma unroll
             for (int ty = 0; ty < T2; ++ty)
 #pragma unroll
-                for (int tx = 0; tx < T2; ++tx)
+                for (int tx = 0; tx < T2; ++tx) {
+                    const int tap = (py[i] + S2 * ty) * K2 + px[i] + S2 * tx;
+                    zb[i][ty * T2 + tx] = g * NZR * NZC + zoff[i] - ty * NZC - tx;
+                    wb[i][ty * T2 + tx] = (tap * C2 + g) * RCW + li;
+                }
+        // Double-buffered operands; the scheduling barriers keep the next
+        // step's LDS reads ahead of this step's MFMAs (one wave per SIMD
+        // has nothing else to hide LDS latency with).
+        float a[2][TW][NTAP], b[2][TW][NTAP];
+        auto load = [&](int ob, float (&av)[TW][NTAP], float (&bv)[TW][NTAP]) {
 #pragma unroll
-                    for (int i = 0; i < TW; ++i) {
-                        const float a = s_dz[o * NZR * NZC + zoff[i] - ty * NZC - tx] * amask[i];
-                        const int tap = (py[i] + S2 * ty) * K2 + px[i] + S2 * tx;
-                        acc[i] = mfma16x16x4(a, s_w[(tap * C2 + o) * RCW + li], acc[i]);
-                    }
+            for (int i = 0; i < TW; ++i)
+#pragma unroll
+                for (int k = 0; k < NTAP; ++k) {
+                    av[i][k] = s_dz[zb[i][k] + ob * 4 * NZR * NZC];
+                    bv[i][k] = s_w[wb[i][k] + ob * 4 * RCW];
+                }
+        };
+        load(0, a[0], b[0]);
+#pragma unroll
+        for (int ob = 0; ob < C2 / 4; ++ob) {
+            const int cur = ob & 1;
+            if (ob + 1 < C2 / 4) load(ob + 1, a[cur ^ 1], b[cur ^ 1]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int k = 0; k < NTAP; ++k)
+#pragma unroll
+                for (int i = 0; i < TW; ++i) acc[i] = mfma16x16x4(a[cur][i][k] * amask[i], b[cur][i][k], acc[i]);
+            __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
         for (int i = 0; i < TW; ++i) {
@@ -545,13 +565,24 @@ __device__ __forceinline__ void s1_bwd_body(const S1BwdParams& p, int bid, unsig
         f4 acc[NTW];
 #pragma unroll
         for (int i = 0; i < NTW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-        for (int st = 0; st < npx / 4; ++st) {
-            const int lp = 4 * st + g;
-            const float a = s_d1[li * LD1 + lp];
-            const int po = s_poff[lp];
+        // Pixel step st covers band pixels 4*st .. 4*st+3 (one per lane
+        // group g), all in conv1 row (4*st)/H1 since H1 is a multiple of 4:
+        // the addresses are a per-lane base plus compile-time offsets.
+        constexpr int NST = NRMAX * H1 / 4;
+        static_assert(H1 % 4 == 0, "a pixel step stays in one row");
+        const int abase = li * LD1 + g;
+        int bbase[NTW];
 #pragma unroll
-            for (int i = 0; i < NTW; ++i) acc[i] = mfma16x16x4(a, (float)s_in[koff[i] + po], acc[i]);
+        for (int i = 0; i < NTW; ++i) bbase[i] = koff[i] + S1 * g;
+#pragma unroll
+        for (int st = 0; st < NST; ++st) {
+            const int y = (4 * st) / H1, x0 = (4 * st) % H1;
+            const float a = s_d1[abase + 4 * st];
+            float b[NTW];
+#pragma unroll
+            for (int i = 0; i < NTW; ++i) b[i] = (float)s_in[bbase[i] + S1 * y * H0 + S1 * x0];
+#pragma unroll
+            for (int i = 0; i < NTW; ++i) acc[i] = mfma16x16x4(a, b[i], acc[i]);
         }
 #pragma unroll
         for (int i = 0; i < NTW; ++i) {
