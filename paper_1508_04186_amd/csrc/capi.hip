@@ -81,6 +81,10 @@ constexpr int kPairMaxBatch = 64;
 // samples per launch, and by 2x at 64).
 constexpr int kFuseMaxRows = 1 << 20;
 bool g_fusion = true;  // dqn_profile_set_fusion
+// Samples per forward launch from which the large network's fp32 conv layers
+// run as one implicit GEMM over all samples (2-3x the per-layer kernel from
+// 256 samples; slower at 64).
+constexpr int kIgemmMinRows = 128;
 
 // fc1 forward split-K: enough slices that the launch covers the chip.
 struct Carver {
@@ -263,6 +267,12 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
                                 tt + ni.b_off[1], t.act[0], t.act[1], src.replay ? &side : nullptr, st));
     for (int l = 0; l < L && !fused_fwd; ++l) {
         const int64_t ae = l > 0 ? act_elems(ni.d[l - 1]) : 0;
+        if (l > 0 && conv_igemm_fwd_supported(ni.conv[l]) && 2 * B >= kIgemmMinRows) {
+            RUN(DQN_K_CONV1_FWD + l,
+                launch_conv_igemm_fwd(ni.conv[l], t.act[l - 1], B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
+                                      tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], st));
+            continue;
+        }
         const ConvIn in_a = l == 0 ? s0 : ConvIn{t.act[l - 1], nullptr, ae * 4, 0};
         const ConvIn in_b = l == 0 ? sn0 : ConvIn{t.act[l - 1] + (int64_t)B * ae, nullptr, ae * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
@@ -506,6 +516,12 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
                                 th + ni.w_off[1], th + ni.b_off[1], th + ni.w_off[0], th + ni.b_off[0],
                                 th + ni.w_off[1], th + ni.b_off[1], f.act[0], f.act[1], nullptr, st));
     for (int l = 0; l < ni.n_conv && !fused_fwd; ++l) {
+        if (l > 0 && conv_igemm_fwd_supported(ni.conv[l]) && batch >= kIgemmMinRows) {
+            RUN(DQN_K_CONV1_FWD + l,
+                launch_conv_igemm_fwd(ni.conv[l], f.act[l - 1], batch, batch, th + ni.w_off[l], th + ni.b_off[l],
+                                      th + ni.w_off[l], th + ni.b_off[l], f.act[l], st));
+            continue;
+        }
         const ConvIn in = l == 0 ? in0
                                  : ConvIn{f.act[l - 1], nullptr, act_elems(ni.d[l - 1]) * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;

@@ -128,6 +128,15 @@ hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float*
                                int batch, float* wpart2, float* bpart2, float* wpart1, float* bpart1,
                                hipStream_t st);
 
+// Forward of the fp32-input large-network layers (CONV_L2, CONV_L3) as one
+// implicit GEMM over all n samples (dense input [n][cin][ih][iw]; samples
+// below n_a use (w_a, b_a), the rest (w_b, b_b)); bias + ReLU; output
+// [n][cout][oh][ow].  Weights 16-byte aligned.
+bool conv_igemm_fwd_supported(ConvId id);
+hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, const float* w_a,
+                                 const float* b_a, const float* w_b, const float* b_b, float* out,
+                                 hipStream_t st);
+
 // Weight and bias gradient partial sums over sample chunks:
 // wpart [chunks][cout][cin*k*k], bpart [chunks][cout].
 int conv_wgrad_chunks(ConvId id, int batch);
