@@ -86,6 +86,12 @@ bool g_fusion = true;  // dqn_profile_set_fusion
 // 256 samples; slower at 64).
 constexpr int kIgemmMinRows = 128;
 
+// Backward layers that run as implicit GEMMs at batch B (measured faster
+// than the per-layer kernels from 128 samples: the weight gradients of
+// conv2/conv3 and the input gradient of conv3 of the large network).
+bool igemm_wgrad(ConvId id, int B) { return (id == CONV_L2 || id == CONV_L3) && B >= kIgemmMinRows; }
+bool igemm_dgrad(ConvId id, int B) { return id == CONV_L3 && B >= kIgemmMinRows; }
+
 // fc1 forward split-K: enough slices that the launch covers the chip.
 struct Carver {
     size_t off = 0;
@@ -135,6 +141,7 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
         int64_t slots = t.chunks[l];
         if (l == 0 && ni.n_conv == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]))
             slots = std::max<int64_t>(slots, conv_s12_bwd_slots(B));
+        if (igemm_wgrad(ni.conv[l], B)) slots = std::max<int64_t>(slots, conv_igemm_wgrad_chunks(ni.conv[l], B));
         t.wpart[l] = cv.take<float>(ws, slots * c.cout * c.cin * c.k * c.k);
         t.bpart[l] = cv.take<float>(ws, slots * c.cout);
     }
@@ -339,7 +346,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // band of conv1 rows).
     const bool fused_bwd = g_fusion && L == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
                            B <= kFuseMaxRows && conv_s12_fwd_aligned(s0);
-    int chunks0 = t.chunks[0];
+    int chunks_used[3] = {t.chunks[0], t.chunks[1], t.chunks[2]};
+    int& chunks0 = chunks_used[0];
     if (fused_bwd) {
         RUN(DQN_K_CONV12_BWD,
             launch_conv_s12_bwd(s0, t.act[0], t.dconv[1], th + ni.w_off[1], B, t.wpart[1], t.bpart[1],
@@ -355,9 +363,19 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
                                 th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], st));
             continue;
         }
-        RUN(DQN_K_CONV1_WGRAD + l,
-            launch_conv_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
-        if (l > 0)
+        if (igemm_wgrad(ni.conv[l], B)) {
+            RUN(DQN_K_CONV1_WGRAD + l,
+                launch_conv_igemm_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
+            chunks_used[l] = conv_igemm_wgrad_chunks(ni.conv[l], B);
+        } else {
+            RUN(DQN_K_CONV1_WGRAD + l,
+                launch_conv_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
+        }
+        if (l > 0 && igemm_dgrad(ni.conv[l], B))
+            RUN(DQN_K_CONV2_DGRAD + (l - 1),
+                launch_conv_igemm_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],
+                                        t.dconv[l - 1], B, st));
+        else if (l > 0)
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
                 launch_conv_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],
                                   t.dconv[l - 1], B, st));
@@ -368,7 +386,7 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
         const ConvDims& c = ni.d[l];
         fa.wpart[l] = t.wpart[l];
         fa.bpart[l] = t.bpart[l];
-        fa.chunks[l] = l == 0 ? chunks0 : t.chunks[l];
+        fa.chunks[l] = chunks_used[l];
         fa.wcount[l] = c.cout * c.cin * c.k * c.k;
         fa.cout[l] = c.cout;
         fa.gw[l] = grad_out + ni.w_off[l];

@@ -137,6 +137,19 @@ hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, con
                                  const float* b_a, const float* w_b, const float* b_b, float* out,
                                  hipStream_t st);
 
+// Input gradient of CONV_L2 / CONV_L3 for n samples as an implicit GEMM per
+// stride phase, masked by [h_in > 0] (as launch_conv_dgrad).
+hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, const float* h_in, float* din,
+                                   int n, hipStream_t st);
+
+// Weight/bias gradient partial sums of a large-network layer for n samples as
+// an implicit GEMM over pixel chunks: conv_igemm_wgrad_chunks(id, n) slots of
+// wpart [slots][cout][cin*k*k] and bpart [slots][cout].  in: the layer input
+// (bytes for CONV_L1, addressed through in.idx when set; floats otherwise).
+int conv_igemm_wgrad_chunks(ConvId id, int n);
+hipError_t launch_conv_igemm_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
+                                   float* bpart, float in_scale, hipStream_t st);
+
 // Weight and bias gradient partial sums over sample chunks:
 // wpart [chunks][cout][cin*k*k], bpart [chunks][cout].
 int conv_wgrad_chunks(ConvId id, int batch);
