@@ -274,6 +274,14 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
                                 tt + ni.b_off[1], t.act[0], t.act[1], src.replay ? &side : nullptr, st));
     for (int l = 0; l < L && !fused_fwd; ++l) {
         const int64_t ae = l > 0 ? act_elems(ni.d[l - 1]) : 0;
+        if (l == 0 && ni.conv[0] == CONV_L1 && 2 * B >= kIgemmMinRows && conv_s12_fwd_aligned(s0) &&
+            conv_s12_fwd_aligned(sn0)) {
+            RUN(DQN_K_CONV1_FWD,
+                launch_conv1_u8_fwd(CONV_L1, s0, sn0, B, 2 * B, th + ni.w_off[0], th + ni.b_off[0],
+                                    tt + ni.w_off[0], tt + ni.b_off[0], t.act[0],
+                                    src.replay ? &side : nullptr, st));
+            continue;
+        }
         if (l > 0 && conv_igemm_fwd_supported(ni.conv[l]) && 2 * B >= kIgemmMinRows) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], t.act[l - 1], B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
@@ -534,6 +542,12 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
                                 th + ni.w_off[1], th + ni.b_off[1], th + ni.w_off[0], th + ni.b_off[0],
                                 th + ni.w_off[1], th + ni.b_off[1], f.act[0], f.act[1], nullptr, st));
     for (int l = 0; l < ni.n_conv && !fused_fwd; ++l) {
+        if (l == 0 && ni.conv[0] == CONV_L1 && batch >= kIgemmMinRows && conv_s12_fwd_aligned(in0)) {
+            RUN(DQN_K_CONV1_FWD,
+                launch_conv1_u8_fwd(CONV_L1, in0, in0, batch, batch, th + ni.w_off[0], th + ni.b_off[0],
+                                    th + ni.w_off[0], th + ni.b_off[0], f.act[0], nullptr, st));
+            continue;
+        }
         if (l > 0 && conv_igemm_fwd_supported(ni.conv[l]) && batch >= kIgemmMinRows) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], f.act[l - 1], batch, batch, th + ni.w_off[l], th + ni.b_off[l],

@@ -150,6 +150,14 @@ int conv_igemm_wgrad_chunks(ConvId id, int n);
 hipError_t launch_conv_igemm_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
                                    float* bpart, float in_scale, hipStream_t st);
 
+// conv1 forward on byte input (CONV_L1 or CONV_S1) for many samples, on bf16
+// MFMA with an exact three-term split of the fp32 weights; roles and
+// alignment as launch_conv_s12_fwd; output [n][cout][20][20].
+bool conv1_u8_fwd_supported(ConvId id);
+hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
+                               const float* w_a, const float* b_a, const float* w_b, const float* b_b,
+                               float* out, const SideFields* side, hipStream_t st);
+
 // Weight and bias gradient partial sums over sample chunks:
 // wpart [chunks][cout][cin*k*k], bpart [chunks][cout].
 int conv_wgrad_chunks(ConvId id, int batch);

@@ -660,3 +660,190 @@ hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float*
 }
 
 }  // namespace dqn
+
+// ---------------------------------------------------------------------------
+// conv1 forward on byte input (4 channels 84x84, 8x8 stride 4 -> 20x20) for
+// many samples: a workgroup splits its weights into three bf16 planes once
+// (exact, as above), then walks its samples with the next sample's bytes
+// loaded into registers while the current one is computed.  Each wave runs
+// its M-tiles (16 pixels) for every N-tile as independent accumulator
+// chains; the A operand is converted from the staged bytes as it is built.
+namespace dqn {
+namespace {
+
+struct U8FwdParams {
+    ConvIn in_a, in_b;
+    int n_a, n, spb, blocks_a;   // samples per workgroup; workgroups of set a
+    const float *w_a, *b_a, *w_b, *b_b;
+    float* out;                  // [n][COUT][20][20]
+    SideFields side;
+};
+
+template <int COUT>
+__global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
+    constexpr int REC = C0 * H0 * H0;            // bytes per sample (28,224)
+    constexpr int RV = REC / 16;                 // 16-byte units (1,764)
+    constexpr int RPER = (RV + WG - 1) / WG;     // per thread (7)
+    constexpr int NT = COUT / 16;
+    constexpr int MT = H1 * H1 / 16;             // 25 M-tiles per sample
+    constexpr int MPW = (MT + 3) / 4;            // M-tiles per wave, at most (7)
+    constexpr int PL = COUT * RS1;               // bf16 per weight plane
+    static_assert(REC % 16 == 0 && (H1 * H1) % 16 == 0, "whole tiles");
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* s_in = smem;                  // u8 [REC]
+    __bf16* s_w = (__bf16*)(smem + ((REC + 15) / 16) * 16);  // bf16 [3][COUT][RS1]
+    float* s_b = (float*)(s_w + 3 * PL);
+
+    const bool second = (int)blockIdx.x >= p.blocks_a;
+    const int blk = second ? (int)blockIdx.x - p.blocks_a : (int)blockIdx.x;
+    const int j0 = (second ? p.n_a : 0) + blk * p.spb;
+    const int j1 = min(second ? p.n : p.n_a, j0 + p.spb);
+    const float* W = second ? p.w_b : p.w_a;
+    const float* bias = second ? p.b_b : p.b_a;
+    const int t = threadIdx.x;
+
+    if (p.side.idx && blockIdx.x == 0) {
+        for (int j = t; j < p.side.batch; j += WG) {
+            const int64_t i = p.side.idx[j];
+            p.side.a_out[j] = p.side.action[i];
+            p.side.r_out[j] = (float)p.side.reward[i];
+            p.side.t_out[j] = p.side.terminal[i];
+        }
+    }
+    if (j0 >= j1) return;  // uniform
+
+    auto sample_src = [&](int j) -> const f4* {
+        return (const f4*)(j < p.n_a ? sample_ptr(p.in_a, j) : sample_ptr(p.in_b, j - p.n_a));
+    };
+    f4 vin[RPER];
+    auto load_in = [&](int j) {
+        const f4* src = sample_src(j);
+#pragma unroll
+        for (int u = 0; u < RPER; ++u) {
+            const int e = t + u * WG;
+            if (e < RV) vin[u] = src[e];
+        }
+    };
+    auto store_in = [&]() {
+#pragma unroll
+        for (int u = 0; u < RPER; ++u) {
+            const int e = t + u * WG;
+            if (e < RV) *(f4*)(s_in + 16 * e) = vin[u];
+        }
+    };
+
+    // weights -> three exact bf16 planes [part][o][k]; bias
+    load_in(j0);
+    for (int e = t; e < COUT * KW1 / 4; e += WG) {
+        const f4 w = ((const f4*)W)[e];
+        const int o = (4 * e) / KW1, k = (4 * e) % KW1;
+        bf16x4 h, m, l;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            __bf16 hi, mid, lo;
+            split3(w[i], hi, mid, lo);
+            h[i] = hi;
+            m[i] = mid;
+            l[i] = lo;
+        }
+        *(bf16x4*)(s_w + 0 * PL + o * RS1 + k) = h;
+        *(bf16x4*)(s_w + 1 * PL + o * RS1 + k) = m;
+        *(bf16x4*)(s_w + 2 * PL + o * RS1 + k) = l;
+    }
+    if (t < COUT) s_b[t] = bias[t];
+
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int ntile = (MT - wave + 3) / 4;       // this wave's M-tiles (uniform)
+    int abase[MPW];
+#pragma unroll
+    for (int i = 0; i < MPW; ++i) {
+        const int mt = wave + 4 * min(i, ntile - 1);
+        const int pa = mt * 16 + li;
+        const int ra = pa / H1, xa = pa - ra * H1;
+        abase[i] = S1 * ra * H0 + S1 * xa;
+    }
+    constexpr float inv255 = (float)(1.0 / 255.0);
+
+    for (int j = j0; j < j1; ++j) {
+        store_in();
+        __syncthreads();
+        if (j + 1 < j1) load_in(j + 1);          // in flight during this sample
+        f4 acc[MPW][NT];
+#pragma unroll
+        for (int i = 0; i < MPW; ++i)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) acc[i][nt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KW1 / 32; ++kb) {
+            const int c = kb >> 1, ky = (kb & 1) * 4 + g;
+            bf16x8 b[NT][3];
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                for (int part = 0; part < 3; ++part)
+                    b[nt][part] = *(const bf16x8*)(s_w + part * PL + (nt * 16 + li) * RS1 + kb * 32 + 8 * g);
+#pragma unroll
+            for (int i = 0; i < MPW; ++i) {
+                const unsigned char* ap = s_in + (c * H0 + ky) * H0 + abase[i];
+                const uint32_t w0 = *(const uint32_t*)ap, w1 = *(const uint32_t*)(ap + 4);
+                bf16x8 a;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    a[q] = (__bf16)(float)((w0 >> (8 * q)) & 0xffu);
+                    a[4 + q] = (__bf16)(float)((w1 >> (8 * q)) & 0xffu);
+                }
+#pragma unroll
+                for (int part = 0; part < 3; ++part)
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) acc[i][nt] = mfma16x16x32bf16(a, b[nt][part], acc[i][nt]);
+            }
+        }
+        // lane holds pixels 16*mt + 4g + r of channel nt*16 + li
+        float* oj = p.out + (size_t)j * COUT * H1 * H1;
+#pragma unroll
+        for (int i = 0; i < MPW; ++i) {
+            if (i < ntile) {
+                const int pb = (wave + 4 * i) * 16 + 4 * g;
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) {
+                    const int o = nt * 16 + li;
+                    const float bo = s_b[o];
+                    f4 v;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[i][nt][r] * inv255 + bo, 0.f);
+                    *(f4*)(oj + (size_t)o * H1 * H1 + pb) = v;
+                }
+            }
+        }
+        __syncthreads();  // all reads of s_in done before the next sample is stored
+    }
+}
+
+}  // namespace
+
+bool conv1_u8_fwd_supported(ConvId id) { return id == CONV_L1 || id == CONV_S1; }
+
+hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
+                               const float* w_a, const float* b_a, const float* w_b, const float* b_b,
+                               float* out, const SideFields* side, hipStream_t st) {
+    if (n <= 0 || n_a < 0 || n_a > n || !conv_s12_fwd_aligned(in_a) || !conv_s12_fwd_aligned(in_b) ||
+        ((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15))
+        return hipErrorInvalidValue;
+    // about 256 workgroups: a few samples each, so the weight split is amortized
+    const int spb = std::max(1, (n + 255) / 256);
+    const int blocks_a = (n_a + spb - 1) / spb, blocks_b = (n - n_a + spb - 1) / spb;
+    U8FwdParams prm{in_a, in_b, n_a, n, spb, blocks_a, w_a, b_a, w_b, b_b, out, side ? *side : SideFields{}};
+    const dim3 grid((unsigned)std::max(1, blocks_a + blocks_b));
+    auto go = [&](auto kern, int cout) -> hipError_t {
+        const size_t lds = ((C0 * H0 * H0 + 15) / 16) * 16 + (size_t)3 * cout * RS1 * 2 + (size_t)cout * 4;
+        if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(kern, grid, dim3(WG), lds, st, prm);
+        return hipGetLastError();
+    };
+    if (id == CONV_L1) return go(conv1_u8_fwd_kernel<32>, 32);
+    if (id == CONV_S1) return go(conv1_u8_fwd_kernel<16>, 16);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace dqn
