@@ -88,7 +88,8 @@ constexpr int kIgemmMinRows = 128;
 
 // Backward layers that run as implicit GEMMs at batch B (measured faster
 // than the per-layer kernels from 128 samples: the weight gradients of
-// conv2/conv3 and the input gradient of conv3 of the large network).
+// conv2/conv3 and the input gradient of conv3 of the large network; its
+// conv1 weight gradient uses a dedicated kernel from the same size).
 bool igemm_wgrad(ConvId id, int B) { return (id == CONV_L2 || id == CONV_L3) && B >= kIgemmMinRows; }
 bool igemm_dgrad(ConvId id, int B) { return id == CONV_L3 && B >= kIgemmMinRows; }
 
@@ -142,6 +143,8 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
         if (l == 0 && ni.n_conv == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]))
             slots = std::max<int64_t>(slots, conv_s12_bwd_slots(B));
         if (igemm_wgrad(ni.conv[l], B)) slots = std::max<int64_t>(slots, conv_igemm_wgrad_chunks(ni.conv[l], B));
+        if (l == 0 && ni.conv[0] == CONV_L1 && B >= kIgemmMinRows)
+            slots = std::max<int64_t>(slots, conv1_u8_wgrad_slots(B));
         t.wpart[l] = cv.take<float>(ws, slots * c.cout * c.cin * c.k * c.k);
         t.bpart[l] = cv.take<float>(ws, slots * c.cout);
     }
@@ -371,7 +374,11 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
                                 th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], st));
             continue;
         }
-        if (igemm_wgrad(ni.conv[l], B)) {
+        if (l == 0 && ni.conv[0] == CONV_L1 && B >= kIgemmMinRows && conv_s12_fwd_aligned(s0)) {
+            RUN(DQN_K_CONV1_WGRAD,
+                launch_conv1_u8_wgrad(CONV_L1, s0, t.dconv[0], B, t.wpart[0], t.bpart[0], scale, st));
+            chunks_used[0] = conv1_u8_wgrad_slots(B);
+        } else if (igemm_wgrad(ni.conv[l], B)) {
             RUN(DQN_K_CONV1_WGRAD + l,
                 launch_conv_igemm_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
             chunks_used[l] = conv_igemm_wgrad_chunks(ni.conv[l], B);

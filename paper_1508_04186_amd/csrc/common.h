@@ -158,6 +158,14 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
                                const float* w_a, const float* b_a, const float* w_b, const float* b_b,
                                float* out, const SideFields* side, hipStream_t st);
 
+// conv1 weight/bias gradient on byte input (CONV_L1 or CONV_S1) for many
+// samples: conv1_u8_wgrad_slots(n) partial-sum slots of wpart
+// [slots][cout][256] and bpart [slots][cout]; input 16-byte aligned, dz
+// [n][cout][20][20].
+int conv1_u8_wgrad_slots(int n);
+hipError_t launch_conv1_u8_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
+                                 float* bpart, float in_scale, hipStream_t st);
+
 // Weight and bias gradient partial sums over sample chunks:
 // wpart [chunks][cout][cin*k*k], bpart [chunks][cout].
 int conv_wgrad_chunks(ConvId id, int batch);

@@ -847,3 +847,148 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
 }
 
 }  // namespace dqn
+
+// ---------------------------------------------------------------------------
+// conv1 weight/bias gradient on byte input for many samples: a workgroup owns
+// all COUT x 256 outputs for a run of samples (one partial-sum slot).  Per
+// sample it stages the input bytes and dz, then each wave contracts the 400
+// pixels for 2 M-tiles (output channels) x NTW N-tiles (weight columns),
+// every accumulator chain independent; lane group g takes pixel 4*st + g.
+namespace dqn {
+namespace {
+
+struct U8WgradParams {
+    ConvIn in;            // network input (bytes)
+    const float* dz;      // [n][COUT][20][20]
+    int n, spb;
+    float* wpart;         // [blocks][COUT][256]
+    float* bpart;         // [blocks][COUT]
+    float in_scale;
+};
+
+template <int COUT>
+__global__ __launch_bounds__(WG) void conv1_u8_wgrad_kernel(U8WgradParams p) {
+    constexpr int REC = C0 * H0 * H0;
+    constexpr int RV = REC / 16, RPER = (RV + WG - 1) / WG;
+    constexpr int P1 = H1 * H1;                        // 400 pixels
+    constexpr int DV = COUT * P1 / 4, DPER = (DV + WG - 1) / WG;
+    constexpr int MT = COUT / 16;
+    constexpr int NTW = KW1 / 16 / 4;                  // N-tiles per wave (4)
+    constexpr int LDZ = P1 + 4;                        // dz row stride (= 20 mod 64: conflict-free)
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* s_in = smem;                        // u8 [REC]
+    float* s_dz = (float*)(smem + REC);                // f32 [COUT][LDZ]
+    static_assert(REC % 16 == 0, "alignment");
+
+    const int j0 = blockIdx.x * p.spb, j1 = min(p.n, j0 + p.spb);
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    int koff[NTW];
+#pragma unroll
+    for (int i = 0; i < NTW; ++i) {
+        const int col = (wave * NTW + i) * 16 + li;
+        const int c = col / (K1 * K1), ky = (col / K1) % K1, kx = col % K1;
+        koff[i] = (c * H0 + ky) * H0 + kx;
+    }
+    f4 acc[MT][NTW];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int i = 0; i < NTW; ++i) acc[m][i] = f4{0.f, 0.f, 0.f, 0.f};
+    float bsum = 0.f;
+
+    for (int j = j0; j < j1; ++j) {
+        f4 vin[RPER], vdz[DPER];
+        const f4* src = (const f4*)sample_ptr(p.in, j);
+        const f4* dzj = (const f4*)(p.dz + (size_t)j * COUT * P1);
+#pragma unroll
+        for (int u = 0; u < RPER; ++u) {
+            const int e = t + u * WG;
+            if (e < RV) vin[u] = src[e];
+        }
+#pragma unroll
+        for (int u = 0; u < DPER; ++u) {
+            const int e = t + u * WG;
+            if (e < DV) vdz[u] = dzj[e];
+        }
+        __syncthreads();  // the previous sample's reads are done
+#pragma unroll
+        for (int u = 0; u < RPER; ++u) {
+            const int e = t + u * WG;
+            if (e < RV) *(f4*)(s_in + 16 * e) = vin[u];
+        }
+#pragma unroll
+        for (int u = 0; u < DPER; ++u) {
+            const int e = t + u * WG;
+            if (e < DV) {
+                const int o = (4 * e) / P1, q = (4 * e) % P1;
+                *(f4*)(s_dz + o * LDZ + q) = vdz[u];
+            }
+        }
+        __syncthreads();
+        if (t < COUT) {
+            const float* row = s_dz + t * LDZ;
+            float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+            for (int q = 0; q < P1; q += 4) {
+                s0 += row[q];
+                s1 += row[q + 1];
+                s2 += row[q + 2];
+                s3 += row[q + 3];
+            }
+            bsum += (s0 + s1) + (s2 + s3);
+        }
+        // pixel q = 4*st + g: row q/20, column q%20 (a step stays in one row)
+#pragma unroll 2
+        for (int st = 0; st < P1 / 4; ++st) {
+            const int q = 4 * st + g;
+            const int y = (4 * st) / H1, x = (4 * st) % H1 + g;
+            const int po = S1 * y * H0 + S1 * x;
+            float a[MT], b[NTW];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) a[m] = s_dz[(m * 16 + li) * LDZ + q];
+#pragma unroll
+            for (int i = 0; i < NTW; ++i) b[i] = (float)s_in[koff[i] + po];
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int i = 0; i < NTW; ++i) acc[m][i] = mfma16x16x4(a[m], b[i], acc[m][i]);
+        }
+    }
+    // D[4g + r][li] of tile (m, i): channel m*16 + 4g + r, column (wave*NTW + i)*16 + li
+    float* wp = p.wpart + (size_t)blockIdx.x * COUT * KW1;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int i = 0; i < NTW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                wp[(size_t)(m * 16 + 4 * g + r) * KW1 + (wave * NTW + i) * 16 + li] = acc[m][i][r] * p.in_scale;
+    if (t < COUT) p.bpart[(size_t)blockIdx.x * COUT + t] = bsum;
+}
+
+}  // namespace
+
+int conv1_u8_wgrad_slots(int n) {
+    const int spb = std::max(1, (n + 511) / 512);
+    return (n + spb - 1) / spb;
+}
+
+hipError_t launch_conv1_u8_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
+                                 float* bpart, float in_scale, hipStream_t st) {
+    if (n <= 0 || !conv_s12_fwd_aligned(in) || in.off != 0 || ((uintptr_t)dz & 15)) return hipErrorInvalidValue;
+    const int spb = std::max(1, (n + 511) / 512);
+    const int blocks = (n + spb - 1) / spb;
+    const U8WgradParams prm{in, dz, n, spb, wpart, bpart, in_scale};
+    auto go = [&](auto kern, int cout) -> hipError_t {
+        const size_t lds = (size_t)C0 * H0 * H0 + (size_t)cout * (H1 * H1 + 4) * 4;
+        if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(WG), lds, st, prm);
+        return hipGetLastError();
+    };
+    if (id == CONV_L1) return go(conv1_u8_wgrad_kernel<32>, 32);
+    if (id == CONV_S1) return go(conv1_u8_wgrad_kernel<16>, 16);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace dqn
