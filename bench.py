@@ -59,6 +59,7 @@ if ROOT not in sys.path:
 METRIC = "DQN TD-gradient+update steps/sec (transitions/sec); % MFMA peak and HBM GB/s"
 PEAK_FP32_MFMA = 157.3e12   # MI355X dense fp32 matrix FLOP/s
 PEAK_HBM = 8.0e12           # MI355X HBM3E bytes/s
+PEAK_BF16_MFMA = 2.5e15     # MI355X dense bf16 matrix FLOP/s
 # In the timed region of the small-batch configs, every SAMPLE_STRIDE-th
 # launch of the dominant kernel is bracketed by events (each pair adds a few
 # microseconds to a step of about seventy).
@@ -291,6 +292,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall time budget of the CPU-oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-denominators", action="store_true",
+                    help="skip the measured matrix-core and HBM copy peaks")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB "
                          "(reference kernel for scaling HBM byte counters)")
@@ -309,6 +312,8 @@ def main():
     torch.cuda.init()
     out = {"0": bench_single, "1": bench_sequential, "2": bench_replicas, "3": bench_large,
            "4a": bench_forward, "4b": bench_large}[args.config](args)
+    if not args.no_denominators:
+        out["denominators"] = measure_denominators()
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib * 2**20
         src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
@@ -318,6 +323,42 @@ def main():
         torch.cuda.synchronize()
         log(f"calibration copy of {args.calib_copy_mib} MiB done")
     print(json.dumps(out), flush=True)
+
+
+def measure_denominators():
+    """The roofline denominators as this GPU reaches them (dqn_profile.h): a
+    pure matrix-core loop for fp32 and bf16 MFMA and a streaming copy of
+    1 GiB, each the best of five launches timed with events; reported beside
+    the spec-sheet peaks that the roofline fractions use."""
+    import torch
+    import paper_1508_04186_amd as dq
+    workgroups = 256 * 8
+    out = torch.empty(workgroups, device="cuda")
+
+    def best_ms(fn, reps=5):
+        fn()
+        t = []
+        for _ in range(reps):
+            t.append(time_region(torch.cuda.synchronize, fn))
+        return min(t)
+
+    res = {}
+    for name, dt, iters, spec in (("mfma_fp32_tflops", dq.DQN_PEAK_FP32, 4096, PEAK_FP32_MFMA / 1e12),
+                                  ("mfma_bf16_tflops", dq.DQN_PEAK_BF16, 8192, PEAK_BF16_MFMA / 1e12)):
+        flop = [0]
+
+        def run():
+            flop[0] = dq.profile_mfma_peak(dt, workgroups, iters, out)
+        ms = best_ms(run)
+        res[name] = {"spec": spec, "measured": round(flop[0] / (ms * 1e-3) / 1e12, 1)}
+    n = 1 << 30
+    src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    ms = best_ms(lambda: dq.profile_stream_copy(src, dst, 256 * 16))
+    res["hbm_copy_gbs"] = {"spec": PEAK_HBM / 1e9, "measured": round(2 * n / (ms * 1e-3) / 1e9, 1)}
+    del src, dst
+    log(f"denominators: {res}")
+    return res
 
 
 def base_record(K, W, ms, unit="steps/s"):

@@ -59,6 +59,28 @@ int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs, int32_t s
 int32_t dqn_profile_used(int32_t kernel);
 int dqn_profile_set_fusion(int32_t enabled);
 
+/* Checks of the roofline denominators on the running device (the spec-sheet
+ * peaks are what the figures are divided by; these show what the chip
+ * reaches with the instruction forms the hot path uses).
+ *
+ * dqn_profile_mfma_peak(dtype, workgroups, iters, out, stream): enqueues one
+ * launch of `workgroups` workgroups of four waves; every wave issues iters x 4
+ * independent matrix-core instructions on register operands (DQN_PEAK_FP32:
+ * v_mfma_f32_16x16x4_f32, 2,048 FLOP each; DQN_PEAK_BF16:
+ * v_mfma_f32_16x16x32_bf16, 16,384 FLOP each) and stores one float per
+ * workgroup to out (device float [workgroups]).  Returns the FLOP count of the
+ * launch (> 0), or DQN_EINVAL / DQN_EHIP.  The caller times the launch with
+ * events on `stream`.
+ *
+ * dqn_profile_stream_copy(src, dst, bytes, workgroups, stream): enqueues a
+ * copy of `bytes` (a multiple of 16; src and dst device pointers, 16-byte
+ * aligned, not overlapping) with 16-byte loads and stores, grid-stride over
+ * `workgroups` workgroups of 256 threads; it moves 2 x bytes through HBM when
+ * the buffers exceed the caches.  Returns DQN_OK, DQN_EINVAL or DQN_EHIP. */
+enum { DQN_PEAK_FP32 = 0, DQN_PEAK_BF16 = 1 };
+int64_t dqn_profile_mfma_peak(int32_t dtype, int32_t workgroups, int32_t iters, float* out, void* stream);
+int dqn_profile_stream_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -130,6 +130,10 @@ def lib():
         L.dqn_profile_set_fusion.restype = ctypes.c_int
         L.dqn_profile_used.argtypes = [ctypes.c_int32]
         L.dqn_profile_used.restype = ctypes.c_int32
+        L.dqn_profile_mfma_peak.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, _P]
+        L.dqn_profile_mfma_peak.restype = ctypes.c_int64
+        L.dqn_profile_stream_copy.argtypes = [_P, _P, ctypes.c_int64, ctypes.c_int32, _P]
+        L.dqn_profile_stream_copy.restype = ctypes.c_int
         _LIB = L
     return _LIB
 
@@ -465,3 +469,27 @@ def profile_set_fusion(enabled: bool) -> None:
 
 def profile_used(kernel: int) -> int:
     return int(lib().dqn_profile_used(kernel))
+
+
+DQN_PEAK_FP32, DQN_PEAK_BF16 = 0, 1
+
+
+def profile_mfma_peak(dtype: int, workgroups: int, iters: int, out, stream=None) -> int:
+    """Enqueue the pure matrix-core loop (include/dqn_profile.h); returns its FLOP count.
+    out: device float32 tensor with at least `workgroups` elements."""
+    import torch
+    if out.numel() < workgroups:
+        raise ValueError("out needs one float per workgroup")
+    v = lib().dqn_profile_mfma_peak(int(dtype), int(workgroups), int(iters),
+                                    _ptr(out, torch.float32, "out"), _stream(stream))
+    _check(0 if v > 0 else int(v), "dqn_profile_mfma_peak")
+    return int(v)
+
+
+def profile_stream_copy(src, dst, workgroups: int, stream=None) -> None:
+    """Enqueue the streaming copy dst <- src (equal-sized device tensors, bytes a multiple of 16)."""
+    nb = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nb:
+        raise ValueError("src and dst must have the same byte size")
+    _check(lib().dqn_profile_stream_copy(_ptr(src, None, "src"), _ptr(dst, None, "dst"), nb,
+                                         int(workgroups), _stream(stream)), "dqn_profile_stream_copy")

@@ -195,6 +195,19 @@ def test_apply_argument_errors():
     assert call(lr=float("inf")) == dq.DQN_EINVAL
 
 
+@fake_ptr_test
+def test_peak_check_argument_errors():
+    L = dq.lib()
+    assert L.dqn_profile_mfma_peak(7, 16, 16, FAKE, None) == dq.DQN_EINVAL       # unknown dtype
+    assert L.dqn_profile_mfma_peak(0, 0, 16, FAKE, None) == dq.DQN_EINVAL
+    assert L.dqn_profile_mfma_peak(1, 16, 0, FAKE, None) == dq.DQN_EINVAL
+    assert L.dqn_profile_mfma_peak(0, 16, 16, None, None) == dq.DQN_EINVAL
+    assert L.dqn_profile_stream_copy(FAKE, FAKE + 4096, 100, 8, None) == dq.DQN_EINVAL   # not whole vectors
+    assert L.dqn_profile_stream_copy(FAKE, FAKE + 64, 4096, 8, None) == dq.DQN_EINVAL    # overlap
+    assert L.dqn_profile_stream_copy(FAKE + 4, FAKE + 8192, 4096, 8, None) == dq.DQN_EINVAL  # misaligned
+    assert L.dqn_profile_stream_copy(FAKE, FAKE + 8192, 4096, 0, None) == dq.DQN_EINVAL
+
+
 def test_status_strings():
     for s in (dq.DQN_OK, dq.DQN_EINVAL, dq.DQN_EWORKSPACE, dq.DQN_EHIP, dq.DQN_EUNSUPPORTED):
         assert dq.dqn_status_string(s) not in ("", "unknown status")
