@@ -28,7 +28,8 @@ class _Net(ctypes.Structure):
     _fields_ = [("in_c", ctypes.c_int32), ("in_h", ctypes.c_int32), ("in_w", ctypes.c_int32),
                 ("n_conv", ctypes.c_int32), ("conv_out", ctypes.c_int32 * 3),
                 ("conv_k", ctypes.c_int32 * 3), ("conv_stride", ctypes.c_int32 * 3),
-                ("fc_hidden", ctypes.c_int32), ("n_actions", ctypes.c_int32)]
+                ("fc_hidden", ctypes.c_int32), ("n_actions", ctypes.c_int32),
+                ("bf16_inputs", ctypes.c_int32)]
 
 
 def lib_path():
@@ -72,7 +73,8 @@ def _lib():
                                            ctypes.c_int64, ctypes.c_double, _P, _P, _P, _P, _P]
         lib.oracle_apply_update.argtypes = [ctypes.c_int32, _P, _P, _P, _P, ctypes.c_int64,
                                             ctypes.c_double, ctypes.c_double, ctypes.c_double]
-        for f in ("oracle_replay_gather", "oracle_forward_q", "oracle_relu_margins",
+        lib.oracle_bf16_round.argtypes = [_P, ctypes.c_int64, _P]
+        for f in ("oracle_replay_gather", "oracle_forward_q", "oracle_relu_margins", "oracle_bf16_round",
                   "oracle_select_actions",
                   "oracle_td_gradient", "oracle_apply_update"):
             getattr(lib, f).restype = ctypes.c_int
@@ -80,13 +82,16 @@ def _lib():
     return _LIB
 
 
-def _net(net):
+def _net(net, bf16=False):
+    """bf16: the bf16-input variant (every layer-contraction operand rounded
+    to bfloat16, round to nearest even, before the double-precision products)."""
     n = _Net()
     n.in_c, n.in_h, n.in_w = net.in_c, net.in_h, net.in_w
     n.n_conv = len(net.conv)
     for i, (o, k, s) in enumerate(net.conv):
         n.conv_out[i], n.conv_k[i], n.conv_stride[i] = o, k, s
     n.fc_hidden, n.n_actions = net.fc_hidden, net.n_actions
+    n.bf16_inputs = 1 if bf16 else 0
     return n
 
 
@@ -138,12 +143,20 @@ def gather_from_host_replay(rep, idx, with_next=True):
                          rep.reward, rep.terminal, idx, with_next)
 
 
-def forward_q(net, theta, states) -> np.ndarray:
+def bf16_round(x) -> np.ndarray:
+    """x rounded to float32 and then to bfloat16 (nearest, ties to even), as float64."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty_like(x)
+    _check(_lib().oracle_bf16_round(x.ctypes.data, x.size, out.ctypes.data), "oracle_bf16_round")
+    return out
+
+
+def forward_q(net, theta, states, bf16=False) -> np.ndarray:
     th = np.ascontiguousarray(theta, dtype=np.float64)
     st = np.ascontiguousarray(states, dtype=np.uint8)
     B = st.shape[0]
     q = np.empty((B, net.n_actions), np.float64)
-    _check(_lib().oracle_forward_q(ctypes.byref(_net(net)), th.ctypes.data, st.ctypes.data, B,
+    _check(_lib().oracle_forward_q(ctypes.byref(_net(net, bf16)), th.ctypes.data, st.ctypes.data, B,
                                    q.ctypes.data), "oracle_forward_q")
     return q
 
@@ -170,8 +183,9 @@ def select_actions(q, epsilon, draws=None) -> np.ndarray:
     return act
 
 
-def td_gradient(net, theta, theta_tgt, s, s_next, a, r, term, gamma):
-    """Returns dict(grad fp64 [p], loss, q [B][A], qn [B][A], y [B])."""
+def td_gradient(net, theta, theta_tgt, s, s_next, a, r, term, gamma, bf16=False):
+    """Returns dict(grad fp64 [p], loss, q [B][A], qn [B][A], y [B]).
+    bf16: the bf16-input variant (see _net)."""
     th = np.ascontiguousarray(theta, dtype=np.float64)
     tt = th if theta_tgt is None else np.ascontiguousarray(theta_tgt, dtype=np.float64)
     s = np.ascontiguousarray(s, dtype=np.uint8)
@@ -186,7 +200,7 @@ def td_gradient(net, theta, theta_tgt, s, s_next, a, r, term, gamma):
     q = np.empty((B, net.n_actions), np.float64)
     qn = np.empty((B, net.n_actions), np.float64)
     y = np.empty(B, np.float64)
-    rc = _lib().oracle_td_gradient(ctypes.byref(_net(net)), th.ctypes.data, tt.ctypes.data,
+    rc = _lib().oracle_td_gradient(ctypes.byref(_net(net, bf16)), th.ctypes.data, tt.ctypes.data,
                                    s.ctypes.data, sn.ctypes.data, a.ctypes.data, r.ctypes.data,
                                    t.ctypes.data, B, float(gamma), grad.ctypes.data,
                                    loss.ctypes.data, q.ctypes.data, qn.ctypes.data, y.ctypes.data)
@@ -211,7 +225,7 @@ def apply_update(rule, theta, state, grad, lr, decay=0.9, eps=0.0):
 # Multi-step drivers
 
 def sequential_training(net, theta0, rep, idx_stream, gamma, lr, rule="sgd", decay=0.9, eps=0.0,
-                        target_period=None, steps=None, state0=None, callback=None):
+                        target_period=None, steps=None, state0=None, callback=None, bf16=False):
     """Sequential worker + server: for n = 0..steps-1, gather the minibatch
     idx_stream[n] from the host replay, compute the TD gradient with the
     target network, and apply the update (Alg. 1 then Alg. 2 with one
@@ -232,7 +246,7 @@ def sequential_training(net, theta0, rep, idx_stream, gamma, lr, rule="sgd", dec
             tgt = theta.copy()
             gen = n // target_period + 1
         s, sn, a, r, t = gather_from_host_replay(rep, idx_stream[n])
-        out = td_gradient(net, theta, tgt, s, sn, a, r, t, gamma)
+        out = td_gradient(net, theta, tgt, s, sn, a, r, t, gamma, bf16)
         losses.append(out["loss"])
         theta, state = apply_update(rule, theta, state, out["grad"], lr, decay, eps)
         if callback is not None:

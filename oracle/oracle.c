@@ -31,6 +31,16 @@
  *                          descent (Sec. III.B), the RMSProp rule of Alg. 2,
  *                          and AdaGrad (named in Sec. IV.D.2).
  *
+ * The bf16-input variant (net->bf16_inputs = 1) computes the same functions
+ * with every operand of the layer contractions -- the conv and fc1 weights,
+ * the conv and fc1 input activations, and the back-propagated gradients
+ * that multiply weights or activations -- first rounded to float32 (the
+ * precision in which they are stored) and then to bfloat16 with round to
+ * nearest, ties to even; products and sums stay in double.  The input bytes
+ * are exact in bfloat16, and the 1/255 scale applies after the sum.  Bias
+ * gradients, the fc2 output layer and the ReLU decisions use the unrounded
+ * values.
+ *
  * Readings where the paper is silent or garbled are stated at each function.
  *
  * Build: gcc -O2 -fopenmp -shared -fPIC oracle.c -o liboracle.so
@@ -50,6 +60,7 @@ typedef struct {
     int32_t conv_k[ORACLE_MAX_CONV];
     int32_t conv_stride[ORACLE_MAX_CONV];
     int32_t fc_hidden, n_actions;
+    int32_t bf16_inputs;   /* 1: the bf16-input variant described above */
 } oracle_net;
 
 enum { ORACLE_OK = 0, ORACLE_EINVAL = -1, ORACLE_ERANGE = -2, ORACLE_ENOMEM = -3 };
@@ -97,6 +108,15 @@ static int make_shapes(const oracle_net* net, shapes_t* sh) {
     return ORACLE_OK;
 }
 
+/* out[i] = the bf16 contraction operand of in[i] (bf16_round below), so the
+ * tests can check the rounding itself. */
+static double bf16_round(double v);
+int oracle_bf16_round(const double* in, int64_t n, double* out) {
+    if (!in || !out || n < 0) return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i) out[i] = bf16_round(in[i]);
+    return ORACLE_OK;
+}
+
 /* Threads the oracle's parallel loops use. */
 int oracle_num_threads(void) { return omp_get_max_threads(); }
 
@@ -136,15 +156,17 @@ static void conv_forward(const double* in, int C, int H, int W_, const double* W
 
 /* Given dz = dL/dz, accumulate dL/dW and dL/db; if din is not NULL also
  * dL/d(in) (the transposed convolution: each output scatters W * dz back
- * onto the input window it read). */
+ * onto the input window it read).  dzm is the dz that multiplies W and the
+ * input (dz itself, or its bf16 rounding in the bf16-input variant); the
+ * bias gradient sums dz. */
 static void conv_backward(const double* in, int C, int H, int W_, const double* Wt,
-                          int O, int k, int s, int OH, int OW, const double* dz,
+                          int O, int k, int s, int OH, int OW, const double* dz, const double* dzm,
                           double* dW, double* db, double* din) {
     for (int o = 0; o < O; ++o)
         for (int y = 0; y < OH; ++y)
             for (int x = 0; x < OW; ++x) {
-                double g = dz[(o * OH + y) * OW + x];
-                db[o] += g;
+                double g = dzm[(o * OH + y) * OW + x];
+                db[o] += dz[(o * OH + y) * OW + x];
                 for (int c = 0; c < C; ++c)
                     for (int ky = 0; ky < k; ++ky)
                         for (int kx = 0; kx < k; ++kx) {
@@ -166,18 +188,39 @@ static void fc_forward(const double* in, int64_t n_in, const double* Wt, const d
     }
 }
 
+/* As conv_backward: dzm multiplies, dz feeds the bias gradient. */
 static void fc_backward(const double* in, int64_t n_in, const double* Wt, int n_out,
-                        const double* dz, double* dW, double* db, double* din) {
+                        const double* dz, const double* dzm, double* dW, double* db, double* din) {
     for (int o = 0; o < n_out; ++o) {
         db[o] += dz[o];
         for (int64_t i = 0; i < n_in; ++i) {
-            dW[(int64_t)o * n_in + i] += dz[o] * in[i];
-            if (din) din[i] += dz[o] * Wt[(int64_t)o * n_in + i];
+            dW[(int64_t)o * n_in + i] += dzm[o] * in[i];
+            if (din) din[i] += dzm[o] * Wt[(int64_t)o * n_in + i];
         }
     }
 }
 
 static inline double relu(double v) { return v > 0.0 ? v : 0.0; }
+
+/* v rounded to float32, then to bfloat16 (the upper 16 bits of a float32)
+ * with round to nearest, ties to even; returned as double.  Non-finite
+ * values are truncated (they do not occur here). */
+static double bf16_round(double v) {
+    float f = (float)v;
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    if ((u & 0x7f800000u) != 0x7f800000u) u += 0x7fffu + ((u >> 16) & 1u);
+    u &= 0xffff0000u;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* dst = the contraction operand of src: src itself, or its bf16 rounding. */
+static const double* operand(const double* src, int64_t n, int bf16, double* dst) {
+    if (!bf16) return src;
+    for (int64_t i = 0; i < n; ++i) dst[i] = bf16_round(src[i]);
+    return dst;
+}
 
 /* Per-sample activations: act[0] = scaled input, act[l+1] = ReLU output of
  * conv l, then fc1's pre-activation z and post-ReLU h, then Q. */
@@ -187,13 +230,15 @@ typedef struct {
     double* z1;
     double* h1;
     double* q;
+    double* opnd[ORACLE_MAX_CONV + 1];  /* contraction operand of act[l] */
 } acts_t;
 
 static int acts_alloc(const oracle_net* net, const shapes_t* sh, acts_t* a) {
     memset(a, 0, sizeof(*a));
     for (int l = 0; l <= net->n_conv; ++l) {
         a->act[l] = (double*)calloc((size_t)sh->c[l] * sh->h[l] * sh->w[l], sizeof(double));
-        if (!a->act[l]) return ORACLE_ENOMEM;
+        a->opnd[l] = (double*)calloc((size_t)sh->c[l] * sh->h[l] * sh->w[l], sizeof(double));
+        if (!a->act[l] || !a->opnd[l]) return ORACLE_ENOMEM;
         if (l < net->n_conv) {
             a->zc[l] = (double*)calloc((size_t)sh->c[l + 1] * sh->h[l + 1] * sh->w[l + 1], sizeof(double));
             if (!a->zc[l]) return ORACLE_ENOMEM;
@@ -206,25 +251,52 @@ static int acts_alloc(const oracle_net* net, const shapes_t* sh, acts_t* a) {
 }
 
 static void acts_free(const oracle_net* net, acts_t* a) {
-    for (int l = 0; l <= net->n_conv; ++l) { free(a->act[l]); if (l < net->n_conv) free(a->zc[l]); }
+    for (int l = 0; l <= net->n_conv; ++l) {
+        free(a->act[l]);
+        free(a->opnd[l]);
+        if (l < net->n_conv) free(a->zc[l]);
+    }
     free(a->z1); free(a->h1); free(a->q);
 }
 
-/* Q(phi; theta) for one state of bytes; input x = byte / 255. */
+/* Q(phi; theta) for one state of bytes; input x = byte / 255.  thw holds the
+ * contraction operands of the conv and fc1 weights (theta itself, or its
+ * bf16 rounding); biases and fc2 come from th.  a->opnd[l] receives the
+ * operand of each layer input (the bytes are exact in bf16; x = byte/255
+ * then equals the scale applied after the sum). */
 static void forward_one(const oracle_net* net, const shapes_t* sh, const double* th,
-                        const uint8_t* state, acts_t* a) {
+                        const double* thw, const uint8_t* state, acts_t* a) {
+    const int bf = net->bf16_inputs;
     int64_t n_in = (int64_t)sh->c[0] * sh->h[0] * sh->w[0];
-    for (int64_t i = 0; i < n_in; ++i) a->act[0][i] = (double)state[i] / 255.0;
+    for (int64_t i = 0; i < n_in; ++i) a->act[0][i] = a->opnd[0][i] = (double)state[i] / 255.0;
     for (int l = 0; l < net->n_conv; ++l) {
-        conv_forward(a->act[l], sh->c[l], sh->h[l], sh->w[l], th + sh->w_off[l], th + sh->b_off[l],
+        const double* x = l == 0 ? a->opnd[0]
+                                 : operand(a->act[l], (int64_t)sh->c[l] * sh->h[l] * sh->w[l], bf, a->opnd[l]);
+        conv_forward(x, sh->c[l], sh->h[l], sh->w[l], thw + sh->w_off[l], th + sh->b_off[l],
                      sh->c[l + 1], net->conv_k[l], net->conv_stride[l], sh->h[l + 1], sh->w[l + 1], a->zc[l]);
         int64_t n = (int64_t)sh->c[l + 1] * sh->h[l + 1] * sh->w[l + 1];
         for (int64_t i = 0; i < n; ++i) a->act[l + 1][i] = relu(a->zc[l][i]);
     }
     int L = net->n_conv;
-    fc_forward(a->act[L], sh->flat, th + sh->w_off[L], th + sh->b_off[L], net->fc_hidden, a->z1);
+    const double* x = operand(a->act[L], sh->flat, bf, a->opnd[L]);
+    fc_forward(x, sh->flat, thw + sh->w_off[L], th + sh->b_off[L], net->fc_hidden, a->z1);
     for (int h = 0; h < net->fc_hidden; ++h) a->h1[h] = relu(a->z1[h]);
     fc_forward(a->h1, net->fc_hidden, th + sh->w_off[L + 1], th + sh->b_off[L + 1], net->n_actions, a->q);
+}
+
+/* The contraction operands of theta's conv and fc1 weights: theta itself, or
+ * a new array with those weights rounded to bf16 (the caller frees it when
+ * it differs from theta).  NULL when out of memory. */
+static const double* weight_operands(const oracle_net* net, const shapes_t* sh, const double* th) {
+    if (!net->bf16_inputs) return th;
+    double* r = (double*)malloc(sizeof(double) * (size_t)sh->n_params);
+    if (!r) return NULL;
+    memcpy(r, th, sizeof(double) * (size_t)sh->n_params);
+    for (int l = 0; l <= net->n_conv; ++l) {
+        int64_t n = sh->b_off[l] - sh->w_off[l];
+        for (int64_t i = 0; i < n; ++i) r[sh->w_off[l] + i] = bf16_round(th[sh->w_off[l] + i]);
+    }
+    return r;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -342,6 +414,8 @@ int oracle_forward_q(const oracle_net* net, const double* theta, const uint8_t* 
     if (make_shapes(net, &sh) != ORACLE_OK || !theta || !states || !q_out || batch < 0)
         return ORACLE_EINVAL;
     int64_t in_bytes = (int64_t)sh.c[0] * sh.h[0] * sh.w[0];
+    const double* thw = weight_operands(net, &sh, theta);
+    if (!thw) return ORACLE_ENOMEM;
     int err = ORACLE_OK;
     #pragma omp parallel
     {
@@ -353,12 +427,13 @@ int oracle_forward_q(const oracle_net* net, const double* theta, const uint8_t* 
         } else {
             #pragma omp for schedule(static)
             for (int64_t j = 0; j < batch; ++j) {
-                forward_one(net, &sh, theta, states + j * in_bytes, &a);
+                forward_one(net, &sh, theta, thw, states + j * in_bytes, &a);
                 for (int k = 0; k < net->n_actions; ++k) q_out[j * net->n_actions + k] = a.q[k];
             }
         }
         acts_free(net, &a);
     }
+    if (thw != theta) free((void*)thw);
     return err;
 }
 
@@ -415,9 +490,17 @@ int oracle_td_gradient(const oracle_net* net, const double* theta, const double*
     if (nthreads > batch) nthreads = (int)batch;
     /* Per-sample gradients are computed in parallel, nthreads at a time, and
      * added to the total strictly in sample order. */
+    const int bf = net->bf16_inputs;
     double* g = (double*)calloc((size_t)nthreads * (size_t)P, sizeof(double));
     double* lj = (double*)calloc((size_t)batch, sizeof(double));
-    if (!g || !lj) { free(g); free(lj); return ORACLE_ENOMEM; }
+    const double* thw = weight_operands(net, &sh, theta);
+    const double* ttw = weight_operands(net, &sh, theta_tgt);
+    if (!g || !lj || !thw || !ttw) {
+        free(g); free(lj);
+        if (thw && thw != theta) free((void*)thw);
+        if (ttw && ttw != theta_tgt) free((void*)ttw);
+        return ORACLE_ENOMEM;
+    }
     memset(grad, 0, sizeof(double) * (size_t)P);
     int err = ORACLE_OK;
     for (int64_t j0 = 0; j0 < batch && err == ORACLE_OK; j0 += nthreads) {
@@ -428,9 +511,10 @@ int oracle_td_gradient(const oracle_net* net, const double* theta, const double*
             int e1 = acts_alloc(net, &sh, &a), e2 = acts_alloc(net, &sh, &an);
             double *d_cur = (double*)calloc((size_t)sh.max_act, sizeof(double));
             double *d_prev = (double*)calloc((size_t)sh.max_act, sizeof(double));
+            double *d_opnd = (double*)calloc((size_t)sh.max_act, sizeof(double));
             double *dq = (double*)calloc((size_t)A, sizeof(double));
             double *dh = (double*)calloc((size_t)H, sizeof(double));
-            if (e1 || e2 || !d_cur || !d_prev || !dq || !dh) {
+            if (e1 || e2 || !d_cur || !d_prev || !d_opnd || !dq || !dh) {
                 #pragma omp atomic write
                 err = ORACLE_ENOMEM;
             } else {
@@ -440,12 +524,12 @@ int oracle_td_gradient(const oracle_net* net, const double* theta, const double*
                     double* gj = g + (size_t)t * (size_t)P;
                     memset(gj, 0, sizeof(double) * (size_t)P);
                     /* target from the held network on the next state */
-                    forward_one(net, &sh, theta_tgt, s_next + j * in_bytes, &an);
+                    forward_one(net, &sh, theta_tgt, ttw, s_next + j * in_bytes, &an);
                     double m = an.q[0];
                     for (int k = 1; k < A; ++k) if (an.q[k] > m) m = an.q[k];
                     double y = terminal[j] ? (double)reward[j] : (double)reward[j] + gamma * m;
                     /* prediction from the learned network on the state */
-                    forward_one(net, &sh, theta, s + j * in_bytes, &a);
+                    forward_one(net, &sh, theta, thw, s + j * in_bytes, &a);
                     double diff = a.q[action[j]] - y;
                     lj[j] = 0.5 * diff * diff / (double)batch;
                     if (q_all) for (int k = 0; k < A; ++k) q_all[j * A + k] = a.q[k];
@@ -455,12 +539,14 @@ int oracle_td_gradient(const oracle_net* net, const double* theta, const double*
                     for (int k = 0; k < A; ++k) dq[k] = (k == action[j]) ? diff / (double)batch : 0.0;
                     /* fc2 (linear) */
                     memset(dh, 0, sizeof(double) * (size_t)H);
-                    fc_backward(a.h1, H, theta + sh.w_off[L + 1], A, dq, gj + sh.w_off[L + 1],
+                    fc_backward(a.h1, H, theta + sh.w_off[L + 1], A, dq, dq, gj + sh.w_off[L + 1],
                                 gj + sh.b_off[L + 1], dh);
                     for (int h = 0; h < H; ++h) dh[h] = a.z1[h] > 0.0 ? dh[h] : 0.0;
-                    /* fc1 */
+                    /* fc1: products with the contraction operands of dh, its
+                     * input and its weights */
                     memset(d_cur, 0, sizeof(double) * (size_t)sh.flat);
-                    fc_backward(a.act[L], sh.flat, theta + sh.w_off[L], H, dh, gj + sh.w_off[L],
+                    fc_backward(bf ? a.opnd[L] : a.act[L], sh.flat,
+                                thw + sh.w_off[L], H, dh, operand(dh, H, bf, d_opnd), gj + sh.w_off[L],
                                 gj + sh.b_off[L], d_cur);
                     /* conv layers, last to first; no gradient into the input */
                     for (int l = L - 1; l >= 0; --l) {
@@ -468,16 +554,16 @@ int oracle_td_gradient(const oracle_net* net, const double* theta, const double*
                         for (int64_t i = 0; i < n_out; ++i) d_cur[i] = a.zc[l][i] > 0.0 ? d_cur[i] : 0.0;
                         int64_t n_in = (int64_t)sh.c[l] * sh.h[l] * sh.w[l];
                         if (l > 0) memset(d_prev, 0, sizeof(double) * (size_t)n_in);
-                        conv_backward(a.act[l], sh.c[l], sh.h[l], sh.w[l], theta + sh.w_off[l],
+                        conv_backward(bf ? a.opnd[l] : a.act[l], sh.c[l], sh.h[l], sh.w[l], thw + sh.w_off[l],
                                       sh.c[l + 1], net->conv_k[l], net->conv_stride[l], sh.h[l + 1],
-                                      sh.w[l + 1], d_cur, gj + sh.w_off[l], gj + sh.b_off[l],
-                                      l > 0 ? d_prev : NULL);
+                                      sh.w[l + 1], d_cur, operand(d_cur, n_out, bf, d_opnd),
+                                      gj + sh.w_off[l], gj + sh.b_off[l], l > 0 ? d_prev : NULL);
                         double* tmp = d_cur; d_cur = d_prev; d_prev = tmp;
                     }
                 }
             }
             acts_free(net, &a); acts_free(net, &an);
-            free(d_cur); free(d_prev); free(dq); free(dh);
+            free(d_cur); free(d_prev); free(d_opnd); free(dq); free(dh);
         }
         for (int64_t t = 0; t < jn && err == ORACLE_OK; ++t) {
             const double* gj = g + (size_t)t * (size_t)P;
@@ -488,6 +574,8 @@ int oracle_td_gradient(const oracle_net* net, const double* theta, const double*
     for (int64_t j = 0; j < batch; ++j) ls += lj[j];
     *loss = ls;
     free(g); free(lj);
+    if (thw != theta) free((void*)thw);
+    if (ttw != theta_tgt) free((void*)ttw);
     return err;
 }
 
