@@ -253,10 +253,11 @@ def measured_traffic(config, name):
     return None
 
 
-def roofline(work, name, avg_us, launches, per_step_launches, raw_us=None, config=None):
+def roofline(work, name, avg_us, launches, per_step_launches, raw_us=None, config=None,
+             peak_flops=PEAK_FP32_MFMA):
     flop, byts = work[name]
     if flop > 0:
-        achieved, peak, unit, bound = flop / (avg_us * 1e-6) / 1e12, PEAK_FP32_MFMA / 1e12, "TFLOP/s", "mfma"
+        achieved, peak, unit, bound = flop / (avg_us * 1e-6) / 1e12, peak_flops / 1e12, "TFLOP/s", "mfma"
     else:
         achieved, peak, unit, bound = byts / (avg_us * 1e-6) / 1e9, PEAK_HBM / 1e9, "GB/s", "hbm"
     out = {"kernel": name, "bound": bound, "achieved": round(achieved, 4), "peak": peak,
@@ -292,6 +293,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="wall time budget of the CPU-oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"],
+                    help="configs 3, 4a, 4b: fp32, or the bf16-input MFMA variant (fp32 accumulation)")
     ap.add_argument("--no-denominators", action="store_true",
                     help="skip the measured matrix-core and HBM copy peaks")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -310,6 +313,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.init()
+    if args.precision == "bf16" and args.config not in ("3", "4a", "4b"):
+        print("--precision bf16 applies to the large network (configs 3, 4a, 4b)", file=sys.stderr)
+        sys.exit(2)
     out = {"0": bench_single, "1": bench_sequential, "2": bench_replicas, "3": bench_large,
            "4a": bench_forward, "4b": bench_large}[args.config](args)
     if not args.no_denominators:
@@ -682,7 +688,8 @@ def bench_large(args):
     dev = torch.device("cuda:0")
     hip = HipEvents()
     prof = Profiler(hip)
-    net, shape = dq.NET_LARGE, di.NET_L
+    bf16 = args.precision == "bf16"
+    net, shape = (dq.NET_LARGE_BF16 if bf16 else dq.NET_LARGE), di.NET_L
     SIZE, SEED, LR, GAMMA = 1_000_000, 1003, 2.5e-4, 0.99
     if args.config == "3":
         B, C = 256, 1000
@@ -728,14 +735,20 @@ def bench_large(args):
     out["config"] = {
         "workload": f"{name}: large Q-network, batch {B}, 1,000,000-transition device replay, "
                     f"{K} sequential gather + TD-gradient + SGD steps"
-                    + (f", target network refreshed every {C} steps" if C else ""),
+                    + (f", target network refreshed every {C} steps" if C else "")
+                    + (", bf16-input MFMA contractions with fp32 accumulation" if bf16 else ""),
         "net": "conv32@8x8/4-conv64@4x4/2-conv64@3x3/1-fc512-fc18", "batch": B,
         "replay_transitions": SIZE, "update": "sgd", "lr": LR, "gamma": GAMMA,
         "target": f"refresh every {C}" if C else "theta"}
+    if bf16:
+        out["dtype"] = "bf16"
+        out["config"]["accumulate"] = "f32"
     out["transitions_per_s"] = round(out["value"] * B, 1)
     out["step_tflops"] = round(sum(v[0] for v in work.values()) * out["value"] / 1e12, 4)
     out["final_loss"] = final_loss
-    out["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us, args.config)
+    out["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us,
+                               args.config + (" bf16" if bf16 else ""),
+                               PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
                         "per_layer_tflops": {k: round(work[k][0] / (v[0] * 1e-6) / 1e12, 3)
                                              for k, v in bd.items() if work[k][0] > 0}}
@@ -745,7 +758,7 @@ def bench_large(args):
         n, c0 = 0, time.perf_counter()
         while True:
             s, sn, a, r, t = di.transitions_at(SEED, idx_host[n], shape.n_actions, SIZE)
-            res = oracle.td_gradient(shape, th, None, s, sn, a, r, t, float(F32(GAMMA)))
+            res = oracle.td_gradient(shape, th, None, s, sn, a, r, t, float(F32(GAMMA)), bf16=bf16)
             th, _ = oracle.apply_update("sgd", th, None, res["grad"], float(F32(LR)))
             n += 1
             el = time.perf_counter() - c0
@@ -754,7 +767,8 @@ def bench_large(args):
         out["cpu_baseline"] = {"value": round(n / el, 4), "unit": "steps/s",
                                "cores": oracle.num_threads(), "kind": "oracle",
                                "sample": f"first {n} step(s) of the same run (batch {B}), fp64 TD "
-                                         f"gradient + SGD, {el:.1f}s wall"}
+                                         f"gradient{' (bf16-input variant)' if bf16 else ''} + SGD, "
+                                         f"{el:.1f}s wall"}
     return out
 
 
@@ -766,7 +780,8 @@ def bench_forward(args):
     dev = torch.device("cuda:0")
     hip = HipEvents()
     prof = Profiler(hip)
-    net, shape = dq.NET_LARGE, di.NET_L
+    bf16 = args.precision == "bf16"
+    net, shape = (dq.NET_LARGE_BF16 if bf16 else dq.NET_LARGE), di.NET_L
     SIZE, SEED, B, EPS = 1_000_000, 1004, 8192, F32(0.05)
     K = args.steps or 200
     W = args.warmup if args.warmup is not None else 10
@@ -801,12 +816,17 @@ def bench_forward(args):
     out = base_record(K, W, ms)
     out["config"] = {
         "workload": "config 4a: large Q-network, epsilon-greedy (eps 0.05) forward pass over 8,192 "
-                    "states gathered from a 1,000,000-transition device replay",
+                    "states gathered from a 1,000,000-transition device replay"
+                    + (", bf16-input MFMA contractions with fp32 accumulation" if bf16 else ""),
         "net": "conv32@8x8/4-conv64@4x4/2-conv64@3x3/1-fc512-fc18", "batch": B,
         "replay_transitions": SIZE, "epsilon": float(EPS)}
+    if bf16:
+        out["dtype"] = "bf16"
+        out["config"]["accumulate"] = "f32"
     out["states_per_s"] = round(out["value"] * B, 1)
     out["step_tflops"] = round(sum(v[0] for v in work.values()) * out["value"] / 1e12, 4)
-    out["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us, "4a")
+    out["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us, "4a" + (" bf16" if bf16 else ""),
+                               PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
                         "per_layer_tflops": {k: round(work[k][0] / (v[0] * 1e-6) / 1e12, 3)
                                              for k, v in bd.items() if work[k][0] > 0}}
@@ -814,7 +834,7 @@ def bench_forward(args):
         n = 512
         s, _, _, _, _ = di.transitions_at(SEED, idx_host[0][:n], shape.n_actions, SIZE)
         c0 = time.perf_counter()
-        qr = oracle.forward_q(shape, th0, s)
+        qr = oracle.forward_q(shape, th0, s, bf16=bf16)
         oracle.select_actions(qr, float(EPS), di.egreedy_draws(B, SEED)[:n])
         el = time.perf_counter() - c0
         out["cpu_baseline"] = {"value": round(n / el / B, 5), "unit": "steps/s",

@@ -51,7 +51,19 @@ typedef enum {
     DQN_EUNSUPPORTED = -4   /* network shape or precision not supported */
 } dqn_status;
 
-enum { DQN_FP32 = 0 };
+/* Arithmetic of the layer contractions (dqn_net.precision):
+ *   DQN_FP32  float32 operands and accumulation (the first conv layer runs
+ *             its byte inputs against an exact three-term bfloat16 split of
+ *             each float32 weight, which reproduces float32 products);
+ *   DQN_BF16  the bf16-input variant, large network only: every operand of
+ *             the conv and fc1 contractions (weights, input activations,
+ *             back-propagated gradients) is rounded to bfloat16 (round to
+ *             nearest, ties to even) and the products are accumulated in
+ *             float32.  Input bytes are exact in bfloat16 and the 1/255 scale
+ *             is applied to the float32 sum.  The output layer, the TD target
+ *             and loss, bias gradients, ReLU decisions and the update stay
+ *             float32.  The small network returns DQN_EUNSUPPORTED. */
+enum { DQN_FP32 = 0, DQN_BF16 = 1 };
 
 typedef struct {
     int32_t in_c, in_h, in_w;      /* 4, 84, 84 */
@@ -61,7 +73,7 @@ typedef struct {
     int32_t conv_stride[3];
     int32_t fc_hidden;             /* 256 or 512 */
     int32_t n_actions;             /* 6 or 18 */
-    int32_t precision;             /* DQN_FP32 */
+    int32_t precision;             /* DQN_FP32 or DQN_BF16 */
 } dqn_net;
 
 /* Replay memory (Sec. III.C): the last N experiences.  Record i holds the

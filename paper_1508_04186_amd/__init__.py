@@ -10,7 +10,7 @@ or PyTorch fallback, and loading fails loudly when the library is missing.
 from .native import (  # noqa: F401
     DQN_OK, DQN_EINVAL, DQN_EWORKSPACE, DQN_EHIP, DQN_EUNSUPPORTED,
     PS_SGD, PS_RMSPROP, PS_ADAGRAD, DQN_OP_FORWARD, DQN_OP_TD_GRADIENT,
-    DqnError, Net, NET_SMALL, NET_LARGE, Replay,
+    DqnError, Net, NET_SMALL, NET_LARGE, NET_LARGE_BF16, DQN_FP32, DQN_BF16, Replay,
     lib, lib_path, dqn_param_count, dqn_param_offset, dqn_workspace_bytes,
     replay_gather, dqn_forward, dqn_td_gradient, dqn_td_gradient_replay, ps_apply_update,
     dqn_status_string,

@@ -19,12 +19,13 @@ struct NetInfo {
     int H, A, flat;
     int64_t P;
     int64_t w_off[5], b_off[5];  // conv layers, then fc1, fc2
+    bool bf16;                   // DQN_BF16: bf16-input contractions
 };
 
 // Only the two network shapes the kernels are built for are accepted.
 int identify(const dqn_net* net, NetInfo* ni) {
     if (!net) return DQN_EINVAL;
-    if (net->precision != DQN_FP32) return DQN_EUNSUPPORTED;
+    if (net->precision != DQN_FP32 && net->precision != DQN_BF16) return DQN_EUNSUPPORTED;
     if (net->in_c != 4 || net->in_h != 84 || net->in_w != 84) return DQN_EUNSUPPORTED;
     if (net->n_conv == 2 && net->conv_out[0] == 16 && net->conv_k[0] == 8 && net->conv_stride[0] == 4 &&
         net->conv_out[1] == 32 && net->conv_k[1] == 4 && net->conv_stride[1] == 2 &&
@@ -47,6 +48,9 @@ int identify(const dqn_net* net, NetInfo* ni) {
     } else {
         return DQN_EUNSUPPORTED;
     }
+    // The bf16-input variant is built for the large network.
+    ni->bf16 = net->precision == DQN_BF16;
+    if (ni->bf16 && ni->n_conv != 3) return DQN_EUNSUPPORTED;
     int64_t off = 0;
     for (int l = 0; l < ni->n_conv; ++l) {
         ni->d[l] = conv_dims(ni->conv[l]);
@@ -89,9 +93,19 @@ constexpr int kIgemmMinRows = 128;
 // Backward layers that run as implicit GEMMs at batch B (measured faster
 // than the per-layer kernels from 128 samples: the weight gradients of
 // conv2/conv3 and the input gradient of conv3 of the large network; its
-// conv1 weight gradient uses a dedicated kernel from the same size).
-bool igemm_wgrad(ConvId id, int B) { return (id == CONV_L2 || id == CONV_L3) && B >= kIgemmMinRows; }
-bool igemm_dgrad(ConvId id, int B) { return id == CONV_L3 && B >= kIgemmMinRows; }
+// conv1 weight gradient uses a dedicated kernel from the same size).  The
+// bf16-input variant runs every large-network layer on these kernels (and
+// conv1 on the byte-input kernels) at any batch.
+bool igemm_wgrad(ConvId id, int B, bool bf16) {
+    return (id == CONV_L2 || id == CONV_L3) && (bf16 || B >= kIgemmMinRows);
+}
+bool igemm_dgrad(ConvId id, int B, bool bf16) {
+    return (id == CONV_L3 && B >= kIgemmMinRows) || (bf16 && (id == CONV_L2 || id == CONV_L3));
+}
+bool igemm_fwd(ConvId id, int rows, bool bf16) {
+    return conv_igemm_fwd_supported(id) && (bf16 || rows >= kIgemmMinRows);
+}
+bool conv1_u8(ConvId id, int rows, bool bf16) { return id == CONV_L1 && (bf16 || rows >= kIgemmMinRows); }
 
 // fc1 forward split-K: enough slices that the launch covers the chip.
 struct Carver {
@@ -142,9 +156,9 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
         int64_t slots = t.chunks[l];
         if (l == 0 && ni.n_conv == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]))
             slots = std::max<int64_t>(slots, conv_s12_bwd_slots(B));
-        if (igemm_wgrad(ni.conv[l], B)) slots = std::max<int64_t>(slots, conv_igemm_wgrad_chunks(ni.conv[l], B));
-        if (l == 0 && ni.conv[0] == CONV_L1 && B >= kIgemmMinRows)
-            slots = std::max<int64_t>(slots, conv1_u8_wgrad_slots(B));
+        if (igemm_wgrad(ni.conv[l], B, ni.bf16))
+            slots = std::max<int64_t>(slots, conv_igemm_wgrad_chunks(ni.conv[l], B));
+        if (l == 0 && conv1_u8(ni.conv[0], B, ni.bf16)) slots = std::max<int64_t>(slots, conv1_u8_wgrad_slots(B));
         t.wpart[l] = cv.take<float>(ws, slots * c.cout * c.cin * c.k * c.k);
         t.bpart[l] = cv.take<float>(ws, slots * c.cout);
     }
@@ -264,6 +278,9 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
         s0 = ConvIn{src.s, nullptr, rec, 0};
         sn0 = ConvIn{src.s_next, nullptr, rec, 0};
     }
+    // The bf16-input variant reads the network input with the byte-input
+    // conv1 kernels, which need 16-byte aligned samples.
+    if (ni.bf16 && (!conv_s12_fwd_aligned(s0) || !conv_s12_fwd_aligned(sn0))) return DQN_EINVAL;
 
     // Forward of s under theta (samples 0..B-1) and of s' under theta^-
     // (samples B..2B-1): one launch per layer, or both conv layers of the
@@ -277,20 +294,21 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
                                 tt + ni.b_off[1], t.act[0], t.act[1], src.replay ? &side : nullptr, st));
     for (int l = 0; l < L && !fused_fwd; ++l) {
         const int64_t ae = l > 0 ? act_elems(ni.d[l - 1]) : 0;
-        if (l == 0 && ni.conv[0] == CONV_L1 && 2 * B >= kIgemmMinRows && conv_s12_fwd_aligned(s0) &&
+        if (l == 0 && conv1_u8(ni.conv[0], 2 * B, ni.bf16) && conv_s12_fwd_aligned(s0) &&
             conv_s12_fwd_aligned(sn0)) {
             RUN(DQN_K_CONV1_FWD,
                 launch_conv1_u8_fwd(CONV_L1, s0, sn0, B, 2 * B, th + ni.w_off[0], th + ni.b_off[0],
                                     tt + ni.w_off[0], tt + ni.b_off[0], t.act[0],
-                                    src.replay ? &side : nullptr, st));
+                                    src.replay ? &side : nullptr, ni.bf16, st));
             continue;
         }
-        if (l > 0 && conv_igemm_fwd_supported(ni.conv[l]) && 2 * B >= kIgemmMinRows) {
+        if (l > 0 && igemm_fwd(ni.conv[l], 2 * B, ni.bf16)) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], t.act[l - 1], B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
-                                      tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], st));
+                                      tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], ni.bf16, st));
             continue;
         }
+        if (ni.bf16) return DQN_EUNSUPPORTED;  // the per-layer kernels are fp32 only
         const ConvIn in_a = l == 0 ? s0 : ConvIn{t.act[l - 1], nullptr, ae * 4, 0};
         const ConvIn in_b = l == 0 ? sn0 : ConvIn{t.act[l - 1] + (int64_t)B * ae, nullptr, ae * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
@@ -304,15 +322,15 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     if (tt == th) {
         RUN(DQN_K_FC1_FWD,
             launch_gemm(GEMM_NT, 2 * B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
-                        t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, st));
+                        t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, ni.bf16, st));
     } else {
         RUN(DQN_K_FC1_FWD,
             launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
-                        t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, st));
+                        t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, ni.bf16, st));
         RUN(DQN_K_FC1_FWD,
             launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast + (int64_t)B * ni.flat, ni.flat,
                         tt + ni.w_off[L], ni.flat, t.fc1p + (int64_t)B * ni.H, ni.H, t.ks,
-                        t.kchunk, slice, nullptr, st));
+                        t.kchunk, slice, nullptr, ni.bf16, st));
     }
     HeadTdArgs h{};
     h.fc1p = t.fc1p;
@@ -343,14 +361,14 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     if (paired) {
         RUN(DQN_K_FC1_BWD,
             launch_gemm_wgrad_dgrad(ni.H, ni.flat, B, t.dz1, xlast, grad_out + ni.w_off[L],
-                                    th + ni.w_off[L], t.dconv[L - 1], st));
+                                    th + ni.w_off[L], t.dconv[L - 1], ni.bf16, st));
     } else {
         RUN(DQN_K_FC1_WGRAD,
             launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat,
-                        grad_out + ni.w_off[L], ni.flat, 1, (B + 31) / 32 * 32, 0, nullptr, st));
+                        grad_out + ni.w_off[L], ni.flat, 1, (B + 31) / 32 * 32, 0, nullptr, ni.bf16, st));
         RUN(DQN_K_FC1_DGRAD,
             launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
-                        t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, st));
+                        t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, ni.bf16, st));
     }
     // The small network's conv layers in one launch: conv2's weight gradient,
     // and conv2's input gradient with conv1's weight gradient per (sample,
@@ -368,28 +386,30 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     for (int l = L - 1; l >= 0 && !fused_bwd; --l) {
         const ConvIn in = l == 0 ? s0 : ConvIn{t.act[l - 1], nullptr, act_elems(ni.d[l - 1]) * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
-        if (l > 0 && paired) {
+        if (l > 0 && paired && !ni.bf16) {
             RUN(DQN_K_CONV2_BWD + (l - 1),
                 launch_conv_bwd(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l],
                                 th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], st));
             continue;
         }
-        if (l == 0 && ni.conv[0] == CONV_L1 && B >= kIgemmMinRows && conv_s12_fwd_aligned(s0)) {
+        if (l == 0 && conv1_u8(ni.conv[0], B, ni.bf16) && conv_s12_fwd_aligned(s0)) {
             RUN(DQN_K_CONV1_WGRAD,
-                launch_conv1_u8_wgrad(CONV_L1, s0, t.dconv[0], B, t.wpart[0], t.bpart[0], scale, st));
+                launch_conv1_u8_wgrad(CONV_L1, s0, t.dconv[0], B, t.wpart[0], t.bpart[0], scale, ni.bf16, st));
             chunks_used[0] = conv1_u8_wgrad_slots(B);
-        } else if (igemm_wgrad(ni.conv[l], B)) {
+        } else if (igemm_wgrad(ni.conv[l], B, ni.bf16)) {
             RUN(DQN_K_CONV1_WGRAD + l,
-                launch_conv_igemm_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
+                launch_conv_igemm_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale,
+                                        ni.bf16, st));
             chunks_used[l] = conv_igemm_wgrad_chunks(ni.conv[l], B);
         } else {
+            if (ni.bf16) return DQN_EUNSUPPORTED;  // the per-layer kernels are fp32 only
             RUN(DQN_K_CONV1_WGRAD + l,
                 launch_conv_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
         }
-        if (l > 0 && igemm_dgrad(ni.conv[l], B))
+        if (l > 0 && igemm_dgrad(ni.conv[l], B, ni.bf16))
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
                 launch_conv_igemm_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],
-                                        t.dconv[l - 1], B, st));
+                                        t.dconv[l - 1], B, ni.bf16, st));
         else if (l > 0)
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
                 launch_conv_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],
@@ -549,18 +569,19 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
                                 th + ni.w_off[1], th + ni.b_off[1], th + ni.w_off[0], th + ni.b_off[0],
                                 th + ni.w_off[1], th + ni.b_off[1], f.act[0], f.act[1], nullptr, st));
     for (int l = 0; l < ni.n_conv && !fused_fwd; ++l) {
-        if (l == 0 && ni.conv[0] == CONV_L1 && batch >= kIgemmMinRows && conv_s12_fwd_aligned(in0)) {
+        if (l == 0 && conv1_u8(ni.conv[0], batch, ni.bf16) && conv_s12_fwd_aligned(in0)) {
             RUN(DQN_K_CONV1_FWD,
                 launch_conv1_u8_fwd(CONV_L1, in0, in0, batch, batch, th + ni.w_off[0], th + ni.b_off[0],
-                                    th + ni.w_off[0], th + ni.b_off[0], f.act[0], nullptr, st));
+                                    th + ni.w_off[0], th + ni.b_off[0], f.act[0], nullptr, ni.bf16, st));
             continue;
         }
-        if (l > 0 && conv_igemm_fwd_supported(ni.conv[l]) && batch >= kIgemmMinRows) {
+        if (l > 0 && igemm_fwd(ni.conv[l], batch, ni.bf16)) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], f.act[l - 1], batch, batch, th + ni.w_off[l], th + ni.b_off[l],
-                                      th + ni.w_off[l], th + ni.b_off[l], f.act[l], st));
+                                      th + ni.w_off[l], th + ni.b_off[l], f.act[l], ni.bf16, st));
             continue;
         }
+        if (ni.bf16) return DQN_EUNSUPPORTED;  // the per-layer kernels are fp32 only
         const ConvIn in = l == 0 ? in0
                                  : ConvIn{f.act[l - 1], nullptr, act_elems(ni.d[l - 1]) * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
@@ -571,7 +592,7 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
     const int L = ni.n_conv;
     RUN(DQN_K_FC1_FWD,
         launch_gemm(GEMM_NT, batch, ni.H, ni.flat, f.act[L - 1], ni.flat, th + ni.w_off[L], ni.flat,
-                    f.fc1p, ni.H, f.ks, f.kchunk, (int64_t)batch * ni.H, nullptr, st));
+                    f.fc1p, ni.H, f.ks, f.kchunk, (int64_t)batch * ni.H, nullptr, ni.bf16, st));
     HeadFwdArgs h{};
     h.fc1p = f.fc1p;
     h.ks = f.ks;

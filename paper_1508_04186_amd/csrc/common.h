@@ -18,6 +18,31 @@ __device__ __forceinline__ f4 mfma16x16x4(float a, float b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// One v_mfma_f32_16x16x32_bf16: D[16x16] += A[16x32] * B[32x16] over a wave.
+// Lane l supplies A[l%16][8*(l/16) + e] and B[8*(l/16) + e][l%16] in element
+// e of its operands; D as mfma16x16x4.
+__device__ __forceinline__ f4 mfma16x16x32bf16(bf16x8 a, bf16x8 b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Operand of the bf16-input contraction step over 32 k-values staged in
+// fp32: element e holds the value at k = 4e + g for lane group g (the
+// contraction is a sum over k, so any assignment of k to (g, e) that both
+// operands share is valid; this one reads, for each e, the addresses the
+// fp32 step kk = e reads, so the LDS access pattern is unchanged).  at(k)
+// returns the staged fp32 value; the conversion rounds to nearest, ties to
+// even.
+template <class At>
+__device__ __forceinline__ bf16x8 bf16_operand(At at, int g) {
+    bf16x8 v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (__bf16)at(4 * e + g);
+    return v;
+}
+
 // Parameter-server update of one parameter theta with gradient g and
 // optimizer state st: RULE 0 gradient descent (Sec. III.B), 1 RMSProp (Alg. 2
 // RMSPROPUPDATE: r <- decay*r + (1-decay)*g^2, theta <- theta - lr*g/sqrt(r),
@@ -128,6 +153,10 @@ hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float*
                                int batch, float* wpart2, float* bpart2, float* wpart1, float* bpart1,
                                hipStream_t st);
 
+// The implicit-GEMM launchers below and the fc GEMMs take `bf16`: false
+// contracts the fp32 operands on fp32 MFMA; true is the bf16-input variant
+// (both operands rounded to bfloat16, nearest-even, fp32 accumulation).
+
 // Forward of the fp32-input large-network layers (CONV_L2, CONV_L3) as one
 // implicit GEMM over all n samples (dense input [n][cin][ih][iw]; samples
 // below n_a use (w_a, b_a), the rest (w_b, b_b)); bias + ReLU; output
@@ -135,12 +164,12 @@ hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float*
 bool conv_igemm_fwd_supported(ConvId id);
 hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, const float* w_a,
                                  const float* b_a, const float* w_b, const float* b_b, float* out,
-                                 hipStream_t st);
+                                 bool bf16, hipStream_t st);
 
 // Input gradient of CONV_L2 / CONV_L3 for n samples as an implicit GEMM per
 // stride phase, masked by [h_in > 0] (as launch_conv_dgrad).
 hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, const float* h_in, float* din,
-                                   int n, hipStream_t st);
+                                   int n, bool bf16, hipStream_t st);
 
 // Weight/bias gradient partial sums of a large-network layer for n samples as
 // an implicit GEMM over pixel chunks: conv_igemm_wgrad_chunks(id, n) slots of
@@ -148,15 +177,16 @@ hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, c
 // (bytes for CONV_L1, addressed through in.idx when set; floats otherwise).
 int conv_igemm_wgrad_chunks(ConvId id, int n);
 hipError_t launch_conv_igemm_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
-                                   float* bpart, float in_scale, hipStream_t st);
+                                   float* bpart, float in_scale, bool bf16, hipStream_t st);
 
 // conv1 forward on byte input (CONV_L1 or CONV_S1) for many samples, on bf16
-// MFMA with an exact three-term split of the fp32 weights; roles and
-// alignment as launch_conv_s12_fwd; output [n][cout][20][20].
+// MFMA with an exact three-term split of the fp32 weights (bf16: the weights
+// rounded to bfloat16 instead); roles and alignment as launch_conv_s12_fwd;
+// output [n][cout][20][20].
 bool conv1_u8_fwd_supported(ConvId id);
 hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
                                const float* w_a, const float* b_a, const float* w_b, const float* b_b,
-                               float* out, const SideFields* side, hipStream_t st);
+                               float* out, const SideFields* side, bool bf16, hipStream_t st);
 
 // conv1 weight/bias gradient on byte input (CONV_L1 or CONV_S1) for many
 // samples: conv1_u8_wgrad_slots(n) partial-sum slots of wpart
@@ -164,7 +194,7 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
 // [n][cout][20][20].
 int conv1_u8_wgrad_slots(int n);
 hipError_t launch_conv1_u8_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
-                                 float* bpart, float in_scale, hipStream_t st);
+                                 float* bpart, float in_scale, bool bf16, hipStream_t st);
 
 // Weight and bias gradient partial sums over sample chunks:
 // wpart [chunks][cout][cin*k*k], bpart [chunks][cout].
@@ -194,13 +224,13 @@ enum GemmKind { GEMM_NT = 0, GEMM_TN = 1, GEMM_NN = 2 };
 void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk);
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
-                       const float* mask, hipStream_t st);
+                       const float* mask, bool bf16, hipStream_t st);
 
 // fc1 backward for batch B: dW [H][F] = dz1^T x (x = first B rows of the last
 // conv output) and dx [B][F] = (dz1 W) masked by [x > 0], as one launch where
 // possible.
 hipError_t launch_gemm_wgrad_dgrad(int H, int F, int B, const float* dz1, const float* x,
-                                   float* dW, const float* W, float* dx, hipStream_t st);
+                                   float* dW, const float* W, float* dx, bool bf16, hipStream_t st);
 
 struct HeadTdArgs {
     const float* fc1p;   // [ks][2B][H] split-K partials of fc1 (rows < B: s, >= B: s')

@@ -27,8 +27,6 @@
 namespace dqn {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 // Small-network geometry.
 constexpr int C0 = 4, H0 = 84;                   // input channels, side
@@ -56,9 +54,6 @@ constexpr int OFF_B = OFF_W2 + C2 * RO2 * 4;               // f32 b1[C1], b2[C2]
 constexpr int LDS_BYTES = OFF_B + (C1 + C2) * 4;
 static_assert(OFF_W1 % 16 == 0 && OFF_A1 % 16 == 0 && OFF_W2 % 16 == 0 && OFF_B % 16 == 0, "alignment");
 
-__device__ __forceinline__ f4 mfma16x16x32bf16(bf16x8 a, bf16x8 b, f4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
 
 // Exact split of an fp32 value into three bf16 terms, w = hi + mid + lo: each
 // remainder is exactly representable in fp32, and after two terms at most 8
@@ -664,8 +659,9 @@ hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float*
 // ---------------------------------------------------------------------------
 // conv1 forward on byte input (4 channels 84x84, 8x8 stride 4 -> 20x20) for
 // many samples: a workgroup splits its weights into three bf16 planes once
-// (exact, as above), then walks its samples with the next sample's bytes
-// loaded into registers while the current one is computed.  Each wave runs
+// (exact, as above; PARTS = 3), or rounds them to one bf16 plane (the
+// bf16-input variant; PARTS = 1), then walks its samples with the next
+// sample's bytes loaded into registers while the current one is computed.  Each wave runs
 // its M-tiles (16 pixels) for every N-tile as independent accumulator
 // chains; the A operand is converted from the staged bytes as it is built.
 namespace dqn {
@@ -679,7 +675,7 @@ struct U8FwdParams {
     SideFields side;
 };
 
-template <int COUT>
+template <int COUT, int PARTS>
 __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
     constexpr int REC = C0 * H0 * H0;            // bytes per sample (28,224)
     constexpr int RV = REC / 16;                 // 16-byte units (1,764)
@@ -691,8 +687,9 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
     static_assert(REC % 16 == 0 && (H1 * H1) % 16 == 0, "whole tiles");
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char* s_in = smem;                  // u8 [REC]
-    __bf16* s_w = (__bf16*)(smem + ((REC + 15) / 16) * 16);  // bf16 [3][COUT][RS1]
-    float* s_b = (float*)(s_w + 3 * PL);
+    __bf16* s_w = (__bf16*)(smem + ((REC + 15) / 16) * 16);  // bf16 [PARTS][COUT][RS1]
+    float* s_b = (float*)(s_w + PARTS * PL);
+    static_assert(PARTS == 1 || PARTS == 3, "exact split or bf16 rounding");
 
     const bool second = (int)blockIdx.x >= p.blocks_a;
     const int blk = second ? (int)blockIdx.x - p.blocks_a : (int)blockIdx.x;
@@ -732,7 +729,7 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
         }
     };
 
-    // weights -> three exact bf16 planes [part][o][k]; bias
+    // weights -> PARTS bf16 planes [part][o][k] (exact split, or rounding); bias
     load_in(j0);
     for (int e = t; e < COUT * KW1 / 4; e += WG) {
         const f4 w = ((const f4*)W)[e];
@@ -747,8 +744,10 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
             l[i] = lo;
         }
         *(bf16x4*)(s_w + 0 * PL + o * RS1 + k) = h;
-        *(bf16x4*)(s_w + 1 * PL + o * RS1 + k) = m;
-        *(bf16x4*)(s_w + 2 * PL + o * RS1 + k) = l;
+        if constexpr (PARTS == 3) {
+            *(bf16x4*)(s_w + 1 * PL + o * RS1 + k) = m;
+            *(bf16x4*)(s_w + 2 * PL + o * RS1 + k) = l;
+        }
     }
     if (t < COUT) s_b[t] = bias[t];
 
@@ -777,11 +776,11 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
 #pragma unroll
         for (int kb = 0; kb < KW1 / 32; ++kb) {
             const int c = kb >> 1, ky = (kb & 1) * 4 + g;
-            bf16x8 b[NT][3];
+            bf16x8 b[NT][PARTS];
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-                for (int part = 0; part < 3; ++part)
+                for (int part = 0; part < PARTS; ++part)
                     b[nt][part] = *(const bf16x8*)(s_w + part * PL + (nt * 16 + li) * RS1 + kb * 32 + 8 * g);
 #pragma unroll
             for (int i = 0; i < MPW; ++i) {
@@ -794,7 +793,7 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
                     a[4 + q] = (__bf16)(float)((w1 >> (8 * q)) & 0xffu);
                 }
 #pragma unroll
-                for (int part = 0; part < 3; ++part)
+                for (int part = 0; part < PARTS; ++part)
 #pragma unroll
                     for (int nt = 0; nt < NT; ++nt) acc[i][nt] = mfma16x16x32bf16(a, b[nt][part], acc[i][nt]);
             }
@@ -826,7 +825,7 @@ bool conv1_u8_fwd_supported(ConvId id) { return id == CONV_L1 || id == CONV_S1; 
 
 hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
                                const float* w_a, const float* b_a, const float* w_b, const float* b_b,
-                               float* out, const SideFields* side, hipStream_t st) {
+                               float* out, const SideFields* side, bool bf16, hipStream_t st) {
     if (n <= 0 || n_a < 0 || n_a > n || !conv_s12_fwd_aligned(in_a) || !conv_s12_fwd_aligned(in_b) ||
         ((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15))
         return hipErrorInvalidValue;
@@ -835,14 +834,14 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
     const int blocks_a = (n_a + spb - 1) / spb, blocks_b = (n - n_a + spb - 1) / spb;
     U8FwdParams prm{in_a, in_b, n_a, n, spb, blocks_a, w_a, b_a, w_b, b_b, out, side ? *side : SideFields{}};
     const dim3 grid((unsigned)std::max(1, blocks_a + blocks_b));
-    auto go = [&](auto kern, int cout) -> hipError_t {
-        const size_t lds = ((C0 * H0 * H0 + 15) / 16) * 16 + (size_t)3 * cout * RS1 * 2 + (size_t)cout * 4;
+    auto go = [&](auto kern, int cout, int parts) -> hipError_t {
+        const size_t lds = ((C0 * H0 * H0 + 15) / 16) * 16 + (size_t)parts * cout * RS1 * 2 + (size_t)cout * 4;
         if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
         hipLaunchKernelGGL(kern, grid, dim3(WG), lds, st, prm);
         return hipGetLastError();
     };
-    if (id == CONV_L1) return go(conv1_u8_fwd_kernel<32>, 32);
-    if (id == CONV_S1) return go(conv1_u8_fwd_kernel<16>, 16);
+    if (id == CONV_L1) return bf16 ? go(conv1_u8_fwd_kernel<32, 1>, 32, 1) : go(conv1_u8_fwd_kernel<32, 3>, 32, 3);
+    if (id == CONV_S1) return bf16 ? go(conv1_u8_fwd_kernel<16, 1>, 16, 1) : go(conv1_u8_fwd_kernel<16, 3>, 16, 3);
     return hipErrorInvalidValue;
 }
 
@@ -854,6 +853,8 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
 // sample it stages the input bytes and dz, then each wave contracts the 400
 // pixels for 2 M-tiles (output channels) x NTW N-tiles (weight columns),
 // every accumulator chain independent; lane group g takes pixel 4*st + g.
+// The bf16-input variant rounds dz to bfloat16 (the bytes are exact) and
+// contracts 32 pixels per step, pixel 32*st + 4*e + g in element e.
 namespace dqn {
 namespace {
 
@@ -866,7 +867,7 @@ struct U8WgradParams {
     float in_scale;
 };
 
-template <int COUT>
+template <int COUT, bool BF16>
 __global__ __launch_bounds__(WG) void conv1_u8_wgrad_kernel(U8WgradParams p) {
     constexpr int REC = C0 * H0 * H0;
     constexpr int RV = REC / 16, RPER = (RV + WG - 1) / WG;
@@ -938,21 +939,46 @@ __global__ __launch_bounds__(WG) void conv1_u8_wgrad_kernel(U8WgradParams p) {
             }
             bsum += (s0 + s1) + (s2 + s3);
         }
-        // pixel q = 4*st + g: row q/20, column q%20 (a step stays in one row)
+        if constexpr (BF16) {
+            // pixel q = 32*st + 4*e + g; the 4 lane groups stay in one row
+            // (20 is a multiple of 4); the last step covers pixels 384..399
+            constexpr int STEPS = (P1 + 31) / 32;
+            for (int st = 0; st < STEPS; ++st) {
+                bf16x8 a[MT], b[NTW];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const bool v = 32 * st + 4 * e < P1;     // uniform across the wave
+                    const int q0 = v ? 32 * st + 4 * e : 0;    // no address past the tile
+                    const int y = q0 / H1, x = q0 % H1 + g;
+                    const int po = S1 * y * H0 + S1 * x;
+#pragma unroll
+                    for (int m = 0; m < MT; ++m)
+                        a[m][e] = v ? (__bf16)s_dz[(m * 16 + li) * LDZ + q0 + g] : (__bf16)0.f;
+#pragma unroll
+                    for (int i = 0; i < NTW; ++i) b[i][e] = v ? (__bf16)(float)s_in[koff[i] + po] : (__bf16)0.f;
+                }
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+#pragma unroll
+                    for (int i = 0; i < NTW; ++i) acc[m][i] = mfma16x16x32bf16(a[m], b[i], acc[m][i]);
+            }
+        } else {
+            // pixel q = 4*st + g: row q/20, column q%20 (a step stays in one row)
 #pragma unroll 2
-        for (int st = 0; st < P1 / 4; ++st) {
-            const int q = 4 * st + g;
-            const int y = (4 * st) / H1, x = (4 * st) % H1 + g;
-            const int po = S1 * y * H0 + S1 * x;
-            float a[MT], b[NTW];
+            for (int st = 0; st < P1 / 4; ++st) {
+                const int q = 4 * st + g;
+                const int y = (4 * st) / H1, x = (4 * st) % H1 + g;
+                const int po = S1 * y * H0 + S1 * x;
+                float a[MT], b[NTW];
 #pragma unroll
-            for (int m = 0; m < MT; ++m) a[m] = s_dz[(m * 16 + li) * LDZ + q];
+                for (int m = 0; m < MT; ++m) a[m] = s_dz[(m * 16 + li) * LDZ + q];
 #pragma unroll
-            for (int i = 0; i < NTW; ++i) b[i] = (float)s_in[koff[i] + po];
+                for (int i = 0; i < NTW; ++i) b[i] = (float)s_in[koff[i] + po];
 #pragma unroll
-            for (int m = 0; m < MT; ++m)
+                for (int m = 0; m < MT; ++m)
 #pragma unroll
-                for (int i = 0; i < NTW; ++i) acc[m][i] = mfma16x16x4(a[m], b[i], acc[m][i]);
+                    for (int i = 0; i < NTW; ++i) acc[m][i] = mfma16x16x4(a[m], b[i], acc[m][i]);
+            }
         }
     }
     // D[4g + r][li] of tile (m, i): channel m*16 + 4g + r, column (wave*NTW + i)*16 + li
@@ -975,7 +1001,7 @@ int conv1_u8_wgrad_slots(int n) {
 }
 
 hipError_t launch_conv1_u8_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
-                                 float* bpart, float in_scale, hipStream_t st) {
+                                 float* bpart, float in_scale, bool bf16, hipStream_t st) {
     if (n <= 0 || !conv_s12_fwd_aligned(in) || in.off != 0 || ((uintptr_t)dz & 15)) return hipErrorInvalidValue;
     const int spb = std::max(1, (n + 511) / 512);
     const int blocks = (n + spb - 1) / spb;
@@ -986,8 +1012,8 @@ hipError_t launch_conv1_u8_wgrad(ConvId id, const ConvIn& in, const float* dz, i
         hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(WG), lds, st, prm);
         return hipGetLastError();
     };
-    if (id == CONV_L1) return go(conv1_u8_wgrad_kernel<32>, 32);
-    if (id == CONV_S1) return go(conv1_u8_wgrad_kernel<16>, 16);
+    if (id == CONV_L1) return bf16 ? go(conv1_u8_wgrad_kernel<32, true>, 32) : go(conv1_u8_wgrad_kernel<32, false>, 32);
+    if (id == CONV_S1) return bf16 ? go(conv1_u8_wgrad_kernel<16, true>, 16) : go(conv1_u8_wgrad_kernel<16, false>, 16);
     return hipErrorInvalidValue;
 }
 

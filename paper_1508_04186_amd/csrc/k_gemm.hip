@@ -4,7 +4,9 @@
 // k-steps of BK (32, or 128 for long contractions so that fewer dependent
 // global round trips are needed) staged through LDS, with the next step's
 // global loads issued before the current step's MFMAs; four waves in a 2x2
-// arrangement.
+// arrangement.  The bf16-input variant rounds both staged operands to
+// bfloat16 as it reads them and runs one v_mfma_f32_16x16x32_bf16 per 32
+// k-values instead of eight fp32 steps.
 #include <algorithm>
 
 #include "common.h"
@@ -45,7 +47,7 @@ struct GemmSmem {
     static constexpr size_t bytes = (size_t)(NA + NB) * 4;
 };
 
-template <int BM, int BN, int BK, bool TA, bool TB, bool MASK>
+template <int BM, int BN, int BK, bool TA, bool TB, bool MASK, bool BF16>
 __device__ __forceinline__ void gemm_body(const GemmParams& p, int bx, int by, int bz, float* smem) {
     using SM = GemmSmem<BM, BN, BK, TA, TB>;
     const int M = p.M, N = p.N, K = p.K, lda = p.lda, ldb = p.ldb, ldc = p.ldc, kchunk = p.kchunk;
@@ -138,17 +140,35 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, int bx, int by, i
         store();
         __syncthreads();
         if (k0 + BK < kend) load(k0 + BK);   // in flight during the MFMAs below
+        if constexpr (BF16) {
+            // one bf16-input step per 32 k-values (bf16_operand's k order)
 #pragma unroll
-        for (int kk = 0; kk < BK / 4; ++kk) {
-            float a[TM], b[TN];
+            for (int kb = 0; kb < BK / 32; ++kb) {
+                bf16x8 a[TM], b[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = a_at(wm + i * 16 + li, kk * 4 + g);
+                for (int i = 0; i < TM; ++i)
+                    a[i] = bf16_operand([&](int k) { return a_at(wm + i * 16 + li, kb * 32 + k); }, g);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) b[j] = b_at(kk * 4 + g, wn + j * 16 + li);
+                for (int j = 0; j < TN; ++j)
+                    b[j] = bf16_operand([&](int k) { return b_at(kb * 32 + k, wn + j * 16 + li); }, g);
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+                for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x4(a[i], b[j], acc[i][j]);
+                    for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x32bf16(a[i], b[j], acc[i][j]);
+            }
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < BK / 4; ++kk) {
+                float a[TM], b[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) a[i] = a_at(wm + i * 16 + li, kk * 4 + g);
+#pragma unroll
+                for (int j = 0; j < TN; ++j) b[j] = b_at(kk * 4 + g, wn + j * 16 + li);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x4(a[i], b[j], acc[i][j]);
+            }
         }
         __syncthreads();
     }
@@ -171,35 +191,35 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, int bx, int by, i
         }
 }
 
-template <int BM, int BN, int BK, bool TA, bool TB, bool MASK>
+template <int BM, int BN, int BK, bool TA, bool TB, bool MASK, bool BF16>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
     extern __shared__ __align__(16) float smem[];
-    gemm_body<BM, BN, BK, TA, TB, MASK>(p, blockIdx.x, blockIdx.y, blockIdx.z, smem);
+    gemm_body<BM, BN, BK, TA, TB, MASK, BF16>(p, blockIdx.x, blockIdx.y, blockIdx.z, smem);
 }
 
 // Two independent GEMMs in one launch (flattened block index; the first
 // n1 = g1x*g1y*g1z blocks run GEMM 1).
 template <int BM1, int BN1, int BK1, bool TA1, bool TB1, bool M1,
-          int BM2, int BN2, int BK2, bool TA2, bool TB2, bool M2>
+          int BM2, int BN2, int BK2, bool TA2, bool TB2, bool M2, bool BF16>
 __global__ __launch_bounds__(256) void gemm_pair_kernel(GemmParams p1, int g1x, int g1y, GemmParams p2,
                                                         int g2x, int g2y, int n1) {
     extern __shared__ __align__(16) float smem[];
     int b = blockIdx.x;
     if (b < n1) {
-        gemm_body<BM1, BN1, BK1, TA1, TB1, M1>(p1, b % g1x, (b / g1x) % g1y, b / (g1x * g1y), smem);
+        gemm_body<BM1, BN1, BK1, TA1, TB1, M1, BF16>(p1, b % g1x, (b / g1x) % g1y, b / (g1x * g1y), smem);
     } else {
         b -= n1;
-        gemm_body<BM2, BN2, BK2, TA2, TB2, M2>(p2, b % g2x, (b / g2x) % g2y, b / (g2x * g2y), smem);
+        gemm_body<BM2, BN2, BK2, TA2, TB2, M2, BF16>(p2, b % g2x, (b / g2x) % g2y, b / (g2x * g2y), smem);
     }
 }
 
-template <int BM, int BN, int BK, bool TA, bool TB, bool MASK>
+template <int BM, int BN, int BK, bool TA, bool TB, bool MASK, bool BF16>
 hipError_t launch_tile(int M, int N, int K, const float* A, int lda, const float* B, int ldb, float* C,
                        int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
                        hipStream_t st) {
     if (kchunk % BK != 0) return hipErrorInvalidValue;
     constexpr size_t lds = GemmSmem<BM, BN, BK, TA, TB>::bytes;
-    auto kern = gemm_kernel<BM, BN, BK, TA, TB, MASK>;
+    auto kern = gemm_kernel<BM, BN, BK, TA, TB, MASK, BF16>;
     if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((N + BN - 1) / BN), (unsigned)kslices);
     const GemmParams p{M, N, K, A, lda, B, ldb, C, ldc, kchunk, c_slice, mask};
@@ -223,13 +243,13 @@ TileCfg fwd_tile(int M, int kchunk) {
 
 TileCfg dgrad_tile(int M, int kchunk) { return TileCfg{32, 32, (M <= 64 && kchunk % 64 == 0) ? 64 : 32}; }
 
-template <bool TA, bool TB, bool MASK>
+template <bool TA, bool TB, bool MASK, bool BF16>
 hipError_t launch_cfg(TileCfg c, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
                       float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
                       hipStream_t st) {
 #define DQN_TILE(TBM, TBN, TBK)                                                                     \
     if (c.bm == TBM && c.bn == TBN && c.bk == TBK)                                                  \
-        return launch_tile<TBM, TBN, TBK, TA, TB, MASK>(M, N, K, A, lda, B, ldb, C, ldc, kslices,     \
+        return launch_tile<TBM, TBN, TBK, TA, TB, MASK, BF16>(M, N, K, A, lda, B, ldb, C, ldc, kslices, \
                                                         kchunk, c_slice, mask, st);
     if constexpr (!TA && TB) {  // forward
         DQN_TILE(32, 32, 32)
@@ -248,10 +268,10 @@ hipError_t launch_cfg(TileCfg c, int M, int N, int K, const float* A, int lda, c
     return hipErrorInvalidValue;
 }
 
-template <int BK2>
+template <int BK2, bool BF16>
 hipError_t pair_tn_nnmask(const GemmParams& w, const GemmParams& d, hipStream_t st) {
     constexpr int BM = 32, BN = 32, BK1 = 32;
-    auto kern = gemm_pair_kernel<BM, BN, BK1, true, false, false, BM, BN, BK2, false, false, true>;
+    auto kern = gemm_pair_kernel<BM, BN, BK1, true, false, false, BM, BN, BK2, false, false, true, BF16>;
     constexpr size_t l1 = GemmSmem<BM, BN, BK1, true, false>::bytes;
     constexpr size_t l2 = GemmSmem<BM, BN, BK2, false, false>::bytes;
     constexpr size_t lds = l1 > l2 ? l1 : l2;
@@ -281,32 +301,44 @@ void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk) {
 // The fc1 weight gradient (TN, one k-slice) and the masked fc1 input gradient
 // (NN, one k-slice) in one launch.
 hipError_t launch_gemm_wgrad_dgrad(int H, int F, int B, const float* dz1, const float* x,
-                                   float* dW, const float* W, float* dx, hipStream_t st) {
+                                   float* dW, const float* W, float* dx, bool bf16, hipStream_t st) {
     const int kw = (B + 31) / 32 * 32, kd = (H + 31) / 32 * 32;
     const GemmParams w{H, F, B, dz1, H, x, F, dW, F, kw, 0, nullptr};
     const GemmParams d{B, F, H, dz1, H, W, F, dx, F, kd, 0, x};
-    if (dgrad_tile(B, kd).bk == 64) return pair_tn_nnmask<64>(w, d, st);
-    return pair_tn_nnmask<32>(w, d, st);
+    if (dgrad_tile(B, kd).bk == 64) return bf16 ? pair_tn_nnmask<64, true>(w, d, st) : pair_tn_nnmask<64, false>(w, d, st);
+    return bf16 ? pair_tn_nnmask<32, true>(w, d, st) : pair_tn_nnmask<32, false>(w, d, st);
 }
 
-hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
-                       int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
-                       const float* mask, hipStream_t st) {
-    if (kchunk % 32 != 0) return hipErrorInvalidValue;
+namespace {
+
+template <bool BF16>
+hipError_t launch_gemm_prec(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
+                            int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
+                            const float* mask, hipStream_t st) {
     switch (kind) {
         case GEMM_NT:
-            return launch_cfg<false, true, false>(fwd_tile(M, kchunk), M, N, K, A, lda, B, ldb, C, ldc,
-                                                  kslices, kchunk, c_slice, nullptr, st);
+            return launch_cfg<false, true, false, BF16>(fwd_tile(M, kchunk), M, N, K, A, lda, B, ldb, C, ldc,
+                                                        kslices, kchunk, c_slice, nullptr, st);
         case GEMM_TN:
-            return launch_cfg<true, false, false>(TileCfg{32, 32, 32}, M, N, K, A, lda, B, ldb, C, ldc,
-                                                  kslices, kchunk, c_slice, nullptr, st);
+            return launch_cfg<true, false, false, BF16>(TileCfg{32, 32, 32}, M, N, K, A, lda, B, ldb, C, ldc,
+                                                        kslices, kchunk, c_slice, nullptr, st);
         case GEMM_NN:
             if (!mask) return hipErrorInvalidValue;
-            return launch_cfg<false, false, true>(dgrad_tile(M, kchunk), M, N, K, A, lda, B, ldb, C,
-                                                  ldc, kslices, kchunk, c_slice, mask, st);
+            return launch_cfg<false, false, true, BF16>(dgrad_tile(M, kchunk), M, N, K, A, lda, B, ldb, C,
+                                                        ldc, kslices, kchunk, c_slice, mask, st);
         default:
             return hipErrorInvalidValue;
     }
+}
+
+}  // namespace
+
+hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
+                       int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
+                       const float* mask, bool bf16, hipStream_t st) {
+    if (kchunk % 32 != 0) return hipErrorInvalidValue;
+    return bf16 ? launch_gemm_prec<true>(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st)
+                : launch_gemm_prec<false>(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
 }
 
 }  // namespace dqn

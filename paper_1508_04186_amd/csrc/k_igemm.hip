@@ -20,6 +20,45 @@ constexpr int IG_WG = 256;
 constexpr int IG_BM = 64, IG_BN = 64, IG_BK = 32;
 constexpr int IG_LD = IG_BK + 4;  // = 4 mod 64 after the 64-row stride math below
 
+// One 32-deep k-stage of a wave's TMxTN block of 16x16 MFMA tiles, both
+// operands staged k-contiguous as [row][IG_LD] fp32 (A rows wm + 16i + li,
+// B rows wn + 16j + li): eight fp32 steps, or with BF16 one bf16-input step
+// on the values rounded to bfloat16 (bf16_operand's k order).
+template <int TM, int TN, bool BF16>
+__device__ __forceinline__ void mfma_stage(f4 (&acc)[TM][TN], const float* As, const float* Bs, int wm, int wn,
+                                           int li, int g) {
+    if constexpr (BF16) {
+        bf16x8 a[TM], b[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const float* r = As + (wm + i * 16 + li) * IG_LD;
+            a[i] = bf16_operand([&](int k) { return r[k]; }, g);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const float* r = Bs + (wn + j * 16 + li) * IG_LD;
+            b[j] = bf16_operand([&](int k) { return r[k]; }, g);
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x32bf16(a[i], b[j], acc[i][j]);
+    } else {
+#pragma unroll
+        for (int kk = 0; kk < IG_BK / 4; ++kk) {
+            float a[TM], b[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) a[i] = As[(wm + i * 16 + li) * IG_LD + kk * 4 + g];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) b[j] = Bs[(wn + j * 16 + li) * IG_LD + kk * 4 + g];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x4(a[i], b[j], acc[i][j]);
+        }
+    }
+}
+
 struct IgemmFwdParams {
     const float* in;       // [n][cin][ih][iw]
     int n, n_a;
@@ -28,7 +67,7 @@ struct IgemmFwdParams {
     float* out;            // [n][cout][oh][ow]
 };
 
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW>
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool BF16>
 __global__ __launch_bounds__(IG_WG) void conv_igemm_fwd_kernel(IgemmFwdParams p) {
     constexpr int P = OH * OW;
     constexpr int KK = K * K;
@@ -96,18 +135,7 @@ __global__ __launch_bounds__(IG_WG) void conv_igemm_fwd_kernel(IgemmFwdParams p)
         store();
         __syncthreads();
         if (k0 + IG_BK < KT) load(k0 + IG_BK);   // in flight during the MFMAs below
-#pragma unroll
-        for (int kk = 0; kk < IG_BK / 4; ++kk) {
-            float a[2], b[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) a[i] = As[(wm + i * 16 + li) * IG_LD + kk * 4 + g];
-#pragma unroll
-            for (int j = 0; j < 2; ++j) b[j] = Bs[(wn + j * 16 + li) * IG_LD + kk * 4 + g];
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j) acc[i][j] = mfma16x16x4(a[i], b[j], acc[i][j]);
-        }
+        mfma_stage<2, 2, BF16>(acc, As, Bs, wm, wn, li, g);
         __syncthreads();
     }
 
@@ -130,7 +158,7 @@ __global__ __launch_bounds__(IG_WG) void conv_igemm_fwd_kernel(IgemmFwdParams p)
     }
 }
 
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW>
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool BF16>
 hipError_t igemm_launch(const float* in, int n_a, int n, const float* w_a, const float* b_a,
                         const float* w_b, const float* b_b, float* out, hipStream_t st) {
     constexpr int P = OH * OW;
@@ -140,7 +168,7 @@ hipError_t igemm_launch(const float* in, int n_a, int n, const float* w_a, const
     const long blocks = (tiles_a + tiles_b) * (COUT / IG_BN);
     if (blocks <= 0 || blocks > 0x7fffffffL || (long)n * P > 0x7fffffffL) return hipErrorInvalidValue;
     IgemmFwdParams prm{in, n, n_a, (int)tiles_a, w_a, b_a, w_b, b_b, out};
-    hipLaunchKernelGGL((conv_igemm_fwd_kernel<CIN, IH, IW, COUT, K, S, OH, OW>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((conv_igemm_fwd_kernel<CIN, IH, IW, COUT, K, S, OH, OW, BF16>), dim3((unsigned)blocks),
                        dim3(IG_WG), 0, st, prm);
     return hipGetLastError();
 }
@@ -160,7 +188,7 @@ struct IgemmDgradParams {
     int n, mtiles;       // samples; M-tiles per phase
 };
 
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int BN>
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int BN, bool BF16>
 __global__ __launch_bounds__(IG_WG) void conv_igemm_dgrad_kernel(IgemmDgradParams p) {
     static_assert(K % S == 0 && IH % S == 0 && IW % S == 0, "phases must tile the input");
     constexpr int T = K / S;
@@ -236,18 +264,7 @@ __global__ __launch_bounds__(IG_WG) void conv_igemm_dgrad_kernel(IgemmDgradParam
         store();
         __syncthreads();
         if (k0 + IG_BK < KT) load(k0 + IG_BK);
-#pragma unroll
-        for (int kk = 0; kk < IG_BK / 4; ++kk) {
-            float a[2], bv[TN];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) a[i] = As[(wm + i * 16 + li) * IG_LD + kk * 4 + g];
-#pragma unroll
-            for (int j = 0; j < TN; ++j) bv[j] = Bs[(wn + j * 16 + li) * IG_LD + kk * 4 + g];
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x4(a[i], bv[j], acc[i][j]);
-        }
+        mfma_stage<2, TN, BF16>(acc, As, Bs, wm, wn, li, g);
         __syncthreads();
     }
 
@@ -269,7 +286,7 @@ __global__ __launch_bounds__(IG_WG) void conv_igemm_dgrad_kernel(IgemmDgradParam
     }
 }
 
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int BN>
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, int BN, bool BF16>
 hipError_t igemm_dgrad_launch(const float* dz, const float* w, const float* h_in, float* din, int n,
                               hipStream_t st) {
     constexpr int QP = (IH / S) * (IW / S);
@@ -277,7 +294,7 @@ hipError_t igemm_dgrad_launch(const float* dz, const float* w, const float* h_in
     const long blocks = (long)S * S * mtiles * (CIN / BN);
     if (n <= 0 || blocks > 0x7fffffffL || (long)n * QP > 0x7fffffffL) return hipErrorInvalidValue;
     IgemmDgradParams prm{dz, w, h_in, din, n, (int)mtiles};
-    hipLaunchKernelGGL((conv_igemm_dgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, BN>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((conv_igemm_dgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, BN, BF16>), dim3((unsigned)blocks),
                        dim3(IG_WG), 0, st, prm);
     return hipGetLastError();
 }
@@ -302,7 +319,7 @@ struct IgemmWgradParams {
     int n, chunk, chunks;
 };
 
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int BM>
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int BM, bool BF16>
 __global__ __launch_bounds__(IG_WG) void conv_igemm_wgrad_kernel(IgemmWgradParams p) {
     constexpr int P = OH * OW;
     constexpr int KK = K * K, KT = CIN * KK;
@@ -385,18 +402,7 @@ __global__ __launch_bounds__(IG_WG) void conv_igemm_wgrad_kernel(IgemmWgradParam
         store();
         __syncthreads();
         if (s0 + IG_BK < pix1) load(s0 + IG_BK);
-#pragma unroll
-        for (int kk = 0; kk < IG_BK / 4; ++kk) {
-            float a[TM], bv[2];
-#pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = As[(wm + i * 16 + li) * IG_LD + kk * 4 + g];
-#pragma unroll
-            for (int j = 0; j < 2; ++j) bv[j] = Bs[(wn + j * 16 + li) * IG_LD + kk * 4 + g];
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < 2; ++j) acc[i][j] = mfma16x16x4(a[i], bv[j], acc[i][j]);
-        }
+        mfma_stage<TM, 2, BF16>(acc, As, Bs, wm, wn, li, g);
         __syncthreads();
     }
 
@@ -435,7 +441,7 @@ int igemm_wgrad_chunk(int n) {
     return (int)std::max<long>(chunk, IG_BK);
 }
 
-template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int BM>
+template <int CIN, int IH, int IW, int COUT, int K, int S, int OH, int OW, bool U8, int BM, bool BF16>
 hipError_t igemm_wgrad_launch(const ConvIn& in, const float* dz, int n, float* wpart, float* bpart,
                               float in_scale, hipStream_t st) {
     constexpr int P = OH * OW;
@@ -444,7 +450,7 @@ hipError_t igemm_wgrad_launch(const ConvIn& in, const float* dz, int n, float* w
     const int chunks = (int)(((long)n * P + chunk - 1) / chunk);
     const long blocks = (long)chunks * (COUT / BM) * (CIN * K * K / IG_BN);
     IgemmWgradParams prm{in.base, in.idx, in.stride, dz, wpart, bpart, in_scale, n, chunk, chunks};
-    hipLaunchKernelGGL((conv_igemm_wgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8, BM>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((conv_igemm_wgrad_kernel<CIN, IH, IW, COUT, K, S, OH, OW, U8, BM, BF16>), dim3((unsigned)blocks),
                        dim3(IG_WG), 0, st, prm);
     return hipGetLastError();
 }
@@ -455,19 +461,27 @@ bool conv_igemm_fwd_supported(ConvId id) { return id == CONV_L2 || id == CONV_L3
 
 hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, const float* w_a,
                                  const float* b_a, const float* w_b, const float* b_b, float* out,
-                                 hipStream_t st) {
+                                 bool bf16, hipStream_t st) {
     switch (id) {
-        case CONV_L2: return igemm_launch<32, 20, 20, 64, 4, 2, 9, 9>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
-        case CONV_L3: return igemm_launch<64, 9, 9, 64, 3, 1, 7, 7>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
+        case CONV_L2:
+            return bf16 ? igemm_launch<32, 20, 20, 64, 4, 2, 9, 9, true>(in, n_a, n, w_a, b_a, w_b, b_b, out, st)
+                        : igemm_launch<32, 20, 20, 64, 4, 2, 9, 9, false>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
+        case CONV_L3:
+            return bf16 ? igemm_launch<64, 9, 9, 64, 3, 1, 7, 7, true>(in, n_a, n, w_a, b_a, w_b, b_b, out, st)
+                        : igemm_launch<64, 9, 9, 64, 3, 1, 7, 7, false>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
         default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, const float* h_in, float* din,
-                                   int n, hipStream_t st) {
+                                   int n, bool bf16, hipStream_t st) {
     switch (id) {
-        case CONV_L2: return igemm_dgrad_launch<32, 20, 20, 64, 4, 2, 9, 9, 32>(dz, w, h_in, din, n, st);
-        case CONV_L3: return igemm_dgrad_launch<64, 9, 9, 64, 3, 1, 7, 7, 64>(dz, w, h_in, din, n, st);
+        case CONV_L2:
+            return bf16 ? igemm_dgrad_launch<32, 20, 20, 64, 4, 2, 9, 9, 32, true>(dz, w, h_in, din, n, st)
+                        : igemm_dgrad_launch<32, 20, 20, 64, 4, 2, 9, 9, 32, false>(dz, w, h_in, din, n, st);
+        case CONV_L3:
+            return bf16 ? igemm_dgrad_launch<64, 9, 9, 64, 3, 1, 7, 7, 64, true>(dz, w, h_in, din, n, st)
+                        : igemm_dgrad_launch<64, 9, 9, 64, 3, 1, 7, 7, 64, false>(dz, w, h_in, din, n, st);
         default: return hipErrorInvalidValue;
     }
 }
@@ -484,13 +498,19 @@ int conv_igemm_wgrad_chunks(ConvId id, int n) {
 }
 
 hipError_t launch_conv_igemm_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
-                                   float* bpart, float in_scale, hipStream_t st) {
+                                   float* bpart, float in_scale, bool bf16, hipStream_t st) {
+#define DQN_WG(CIN, IH, IW, COUT, K, S, OH, OW, U8, BM)                                                      \
+    return bf16 ? igemm_wgrad_launch<CIN, IH, IW, COUT, K, S, OH, OW, U8, BM, true>(in, dz, n, wpart, bpart,  \
+                                                                                     in_scale, st)           \
+                : igemm_wgrad_launch<CIN, IH, IW, COUT, K, S, OH, OW, U8, BM, false>(in, dz, n, wpart, bpart, \
+                                                                                      in_scale, st)
     switch (id) {
-        case CONV_L1: return igemm_wgrad_launch<4, 84, 84, 32, 8, 4, 20, 20, true, 32>(in, dz, n, wpart, bpart, in_scale, st);
-        case CONV_L2: return igemm_wgrad_launch<32, 20, 20, 64, 4, 2, 9, 9, false, 64>(in, dz, n, wpart, bpart, in_scale, st);
-        case CONV_L3: return igemm_wgrad_launch<64, 9, 9, 64, 3, 1, 7, 7, false, 64>(in, dz, n, wpart, bpart, in_scale, st);
+        case CONV_L1: DQN_WG(4, 84, 84, 32, 8, 4, 20, 20, true, 32);
+        case CONV_L2: DQN_WG(32, 20, 20, 64, 4, 2, 9, 9, false, 64);
+        case CONV_L3: DQN_WG(64, 9, 9, 64, 3, 1, 7, 7, false, 64);
         default: return hipErrorInvalidValue;
     }
+#undef DQN_WG
 }
 
 }  // namespace dqn

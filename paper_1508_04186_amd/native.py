@@ -46,8 +46,11 @@ class Net:
     precision: int = 0
 
 
+DQN_FP32, DQN_BF16 = 0, 1   # Net.precision (include/dqn.h)
 NET_SMALL = Net(4, 84, 84, ((16, 8, 4), (32, 4, 2)), 256, 6)
 NET_LARGE = Net(4, 84, 84, ((32, 8, 4), (64, 4, 2), (64, 3, 1)), 512, 18)
+# The large network with bf16-input contractions (fp32 accumulation).
+NET_LARGE_BF16 = Net(4, 84, 84, ((32, 8, 4), (64, 4, 2), (64, 3, 1)), 512, 18, DQN_BF16)
 
 
 @dataclass

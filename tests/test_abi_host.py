@@ -78,8 +78,19 @@ def test_unsupported_networks_and_bad_batch():
     assert e.value.status == dq.DQN_EUNSUPPORTED
 
 
+def test_bf16_variant_is_large_network_only():
+    assert dq.dqn_param_count(dq.NET_LARGE_BF16) == dq.dqn_param_count(dq.NET_LARGE)
+    for l in range(5):
+        for b in (0, 1):
+            assert dq.dqn_param_offset(dq.NET_LARGE_BF16, l, b) == dq.dqn_param_offset(dq.NET_LARGE, l, b)
+    small_bf16 = dq.Net(4, 84, 84, ((16, 8, 4), (32, 4, 2)), 256, 6, precision=dq.DQN_BF16)
+    with pytest.raises(dq.DqnError) as e:
+        dq.dqn_workspace_bytes(small_bf16, 32, dq.DQN_OP_TD_GRADIENT)
+    assert e.value.status == dq.DQN_EUNSUPPORTED
+
+
 def test_workspace_grows_with_batch():
-    for net in (dq.NET_SMALL, dq.NET_LARGE):
+    for net in (dq.NET_SMALL, dq.NET_LARGE, dq.NET_LARGE_BF16):
         for op in (dq.DQN_OP_FORWARD, dq.DQN_OP_TD_GRADIENT):
             a = dq.dqn_workspace_bytes(net, 32, op)
             b = dq.dqn_workspace_bytes(net, 2048, op)
