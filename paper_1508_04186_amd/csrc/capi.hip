@@ -99,9 +99,10 @@ constexpr int kIgemmMinRows = 128;
 bool igemm_wgrad(ConvId id, int B, bool bf16) {
     return (id == CONV_L2 || id == CONV_L3) && (bf16 || B >= kIgemmMinRows);
 }
-bool igemm_dgrad(ConvId id, int B, bool bf16) {
-    return (id == CONV_L3 && B >= kIgemmMinRows) || (bf16 && (id == CONV_L2 || id == CONV_L3));
-}
+bool igemm_dgrad(ConvId id, int B, bool bf16) { return id == CONV_L3 && (bf16 || B >= kIgemmMinRows); }
+// conv2's input gradient of the large network by stride phase, weights in
+// registers (from the same batch size).
+bool phase_dgrad(ConvId id, int B, bool bf16) { return id == CONV_L2 && (bf16 || B >= kIgemmMinRows); }
 bool igemm_fwd(ConvId id, int rows, bool bf16) {
     return conv_igemm_fwd_supported(id) && (bf16 || rows >= kIgemmMinRows);
 }
@@ -406,7 +407,11 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             RUN(DQN_K_CONV1_WGRAD + l,
                 launch_conv_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale, st));
         }
-        if (l > 0 && igemm_dgrad(ni.conv[l], B, ni.bf16))
+        if (l > 0 && phase_dgrad(ni.conv[l], B, ni.bf16))
+            RUN(DQN_K_CONV2_DGRAD + (l - 1),
+                launch_conv2_dgrad_phase(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
+                                         ni.bf16, st));
+        else if (l > 0 && igemm_dgrad(ni.conv[l], B, ni.bf16))
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
                 launch_conv_igemm_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],
                                         t.dconv[l - 1], B, ni.bf16, st));

@@ -171,6 +171,12 @@ hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, con
 hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, const float* h_in, float* din,
                                    int n, bool bf16, hipStream_t st);
 
+// Input gradient of CONV_L2 for n samples by stride phase, masked by
+// [h_in > 0] (as launch_conv_dgrad), with each phase's weights held in
+// registers and dz staged in LDS with a zero border.
+hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
+                                    bool bf16, hipStream_t st);
+
 // Weight/bias gradient partial sums of a large-network layer for n samples as
 // an implicit GEMM over pixel chunks: conv_igemm_wgrad_chunks(id, n) slots of
 // wpart [slots][cout][cin*k*k] and bpart [slots][cout].  in: the layer input

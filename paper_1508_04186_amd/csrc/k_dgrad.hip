@@ -1,0 +1,231 @@
+// Input gradient of the large network's second convolution (32 -> 64
+// channels, 4x4 stride 2, 20x20 -> 9x9) at large batch, by stride phase
+// (py, px): input pixel (2qy + py, 2qx + px), qy, qx in [0, 10), receives
+//   din = [h_in > 0] * sum_{o, ty, tx} W[o][c][py + 2ty][px + 2tx] * dz[o][qy - ty][qx - tx]
+// with dz = 0 outside the 9x9 map, so no product multiplies a structural
+// zero of the strided kernel.
+//
+// A workgroup walks a group of samples, one per round; its eight waves are
+// (phase, N-tile of 16 input channels) pairs, and each wave holds its 16 x 256
+// slice of the weights (c x (tap, o)) in registers for the whole launch: the
+// B operand of every k-step.  A sample's dz is staged in LDS with a zero
+// border (row -1, row 9, column 9 and two spare slots per channel), so the A
+// operand of pixel m and tap (ty, tx) sits at a per-lane base plus a
+// compile-time offset and needs no bounds test: channel stride 112 floats
+// (= 48 mod 64) and 16 consecutive pixels contiguous, so a wave's 64 reads
+// hit 64 banks.  A phase has 100 pixels: 7 M-tiles of 16, the last one
+// partly unused.  The four phases' results are assembled into the sample's
+// whole input gradient in LDS, then written with 16-byte stores next to
+// 16-byte reads of the ReLU mask.  The next sample's dz is read into
+// registers while the current one is computed.  Both precisions: fp32 MFMA,
+// or the bf16-input variant (operands rounded to bfloat16 in registers, one
+// 16x16x32 step per 32 output channels).
+#include <algorithm>
+#include <type_traits>
+
+#include "common.h"
+
+namespace dqn {
+namespace {
+
+constexpr int D2_WG = 512;
+constexpr int D2_CIN = 32, D2_IH = 20, D2_COUT = 64, D2_OH = 9, D2_K = 4;
+constexpr int D2_Q = 10;                       // phase grid side
+constexpr int D2_QP = D2_Q * D2_Q;             // phase pixels per sample
+constexpr int D2_MT = (D2_QP + 15) / 16;       // M-tiles per phase (7)
+constexpr int D2_CS = 112;                     // staged floats per dz channel
+constexpr int D2_LEAD = 16;                    // zeros before the stage (offset -1 reads)
+constexpr int D2_TAIL = 32;                    // slack after it (rows of the unused pixels)
+constexpr int D2_STAGE = D2_LEAD + D2_COUT * D2_CS + D2_TAIL;
+constexpr int D2_DZ = D2_COUT * D2_OH * D2_OH; // dz floats per sample (5,184)
+constexpr int D2_IN = D2_CIN * D2_IH * D2_IH;  // input-gradient floats per sample (12,800)
+constexpr int D2_KT = D2_COUT * 4;             // contraction length (o, tap): 256
+constexpr int D2_PER = (D2_DZ + D2_WG - 1) / D2_WG;       // dz floats per thread (11)
+constexpr int D2_OUT4 = (D2_IN / 4 + D2_WG - 1) / D2_WG;  // float4 of din per thread (7)
+static_assert(D2_CS >= (D2_OH + 2) * D2_Q && D2_CS % 64 == 48, "channel stride: border and banks");
+static_assert(D2_IN % 4 == 0, "whole float4 rows");
+
+struct Dgrad2Params {
+    const float* dz;    // [n][64][9][9]
+    const float* w;     // [64][32][4][4]
+    const float* h_in;  // [n][32][20][20]
+    float* din;         // [n][32][20][20]
+    int n, spg;         // samples, samples per workgroup
+};
+
+template <bool BF16>
+__global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p) {
+    __shared__ float s_dz[D2_STAGE];
+    __shared__ __align__(16) float s_din[D2_IN];
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int ph = wave >> 1, nt = wave & 1;   // phase; N-tile
+    const int py = ph >> 1, px = ph & 1;
+
+    for (int e = t; e < D2_STAGE; e += D2_WG) s_dz[e] = 0.f;
+
+    const int j_lo = blockIdx.x * p.spg;
+    const int j_hi = min(p.n, j_lo + p.spg);
+    if (j_lo >= j_hi) return;  // uniform
+
+    // B operands of this lane for every k-step: k = tap * 64 + o, tap = 2ty + tx.
+    const int c = nt * 16 + li;
+    constexpr int KS = BF16 ? D2_KT / 32 : D2_KT / 4;
+    using BOp = typename std::conditional<BF16, bf16x8, float>::type;
+    BOp wreg[KS];
+    {
+        const float* wc = p.w + (size_t)c * D2_K * D2_K + py * D2_K + px;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            if constexpr (BF16) {
+                // k-step s: tap s / 2, o = 32 * (s % 2) + 4e + g
+                const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int o = 32 * (s % 2) + 4 * e + g;
+                    wreg[s][e] = (__bf16)wc[(size_t)o * D2_CIN * D2_K * D2_K + 2 * ty * D2_K + 2 * tx];
+                }
+            } else {
+                // k-step s: tap s / 16, o = 4 * (s % 16) + g
+                const int tap = s / 16, ty = tap >> 1, tx = tap & 1;
+                const int o = 4 * (s % 16) + g;
+                wreg[s] = wc[(size_t)o * D2_CIN * D2_K * D2_K + 2 * ty * D2_K + 2 * tx];
+            }
+        }
+    }
+
+    // Per-lane LDS base of each M-tile: pixel m = 16 mt + li, channel g, row
+    // shifted by one (the zero row above the map).  The A operand of tap
+    // (ty, tx) and channel o0 + g is then at base + o0*D2_CS - 10ty - tx, a
+    // compile-time offset.
+    int base[D2_MT];
+#pragma unroll
+    for (int i = 0; i < D2_MT; ++i) base[i] = D2_LEAD + g * D2_CS + i * 16 + li + D2_Q;
+
+    // A sample's dz in registers (thread t holds flat elements t + u*D2_WG),
+    // then into LDS at channel e / 81, row oy + 1, column ox: offset q + q/9
+    // past the row shift.
+    float v[D2_PER];
+    auto fetch = [&](int j) {
+        const float* src = p.dz + (size_t)j * D2_DZ;
+#pragma unroll
+        for (int u = 0; u < D2_PER; ++u) {
+            const int e = t + u * D2_WG;
+            v[u] = e < D2_DZ ? src[e] : 0.f;
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < D2_PER; ++u) {
+            const int e = t + u * D2_WG;
+            if (e < D2_DZ) {
+                const int row = e / (D2_OH * D2_OH), q = e - row * (D2_OH * D2_OH);
+                s_dz[D2_LEAD + D2_Q + row * D2_CS + q + q / D2_OH] = v[u];
+            }
+        }
+    };
+
+    fetch(j_lo);
+    for (int j = j_lo; j < j_hi; ++j) {
+        __syncthreads();  // the zero fill, or the previous round's LDS reads, are done
+        stage();
+        __syncthreads();
+        if (j + 1 < j_hi) fetch(j + 1);  // in flight during this sample's MFMAs
+
+        f4 acc[D2_MT];
+#pragma unroll
+        for (int i = 0; i < D2_MT; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        // The k-steps run in order with the next step's A operands read
+        // before the current step's MFMAs issue (scheduling groups), and a
+        // barrier per step keeps the compiler from hoisting every LDS read.
+        if constexpr (BF16) {
+            auto load = [&](int s, bf16x8 (&a)[D2_MT]) {
+                const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
+                const int off = 32 * (s % 2) * D2_CS - D2_Q * ty - tx;
+#pragma unroll
+                for (int i = 0; i < D2_MT; ++i) {
+                    const float* ap = s_dz + base[i] + off;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) a[i][e] = (__bf16)ap[4 * e * D2_CS];
+                }
+            };
+            bf16x8 a[2][D2_MT];
+            load(0, a[0]);
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                if (s + 1 < KS) load(s + 1, a[(s + 1) & 1]);
+#pragma unroll
+                for (int i = 0; i < D2_MT; ++i) acc[i] = mfma16x16x32bf16(a[s & 1][i], wreg[s], acc[i]);
+                if (s + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 8 * D2_MT, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, D2_MT, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+            auto load = [&](int s, float (&a)[D2_MT]) {
+                const int tap = s / 16, ty = tap >> 1, tx = tap & 1;
+                const int off = 4 * (s % 16) * D2_CS - D2_Q * ty - tx;
+#pragma unroll
+                for (int i = 0; i < D2_MT; ++i) a[i] = s_dz[base[i] + off];
+            };
+            float a[2][D2_MT];
+            load(0, a[0]);
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                if (s + 1 < KS) load(s + 1, a[(s + 1) & 1]);
+#pragma unroll
+                for (int i = 0; i < D2_MT; ++i) acc[i] = mfma16x16x4(a[s & 1][i], wreg[s], acc[i]);
+                if (s + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x100, D2_MT, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, D2_MT, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+
+        // D[4g + r][li] of tile i: phase pixel m = 16 i + 4g + r, channel c,
+        // into the sample's gradient in LDS (the previous sample's write-out
+        // finished before this round's second barrier).
+#pragma unroll
+        for (int i = 0; i < D2_MT; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = i * 16 + 4 * g + r;
+                if (m < D2_QP) {
+                    const int qy = m / D2_Q, qx = m - qy * D2_Q;
+                    s_din[c * D2_IH * D2_IH + (2 * qy + py) * D2_IH + 2 * qx + px] = acc[i][r];
+                }
+            }
+        __syncthreads();
+        // masked write-out with 16-byte accesses
+        const size_t o0 = (size_t)j * D2_IN;
+#pragma unroll
+        for (int u = 0; u < D2_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D2_IN / 4) {
+                const f4 h = *(const f4*)(p.h_in + o0 + 4 * e4);
+                const f4 d = *(const f4*)(s_din + 4 * e4);
+                f4 o;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) o[k] = h[k] > 0.f ? d[k] : 0.f;
+                *(f4*)(p.din + o0 + 4 * e4) = o;
+            }
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
+                                    bool bf16, hipStream_t st) {
+    if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15)) return hipErrorInvalidValue;
+    // about one workgroup per CU, one sample per round
+    const int spg = std::max(1, (n + 255) / 256);
+    const int blocks = (n + spg - 1) / spg;
+    const Dgrad2Params prm{dz, w, h_in, din, n, spg};
+    if (bf16)
+        hipLaunchKernelGGL(conv2_dgrad_phase_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    else
+        hipLaunchKernelGGL(conv2_dgrad_phase_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    return hipGetLastError();
+}
+
+}  // namespace dqn
