@@ -218,14 +218,22 @@ __global__ __launch_bounds__(HT) void head_fwd_kernel(HeadFwdArgs p) {
     }
 }
 
-// Eight lanes per output value; each output's terms are summed in a fixed
-// association.  Segments: conv weight and bias gradients (partial sums over
-// wgrad chunks), fc1 bias (over samples), fc2 weight and bias (over the
-// samples that took each action), and the loss.
+// Each output's terms are summed in a fixed association, without atomics.
+// Segments, in slots of eight lanes:
+//  - sums over the B samples, one wave per output (lane L takes samples
+//    j = L, L + 64, ... with every load unconditional and eight samples in
+//    flight; the wave then combines its lanes in a fixed butterfly): the fc2
+//    weights of hidden unit h for all actions at once (delta_j * h1[j][h]
+//    added to the sum of the action j took), the fc1 bias of h, the fc2 bias
+//    of every action, and the loss;
+//  - the conv weight and bias gradients, eight lanes per output over the
+//    wgrad partial-sum slots.
 //
 // MODE < 0 stores the gradient; MODE = 0, 1, 2 applies update rule MODE to
 // each parameter instead (fused parameter-server update), and the blocks
 // from n_fin on update the fc1 weights from the gradient stored there.
+constexpr int FIN_U = 8;       // samples in flight per lane
+
 template <int MODE>
 __device__ __forceinline__ void emit(const FinalizeArgs& a, const PsUpdate& u, float* dst, float v) {
     if constexpr (MODE < 0) {
@@ -258,7 +266,65 @@ __device__ __forceinline__ void apply_fc1w(const FinalizeArgs& a, const PsUpdate
     if constexpr (MODE != 0) *(f4*)(u.state + off) = sv;
 }
 
-template <int MODE>
+// Sums over samples of one wave (see above).  kind 0: fc2 weights of hidden
+// unit h for every action; 1: fc1 bias of h; 2: fc2 bias of every action;
+// 3: the loss.
+template <int MODE, int A>
+__device__ __forceinline__ void sample_sums(const FinalizeArgs& a, const PsUpdate& u, int kind, int h) {
+    const int L = threadIdx.x & 63;
+    float s[A];
+#pragma unroll
+    for (int k = 0; k < A; ++k) s[k] = 0.f;
+    const bool per_action = kind == 0 || kind == 2;
+    for (int j0 = L; j0 < a.B; j0 += 64 * FIN_U) {
+        int act[FIN_U];
+        float d[FIN_U];
+#pragma unroll
+        for (int e = 0; e < FIN_U; ++e) {
+            const int j = j0 + 64 * e;
+            const bool v = j < a.B;
+            act[e] = -1;
+            d[e] = 0.f;
+            if (v) {
+                if (kind == 0) {
+                    act[e] = min(max(a.action[j], 0), A - 1);   // clamped as in the head
+                    d[e] = a.delta[j] * a.h1s[(int64_t)j * a.H + h];
+                } else if (kind == 1) {
+                    d[e] = a.dz1[(int64_t)j * a.H + h];
+                } else if (kind == 2) {
+                    act[e] = min(max(a.action[j], 0), A - 1);
+                    d[e] = a.delta[j];
+                } else {
+                    d[e] = a.lossj[j];
+                }
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < FIN_U; ++e) {
+            if (per_action) {
+#pragma unroll
+                for (int k = 0; k < A; ++k) s[k] += act[e] == k ? d[e] : 0.f;
+            } else {
+                s[0] += d[e];
+            }
+        }
+    }
+    const int nk = per_action ? A : 1;
+#pragma unroll
+    for (int k = 0; k < A; ++k) {
+        if (k < nk) {
+            float t = wave_sum(s[k]);
+            if (L == 0) {
+                if (kind == 0) emit<MODE>(a, u, a.g_W2 + (int64_t)k * a.H + h, t);
+                else if (kind == 1) emit<MODE>(a, u, a.g_b1 + h, t);
+                else if (kind == 2) emit<MODE>(a, u, a.g_b2 + k, t);
+                else a.loss_out[0] = t;
+            }
+        }
+    }
+}
+
+template <int MODE, int A>
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a, PsUpdate u, int n_fin) {
     if constexpr (MODE >= 0) {
         if ((int)blockIdx.x >= n_fin) {
@@ -267,6 +333,16 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a, PsUpdate 
         }
     }
     int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3;
+    // one wave per output of the sums over samples: waves 0 .. 2H + 1
+    const int64_t n_wave = 2 * (int64_t)a.H + 2;
+    if (i < 8 * n_wave) {
+        const int w = (int)(i >> 3);
+        if (w < a.H) sample_sums<MODE, A>(a, u, 0, w);
+        else if (w < 2 * a.H) sample_sums<MODE, A>(a, u, 1, w - a.H);
+        else sample_sums<MODE, A>(a, u, w == 2 * a.H ? 2 : 3, 0);
+        return;
+    }
+    i -= 8 * n_wave;
     const bool lead = (threadIdx.x & 7) == 0;
     for (int l = 0; l < a.n_conv; ++l) {
         if (i < a.wcount[l]) {
@@ -281,46 +357,6 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a, PsUpdate 
             return;
         }
         i -= a.cout[l];
-    }
-    if (i < a.H) {
-        const float v = sum_strided_x8(a.dz1 + i, a.B, a.H);
-        if (lead) emit<MODE>(a, u, a.g_b1 + i, v);
-        return;
-    }
-    i -= a.H;
-    if (i < (int64_t)a.A * a.H) {
-        const int k = (int)(i / a.H), h = (int)(i - (int64_t)k * a.H);
-        const int q = threadIdx.x & 7;
-        float s0 = 0.f, s1 = 0.f;
-        for (int j = q; j < a.B; j += 16) {
-            const float t0 = a.action[j] == k ? a.delta[j] * a.h1s[(int64_t)j * a.H + h] : 0.f;
-            const float t1 = (j + 8 < a.B && a.action[j + 8] == k)
-                                 ? a.delta[j + 8] * a.h1s[(int64_t)(j + 8) * a.H + h] : 0.f;
-            s0 += t0;
-            s1 += t1;
-        }
-        float t = s0 + s1;
-        t += __shfl_xor(t, 1, 64);
-        t += __shfl_xor(t, 2, 64);
-        t += __shfl_xor(t, 4, 64);
-        if (lead) emit<MODE>(a, u, a.g_W2 + i, t);
-        return;
-    }
-    i -= (int64_t)a.A * a.H;
-    if (i < a.A) {
-        const int q = threadIdx.x & 7;
-        float s = 0.f;
-        for (int j = q; j < a.B; j += 8) s += a.action[j] == (int)i ? a.delta[j] : 0.f;
-        s += __shfl_xor(s, 1, 64);
-        s += __shfl_xor(s, 2, 64);
-        s += __shfl_xor(s, 4, 64);
-        if (lead) emit<MODE>(a, u, a.g_b2 + i, s);
-        return;
-    }
-    i -= a.A;
-    if (i == 0) {
-        const float v = sum_strided_x8(a.lossj, a.B, 1);
-        if (lead) a.loss_out[0] = v;
     }
 }
 
@@ -350,24 +386,31 @@ hipError_t launch_head_fwd(int H, int A, const HeadFwdArgs& a, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_finalize(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
-    int64_t total = a.H + (int64_t)a.A * a.H + a.A + 1;
+template <int A>
+hipError_t finalize_launch(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
+    int64_t total = 8 * (2 * (int64_t)a.H + 2);   // slots: one wave per sum over samples
     for (int l = 0; l < a.n_conv; ++l) total += a.wcount[l] + a.cout[l];
     const int n_fin = (int)((total * 8 + 255) / 256);
     if (!upd) {
-        hipLaunchKernelGGL(finalize_kernel<-1>, dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{},
+        hipLaunchKernelGGL((finalize_kernel<-1, A>), dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{},
                            n_fin);
         return hipGetLastError();
     }
     if (a.fc1w_off % 4 != 0 || a.fc1w_count % 4 != 0 || !a.grad_base) return hipErrorInvalidValue;
     const dim3 grid((unsigned)(n_fin + (a.fc1w_count / 4 + 255) / 256));
     switch (upd->rule) {
-        case 0: hipLaunchKernelGGL(finalize_kernel<0>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
-        case 1: hipLaunchKernelGGL(finalize_kernel<1>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
-        case 2: hipLaunchKernelGGL(finalize_kernel<2>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 0: hipLaunchKernelGGL((finalize_kernel<0, A>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 1: hipLaunchKernelGGL((finalize_kernel<1, A>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 2: hipLaunchKernelGGL((finalize_kernel<2, A>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+hipError_t launch_finalize(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
+    if (a.A == 6) return finalize_launch<6>(a, upd, st);
+    if (a.A == 18) return finalize_launch<18>(a, upd, st);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace dqn

@@ -277,6 +277,25 @@ def test_td_gradient_deterministic_and_all_terminal(dev):
     assert np.array_equal(y, r)
 
 
+@pytest.mark.parametrize("name", ["small", "large"])
+def test_td_gradient_clamps_out_of_range_actions(dev, name):
+    # An action outside [0, A) is clamped into that range (include/dqn.h):
+    # every output equals the one for the clamped actions, bit for bit,
+    # including the output-layer gradient rows the clamped actions select.
+    net, shape = NETS[name]
+    B = 24
+    th = di.xavier_theta(shape, 90, bias_scale=0.05)
+    s, sn, a, r, t = _td_inputs(shape, B, 91)
+    bad = a.copy()
+    bad[::3] = -5
+    bad[1::3] = shape.n_actions + 7
+    clamped = np.clip(bad, 0, shape.n_actions - 1).astype(np.int32)
+    say(f"[td] out-of-range actions, net={name}")
+    g1, l1, q1, y1 = _run_td(dev, net, th, None, s, sn, bad, r, t, 0.99)
+    g2, l2, q2, y2 = _run_td(dev, net, th, None, s, sn, clamped, r, t, 0.99)
+    assert np.array_equal(g1, g2) and l1 == l2 and np.array_equal(q1, q2) and np.array_equal(y1, y2)
+
+
 def test_td_gradient_zero_when_q_equals_target(dev):
     # fc2.W = 0 and fc2.b = 0.5 everywhere, all terminal with r = 0.5
     net, shape = NETS["small"]
