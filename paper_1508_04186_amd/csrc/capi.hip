@@ -100,9 +100,11 @@ bool igemm_wgrad(ConvId id, int B, bool bf16) {
     return (id == CONV_L2 || id == CONV_L3) && (bf16 || B >= kIgemmMinRows);
 }
 bool igemm_dgrad(ConvId id, int B, bool bf16) { return id == CONV_L3 && (bf16 || B >= kIgemmMinRows); }
-// conv2's input gradient of the large network by stride phase, weights in
-// registers (from the same batch size).
-bool phase_dgrad(ConvId id, int B, bool bf16) { return id == CONV_L2 && (bf16 || B >= kIgemmMinRows); }
+// conv2's and conv3's input gradients of the large network with the weights
+// in registers (from the same batch size; k_dgrad.hip).
+bool phase_dgrad(ConvId id, int B, bool bf16) {
+    return (id == CONV_L2 || id == CONV_L3) && (bf16 || B >= kIgemmMinRows);
+}
 bool igemm_fwd(ConvId id, int rows, bool bf16) {
     return conv_igemm_fwd_supported(id) && (bf16 || rows >= kIgemmMinRows);
 }
@@ -409,7 +411,10 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
         }
         if (l > 0 && phase_dgrad(ni.conv[l], B, ni.bf16))
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
-                launch_conv2_dgrad_phase(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
+                ni.conv[l] == CONV_L2
+                    ? launch_conv2_dgrad_phase(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
+                                               ni.bf16, st)
+                    : launch_conv3_dgrad(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
                                          ni.bf16, st));
         else if (l > 0 && igemm_dgrad(ni.conv[l], B, ni.bf16))
             RUN(DQN_K_CONV2_DGRAD + (l - 1),

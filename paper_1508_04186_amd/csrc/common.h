@@ -177,6 +177,12 @@ hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, c
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
                                     bool bf16, hipStream_t st);
 
+// Input gradient of CONV_L3 for n samples, masked by [h_in > 0], in the same
+// arrangement (weights in registers, zero-bordered dz in LDS, the sample's
+// gradient assembled in LDS).  h_in and din 16-byte aligned.
+hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
+                              hipStream_t st);
+
 // Weight/bias gradient partial sums of a large-network layer for n samples as
 // an implicit GEMM over pixel chunks: conv_igemm_wgrad_chunks(id, n) slots of
 // wpart [slots][cout][cin*k*k] and bpart [slots][cout].  in: the layer input

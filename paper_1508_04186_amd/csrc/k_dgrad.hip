@@ -212,7 +212,189 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p
     }
 }
 
+// ---------------------------------------------------------------------------
+// Input gradient of the large network's third convolution (64 -> 64
+// channels, 3x3 stride 1, 9x9 -> 7x7):
+//   din[c][y][x] = [h_in > 0] * sum_{o, ky, kx} W[o][c][ky][kx] * dz[o][y - ky][x - kx]
+// with dz = 0 outside the 7x7 map, in the same arrangement: a workgroup walks
+// samples; its eight waves are (N-tile of 16 input channels, half of the six
+// M-tiles of the 81 pixels) pairs, each holding its 16 x 576 weight slice in
+// registers.  dz is staged with two zero rows above and below and two zero
+// columns on the right of each 7-wide row, at a row stride of 9, so pixel m
+// = 9y + x reads tap (ky, kx) at m + 18 - 9ky - kx past its channel's base:
+// 16 consecutive pixels are contiguous and reads that leave a row land on
+// zeros.
+constexpr int D3_CIN = 64, D3_IH = 9, D3_COUT = 64, D3_OH = 7, D3_K = 3;
+constexpr int D3_P = D3_IH * D3_IH;            // input pixels per sample (81)
+constexpr int D3_MT = (D3_P + 15) / 16;        // M-tiles (6)
+constexpr int D3_TPW = D3_MT / 2;              // M-tiles per wave (3)
+constexpr int D3_CS = 112;                     // staged floats per dz channel
+constexpr int D3_ROW0 = 2 * D3_IH;             // two zero rows
+constexpr int D3_LEAD = 16, D3_TAIL = 32;
+constexpr int D3_STAGE = D3_LEAD + D3_COUT * D3_CS + D3_TAIL;
+constexpr int D3_DZ = D3_COUT * D3_OH * D3_OH; // dz floats per sample (3,136)
+constexpr int D3_IN = D3_CIN * D3_P;           // input-gradient floats per sample (5,184)
+constexpr int D3_KT = D3_COUT * D3_K * D3_K;   // contraction length (tap, o): 576
+constexpr int D3_PER = (D3_DZ + D2_WG - 1) / D2_WG;
+constexpr int D3_OUT4 = (D3_IN / 4 + D2_WG - 1) / D2_WG;
+static_assert(D3_CS >= (D3_OH + 4) * D3_IH && D3_CS % 64 == 48, "channel stride: border and banks");
+static_assert(D3_MT % 2 == 0 && D3_IN % 4 == 0, "tile split and float4 rows");
+
+template <bool BF16>
+__global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
+    __shared__ float s_dz[D3_STAGE];
+    __shared__ __align__(16) float s_din[D3_IN];
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int nt = wave & 3, mh = wave >> 2;   // N-tile; half of the M-tiles
+
+    for (int e = t; e < D3_STAGE; e += D2_WG) s_dz[e] = 0.f;
+
+    const int j_lo = blockIdx.x * p.spg;
+    const int j_hi = min(p.n, j_lo + p.spg);
+    if (j_lo >= j_hi) return;  // uniform
+
+    // B operands for every k-step: k = tap * 64 + o, tap = 3ky + kx.
+    const int c = nt * 16 + li;
+    constexpr int KS = BF16 ? D3_KT / 32 : D3_KT / 4;
+    using BOp = typename std::conditional<BF16, bf16x8, float>::type;
+    BOp wreg[KS];
+    {
+        const float* wc = p.w + (size_t)c * D3_K * D3_K;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            if constexpr (BF16) {
+                const int tap = s / 2;   // o = 32 * (s % 2) + 4e + g
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int o = 32 * (s % 2) + 4 * e + g;
+                    wreg[s][e] = (__bf16)wc[(size_t)o * D3_CIN * D3_K * D3_K + tap];
+                }
+            } else {
+                const int tap = s / 16, o = 4 * (s % 16) + g;
+                wreg[s] = wc[(size_t)o * D3_CIN * D3_K * D3_K + tap];
+            }
+        }
+    }
+
+    int base[D3_TPW];
+#pragma unroll
+    for (int i = 0; i < D3_TPW; ++i)
+        base[i] = D3_LEAD + g * D3_CS + (mh * D3_TPW + i) * 16 + li + D3_ROW0;
+
+    float v[D3_PER];
+    auto fetch = [&](int j) {
+        const float* src = p.dz + (size_t)j * D3_DZ;
+#pragma unroll
+        for (int u = 0; u < D3_PER; ++u) {
+            const int e = t + u * D2_WG;
+            v[u] = e < D3_DZ ? src[e] : 0.f;
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < D3_PER; ++u) {
+            const int e = t + u * D2_WG;
+            if (e < D3_DZ) {
+                const int o = e / (D3_OH * D3_OH), q = e - o * (D3_OH * D3_OH);
+                // row oy + 2 at stride 9: offset 18 + q + 2 * (q / 7)
+                s_dz[D3_LEAD + o * D3_CS + D3_ROW0 + q + 2 * (q / D3_OH)] = v[u];
+            }
+        }
+    };
+
+    fetch(j_lo);
+    for (int j = j_lo; j < j_hi; ++j) {
+        __syncthreads();
+        stage();
+        __syncthreads();
+        if (j + 1 < j_hi) fetch(j + 1);
+
+        f4 acc[D3_TPW];
+#pragma unroll
+        for (int i = 0; i < D3_TPW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        if constexpr (BF16) {
+            auto load = [&](int s, bf16x8 (&a)[D3_TPW]) {
+                const int tap = s / 2, ky = tap / 3, kx = tap % 3;
+                const int off = 32 * (s % 2) * D3_CS - D3_IH * ky - kx;
+#pragma unroll
+                for (int i = 0; i < D3_TPW; ++i) {
+                    const float* ap = s_dz + base[i] + off;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) a[i][e] = (__bf16)ap[4 * e * D3_CS];
+                }
+            };
+            bf16x8 a[2][D3_TPW];
+            load(0, a[0]);
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                if (s + 1 < KS) load(s + 1, a[(s + 1) & 1]);
+#pragma unroll
+                for (int i = 0; i < D3_TPW; ++i) acc[i] = mfma16x16x32bf16(a[s & 1][i], wreg[s], acc[i]);
+                if (s + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 8 * D3_TPW, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, D3_TPW, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+            auto load = [&](int s, float (&a)[D3_TPW]) {
+                const int tap = s / 16, ky = tap / 3, kx = tap % 3;
+                const int off = 4 * (s % 16) * D3_CS - D3_IH * ky - kx;
+#pragma unroll
+                for (int i = 0; i < D3_TPW; ++i) a[i] = s_dz[base[i] + off];
+            };
+            float a[2][D3_TPW];
+            load(0, a[0]);
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                if (s + 1 < KS) load(s + 1, a[(s + 1) & 1]);
+#pragma unroll
+                for (int i = 0; i < D3_TPW; ++i) acc[i] = mfma16x16x4(a[s & 1][i], wreg[s], acc[i]);
+                if (s + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x100, D3_TPW, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, D3_TPW, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+
+        // D[4g + r][li] of tile i: pixel m, channel c
+#pragma unroll
+        for (int i = 0; i < D3_TPW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = (mh * D3_TPW + i) * 16 + 4 * g + r;
+                if (m < D3_P) s_din[c * D3_P + m] = acc[i][r];
+            }
+        __syncthreads();
+        const size_t o0 = (size_t)j * D3_IN;
+#pragma unroll
+        for (int u = 0; u < D3_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D3_IN / 4) {
+                const f4 h = *(const f4*)(p.h_in + o0 + 4 * e4);
+                const f4 d = *(const f4*)(s_din + 4 * e4);
+                f4 o;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) o[k] = h[k] > 0.f ? d[k] : 0.f;
+                *(f4*)(p.din + o0 + 4 * e4) = o;
+            }
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
+                              hipStream_t st) {
+    if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15)) return hipErrorInvalidValue;
+    const int spg = std::max(1, (n + 255) / 256);
+    const int blocks = (n + spg - 1) / spg;
+    const Dgrad2Params prm{dz, w, h_in, din, n, spg};
+    if (bf16)
+        hipLaunchKernelGGL(conv3_dgrad_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    else
+        hipLaunchKernelGGL(conv3_dgrad_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    return hipGetLastError();
+}
 
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
                                     bool bf16, hipStream_t st) {
