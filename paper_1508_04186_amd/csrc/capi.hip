@@ -89,6 +89,9 @@ bool g_fusion = true;  // dqn_profile_set_fusion
 // run as one implicit GEMM over all samples (2-3x the per-layer kernel from
 // 256 samples; slower at 64).
 constexpr int kIgemmMinRows = 128;
+// Batch from which the conv2/conv3 weight gradients run with the outputs in
+// registers across samples.
+constexpr int kRegWgradMinRows = 128;
 
 // Backward layers that run as implicit GEMMs at batch B (measured faster
 // than the per-layer kernels from 128 samples: the weight gradients of
@@ -99,6 +102,9 @@ constexpr int kIgemmMinRows = 128;
 bool igemm_wgrad(ConvId id, int B, bool bf16) {
     return (id == CONV_L2 || id == CONV_L3) && (bf16 || B >= kIgemmMinRows);
 }
+// ... of which the samples-per-workgroup kernel with register-held outputs
+// (k_wgrad.hip) takes the batches it is faster for.
+bool reg_wgrad(ConvId id, int B, bool bf16) { return igemm_wgrad(id, B, bf16) && B >= kRegWgradMinRows; }
 bool igemm_dgrad(ConvId id, int B, bool bf16) { return id == CONV_L3 && (bf16 || B >= kIgemmMinRows); }
 // conv2's and conv3's input gradients of the large network with the weights
 // in registers (from the same batch size; k_dgrad.hip).
@@ -161,6 +167,7 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
             slots = std::max<int64_t>(slots, conv_s12_bwd_slots(B));
         if (igemm_wgrad(ni.conv[l], B, ni.bf16))
             slots = std::max<int64_t>(slots, conv_igemm_wgrad_chunks(ni.conv[l], B));
+        if (reg_wgrad(ni.conv[l], B, ni.bf16)) slots = std::max<int64_t>(slots, conv_wgrad_reg_slots(ni.conv[l], B));
         if (l == 0 && conv1_u8(ni.conv[0], B, ni.bf16)) slots = std::max<int64_t>(slots, conv1_u8_wgrad_slots(B));
         t.wpart[l] = cv.take<float>(ws, slots * c.cout * c.cin * c.k * c.k);
         t.bpart[l] = cv.take<float>(ws, slots * c.cout);
@@ -399,6 +406,10 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             RUN(DQN_K_CONV1_WGRAD,
                 launch_conv1_u8_wgrad(CONV_L1, s0, t.dconv[0], B, t.wpart[0], t.bpart[0], scale, ni.bf16, st));
             chunks_used[0] = conv1_u8_wgrad_slots(B);
+        } else if (reg_wgrad(ni.conv[l], B, ni.bf16)) {
+            RUN(DQN_K_CONV1_WGRAD + l,
+                launch_conv_wgrad_reg(ni.conv[l], t.act[l - 1], t.dconv[l], B, t.wpart[l], t.bpart[l], ni.bf16, st));
+            chunks_used[l] = conv_wgrad_reg_slots(ni.conv[l], B);
         } else if (igemm_wgrad(ni.conv[l], B, ni.bf16)) {
             RUN(DQN_K_CONV1_WGRAD + l,
                 launch_conv_igemm_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale,

@@ -183,6 +183,14 @@ hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float
 hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
                               hipStream_t st);
 
+// Weight/bias gradient partial sums of CONV_L2 or CONV_L3 for n samples, one
+// workgroup per run of samples holding every output in registers:
+// conv_wgrad_reg_slots(id, n) slots of wpart [slots][64][cin*k*k] and bpart
+// [slots][64].  in: the layer input [n][cin][ih][iw] (floats).
+int conv_wgrad_reg_slots(ConvId id, int n);
+hipError_t launch_conv_wgrad_reg(ConvId id, const float* in, const float* dz, int n, float* wpart, float* bpart,
+                                 bool bf16, hipStream_t st);
+
 // Weight/bias gradient partial sums of a large-network layer for n samples as
 // an implicit GEMM over pixel chunks: conv_igemm_wgrad_chunks(id, n) slots of
 // wpart [slots][cout][cin*k*k] and bpart [slots][cout].  in: the layer input
