@@ -295,6 +295,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--precision", default="fp32", choices=["fp32", "bf16"],
                     help="configs 3, 4a, 4b: fp32, or the bf16-input MFMA variant (fp32 accumulation)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="config 2: the server-bottleneck sweep over replicas and batch instead of the fixed run")
     ap.add_argument("--no-denominators", action="store_true",
                     help="skip the measured matrix-core and HBM copy peaks")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -316,8 +318,11 @@ def main():
     if args.precision == "bf16" and args.config not in ("3", "4a", "4b"):
         print("--precision bf16 applies to the large network (configs 3, 4a, 4b)", file=sys.stderr)
         sys.exit(2)
-    out = {"0": bench_single, "1": bench_sequential, "2": bench_replicas, "3": bench_large,
-           "4a": bench_forward, "4b": bench_large}[args.config](args)
+    if args.sweep and args.config != "2":
+        print("--sweep applies to config 2", file=sys.stderr)
+        sys.exit(2)
+    out = {"0": bench_single, "1": bench_sequential, "2": bench_replica_sweep if args.sweep else bench_replicas,
+           "3": bench_large, "4a": bench_forward, "4b": bench_large}[args.config](args)
     if not args.no_denominators:
         out["denominators"] = measure_denominators()
     if args.calib_copy_mib > 0:
@@ -552,6 +557,91 @@ def bench_sequential(args):
 
 # ---------------------------------------------------------------------------
 # config 2
+
+def bench_replica_sweep(args):
+    """The server-bottleneck study on one GPU (Sec. IV.D.1, Fig. 3's
+    question): updates/s of the replica schedule for P worker replicas and
+    batch B, against the paper's model min(P/T, 1/tau) with T the time of
+    one worker gradient and tau of one server update, both measured here
+    alone.  Staleness is min(4, P - 1).  AdaGrad, small network, the
+    100,000-transition replay."""
+    import torch
+    import dqn_inputs as di
+    import paper_1508_04186_amd as dq
+    dev = torch.device("cuda:0")
+    net, shape = _small_setup(dev)
+    SIZE, SEED, LR, EPS, GAMMA = 100_000, 1002, 0.01, 1e-8, 0.99
+    U = args.steps or 1000
+    log(f"replay: generating {SIZE} transitions (seed {SEED})")
+    hr = di.host_replay(SIZE, shape.n_actions, SEED)
+    rec, ra, rr, rt = di.device_replay(SIZE, shape.n_actions, SEED, device=dev, host=hr)
+    rp = dq.Replay(rec, ra, rr, rt, SIZE)
+    th0 = torch.from_numpy(di.xavier_theta(shape, SEED)).to(dev)
+    P = dq.dqn_param_count(net)
+    RS = dq.dqn_train_ring_stride(net)
+    rows = []
+    for B in (32, 128, 512):
+        idx = torch.from_numpy(di.index_stream(U, B, SIZE, SEED + B)).to(dev)
+        # T and tau alone
+        s = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
+        sn = torch.empty_like(s)
+        a = torch.empty(B, dtype=torch.int32, device=dev)
+        r = torch.empty(B, dtype=torch.float32, device=dev)
+        t = torch.empty(B, dtype=torch.uint8, device=dev)
+        g = torch.empty(P, dtype=torch.float32, device=dev)
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+        G = torch.zeros(P, dtype=torch.float32, device=dev)
+        tws = dq.workspace(net, B, dq.DQN_OP_TD_GRADIENT, dev)
+        th = th0.clone()
+
+        def grad_only(n):
+            for i in range(n):
+                dq.dqn_td_gradient_replay(net, th, th, rp, idx[i], GAMMA, g, loss, ws=tws)
+
+        def update_only(n):
+            for _ in range(n):
+                dq.ps_apply_update(dq.PS_ADAGRAD, th, th, G, g, LR, 0.0, EPS)
+        grad_only(20)
+        update_only(20)
+        T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(200)) / 200
+        tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(200)) / 200
+        del tws
+        for R in (1, 2, 4, 8, 16, 32):
+            S = min(4, R - 1)
+            ring = torch.empty((S + 1) * RS, dtype=torch.float32, device=dev)
+            ws = torch.empty(dq.dqn_train_workspace_bytes(net, B, R), dtype=torch.uint8, device=dev)
+            hs = dq.HipStreams(R + 1)
+
+            def run(n):
+                ring[:P].copy_(th0)
+                G.zero_()
+                torch.cuda.synchronize()
+                dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA, rp, idx[:n], R, S,
+                                      hs.handles, ws=ws)
+            run(min(50, U))
+            ring[:P].copy_(th0)
+            G.zero_()
+            ms = time_region(torch.cuda.synchronize,
+                             lambda: dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA, rp,
+                                                           idx, R, S, hs.handles, ws=ws))
+            hs.close()
+            ups = U / (ms * 1e-3)
+            model = min(R / (T_us * 1e-6), 1.0 / (tau_us * 1e-6))
+            rows.append({"batch": B, "replicas": R, "staleness": S, "updates_per_s": round(ups, 1),
+                         "transitions_per_s": round(ups * B, 1), "T_us": round(T_us, 2),
+                         "tau_us": round(tau_us, 2), "model_updates_per_s": round(model, 1)})
+            log(f"B={B} P={R} S={S}: {ups:.0f} updates/s (T {T_us:.1f} us, tau {tau_us:.1f} us, "
+                f"model {model:.0f})")
+            del ring, ws
+    best = max(rows, key=lambda x: x["transitions_per_s"])
+    out = base_record(U, 0, U / best["updates_per_s"] * 1e3)
+    out["config"] = {"workload": "server-bottleneck sweep: small Q-network, AdaGrad, replicas P in 1..32 on "
+                                 "streams, batch B in 32/128/512, 100,000-transition device replay",
+                     "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "replay_transitions": SIZE}
+    out["note"] = "value is the best updates/s over the sweep; every point is in sweep"
+    out["sweep"] = rows
+    return out
+
 
 def bench_replicas(args):
     import torch
