@@ -74,6 +74,15 @@ def _lib():
         lib.oracle_apply_update.argtypes = [ctypes.c_int32, _P, _P, _P, _P, ctypes.c_int64,
                                             ctypes.c_double, ctypes.c_double, ctypes.c_double]
         lib.oracle_bf16_round.argtypes = [_P, ctypes.c_int64, _P]
+        lib.oracle_snake_reset.argtypes = [_P, ctypes.c_int64, _P, _P]
+        lib.oracle_snake_step.argtypes = [_P, ctypes.c_int64, _P, _P, _P, _P, _P]
+        lib.oracle_replay_append.argtypes = [_P, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                             ctypes.c_int64, _P, _P, _P, _P, _P, _P, _P]
+        lib.oracle_anneal_epsilon.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_double,
+                                              ctypes.c_double]
+        lib.oracle_anneal_epsilon.restype = ctypes.c_double
+        for f in ("oracle_snake_reset", "oracle_snake_step", "oracle_replay_append"):
+            getattr(lib, f).restype = ctypes.c_int
         for f in ("oracle_replay_gather", "oracle_forward_q", "oracle_relu_margins", "oracle_bf16_round",
                   "oracle_select_actions",
                   "oracle_td_gradient", "oracle_apply_update"):
@@ -279,3 +288,64 @@ def stale_replica_training(net, theta0, rep, idx_stream, gamma, lr, staleness, r
         if callback is not None:
             callback(u, new, state, out)
     return versions[-1], state, np.array(losses)
+
+
+# ----------------------------------------------------------------------------
+# The actor side of Alg. 1: Snake games and the replay memory they fill
+
+SNAKE_GRID = 12
+SNAKE_STATE_INTS = SNAKE_GRID * SNAKE_GRID + 3   # body cells, length, heading, apple
+
+
+class SnakeGames:
+    """E Snake games (oracle.c states the rules and the readings) with their
+    stacked-frame states uint8 [E][4][84][84]."""
+
+    def __init__(self, E: int, draws):
+        self.E = E
+        self.games = np.zeros((E, SNAKE_STATE_INTS), np.int32)
+        self.states = np.zeros((E, 4, 84, 84), np.uint8)
+        d = np.ascontiguousarray(draws, dtype=np.uint64).reshape(E, 2)
+        _check(_lib().oracle_snake_reset(self.games.ctypes.data, E, d.ctypes.data, self.states.ctypes.data),
+               "oracle_snake_reset")
+
+    def step(self, actions, draws):
+        """Returns (reward float32 [E], terminal uint8 [E]); states advance."""
+        a = np.ascontiguousarray(actions, dtype=np.int32)
+        d = np.ascontiguousarray(draws, dtype=np.uint64).reshape(self.E, 2)
+        r = np.empty(self.E, np.float32)
+        t = np.empty(self.E, np.uint8)
+        _check(_lib().oracle_snake_step(self.games.ctypes.data, self.E, a.ctypes.data, d.ctypes.data,
+                                        self.states.ctypes.data, r.ctypes.data, t.ctypes.data),
+               "oracle_snake_step")
+        return r, t
+
+    def lengths(self):
+        return self.games[:, SNAKE_GRID * SNAKE_GRID].copy()
+
+
+class SegmentedReplay:
+    """Replay memory pooled over E games, each keeping its last N states in
+    N + 1 records (slot N repeats slot 0): see oracle_replay_append."""
+
+    def __init__(self, E: int, N: int, rec_bytes: int = 4 * 84 * 84):
+        self.E, self.N, self.rec = E, N, rec_bytes
+        self.frames = np.zeros((E * (N + 1), rec_bytes), np.uint8)
+        self.action = np.zeros(E * (N + 1), np.uint8)
+        self.reward = np.zeros(E * (N + 1), np.int8)
+        self.terminal = np.zeros(E * (N + 1), np.uint8)
+
+    def append(self, t, states, actions=None, reward=None, terminal=None):
+        st = np.ascontiguousarray(states, dtype=np.uint8)
+        a = None if actions is None else np.ascontiguousarray(actions, dtype=np.int32)
+        r = None if reward is None else np.ascontiguousarray(reward, dtype=np.float32)
+        tt = None if terminal is None else np.ascontiguousarray(terminal, dtype=np.uint8)
+        _check(_lib().oracle_replay_append(self.frames.ctypes.data, self.rec, self.E, self.N, int(t),
+                                           st.ctypes.data, _ptr(a), _ptr(r), _ptr(tt),
+                                           self.action.ctypes.data, self.reward.ctypes.data,
+                                           self.terminal.ctypes.data), "oracle_replay_append")
+
+
+def anneal_epsilon(n, n_max, eps_min, eps_max) -> float:
+    """Alg. 1: q = max((N_max - n)/N_max, 0); epsilon = (1 - q) eps_min + q eps_max."""
+    return float(_lib().oracle_anneal_epsilon(int(n), int(n_max), float(eps_min), float(eps_max)))

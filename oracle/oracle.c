@@ -31,6 +31,12 @@
  *                          descent (Sec. III.B), the RMSProp rule of Alg. 2,
  *                          and AdaGrad (named in Sec. IV.D.2).
  *
+ *   oracle_snake_*         the actor side of Alg. 1: the Snake game of
+ *                          Sec. V.A stepped by a chosen action, rendered as
+ *                          stacked 84x84 frames, and the experiences stored
+ *                          in a replay memory that keeps the last N of them
+ *                          (Sec. III.C), pooled over game instances.
+ *
  * The bf16-input variant (net->bf16_inputs = 1) computes the same functions
  * with every operand of the layer contractions -- the conv and fc1 weights,
  * the conv and fc1 input activations, and the back-propagated gradients
@@ -613,4 +619,174 @@ int oracle_apply_update(int32_t rule, const float* theta_in, float* theta_out, f
         theta_out[i] = (float)th;
     }
     return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* The actor side of Alg. 1 ("Execute action a_t and observe reward r_t and
+ * frame x_{t+1}; store the experience in D").  The game is Snake as Sec. V.A
+ * describes it: an n x n array; the snake starts with a body of length two
+ * and grows by one when it eats an apple, which scores +1; hitting itself
+ * ends the game and scores -1.  Readings where the text is silent:
+ *  - the board wraps around at its edges (a torus), so hitting itself is the
+ *    only way a game ends, as the text says;
+ *  - actions 0..3 set the heading (up, right, down, left); any other action,
+ *    and the reverse of the current heading, keep it;
+ *  - the tail leaves its cell in the same move, so moving into it is not a
+ *    collision; when the snake eats, the tail stays;
+ *  - random placement uses two caller-supplied 64-bit words per game and
+ *    step: a new game puts the head on cell floor(lo32(w0) * n^2 / 2^32)
+ *    with heading hi2(w0), the second body cell behind it; an apple goes to
+ *    the k-th free cell in row-major order, k = floor(hi32(w1) * free / 2^32);
+ *  - a finished game restarts at once; the experience that ended it stores
+ *    the new game's first state as its next state (its target is r alone, so
+ *    that state is never evaluated);
+ *  - a frame is 84 x 84 bytes, each cell a 7 x 7 block: 0 empty, 128 body,
+ *    255 head, 192 apple; a state stacks the last four frames, oldest first,
+ *    and a new game's state is four copies of its first frame. */
+
+#define SNAKE_N 12
+#define SNAKE_CELLS (SNAKE_N * SNAKE_N)
+#define SNAKE_PX 7
+#define SNAKE_FRAME (84 * 84)
+
+typedef struct {
+    int32_t body[SNAKE_CELLS]; /* cell indices, body[0] the head */
+    int32_t len, heading, apple;
+} oracle_snake;
+
+static const int snake_dy[4] = {-1, 0, 1, 0};
+static const int snake_dx[4] = {0, 1, 0, -1};
+
+static int snake_move(int cell, int heading) {
+    int y = cell / SNAKE_N, x = cell % SNAKE_N;
+    y = (y + snake_dy[heading] + SNAKE_N) % SNAKE_N;
+    x = (x + snake_dx[heading] + SNAKE_N) % SNAKE_N;
+    return y * SNAKE_N + x;
+}
+
+static int snake_on_body(const oracle_snake* g, int cell, int upto) {
+    for (int i = 0; i < upto; ++i)
+        if (g->body[i] == cell) return 1;
+    return 0;
+}
+
+static void snake_place_apple(oracle_snake* g, uint64_t w1) {
+    int free_cells = SNAKE_CELLS - g->len;
+    uint64_t k = ((w1 >> 32) * (uint64_t)free_cells) >> 32;
+    for (int c = 0; c < SNAKE_CELLS; ++c) {
+        if (snake_on_body(g, c, g->len)) continue;
+        if (k == 0) { g->apple = c; return; }
+        --k;
+    }
+    g->apple = -1; /* the board is full */
+}
+
+static void snake_new_game(oracle_snake* g, uint64_t w0, uint64_t w1) {
+    int head = (int)(((w0 & 0xffffffffull) * (uint64_t)SNAKE_CELLS) >> 32);
+    g->heading = (int)(w0 >> 62);
+    g->body[0] = head;
+    g->body[1] = snake_move(head, (g->heading + 2) % 4);
+    g->len = 2;
+    snake_place_apple(g, w1);
+}
+
+static void snake_render(const oracle_snake* g, uint8_t* frame) {
+    for (int p = 0; p < SNAKE_FRAME; ++p) {
+        int y = p / 84, x = p % 84;
+        int cell = (y / SNAKE_PX) * SNAKE_N + x / SNAKE_PX;
+        uint8_t v = 0;
+        if (cell == g->apple) v = 192;
+        if (snake_on_body(g, cell, g->len)) v = 128;
+        if (cell == g->body[0]) v = 255;
+        frame[p] = v;
+    }
+}
+
+/* New games for every env: states [E][4][84][84] get four copies of the
+ * first frame.  draws: [E][2]. */
+int oracle_snake_reset(oracle_snake* games, int64_t E, const uint64_t* draws, uint8_t* states) {
+    if (!games || !draws || !states || E < 0) return ORACLE_EINVAL;
+    for (int64_t e = 0; e < E; ++e) {
+        snake_new_game(&games[e], draws[2 * e], draws[2 * e + 1]);
+        uint8_t* st = states + e * 4 * SNAKE_FRAME;
+        snake_render(&games[e], st);
+        for (int f = 1; f < 4; ++f) memcpy(st + f * SNAKE_FRAME, st, SNAKE_FRAME);
+    }
+    return ORACLE_OK;
+}
+
+/* One step of every game with its action; states advance by one frame (or
+ * restart on a finished game).  reward [E] (float), terminal [E]. */
+int oracle_snake_step(oracle_snake* games, int64_t E, const int32_t* actions, const uint64_t* draws,
+                      uint8_t* states, float* reward, uint8_t* terminal) {
+    if (!games || !actions || !draws || !states || !reward || !terminal || E < 0) return ORACLE_EINVAL;
+    for (int64_t e = 0; e < E; ++e) {
+        oracle_snake* g = &games[e];
+        int a = actions[e];
+        if (a >= 0 && a < 4 && a != (g->heading + 2) % 4) g->heading = a;
+        int nh = snake_move(g->body[0], g->heading);
+        float r = 0.f;
+        uint8_t term = 0;
+        int eats = nh == g->apple;
+        /* every segment but the tail, which moves away unless the snake eats */
+        if (snake_on_body(g, nh, eats ? g->len : g->len - 1)) {
+            r = -1.f;
+            term = 1;
+        } else {
+            int keep = eats ? g->len : g->len - 1;
+            for (int i = keep; i > 0; --i) g->body[i] = g->body[i - 1];
+            g->body[0] = nh;
+            if (eats) {
+                g->len += 1;
+                r = 1.f;
+                snake_place_apple(g, draws[2 * e + 1]);
+            }
+        }
+        uint8_t* st = states + e * 4 * SNAKE_FRAME;
+        if (term) {
+            snake_new_game(g, draws[2 * e], draws[2 * e + 1]);
+            snake_render(g, st);
+            for (int f = 1; f < 4; ++f) memcpy(st + f * SNAKE_FRAME, st, SNAKE_FRAME);
+        } else {
+            memmove(st, st + SNAKE_FRAME, 3 * SNAKE_FRAME);
+            snake_render(g, st + 3 * SNAKE_FRAME);
+        }
+        reward[e] = r;
+        terminal[e] = term;
+    }
+    return ORACLE_OK;
+}
+
+/* The replay memory keeps the last N states of each game (Sec. III.C): game
+ * e owns records e*(N+1) .. e*(N+1)+N of `frames` (rec_bytes each); state t
+ * of the game lives in slot t mod N, and slot N repeats slot 0, so the
+ * successor of every slot is the next record.  Experience t of game e is
+ * (state t, a_t, r_t, term_t, state t+1): its side fields are stored at the
+ * record of state t.  t = -1 stores the initial states only. */
+int oracle_replay_append(uint8_t* frames, int64_t rec_bytes, int64_t E, int64_t N, int64_t t,
+                         const uint8_t* states, const int32_t* actions, const float* reward,
+                         const uint8_t* terminal, uint8_t* action_mem, int8_t* reward_mem,
+                         uint8_t* terminal_mem) {
+    if (!frames || !states || E < 0 || N < 2 || t < -1 || rec_bytes <= 0) return ORACLE_EINVAL;
+    for (int64_t e = 0; e < E; ++e) {
+        int64_t base = e * (N + 1);
+        int64_t slot = (t + 1) % N;
+        memcpy(frames + (base + slot) * rec_bytes, states + e * rec_bytes, (size_t)rec_bytes);
+        if (slot == 0) memcpy(frames + (base + N) * rec_bytes, states + e * rec_bytes, (size_t)rec_bytes);
+        if (t >= 0) {
+            int64_t r = base + t % N;
+            action_mem[r] = (uint8_t)actions[e];
+            reward_mem[r] = (int8_t)reward[e];
+            terminal_mem[r] = terminal[e];
+        }
+    }
+    return ORACLE_OK;
+}
+
+/* Exploration rate of Alg. 1 at iteration n: q = max((N_max - n)/N_max, 0),
+ * epsilon = (1 - q) eps_min + q eps_max. */
+double oracle_anneal_epsilon(int64_t n, int64_t n_max, double eps_min, double eps_max) {
+    double q = n_max > 0 ? (double)(n_max - n) / (double)n_max : 0.0;
+    if (q < 0.0) q = 0.0;
+    return (1.0 - q) * eps_min + q * eps_max;
 }
