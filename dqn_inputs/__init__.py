@@ -145,6 +145,30 @@ def index_stream(steps: int, batch: int, size: int, seed: int) -> np.ndarray:
     return rng.integers(0, size - 1, size=(steps, batch), dtype=np.int64)
 
 
+def game_draws(n_games: int, seed: int, step: int) -> np.ndarray:
+    """uint64 [n_games][2] placement words for the games at one step (a new
+    game's head and heading from word 0, an apple's cell from word 1); step
+    -1 is the first reset."""
+    rng = np.random.default_rng([seed, 0x5A4E, step + 1])
+    return rng.integers(0, 2**64, size=(n_games, 2), dtype=np.uint64)
+
+
+def actor_minibatch(batch: int, seed: int, step: int, n_games: int, capacity: int, moves: int) -> np.ndarray:
+    """int64 [batch] record indices drawn uniformly with replacement over the
+    valid experiences of a replay pooled over n_games games that each keep
+    their last `capacity` states (include/dqn_actor.h), after `moves` moves
+    of every game: experiences t = max(0, moves-capacity+1) .. moves-1 of game
+    e sit at record e*(capacity+1) + t mod capacity."""
+    count = min(moves, capacity - 1)
+    if count <= 0:
+        raise ValueError("no complete experience yet")
+    rng = np.random.default_rng([seed, 0xAC70, step])
+    k = rng.integers(0, n_games * count, size=batch)
+    e, off = k // count, k % count
+    t = moves - count + off
+    return (e * (capacity + 1) + t % capacity).astype(np.int64)
+
+
 def egreedy_draws(batch: int, seed: int) -> np.ndarray:
     """uint64 [batch] exploration draws: high 32 bits decide exploration,
     low 32 bits pick the random action."""

@@ -17,4 +17,5 @@ from .native import (  # noqa: F401
     workspace, profile_attach, profile_used, profile_set_fusion, KERNEL_NAMES,
     dqn_train_workspace_bytes, dqn_train_ring_stride, dqn_train_steps, dqn_train_replicas,
     HipStreams, DQN_PEAK_FP32, DQN_PEAK_BF16, profile_mfma_peak, profile_stream_copy,
+    ActorReplay, snake_games, snake_reset, snake_step, dqn_anneal_epsilon, dqn_act, SNAKE_STATE_BYTES,
 )

@@ -34,6 +34,11 @@ class _CReplay(ctypes.Structure):
                 ("c", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32)]
 
 
+class _CReplayOut(ctypes.Structure):
+    _fields_ = [("frames", ctypes.c_void_p), ("action", ctypes.c_void_p), ("reward", ctypes.c_void_p),
+                ("terminal", ctypes.c_void_p), ("record_stride", ctypes.c_int64), ("capacity", ctypes.c_int64)]
+
+
 @dataclass(frozen=True)
 class Net:
     """Q-network shape: conv layers as (out_channels, kernel, stride)."""
@@ -133,6 +138,18 @@ def lib():
         L.dqn_profile_set_fusion.restype = ctypes.c_int
         L.dqn_profile_used.argtypes = [ctypes.c_int32]
         L.dqn_profile_used.restype = ctypes.c_int32
+        L.snake_state_bytes.argtypes = [ctypes.c_int32]
+        L.snake_state_bytes.restype = ctypes.c_int64
+        L.snake_reset.argtypes = [_P, ctypes.c_int32, _P, _P, ctypes.POINTER(_CReplayOut), _P]
+        L.snake_reset.restype = ctypes.c_int
+        L.snake_step.argtypes = [_P, ctypes.c_int32, _P, _P, _P, _P, _P, ctypes.POINTER(_CReplayOut),
+                                 ctypes.c_int64, _P]
+        L.snake_step.restype = ctypes.c_int
+        L.dqn_anneal_epsilon.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_double, ctypes.c_double]
+        L.dqn_anneal_epsilon.restype = ctypes.c_double
+        L.dqn_act.argtypes = [ctypes.POINTER(_CNet), _P, _P, ctypes.c_int32, _P, ctypes.c_float, _P, _P, _P,
+                              _P, _P, ctypes.POINTER(_CReplayOut), ctypes.c_int64, _P, ctypes.c_size_t, _P]
+        L.dqn_act.restype = ctypes.c_int
         L.dqn_profile_mfma_peak.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, _P]
         L.dqn_profile_mfma_peak.restype = ctypes.c_int64
         L.dqn_profile_stream_copy.argtypes = [_P, _P, ctypes.c_int64, ctypes.c_int32, _P]
@@ -496,3 +513,83 @@ def profile_stream_copy(src, dst, workgroups: int, stream=None) -> None:
         raise ValueError("src and dst must have the same byte size")
     _check(lib().dqn_profile_stream_copy(_ptr(src, None, "src"), _ptr(dst, None, "dst"), nb,
                                          int(workgroups), _stream(stream)), "dqn_profile_stream_copy")
+
+
+# ----------------------------------------------------------------------------
+# The actor side of Alg. 1 (include/dqn_actor.h)
+
+SNAKE_STATE_BYTES = 512
+
+
+class ActorReplay:
+    """Replay memory pooled over n_games games, each keeping its last
+    `capacity` states in capacity + 1 device records (include/dqn_actor.h);
+    `view` is the same memory as a Replay for replay_gather and
+    dqn_td_gradient_replay."""
+
+    def __init__(self, n_games: int, capacity: int, device="cuda"):
+        import torch
+        self.n_games, self.capacity = n_games, capacity
+        n = n_games * (capacity + 1)
+        self.frames = torch.zeros((n, 4, 84, 84), dtype=torch.uint8, device=device)
+        self.action = torch.zeros(n, dtype=torch.uint8, device=device)
+        self.reward = torch.zeros(n, dtype=torch.int8, device=device)
+        self.terminal = torch.zeros(n, dtype=torch.uint8, device=device)
+        self.view = Replay(self.frames, self.action, self.reward, self.terminal, n)
+
+    def _c(self):
+        r = _CReplayOut()
+        r.frames, r.action = self.frames.data_ptr(), self.action.data_ptr()
+        r.reward, r.terminal = self.reward.data_ptr(), self.terminal.data_ptr()
+        r.record_stride, r.capacity = 4 * 84 * 84, self.capacity
+        return r
+
+
+def snake_games(n_games: int, device="cuda"):
+    """Device state of n_games games (uninitialized until snake_reset)."""
+    import torch
+    v = lib().snake_state_bytes(n_games)
+    _check(0 if v > 0 else int(v), "snake_state_bytes")
+    return torch.empty(int(v), dtype=torch.uint8, device=device)
+
+
+def snake_reset(games, draws, states, replay: ActorReplay | None = None, stream=None) -> None:
+    import torch
+    E = states.shape[0]
+    rp = replay._c() if replay is not None else None
+    _check(lib().snake_reset(_ptr(games, torch.uint8, "games"), E, _ptr(draws, torch.uint64, "draws"),
+                             _ptr(states, torch.uint8, "states"), ctypes.byref(rp) if rp else None,
+                             _stream(stream)), "snake_reset")
+
+
+def snake_step(games, actions, draws, states, reward_out, terminal_out, replay: ActorReplay | None = None,
+               t: int = 0, stream=None) -> None:
+    import torch
+    E = states.shape[0]
+    rp = replay._c() if replay is not None else None
+    _check(lib().snake_step(_ptr(games, torch.uint8, "games"), E, _ptr(actions, torch.int32, "actions"),
+                            _ptr(draws, torch.uint64, "draws"), _ptr(states, torch.uint8, "states"),
+                            _ptr(reward_out, torch.float32, "reward_out"),
+                            _ptr(terminal_out, torch.uint8, "terminal_out"), ctypes.byref(rp) if rp else None,
+                            int(t), _stream(stream)), "snake_step")
+
+
+def dqn_anneal_epsilon(n: int, n_max: int, eps_min: float, eps_max: float) -> float:
+    return float(lib().dqn_anneal_epsilon(int(n), int(n_max), float(eps_min), float(eps_max)))
+
+
+def dqn_act(net, theta, games, states, epsilon, eps_draws, env_draws, actions_out, reward_out, terminal_out,
+            replay: ActorReplay | None = None, t: int = 0, ws=None, stream=None) -> None:
+    """One acting step of Alg. 1 (include/dqn_actor.h dqn_act)."""
+    import torch
+    E = states.shape[0]
+    if ws is None:
+        ws = workspace(net, E, DQN_OP_FORWARD, states.device)
+    rp = replay._c() if replay is not None else None
+    _check(lib().dqn_act(ctypes.byref(_cnet(net)), _ptr(theta, torch.float32, "theta"),
+                         _ptr(games, torch.uint8, "games"), E, _ptr(states, torch.uint8, "states"),
+                         ctypes.c_float(epsilon), _ptr(eps_draws, torch.uint64, "eps_draws"),
+                         _ptr(env_draws, torch.uint64, "env_draws"), _ptr(actions_out, torch.int32, "actions_out"),
+                         _ptr(reward_out, torch.float32, "reward_out"),
+                         _ptr(terminal_out, torch.uint8, "terminal_out"), ctypes.byref(rp) if rp else None,
+                         int(t), _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)), "dqn_act")

@@ -219,6 +219,27 @@ def test_peak_check_argument_errors():
     assert L.dqn_profile_stream_copy(FAKE, FAKE + 8192, 4096, 0, None) == dq.DQN_EINVAL
 
 
+@fake_ptr_test
+def test_actor_argument_errors():
+    L = dq.lib()
+    assert L.snake_state_bytes(0) == dq.DQN_EINVAL
+    assert L.snake_state_bytes(3) == 3 * dq.SNAKE_STATE_BYTES
+    assert L.snake_reset(None, 4, FAKE, FAKE, None, None) == dq.DQN_EINVAL
+    assert L.snake_reset(FAKE, 0, FAKE, FAKE, None, None) == dq.DQN_EINVAL
+    assert L.snake_reset(FAKE + 8, 4, FAKE, FAKE, None, None) == dq.DQN_EINVAL      # misaligned games
+    rp = native._CReplayOut()
+    rp.frames, rp.action, rp.reward, rp.terminal = FAKE, FAKE, FAKE, FAKE
+    rp.record_stride, rp.capacity = 28224, 1                                        # capacity < 2
+    assert L.snake_reset(FAKE, 4, FAKE, FAKE, ctypes.byref(rp), None) == dq.DQN_EINVAL
+    rp.capacity, rp.record_stride = 8, 28220                                        # stride not a multiple of 16
+    assert L.snake_reset(FAKE, 4, FAKE, FAKE, ctypes.byref(rp), None) == dq.DQN_EINVAL
+    rp.record_stride = 28224
+    assert L.snake_step(FAKE, 4, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.byref(rp), -1, None) == dq.DQN_EINVAL
+    assert L.snake_step(FAKE, 4, None, FAKE, FAKE, FAKE, FAKE, None, 0, None) == dq.DQN_EINVAL
+    assert dq.dqn_anneal_epsilon(0, 100, 0.1, 1.0) == 1.0
+    assert dq.dqn_anneal_epsilon(250, 100, 0.1, 1.0) == 0.1
+
+
 def test_status_strings():
     for s in (dq.DQN_OK, dq.DQN_EINVAL, dq.DQN_EWORKSPACE, dq.DQN_EHIP, dq.DQN_EUNSUPPORTED):
         assert dq.dqn_status_string(s) not in ("", "unknown status")
