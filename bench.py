@@ -16,6 +16,13 @@ Configurations (--config; the default line is config 1):
   4a  large Q-network, epsilon-greedy forward pass (eps 0.05) over 8,192
       states gathered from the 1,000,000-transition replay.
   4b  large Q-network, TD gradient + SGD at batch 2,048 from that replay.
+  actor  Alg. 1 closed: 32 Snake games act with the small network
+      (epsilon-greedy, annealed epsilon), store into a replay pooled over
+      the games, and one TD gradient + SGD step follows on a minibatch of 32
+      drawn from it (a step = one such iteration).
+
+--precision bf16 runs configs 3, 4a and 4b with the bf16-input variant;
+--config 2 --sweep runs the server-bottleneck study over replicas and batch.
 
 A step is one pass of the whole hot path over one batch (config 2: one
 update; config 4a: one forward pass over 8,192 states).  Inputs are resident
@@ -286,7 +293,7 @@ def time_region(stream_sync, fn):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--config", default="1", choices=["0", "1", "2", "3", "4a", "4b"])
+    ap.add_argument("--config", default="1", choices=["0", "1", "2", "3", "4a", "4b", "actor"])
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default per config)")
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--breakdown-steps", type=int, default=50)
@@ -322,7 +329,7 @@ def main():
         print("--sweep applies to config 2", file=sys.stderr)
         sys.exit(2)
     out = {"0": bench_single, "1": bench_sequential, "2": bench_replica_sweep if args.sweep else bench_replicas,
-           "3": bench_large, "4a": bench_forward, "4b": bench_large}[args.config](args)
+           "3": bench_large, "4a": bench_forward, "4b": bench_large, "actor": bench_actor}[args.config](args)
     if not args.no_denominators:
         out["denominators"] = measure_denominators()
     if args.calib_copy_mib > 0:
@@ -557,6 +564,122 @@ def bench_sequential(args):
 
 # ---------------------------------------------------------------------------
 # config 2
+
+def bench_actor(args):
+    """Alg. 1 closed on one GPU: 32 Snake games act (epsilon-greedy forward
+    with the annealed epsilon, one move each, the experiences stored in a
+    replay pooled over the games that keeps the last 3,125 states per game,
+    100,000 in all), then one TD gradient + SGD step on a minibatch of 32
+    drawn uniformly from that replay, target network refreshed every 1,000
+    iterations.  A step is one such iteration."""
+    import torch
+    import dqn_inputs as di
+    import oracle
+    import paper_1508_04186_amd as dq
+    dev = torch.device("cuda:0")
+    net, shape = _small_setup(dev)
+    E, N, B, SEED, LR, GAMMA, C = 32, 3125, 32, 1005, 2.5e-4, 0.99, 1000
+    NMAX, EMIN, EMAX = 1000, 0.1, 1.0
+    FILL = 64
+    K = args.steps or 2000
+    W = args.warmup if args.warmup is not None else 50
+    total = FILL + W + K
+    th0 = di.xavier_theta(shape, SEED)
+    theta = torch.from_numpy(th0).to(dev)
+    tgt = torch.empty_like(theta)
+    games = dq.snake_games(E, dev)
+    states = torch.empty((E, 4, 84, 84), dtype=torch.uint8, device=dev)
+    rp = dq.ActorReplay(E, N, dev)
+    gd_host = np.stack([di.game_draws(E, SEED, t) for t in range(-1, total)])
+    gd = torch.from_numpy(gd_host).to(dev)
+    ed = torch.from_numpy(np.stack([di.egreedy_draws(E, SEED * 100003 + t) for t in range(total)])).to(dev)
+    eps = [float(F32(dq.dqn_anneal_epsilon(t, NMAX, EMIN, EMAX))) for t in range(total)]
+    # minibatch of iteration t is drawn after its move: t + 1 moves made
+    idx_host = np.stack([di.actor_minibatch(B, SEED, t, E, N, t + 1) for t in range(total)])
+    idx = torch.from_numpy(idx_host).to(dev)
+    acts = torch.empty(E, dtype=torch.int32, device=dev)
+    rew = torch.empty(E, dtype=torch.float32, device=dev)
+    term = torch.empty(E, dtype=torch.uint8, device=dev)
+    fws = dq.workspace(net, E, dq.DQN_OP_FORWARD, dev)
+    tws = torch.empty(dq.dqn_train_workspace_bytes(net, B, 1), dtype=torch.uint8, device=dev)
+    losses = torch.empty(total, dtype=torch.float32, device=dev)
+
+    def act(t):
+        dq.dqn_act(net, theta, games, states, eps[t], ed[t], gd[t + 1], acts, rew, term, rp, t, ws=fws)
+
+    def run(lo, hi):
+        for t in range(lo, hi):
+            act(t)
+            if t >= FILL:
+                dq.dqn_train_steps(net, theta, tgt, None, dq.PS_SGD, LR, 0.9, 0.0, GAMMA, rp.view, idx[t:t + 1],
+                                   step0=t - FILL, target_period=C, losses_out=losses[t:t + 1], ws=tws)
+
+    dq.snake_reset(games, gd[0], states, rp)
+    run(0, FILL + W)
+    torch.cuda.synchronize()
+    hip = HipEvents()
+    prof = Profiler(hip)
+    work = kernel_work(shape, B)
+    ebytes = E * 11 * 84 * 84          # read 3 frames, write the 4-frame state and its replay record
+    work["snake_step"] = (0, ebytes)
+    # the acting forward shares conv12_fwd, fc1_fwd and head with the TD step, so the roofline is
+    # taken over kernels that only one of them launches
+    cands = ("conv12_bwd", "fc1_bwd", "finalize_apply", "snake_step")
+    nb = min(args.breakdown_steps, K, 50)
+    bd = prof.breakdown(lambda: run(FILL + W, FILL + W + nb), nb, [k for k in work if k in cands] +
+                        ["conv12_fwd", "fc1_fwd", "head"])
+    # the games and the learner go on from where the breakdown left them
+    dom = max((k for k in bd if k in cands), key=lambda k: bd[k][0] * bd[k][1])
+    kid, ev = prof.attach(dom, K // SAMPLE_STRIDE + 4, SAMPLE_STRIDE)
+    lo = FILL + W + nb
+    Kt = K - nb
+    ms = time_region(torch.cuda.synchronize, lambda: run(lo, lo + Kt))
+    raw_us, used = prof.collect(kid, ev)
+    dom_us = raw_us - prof.overhead()
+    out = base_record(Kt, W, ms)
+    out["config"] = {
+        "workload": f"Alg. 1 closed: {E} Snake games (12x12 board, 84x84 frames) act epsilon-greedily with "
+                    f"annealed epsilon and store into a {E * N:,}-experience replay pooled over the games, then "
+                    f"one TD gradient + SGD step on a minibatch of {B}; target refreshed every {C}",
+        "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "games": E, "batch": B, "replay_states": E * N,
+        "update": "sgd", "lr": LR, "gamma": GAMMA, "epsilon": f"{EMAX} -> {EMIN} over {NMAX} iterations"}
+    out["env_steps_per_s"] = round(out["value"] * E, 1)
+    out["transitions_per_s"] = round(out["value"] * B, 1)
+    out["final_loss"] = float(losses[lo + Kt - 1].item())
+    out["roofline"] = roofline(work, dom, dom_us, used, 1, raw_us, None)
+    out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
+                        "launches_per_step": {k: v[1] / nb for k, v in bd.items()}}
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle loop for about {args.cpu_seconds:.0f}s")
+        og = oracle.SnakeGames(E, gd_host[0])
+        orp = oracle.SegmentedReplay(E, N)
+        orp.append(-1, og.states)
+        th = th0.copy()
+        n, c0 = 0, time.perf_counter()
+        while True:
+            q = oracle.forward_q(shape, th, og.states)
+            a = oracle.select_actions(q, eps[n], host_u64(ed, n))
+            r, tt = og.step(a, gd_host[n + 1])
+            orp.append(n, og.states, a, r, tt)
+            s, sn, aa, rr, ttt = oracle.replay_gather(orp.frames, orp.rec, orp.rec, len(orp.frames), orp.action,
+                                                      orp.reward, orp.terminal, idx_host[n])
+            res = oracle.td_gradient(shape, th, None, s.reshape(B, 4, 84, 84), sn.reshape(B, 4, 84, 84), aa, rr,
+                                     ttt, float(F32(GAMMA)))
+            th, _ = oracle.apply_update("sgd", th, None, res["grad"], float(F32(LR)))
+            n += 1
+            el = time.perf_counter() - c0
+            if el >= args.cpu_seconds or n >= total:
+                break
+        out["cpu_baseline"] = {"value": round(n / el, 3), "unit": "steps/s", "cores": oracle.num_threads(),
+                               "kind": "oracle",
+                               "sample": f"first {n} iterations of the same loop (act {E} games, store, "
+                                         f"minibatch {B} TD gradient + SGD), {el:.1f}s wall"}
+    return out
+
+
+def host_u64(t, i):
+    return t[i].cpu().numpy()
+
 
 def bench_replica_sweep(args):
     """The server-bottleneck study on one GPU (Sec. IV.D.1, Fig. 3's

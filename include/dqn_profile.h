@@ -52,7 +52,8 @@ typedef enum {
     DQN_K_FINALIZE_APPLY = 18, /* finalize with the update applied (dqn_train_steps) */
     DQN_K_CONV12_FWD = 19,  /* both conv layers of the small network */
     DQN_K_CONV12_BWD = 20,  /* conv2 weight + input gradient and conv1 weight gradient, small network */
-    DQN_K_COUNT = 21
+    DQN_K_SNAKE_STEP = 21,  /* one move of every game with its replay write (dqn_actor.h) */
+    DQN_K_COUNT = 22
 } dqn_kernel;
 
 int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs, int32_t stride);

@@ -230,6 +230,15 @@ inline void prof_end(int k, hipStream_t st) {
     }
 }
 
+}  // namespace
+
+namespace dqn {
+void prof_mark_begin(int kid, hipStream_t st) { prof_begin(kid, st); }
+void prof_mark_end(int kid, hipStream_t st) { prof_end(kid, st); }
+}  // namespace dqn
+
+namespace {
+
 // Launch one kernel of the hot path, bracketed by the profiling events of
 // kernel id `kid` when attached.
 #define RUN(kid, expr)                                  \

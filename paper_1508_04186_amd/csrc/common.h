@@ -115,6 +115,11 @@ struct SideFields {
 
 // ---- launchers (host side); every one returns hipGetLastError() ----------
 
+// Measurement hook (dqn_profile.h): the event pair of kernel id `kid` around
+// a launch made outside the C ABI file.
+void prof_mark_begin(int kid, hipStream_t st);
+void prof_mark_end(int kid, hipStream_t st);
+
 // Raise a kernel's dynamic LDS limit to `bytes` if it is below (once per
 // kernel and size; thread-safe).  False if the runtime refuses.
 bool allow_lds(const void* kern, size_t bytes);

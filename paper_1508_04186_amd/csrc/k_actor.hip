@@ -12,13 +12,15 @@
 // head, 192 apple; a state stacks the last four frames, oldest first.
 //
 // Device game state: a ring of body cells (segment i at ring[(hp + i) % 144])
-// and an occupancy grid, so a move touches two cells; the workgroup (one
-// wave) copies them to LDS, every lane runs the same control logic on the
-// same values, and the lanes share the free-cell count of an apple placement
-// (a prefix sum over three cells per lane), the rendering (16-byte vectors)
-// and the state and replay writes.
+// and an occupancy grid, so a move touches two cells; the workgroup (four
+// waves) copies them to LDS, every thread runs the same control logic on the
+// same values, the lanes of each wave compute the free-cell count of an apple
+// placement (a prefix sum over three cells per lane), and the threads share
+// the rendering (16-byte vectors) and the state and replay writes, with the
+// kept frames read before the game logic runs.
 #include "common.h"
 #include "dqn_actor.h"
+#include "dqn_profile.h"
 
 namespace dqn {
 namespace {
@@ -28,7 +30,9 @@ constexpr int SC = SG * SG;                  // cells
 constexpr int SPX = 84 / SG;                 // pixels per cell side
 constexpr int FB = 84 * 84;                  // frame bytes
 constexpr int FV = FB / 16;                  // 16-byte vectors per frame
-constexpr int AW = 64;                       // threads per game
+constexpr int AW = 256;                      // threads per game (four waves)
+constexpr int WL = 64;                       // wavefront
+constexpr int VPT = (FV + AW - 1) / AW;      // frame vectors per thread (2)
 static_assert(SG * SPX == 84 && FB % 16 == 0, "frame geometry");
 
 struct SnakeDev {
@@ -54,19 +58,20 @@ struct Lds {
 };
 
 // k-th free cell in row-major order (k from the high 32 bits of w1 scaled to
-// the free count), or -1 on a full board.  Lane l counts cells 3l .. 3l+2.
+// the free count), or -1 on a full board.  Lane l counts cells 3l .. 3l+2;
+// every wave computes the same result.
 __device__ int place_apple(const Lds& g, uint64_t w1) {
-    const int l = threadIdx.x;
+    const int l = threadIdx.x & (WL - 1);
     int cnt = 0;
     if (l * 3 < SC)
         for (int i = 0; i < 3; ++i) cnt += g.occ[3 * l + i] == 0;
     int incl = cnt;
 #pragma unroll
-    for (int d = 1; d < AW; d <<= 1) {
-        const int v = __shfl_up(incl, d, AW);
+    for (int d = 1; d < WL; d <<= 1) {
+        const int v = __shfl_up(incl, d, WL);
         if (l >= d) incl += v;
     }
-    const int free_cells = __shfl(incl, AW - 1, AW);
+    const int free_cells = __shfl(incl, WL - 1, WL);
     if (free_cells == 0) return -1;
     const uint32_t k = (uint32_t)(((w1 >> 32) * (uint64_t)free_cells) >> 32);
     const int excl = incl - cnt;
@@ -81,11 +86,11 @@ __device__ int place_apple(const Lds& g, uint64_t w1) {
     }
     // exactly one lane found it
     const uint64_t m = __ballot(found >= 0);
-    return __shfl(found, __ffsll((unsigned long long)m) - 1, AW);
+    return __shfl(found, __ffsll((unsigned long long)m) - 1, WL);
 }
 
 __device__ void new_game(Lds& g, uint64_t w0, uint64_t w1) {
-    const int l = threadIdx.x;
+    const int l = threadIdx.x;  // 0 .. AW-1
     for (int c = l; c < SC; c += AW) g.occ[c] = 0;
     __syncthreads();
     const int head = (int)(((w0 & 0xffffffffull) * (uint64_t)SC) >> 32);
@@ -165,10 +170,25 @@ struct ReplayOut {
     int64_t t;               // step index (-1: initial states)
 };
 
-// State write of game e (new frame in every slot, or shifted by one) and the
-// replay copy of the same state.
-__device__ void write_state(const Lds& g, uint8_t* st, bool fresh, const ReplayOut& rp, int e) {
-    const int l = threadIdx.x;
+// The three frames a move keeps (frames 1..3 of the state), read by each
+// thread for its vectors before anything is written.
+struct Kept {
+    uint4 f[3][VPT];
+};
+
+__device__ void read_kept(const uint8_t* st, Kept& k) {
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+        const int q = threadIdx.x + i * AW;
+        if (q < FV)
+#pragma unroll
+            for (int f = 0; f < 3; ++f) k.f[f][i] = ((const uint4*)(st + (f + 1) * FB))[q];
+    }
+}
+
+// State write of game e (the new frame in every slot, or the kept frames
+// shifted by one) and the replay copy of the same state.
+__device__ void write_state(const Lds& g, uint8_t* st, bool fresh, const Kept& kept, const ReplayOut& rp, int e) {
     uint8_t* rec = nullptr;
     uint8_t* mirror = nullptr;
     if (rp.frames) {
@@ -177,15 +197,18 @@ __device__ void write_state(const Lds& g, uint8_t* st, bool fresh, const ReplayO
         rec = rp.frames + (base + slot) * rp.stride;
         if (slot == 0) mirror = rp.frames + (base + rp.cap) * rp.stride;
     }
-    for (int q = l; q < FV; q += AW) {
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+        const int q = threadIdx.x + i * AW;
+        if (q >= FV) continue;
         const uint4 nf = render16(g, q);
         uint4 f[4];
         if (fresh) {
             f[0] = f[1] = f[2] = f[3] = nf;
         } else {
-            f[0] = ((const uint4*)(st + 1 * FB))[q];
-            f[1] = ((const uint4*)(st + 2 * FB))[q];
-            f[2] = ((const uint4*)(st + 3 * FB))[q];
+            f[0] = kept.f[0][i];
+            f[1] = kept.f[1][i];
+            f[2] = kept.f[2][i];
             f[3] = nf;
         }
 #pragma unroll
@@ -205,7 +228,8 @@ __global__ __launch_bounds__(AW) void snake_reset_kernel(SnakeDev* games, const 
     const int e = blockIdx.x;
     new_game(g, draws[2 * e], draws[2 * e + 1]);
     store_game(g, games + e);
-    write_state(g, states + (size_t)e * 4 * FB, true, rp, e);
+    Kept none;
+    write_state(g, states + (size_t)e * 4 * FB, true, none, rp, e);
 }
 
 __global__ __launch_bounds__(AW) void snake_step_kernel(SnakeDev* games, const int32_t* actions,
@@ -214,6 +238,8 @@ __global__ __launch_bounds__(AW) void snake_step_kernel(SnakeDev* games, const i
     __shared__ Lds g;
     const int e = blockIdx.x;
     const int l = threadIdx.x;
+    Kept kept;
+    read_kept(states + (size_t)e * 4 * FB, kept);   // in flight during the game logic
     load_game(g, games + e);
     const uint64_t w0 = draws[2 * e], w1 = draws[2 * e + 1];
     const int a = actions[e];
@@ -250,7 +276,7 @@ __global__ __launch_bounds__(AW) void snake_step_kernel(SnakeDev* games, const i
         }
     }
     store_game(g, games + e);
-    write_state(g, states + (size_t)e * 4 * FB, hit, rp, e);
+    write_state(g, states + (size_t)e * 4 * FB, hit, kept, rp, e);
     if (l == 0) {
         reward[e] = r;
         terminal[e] = hit ? 1 : 0;
@@ -306,9 +332,12 @@ int snake_step(void* games, int32_t n_games, const int32_t* actions, const uint6
                        replay->capacity, t};
     }
     if (!replay_ok(rp)) return DQN_EINVAL;
+    prof_mark_begin(DQN_K_SNAKE_STEP, (hipStream_t)stream);
     hipLaunchKernelGGL(snake_step_kernel, dim3((unsigned)n_games), dim3(AW), 0, (hipStream_t)stream,
                        (SnakeDev*)games, actions, draws, states, reward_out, terminal_out, rp);
-    return hipGetLastError() == hipSuccess ? DQN_OK : DQN_EHIP;
+    if (hipGetLastError() != hipSuccess) return DQN_EHIP;
+    prof_mark_end(DQN_K_SNAKE_STEP, (hipStream_t)stream);
+    return DQN_OK;
 }
 
 double dqn_anneal_epsilon(int64_t n, int64_t n_max, double eps_min, double eps_max) {
