@@ -220,9 +220,10 @@ __global__ __launch_bounds__(HT) void head_fwd_kernel(HeadFwdArgs p) {
 
 // Each output's terms are summed in a fixed association, without atomics.
 // Segments, in slots of eight lanes:
-//  - sums over the B samples, one wave per output (lane L takes samples
-//    j = L, L + 64, ... with every load unconditional and eight samples in
-//    flight; the wave then combines its lanes in a fixed butterfly): the fc2
+//  - sums over the B samples, one wave per output (G = 64 lanes; lane L takes
+//    samples j = L, L + G, ... with every load unconditional and eight
+//    samples in flight; the wave then combines its lanes in a fixed
+//    butterfly): the fc2
 //    weights of hidden unit h for all actions at once (delta_j * h1[j][h]
 //    added to the sum of the action j took), the fc1 bias of h, the fc2 bias
 //    of every action, and the loss;
@@ -269,19 +270,19 @@ __device__ __forceinline__ void apply_fc1w(const FinalizeArgs& a, const PsUpdate
 // Sums over samples of one wave (see above).  kind 0: fc2 weights of hidden
 // unit h for every action; 1: fc1 bias of h; 2: fc2 bias of every action;
 // 3: the loss.
-template <int MODE, int A>
+template <int MODE, int A, int GL>
 __device__ __forceinline__ void sample_sums(const FinalizeArgs& a, const PsUpdate& u, int kind, int h) {
-    const int L = threadIdx.x & 63;
+    const int L = threadIdx.x & (GL - 1);
     float s[A];
 #pragma unroll
     for (int k = 0; k < A; ++k) s[k] = 0.f;
     const bool per_action = kind == 0 || kind == 2;
-    for (int j0 = L; j0 < a.B; j0 += 64 * FIN_U) {
+    for (int j0 = L; j0 < a.B; j0 += GL * FIN_U) {
         int act[FIN_U];
         float d[FIN_U];
 #pragma unroll
         for (int e = 0; e < FIN_U; ++e) {
-            const int j = j0 + 64 * e;
+            const int j = j0 + GL * e;
             const bool v = j < a.B;
             act[e] = -1;
             d[e] = 0.f;
@@ -313,7 +314,9 @@ __device__ __forceinline__ void sample_sums(const FinalizeArgs& a, const PsUpdat
 #pragma unroll
     for (int k = 0; k < A; ++k) {
         if (k < nk) {
-            float t = wave_sum(s[k]);
+            float t = s[k];
+#pragma unroll
+            for (int m = 1; m < GL; m <<= 1) t += __shfl_xor(t, m, 64);
             if (L == 0) {
                 if (kind == 0) emit<MODE>(a, u, a.g_W2 + (int64_t)k * a.H + h, t);
                 else if (kind == 1) emit<MODE>(a, u, a.g_b1 + h, t);
@@ -324,7 +327,81 @@ __device__ __forceinline__ void sample_sums(const FinalizeArgs& a, const PsUpdat
     }
 }
 
-template <int MODE, int A>
+// Actions outside [0, A) count as the nearest valid one, as in the head.
+__device__ __forceinline__ int clamp_action(int a, int A) { return min(max(a, 0), A - 1); }
+
+// The layout for small batches (up to 128 samples): eight lanes per output
+// throughout, in segment order conv weights and biases, fc1 bias, fc2
+// weights (per action and hidden unit, over the samples that took the
+// action), fc2 bias, loss.  Measured faster than the wave-per-output sums at
+// batch 32 (6.6 against 7.1 us under rocprofv3).
+template <int MODE>
+__global__ __launch_bounds__(256) void finalize_small_kernel(FinalizeArgs a, PsUpdate u, int n_fin) {
+    if constexpr (MODE >= 0) {
+        if ((int)blockIdx.x >= n_fin) {
+            apply_fc1w<MODE>(a, u, (int64_t)(blockIdx.x - n_fin) * 256 + threadIdx.x);
+            return;
+        }
+    }
+    int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3;
+    const bool lead = (threadIdx.x & 7) == 0;
+    for (int l = 0; l < a.n_conv; ++l) {
+        if (i < a.wcount[l]) {
+            const float v = sum_strided_x8(a.wpart[l] + i, a.chunks[l], a.wcount[l]);
+            if (lead) emit<MODE>(a, u, a.gw[l] + i, v);
+            return;
+        }
+        i -= a.wcount[l];
+        if (i < a.cout[l]) {
+            const float v = sum_strided_x8(a.bpart[l] + i, a.chunks[l], a.cout[l]);
+            if (lead) emit<MODE>(a, u, a.gb[l] + i, v);
+            return;
+        }
+        i -= a.cout[l];
+    }
+    if (i < a.H) {
+        const float v = sum_strided_x8(a.dz1 + i, a.B, a.H);
+        if (lead) emit<MODE>(a, u, a.g_b1 + i, v);
+        return;
+    }
+    i -= a.H;
+    if (i < (int64_t)a.A * a.H) {
+        const int k = (int)(i / a.H), h = (int)(i - (int64_t)k * a.H);
+        const int q = threadIdx.x & 7;
+        float s0 = 0.f, s1 = 0.f;
+        for (int j = q; j < a.B; j += 16) {
+            const float t0 = clamp_action(a.action[j], a.A) == k ? a.delta[j] * a.h1s[(int64_t)j * a.H + h] : 0.f;
+            const float t1 = (j + 8 < a.B && clamp_action(a.action[j + 8], a.A) == k)
+                                 ? a.delta[j + 8] * a.h1s[(int64_t)(j + 8) * a.H + h] : 0.f;
+            s0 += t0;
+            s1 += t1;
+        }
+        float t = s0 + s1;
+        t += __shfl_xor(t, 1, 64);
+        t += __shfl_xor(t, 2, 64);
+        t += __shfl_xor(t, 4, 64);
+        if (lead) emit<MODE>(a, u, a.g_W2 + i, t);
+        return;
+    }
+    i -= (int64_t)a.A * a.H;
+    if (i < a.A) {
+        const int q = threadIdx.x & 7;
+        float s = 0.f;
+        for (int j = q; j < a.B; j += 8) s += clamp_action(a.action[j], a.A) == (int)i ? a.delta[j] : 0.f;
+        s += __shfl_xor(s, 1, 64);
+        s += __shfl_xor(s, 2, 64);
+        s += __shfl_xor(s, 4, 64);
+        if (lead) emit<MODE>(a, u, a.g_b2 + i, s);
+        return;
+    }
+    i -= a.A;
+    if (i == 0) {
+        const float v = sum_strided_x8(a.lossj, a.B, 1);
+        if (lead) a.loss_out[0] = v;
+    }
+}
+
+template <int MODE, int A, int GL>
 __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a, PsUpdate u, int n_fin) {
     if constexpr (MODE >= 0) {
         if ((int)blockIdx.x >= n_fin) {
@@ -333,16 +410,17 @@ __global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a, PsUpdate 
         }
     }
     int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3;
-    // one wave per output of the sums over samples: waves 0 .. 2H + 1
-    const int64_t n_wave = 2 * (int64_t)a.H + 2;
-    if (i < 8 * n_wave) {
-        const int w = (int)(i >> 3);
-        if (w < a.H) sample_sums<MODE, A>(a, u, 0, w);
-        else if (w < 2 * a.H) sample_sums<MODE, A>(a, u, 1, w - a.H);
-        else sample_sums<MODE, A>(a, u, w == 2 * a.H ? 2 : 3, 0);
+    // one group of GL lanes per output of the sums over samples: groups 0 .. 2H + 1
+    constexpr int SPG = GL / 8;   // slots per group
+    const int64_t n_grp = 2 * (int64_t)a.H + 2;
+    if (i < SPG * n_grp) {
+        const int w = (int)(i / SPG);
+        if (w < a.H) sample_sums<MODE, A, GL>(a, u, 0, w);
+        else if (w < 2 * a.H) sample_sums<MODE, A, GL>(a, u, 1, w - a.H);
+        else sample_sums<MODE, A, GL>(a, u, w == 2 * a.H ? 2 : 3, 0);
         return;
     }
-    i -= 8 * n_wave;
+    i -= SPG * n_grp;
     const bool lead = (threadIdx.x & 7) == 0;
     for (int l = 0; l < a.n_conv; ++l) {
         if (i < a.wcount[l]) {
@@ -386,30 +464,51 @@ hipError_t launch_head_fwd(int H, int A, const HeadFwdArgs& a, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
-template <int A>
+template <int A, int GL>
 hipError_t finalize_launch(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
-    int64_t total = 8 * (2 * (int64_t)a.H + 2);   // slots: one wave per sum over samples
+    int64_t total = (GL / 8) * (2 * (int64_t)a.H + 2);   // slots: one group per sum over samples
     for (int l = 0; l < a.n_conv; ++l) total += a.wcount[l] + a.cout[l];
     const int n_fin = (int)((total * 8 + 255) / 256);
     if (!upd) {
-        hipLaunchKernelGGL((finalize_kernel<-1, A>), dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{},
+        hipLaunchKernelGGL((finalize_kernel<-1, A, GL>), dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{},
                            n_fin);
         return hipGetLastError();
     }
     if (a.fc1w_off % 4 != 0 || a.fc1w_count % 4 != 0 || !a.grad_base) return hipErrorInvalidValue;
     const dim3 grid((unsigned)(n_fin + (a.fc1w_count / 4 + 255) / 256));
     switch (upd->rule) {
-        case 0: hipLaunchKernelGGL((finalize_kernel<0, A>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
-        case 1: hipLaunchKernelGGL((finalize_kernel<1, A>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
-        case 2: hipLaunchKernelGGL((finalize_kernel<2, A>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 0: hipLaunchKernelGGL((finalize_kernel<0, A, GL>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 1: hipLaunchKernelGGL((finalize_kernel<1, A, GL>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 2: hipLaunchKernelGGL((finalize_kernel<2, A, GL>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t finalize_small_launch(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
+    int64_t total = a.H + (int64_t)a.A * a.H + a.A + 1;
+    for (int l = 0; l < a.n_conv; ++l) total += a.wcount[l] + a.cout[l];
+    const int n_fin = (int)((total * 8 + 255) / 256);
+    if (!upd) {
+        hipLaunchKernelGGL(finalize_small_kernel<-1>, dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{}, n_fin);
+        return hipGetLastError();
+    }
+    if (a.fc1w_off % 4 != 0 || a.fc1w_count % 4 != 0 || !a.grad_base) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)(n_fin + (a.fc1w_count / 4 + 255) / 256));
+    switch (upd->rule) {
+        case 0: hipLaunchKernelGGL(finalize_small_kernel<0>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 1: hipLaunchKernelGGL(finalize_small_kernel<1>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 2: hipLaunchKernelGGL(finalize_small_kernel<2>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_finalize(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
-    if (a.A == 6) return finalize_launch<6>(a, upd, st);
-    if (a.A == 18) return finalize_launch<18>(a, upd, st);
+    // up to 128 samples the eight-lane layout; above, a wave per sum over samples
+    if (a.B <= 128) return finalize_small_launch(a, upd, st);
+    if (a.A == 6) return finalize_launch<6, 64>(a, upd, st);
+    if (a.A == 18) return finalize_launch<18, 64>(a, upd, st);
     return hipErrorInvalidValue;
 }
 
