@@ -21,6 +21,12 @@ Configurations (--config; the default line is config 1):
       the games, and one TD gradient + SGD step follows on a minibatch of 32
       drawn from it (a step = one such iteration).
 
+  observe  preprocessing phi on the device: 1,024 games each hand over a
+      raw 176 x 176 RGB screen per step; phi (gray, crop, 2 x 2 mean) goes
+      into each game's 4-frame state and the state into a replay keeping
+      64 states per game, 10% of the games restarting per step (a step = one
+      observe launch over all games).
+
 --precision bf16 runs configs 3, 4a and 4b with the bf16-input variant;
 --config 2 --sweep runs the server-bottleneck study over replicas and batch.
 
@@ -293,7 +299,7 @@ def time_region(stream_sync, fn):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--config", default="1", choices=["0", "1", "2", "3", "4a", "4b", "actor"])
+    ap.add_argument("--config", default="1", choices=["0", "1", "2", "3", "4a", "4b", "actor", "observe"])
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default per config)")
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--breakdown-steps", type=int, default=50)
@@ -329,7 +335,8 @@ def main():
         print("--sweep applies to config 2", file=sys.stderr)
         sys.exit(2)
     out = {"0": bench_single, "1": bench_sequential, "2": bench_replica_sweep if args.sweep else bench_replicas,
-           "3": bench_large, "4a": bench_forward, "4b": bench_large, "actor": bench_actor}[args.config](args)
+           "3": bench_large, "4a": bench_forward, "4b": bench_large, "actor": bench_actor,
+           "observe": bench_observe}[args.config](args)
     if not args.no_denominators:
         out["denominators"] = measure_denominators()
     if args.calib_copy_mib > 0:
@@ -674,6 +681,88 @@ def bench_actor(args):
                                "kind": "oracle",
                                "sample": f"first {n} iterations of the same loop (act {E} games, store, "
                                          f"minibatch {B} TD gradient + SGD), {el:.1f}s wall"}
+    return out
+
+
+def bench_observe(args):
+    """Preprocessing phi on the device (Sec. III.A, Fig. 2): every step, E
+    games hand over one raw RGB screen each (resident in device memory, a
+    pool of 8 screen sets cycled so that no step finds its screens in a
+    cache); dqn_observe turns them into 84 x 84 gray frames, shifts them
+    into the games' 4-frame states (restarting the games flagged terminal)
+    and stores the states with the step's action, reward and flag in a
+    replay that keeps the last N states per game."""
+    import torch
+    import dqn_inputs as di
+    import oracle
+    import paper_1508_04186_amd as dq
+    dev = torch.device("cuda:0")
+    E, N, H, Wd, TOP, LEFT, F, POOL, SEED = 1024, 64, 176, 176, 4, 4, 2, 8, 1006
+    K = args.steps or 2000
+    W = args.warmup if args.warmup is not None else 50
+    total = W + K
+    log(f"observe: generating {POOL} sets of {E} screens {H}x{Wd}")
+    screens_host = [di.rgb_screens(E, SEED * 100 + i, H, Wd) for i in range(POOL)]
+    screens = [torch.from_numpy(x).to(dev) for x in screens_host]
+    rng = np.random.default_rng(SEED)
+    acts_h = rng.integers(0, 18, size=(total, E)).astype(np.int32)
+    rew_h = rng.integers(-1, 2, size=(total, E)).astype(np.int8)
+    term_h = (rng.random((total, E)) < 0.1).astype(np.uint8)
+    acts, rew, term = (torch.from_numpy(x).to(dev) for x in (acts_h, rew_h, term_h))
+    states = torch.empty((E, 4, 84, 84), dtype=torch.uint8, device=dev)
+    rp = dq.ActorReplay(E, N, dev)
+
+    def run(lo, hi):
+        for t in range(lo, hi):
+            dq.dqn_observe(screens[(t + 1) % POOL], TOP, LEFT, F, states, acts[t], rew[t], term[t], rp, t)
+
+    dq.dqn_observe(screens[0], TOP, LEFT, F, states, replay=rp, t=-1)
+    run(0, W)
+    torch.cuda.synchronize()
+    hip = HipEvents()
+    prof = Profiler(hip)
+    kid, ev = prof.attach("observe", K + 4, 1)
+    ms = time_region(torch.cuda.synchronize, lambda: run(W, W + K))
+    raw_us, used = prof.collect(kid, ev)
+    dom_us = raw_us - prof.overhead()
+    # algorithmic bytes per launch, averaged over the timed steps: the 168 x 168 x 3 window of
+    # every screen, the three kept frames of the games that go on, the 4-frame state and its
+    # replay record (twice when the record lands in slot 0, which slot N repeats), the side
+    # fields (read 4 + 1 + 1 bytes, write 3)
+    FB = 84 * 84
+    win = (84 * F) ** 2 * 3
+    steps = np.arange(W, W + K)
+    kept = 3 * FB * (1 - term_h[W:W + K]).sum(axis=1)
+    mirror = ((steps + 1) % N == 0) * E * 4 * FB
+    per = E * (win + 2 * 4 * FB + 9) + kept + mirror
+    work = {"observe": (0, int(round(per.mean())))}
+    out = base_record(K, W, ms)
+    out["metric"] = "observe steps/sec (raw RGB screens -> phi -> 4-frame states + replay); HBM GB/s"
+    out["dtype"] = "u8"
+    out["config"] = {
+        "workload": f"phi of {E} raw {H}x{Wd} RGB screens per step (BT.601 gray, {84 * F}x{84 * F} crop at "
+                    f"({TOP},{LEFT}), {F}x{F} mean) into {E} 4-frame states and a replay of {N} states per game; "
+                    f"10% of the games restart per step",
+        "games": E, "screen": [H, Wd, 3], "factor": F, "replay_states": E * N}
+    out["screens_per_s"] = round(out["value"] * E, 1)
+    out["roofline"] = roofline(work, "observe", dom_us, used, 1, raw_us, "observe")
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline: oracle observe loop for about {args.cpu_seconds:.0f}s")
+        orp = oracle.SegmentedReplay(E, N)
+        ost = oracle.stack_frames(np.zeros((E, 4, 84, 84), np.uint8),
+                                  oracle.preprocess(screens_host[0], TOP, LEFT, F), None, -1)
+        orp.append(-1, ost)
+        n, c0 = 0, time.perf_counter()
+        while True:
+            x = oracle.preprocess(screens_host[(n + 1) % POOL], TOP, LEFT, F)
+            ost = oracle.stack_frames(ost, x, term_h[n], n)
+            orp.append(n, ost, acts_h[n], rew_h[n].astype(np.float32), term_h[n])
+            n += 1
+            el = time.perf_counter() - c0
+            if el >= args.cpu_seconds or n >= total:
+                break
+        out["cpu_baseline"] = {"value": round(n / el, 3), "unit": "steps/s", "cores": 1, "kind": "oracle",
+                               "sample": f"first {n} steps of the same loop ({E} screens each), {el:.1f}s wall"}
     return out
 
 

@@ -169,6 +169,19 @@ def actor_minibatch(batch: int, seed: int, step: int, n_games: int, capacity: in
     return (e * (capacity + 1) + t % capacity).astype(np.int64)
 
 
+def rgb_screens(n: int, seed: int, h: int = 176, w: int = 176) -> np.ndarray:
+    """uint8 [n][h][w][3] raw color screens: a dark noisy background with 1-4
+    solid colored rectangles each (stand-ins for a game's raw frames)."""
+    rng = np.random.default_rng([seed, 0x26B])
+    out = rng.integers(0, 24, size=(n, h, w, 3), dtype=np.uint8)
+    for i in range(n):
+        for _ in range(int(rng.integers(1, 5))):
+            rh, rw = int(rng.integers(4, h // 3)), int(rng.integers(4, w // 3))
+            y0, x0 = int(rng.integers(0, h - rh)), int(rng.integers(0, w - rw))
+            out[i, y0:y0 + rh, x0:x0 + rw] = rng.integers(64, 256, size=3, dtype=np.uint8)
+    return out
+
+
 def egreedy_draws(batch: int, seed: int) -> np.ndarray:
     """uint64 [batch] exploration draws: high 32 bits decide exploration,
     low 32 bits pick the random action."""

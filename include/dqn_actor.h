@@ -37,6 +37,23 @@
  * viewed as a dqn_replay of size n_games*(N+1) feed replay_gather and
  * dqn_td_gradient_replay with those indices.
  *
+ * Games whose screens come from outside the library (an emulator stepped on
+ * the host, its raw screens copied to the device) use dqn_preprocess and
+ * dqn_observe instead of the Snake entry points.  Sec. III.A and Fig. 2 say
+ * that phi gray-scales the RGB screen, down-samples it to a fixed size and
+ * crops it to the network's 84 x 84 input, and stacks the last four frames;
+ * the text gives no formulas.  Readings:
+ *  - gray = (299 R + 587 G + 114 B + 500) / 1000 per pixel in integers (the
+ *    ITU-R BT.601 luma weights, rounded half up);
+ *  - down-sampling by an integer factor F (1..8) averages F x F blocks,
+ *    (sum + F*F/2) / (F*F) in integers, over the 84F x 84F window of the
+ *    screen whose top-left pixel is (top, left): the crop.  Gray-scaling a
+ *    block mean and averaging gray pixels agree in exact arithmetic, so the
+ *    order of the two steps only decides where the roundings fall; gray is
+ *    rounded per pixel, then the block mean;
+ *  - the stack and replay rules are those of the Snake games above: a
+ *    terminal flag means the screen passed is the first one of a new game.
+ *
  * Conventions as in dqn.h: device pointers, caller-owned memory, work
  * enqueued on `stream`, DQN_OK or a negative dqn_status, checks on the host
  * before anything is enqueued.
@@ -98,6 +115,29 @@ int dqn_act(const dqn_net* net, const float* theta, void* games, int32_t n_games
             float epsilon, const uint64_t* eps_draws, const uint64_t* env_draws, int32_t* actions_out,
             float* reward_out, uint8_t* terminal_out, const dqn_replay_out* replay, int64_t t, void* ws,
             size_t ws_bytes, void* stream);
+
+/* phi of n raw screens: rgb uint8 [n][h][w][3] (4-byte aligned), window
+ * top-left (top, left), factor 1..8 with top + 84*factor <= h and left +
+ * 84*factor <= w.  Screen i's 84 x 84 result goes to out + i*out_stride (out
+ * 16-byte aligned, out_stride a multiple of 16, >= 84*84; so out may be the
+ * newest frame of a [n][4][84][84] state array with out_stride 4*84*84).
+ * out must not overlap rgb.  n = 0 does nothing (rgb and out may then be
+ * NULL). */
+int dqn_preprocess(const uint8_t* rgb, int64_t n, int32_t h, int32_t w, int32_t top, int32_t left,
+                   int32_t factor, uint8_t* out, int64_t out_stride, void* stream);
+
+/* Observe step of Alg. 1 for n_games games with raw screens rgb (as in
+ * dqn_preprocess, one screen per game).  t = -1 starts the games: each state
+ * (uint8 [n_games][4][84][84], 16-byte aligned) becomes four copies of phi of
+ * its screen and is stored as state 0 (replay nullable; actions, rewards,
+ * terminal unused and nullable).  t >= 0 stores experience t: terminal uint8
+ * [n_games] (required) restarts a game's state from its screen, otherwise the
+ * state drops its oldest frame and appends phi of the screen; with a replay,
+ * actions int32 [n_games] and rewards int8 [n_games] (required) go into the
+ * side fields of state t, and state t+1 into its slot, as snake_step does. */
+int dqn_observe(const uint8_t* rgb, int32_t n_games, int32_t h, int32_t w, int32_t top, int32_t left,
+                int32_t factor, const int32_t* actions, const int8_t* rewards, const uint8_t* terminal,
+                uint8_t* states, const dqn_replay_out* replay, int64_t t, void* stream);
 
 #ifdef __cplusplus
 }

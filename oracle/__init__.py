@@ -81,7 +81,9 @@ def _lib():
         lib.oracle_anneal_epsilon.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_double,
                                               ctypes.c_double]
         lib.oracle_anneal_epsilon.restype = ctypes.c_double
-        for f in ("oracle_snake_reset", "oracle_snake_step", "oracle_replay_append"):
+        lib.oracle_preprocess.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.c_int32, ctypes.c_int32, _P]
+        for f in ("oracle_snake_reset", "oracle_snake_step", "oracle_replay_append", "oracle_preprocess"):
             getattr(lib, f).restype = ctypes.c_int
         for f in ("oracle_replay_gather", "oracle_forward_q", "oracle_relu_margins", "oracle_bf16_round",
                   "oracle_select_actions",
@@ -349,3 +351,28 @@ class SegmentedReplay:
 def anneal_epsilon(n, n_max, eps_min, eps_max) -> float:
     """Alg. 1: q = max((N_max - n)/N_max, 0); epsilon = (1 - q) eps_min + q eps_max."""
     return float(_lib().oracle_anneal_epsilon(int(n), int(n_max), float(eps_min), float(eps_max)))
+
+
+def preprocess(rgb, top, left, factor) -> np.ndarray:
+    """phi of uint8 RGB frames [n][h][w][3] -> uint8 [n][84][84] (oracle.c states the reading)."""
+    x = np.ascontiguousarray(rgb, dtype=np.uint8)
+    n, h, w, _ = x.shape
+    out = np.empty((n, 84, 84), np.uint8)
+    _check(_lib().oracle_preprocess(x.ctypes.data, n, h, w, top, left, factor, out.ctypes.data),
+           "oracle_preprocess")
+    return out
+
+
+def stack_frames(states, frames, terminal, t) -> np.ndarray:
+    """Alg. 1's next state over the last four preprocessed frames: a state
+    drops its oldest frame and appends the new one, oldest first; a game that
+    starts (t = -1) or restarts (its terminal flag) holds four copies of its
+    first frame.  states uint8 [n][4][84][84], frames uint8 [n][84][84]."""
+    out = np.empty_like(states)
+    for e in range(states.shape[0]):
+        if t < 0 or terminal[e]:
+            out[e] = frames[e][None]
+        else:
+            out[e, :3] = states[e, 1:]
+            out[e, 3] = frames[e]
+    return out

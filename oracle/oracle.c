@@ -36,6 +36,8 @@
  *                          stacked 84x84 frames, and the experiences stored
  *                          in a replay memory that keeps the last N of them
  *                          (Sec. III.C), pooled over game instances.
+ *   oracle_preprocess      phi (Sec. III.A, Fig. 2): raw RGB screens
+ *                          gray-scaled, cropped and down-sampled to 84x84.
  *
  * The bf16-input variant (net->bf16_inputs = 1) computes the same functions
  * with every operand of the layer contractions -- the conv and fc1 weights,
@@ -789,4 +791,31 @@ double oracle_anneal_epsilon(int64_t n, int64_t n_max, double eps_min, double ep
     double q = n_max > 0 ? (double)(n_max - n) / (double)n_max : 0.0;
     if (q < 0.0) q = 0.0;
     return (1.0 - q) * eps_min + q * eps_max;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Preprocessing phi (Sec. III.A): raw RGB frames are gray-scaled and
+ * down-sampled to 84 x 84.  The text names the steps only; the reading:
+ * gray = (299 R + 587 G + 114 B + 500) / 1000 in integers (ITU-R BT.601
+ * weights, rounded half up), then the 84f x 84f window at (top, left) is
+ * averaged over f x f blocks, (sum + f*f/2) / (f*f), rounded half up.
+ * rgb: uint8 [n][h][w][3]; out: uint8 [n][84][84]. */
+int oracle_preprocess(const uint8_t* rgb, int64_t n, int32_t h, int32_t w, int32_t top, int32_t left,
+                      int32_t f, uint8_t* out) {
+    if (!rgb || !out || n < 0 || f < 1 || top < 0 || left < 0 || top + 84 * f > h || left + 84 * f > w)
+        return ORACLE_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        const uint8_t* fr = rgb + i * (int64_t)h * w * 3;
+        for (int y = 0; y < 84; ++y)
+            for (int x = 0; x < 84; ++x) {
+                int64_t sum = 0;
+                for (int dy = 0; dy < f; ++dy)
+                    for (int dx = 0; dx < f; ++dx) {
+                        const uint8_t* px = fr + ((int64_t)(top + y * f + dy) * w + (left + x * f + dx)) * 3;
+                        sum += (299 * px[0] + 587 * px[1] + 114 * px[2] + 500) / 1000;
+                    }
+                out[(i * 84 + y) * 84 + x] = (uint8_t)((sum + (f * f) / 2) / (f * f));
+            }
+    }
+    return ORACLE_OK;
 }

@@ -120,6 +120,23 @@ struct SideFields {
 void prof_mark_begin(int kid, hipStream_t st);
 void prof_mark_end(int kid, hipStream_t st);
 
+// Replay destination of the actor-side kernels (dqn_replay_out in
+// dqn_actor.h): game e keeps states in records e*(cap+1) .. e*(cap+1)+cap,
+// state t in slot t mod cap, slot cap repeating slot 0.  frames == NULL: no
+// replay write.  t: index of the experience being stored (-1: initial
+// states).
+struct ReplayOut {
+    uint8_t* frames;
+    int64_t stride;          // bytes between records
+    uint8_t* action;
+    int8_t* reward;
+    uint8_t* terminal;
+    int64_t cap;
+    int64_t t;
+};
+// Pointer, stride and capacity checks of a replay destination.
+bool replay_ok(const ReplayOut& rp);
+
 // Raise a kernel's dynamic LDS limit to `bytes` if it is below (once per
 // kernel and size; thread-safe).  False if the runtime refuses.
 bool allow_lds(const void* kern, size_t bytes);

@@ -160,16 +160,6 @@ __device__ void store_game(const Lds& g, SnakeDev* dst) {
     }
 }
 
-struct ReplayOut {
-    uint8_t* frames;         // NULL: no replay write
-    int64_t stride;          // bytes between records
-    uint8_t* action;
-    int8_t* reward;
-    uint8_t* terminal;
-    int64_t cap;             // N states kept per game (N + 1 records per game)
-    int64_t t;               // step index (-1: initial states)
-};
-
 // The three frames a move keeps (frames 1..3 of the state), read by each
 // thread for its vectors before anything is written.
 struct Kept {

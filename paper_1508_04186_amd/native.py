@@ -150,6 +150,13 @@ def lib():
         L.dqn_act.argtypes = [ctypes.POINTER(_CNet), _P, _P, ctypes.c_int32, _P, ctypes.c_float, _P, _P, _P,
                               _P, _P, ctypes.POINTER(_CReplayOut), ctypes.c_int64, _P, ctypes.c_size_t, _P]
         L.dqn_act.restype = ctypes.c_int
+        L.dqn_preprocess.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                     ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P]
+        L.dqn_preprocess.restype = ctypes.c_int
+        L.dqn_observe.argtypes = [_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P, ctypes.POINTER(_CReplayOut),
+                                  ctypes.c_int64, _P]
+        L.dqn_observe.restype = ctypes.c_int
         L.dqn_profile_mfma_peak.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, _P]
         L.dqn_profile_mfma_peak.restype = ctypes.c_int64
         L.dqn_profile_stream_copy.argtypes = [_P, _P, ctypes.c_int64, ctypes.c_int32, _P]
@@ -462,7 +469,7 @@ def dqn_train_replicas(net, theta_ring, opt_state, rule, lr, decay, eps, gamma, 
 KERNEL_NAMES = ["gather", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head", "fc1_wgrad",
                 "fc1_dgrad", "conv1_wgrad", "conv2_wgrad", "conv3_wgrad", "conv2_dgrad",
                 "conv3_dgrad", "finalize", "apply", "fc1_bwd", "conv2_bwd", "conv3_bwd",
-                "finalize_apply", "conv12_fwd", "conv12_bwd", "snake_step"]
+                "finalize_apply", "conv12_fwd", "conv12_bwd", "snake_step", "observe"]
 _ATTACHED = {}
 
 
@@ -593,3 +600,40 @@ def dqn_act(net, theta, games, states, epsilon, eps_draws, env_draws, actions_ou
                          _ptr(reward_out, torch.float32, "reward_out"),
                          _ptr(terminal_out, torch.uint8, "terminal_out"), ctypes.byref(rp) if rp else None,
                          int(t), _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)), "dqn_act")
+
+
+def dqn_preprocess(rgb, top: int, left: int, factor: int, out=None, stream=None):
+    """phi of raw screens rgb uint8 [n][h][w][3] (include/dqn_actor.h).  out:
+    uint8 [n][84][84], or any uint8 tensor whose dim-0 slices hold one 84 x 84
+    frame each at a 16-byte multiple stride (e.g. states[:, 3] of a
+    [n][4][84][84] state array).  Returns out."""
+    import torch
+    n, h, w, c = rgb.shape
+    if c != 3:
+        raise ValueError("rgb must be [n][h][w][3]")
+    if out is None:
+        out = torch.empty((n, 84, 84), dtype=torch.uint8, device=rgb.device)
+    if out.dtype != torch.uint8 or not out.is_cuda:
+        raise TypeError("out must be a uint8 device tensor")
+    if out.shape[0] != n or (n > 0 and (out[0].numel() != 84 * 84 or not out[0].is_contiguous())):
+        raise ValueError("out must hold n contiguous 84 x 84 frames")
+    stride = out.stride(0) if n > 1 else 84 * 84
+    _check(lib().dqn_preprocess(_ptr(rgb, torch.uint8, "rgb"), n, h, w, top, left, factor, out.data_ptr(),
+                                stride, _stream(stream)), "dqn_preprocess")
+    return out
+
+
+def dqn_observe(rgb, top: int, left: int, factor: int, states, actions=None, rewards=None, terminal=None,
+                replay: ActorReplay | None = None, t: int = -1, stream=None) -> None:
+    """Observe step of Alg. 1 for games with raw screens (include/dqn_actor.h):
+    phi of each game's screen into its state stack and, with a replay, the
+    experience into it.  t = -1 starts the games."""
+    import torch
+    E, h, w, _ = rgb.shape
+    if tuple(states.shape) != (E, 4, 84, 84):
+        raise ValueError("states must be [n_games][4][84][84]")
+    rp = replay._c() if replay is not None else None
+    _check(lib().dqn_observe(_ptr(rgb, torch.uint8, "rgb"), E, h, w, top, left, factor,
+                             _ptr(actions, torch.int32, "actions"), _ptr(rewards, torch.int8, "rewards"),
+                             _ptr(terminal, torch.uint8, "terminal"), _ptr(states, torch.uint8, "states"),
+                             ctypes.byref(rp) if rp else None, int(t), _stream(stream)), "dqn_observe")

@@ -240,6 +240,61 @@ def test_actor_argument_errors():
     assert dq.dqn_anneal_epsilon(250, 100, 0.1, 1.0) == 0.1
 
 
+@fake_ptr_test
+def test_preprocess_argument_errors():
+    L = dq.lib()
+    OUT = FAKE + 2**32
+    ok = dict(rgb=FAKE, n=4, h=176, w=176, top=4, left=4, f=2, out=OUT, stride=7056)
+
+    def pre(**kw):
+        a = {**ok, **kw}
+        return L.dqn_preprocess(a["rgb"], a["n"], a["h"], a["w"], a["top"], a["left"], a["f"], a["out"],
+                                a["stride"], None)
+    assert pre(n=0) == dq.DQN_OK                                    # nothing to do
+    assert pre(n=0, rgb=None, out=None) == dq.DQN_OK
+    assert pre(rgb=None) == dq.DQN_EINVAL
+    assert pre(out=None) == dq.DQN_EINVAL
+    assert pre(n=-1) == dq.DQN_EINVAL
+    for f in (0, 9):
+        assert pre(f=f, h=2000, w=2000) == dq.DQN_EINVAL           # factor outside 1..8
+    assert pre(top=9) == dq.DQN_EINVAL                              # window past the bottom edge
+    assert pre(left=9) == dq.DQN_EINVAL                             # past the right edge
+    assert pre(top=-1) == dq.DQN_EINVAL
+    assert pre(rgb=FAKE + 2) == dq.DQN_EINVAL                      # rgb not 4-byte aligned
+    assert pre(out=OUT + 4) == dq.DQN_EINVAL                       # out not 16-byte aligned
+    assert pre(stride=7040) == dq.DQN_EINVAL                       # stride < 84*84
+    assert pre(stride=7064) == dq.DQN_EINVAL                       # stride not a multiple of 16
+    assert pre(out=FAKE + 4096) == dq.DQN_EINVAL                   # out overlaps rgb
+
+
+@fake_ptr_test
+def test_observe_argument_errors():
+    L = dq.lib()
+    ST = FAKE + 2**32
+    rp = native._CReplayOut()
+    rp.frames, rp.action, rp.reward, rp.terminal = FAKE + 2**33, FAKE + 2**34, FAKE + 2**34 + 4096, FAKE + 2**35
+    rp.record_stride, rp.capacity = 28224, 16
+
+    def obs(n=4, states=ST, actions=FAKE + 2**36, rewards=FAKE + 2**37, terminal=FAKE + 2**38, replay=rp, t=3,
+            top=4, f=2, rgb=FAKE):
+        return L.dqn_observe(rgb, n, 176, 176, top, 4, f, actions, rewards, terminal, states,
+                             ctypes.byref(replay) if replay is not None else None, t, None)
+    assert obs(n=0) == dq.DQN_EINVAL
+    assert obs(t=-2) == dq.DQN_EINVAL
+    assert obs(states=None) == dq.DQN_EINVAL
+    assert obs(states=ST + 8) == dq.DQN_EINVAL                      # states not 16-byte aligned
+    assert obs(terminal=None) == dq.DQN_EINVAL                      # t >= 0 needs the terminal flags
+    assert obs(actions=None) == dq.DQN_EINVAL                       # ... and, with a replay, actions
+    assert obs(rewards=None) == dq.DQN_EINVAL                       # ... and rewards
+    assert obs(top=9) == dq.DQN_EINVAL
+    assert obs(f=9) == dq.DQN_EINVAL
+    assert obs(states=FAKE + 1024) == dq.DQN_EINVAL                 # states overlap the screens
+    rp.capacity = 1
+    assert obs() == dq.DQN_EINVAL                                   # replay capacity < 2
+    rp.capacity, rp.record_stride = 16, 28200
+    assert obs() == dq.DQN_EINVAL                                   # record stride too small
+
+
 def test_status_strings():
     for s in (dq.DQN_OK, dq.DQN_EINVAL, dq.DQN_EWORKSPACE, dq.DQN_EHIP, dq.DQN_EUNSUPPORTED):
         assert dq.dqn_status_string(s) not in ("", "unknown status")

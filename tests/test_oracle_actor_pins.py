@@ -167,3 +167,36 @@ def test_replay_keeps_the_last_n_states_per_game():
 @pytest.mark.parametrize("n,expect", [(0, 1.0), (500, 0.55), (1000, 0.1), (5000, 0.1)])
 def test_annealed_epsilon(n, expect):
     assert oracle.anneal_epsilon(n, 1000, 0.1, 1.0) == pytest.approx(expect, abs=1e-15)
+
+
+# ---------------------------------------------------------------------------
+# Preprocessing phi (Sec. III.A): gray-scale, crop, f x f box down-sampling.
+
+def test_preprocess_constant_colors_closed_form():
+    for (r, g, b) in [(0, 0, 0), (255, 255, 255), (255, 0, 0), (0, 255, 0), (0, 0, 255), (12, 200, 77)]:
+        rgb = np.zeros((1, 170, 172, 3), np.uint8)
+        rgb[...] = (r, g, b)
+        gray = (299 * r + 587 * g + 114 * b + 500) // 1000
+        out = oracle.preprocess(rgb, 1, 2, 2)
+        assert np.all(out == gray)
+    # the BT.601 weights on the primaries
+    assert [(299 * 255 + 500) // 1000, (587 * 255 + 500) // 1000, (114 * 255 + 500) // 1000] == [76, 150, 29]
+
+
+def test_preprocess_one_bright_pixel_lands_in_its_block():
+    rgb = np.zeros((1, 260, 260, 3), np.uint8)
+    top, left, f = 5, 7, 3
+    yy, xx = 40, 61                                   # output block (40, 61), offset (1, 2) inside it
+    rgb[0, top + f * yy + 1, left + f * xx + 2] = (255, 255, 255)
+    out = oracle.preprocess(rgb, top, left, f)
+    expect = np.zeros((84, 84), np.uint8)
+    expect[yy, xx] = (255 + 4) // 9                   # (sum + f*f/2) / (f*f)
+    assert np.array_equal(out[0], expect)
+
+
+def test_preprocess_is_the_mean_of_blocks_of_gray():
+    rgb = np.random.default_rng(3).integers(0, 256, size=(2, 180, 175, 3), dtype=np.uint8)
+    c = rgb.astype(np.int64)
+    g = (299 * c[..., 0] + 587 * c[..., 1] + 114 * c[..., 2] + 500) // 1000
+    win = g[:, 6:6 + 168, 3:3 + 168].reshape(2, 84, 2, 84, 2).sum(axis=(2, 4))
+    assert np.array_equal(oracle.preprocess(rgb, 6, 3, 2), ((win + 2) // 4).astype(np.uint8))
