@@ -116,7 +116,7 @@ int dqn_act(const dqn_net* net, const float* theta, void* games, int32_t n_games
             float* reward_out, uint8_t* terminal_out, const dqn_replay_out* replay, int64_t t, void* ws,
             size_t ws_bytes, void* stream);
 
-/* phi of n raw screens: rgb uint8 [n][h][w][3] (4-byte aligned), window
+/* phi of n raw screens: rgb uint8 [n][h][w][3] (16-byte aligned), window
  * top-left (top, left), factor 1..8 with top + 84*factor <= h and left +
  * 84*factor <= w.  Screen i's 84 x 84 result goes to out + i*out_stride (out
  * 16-byte aligned, out_stride a multiple of 16, >= 84*84; so out may be the

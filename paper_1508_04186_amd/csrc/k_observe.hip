@@ -10,12 +10,13 @@
 // so results are exact.
 //
 // A workgroup owns a band of R output rows of one screen.  It stages the R*F
-// source rows of the window in LDS with 4-byte loads over the aligned cover
+// source rows of the window in LDS with 16-byte loads over the aligned cover
 // of each row (a row of the window starts at any byte), reduces them from
 // LDS, assembles the band's bytes in LDS, and writes 16-byte vectors: the
 // band of phi alone, or, for the observe step, the band of all four frames
-// of the state (three kept frames shifted down by one, read before anything
-// is written) and the same band of the replay record.
+// of the state (three kept frames shifted down by one, staged in LDS with
+// the screen rows so that every read precedes every write) and the same
+// band of the replay record, one vector per thread.
 #include <cstdint>
 
 #include "common.h"
@@ -49,56 +50,72 @@ struct ObsParams {
 // Band height: a multiple of 4 so that a band of a frame is whole 16-byte
 // vectors (R * 84 bytes), and small enough that the staged rows fit in LDS.
 constexpr int band_rows(int f) { return f <= 3 ? 12 : 4; }
-// 4-byte words of the aligned cover of a window row (84F * 3 bytes from any
-// byte offset).
-constexpr int row_words(int f) { return 63 * f + 1; }
+// 16-byte vectors of the aligned cover of a window row (84F * 3 bytes from
+// any byte offset).
+constexpr int row_vecs(int f) { return (252 * f + 30) / 16; }
+constexpr int XCDS = 8;  // workgroups go to the chip's dies round-robin
 
 __device__ __forceinline__ uint32_t gray(uint32_t r, uint32_t g, uint32_t b) {
     return (299u * r + 587u * g + 114u * b + 500u) / 1000u;
 }
 
 template <int F, bool OBSERVE>
-__global__ __launch_bounds__(OBW) void observe_kernel(ObsParams p) {
+__global__ __launch_bounds__(OBW) void observe_kernel(ObsParams p, int64_t n) {
     constexpr int R = band_rows(F);
-    constexpr int RW = row_words(F);
+    constexpr int RV = row_vecs(F);
     constexpr int ROWS = R * F;
     constexpr int BV = R * 84 / 16;            // 16-byte vectors per frame band
-    static_assert(BV <= OBW, "one vector of each frame per thread");
-    extern __shared__ __align__(16) uint32_t s_rgb[];          // [ROWS][RW]
-    uint8_t* s_new = (uint8_t*)(s_rgb + ROWS * RW);            // [R * 84], 16-byte aligned
+    constexpr int LOADS = (ROWS * RV + OBW - 1) / OBW;
+    static_assert(4 * BV <= OBW, "one vector of the state band per thread");
+    extern __shared__ __align__(16) uint4 s_rgb[];             // [ROWS][RV]
+    uint8_t* s_new = (uint8_t*)(s_rgb + ROWS * RV);            // [R * 84]
+    uint4* s_kept = s_rgb + ROWS * RV + BV;                    // [3][BV]
 
+    // All bands of a game run on one die, so the 16-byte pieces of a cache
+    // line that two bands write meet in the same L2.
     const int t = threadIdx.x;
-    const int64_t e = blockIdx.x / p.bands;
-    const int band = blockIdx.x - (int)e * p.bands;
+    const int64_t slot = blockIdx.x / XCDS;
+    const int64_t e = (slot / p.bands) * XCDS + blockIdx.x % XCDS;
+    if (e >= n) return;  // whole workgroup
+    const int band = (int)(slot % p.bands);
     const int y0 = band * R;
     const int64_t row0 = e * p.frame_bytes + (int64_t)(p.top + y0 * F) * p.w3 + (int64_t)p.left * 3;
 
-    // observe: the kept frames 1..3 of this band, in flight during the rest
     bool fresh = true;
-    uint4 kept[3];
     uint8_t* st = nullptr;
+    uint4 kept = {0, 0, 0, 0};
     if constexpr (OBSERVE) {
         fresh = p.rp.t < 0 || p.term[e] != 0;
         st = p.states + e * 4 * OFB + y0 * 84;
-        if (!fresh && t < BV)
-#pragma unroll
-            for (int k = 0; k < 3; ++k) kept[k] = ((const uint4*)(st + (k + 1) * OFB))[t];
+        // the kept frames 1..3 of this band
+        if (!fresh && t < 3 * BV) kept = ((const uint4*)(st + (t / BV + 1) * OFB))[t % BV];
     }
 
-    // stage the aligned cover of every source row; a word that reaches past
-    // the end of the screens is read byte by byte
-    for (int i = t; i < ROWS * RW; i += OBW) {
-        const int r = i / RW, d = i - r * RW;
-        const int64_t a = ((row0 + (int64_t)r * p.w3) & ~(int64_t)3) + 4 * d;
-        uint32_t v = 0;
-        if (a + 4 <= p.total_bytes) {
-            v = *(const uint32_t*)(p.rgb + a);
-        } else {
-            for (int b = 0; b < 4; ++b)
-                if (a + b < p.total_bytes) v |= (uint32_t)p.rgb[a + b] << (8 * b);
+    // the aligned cover of every source row; a vector that reaches past the
+    // end of the screens is read byte by byte
+    uint4 v[LOADS];
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+        const int i = t + u * OBW;
+        if (i < ROWS * RV) {
+            const int r = i / RV, d = i - r * RV;
+            const int64_t a = ((row0 + (int64_t)r * p.w3) & ~(int64_t)15) + 16 * d;
+            if (a + 16 <= p.total_bytes) {
+                v[u] = *(const uint4*)(p.rgb + a);
+            } else {
+                uint32_t w[4] = {0, 0, 0, 0};
+                for (int b = 0; b < 16; ++b)
+                    if (a + b < p.total_bytes) w[b >> 2] |= (uint32_t)p.rgb[a + b] << (8 * (b & 3));
+                v[u] = uint4{w[0], w[1], w[2], w[3]};
+            }
         }
-        s_rgb[i] = v;
     }
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+        const int i = t + u * OBW;
+        if (i < ROWS * RV) s_rgb[i] = v[u];
+    }
+    if (OBSERVE && !fresh && t < 3 * BV) s_kept[t] = kept;
     __syncthreads();
 
     const uint8_t* s_bytes = (const uint8_t*)s_rgb;
@@ -108,8 +125,8 @@ __global__ __launch_bounds__(OBW) void observe_kernel(ObsParams p) {
 #pragma unroll
         for (int dy = 0; dy < F; ++dy) {
             const int r = yl * F + dy;
-            const int shift = (int)((row0 + (int64_t)r * p.w3) & 3);
-            const uint8_t* px = s_bytes + r * RW * 4 + shift + 3 * F * x;
+            const int shift = (int)((row0 + (int64_t)r * p.w3) & 15);
+            const uint8_t* px = s_bytes + r * RV * 16 + shift + 3 * F * x;
 #pragma unroll
             for (int dx = 0; dx < F; ++dx) sum += gray(px[3 * dx], px[3 * dx + 1], px[3 * dx + 2]);
         }
@@ -117,33 +134,20 @@ __global__ __launch_bounds__(OBW) void observe_kernel(ObsParams p) {
     }
     __syncthreads();
 
-    if (t >= BV) return;
-    const uint4 nf = ((const uint4*)s_new)[t];
     if constexpr (!OBSERVE) {
-        ((uint4*)(p.out + e * p.out_stride + y0 * 84))[t] = nf;
+        if (t < BV) ((uint4*)(p.out + e * p.out_stride + y0 * 84))[t] = ((const uint4*)s_new)[t];
     } else {
-        uint4 f[4];
-        if (fresh) {
-            f[0] = f[1] = f[2] = f[3] = nf;
-        } else {
-            f[0] = kept[0];
-            f[1] = kept[1];
-            f[2] = kept[2];
-            f[3] = nf;
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) ((uint4*)(st + k * OFB))[t] = f[k];
+        // thread t: vector t % BV of frame t / BV of the state band; every
+        // load of the band has landed in LDS before the first store
+        if (t >= 4 * BV) return;
+        const int k = t / BV, q = t - k * BV;
+        const uint4 f = (fresh || k == 3) ? ((const uint4*)s_new)[q] : s_kept[t];
+        ((uint4*)(st + k * OFB))[q] = f;
         if (p.rp.frames) {
             const int64_t base = e * (p.rp.cap + 1);
-            const int64_t slot = (p.rp.t + 1) % p.rp.cap;
-            uint8_t* rec = p.rp.frames + (base + slot) * p.rp.stride + y0 * 84;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) ((uint4*)(rec + k * OFB))[t] = f[k];
-            if (slot == 0) {
-                uint8_t* mirror = p.rp.frames + (base + p.rp.cap) * p.rp.stride + y0 * 84;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) ((uint4*)(mirror + k * OFB))[t] = f[k];
-            }
+            const int64_t rslot = (p.rp.t + 1) % p.rp.cap;
+            ((uint4*)(p.rp.frames + (base + rslot) * p.rp.stride + y0 * 84 + k * OFB))[q] = f;
+            if (rslot == 0) ((uint4*)(p.rp.frames + (base + p.rp.cap) * p.rp.stride + y0 * 84 + k * OFB))[q] = f;
             if (band == 0 && t == 0 && p.rp.t >= 0) {
                 const int64_t i = base + p.rp.t % p.rp.cap;
                 p.rp.action[i] = (uint8_t)p.actions[e];
@@ -157,11 +161,12 @@ __global__ __launch_bounds__(OBW) void observe_kernel(ObsParams p) {
 template <int F, bool OBSERVE>
 hipError_t observe_launch(ObsParams prm, int64_t n, hipStream_t st) {
     constexpr int R = band_rows(F);
-    const size_t lds = (size_t)R * F * row_words(F) * 4 + (size_t)R * 84;
+    const size_t lds = (size_t)R * F * row_vecs(F) * 16 + (size_t)R * 84 + (size_t)3 * R * 84;
     auto kern = observe_kernel<F, OBSERVE>;
     if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
     prm.bands = 84 / R;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(n * prm.bands)), dim3(OBW), lds, st, prm);
+    const int64_t blocks = (n + XCDS - 1) / XCDS * XCDS * prm.bands;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(OBW), lds, st, prm, n);
     return hipGetLastError();
 }
 
@@ -185,11 +190,11 @@ int screen_args(const uint8_t* rgb, int64_t n, int32_t h, int32_t w, int32_t top
                 ObsParams& prm) {
     if ((!rgb && n > 0) || n < 0 || h < 1 || w < 1 || f < 1 || f > MAX_F || top < 0 || left < 0) return DQN_EINVAL;
     if ((int64_t)top + 84 * f > h || (int64_t)left + 84 * f > w) return DQN_EINVAL;
-    if ((uintptr_t)rgb % 4) return DQN_EINVAL;
+    if ((uintptr_t)rgb % 16) return DQN_EINVAL;
     const int64_t fb = (int64_t)h * w * 3;
     if (n > 0 && fb > INT64_MAX / n) return DQN_EINVAL;
     // one workgroup per band of a screen; the grid's thread count fits 32 bits
-    if (n * (84 / band_rows(f)) > (int64_t)(UINT32_MAX / OBW)) return DQN_EINVAL;
+    if ((n + XCDS) * (84 / band_rows(f)) > (int64_t)(UINT32_MAX / OBW)) return DQN_EINVAL;
     prm.rgb = rgb;
     prm.frame_bytes = fb;
     prm.total_bytes = n * fb;

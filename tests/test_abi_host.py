@@ -260,7 +260,7 @@ def test_preprocess_argument_errors():
     assert pre(top=9) == dq.DQN_EINVAL                              # window past the bottom edge
     assert pre(left=9) == dq.DQN_EINVAL                             # past the right edge
     assert pre(top=-1) == dq.DQN_EINVAL
-    assert pre(rgb=FAKE + 2) == dq.DQN_EINVAL                      # rgb not 4-byte aligned
+    assert pre(rgb=FAKE + 4) == dq.DQN_EINVAL                      # rgb not 16-byte aligned
     assert pre(out=OUT + 4) == dq.DQN_EINVAL                       # out not 16-byte aligned
     assert pre(stride=7040) == dq.DQN_EINVAL                       # stride < 84*84
     assert pre(stride=7064) == dq.DQN_EINVAL                       # stride not a multiple of 16
