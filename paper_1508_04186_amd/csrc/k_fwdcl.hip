@@ -1,0 +1,244 @@
+// Forward convolution + bias + ReLU of the large network's conv2 and conv3
+// (Sec. III.A) in the bf16-input variant at large batch: bf16 operands,
+// fp32 accumulation, fp32 activations in and out.
+//
+// A workgroup (eight waves, one per compute unit) runs a run of samples with
+// the layer's weights held in registers as bf16 MFMA operands: wave (nt, mh)
+// owns output-channel tile nt (16 channels, about 70 registers of weights)
+// and half of the sample's 16-pixel M-tiles.  Each sample's input is staged
+// in LDS as bf16, channels-last, so that the eight k-values a lane feeds one
+// v_mfma_f32_16x16x32_bf16 (eight consecutive input channels at one pixel of
+// one filter tap) are one 16-byte LDS read, issued two k-steps ahead of its
+// MFMA.  The k order of a step is (tap, 32 channels).  A round takes SPR
+// samples; the next round's input is read from HBM into registers during
+// the current round's MFMAs, and the output maps are assembled in LDS and
+// written as whole 16-byte vectors.  Weights reach the registers through
+// LDS: coalesced loads, converted to bf16 and stored in the order the lanes
+// read them.
+#include <algorithm>
+
+#include "common.h"
+
+namespace dqn {
+namespace {
+
+constexpr int FC_WG = 512;               // eight waves: 4 output-channel tiles x 2 M-halves
+constexpr int FC_TARGET_BLOCKS = 256;   // one workgroup per compute unit
+
+template <int CIN, int IH, int K, int S, int OH, int SPR>
+struct FwdClGeom {
+    static constexpr int COUT = 64;
+    static constexpr int P = OH * OH;                   // output pixels
+    static constexpr int MT = (P + 15) / 16;            // M-tiles per sample
+    static constexpr int MPW = MT / 2;                  // M-tiles per wave
+    static constexpr int KK = K * K;                    // taps
+    static constexpr int CH = CIN / 32;                 // k-steps per tap
+    static constexpr int KS = KK * CH;                  // k-steps
+    static constexpr int KT = CIN * KK;                 // contraction length
+    static constexpr int IP = IH * IH;                  // input pixels
+    static constexpr int PSB = CIN * 2 + 16;            // LDS bytes per staged pixel (16-byte multiple)
+    static constexpr int IN = CIN * IP;                 // input floats per sample
+    static constexpr int PAIRS = IN / 2;                // (channel pair, pixel) items
+    static constexpr int PER = (PAIRS + FC_WG - 1) / FC_WG;
+    static constexpr int OUTF = COUT * P;               // output floats per sample
+    static constexpr int LDS_MAIN = SPR * (IP * PSB + OUTF * 4);
+    static constexpr int LDS_W = COUT * KT * 2;         // all weights as bf16 operands
+    static constexpr int WPER = COUT * KT / 4 / FC_WG;  // weight float4s per thread
+    static_assert(COUT * KT % (4 * FC_WG) == 0, "whole weight float4s per thread");
+    static constexpr int LDS = LDS_MAIN > LDS_W ? LDS_MAIN : LDS_W;
+    static_assert(MT % 2 == 0 && CIN % 32 == 0, "geometry");
+    static_assert(OUTF % 4 == 0 && KT % 4 == 0 && PSB % 16 == 0, "vector widths");
+};
+
+struct FwdClParams {
+    const float* in;           // [n][cin][ih][ih]
+    float* out;                // [n][64][oh][oh]
+    const float *w_a, *b_a, *w_b, *b_b;
+    int n, n_a, g_a, spg;      // blocks [0, g_a) take samples [0, n_a), the rest [n_a, n); runs of spg
+};
+
+template <int CIN, int IH, int K, int S, int OH, int SPR>
+__global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
+    using G = FwdClGeom<CIN, IH, K, S, OH, SPR>;
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* s_in = smem;                                  // [SPR][IP][PSB] bf16, channels-last
+    float* s_out = (float*)(smem + SPR * G::IP * G::PSB);        // [SPR][64][P]
+    __bf16* s_w = (__bf16*)smem;                                 // [4][KS][64][8] bf16 (weights, before the samples)
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int nt = wave & 3, mh = wave >> 2;   // output channels 16nt .. 16nt+15
+
+    const bool second = (int)blockIdx.x >= p.g_a;
+    const int blk = second ? (int)blockIdx.x - p.g_a : (int)blockIdx.x;
+    const int first = second ? p.n_a : 0;
+    const int end = second ? p.n : p.n_a;
+    const int j_lo = first + blk * p.spg;
+    const int j_hi = min(end, j_lo + p.spg);
+    if (j_lo >= j_hi) return;  // whole workgroup
+    const float* __restrict__ W = second ? p.w_b : p.w_a;
+    const float* __restrict__ bias = second ? p.b_b : p.b_a;
+
+    // SPR samples per round: sample j + s of the round is read into
+    // registers (va, vb) and staged into s_in buffer s.
+    float va[SPR][G::PER], vb[SPR][G::PER];
+    auto fetch = [&](int j) {
+#pragma unroll
+        for (int s = 0; s < SPR; ++s) {
+            if (j + s >= j_hi) break;
+            const float* x = p.in + (size_t)(j + s) * G::IN;
+#pragma unroll
+            for (int u = 0; u < G::PER; ++u) {
+                const int q = t + u * FC_WG;
+                if (q < G::PAIRS) {
+                    const int cp = q / G::IP, pix = q - cp * G::IP;
+                    va[s][u] = x[(2 * cp) * G::IP + pix];
+                    vb[s][u] = x[(2 * cp + 1) * G::IP + pix];
+                }
+            }
+        }
+    };
+    auto stage = [&](int j) {
+#pragma unroll
+        for (int s = 0; s < SPR; ++s) {
+            if (j + s >= j_hi) break;
+#pragma unroll
+            for (int u = 0; u < G::PER; ++u) {
+                const int q = t + u * FC_WG;
+                if (q < G::PAIRS) {
+                    const int cp = q / G::IP, pix = q - cp * G::IP;
+                    const uint32_t lo = __builtin_bit_cast(unsigned short, (__bf16)va[s][u]);
+                    const uint32_t hi = __builtin_bit_cast(unsigned short, (__bf16)vb[s][u]);
+                    *(uint32_t*)(s_in + (s * G::IP + pix) * G::PSB + 4 * cp) = lo | (hi << 16);
+                }
+            }
+        }
+    };
+    fetch(j_lo);  // in flight while the weights are loaded
+
+    // Weights: every thread converts its share of W (coalesced float4s) to
+    // bf16 and stores each value where the lane that feeds it to the MFMAs
+    // reads it: lane (li, g) of the wave owning N-tile nt holds, at k-step
+    // ks, W[o][c][tap] for o = 16nt + li, tap = ks / CH, c = 32 (ks % CH) +
+    // 8g + e in element e, at s_w[((nt KS + ks) 64 + lane) 8 + e].
+    {
+        f4 wr[G::WPER];
+#pragma unroll
+        for (int u = 0; u < G::WPER; ++u) wr[u] = ((const f4*)W)[t + u * FC_WG];
+#pragma unroll
+        for (int u = 0; u < G::WPER; ++u) {
+            const int q = t + u * FC_WG;
+            const int o = (4 * q) / G::KT, k0 = 4 * q - o * G::KT;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int k = k0 + v, c = k / G::KK, tap = k - c * G::KK;
+                const int ks = tap * G::CH + c / 32, ln = (o & 15) + 16 * ((c & 31) >> 3);
+                s_w[(((o >> 4) * G::KS + ks) * 64 + ln) * 8 + (c & 7)] = (__bf16)wr[u][v];
+            }
+        }
+    }
+    __syncthreads();
+    bf16x8 wv[G::KS];
+#pragma unroll
+    for (int ks = 0; ks < G::KS; ++ks) wv[ks] = *(const bf16x8*)&s_w[((nt * G::KS + ks) * 64 + lane) * 8];
+    const float bo = bias[16 * nt + li];
+
+    // byte offset in s_in of the lane's first input pixel for each of its
+    // M-tiles (rows past the map read pixel 0; their results are dropped)
+    int pb[G::MPW];
+#pragma unroll
+    for (int i = 0; i < G::MPW; ++i) {
+        const int pp = 16 * (mh * G::MPW + i) + li;
+        const int pc = pp < G::P ? pp : 0;
+        const int oy = pc / OH, ox = pc - oy * OH;
+        pb[i] = ((S * oy) * IH + S * ox) * G::PSB + 16 * g;
+    }
+
+    for (int j = j_lo; j < j_hi; j += SPR) {
+        __syncthreads();  // weight staging, or the previous round's reads of s_in / s_out, done
+        stage(j);
+        __syncthreads();
+        if (j + SPR < j_hi) fetch(j + SPR);
+        // (the MFMAs of a sample past j_hi read stale LDS; their results are not written)
+        f4 acc[SPR][G::MPW];
+#pragma unroll
+        for (int s = 0; s < SPR; ++s)
+#pragma unroll
+            for (int i = 0; i < G::MPW; ++i) acc[s][i] = f4{0.f, 0.f, 0.f, 0.f};
+        // The A operands of step ks + AHEAD are read while step ks multiplies
+        // (LDS latency covered by AHEAD steps of MFMAs).
+        constexpr int AHEAD = 2;
+        auto a_addr = [&](int ks, int s, int i) {
+            const int tap = ks / G::CH;
+            return s_in + s * G::IP * G::PSB + pb[i] + ((tap / K) * IH + tap % K) * G::PSB + 64 * (ks % G::CH);
+        };
+        bf16x8 abuf[AHEAD + 1][SPR][G::MPW];
+#pragma unroll
+        for (int d = 0; d < AHEAD; ++d)
+#pragma unroll
+            for (int s = 0; s < SPR; ++s)
+#pragma unroll
+                for (int i = 0; i < G::MPW; ++i) abuf[d][s][i] = *(const bf16x8*)a_addr(d, s, i);
+#pragma unroll
+        for (int ks = 0; ks < G::KS; ++ks) {
+            if (ks + AHEAD < G::KS) {
+#pragma unroll
+                for (int s = 0; s < SPR; ++s)
+#pragma unroll
+                    for (int i = 0; i < G::MPW; ++i)
+                        abuf[(ks + AHEAD) % (AHEAD + 1)][s][i] = *(const bf16x8*)a_addr(ks + AHEAD, s, i);
+            }
+#pragma unroll
+            for (int s = 0; s < SPR; ++s)
+#pragma unroll
+                for (int i = 0; i < G::MPW; ++i)
+                    acc[s][i] = mfma16x16x32bf16(abuf[ks % (AHEAD + 1)][s][i], wv[ks], acc[s][i]);
+            __builtin_amdgcn_sched_barrier(0);  // keep the reads of later steps where they are
+        }
+        // D[4g + r][li] of an M-tile: pixel 16 mt + 4g + r, channel 16nt + li
+#pragma unroll
+        for (int s = 0; s < SPR; ++s)
+#pragma unroll
+            for (int i = 0; i < G::MPW; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int pp = 16 * (mh * G::MPW + i) + 4 * g + r;
+                    if (pp < G::P) s_out[(s * G::COUT + 16 * nt + li) * G::P + pp] = fmaxf(acc[s][i][r] + bo, 0.f);
+                }
+        __syncthreads();
+        const int ns = min(SPR, j_hi - j);
+        f4* dst = (f4*)(p.out + (size_t)j * G::OUTF);
+        for (int q = t; q < ns * G::OUTF / 4; q += FC_WG) dst[q] = ((const f4*)s_out)[q];
+    }
+}
+
+template <int CIN, int IH, int K, int S, int OH, int SPR>
+hipError_t fwd_cl_launch(const float* in, int n_a, int n, const float* w_a, const float* b_a, const float* w_b,
+                         const float* b_b, float* out, hipStream_t st) {
+    using G = FwdClGeom<CIN, IH, K, S, OH, SPR>;
+    if (n <= 0 || n_a < 0 || n_a > n) return hipErrorInvalidValue;
+    if (((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15) || ((uintptr_t)out & 15)) return hipErrorInvalidValue;
+    const int spg = std::max(1, (n + FC_TARGET_BLOCKS - 1) / FC_TARGET_BLOCKS);
+    const int g_a = (n_a + spg - 1) / spg, g_b = (n - n_a + spg - 1) / spg;
+    const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg};
+    auto kern = conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR>;
+    if (!allow_lds((const void*)kern, G::LDS)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(g_a + g_b)), dim3(FC_WG), G::LDS, st, prm);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool conv_fwd_cl_use(ConvId id, int n, bool bf16) {
+    return bf16 && (id == CONV_L2 || id == CONV_L3) && n >= kFwdClMinRows;
+}
+
+hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const float* w_a, const float* b_a,
+                              const float* w_b, const float* b_b, float* out, hipStream_t st) {
+    switch (id) {
+        case CONV_L2: return fwd_cl_launch<32, 20, 4, 2, 9, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
+        case CONV_L3: return fwd_cl_launch<64, 9, 3, 1, 7, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace dqn
