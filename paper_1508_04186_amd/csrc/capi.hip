@@ -147,7 +147,7 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
     Carver cv;
     const int n2 = 2 * B;
     for (int l = 0; l < ni.n_conv; ++l) t.act[l] = cv.take<float>(ws, (int64_t)n2 * act_elems(ni.d[l]));
-    gemm_fwd_split(n2, ni.H, ni.flat, &t.ks, &t.kchunk);
+    (ni.bf16 ? gemm_fwd_split_bf16 : gemm_fwd_split)(n2, ni.H, ni.flat, &t.ks, &t.kchunk);
     t.fc1p = cv.take<float>(ws, (int64_t)t.ks * n2 * ni.H);
     t.h1s = cv.take<float>(ws, (int64_t)B * ni.H);
     t.dz1 = cv.take<float>(ws, (int64_t)B * ni.H);
@@ -187,7 +187,7 @@ FwdLayout fwd_layout(const NetInfo& ni, int B, void* ws) {
     FwdLayout f{};
     Carver cv;
     for (int l = 0; l < ni.n_conv; ++l) f.act[l] = cv.take<float>(ws, (int64_t)B * act_elems(ni.d[l]));
-    gemm_fwd_split(B, ni.H, ni.flat, &f.ks, &f.kchunk);
+    (ni.bf16 ? gemm_fwd_split_bf16 : gemm_fwd_split)(B, ni.H, ni.flat, &f.ks, &f.kchunk);
     f.fc1p = cv.take<float>(ws, (int64_t)f.ks * B * ni.H);
     f.bytes = cv.off;
     return f;

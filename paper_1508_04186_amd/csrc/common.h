@@ -272,6 +272,13 @@ enum GemmKind { GEMM_NT = 0, GEMM_TN = 1, GEMM_NN = 2 };
 // k-slicing of the fc1 forward GEMM for `rows` output rows: ks slices of
 // kchunk (a multiple of 64, the last one possibly shorter).
 void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk);
+// The same for the bf16-input variant's forward GEMM (its own tiles).
+void gemm_fwd_split_bf16(int rows, int N, int K, int* ks, int* kchunk);
+// The bf16-input contractions of launch_gemm (same arguments; operands
+// rounded to bfloat16 as they are staged).
+hipError_t launch_gemm_bf16(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
+                            float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
+                            hipStream_t st);
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
                        const float* mask, bool bf16, hipStream_t st);

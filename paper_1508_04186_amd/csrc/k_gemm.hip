@@ -337,7 +337,7 @@ hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int l
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
                        const float* mask, bool bf16, hipStream_t st) {
     if (kchunk % 32 != 0) return hipErrorInvalidValue;
-    return bf16 ? launch_gemm_prec<true>(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st)
+    return bf16 ? launch_gemm_bf16(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st)
                 : launch_gemm_prec<false>(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
 }
 

@@ -1,0 +1,218 @@
+// The fully connected layer contractions of the bf16-input variant (fc1
+// forward with split-K partial sums, fc1 weight gradient, fc1 input gradient
+// with the ReLU mask of the last conv layer): both operands rounded to
+// bfloat16 (nearest-even) as they are staged, fp32 accumulation.
+//
+// BMxBN output tiles on WGM x WGN waves, each wave a block of 16x16
+// v_mfma_f32_16x16x32_bf16 tiles, k-stages of BK.  Each operand is staged
+// in LDS as bf16 rows of k-values, [mn][BK + 8], so that the eight k-values
+// a lane feeds one MFMA are one 16-byte read; the padded row stride puts
+// the 16 rows a lane group reads in 16 distinct groups of four banks.  An
+// operand contiguous along k in memory is loaded as float4s along k; one
+// contiguous along m or n as 4x4 blocks (four k-rows of four values)
+// transposed in registers, so every LDS store is 8 bytes.  The next stage's
+// global loads are in flight during the current stage's MFMAs.  The tiles
+// are large where the batch is (each operand is re-read once per tile of
+// the other dimension, from L2), and the forward pass splits K so that the
+// launch still covers the chip.
+#include <algorithm>
+
+#include "common.h"
+
+namespace dqn {
+namespace {
+
+struct GemmBf16Params {
+    int M, N, K;
+    const float* A;
+    int lda;
+    const float* B;
+    int ldb;
+    float* C;
+    int ldc, kchunk;
+    int64_t c_slice;
+    const float* mask;
+};
+
+__device__ __forceinline__ uint2 pack4(f4 v) {
+    const uint32_t a = __builtin_bit_cast(unsigned short, (__bf16)v[0]);
+    const uint32_t b = __builtin_bit_cast(unsigned short, (__bf16)v[1]);
+    const uint32_t c = __builtin_bit_cast(unsigned short, (__bf16)v[2]);
+    const uint32_t d = __builtin_bit_cast(unsigned short, (__bf16)v[3]);
+    return uint2{a | (b << 16), c | (d << 16)};
+}
+
+// One operand's stage: ROWS rows (m or n) x BK k, staged by NT threads.
+// KCONT: the operand is contiguous along k in memory (element (r, k) at
+// src[r*ld + k]); otherwise along r (element (r, k) at src[k*ld + r]).
+template <int ROWS, int BK, int NT, bool KCONT>
+struct Stage {
+    static constexpr int KQ = BK / 4;                 // float4s along k per row
+    static constexpr int NV = ROWS * BK / 4 / NT;     // float4s per thread
+    static constexpr int RS = BK + 8;                 // LDS row stride (bf16)
+    static_assert(NV * NT * 4 == ROWS * BK && (KCONT || NV % 4 == 0), "stage split");
+    f4 v[NV];
+    __device__ __forceinline__ void load(const float* __restrict__ src, int ld, int r0, int rlim, int k0, int klim) {
+        const int t = threadIdx.x;
+        if constexpr (KCONT) {
+#pragma unroll
+            for (int u = 0; u < NV; ++u) {
+                const int q = t + NT * u, r = q / KQ, k = k0 + 4 * (q % KQ);
+                v[u] = (r0 + r < rlim && k < klim) ? *(const f4*)(src + (size_t)(r0 + r) * ld + k)
+                                                   : f4{0.f, 0.f, 0.f, 0.f};
+            }
+        } else {
+            // 4x4 block b: rows 4 (b % (ROWS/4)) .. +3, k-rows 4 (b / (ROWS/4)) .. +3
+#pragma unroll
+            for (int w = 0; w < NV / 4; ++w) {
+                const int b = t + NT * w;
+                const int r = r0 + 4 * (b % (ROWS / 4)), kb = k0 + 4 * (b / (ROWS / 4));
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    v[4 * w + u] = (kb + u < klim && r < rlim) ? *(const f4*)(src + (size_t)(kb + u) * ld + r)
+                                                               : f4{0.f, 0.f, 0.f, 0.f};
+            }
+        }
+    }
+    __device__ __forceinline__ void store(__bf16* s) const {
+        const int t = threadIdx.x;
+        if constexpr (KCONT) {
+#pragma unroll
+            for (int u = 0; u < NV; ++u) {
+                const int q = t + NT * u, r = q / KQ, k = 4 * (q % KQ);
+                *(uint2*)&s[r * RS + k] = pack4(v[u]);
+            }
+        } else {
+#pragma unroll
+            for (int w = 0; w < NV / 4; ++w) {
+                const int b = t + NT * w;
+                const int r = 4 * (b % (ROWS / 4)), k = 4 * (b / (ROWS / 4));
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    *(uint2*)&s[(r + i) * RS + k] =
+                        pack4(f4{v[4 * w][i], v[4 * w + 1][i], v[4 * w + 2][i], v[4 * w + 3][i]});
+            }
+        }
+    }
+};
+
+// TA: A(m,k) = A[k*lda + m] else A[m*lda + k].
+// TB: B(k,n) = B[n*ldb + k] else B[k*ldb + n].
+// MASK: C(m,n) = 0 where mask[m*ldc + n] <= 0.
+template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Params p) {
+    constexpr int NT = 64 * WGM * WGN;
+    constexpr int WTM = BM / WGM, WTN = BN / WGN;     // wave tile
+    constexpr int TM = WTM / 16, TN = WTN / 16;       // MFMA tiles per wave
+    constexpr int RS = BK + 8;
+    static_assert(BK % 32 == 0 && WTM % 16 == 0 && WTN % 16 == 0, "tile shape");
+    __shared__ __align__(16) __bf16 As[BM * RS];
+    __shared__ __align__(16) __bf16 Bs[BN * RS];
+    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN, z = blockIdx.z;
+    const int kbeg = z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int wm = (wave / WGN) * WTM, wn = (wave % WGN) * WTN;
+
+    Stage<BM, BK, NT, !TA> sa;
+    Stage<BN, BK, NT, TB> sb;
+    f4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    if (kbeg < kend) {
+        sa.load(p.A, p.lda, m0, p.M, kbeg, kend);
+        sb.load(p.B, p.ldb, n0, p.N, kbeg, kend);
+    }
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+        sa.store(As);
+        sb.store(Bs);
+        __syncthreads();
+        if (k0 + BK < kend) {   // in flight during the MFMAs below
+            sa.load(p.A, p.lda, m0, p.M, k0 + BK, kend);
+            sb.load(p.B, p.ldb, n0, p.N, k0 + BK, kend);
+        }
+#pragma unroll
+        for (int kb = 0; kb < BK / 32; ++kb) {
+            bf16x8 a[TM], b[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) a[i] = *(const bf16x8*)&As[(wm + 16 * i + li) * RS + 32 * kb + 8 * g];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) b[j] = *(const bf16x8*)&Bs[(wn + 16 * j + li) * RS + 32 * kb + 8 * g];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x32bf16(a[i], b[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+
+    // D[4g + r][li] of tile (i, j): row m0 + wm + 16i + 4g + r, column n0 + wn + 16j + li
+    float* Cz = p.C + (size_t)z * p.c_slice;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int n = n0 + wn + 16 * j + li;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = m0 + wm + 16 * i + 4 * g + r;
+                if (m < p.M && n < p.N) {
+                    float v = acc[i][j][r];
+                    if constexpr (MASK) v = p.mask[(size_t)m * p.ldc + n] > 0.f ? v : 0.f;
+                    Cz[(size_t)m * p.ldc + n] = v;
+                }
+            }
+        }
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
+hipError_t gemm_bf16_launch(const GemmBf16Params& prm, int kslices, hipStream_t st) {
+    const dim3 grid((unsigned)((prm.M + BM - 1) / BM), (unsigned)((prm.N + BN - 1) / BN), (unsigned)kslices);
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, TA, TB, MASK>), grid, dim3(64 * WGM * WGN), 0, st,
+                       prm);
+    return hipGetLastError();
+}
+
+// Forward and input-gradient tiles: 128x256 and 128x128 from kBf16BigRows
+// rows on (fewer re-reads of the operands), else 64x64 (more workgroups).
+constexpr int kBf16BigRows = 1024;
+
+}  // namespace
+
+void gemm_fwd_split_bf16(int rows, int N, int K, int* ks, int* kchunk) {
+    const bool big = rows >= kBf16BigRows;
+    const int bm = big ? 128 : 64, bn = big ? 256 : 64;
+    const long tiles = (long)((rows + bm - 1) / bm) * ((N + bn - 1) / bn);
+    const int steps = (K + 63) / 64;                       // 64-wide k-steps
+    const long target = big ? 256 : 768;                   // workgroups: one (large tiles) or three per CU
+    const int want = (int)std::min<long>(steps, std::max<long>(1, (target + tiles - 1) / tiles));
+    *kchunk = (steps + want - 1) / want * 64;
+    *ks = (K + *kchunk - 1) / *kchunk;
+}
+
+hipError_t launch_gemm_bf16(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
+                            float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
+                            hipStream_t st) {
+    if (M <= 0 || N <= 0 || K <= 0 || kslices <= 0 || kchunk % 32 != 0) return hipErrorInvalidValue;
+    if ((uintptr_t)A % 16 || (uintptr_t)B % 16 || lda % 4 || ldb % 4) return hipErrorInvalidValue;
+    const GemmBf16Params prm{M, N, K, A, lda, B, ldb, C, ldc, kchunk, c_slice, mask};
+    switch (kind) {
+        case GEMM_NT:
+            if (K % 4) return hipErrorInvalidValue;
+            if (M >= kBf16BigRows) return gemm_bf16_launch<128, 256, 64, 2, 4, false, true, false>(prm, kslices, st);
+            return gemm_bf16_launch<64, 64, 128, 2, 2, false, true, false>(prm, kslices, st);
+        case GEMM_TN:
+            if (M % 4 || N % 4) return hipErrorInvalidValue;
+            return gemm_bf16_launch<64, 64, 128, 2, 2, true, false, false>(prm, kslices, st);
+        case GEMM_NN:
+            if (!mask || K % 4 || N % 4) return hipErrorInvalidValue;
+            if (M >= kBf16BigRows) return gemm_bf16_launch<128, 128, 64, 2, 4, false, false, true>(prm, kslices, st);
+            return gemm_bf16_launch<64, 64, 128, 2, 2, false, false, true>(prm, kslices, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace dqn
