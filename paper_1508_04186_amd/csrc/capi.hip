@@ -139,6 +139,7 @@ struct TdLayout {
     float* bpart[3];
     int chunks[3];
     int ks, kchunk;
+    float* spart;   // sample-sum chunk slots of the finalize (above 128 samples)
     size_t bytes;
 };
 
@@ -172,6 +173,7 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
         t.wpart[l] = cv.take<float>(ws, slots * c.cout * c.cin * c.k * c.k);
         t.bpart[l] = cv.take<float>(ws, slots * c.cout);
     }
+    t.spart = cv.take<float>(ws, (int64_t)finalize_sample_chunks(B) * ((int64_t)ni.A * ni.H + ni.H + ni.A + 1));
     t.bytes = cv.off;
     return t;
 }
@@ -472,6 +474,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     fa.grad_base = grad_out;
     fa.fc1w_off = ni.w_off[L];
     fa.fc1w_count = (int64_t)ni.H * ni.flat;
+    fa.spart = t.spart;
+    fa.schunks = finalize_sample_chunks(B);
     if (upd)
         RUN(DQN_K_FINALIZE_APPLY, launch_finalize(fa, upd, st));
     else

@@ -329,7 +329,13 @@ struct FinalizeArgs {
     // (the fc1 weights) that an earlier kernel wrote in full.
     const float* grad_base;
     int64_t fc1w_off, fc1w_count;
+    // Above 128 samples: sample-sum partial slots, one per chunk of 32
+    // samples, each A*H + H + A + 1 floats (workspace).
+    float* spart;
+    int schunks;
 };
+// Chunk slots of the sums over samples for batch B (0 up to 128 samples).
+inline int finalize_sample_chunks(int B) { return B > 128 ? (B + 31) / 32 : 0; }
 
 // A parameter-server update fused into the last kernel of a TD step.
 struct PsUpdate {

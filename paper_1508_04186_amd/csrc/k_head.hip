@@ -219,22 +219,20 @@ __global__ __launch_bounds__(HT) void head_fwd_kernel(HeadFwdArgs p) {
 }
 
 // Each output's terms are summed in a fixed association, without atomics.
-// Segments, in slots of eight lanes:
-//  - sums over the B samples, one wave per output (G = 64 lanes; lane L takes
-//    samples j = L, L + G, ... with every load unconditional and eight
-//    samples in flight; the wave then combines its lanes in a fixed
-//    butterfly): the fc2
-//    weights of hidden unit h for all actions at once (delta_j * h1[j][h]
-//    added to the sum of the action j took), the fc1 bias of h, the fc2 bias
-//    of every action, and the loss;
-//  - the conv weight and bias gradients, eight lanes per output over the
-//    wgrad partial-sum slots.
+// Up to 128 samples, finalize_small_kernel below.  Above, two launches:
+//  - sample_partials_kernel: for chunks of 32 samples, the chunk's sums of
+//    the fc2 weight gradient (delta_j * h1[j][h] added to the sum of the
+//    action j took), the fc1 bias gradient, the fc2 bias gradient and the
+//    loss, into one partial-sum slot per chunk.  A workgroup takes 64 hidden
+//    units of a chunk, so its loads are 256-byte rows;
+//  - finalize_wide_kernel: one lane per output (consecutive outputs, so
+//    every load is a 256-byte row of a slot) sums its slots in slot order:
+//    the conv weight and bias gradients over the wgrad partial-sum slots,
+//    then the sample sums over the chunk slots.
 //
 // MODE < 0 stores the gradient; MODE = 0, 1, 2 applies update rule MODE to
 // each parameter instead (fused parameter-server update), and the blocks
 // from n_fin on update the fc1 weights from the gradient stored there.
-constexpr int FIN_U = 8;       // samples in flight per lane
-
 template <int MODE>
 __device__ __forceinline__ void emit(const FinalizeArgs& a, const PsUpdate& u, float* dst, float v) {
     if constexpr (MODE < 0) {
@@ -265,66 +263,6 @@ __device__ __forceinline__ void apply_fc1w(const FinalizeArgs& a, const PsUpdate
     }
     *(f4*)(u.theta + off) = th;
     if constexpr (MODE != 0) *(f4*)(u.state + off) = sv;
-}
-
-// Sums over samples of one wave (see above).  kind 0: fc2 weights of hidden
-// unit h for every action; 1: fc1 bias of h; 2: fc2 bias of every action;
-// 3: the loss.
-template <int MODE, int A, int GL>
-__device__ __forceinline__ void sample_sums(const FinalizeArgs& a, const PsUpdate& u, int kind, int h) {
-    const int L = threadIdx.x & (GL - 1);
-    float s[A];
-#pragma unroll
-    for (int k = 0; k < A; ++k) s[k] = 0.f;
-    const bool per_action = kind == 0 || kind == 2;
-    for (int j0 = L; j0 < a.B; j0 += GL * FIN_U) {
-        int act[FIN_U];
-        float d[FIN_U];
-#pragma unroll
-        for (int e = 0; e < FIN_U; ++e) {
-            const int j = j0 + GL * e;
-            const bool v = j < a.B;
-            act[e] = -1;
-            d[e] = 0.f;
-            if (v) {
-                if (kind == 0) {
-                    act[e] = min(max(a.action[j], 0), A - 1);   // clamped as in the head
-                    d[e] = a.delta[j] * a.h1s[(int64_t)j * a.H + h];
-                } else if (kind == 1) {
-                    d[e] = a.dz1[(int64_t)j * a.H + h];
-                } else if (kind == 2) {
-                    act[e] = min(max(a.action[j], 0), A - 1);
-                    d[e] = a.delta[j];
-                } else {
-                    d[e] = a.lossj[j];
-                }
-            }
-        }
-#pragma unroll
-        for (int e = 0; e < FIN_U; ++e) {
-            if (per_action) {
-#pragma unroll
-                for (int k = 0; k < A; ++k) s[k] += act[e] == k ? d[e] : 0.f;
-            } else {
-                s[0] += d[e];
-            }
-        }
-    }
-    const int nk = per_action ? A : 1;
-#pragma unroll
-    for (int k = 0; k < A; ++k) {
-        if (k < nk) {
-            float t = s[k];
-#pragma unroll
-            for (int m = 1; m < GL; m <<= 1) t += __shfl_xor(t, m, 64);
-            if (L == 0) {
-                if (kind == 0) emit<MODE>(a, u, a.g_W2 + (int64_t)k * a.H + h, t);
-                else if (kind == 1) emit<MODE>(a, u, a.g_b1 + h, t);
-                else if (kind == 2) emit<MODE>(a, u, a.g_b2 + k, t);
-                else a.loss_out[0] = t;
-            }
-        }
-    }
 }
 
 // Actions outside [0, A) count as the nearest valid one, as in the head.
@@ -401,41 +339,104 @@ __global__ __launch_bounds__(256) void finalize_small_kernel(FinalizeArgs a, PsU
     }
 }
 
-template <int MODE, int A, int GL>
-__global__ __launch_bounds__(256) void finalize_kernel(FinalizeArgs a, PsUpdate u, int n_fin) {
+// Chunk c of 32 samples, hidden units 64 bx .. 64 bx + 63 (one per lane);
+// wave w takes samples 32c + w + 4i in order, the four wave sums are added
+// in wave order.  Block x = 0 also forms the chunk's fc2 bias gradient and
+// loss (lane = sample, fixed butterfly).  Slot layout: fc2 weights [A][H],
+// fc1 bias [H], fc2 bias [A], loss.
+constexpr int SP_CHUNK = 32;
+template <int A>
+__global__ __launch_bounds__(256) void sample_partials_kernel(FinalizeArgs a) {
+    __shared__ float red[4][A + 1][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int h = blockIdx.x * 64 + lane;
+    const int c = blockIdx.y;
+    const int j0 = c * SP_CHUNK, j1 = min(a.B, j0 + SP_CHUNK);
+    const int64_t count = (int64_t)A * a.H + a.H + A + 1;
+    float* slot = a.spart + (int64_t)c * count;
+    float sw[A], sb = 0.f;
+#pragma unroll
+    for (int k = 0; k < A; ++k) sw[k] = 0.f;
+#pragma unroll
+    for (int i = 0; i < SP_CHUNK / 4; ++i) {
+        const int j = j0 + w + 4 * i;
+        if (j < j1) {
+            const int act = clamp_action(a.action[j], A);
+            const float d = a.delta[j] * a.h1s[(int64_t)j * a.H + h];
+#pragma unroll
+            for (int k = 0; k < A; ++k) sw[k] += act == k ? d : 0.f;
+            sb += a.dz1[(int64_t)j * a.H + h];
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < A; ++k) red[w][k][lane] = sw[k];
+    red[w][A][lane] = sb;
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+        for (int k = 0; k <= A; ++k) {
+            const float v = ((red[0][k][lane] + red[1][k][lane]) + red[2][k][lane]) + red[3][k][lane];
+            slot[(k < A ? (int64_t)k * a.H : (int64_t)A * a.H) + h] = v;
+        }
+    } else if (w == 1 && blockIdx.x == 0) {
+        const int j = j0 + lane;
+        const bool v = lane < SP_CHUNK && j < j1;
+        const int act = v ? clamp_action(a.action[j], A) : -1;
+        const float d = v ? a.delta[j] : 0.f;
+        const float l = v ? a.lossj[j] : 0.f;
+#pragma unroll
+        for (int k = 0; k < A; ++k) {
+            const float t = wave_sum(act == k ? d : 0.f);
+            if (lane == 0) slot[(int64_t)A * a.H + a.H + k] = t;
+        }
+        const float t = wave_sum(l);
+        if (lane == 0) slot[count - 1] = t;
+    }
+}
+
+constexpr int FW_U = 32;   // slots in flight per lane
+template <int MODE>
+__global__ __launch_bounds__(256) void finalize_wide_kernel(FinalizeArgs a, PsUpdate u, int n_fin) {
     if constexpr (MODE >= 0) {
         if ((int)blockIdx.x >= n_fin) {
             apply_fc1w<MODE>(a, u, (int64_t)(blockIdx.x - n_fin) * 256 + threadIdx.x);
             return;
         }
     }
-    int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3;
-    // one group of GL lanes per output of the sums over samples: groups 0 .. 2H + 1
-    constexpr int SPG = GL / 8;   // slots per group
-    const int64_t n_grp = 2 * (int64_t)a.H + 2;
-    if (i < SPG * n_grp) {
-        const int w = (int)(i / SPG);
-        if (w < a.H) sample_sums<MODE, A, GL>(a, u, 0, w);
-        else if (w < 2 * a.H) sample_sums<MODE, A, GL>(a, u, 1, w - a.H);
-        else sample_sums<MODE, A, GL>(a, u, w == 2 * a.H ? 2 : 3, 0);
-        return;
-    }
-    i -= SPG * n_grp;
-    const bool lead = (threadIdx.x & 7) == 0;
-    for (int l = 0; l < a.n_conv; ++l) {
+    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const float* part = nullptr;
+    int64_t count = 0;
+    int slots = 0;
+    float* dst = nullptr;
+    bool loss = false;
+    for (int l = 0; l < a.n_conv && !part; ++l) {
         if (i < a.wcount[l]) {
-            const float v = sum_strided_x8(a.wpart[l] + i, a.chunks[l], a.wcount[l]);
-            if (lead) emit<MODE>(a, u, a.gw[l] + i, v);
-            return;
+            part = a.wpart[l] + i, count = a.wcount[l], slots = a.chunks[l], dst = a.gw[l] + i;
+        } else if ((i -= a.wcount[l]) < a.cout[l]) {
+            part = a.bpart[l] + i, count = a.cout[l], slots = a.chunks[l], dst = a.gb[l] + i;
+        } else {
+            i -= a.cout[l];
         }
-        i -= a.wcount[l];
-        if (i < a.cout[l]) {
-            const float v = sum_strided_x8(a.bpart[l] + i, a.chunks[l], a.cout[l]);
-            if (lead) emit<MODE>(a, u, a.gb[l] + i, v);
-            return;
-        }
-        i -= a.cout[l];
     }
+    if (!part) {
+        const int64_t wh = (int64_t)a.A * a.H, cs = wh + a.H + a.A + 1;
+        if (i >= cs) return;
+        part = a.spart + i, count = cs, slots = a.schunks;
+        if (i < wh) dst = a.g_W2 + i;
+        else if (i < wh + a.H) dst = a.g_b1 + (i - wh);
+        else if (i < wh + a.H + a.A) dst = a.g_b2 + (i - wh - a.H);
+        else loss = true;
+    }
+    float s = 0.f;
+    for (int q = 0; q < slots; q += FW_U) {
+        float v[FW_U];
+#pragma unroll
+        for (int e = 0; e < FW_U; ++e) v[e] = q + e < slots ? part[(int64_t)(q + e) * count] : 0.f;
+#pragma unroll
+        for (int e = 0; e < FW_U; ++e) s += v[e];
+    }
+    if (loss) a.loss_out[0] = s;
+    else emit<MODE>(a, u, dst, s);
 }
 
 template <int H, int A>
@@ -464,22 +465,25 @@ hipError_t launch_head_fwd(int H, int A, const HeadFwdArgs& a, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
-template <int A, int GL>
-hipError_t finalize_launch(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
-    int64_t total = (GL / 8) * (2 * (int64_t)a.H + 2);   // slots: one group per sum over samples
+template <int A>
+hipError_t finalize_wide_launch(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
+    if (!a.spart || a.schunks != (a.B + SP_CHUNK - 1) / SP_CHUNK || a.H % 64) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(sample_partials_kernel<A>, dim3((unsigned)(a.H / 64), (unsigned)a.schunks), dim3(256), 0, st,
+                       a);
+    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+    int64_t total = (int64_t)A * a.H + a.H + A + 1;
     for (int l = 0; l < a.n_conv; ++l) total += a.wcount[l] + a.cout[l];
-    const int n_fin = (int)((total * 8 + 255) / 256);
+    const int n_fin = (int)((total + 255) / 256);
     if (!upd) {
-        hipLaunchKernelGGL((finalize_kernel<-1, A, GL>), dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{},
-                           n_fin);
+        hipLaunchKernelGGL(finalize_wide_kernel<-1>, dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{}, n_fin);
         return hipGetLastError();
     }
     if (a.fc1w_off % 4 != 0 || a.fc1w_count % 4 != 0 || !a.grad_base) return hipErrorInvalidValue;
     const dim3 grid((unsigned)(n_fin + (a.fc1w_count / 4 + 255) / 256));
     switch (upd->rule) {
-        case 0: hipLaunchKernelGGL((finalize_kernel<0, A, GL>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
-        case 1: hipLaunchKernelGGL((finalize_kernel<1, A, GL>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
-        case 2: hipLaunchKernelGGL((finalize_kernel<2, A, GL>), grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 0: hipLaunchKernelGGL(finalize_wide_kernel<0>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 1: hipLaunchKernelGGL(finalize_wide_kernel<1>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
+        case 2: hipLaunchKernelGGL(finalize_wide_kernel<2>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -505,10 +509,10 @@ hipError_t finalize_small_launch(const FinalizeArgs& a, const PsUpdate* upd, hip
 }
 
 hipError_t launch_finalize(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st) {
-    // up to 128 samples the eight-lane layout; above, a wave per sum over samples
+    // up to 128 samples the eight-lane layout; above, chunk slots and a lane per output
     if (a.B <= 128) return finalize_small_launch(a, upd, st);
-    if (a.A == 6) return finalize_launch<6, 64>(a, upd, st);
-    if (a.A == 18) return finalize_launch<18, 64>(a, upd, st);
+    if (a.A == 6) return finalize_wide_launch<6>(a, upd, st);
+    if (a.A == 18) return finalize_wide_launch<18>(a, upd, st);
     return hipErrorInvalidValue;
 }
 
