@@ -8,6 +8,8 @@
 //         epsilon-greedy exploration, the caller-drawn random action.
 // The finalize kernel then reduces everything that sums over samples or over
 // wgrad chunks in a fixed order (no atomics), so results are deterministic.
+#include <algorithm>
+
 #include "common.h"
 
 namespace dqn {
@@ -170,6 +172,100 @@ __global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
 #pragma unroll
         for (int k = 1; k < A; ++k) q = (k == (int)threadIdx.x) ? v[k] : q;
         p.q_out[(int64_t)j * A + threadIdx.x] = q + p.b2[threadIdx.x];
+    }
+}
+
+// The TD head for large batches: a workgroup stages both fc2 weight sets in
+// LDS once and its four waves take whole samples (wave w: samples j_lo + w,
+// j_lo + w + 4, ...), lane l owning hidden units l + 64e.  The fc1 slices
+// are summed in slice order, the fc2 outputs with one wave reduction each;
+// no workgroup barrier after the staging.  Same arithmetic per sample as
+// head_td_kernel, in a different association of the hidden-unit sums.
+template <int H, int A>
+__global__ __launch_bounds__(256) void head_td_wide_kernel(HeadTdArgs p, int spg) {
+    constexpr int E = H / 64;
+    extern __shared__ float s_w2[];   // [2][A][H]: W2, then W2t
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    for (int i = threadIdx.x; i < A * H / 4; i += 256) {
+        ((f4*)s_w2)[i] = ((const f4*)p.W2)[i];
+        ((f4*)s_w2)[A * H / 4 + i] = ((const f4*)p.W2t)[i];
+    }
+    float b1v[E], b1tv[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        b1v[e] = p.b1[lane + 64 * e];
+        b1tv[e] = p.b1t[lane + 64 * e];
+    }
+    __syncthreads();
+    const float* W2 = s_w2;
+    const float* W2t = s_w2 + A * H;
+    const int B = p.B;
+    const int64_t slice = (int64_t)2 * B * H;
+    const int j_lo = blockIdx.x * spg, j_hi = min(B, j_lo + spg);
+    for (int j = j_lo + w; j < j_hi; j += 4) {
+        const int act = min(max(p.action[j], 0), A - 1);
+        const float r = p.reward[j];
+        const bool term = p.terminal[j] != 0;
+        float zs[E], zn[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) zs[e] = zn[e] = 0.f;
+        for (int z = 0; z < p.ks; ++z) {
+            const float* sl = p.fc1p + (int64_t)z * slice;
+            float a[E], b[E];
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                a[e] = sl[(int64_t)j * H + lane + 64 * e];
+                b[e] = sl[(int64_t)(B + j) * H + lane + 64 * e];
+            }
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                zs[e] += a[e];
+                zn[e] += b[e];
+            }
+        }
+        float hs[E], v[2 * A];
+#pragma unroll
+        for (int k = 0; k < 2 * A; ++k) v[k] = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int h = lane + 64 * e;
+            zs[e] += b1v[e];
+            hs[e] = fmaxf(zs[e], 0.f);
+            const float hn = fmaxf(zn[e] + b1tv[e], 0.f);
+#pragma unroll
+            for (int k = 0; k < A; ++k) {
+                v[k] = fmaf(W2[k * H + h], hs[e], v[k]);
+                v[A + k] = fmaf(W2t[k * H + h], hn, v[A + k]);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 2 * A; ++k) v[k] = wave_sum(v[k]);
+        float m = v[A] + p.b2t[0];
+#pragma unroll
+        for (int k = 1; k < A; ++k) m = fmaxf(m, v[A + k] + p.b2t[k]);
+        const float y = term ? r : fmaf(p.gamma, m, r);
+        float qa = v[0] + p.b2[0];
+#pragma unroll
+        for (int k = 1; k < A; ++k) qa = (k == act) ? v[k] + p.b2[k] : qa;
+        const float diff = qa - y;
+        const float delta = diff / (float)B;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int h = lane + 64 * e;
+            p.h1s[(int64_t)j * H + h] = hs[e];
+            p.dz1[(int64_t)j * H + h] = zs[e] > 0.f ? delta * W2[act * H + h] : 0.f;
+        }
+        if (lane == 0) {
+            p.delta[j] = delta;
+            p.lossj[j] = 0.5f * diff * diff / (float)B;
+            if (p.y_out) p.y_out[j] = y;
+        }
+        if (p.q_out && lane < A) {
+            float q = v[0];
+#pragma unroll
+            for (int k = 1; k < A; ++k) q = (k == lane) ? v[k] : q;
+            p.q_out[(int64_t)j * A + lane] = q + p.b2[lane];
+        }
     }
 }
 
@@ -439,8 +535,21 @@ __global__ __launch_bounds__(256) void finalize_wide_kernel(FinalizeArgs a, PsUp
     else emit<MODE>(a, u, dst, s);
 }
 
+// From kHeadWideRows samples on, the wide head on up to 256 workgroups
+// (below, one workgroup per sample is faster).
+constexpr int kHeadWideRows = 1024;
 template <int H, int A>
 hipError_t td_launch(const HeadTdArgs& a, hipStream_t st) {
+    if (a.B >= kHeadWideRows) {
+        if (((uintptr_t)a.W2 & 15) || ((uintptr_t)a.W2t & 15)) return hipErrorInvalidValue;
+        const int blocks = std::min(256, (a.B + 3) / 4);
+        const int spg = (a.B + blocks - 1) / blocks;
+        constexpr size_t lds = (size_t)2 * A * H * 4;
+        auto kern = head_td_wide_kernel<H, A>;
+        if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(kern, dim3((unsigned)((a.B + spg - 1) / spg)), dim3(256), lds, st, a, spg);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL((head_td_kernel<H, A>), dim3((unsigned)a.B), dim3(HT), 0, st, a);
     return hipGetLastError();
 }
