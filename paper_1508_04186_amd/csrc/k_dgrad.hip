@@ -15,11 +15,10 @@
 // (= 48 mod 64) and 16 consecutive pixels contiguous, so a wave's 64 reads
 // hit 64 banks.  A phase has 100 pixels: 7 M-tiles of 16, the last one
 // partly unused.  The four phases' results are assembled into the sample's
-// whole input gradient in LDS, then written with 16-byte stores next to
-// 16-byte reads of the ReLU mask.  The next sample's dz is read into
-// registers while the current one is computed.  Both precisions: fp32 MFMA,
-// or the bf16-input variant (operands rounded to bfloat16 in registers, one
-// 16x16x32 step per 32 output channels).
+// whole input gradient in LDS, then written with 16-byte stores, masked by
+// the ReLU mask read into registers at the start of the sample's round.  The
+// next sample's dz is read into registers while the current one is
+// computed.  fp32 MFMA; the bf16-input variant is conv2_dgrad_cl_kernel.
 #include <algorithm>
 #include <type_traits>
 
@@ -53,7 +52,6 @@ struct Dgrad2Params {
     int n, spg;         // samples, samples per workgroup
 };
 
-template <bool BF16>
 __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p) {
     __shared__ float s_dz[D2_STAGE];
     __shared__ __align__(16) float s_din[D2_IN];
@@ -71,27 +69,16 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p
 
     // B operands of this lane for every k-step: k = tap * 64 + o, tap = 2ty + tx.
     const int c = nt * 16 + li;
-    constexpr int KS = BF16 ? D2_KT / 32 : D2_KT / 4;
-    using BOp = typename std::conditional<BF16, bf16x8, float>::type;
-    BOp wreg[KS];
+    constexpr int KS = D2_KT / 4;
+    float wreg[KS];
     {
         const float* wc = p.w + (size_t)c * D2_K * D2_K + py * D2_K + px;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-            if constexpr (BF16) {
-                // k-step s: tap s / 2, o = 32 * (s % 2) + 4e + g
-                const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int o = 32 * (s % 2) + 4 * e + g;
-                    wreg[s][e] = (__bf16)wc[(size_t)o * D2_CIN * D2_K * D2_K + 2 * ty * D2_K + 2 * tx];
-                }
-            } else {
-                // k-step s: tap s / 16, o = 4 * (s % 16) + g
-                const int tap = s / 16, ty = tap >> 1, tx = tap & 1;
-                const int o = 4 * (s % 16) + g;
-                wreg[s] = wc[(size_t)o * D2_CIN * D2_K * D2_K + 2 * ty * D2_K + 2 * tx];
-            }
+            // k-step s: tap s / 16, o = 4 * (s % 16) + g
+            const int tap = s / 16, ty = tap >> 1, tx = tap & 1;
+            const int o = 4 * (s % 16) + g;
+            wreg[s] = wc[(size_t)o * D2_CIN * D2_K * D2_K + 2 * ty * D2_K + 2 * tx];
         }
     }
 
@@ -132,6 +119,14 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p
         stage();
         __syncthreads();
         if (j + 1 < j_hi) fetch(j + 1);  // in flight during this sample's MFMAs
+        // this sample's ReLU mask, for the write-out below
+        const size_t o0 = (size_t)j * D2_IN;
+        f4 mreg[D2_OUT4];
+#pragma unroll
+        for (int u = 0; u < D2_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D2_IN / 4) mreg[u] = *(const f4*)(p.h_in + o0 + 4 * e4);
+        }
 
         f4 acc[D2_MT];
 #pragma unroll
@@ -139,29 +134,7 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p
         // The k-steps run in order with the next step's A operands read
         // before the current step's MFMAs issue (scheduling groups), and a
         // barrier per step keeps the compiler from hoisting every LDS read.
-        if constexpr (BF16) {
-            auto load = [&](int s, bf16x8 (&a)[D2_MT]) {
-                const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
-                const int off = 32 * (s % 2) * D2_CS - D2_Q * ty - tx;
-#pragma unroll
-                for (int i = 0; i < D2_MT; ++i) {
-                    const float* ap = s_dz + base[i] + off;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) a[i][e] = (__bf16)ap[4 * e * D2_CS];
-                }
-            };
-            bf16x8 a[2][D2_MT];
-            load(0, a[0]);
-#pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                if (s + 1 < KS) load(s + 1, a[(s + 1) & 1]);
-#pragma unroll
-                for (int i = 0; i < D2_MT; ++i) acc[i] = mfma16x16x32bf16(a[s & 1][i], wreg[s], acc[i]);
-                if (s + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 8 * D2_MT, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, D2_MT, 0);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        } else {
+        {
             auto load = [&](int s, float (&a)[D2_MT]) {
                 const int tap = s / 16, ty = tap >> 1, tx = tap & 1;
                 const int off = 4 * (s % 16) * D2_CS - D2_Q * ty - tx;
@@ -196,12 +169,156 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p
             }
         __syncthreads();
         // masked write-out with 16-byte accesses
-        const size_t o0 = (size_t)j * D2_IN;
 #pragma unroll
         for (int u = 0; u < D2_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
             if (e4 < D2_IN / 4) {
-                const f4 h = *(const f4*)(p.h_in + o0 + 4 * e4);
+                const f4 h = mreg[u];
+                const f4 d = *(const f4*)(s_din + 4 * e4);
+                f4 o;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) o[k] = h[k] > 0.f ? d[k] : 0.f;
+                *(f4*)(p.din + o0 + 4 * e4) = o;
+            }
+        }
+    }
+}
+
+// The bf16-input variant of the same computation with dz staged as bf16,
+// channels-last: slot sigma(y, x) = 10 (y + 1) + x + 1 of the zero-bordered
+// 10-wide map (rows -1 .. 10; a row's column 9 is the next row's column -1)
+// holds dz[o][y][x] for the 64 channels o, 144 bytes per slot.  The eight
+// k-values a lane feeds one v_mfma_f32_16x16x32_bf16 are then eight
+// consecutive channels at one slot: one 16-byte read at a per-lane base and
+// a compile-time tap offset, issued two k-steps ahead of its MFMA.  k-step
+// s: tap s / 2, channels 32 (s % 2) + 8g + e in element e of lane group g
+// (the weights in registers follow the same order).
+constexpr int D2C_SLOTS = 132;                 // sigma of every read: 0 .. 122
+constexpr int D2C_PSB = 144;                   // bytes per slot: 64 bf16 + 16
+constexpr int D2C_PAIRS = D2_DZ / 2;           // (channel pair, pixel) items
+constexpr int D2C_PER = (D2C_PAIRS + D2_WG - 1) / D2_WG;
+static_assert(D2C_PSB % 16 == 0 && D2C_PSB >= 2 * D2_COUT, "slot size");
+
+__global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
+    __shared__ __align__(16) unsigned char s_cl[D2C_SLOTS * D2C_PSB];
+    __shared__ __align__(16) float s_din[D2_IN];
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int ph = wave >> 1, nt = wave & 1;   // phase; N-tile
+    const int py = ph >> 1, px = ph & 1;
+
+    for (int e = t; e < D2C_SLOTS * D2C_PSB / 16; e += D2_WG) ((uint4*)s_cl)[e] = uint4{0u, 0u, 0u, 0u};
+
+    const int j_lo = blockIdx.x * p.spg;
+    const int j_hi = min(p.n, j_lo + p.spg);
+    if (j_lo >= j_hi) return;  // uniform
+
+    constexpr int KS = D2_KT / 32;
+    const int c = nt * 16 + li;
+    bf16x8 wreg[KS];
+    {
+        const float* wc = p.w + (size_t)c * D2_K * D2_K + py * D2_K + px;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int o = 32 * (s % 2) + 8 * g + e;
+                wreg[s][e] = (__bf16)wc[(size_t)o * D2_CIN * D2_K * D2_K + 2 * ty * D2_K + 2 * tx];
+            }
+        }
+    }
+    // byte base of each M-tile's slot for this lane: phase pixel m = 16 mt + li
+    int base[D2_MT];
+#pragma unroll
+    for (int i = 0; i < D2_MT; ++i) {
+        const int m = i * 16 + li, qy = m / D2_Q, qx = m - qy * D2_Q;
+        base[i] = (D2_Q * (qy + 1) + qx + 1) * D2C_PSB + 16 * g;
+    }
+
+    float va[D2C_PER], vb[D2C_PER];
+    auto fetch = [&](int j) {
+        const float* src = p.dz + (size_t)j * D2_DZ;
+#pragma unroll
+        for (int u = 0; u < D2C_PER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < D2C_PAIRS) {
+                const int op = q2 / (D2_OH * D2_OH), q = q2 - op * (D2_OH * D2_OH);
+                va[u] = src[(2 * op) * D2_OH * D2_OH + q];
+                vb[u] = src[(2 * op + 1) * D2_OH * D2_OH + q];
+            }
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < D2C_PER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < D2C_PAIRS) {
+                const int op = q2 / (D2_OH * D2_OH), q = q2 - op * (D2_OH * D2_OH);
+                const int oy = q / D2_OH, ox = q - oy * D2_OH;
+                const uint32_t lo = __builtin_bit_cast(unsigned short, (__bf16)va[u]);
+                const uint32_t hi = __builtin_bit_cast(unsigned short, (__bf16)vb[u]);
+                *(uint32_t*)(s_cl + (D2_Q * (oy + 1) + ox + 1) * D2C_PSB + 4 * op) = lo | (hi << 16);
+            }
+        }
+    };
+
+    fetch(j_lo);
+    for (int j = j_lo; j < j_hi; ++j) {
+        __syncthreads();  // the zero fill, or the previous round's LDS reads, are done
+        stage();
+        __syncthreads();
+        if (j + 1 < j_hi) fetch(j + 1);  // in flight during this sample's MFMAs
+        // this sample's ReLU mask, for the write-out below
+        const size_t o0 = (size_t)j * D2_IN;
+        f4 mreg[D2_OUT4];
+#pragma unroll
+        for (int u = 0; u < D2_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D2_IN / 4) mreg[u] = *(const f4*)(p.h_in + o0 + 4 * e4);
+        }
+
+        f4 acc[D2_MT];
+#pragma unroll
+        for (int i = 0; i < D2_MT; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        constexpr int AHEAD = 2;
+        auto a_at = [&](int s, int i) {
+            const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
+            return *(const bf16x8*)(s_cl + base[i] - (D2_Q * ty + tx) * D2C_PSB + 64 * (s % 2));
+        };
+        bf16x8 abuf[AHEAD + 1][D2_MT];
+#pragma unroll
+        for (int d = 0; d < AHEAD; ++d)
+#pragma unroll
+            for (int i = 0; i < D2_MT; ++i) abuf[d][i] = a_at(d, i);
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            if (s + AHEAD < KS) {
+#pragma unroll
+                for (int i = 0; i < D2_MT; ++i) abuf[(s + AHEAD) % (AHEAD + 1)][i] = a_at(s + AHEAD, i);
+            }
+#pragma unroll
+            for (int i = 0; i < D2_MT; ++i) acc[i] = mfma16x16x32bf16(abuf[s % (AHEAD + 1)][i], wreg[s], acc[i]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+
+#pragma unroll
+        for (int i = 0; i < D2_MT; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = i * 16 + 4 * g + r;
+                if (m < D2_QP) {
+                    const int qy = m / D2_Q, qx = m - qy * D2_Q;
+                    s_din[c * D2_IH * D2_IH + (2 * qy + py) * D2_IH + 2 * qx + px] = acc[i][r];
+                }
+            }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < D2_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D2_IN / 4) {
+                const f4 h = mreg[u];
                 const f4 d = *(const f4*)(s_din + 4 * e4);
                 f4 o;
 #pragma unroll
@@ -404,9 +521,9 @@ hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float
     const int blocks = (n + spg - 1) / spg;
     const Dgrad2Params prm{dz, w, h_in, din, n, spg};
     if (bf16)
-        hipLaunchKernelGGL(conv2_dgrad_phase_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+        hipLaunchKernelGGL(conv2_dgrad_cl_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else
-        hipLaunchKernelGGL(conv2_dgrad_phase_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+        hipLaunchKernelGGL(conv2_dgrad_phase_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     return hipGetLastError();
 }
 
