@@ -357,7 +357,6 @@ constexpr int D3_OUT4 = (D3_IN / 4 + D2_WG - 1) / D2_WG;
 static_assert(D3_CS >= (D3_OH + 4) * D3_IH && D3_CS % 64 == 48, "channel stride: border and banks");
 static_assert(D3_MT % 2 == 0 && D3_IN % 4 == 0, "tile split and float4 rows");
 
-template <bool BF16>
 __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
     __shared__ float s_dz[D3_STAGE];
     __shared__ __align__(16) float s_din[D3_IN];
@@ -374,24 +373,14 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
 
     // B operands for every k-step: k = tap * 64 + o, tap = 3ky + kx.
     const int c = nt * 16 + li;
-    constexpr int KS = BF16 ? D3_KT / 32 : D3_KT / 4;
-    using BOp = typename std::conditional<BF16, bf16x8, float>::type;
-    BOp wreg[KS];
+    constexpr int KS = D3_KT / 4;
+    float wreg[KS];
     {
         const float* wc = p.w + (size_t)c * D3_K * D3_K;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-            if constexpr (BF16) {
-                const int tap = s / 2;   // o = 32 * (s % 2) + 4e + g
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int o = 32 * (s % 2) + 4 * e + g;
-                    wreg[s][e] = (__bf16)wc[(size_t)o * D3_CIN * D3_K * D3_K + tap];
-                }
-            } else {
-                const int tap = s / 16, o = 4 * (s % 16) + g;
-                wreg[s] = wc[(size_t)o * D3_CIN * D3_K * D3_K + tap];
-            }
+            const int tap = s / 16, o = 4 * (s % 16) + g;
+            wreg[s] = wc[(size_t)o * D3_CIN * D3_K * D3_K + tap];
         }
     }
 
@@ -427,33 +416,19 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
         stage();
         __syncthreads();
         if (j + 1 < j_hi) fetch(j + 1);
+        // this sample's ReLU mask, for the write-out below
+        const size_t o0 = (size_t)j * D3_IN;
+        f4 mreg[D3_OUT4];
+#pragma unroll
+        for (int u = 0; u < D3_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D3_IN / 4) mreg[u] = *(const f4*)(p.h_in + o0 + 4 * e4);
+        }
 
         f4 acc[D3_TPW];
 #pragma unroll
         for (int i = 0; i < D3_TPW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
-        if constexpr (BF16) {
-            auto load = [&](int s, bf16x8 (&a)[D3_TPW]) {
-                const int tap = s / 2, ky = tap / 3, kx = tap % 3;
-                const int off = 32 * (s % 2) * D3_CS - D3_IH * ky - kx;
-#pragma unroll
-                for (int i = 0; i < D3_TPW; ++i) {
-                    const float* ap = s_dz + base[i] + off;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) a[i][e] = (__bf16)ap[4 * e * D3_CS];
-                }
-            };
-            bf16x8 a[2][D3_TPW];
-            load(0, a[0]);
-#pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                if (s + 1 < KS) load(s + 1, a[(s + 1) & 1]);
-#pragma unroll
-                for (int i = 0; i < D3_TPW; ++i) acc[i] = mfma16x16x32bf16(a[s & 1][i], wreg[s], acc[i]);
-                if (s + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 8 * D3_TPW, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, D3_TPW, 0);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        } else {
+        {
             auto load = [&](int s, float (&a)[D3_TPW]) {
                 const int tap = s / 16, ky = tap / 3, kx = tap % 3;
                 const int off = 4 * (s % 16) * D3_CS - D3_IH * ky - kx;
@@ -482,16 +457,147 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
                 if (m < D3_P) s_din[c * D3_P + m] = acc[i][r];
             }
         __syncthreads();
-        const size_t o0 = (size_t)j * D3_IN;
 #pragma unroll
         for (int u = 0; u < D3_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
             if (e4 < D3_IN / 4) {
-                const f4 h = *(const f4*)(p.h_in + o0 + 4 * e4);
+                const f4 h = mreg[u];
                 const f4 d = *(const f4*)(s_din + 4 * e4);
                 f4 o;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) o[k] = h[k] > 0.f ? d[k] : 0.f;
+                *(f4*)(p.din + o0 + 4 * e4) = o;
+            }
+        }
+    }
+}
+
+
+// The bf16-input variant with dz staged channels-last as bf16: slot
+// sigma = 9 (y + 2) + x + 2 of the zero-bordered map (two zero rows above
+// and below, columns 7 and 8 of a row zero, two lead slots) holds dz[o][y][x]
+// for the 64 channels, 144 bytes per slot; pixel m reads tap (ky, kx) at
+// slot m + 20 - 9ky - kx.  k-step s: tap s / 2, channels 32 (s % 2) + 8g + e.
+constexpr int D3C_SLOTS = 120;                 // every read: slot 0 .. 115
+constexpr int D3C_PSB = 144;
+constexpr int D3C_PAIRS = D3_DZ / 2;
+constexpr int D3C_PER = (D3C_PAIRS + D2_WG - 1) / D2_WG;
+
+__global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
+    __shared__ __align__(16) unsigned char s_cl[D3C_SLOTS * D3C_PSB];
+    __shared__ __align__(16) float s_din[D3_IN];
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int nt = wave & 3, mh = wave >> 2;   // N-tile; half of the M-tiles
+
+    for (int e = t; e < D3C_SLOTS * D3C_PSB / 16; e += D2_WG) ((uint4*)s_cl)[e] = uint4{0u, 0u, 0u, 0u};
+
+    const int j_lo = blockIdx.x * p.spg;
+    const int j_hi = min(p.n, j_lo + p.spg);
+    if (j_lo >= j_hi) return;  // uniform
+
+    constexpr int KS = D3_KT / 32;
+    const int c = nt * 16 + li;
+    bf16x8 wreg[KS];
+    {
+        const float* wc = p.w + (size_t)c * D3_K * D3_K;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            const int tap = s / 2;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int o = 32 * (s % 2) + 8 * g + e;
+                wreg[s][e] = (__bf16)wc[(size_t)o * D3_CIN * D3_K * D3_K + tap];
+            }
+        }
+    }
+    int base[D3_TPW];
+#pragma unroll
+    for (int i = 0; i < D3_TPW; ++i) base[i] = ((mh * D3_TPW + i) * 16 + li + 20) * D3C_PSB + 16 * g;
+
+    float va[D3C_PER], vb[D3C_PER];
+    auto fetch = [&](int j) {
+        const float* src = p.dz + (size_t)j * D3_DZ;
+#pragma unroll
+        for (int u = 0; u < D3C_PER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < D3C_PAIRS) {
+                const int op = q2 / (D3_OH * D3_OH), q = q2 - op * (D3_OH * D3_OH);
+                va[u] = src[(2 * op) * D3_OH * D3_OH + q];
+                vb[u] = src[(2 * op + 1) * D3_OH * D3_OH + q];
+            }
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < D3C_PER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < D3C_PAIRS) {
+                const int op = q2 / (D3_OH * D3_OH), q = q2 - op * (D3_OH * D3_OH);
+                const int oy = q / D3_OH, ox = q - oy * D3_OH;
+                const uint32_t lo = __builtin_bit_cast(unsigned short, (__bf16)va[u]);
+                const uint32_t hi = __builtin_bit_cast(unsigned short, (__bf16)vb[u]);
+                *(uint32_t*)(s_cl + (D3_IH * (oy + 2) + ox + 2) * D3C_PSB + 4 * op) = lo | (hi << 16);
+            }
+        }
+    };
+
+    fetch(j_lo);
+    for (int j = j_lo; j < j_hi; ++j) {
+        __syncthreads();
+        stage();
+        __syncthreads();
+        if (j + 1 < j_hi) fetch(j + 1);
+        const size_t o0 = (size_t)j * D3_IN;
+        f4 mreg[D3_OUT4];
+#pragma unroll
+        for (int u = 0; u < D3_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D3_IN / 4) mreg[u] = *(const f4*)(p.h_in + o0 + 4 * e4);
+        }
+
+        f4 acc[D3_TPW];
+#pragma unroll
+        for (int i = 0; i < D3_TPW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        constexpr int AHEAD = 2;
+        auto a_at = [&](int s, int i) {
+            const int tap = s / 2, ky = tap / 3, kx = tap % 3;
+            return *(const bf16x8*)(s_cl + base[i] - (D3_IH * ky + kx) * D3C_PSB + 64 * (s % 2));
+        };
+        bf16x8 abuf[AHEAD + 1][D3_TPW];
+#pragma unroll
+        for (int d = 0; d < AHEAD; ++d)
+#pragma unroll
+            for (int i = 0; i < D3_TPW; ++i) abuf[d][i] = a_at(d, i);
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            if (s + AHEAD < KS) {
+#pragma unroll
+                for (int i = 0; i < D3_TPW; ++i) abuf[(s + AHEAD) % (AHEAD + 1)][i] = a_at(s + AHEAD, i);
+            }
+#pragma unroll
+            for (int i = 0; i < D3_TPW; ++i) acc[i] = mfma16x16x32bf16(abuf[s % (AHEAD + 1)][i], wreg[s], acc[i]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+
+#pragma unroll
+        for (int i = 0; i < D3_TPW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = (mh * D3_TPW + i) * 16 + 4 * g + r;
+                if (m < D3_P) s_din[c * D3_P + m] = acc[i][r];
+            }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < D3_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D3_IN / 4) {
+                const f4 h = mreg[u];
+                const f4 d = *(const f4*)(s_din + 4 * e4);
+                f4 o;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) o[q] = h[q] > 0.f ? d[q] : 0.f;
                 *(f4*)(p.din + o0 + 4 * e4) = o;
             }
         }
@@ -507,9 +613,9 @@ hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in
     const int blocks = (n + spg - 1) / spg;
     const Dgrad2Params prm{dz, w, h_in, din, n, spg};
     if (bf16)
-        hipLaunchKernelGGL(conv3_dgrad_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+        hipLaunchKernelGGL(conv3_dgrad_cl_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else
-        hipLaunchKernelGGL(conv3_dgrad_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+        hipLaunchKernelGGL(conv3_dgrad_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     return hipGetLastError();
 }
 
