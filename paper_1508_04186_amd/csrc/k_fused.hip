@@ -829,8 +829,9 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
     if (n <= 0 || n_a < 0 || n_a > n || !conv_s12_fwd_aligned(in_a) || !conv_s12_fwd_aligned(in_b) ||
         ((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15))
         return hipErrorInvalidValue;
-    // about 256 workgroups: a few samples each, so the weight split is amortized
-    const int spb = std::max(1, (n + 255) / 256);
+    // about 512 workgroups (two per compute unit, so one's loads overlap the
+    // other's MFMAs): a few samples each, so the weight split is amortized
+    const int spb = std::max(1, (n + 511) / 512);
     const int blocks_a = (n_a + spb - 1) / spb, blocks_b = (n - n_a + spb - 1) / spb;
     U8FwdParams prm{in_a, in_b, n_a, n, spb, blocks_a, w_a, b_a, w_b, b_b, out, side ? *side : SideFields{}};
     const dim3 grid((unsigned)std::max(1, blocks_a + blocks_b));
