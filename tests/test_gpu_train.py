@@ -79,16 +79,18 @@ def test_train_steps_resumes_across_calls(dev, small_replay):
     assert torch.equal(a, b) and torch.equal(ta, tb)
 
 
+@pytest.mark.parametrize("B", [32, 300])
 @pytest.mark.parametrize("rule,lr,decay,eps", [("sgd", 1e-2, 0.9, 0.0), ("rmsprop", 1e-3, 0.9, 0.0),
                                                ("adagrad", 1e-3, 0.0, 1e-8)])
-def test_train_steps_fused_update_is_bitwise_two_calls(dev, small_replay, rule, lr, decay, eps):
+def test_train_steps_fused_update_is_bitwise_two_calls(dev, small_replay, rule, lr, decay, eps, B):
     """The update fused into each step's last kernel equals, bit for bit,
     dqn_td_gradient_replay followed by ps_apply_update (target refresh
-    every 3 steps, so both theta and theta^- paths run)."""
+    every 3 steps, so both theta and theta^- paths run); batch 300 runs the
+    reductions for batches above 128."""
     import torch
     _, rp = small_replay
     net = dq.NET_SMALL
-    N, B, C = 7, 32, 3
+    N, C = 7, 3
     idx = dev_tensor(di.index_stream(N, B, rp.size, 50))
     th0 = dev_tensor(di.xavier_theta(di.NET_S, 51))
     a, ta = th0.clone(), torch.empty_like(th0)
@@ -97,7 +99,7 @@ def test_train_steps_fused_update_is_bitwise_two_calls(dev, small_replay, rule, 
     sb = None if sa is None else sa.clone()
     la = torch.empty(N, dtype=torch.float32, device=dev)
     lb = torch.empty(N, dtype=torch.float32, device=dev)
-    say(f"[train] fused vs two calls, rule={rule}")
+    say(f"[train] fused vs two calls, rule={rule} batch={B}")
     dq.dqn_train_steps(net, a, ta, sa, rule, lr, decay, eps, 0.99, rp, idx, target_period=C,
                        losses_out=la)
     g = torch.empty_like(th0)
