@@ -188,13 +188,14 @@ hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, con
                                  const float* b_a, const float* w_b, const float* b_b, float* out,
                                  bool bf16, hipStream_t st);
 
-// The bf16-input forward of CONV_L2 / CONV_L3 from kFwdClMinRows samples on:
-// weights held in registers, each sample staged channels-last in LDS (same
-// arguments and result as launch_conv_igemm_fwd, which routes to it).
+// The forward of CONV_L2 / CONV_L3 from kFwdClMinRows samples on, both
+// precisions: weights held in registers, each sample staged channels-last in
+// LDS (same arguments and result as launch_conv_igemm_fwd, which routes to
+// it).
 constexpr int kFwdClMinRows = 256;
 bool conv_fwd_cl_use(ConvId id, int n, bool bf16);
 hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const float* w_a, const float* b_a,
-                              const float* w_b, const float* b_b, float* out, hipStream_t st);
+                              const float* w_b, const float* b_b, float* out, bool bf16, hipStream_t st);
 
 // Input gradient of CONV_L2 / CONV_L3 for n samples as an implicit GEMM per
 // stride phase, masked by [h_in > 0] (as launch_conv_dgrad).

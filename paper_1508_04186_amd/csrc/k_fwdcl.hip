@@ -226,17 +226,168 @@ hipError_t fwd_cl_launch(const float* in, int n_a, int n, const float* w_a, cons
     return hipGetLastError();
 }
 
+// The fp32 variant: v_mfma_f32_16x16x4_f32, weights held in registers as
+// fp32 (wave (nt, mh): 16 output channels, KT/4 registers), each sample's
+// input staged in LDS as fp32, channels-last (pixel stride CIN + 4 floats).
+// Per tap the channels go in blocks of 16, four k-steps per block: at k-step
+// i of block b lane group g supplies channel 16b + 4g + i, so one 16-byte
+// LDS read gives a lane its A values for four consecutive k-steps.  Weights
+// are read straight from global memory into registers (each lane's channels
+// are runs of k*k consecutive taps).
+template <int CIN, int IH, int K, int S, int OH>
+struct FwdCl32Geom {
+    static constexpr int COUT = 64;
+    static constexpr int P = OH * OH;
+    static constexpr int MT = (P + 15) / 16;
+    static constexpr int MPW = MT / 2;
+    static constexpr int KK = K * K;
+    static constexpr int CB = CIN / 16;                 // channel blocks per tap
+    static constexpr int KS = KK * CB * 4;              // fp32 k-steps
+    static constexpr int IP = IH * IH;
+    static constexpr int PSF = CIN + 4;                 // LDS floats per staged pixel
+    static constexpr int IN = CIN * IP;
+    static constexpr int PER = (IN + FC_WG - 1) / FC_WG;
+    static constexpr int OUTF = COUT * P;
+    static constexpr int LDS = IP * PSF * 4 + OUTF * 4;
+    static_assert(MT % 2 == 0 && CIN % 16 == 0 && (PSF * 4) % 16 == 0 && OUTF % 4 == 0, "geometry");
+};
+
+template <int CIN, int IH, int K, int S, int OH>
+__global__ __launch_bounds__(FC_WG) void conv_fwd_cl32_kernel(FwdClParams p) {
+    using G = FwdCl32Geom<CIN, IH, K, S, OH>;
+    extern __shared__ __align__(16) float smem32[];
+    float* s_in = smem32;                                  // [IP][PSF]
+    float* s_out = smem32 + G::IP * G::PSF;                // [64][P]
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int nt = wave & 3, mh = wave >> 2;
+
+    const bool second = (int)blockIdx.x >= p.g_a;
+    const int blk = second ? (int)blockIdx.x - p.g_a : (int)blockIdx.x;
+    const int first = second ? p.n_a : 0;
+    const int end = second ? p.n : p.n_a;
+    const int j_lo = first + blk * p.spg;
+    const int j_hi = min(end, j_lo + p.spg);
+    if (j_lo >= j_hi) return;  // whole workgroup
+    const float* __restrict__ W = second ? p.w_b : p.w_a;
+    const float* __restrict__ bias = second ? p.b_b : p.b_a;
+
+    float v[G::PER];
+    auto fetch = [&](int j) {
+        const float* x = p.in + (size_t)j * G::IN;
+#pragma unroll
+        for (int u = 0; u < G::PER; ++u) {
+            const int e = t + u * FC_WG;
+            if (e < G::IN) v[u] = x[e];
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < G::PER; ++u) {
+            const int e = t + u * FC_WG;
+            if (e < G::IN) {
+                const int c = e / G::IP, pix = e - c * G::IP;
+                s_in[pix * G::PSF + c] = v[u];
+            }
+        }
+    };
+    fetch(j_lo);
+
+    // k-step s = (tap, block b, i): lane (li, g) holds W[16nt + li][16b + 4g + i][tap]
+    float wv[G::KS];
+    {
+        const float* wr = W + (size_t)(16 * nt + li) * CIN * G::KK;
+#pragma unroll
+        for (int tap = 0; tap < G::KK; ++tap)
+#pragma unroll
+            for (int b = 0; b < G::CB; ++b)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    wv[(tap * G::CB + b) * 4 + i] = wr[(16 * b + 4 * g + i) * G::KK + tap];
+    }
+    const float bo = bias[16 * nt + li];
+
+    // float offset in s_in of the lane's first pixel for each M-tile, plus its channel group
+    int pb[G::MPW];
+#pragma unroll
+    for (int i = 0; i < G::MPW; ++i) {
+        const int pp = 16 * (mh * G::MPW + i) + li;
+        const int pc = pp < G::P ? pp : 0;
+        const int oy = pc / OH, ox = pc - oy * OH;
+        pb[i] = ((S * oy) * IH + S * ox) * G::PSF + 4 * g;
+    }
+
+    for (int j = j_lo; j < j_hi; ++j) {
+        __syncthreads();  // the previous sample's reads of s_in / s_out are done
+        stage();
+        __syncthreads();
+        if (j + 1 < j_hi) fetch(j + 1);
+        f4 acc[G::MPW];
+#pragma unroll
+        for (int i = 0; i < G::MPW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        // one 16-byte read per (tap, block) and M-tile, a (tap, block) ahead
+        constexpr int NB = G::KK * G::CB;
+        auto a_at = [&](int q, int i) {
+            const int tap = q / G::CB, b = q % G::CB;
+            return *(const f4*)(s_in + pb[i] + ((tap / K) * IH + tap % K) * G::PSF + 16 * b);
+        };
+        f4 abuf[2][G::MPW];
+#pragma unroll
+        for (int i = 0; i < G::MPW; ++i) abuf[0][i] = a_at(0, i);
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+            if (q + 1 < NB) {
+#pragma unroll
+                for (int i = 0; i < G::MPW; ++i) abuf[(q + 1) & 1][i] = a_at(q + 1, i);
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int i = 0; i < G::MPW; ++i) acc[i] = mfma16x16x4(abuf[q & 1][i][k], wv[q * 4 + k], acc[i]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int i = 0; i < G::MPW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int pp = 16 * (mh * G::MPW + i) + 4 * g + r;
+                if (pp < G::P) s_out[(16 * nt + li) * G::P + pp] = fmaxf(acc[i][r] + bo, 0.f);
+            }
+        __syncthreads();
+        f4* dst = (f4*)(p.out + (size_t)j * G::OUTF);
+        for (int q = t; q < G::OUTF / 4; q += FC_WG) dst[q] = ((const f4*)s_out)[q];
+    }
+}
+
+template <int CIN, int IH, int K, int S, int OH>
+hipError_t fwd_cl32_launch(const float* in, int n_a, int n, const float* w_a, const float* b_a, const float* w_b,
+                           const float* b_b, float* out, hipStream_t st) {
+    using G = FwdCl32Geom<CIN, IH, K, S, OH>;
+    if (n <= 0 || n_a < 0 || n_a > n || ((uintptr_t)out & 15)) return hipErrorInvalidValue;
+    const int spg = std::max(1, (n + FC_TARGET_BLOCKS - 1) / FC_TARGET_BLOCKS);
+    const int g_a = (n_a + spg - 1) / spg, g_b = (n - n_a + spg - 1) / spg;
+    const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg};
+    auto kern = conv_fwd_cl32_kernel<CIN, IH, K, S, OH>;
+    if (!allow_lds((const void*)kern, G::LDS)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(g_a + g_b)), dim3(FC_WG), G::LDS, st, prm);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 bool conv_fwd_cl_use(ConvId id, int n, bool bf16) {
-    return bf16 && (id == CONV_L2 || id == CONV_L3) && n >= kFwdClMinRows;
+    return (id == CONV_L2 || id == CONV_L3) && n >= kFwdClMinRows;
 }
 
 hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const float* w_a, const float* b_a,
-                              const float* w_b, const float* b_b, float* out, hipStream_t st) {
+                              const float* w_b, const float* b_b, float* out, bool bf16, hipStream_t st) {
     switch (id) {
-        case CONV_L2: return fwd_cl_launch<32, 20, 4, 2, 9, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
-        case CONV_L3: return fwd_cl_launch<64, 9, 3, 1, 7, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
+        case CONV_L2:
+            return bf16 ? fwd_cl_launch<32, 20, 4, 2, 9, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, st)
+                        : fwd_cl32_launch<32, 20, 4, 2, 9>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
+        case CONV_L3:
+            return bf16 ? fwd_cl_launch<64, 9, 3, 1, 7, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, st)
+                        : fwd_cl32_launch<64, 9, 3, 1, 7>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
         default: return hipErrorInvalidValue;
     }
 }
