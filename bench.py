@@ -483,8 +483,8 @@ def bench_sequential(args):
     t0 = time.time()
     log(f"replay: generating {SIZE} transitions (seed {SEED})")
     hr = di.host_replay(SIZE, shape.n_actions, SEED)
-    rec, ra, rr, rt = di.device_replay(SIZE, shape.n_actions, SEED, device=dev, host=hr)
-    rp = dq.Replay(rec, ra, rr, rt, SIZE)
+    rp = _filled_replay(dev, SIZE, shape.n_actions, SEED)
+    rec = rp.frames
     log(f"replay ready in {time.time() - t0:.1f}s ({rec.numel() / 2**30:.2f} GiB on device)")
     th0 = di.xavier_theta(shape, SEED)
     idx_host = di.index_stream(total, B, SIZE, SEED)
@@ -785,9 +785,7 @@ def bench_replica_sweep(args):
     SIZE, SEED, LR, EPS, GAMMA = 100_000, 1002, 0.01, 1e-8, 0.99
     U = args.steps or 1000
     log(f"replay: generating {SIZE} transitions (seed {SEED})")
-    hr = di.host_replay(SIZE, shape.n_actions, SEED)
-    rec, ra, rr, rt = di.device_replay(SIZE, shape.n_actions, SEED, device=dev, host=hr)
-    rp = dq.Replay(rec, ra, rr, rt, SIZE)
+    rp = _filled_replay(dev, SIZE, shape.n_actions, SEED)
     th0 = torch.from_numpy(di.xavier_theta(shape, SEED)).to(dev)
     P = dq.dqn_param_count(net)
     RS = dq.dqn_train_ring_stride(net)
@@ -867,8 +865,7 @@ def bench_replicas(args):
     W = args.warmup if args.warmup is not None else 100
     log(f"replay: generating {SIZE} transitions (seed {SEED})")
     hr = di.host_replay(SIZE, shape.n_actions, SEED)
-    rec, ra, rr, rt = di.device_replay(SIZE, shape.n_actions, SEED, device=dev, host=hr)
-    rp = dq.Replay(rec, ra, rr, rt, SIZE)
+    rp = _filled_replay(dev, SIZE, shape.n_actions, SEED)
     th0 = di.xavier_theta(shape, SEED)
     idx_host = di.index_stream(U, B, SIZE, SEED)
     idx = torch.from_numpy(idx_host).to(dev)
@@ -972,14 +969,30 @@ def bench_replicas(args):
 # ---------------------------------------------------------------------------
 # configs 3, 4a and 4b (large network, 1,000,000-transition replay)
 
+def _filled_replay(dev, size, n_actions, seed):
+    """Device replay of `size` stacked 4 x 84 x 84 records and side arrays,
+    written on the device by replay_fill_synthetic (the same bytes as the
+    host generator dqn_inputs.host_replay)."""
+    import torch
+    import paper_1508_04186_amd as dq
+    rec = torch.empty((size, 4, 84, 84), dtype=torch.uint8, device=dev)
+    a = torch.empty(size, dtype=torch.uint8, device=dev)
+    r = torch.empty(size, dtype=torch.int8, device=dev)
+    t = torch.empty(size, dtype=torch.uint8, device=dev)
+    rp = dq.Replay(rec, a, r, t, size)
+    dq.replay_fill_synthetic(rp, n_actions, seed)
+    torch.cuda.synchronize()
+    return rp
+
+
 def _large_replay(dev, size, seed):
     import dqn_inputs as di
     import paper_1508_04186_amd as dq
     t0 = time.time()
     log(f"replay: generating {size} transitions (seed {seed}) into device memory")
-    rec, ra, rr, rt = di.device_replay(size, di.NET_L.n_actions, seed, device=dev)
-    log(f"replay ready in {time.time() - t0:.1f}s ({rec.numel() / 2**30:.2f} GiB on device)")
-    return dq.Replay(rec, ra, rr, rt, size)
+    rp = _filled_replay(dev, size, di.NET_L.n_actions, seed)
+    log(f"replay ready in {time.time() - t0:.1f}s ({rp.frames.numel() / 2**30:.2f} GiB on device)")
+    return rp
 
 
 def bench_large(args):

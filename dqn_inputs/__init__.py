@@ -138,6 +138,16 @@ def side_arrays(size: int, n_actions: int, seed: int, p_terminal=0.01):
     return a, r, t
 
 
+def side_arrays_hashed(size: int, n_actions: int, seed: int):
+    """The hashed side arrays of the seeded stream (action uint8, reward int8,
+    terminal uint8 [size]): the ones replay_fill_synthetic writes."""
+    a = np.empty(size, np.uint8)
+    r = np.empty(size, np.int8)
+    t = np.empty(size, np.uint8)
+    _lib().synth_side(seed, n_actions, 0, size, a.ctypes.data, r.ctypes.data, t.ctypes.data)
+    return a, r, t
+
+
 def index_stream(steps: int, batch: int, size: int, seed: int) -> np.ndarray:
     """int64 [steps][batch], uniform with replacement on [0, size-2]: valid
     transitions i need record i+1 for the next state."""
@@ -224,6 +234,9 @@ def _lib():
         lib = ctypes.CDLL(path)
         lib.synth_frames.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
         lib.synth_frames.restype = None
+        lib.synth_side.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64, ctypes.c_int64,
+                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        lib.synth_side.restype = None
         lib.synth_hash.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64]
         lib.synth_hash.restype = ctypes.c_uint64
         _LIB = lib
@@ -275,7 +288,7 @@ class HostReplay:
 
 def host_replay(size: int, n_actions: int, seed: int, c: int = 4) -> HostReplay:
     fr = frames(seed, 0, size + c - 1)
-    a, r, t = side_arrays(size, n_actions, seed)
+    a, r, t = side_arrays_hashed(size, n_actions, seed)
     return HostReplay(fr, a, r, t, size, c)
 
 
@@ -301,7 +314,7 @@ def device_replay(size: int, n_actions: int, seed: int, device="cuda", c: int = 
     if host is not None:
         a, r, t = host.action, host.reward, host.terminal
     else:
-        a, r, t = side_arrays(size, n_actions, seed)
+        a, r, t = side_arrays_hashed(size, n_actions, seed)
     torch.cuda.synchronize()
     return (rec, torch.from_numpy(a).to(device), torch.from_numpy(r).to(device),
             torch.from_numpy(t).to(device))
@@ -321,5 +334,5 @@ def transitions_at(seed: int, idx, n_actions: int, size: int, c: int = 4):
         frames(seed, int(i), c + 1, buf)
         s[j] = buf[:c]
         sn[j] = buf[1:]
-    a, r, t = side_arrays(size, n_actions, seed)
+    a, r, t = side_arrays_hashed(size, n_actions, seed)
     return s, sn, a[idx].astype(np.int32), r[idx].astype(np.float32), t[idx].astype(np.uint8)

@@ -15,6 +15,9 @@
  * output mix (Steele, Lea and Flood, "Fast splittable pseudorandom number
  * generators", OOPSLA 2014) applied to seed + golden_gamma * counter.
  *
+ * synth_side gives hashed side fields (action, reward, terminal) for the
+ * same stream, the ones a device-filled replay holds.
+ *
  * Build: gcc -O2 -fopenmp -shared -fPIC frames.c -o libframes.so
  */
 #include <stdint.h>
@@ -24,6 +27,10 @@
 #define SEGMENT 100
 #define STREAM_RECT 1ull
 #define STREAM_NOISE 2ull
+#define STREAM_ACT 3ull
+#define STREAM_REW 4ull
+#define STREAM_TERM 5ull
+#define TERM_BELOW 42949672ull   /* floor(0.01 * 2^32): P(terminal) = 0.01 */
 
 static inline uint64_t mix64(uint64_t z) {
     z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
@@ -99,4 +106,18 @@ void synth_frames(uint64_t seed, int64_t t0, int64_t count, uint8_t* out) {
     #pragma omp parallel for schedule(static)
     for (int64_t k = 0; k < count; ++k)
         one_frame(seed, t0 + k, out + k * (int64_t)(FRAME_H * FRAME_W));
+}
+
+/* Hashed side fields of records i0 .. i0+count-1: action bounded(H(ACT, i),
+ * n_actions), reward bounded(H(REW, i), 3) - 1, terminal iff the top 32
+ * bits of H(TERM, i) are below TERM_BELOW. */
+void synth_side(uint64_t seed, uint32_t n_actions, int64_t i0, int64_t count, uint8_t* action, int8_t* reward,
+                uint8_t* terminal) {
+    #pragma omp parallel for schedule(static)
+    for (int64_t k = 0; k < count; ++k) {
+        const uint64_t i = (uint64_t)(i0 + k);
+        action[k] = (uint8_t)bounded(synth_hash(seed, STREAM_ACT, i), n_actions);
+        reward[k] = (int8_t)((int)bounded(synth_hash(seed, STREAM_REW, i), 3) - 1);
+        terminal[k] = (synth_hash(seed, STREAM_TERM, i) >> 32) < TERM_BELOW ? 1 : 0;
+    }
 }

@@ -125,6 +125,21 @@ int replay_gather(const dqn_replay* replay, const int64_t* idx, int32_t batch,
                   uint8_t* s_out, uint8_t* s_next_out, int32_t* a_out, float* r_out,
                   uint8_t* term_out, void* stream);
 
+/* Setup, not part of the method: fills the replay memory that `replay`
+ * describes (records 0 .. size-1 and the side arrays; the call writes through
+ * its pointers) with a seeded synthetic stream standing in for preprocessed
+ * game frames (Sec. III.A).  Record i stacks stream frames i .. i+c-1; a frame
+ * is 84 x 84 bytes: noise uniform on 0..8 under one to four bright moving
+ * rectangles (a fresh set every 100 frames).  Every byte and side field is a
+ * pure function of (seed, frame, pixel) or (seed, record) through
+ * SplitMix64's output mix of seed + 0x9E3779B97F4A7C15 * ((stream << 40) |
+ * counter); side fields: action = bounded(H(3, i), n_actions), reward =
+ * bounded(H(4, i), 3) - 1, terminal iff (H(5, i) >> 32) < floor(0.01 * 2^32),
+ * with bounded(h, n) = ((h >> 32) * n) >> 32.  Requires h = w = 84, c >= 1,
+ * n_actions in 1..256, the frames pointer 16-byte aligned and record_stride a
+ * multiple of 16 of at least c*84*84. */
+int replay_fill_synthetic(const dqn_replay* replay, int32_t n_actions, uint64_t seed, void* stream);
+
 /* Q-network forward pass and epsilon-greedy action choice (Sec. II.A,
  * Sec. III.A-B; Alg. 1 "select action").
  * states: uint8 [batch][4][84][84]; theta: flat parameters.

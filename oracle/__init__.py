@@ -266,16 +266,18 @@ def sequential_training(net, theta0, rep, idx_stream, gamma, lr, rule="sgd", dec
 
 
 def stale_replica_training(net, theta0, rep, idx_stream, gamma, lr, staleness, rule="adagrad",
-                           decay=0.9, eps=1e-8, updates=None, callback=None):
+                           decay=0.9, eps=1e-8, updates=None, callback=None, state0=None):
     """Asynchronous workers with bounded staleness, replayed deterministically
     (Sec. IV.A, Alg. 2): update u is a gradient computed on the parameter
     version v(u) = max(0, u - staleness), which also serves as that worker's
     target network; the server applies updates in order u = 0, 1, ...,
     producing version u + 1.  Which replica computed update u does not
-    change the arithmetic.  Returns (theta, state, losses)."""
+    change the arithmetic.  state0 is the optimizer state before update 0
+    (zero when None).  Returns (theta, state, losses)."""
     updates = idx_stream.shape[0] if updates is None else updates
     versions = [np.array(theta0, dtype=np.float32, copy=True)]
-    state = None if rule == "sgd" else np.zeros_like(versions[0])
+    state = None if rule == "sgd" else (np.zeros_like(versions[0]) if state0 is None
+                                        else np.array(state0, dtype=np.float32, copy=True))
     losses = []
     for u in range(updates):
         v = max(0, u - staleness)

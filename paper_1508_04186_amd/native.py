@@ -150,6 +150,8 @@ def lib():
         L.dqn_act.argtypes = [ctypes.POINTER(_CNet), _P, _P, ctypes.c_int32, _P, ctypes.c_float, _P, _P, _P,
                               _P, _P, ctypes.POINTER(_CReplayOut), ctypes.c_int64, _P, ctypes.c_size_t, _P]
         L.dqn_act.restype = ctypes.c_int
+        L.replay_fill_synthetic.argtypes = [ctypes.POINTER(_CReplay), ctypes.c_int32, ctypes.c_uint64, _P]
+        L.replay_fill_synthetic.restype = ctypes.c_int
         L.dqn_preprocess.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                      ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int64, _P]
         L.dqn_preprocess.restype = ctypes.c_int
@@ -637,3 +639,9 @@ def dqn_observe(rgb, top: int, left: int, factor: int, states, actions=None, rew
                              _ptr(actions, torch.int32, "actions"), _ptr(rewards, torch.int8, "rewards"),
                              _ptr(terminal, torch.uint8, "terminal"), _ptr(states, torch.uint8, "states"),
                              ctypes.byref(rp) if rp else None, int(t), _stream(stream)), "dqn_observe")
+
+
+def replay_fill_synthetic(replay: "Replay", n_actions: int, seed: int, stream=None) -> None:
+    """Fill a replay memory with the seeded synthetic stream (include/dqn.h)."""
+    _check(lib().replay_fill_synthetic(ctypes.byref(_creplay(replay)), int(n_actions), int(seed) & (2**64 - 1),
+                                       _stream(stream)), "replay_fill_synthetic")

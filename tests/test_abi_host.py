@@ -189,6 +189,33 @@ def test_gather_argument_errors():
 
 
 @fake_ptr_test
+def test_fill_argument_errors():
+    L = dq.lib()
+    rp = native._CReplay()
+    rp.frames, rp.action, rp.reward, rp.terminal = FAKE, FAKE, FAKE, FAKE
+    rp.record_stride, rp.size, rp.c, rp.h, rp.w = 28224, 100, 4, 84, 84
+
+    def call(n_actions=6, **kw):
+        for k, v in kw.items():
+            setattr(rp, k, v)
+        return L.replay_fill_synthetic(ctypes.byref(rp), n_actions, 7, None)
+    assert call(n_actions=0) == dq.DQN_EINVAL
+    assert call(n_actions=257) == dq.DQN_EINVAL
+    assert call(frames=FAKE + 4) == dq.DQN_EINVAL             # frames not 16-byte aligned
+    rp.frames = FAKE
+    assert call(record_stride=28224 + 8) == dq.DQN_EINVAL     # stride not a multiple of 16
+    assert call(record_stride=28224 - 16) == dq.DQN_EINVAL    # stride below c frames
+    rp.record_stride = 28224
+    assert call(size=0) == dq.DQN_EINVAL
+    rp.size = 100
+    assert call(h=80, w=80) == dq.DQN_EINVAL                  # the stream's frames are 84 x 84
+    rp.h, rp.w = 84, 84
+    assert call(c=0) == dq.DQN_EINVAL
+    rp.c = 4
+    assert call(terminal=None) == dq.DQN_EINVAL
+
+
+@fake_ptr_test
 def test_apply_argument_errors():
     L = dq.lib()
 

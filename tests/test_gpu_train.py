@@ -10,7 +10,7 @@ import pytest
 import dqn_inputs as di
 import oracle
 import paper_1508_04186_amd as dq
-from gpu_util import FP32_TOL, assert_grad_close, dev_tensor, host, rel_l2, say
+from gpu_util import FP32_TOL, assert_grad_close, dev_tensor, host, say
 
 pytestmark = pytest.mark.gpu
 F32 = np.float32
@@ -25,39 +25,66 @@ def small_replay(dev):
     return hr, dq.Replay(rec, a, r, t, size)
 
 
-def _check_trajectory(shape, th0, th_gpu, th_ref, losses_gpu, losses_ref, st_gpu=None, st_ref=None):
-    assert np.allclose(losses_gpu, losses_ref, rtol=FP32_TOL, atol=0), (losses_gpu, losses_ref)
-    d_gpu = th_gpu.astype(np.float64) - th0
-    d_ref = th_ref.astype(np.float64) - th0
-    assert_grad_close(shape, d_gpu, d_ref, what="parameter change")
-    if st_gpu is not None:
-        assert_grad_close(shape, st_gpu, st_ref, what="optimizer state")
+# Whole trajectories are compared teacher-forced: each step's oracle result
+# starts from the GPU's own parameters, optimizer state and target network
+# before that step.  A free-running comparison over many steps is not held to
+# the 1e-4 bar: the gradient is discontinuous in the parameters (ReLU masks),
+# so a difference at the rounding level can flip a mask a few steps later and
+# move a trajectory by far more than rounding -- the fp64 oracle against
+# itself with 1e-5 relative noise on its gradients does so on about one run in
+# three here.  Normalized rules start from a state of 0.01 so that the update
+# is smooth in the gradient; the zero-state start, where the first step is
+# about lr * sign(g), is covered by the update parity tests on identical
+# gradients and by the bitwise equivalence tests below.
+
+
+def _step_oracle(shape, hr, idx_n, theta, target, state, rule, lr, decay, eps):
+    s, sn, a, r, t = oracle.gather_from_host_replay(hr, idx_n)
+    out = oracle.td_gradient(shape, theta, target, s, sn, a, r, t, float(F32(0.99)))
+    th1, st1 = oracle.apply_update(rule, theta, state, out["grad"], float(F32(lr)), float(F32(decay)),
+                                   float(F32(eps)))
+    return out, th1, st1
 
 
 @pytest.mark.parametrize("rule,lr,period", [("sgd", 1e-2, 0), ("sgd", 1e-2, 4), ("rmsprop", 1e-3, 3),
                                             ("adagrad", 1e-3, 0)])
 def test_train_steps_trajectory(dev, small_replay, rule, lr, period):
+    """Ten steps of dqn_train_steps, one call per step (a single call of N
+    steps equals N one-step calls bit for bit, tested below); each step's
+    loss, parameter change and optimizer state against the oracle's step
+    from the same parameters, state and target network."""
     import torch
     hr, rp = small_replay
     net, shape = dq.NET_SMALL, di.NET_S
     N, B = 10, 32
     idx = di.index_stream(N, B, hr.size, 42)
+    idx_d = dev_tensor(idx)
     th0 = di.xavier_theta(shape, 43)
     theta = dev_tensor(th0)
     tgt = torch.empty_like(theta) if period else None
-    state = None if rule == "sgd" else torch.zeros_like(theta)
-    losses = torch.empty(N, dtype=torch.float32, device=dev)
+    state = None if rule == "sgd" else torch.full_like(theta, 0.01)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
     decay, eps = (0.9, 0.0) if rule != "adagrad" else (0.0, 1e-8)
-    say(f"[train] rule={rule} lr={lr} period={period}: GPU {N} steps")
-    dq.dqn_train_steps(net, theta, tgt, state, rule, lr, decay, eps, 0.99, rp, dev_tensor(idx),
-                       target_period=period, losses_out=losses)
-    torch.cuda.synchronize()
-    say(f"[train] rule={rule}: oracle")
-    th_ref, st_ref, l_ref = oracle.sequential_training(
-        shape, th0, hr, idx, float(F32(0.99)), float(F32(lr)), rule=rule, decay=float(F32(decay)),
-        eps=float(F32(eps)), target_period=period or None)
-    _check_trajectory(shape, th0, host(theta), th_ref, host(losses), l_ref,
-                      None if state is None else host(state), st_ref)
+    say(f"[train] rule={rule} lr={lr} period={period}: {N} teacher-forced steps")
+    for n in range(N):
+        th_n = host(theta).copy()
+        st_n = None if state is None else host(state).copy()
+        tg_prev = None if tgt is None else host(tgt).copy()
+        dq.dqn_train_steps(net, theta, tgt, state, rule, lr, decay, eps, 0.99, rp, idx_d[n:n + 1],
+                           step0=n, target_period=period, losses_out=loss)
+        torch.cuda.synchronize()
+        if period:
+            tg_n = host(tgt)
+            want = th_n if n % period == 0 else tg_prev
+            assert np.array_equal(tg_n, want), f"target network at step {n}"
+        else:
+            tg_n = th_n
+        out, th_ref, st_ref = _step_oracle(shape, hr, idx[n], th_n, tg_n, st_n, rule, lr, decay, eps)
+        assert abs(float(loss.item()) - out["loss"]) <= FP32_TOL * abs(out["loss"]), (n, loss.item(), out["loss"])
+        d_gpu = host(theta).astype(np.float64) - th_n
+        assert_grad_close(shape, d_gpu, th_ref.astype(np.float64) - th_n, what=f"parameter change at step {n}")
+        if state is not None:
+            assert_grad_close(shape, host(state), st_ref, what=f"optimizer state at step {n}")
 
 
 def test_train_steps_resumes_across_calls(dev, small_replay):
@@ -134,18 +161,47 @@ def _replica_run(dev, rp, shape, net, th0, idx, R, S, lr=0.01, eps=1e-8):
 
 
 def test_replicas_match_stale_schedule_oracle(dev, small_replay):
+    """16 replicas, staleness 4, AdaGrad (lr 0.01, eps 1e-8) from a zero
+    state: the replica run equals, bit for bit, the same schedule driven
+    from the host with the public calls (update u = the gradient on version
+    max(0, u - 4), which is also its target, applied in order u); every
+    update of that schedule is checked against the oracle from the same
+    version -- the gradient and loss to 1e-4, the AdaGrad step on the GPU's
+    own gradient (identical inputs: the zero-state step is about
+    lr * sign(g)) to 1e-4 per tensor."""
+    import torch
     hr, rp = small_replay
     net, shape = dq.NET_SMALL, di.NET_S
-    U, B, R, S = 24, 32, 16, 4
+    U, B, R, S, LR, EPS = 24, 32, 16, 4, 0.01, 1e-8
     idx = di.index_stream(U, B, hr.size, 46)
+    idx_d = dev_tensor(idx)
     th0 = di.xavier_theta(shape, 47)
-    say(f"[replicas] R={R} S={S} U={U}: GPU")
-    th, G, losses = _replica_run(dev, rp, shape, net, th0, dev_tensor(idx), R, S)
-    say("[replicas] oracle")
-    th_ref, G_ref, l_ref = oracle.stale_replica_training(
-        shape, th0, hr, idx, float(F32(0.99)), float(F32(0.01)), S, rule="adagrad",
-        eps=float(F32(1e-8)))
-    _check_trajectory(shape, th0, th, th_ref, losses, l_ref, G, G_ref)
+    say(f"[replicas] R={R} S={S} U={U}: GPU replicas")
+    th, G, losses = _replica_run(dev, rp, shape, net, th0, idx_d, R, S, lr=LR, eps=EPS)
+    say("[replicas] host-driven schedule + oracle per update")
+    versions = [dev_tensor(th0)]
+    Gd = torch.zeros_like(versions[0])
+    g = torch.empty_like(Gd)
+    loss = torch.empty(U, dtype=torch.float32, device=dev)
+    for u in range(U):
+        v = max(0, u - S)
+        dq.dqn_td_gradient_replay(net, versions[v], versions[v], rp, idx_d[u], 0.99, g, loss[u:u + 1])
+        th_u, G_u = host(versions[-1]).copy(), host(Gd).copy()
+        new = torch.empty_like(Gd)
+        dq.ps_apply_update("adagrad", versions[-1], new, Gd, g, LR, 0.0, EPS)
+        versions.append(new)
+        torch.cuda.synchronize()
+        th_v = host(versions[v])
+        s, sn, a, r, t = oracle.gather_from_host_replay(hr, idx[u])
+        ref = oracle.td_gradient(shape, th_v, th_v, s, sn, a, r, t, float(F32(0.99)))
+        assert abs(float(loss[u].item()) - ref["loss"]) <= FP32_TOL * abs(ref["loss"]), u
+        assert_grad_close(shape, host(g), ref["grad"], what=f"gradient of update {u}")
+        th_ref, G_ref = oracle.apply_update("adagrad", th_u, G_u, host(g), float(F32(LR)), 0.0, float(F32(EPS)))
+        assert_grad_close(shape, host(new).astype(np.float64) - th_u, th_ref.astype(np.float64) - th_u,
+                          what=f"AdaGrad step of update {u}")
+        assert_grad_close(shape, host(Gd), G_ref, what=f"AdaGrad state after update {u}")
+    assert np.array_equal(th, host(versions[-1])), "replica run differs from the host-driven schedule"
+    assert np.array_equal(G, host(Gd)) and np.array_equal(losses, host(loss))
 
 
 def test_replicas_zero_staleness_is_sequential_and_deterministic(dev, small_replay):
