@@ -268,7 +268,9 @@ def measured_traffic(config, name):
 
 def roofline(work, name, avg_us, launches, per_step_launches, raw_us=None, config=None,
              peak_flops=PEAK_FP32_MFMA):
-    flop, byts = work[name]
+    flop, byts = work[name]           # per step: per launch when a step launches the kernel several times
+    if per_step_launches > 1:
+        flop, byts = flop // per_step_launches, byts // per_step_launches
     if flop > 0:
         achieved, peak, unit, bound = flop / (avg_us * 1e-6) / 1e12, peak_flops / 1e12, "TFLOP/s", "mfma"
     else:
@@ -532,8 +534,9 @@ def bench_sequential(args):
     def update_only(n):
         for _ in range(n):
             dq.ps_apply_update(dq.PS_SGD, th_copy, th_copy, None, g, LR)
-    T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(200)) / 200
-    tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(200)) / 200
+    nT = min(200, idx.shape[0])
+    T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(nT)) / nT
+    tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(nT)) / nT
 
     rec_ = base_record(K, W, ms)
     rec_["config"] = {
@@ -813,8 +816,9 @@ def bench_replica_sweep(args):
                 dq.ps_apply_update(dq.PS_ADAGRAD, th, th, G, g, LR, 0.0, EPS)
         grad_only(20)
         update_only(20)
-        T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(200)) / 200
-        tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(200)) / 200
+        nT = min(200, idx.shape[0])
+        T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(nT)) / nT
+        tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(nT)) / nT
         del tws
         for R in (1, 2, 4, 8, 16, 32):
             S = min(4, R - 1)
@@ -927,8 +931,9 @@ def bench_replicas(args):
     def update_only(n):
         for _ in range(n):
             dq.ps_apply_update(dq.PS_ADAGRAD, th, th, G, g, LR, 0.0, EPS)
-    T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(200)) / 200
-    tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(200)) / 200
+    nT = min(200, idx.shape[0])
+    T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(nT)) / nT
+    tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(nT)) / nT
 
     out = base_record(U, W, ms)
     out["config"] = {
@@ -1065,7 +1070,7 @@ def bench_large(args):
                                args.config + (" bf16" if bf16 else ""),
                                PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
-                        "per_layer_tflops": {k: round(work[k][0] / (v[0] * 1e-6) / 1e12, 3)
+                        "per_layer_tflops": {k: round(work[k][0] / (v[0] * (v[1] / nb) * 1e-6) / 1e12, 3)
                                              for k, v in bd.items() if work[k][0] > 0}}
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle steps for about {args.cpu_seconds:.0f}s")
@@ -1143,7 +1148,7 @@ def bench_forward(args):
     out["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us, "4a" + (" bf16" if bf16 else ""),
                                PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
-                        "per_layer_tflops": {k: round(work[k][0] / (v[0] * 1e-6) / 1e12, 3)
+                        "per_layer_tflops": {k: round(work[k][0] / (v[0] * (v[1] / nb) * 1e-6) / 1e12, 3)
                                              for k, v in bd.items() if work[k][0] > 0}}
     if not args.no_cpu_baseline:
         n = 512

@@ -346,12 +346,9 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
                         t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, ni.bf16, st));
     } else {
         RUN(DQN_K_FC1_FWD,
-            launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
-                        t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, ni.bf16, st));
-        RUN(DQN_K_FC1_FWD,
-            launch_gemm(GEMM_NT, B, ni.H, ni.flat, xlast + (int64_t)B * ni.flat, ni.flat,
-                        tt + ni.w_off[L], ni.flat, t.fc1p + (int64_t)B * ni.H, ni.H, t.ks,
-                        t.kchunk, slice, nullptr, ni.bf16, st));
+            launch_gemm_fwd2(B, ni.H, ni.flat, xlast, th + ni.w_off[L], t.fc1p, xlast + (int64_t)B * ni.flat,
+                             tt + ni.w_off[L], t.fc1p + (int64_t)B * ni.H, ni.flat, ni.flat, ni.H, t.ks,
+                             t.kchunk, slice, ni.bf16, st));
     }
     HeadTdArgs h{};
     h.fc1p = t.fc1p;

@@ -283,6 +283,14 @@ hipError_t launch_gemm_bf16(GemmKind kind, int M, int N, int K, const float* A, 
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
                        const float* mask, bool bf16, hipStream_t st);
+// Two fc1 forward contractions of one shape in one launch (GEMM_NT, split-K
+// as above): C0 = A0 B0^T and C1 = A1 B1^T, each in its own k-slices.
+hipError_t launch_gemm_bf16_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0,
+                                 const float* A1, const float* B1, float* C1, int lda, int ldb, int ldc,
+                                 int kslices, int kchunk, int64_t c_slice, hipStream_t st);
+hipError_t launch_gemm_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0, const float* A1,
+                            const float* B1, float* C1, int lda, int ldb, int ldc, int kslices, int kchunk,
+                            int64_t c_slice, bool bf16, hipStream_t st);
 
 // fc1 backward for batch B: dW [H][F] = dz1^T x (x = first B rows of the last
 // conv output) and dx [B][F] = (dz1 W) masked by [x > 0], as one launch where

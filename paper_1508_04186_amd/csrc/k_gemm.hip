@@ -197,6 +197,29 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
     gemm_body<BM, BN, BK, TA, TB, MASK, BF16>(p, blockIdx.x, blockIdx.y, blockIdx.z, smem);
 }
 
+// Two forward GEMMs of one shape in one launch (the online network on s and
+// the target network on s'): k-slices z < ks0 run p0, the rest p1.
+template <int BM, int BN, int BK, bool BF16>
+__global__ __launch_bounds__(256) void gemm_fwd2_kernel(GemmParams p0, GemmParams p1, int ks0) {
+    extern __shared__ __align__(16) float smem[];
+    const int z = blockIdx.z;
+    if (z < ks0)
+        gemm_body<BM, BN, BK, false, true, false, BF16>(p0, blockIdx.x, blockIdx.y, z, smem);
+    else
+        gemm_body<BM, BN, BK, false, true, false, BF16>(p1, blockIdx.x, blockIdx.y, z - ks0, smem);
+}
+
+template <int BM, int BN, int BK>
+hipError_t launch_fwd2_tile(const GemmParams& p0, const GemmParams& p1, int kslices, hipStream_t st) {
+    if (p0.kchunk % BK != 0) return hipErrorInvalidValue;
+    constexpr size_t lds = GemmSmem<BM, BN, BK, false, true>::bytes;
+    auto kern = gemm_fwd2_kernel<BM, BN, BK, false>;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((p0.M + BM - 1) / BM), (unsigned)((p0.N + BN - 1) / BN), (unsigned)(2 * kslices));
+    hipLaunchKernelGGL(kern, grid, dim3(256), lds, st, p0, p1, kslices);
+    return hipGetLastError();
+}
+
 // Two independent GEMMs in one launch (flattened block index; the first
 // n1 = g1x*g1y*g1z blocks run GEMM 1).
 template <int BM1, int BN1, int BK1, bool TA1, bool TB1, bool M1,
@@ -332,6 +355,27 @@ hipError_t launch_gemm_prec(GemmKind kind, int M, int N, int K, const float* A, 
 }
 
 }  // namespace
+
+hipError_t launch_gemm_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0, const float* A1,
+                            const float* B1, float* C1, int lda, int ldb, int ldc, int kslices, int kchunk,
+                            int64_t c_slice, bool bf16, hipStream_t st) {
+    if (kchunk % 32 != 0 || kslices <= 0) return hipErrorInvalidValue;
+    if (bf16) return launch_gemm_bf16_fwd2(M, N, K, A0, B0, C0, A1, B1, C1, lda, ldb, ldc, kslices, kchunk,
+                                           c_slice, st);
+    const GemmParams p0{M, N, K, A0, lda, B0, ldb, C0, ldc, kchunk, c_slice, nullptr};
+    const GemmParams p1{M, N, K, A1, lda, B1, ldb, C1, ldc, kchunk, c_slice, nullptr};
+    const TileCfg c = fwd_tile(M, kchunk);
+#define DQN_TILE(TBM, TBN, TBK) \
+    if (c.bm == TBM && c.bn == TBN && c.bk == TBK) return launch_fwd2_tile<TBM, TBN, TBK>(p0, p1, kslices, st);
+    DQN_TILE(32, 32, 32)
+    DQN_TILE(32, 32, 64)
+    DQN_TILE(64, 32, 32)
+    DQN_TILE(64, 32, 64)
+    DQN_TILE(64, 64, 32)
+    DQN_TILE(64, 64, 64)
+#undef DQN_TILE
+    return hipErrorInvalidValue;
+}
 
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,

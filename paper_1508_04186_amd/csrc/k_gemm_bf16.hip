@@ -16,6 +16,7 @@
 // the other dimension, from L2), and the forward pass splits K so that the
 // launch still covers the chip.
 #include <algorithm>
+#include <initializer_list>
 
 #include "common.h"
 
@@ -100,7 +101,7 @@ struct Stage {
 // TB: B(k,n) = B[n*ldb + k] else B[k*ldb + n].
 // MASK: C(m,n) = 0 where mask[m*ldc + n] <= 0.
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
-__global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Params p) {
+__device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z) {
     constexpr int NT = 64 * WGM * WGN;
     constexpr int WTM = BM / WGM, WTN = BN / WGN;     // wave tile
     constexpr int TM = WTM / 16, TN = WTN / 16;       // MFMA tiles per wave
@@ -108,7 +109,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Param
     static_assert(BK % 32 == 0 && WTM % 16 == 0 && WTN % 16 == 0, "tile shape");
     __shared__ __align__(16) __bf16 As[BM * RS];
     __shared__ __align__(16) __bf16 Bs[BN * RS];
-    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN, z = blockIdx.z;
+    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
     const int kbeg = z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
@@ -169,6 +170,31 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Param
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Params p) {
+    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK>(p, blockIdx.z);
+}
+
+// Two forward contractions of one shape (the online network on s, the
+// target network on s'): k-slices z < ks0 run p0, the rest p1.
+template <int BM, int BN, int BK, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_fwd2_kernel(GemmBf16Params p0, GemmBf16Params p1,
+                                                                       int ks0) {
+    const int z = blockIdx.z;
+    if (z < ks0)
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false>(p0, z);
+    else
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false>(p1, z - ks0);
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN>
+hipError_t gemm_bf16_fwd2_launch(const GemmBf16Params& p0, const GemmBf16Params& p1, int kslices, hipStream_t st) {
+    const dim3 grid((unsigned)((p0.M + BM - 1) / BM), (unsigned)((p0.N + BN - 1) / BN), (unsigned)(2 * kslices));
+    hipLaunchKernelGGL((gemm_bf16_fwd2_kernel<BM, BN, BK, WGM, WGN>), grid, dim3(64 * WGM * WGN), 0, st, p0, p1,
+                       kslices);
+    return hipGetLastError();
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
 hipError_t gemm_bf16_launch(const GemmBf16Params& prm, int kslices, hipStream_t st) {
     const dim3 grid((unsigned)((prm.M + BM - 1) / BM), (unsigned)((prm.N + BN - 1) / BN), (unsigned)kslices);
     hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, TA, TB, MASK>), grid, dim3(64 * WGM * WGN), 0, st,
@@ -191,6 +217,19 @@ void gemm_fwd_split_bf16(int rows, int N, int K, int* ks, int* kchunk) {
     const int want = (int)std::min<long>(steps, std::max<long>(1, (target + tiles - 1) / tiles));
     *kchunk = (steps + want - 1) / want * 64;
     *ks = (K + *kchunk - 1) / *kchunk;
+}
+
+hipError_t launch_gemm_bf16_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0,
+                                 const float* A1, const float* B1, float* C1, int lda, int ldb, int ldc,
+                                 int kslices, int kchunk, int64_t c_slice, hipStream_t st) {
+    if (M <= 0 || N <= 0 || K <= 0 || kslices <= 0 || kchunk % 32 != 0 || K % 4) return hipErrorInvalidValue;
+    for (const float* x : {A0, B0, A1, B1})
+        if ((uintptr_t)x % 16) return hipErrorInvalidValue;
+    if (lda % 4 || ldb % 4) return hipErrorInvalidValue;
+    const GemmBf16Params p0{M, N, K, A0, lda, B0, ldb, C0, ldc, kchunk, c_slice, nullptr};
+    const GemmBf16Params p1{M, N, K, A1, lda, B1, ldb, C1, ldc, kchunk, c_slice, nullptr};
+    if (M >= kBf16BigRows) return gemm_bf16_fwd2_launch<128, 256, 64, 2, 4>(p0, p1, kslices, st);
+    return gemm_bf16_fwd2_launch<64, 64, 128, 2, 2>(p0, p1, kslices, st);
 }
 
 hipError_t launch_gemm_bf16(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
