@@ -73,10 +73,17 @@ METRIC = "DQN TD-gradient+update steps/sec (transitions/sec); % MFMA peak and HB
 PEAK_FP32_MFMA = 157.3e12   # MI355X dense fp32 matrix FLOP/s
 PEAK_HBM = 8.0e12           # MI355X HBM3E bytes/s
 PEAK_BF16_MFMA = 2.5e15     # MI355X dense bf16 matrix FLOP/s
-# In the timed region of the small-batch configs, every SAMPLE_STRIDE-th
-# launch of the dominant kernel is bracketed by events (each pair adds a few
-# microseconds to a step of about seventy).
+# In the timed region, every SAMPLE_STRIDE-th launch of the dominant kernel
+# is bracketed by events: a pair adds about five microseconds of idle time
+# around the launch it brackets (the command processor executes the event
+# records), a few per cent of a large-network step at batch 256.
 SAMPLE_STRIDE = 10
+
+
+def sample_stride(steps):
+    """Stride of the bracketed launches: SAMPLE_STRIDE, or smaller for short
+    runs so that at least 20 launches are timed."""
+    return max(1, min(SAMPLE_STRIDE, steps // 20))
 F32 = np.float32
 
 
@@ -1044,7 +1051,9 @@ def bench_large(args):
     if tgt is not None:
         tgt.copy_(saved_t)
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
-    kid, ev = prof.attach(dom, K * 4)
+    lps = max(1, round(bd[dom][1] / nb))          # launches of the kernel per step
+    stride = sample_stride(K)
+    kid, ev = prof.attach(dom, K * lps // stride + 4, stride)
     ms = time_region(torch.cuda.synchronize, lambda: run(W, total))
     raw_us, used = prof.collect(kid, ev)
     dom_us = raw_us - prof.overhead()
@@ -1066,7 +1075,7 @@ def bench_large(args):
     out["transitions_per_s"] = round(out["value"] * B, 1)
     out["step_tflops"] = round(sum(v[0] for v in work.values()) * out["value"] / 1e12, 4)
     out["final_loss"] = final_loss
-    out["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us,
+    out["roofline"] = roofline(work, dom, dom_us, used, lps, raw_us,
                                args.config + (" bf16" if bf16 else ""),
                                PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
@@ -1128,7 +1137,9 @@ def bench_forward(args):
     nb = min(args.breakdown_steps, K, 20)
     bd = prof.breakdown(lambda: run(W, W + nb), nb, list(work))
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
-    kid, ev = prof.attach(dom, K * 4)
+    lps = max(1, round(bd[dom][1] / nb))
+    stride = sample_stride(K)
+    kid, ev = prof.attach(dom, K * lps // stride + 4, stride)
     ms = time_region(torch.cuda.synchronize, lambda: run(W, K + W))
     raw_us, used = prof.collect(kid, ev)
     dom_us = raw_us - prof.overhead()
@@ -1145,7 +1156,7 @@ def bench_forward(args):
         out["config"]["accumulate"] = "f32"
     out["states_per_s"] = round(out["value"] * B, 1)
     out["step_tflops"] = round(sum(v[0] for v in work.values()) * out["value"] / 1e12, 4)
-    out["roofline"] = roofline(work, dom, dom_us, used, used // K, raw_us, "4a" + (" bf16" if bf16 else ""),
+    out["roofline"] = roofline(work, dom, dom_us, used, lps, raw_us, "4a" + (" bf16" if bf16 else ""),
                                PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
                         "per_layer_tflops": {k: round(work[k][0] / (v[0] * (v[1] / nb) * 1e-6) / 1e12, 3)

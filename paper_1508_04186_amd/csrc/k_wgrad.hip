@@ -5,10 +5,16 @@
 // A workgroup owns every output of the layer (64 x cin*k*k) for a run of
 // samples and keeps them in registers across the samples; it writes one
 // partial-sum slot at the end, which the finalize kernel reduces in a fixed
-// order (no atomics).  Per sample, dz and the layer input are staged in LDS
+// order (no atomics).  For conv3 up to 256 samples (MS = 2) two workgroups
+// share a slot, each owning 32 of the 64 output channels for a run of two
+// samples: as many workgroups, half the partial-sum bytes written here and
+// read back by the finalize kernel (batch 256: conv3 17.1 -> 15.9 us,
+// finalize 27.5 -> 27.4; conv2's input is 2.5 times conv3's, and staging it
+// twice per workgroup cost more than its halved slots saved).  Per sample, dz and the layer input are staged in LDS
 // (the next sample's values read into registers during the MFMAs); the
 // contraction runs over the output pixels.  Eight waves: (half of the four
-// M-tiles of output channels) x (quarter of the weight columns).  A operand
+// M-tiles of output channels, or one of the workgroup's two M-tiles when
+// MS = 2) x (quarter of the weight columns).  A operand
 // dz[o][p]: row stride = 4 (mod 16) floats so the 64 lanes of a read hit 64
 // banks; pixels past the map are zero in the stage, so their products
 // vanish.  B operand in[c][S*oy + ky][S*ox + kx]: a per-lane column base
@@ -51,20 +57,25 @@ struct WgradRegParams {
     int n, spg;         // samples; samples per workgroup (slot)
 };
 
-template <int CIN, int IH, int K, int S, int OH, bool BF16>
+template <int CIN, int IH, int K, int S, int OH, bool BF16, int MS>
 __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p) {
     using G = WgradGeom<CIN, IH, K, S, OH>;
+    static_assert(MS == 1 || MS == 2, "one or two workgroups per slot");
+    constexpr int MT = 2 / MS;           // M-tiles (16 output channels) per wave
     extern __shared__ __align__(16) float smem[];
     float* s_dz = smem;                  // [64][DCS]
     float* s_in = smem + G::COUT * G::DCS;  // [CIN][IH*IH]
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
-    const int mh = wave >> 2, ng = wave & 3;   // M-tiles 2mh, 2mh+1; N-tiles ng*NPW ...
+    const int mh = wave >> 2, ng = wave & 3;   // N-tiles ng*NPW ...
+    const int slot = blockIdx.x / MS, half = blockIdx.x % MS;
+    // M-tile of accumulator m: 2mh + m (MS = 1), or 2half + mh (MS = 2)
+    auto mtile = [&](int m) { return MS == 1 ? 2 * mh + m : 2 * half + mh; };
 
     for (int e = t; e < G::COUT * G::DCS; e += WR_WG) s_dz[e] = 0.f;
 
-    const int j_lo = blockIdx.x * p.spg;
+    const int j_lo = slot * p.spg;
     const int j_hi = min(p.n, j_lo + p.spg);
 
     // column bases: column n = c*K*K + ky*K + kx of N-tile (ng*NPW + i)
@@ -84,11 +95,13 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p)
         const int pc = pix < G::P ? pix : 0;
         pb[q] = (S * (pc / OH)) * IH + S * (pc % OH);
     }
-    const int arow[2] = {((2 * mh) * 16 + li) * G::DCS + g, ((2 * mh + 1) * 16 + li) * G::DCS + g};
-
-    f4 acc[2][G::NPW];
+    int arow[MT];
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < MT; ++m) arow[m] = (mtile(m) * 16 + li) * G::DCS + g;
+
+    f4 acc[MT][G::NPW];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
 #pragma unroll
         for (int i = 0; i < G::NPW; ++i) acc[m][i] = f4{0.f, 0.f, 0.f, 0.f};
     float bsum = 0.f;
@@ -135,7 +148,7 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p)
         // of it (NPW x NPB live registers).
 #pragma unroll
         for (int i = 0; i < G::NPW; ++i) asm volatile("" : "+v"(cb[i]));
-        if (t < G::COUT) {
+        if (half == 0 && t < G::COUT) {
             const float* row = s_dz + t * G::DCS;
             float s0 = 0.f, s1 = 0.f;
             for (int q = 0; q + 1 < G::P; q += 2) {
@@ -148,9 +161,9 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p)
         if constexpr (BF16) {
 #pragma unroll
             for (int st = 0; st < G::PSTEP32; ++st) {
-                bf16x8 a[2], b[G::NPW];
+                bf16x8 a[MT], b[G::NPW];
 #pragma unroll
-                for (int m = 0; m < 2; ++m)
+                for (int m = 0; m < MT; ++m)
 #pragma unroll
                     for (int e = 0; e < 8; ++e) a[m][e] = (__bf16)s_dz[arow[m] + 32 * st + 4 * e];
 #pragma unroll
@@ -158,20 +171,20 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p)
 #pragma unroll
                     for (int e = 0; e < 8; ++e) b[i][e] = (__bf16)s_in[cb[i] + pb[st * 8 + e]];
 #pragma unroll
-                for (int m = 0; m < 2; ++m)
+                for (int m = 0; m < MT; ++m)
 #pragma unroll
                     for (int i = 0; i < G::NPW; ++i) acc[m][i] = mfma16x16x32bf16(a[m], b[i], acc[m][i]);
             }
         } else {
 #pragma unroll
             for (int st = 0; st < NPB; ++st) {
-                float a[2], b[G::NPW];
+                float a[MT], b[G::NPW];
 #pragma unroll
-                for (int m = 0; m < 2; ++m) a[m] = s_dz[arow[m] + 4 * st];
+                for (int m = 0; m < MT; ++m) a[m] = s_dz[arow[m] + 4 * st];
 #pragma unroll
                 for (int i = 0; i < G::NPW; ++i) b[i] = s_in[cb[i] + pb[st]];
 #pragma unroll
-                for (int m = 0; m < 2; ++m)
+                for (int m = 0; m < MT; ++m)
 #pragma unroll
                     for (int i = 0; i < G::NPW; ++i) acc[m][i] = mfma16x16x4(a[m], b[i], acc[m][i]);
                 __builtin_amdgcn_sched_barrier(0);
@@ -179,31 +192,33 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p)
         }
     }
 
-    // D[4g + r][li] of tile (m, i): channel (2mh + m)*16 + 4g + r, column (ng*NPW + i)*16 + li
+    // D[4g + r][li] of tile (m, i): channel mtile(m)*16 + 4g + r, column (ng*NPW + i)*16 + li
     if (j_lo >= j_hi) return;  // uniform; padding slot of nothing
-    float* wp = p.wpart + (size_t)blockIdx.x * G::COUT * G::KT;
+    float* wp = p.wpart + (size_t)slot * G::COUT * G::KT;
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < MT; ++m)
 #pragma unroll
         for (int i = 0; i < G::NPW; ++i)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                wp[(size_t)((2 * mh + m) * 16 + 4 * g + r) * G::KT + (ng * G::NPW + i) * 16 + li] = acc[m][i][r];
-    if (t < G::COUT) p.bpart[(size_t)blockIdx.x * G::COUT + t] = bsum;
+                wp[(size_t)(mtile(m) * 16 + 4 * g + r) * G::KT + (ng * G::NPW + i) * 16 + li] = acc[m][i][r];
+    if (half == 0 && t < G::COUT) p.bpart[(size_t)slot * G::COUT + t] = bsum;
 }
 
-template <int CIN, int IH, int K, int S, int OH>
-int wgrad_reg_spg(int n) {
-    return std::max(1, (n + 255) / 256);
-}
+// Up to 256 samples: two samples per slot, a slot's two workgroups taking
+// half of the output channels each; above, one workgroup per slot and
+// enough samples per slot that there are at most 256 slots.
+constexpr bool kSplitConv2 = false, kSplitConv3 = true;   // layers whose slots split up to 256 samples
+int wgrad_reg_ms(int cin, int n) { return n <= 256 && (cin == 32 ? kSplitConv2 : kSplitConv3) ? 2 : 1; }
+int wgrad_reg_spg(int cin, int n) { return wgrad_reg_ms(cin, n) == 2 ? 2 : std::max(1, (n + 255) / 256); }
 
 template <int CIN, int IH, int K, int S, int OH>
 hipError_t wgrad_reg_launch(const float* in, const float* dz, int n, float* wpart, float* bpart, bool bf16,
                             hipStream_t st) {
     using G = WgradGeom<CIN, IH, K, S, OH>;
     if (n <= 0) return hipErrorInvalidValue;
-    const int spg = wgrad_reg_spg<CIN, IH, K, S, OH>(n);
-    const int blocks = (n + spg - 1) / spg;
+    const int spg = wgrad_reg_spg(CIN, n), ms = wgrad_reg_ms(CIN, n);
+    const int blocks = (n + spg - 1) / spg * ms;
     const WgradRegParams prm{in, dz, wpart, bpart, n, spg};
     constexpr size_t lds = (size_t)G::LDS * 4;
     auto go = [&](auto kern) -> hipError_t {
@@ -211,15 +226,18 @@ hipError_t wgrad_reg_launch(const float* in, const float* dz, int n, float* wpar
         hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(WR_WG), lds, st, prm);
         return hipGetLastError();
     };
-    return bf16 ? go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, true>)
-                : go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, false>);
+    if (ms == 2)
+        return bf16 ? go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, true, 2>)
+                    : go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, false, 2>);
+    return bf16 ? go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, true, 1>)
+                : go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, false, 1>);
 }
 
 }  // namespace
 
 int conv_wgrad_reg_slots(ConvId id, int n) {
     if (id != CONV_L2 && id != CONV_L3) return -1;
-    const int spg = std::max(1, (n + 255) / 256);
+    const int spg = wgrad_reg_spg(id == CONV_L2 ? 32 : 64, n);
     return (n + spg - 1) / spg;
 }
 

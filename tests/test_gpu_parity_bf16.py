@@ -47,7 +47,7 @@ def _run_td(dev, th, tt, s, sn, a, r, t, gamma=0.99):
     return host(g), float(host(loss)[0]), host(q), host(y)
 
 
-@pytest.mark.parametrize("B,held", [(3, False), (17, True), (64, False), (256, True), (2048, False)])
+@pytest.mark.parametrize("B,held", [(3, False), (17, True), (64, False), (131, True), (256, True), (2048, False)])
 def test_bf16_td_gradient_matches_oracle(dev, B, held):
     say(f"[bf16-td] batch={B} held={held}: inputs")
     th, tt, s, sn, a, r, t = _inputs(B, 500 + B, held)

@@ -37,7 +37,8 @@ def _run_td(dev, net, th, tt, s, sn, a, r, t, gamma):
 
 
 @pytest.mark.parametrize("name,B,target", [("small", 700, "same"), ("small", 1024, "held"),
-                                           ("large", 256, "held"), ("large", 2048, "same")])
+                                           ("large", 131, "held"), ("large", 256, "held"),
+                                           ("large", 2048, "same")])
 def test_td_gradient_full_size(dev, name, B, target):
     net, shape = (dq.NET_SMALL, di.NET_S) if name == "small" else (dq.NET_LARGE, di.NET_L)
     size = 4 * B + 10
