@@ -73,17 +73,17 @@ METRIC = "DQN TD-gradient+update steps/sec (transitions/sec); % MFMA peak and HB
 PEAK_FP32_MFMA = 157.3e12   # MI355X dense fp32 matrix FLOP/s
 PEAK_HBM = 8.0e12           # MI355X HBM3E bytes/s
 PEAK_BF16_MFMA = 2.5e15     # MI355X dense bf16 matrix FLOP/s
-# In the timed region, every SAMPLE_STRIDE-th launch of the dominant kernel
-# is bracketed by events: a pair adds about five microseconds of idle time
-# around the launch it brackets (the command processor executes the event
-# records), a few per cent of a large-network step at batch 256.
-SAMPLE_STRIDE = 10
+# In the timed region, one launch of the dominant kernel in `stride` is
+# bracketed by events: a pair idles the GPU for a few microseconds around
+# the launch it brackets (a few per cent of a large-network step at batch
+# 256 when every launch was bracketed), so about 40 launches of a run are.
+SAMPLE_STRIDE = 50
 
 
 def sample_stride(steps):
     """Stride of the bracketed launches: SAMPLE_STRIDE, or smaller for short
-    runs so that at least 20 launches are timed."""
-    return max(1, min(SAMPLE_STRIDE, steps // 20))
+    runs so that at least 40 launches are timed."""
+    return max(1, min(SAMPLE_STRIDE, steps // 40))
 F32 = np.float32
 
 
@@ -446,7 +446,7 @@ def bench_single(args):
     bd = prof.breakdown(lambda: steps(args.breakdown_steps), args.breakdown_steps, list(work))
     theta.copy_(saved)
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
-    kid, ev = prof.attach(dom, K * 4 // SAMPLE_STRIDE + 4, SAMPLE_STRIDE)
+    kid, ev = prof.attach(dom, K * 4 // sample_stride(K) + 4, sample_stride(K))
     ms = time_region(torch.cuda.synchronize, lambda: steps(K))
     raw_us, used = prof.collect(kid, ev)
     dom_us = raw_us - prof.overhead()
@@ -514,7 +514,7 @@ def bench_sequential(args):
     bd = prof.breakdown(lambda: run(W, W + nb), nb, list(work))
     theta.copy_(saved)
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
-    kid, ev = prof.attach(dom, K * 4 // SAMPLE_STRIDE + 4, SAMPLE_STRIDE)
+    kid, ev = prof.attach(dom, K * 4 // sample_stride(K) + 4, sample_stride(K))
     ms = time_region(torch.cuda.synchronize, lambda: run(W, total))
     raw_us, used = prof.collect(kid, ev)
     dom_us = raw_us - prof.overhead()
@@ -647,7 +647,7 @@ def bench_actor(args):
                         ["conv12_fwd", "fc1_fwd", "head"])
     # the games and the learner go on from where the breakdown left them
     dom = max((k for k in bd if k in cands), key=lambda k: bd[k][0] * bd[k][1])
-    kid, ev = prof.attach(dom, K // SAMPLE_STRIDE + 4, SAMPLE_STRIDE)
+    kid, ev = prof.attach(dom, K // sample_stride(K) + 4, sample_stride(K))
     lo = FILL + W + nb
     Kt = K - nb
     ms = time_region(torch.cuda.synchronize, lambda: run(lo, lo + Kt))
@@ -731,7 +731,7 @@ def bench_observe(args):
     torch.cuda.synchronize()
     hip = HipEvents()
     prof = Profiler(hip)
-    kid, ev = prof.attach("observe", K + 4, 1)
+    kid, ev = prof.attach("observe", K // sample_stride(K) + 4, sample_stride(K))
     ms = time_region(torch.cuda.synchronize, lambda: run(W, W + K))
     raw_us, used = prof.collect(kid, ev)
     dom_us = raw_us - prof.overhead()
@@ -907,7 +907,7 @@ def bench_replicas(args):
     # above are outside the region)
     ring[:P].copy_(torch.from_numpy(th0).to(dev))
     G.zero_()
-    kid, ev = prof.attach(dom, U * 4 // SAMPLE_STRIDE + 4, SAMPLE_STRIDE)
+    kid, ev = prof.attach(dom, U * 4 // sample_stride(U) + 4, sample_stride(U))
     e0 = time.perf_counter()
     ms = time_region(torch.cuda.synchronize,
                      lambda: dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA,
