@@ -321,10 +321,12 @@ __global__ __launch_bounds__(HT) void head_fwd_kernel(HeadFwdArgs p) {
 //    action j took), the fc1 bias gradient, the fc2 bias gradient and the
 //    loss, into one partial-sum slot per chunk.  A workgroup takes 64 hidden
 //    units of a chunk, so its loads are 256-byte rows;
-//  - finalize_wide_kernel: one lane per output (consecutive outputs, so
-//    every load is a 256-byte row of a slot) sums its slots in slot order:
-//    the conv weight and bias gradients over the wgrad partial-sum slots,
-//    then the sample sums over the chunk slots.
+//  - finalize_wide_kernel: four lanes per output (sixteen consecutive
+//    outputs per wave, so every load is four 64-byte row pieces), lane q
+//    summing slots q, q + 4, ... in order, then the four lane sums by a
+//    butterfly: the conv weight and bias gradients over the wgrad
+//    partial-sum slots, then the sample sums over the chunk slots.  With
+//    one lane per output, 256 slots took eight dependent rounds of 32 loads.
 //
 // MODE < 0 stores the gradient; MODE = 0, 1, 2 applies update rule MODE to
 // each parameter instead (fused parameter-server update), and the blocks
@@ -453,15 +455,29 @@ __global__ __launch_bounds__(256) void sample_partials_kernel(FinalizeArgs a) {
     float sw[A], sb = 0.f;
 #pragma unroll
     for (int k = 0; k < A; ++k) sw[k] = 0.f;
+    // Every load of the eight samples is issued before the first use (an
+    // index past the chunk reads sample j0 and is not added), so the loads
+    // are one round trip instead of eight dependent ones.
+    constexpr int NS = SP_CHUNK / 4;
+    int acts[NS];
+    float dl[NS], hv[NS], zv[NS];
 #pragma unroll
-    for (int i = 0; i < SP_CHUNK / 4; ++i) {
+    for (int i = 0; i < NS; ++i) {
         const int j = j0 + w + 4 * i;
-        if (j < j1) {
-            const int act = clamp_action(a.action[j], A);
-            const float d = a.delta[j] * a.h1s[(int64_t)j * a.H + h];
+        const int jc = j < j1 ? j : j0;
+        acts[i] = a.action[jc];
+        dl[i] = a.delta[jc];
+        hv[i] = a.h1s[(int64_t)jc * a.H + h];
+        zv[i] = a.dz1[(int64_t)jc * a.H + h];
+    }
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+        if (j0 + w + 4 * i < j1) {
+            const int act = clamp_action(acts[i], A);
+            const float d = dl[i] * hv[i];
 #pragma unroll
             for (int k = 0; k < A; ++k) sw[k] += act == k ? d : 0.f;
-            sb += a.dz1[(int64_t)j * a.H + h];
+            sb += zv[i];
         }
     }
 #pragma unroll
@@ -491,6 +507,7 @@ __global__ __launch_bounds__(256) void sample_partials_kernel(FinalizeArgs a) {
 }
 
 constexpr int FW_U = 32;   // slots in flight per lane
+constexpr int FW_L = 4;    // lanes per output
 template <int MODE>
 __global__ __launch_bounds__(256) void finalize_wide_kernel(FinalizeArgs a, PsUpdate u, int n_fin) {
     if constexpr (MODE >= 0) {
@@ -499,7 +516,9 @@ __global__ __launch_bounds__(256) void finalize_wide_kernel(FinalizeArgs a, PsUp
             return;
         }
     }
-    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    // FW_L consecutive lanes share an output (a group exits or stays as one)
+    const int ql = threadIdx.x & (FW_L - 1);
+    int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) / FW_L;
     const float* part = nullptr;
     int64_t count = 0;
     int slots = 0;
@@ -523,14 +542,24 @@ __global__ __launch_bounds__(256) void finalize_wide_kernel(FinalizeArgs a, PsUp
         else if (i < wh + a.H + a.A) dst = a.g_b2 + (i - wh - a.H);
         else loss = true;
     }
+    // lane ql of the group sums slots ql, ql + FW_L, ... in order; the
+    // group's lane sums are then combined by a butterfly, which gives every
+    // lane the same value (float addition is commutative)
     float s = 0.f;
-    for (int q = 0; q < slots; q += FW_U) {
+    for (int q = ql; q < slots; q += FW_L * FW_U) {
         float v[FW_U];
 #pragma unroll
-        for (int e = 0; e < FW_U; ++e) v[e] = q + e < slots ? part[(int64_t)(q + e) * count] : 0.f;
+        for (int e = 0; e < FW_U; ++e) {
+            const int z = q + FW_L * e;
+            v[e] = z < slots ? part[(int64_t)z * count] : 0.f;
+        }
 #pragma unroll
         for (int e = 0; e < FW_U; ++e) s += v[e];
     }
+    static_assert(FW_L == 4, "two butterfly steps");
+    s += __shfl_xor(s, 1, 64);
+    s += __shfl_xor(s, 2, 64);
+    if (ql != 0) return;
     if (loss) a.loss_out[0] = s;
     else emit<MODE>(a, u, dst, s);
 }
@@ -582,7 +611,7 @@ hipError_t finalize_wide_launch(const FinalizeArgs& a, const PsUpdate* upd, hipS
     if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
     int64_t total = (int64_t)A * a.H + a.H + A + 1;
     for (int l = 0; l < a.n_conv; ++l) total += a.wcount[l] + a.cout[l];
-    const int n_fin = (int)((total + 255) / 256);
+    const int n_fin = (int)((total * FW_L + 255) / 256);
     if (!upd) {
         hipLaunchKernelGGL(finalize_wide_kernel<-1>, dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{}, n_fin);
         return hipGetLastError();
