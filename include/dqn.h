@@ -125,6 +125,15 @@ int replay_gather(const dqn_replay* replay, const int64_t* idx, int32_t batch,
                   uint8_t* s_out, uint8_t* s_next_out, int32_t* a_out, float* r_out,
                   uint8_t* term_out, void* stream);
 
+/* Check of an index stream before replay_gather, which does not check on
+ * the device (Sec. III.C: transition i needs record i+1 when with_next is
+ * nonzero): writes to *bad_count (device int32) the number of idx[0..batch)
+ * outside [0, size-2] (with_next != 0) or [0, size-1] (with_next == 0).
+ * Only replay->size is read.  DQN_EINVAL for null pointers, batch <= 0 or a
+ * replay too small for any valid index. */
+int replay_gather_validate(const dqn_replay* replay, const int64_t* idx, int32_t batch, int32_t with_next,
+                           int32_t* bad_count, void* stream);
+
 /* Setup, not part of the method: fills the replay memory that `replay`
  * describes (records 0 .. size-1 and the side arrays; the call writes through
  * its pointers) with a seeded synthetic stream standing in for preprocessed

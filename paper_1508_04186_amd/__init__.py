@@ -18,5 +18,5 @@ from .native import (  # noqa: F401
     dqn_train_workspace_bytes, dqn_train_ring_stride, dqn_train_steps, dqn_train_replicas,
     HipStreams, DQN_PEAK_FP32, DQN_PEAK_BF16, profile_mfma_peak, profile_stream_copy,
     ActorReplay, snake_games, snake_reset, snake_step, dqn_anneal_epsilon, dqn_act, SNAKE_STATE_BYTES,
-    dqn_preprocess, dqn_observe, replay_fill_synthetic,
+    dqn_preprocess, dqn_observe, replay_fill_synthetic, replay_gather_validate,
 )

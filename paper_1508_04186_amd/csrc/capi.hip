@@ -574,6 +574,15 @@ int replay_gather(const dqn_replay* rp, const int64_t* idx, int32_t batch, uint8
     return DQN_OK;
 }
 
+int replay_gather_validate(const dqn_replay* rp, const int64_t* idx, int32_t batch, int32_t with_next,
+                           int32_t* bad_count, void* stream) {
+    if (!rp || !idx || !bad_count || batch <= 0) return DQN_EINVAL;
+    if (rp->size < (with_next ? 2 : 1)) return DQN_EINVAL;
+    hipStream_t st = (hipStream_t)stream;
+    if (launch_validate(idx, batch, rp->size - (with_next ? 2 : 1), bad_count, st) != hipSuccess) return DQN_EHIP;
+    return DQN_OK;
+}
+
 int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, int32_t batch,
                 float epsilon, const uint64_t* draws, float* q_out, int32_t* action_out, void* ws,
                 size_t ws_bytes, void* stream) {

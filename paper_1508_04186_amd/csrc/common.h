@@ -359,6 +359,8 @@ struct PsUpdate {
 // weight range is then read from grad_base.  The loss is stored either way.
 hipError_t launch_finalize(const FinalizeArgs& a, const PsUpdate* upd, hipStream_t st);
 
+// Count of idx[0..batch) outside [0, hi] into *bad (one workgroup).
+hipError_t launch_validate(const int64_t* idx, int batch, int64_t hi, int32_t* bad, hipStream_t st);
 hipError_t launch_gather(const uint8_t* frames, int64_t stride, int64_t rec_bytes,
                          const uint8_t* act, const int8_t* rew, const uint8_t* term,
                          const int64_t* idx, int batch, uint8_t* s, uint8_t* sn, int32_t* a,

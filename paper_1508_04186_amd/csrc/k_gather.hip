@@ -29,7 +29,29 @@ __global__ __launch_bounds__(256) void gather_kernel(
     }
 }
 
+// Counts the indices outside [0, hi] into *bad: one workgroup walks the
+// stream, wave counts by ballot, the four wave counts added through LDS and
+// stored by one lane (no atomics).
+__global__ __launch_bounds__(256) void validate_kernel(const int64_t* __restrict__ idx, int batch, int64_t hi,
+                                                       int32_t* __restrict__ bad) {
+    __shared__ int32_t wc[4];
+    int32_t n = 0;
+    for (int j0 = 0; j0 < batch; j0 += 256) {
+        const int j = j0 + (int)threadIdx.x;
+        const bool out = j < batch && (idx[j] < 0 || idx[j] > hi);
+        n += __popcll(__ballot(out));
+    }
+    if ((threadIdx.x & 63) == 0) wc[threadIdx.x >> 6] = n;
+    __syncthreads();
+    if (threadIdx.x == 0) *bad = (wc[0] + wc[1]) + (wc[2] + wc[3]);
+}
+
 }  // namespace
+
+hipError_t launch_validate(const int64_t* idx, int batch, int64_t hi, int32_t* bad, hipStream_t st) {
+    hipLaunchKernelGGL(validate_kernel, dim3(1), dim3(256), 0, st, idx, batch, hi, bad);
+    return hipGetLastError();
+}
 
 hipError_t launch_gather(const uint8_t* frames, int64_t stride, int64_t rec_bytes,
                          const uint8_t* act, const int8_t* rew, const uint8_t* term,

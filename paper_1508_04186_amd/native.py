@@ -150,6 +150,8 @@ def lib():
         L.dqn_act.argtypes = [ctypes.POINTER(_CNet), _P, _P, ctypes.c_int32, _P, ctypes.c_float, _P, _P, _P,
                               _P, _P, ctypes.POINTER(_CReplayOut), ctypes.c_int64, _P, ctypes.c_size_t, _P]
         L.dqn_act.restype = ctypes.c_int
+        L.replay_gather_validate.argtypes = [ctypes.POINTER(_CReplay), _P, ctypes.c_int32, ctypes.c_int32, _P, _P]
+        L.replay_gather_validate.restype = ctypes.c_int
         L.replay_fill_synthetic.argtypes = [ctypes.POINTER(_CReplay), ctypes.c_int32, ctypes.c_uint64, _P]
         L.replay_fill_synthetic.restype = ctypes.c_int
         L.dqn_preprocess.argtypes = [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -645,3 +647,13 @@ def replay_fill_synthetic(replay: "Replay", n_actions: int, seed: int, stream=No
     """Fill a replay memory with the seeded synthetic stream (include/dqn.h)."""
     _check(lib().replay_fill_synthetic(ctypes.byref(_creplay(replay)), int(n_actions), int(seed) & (2**64 - 1),
                                        _stream(stream)), "replay_fill_synthetic")
+
+
+def replay_gather_validate(replay: "Replay", idx, bad_count, with_next: bool = True, stream=None) -> None:
+    """Count the indices of idx outside the valid range into bad_count
+    (device int32 [1]; include/dqn.h)."""
+    import torch
+    _check(lib().replay_gather_validate(ctypes.byref(_creplay(replay)), _ptr(idx, torch.int64, "idx"),
+                                        int(idx.numel()), 1 if with_next else 0,
+                                        _ptr(bad_count, torch.int32, "bad_count"), _stream(stream)),
+           "replay_gather_validate")

@@ -189,6 +189,20 @@ def test_gather_argument_errors():
 
 
 @fake_ptr_test
+def test_validate_argument_errors():
+    L = dq.lib()
+    rp = native._CReplay()
+    rp.frames, rp.action, rp.reward, rp.terminal = FAKE, FAKE, FAKE, FAKE
+    rp.record_stride, rp.size, rp.c, rp.h, rp.w = 28224, 100, 4, 84, 84
+    assert L.replay_gather_validate(None, FAKE, 4, 1, FAKE + 64, None) == dq.DQN_EINVAL
+    assert L.replay_gather_validate(ctypes.byref(rp), None, 4, 1, FAKE + 64, None) == dq.DQN_EINVAL
+    assert L.replay_gather_validate(ctypes.byref(rp), FAKE, 0, 1, FAKE + 64, None) == dq.DQN_EINVAL
+    assert L.replay_gather_validate(ctypes.byref(rp), FAKE, 4, 1, None, None) == dq.DQN_EINVAL
+    rp.size = 1                                               # no transition has a next state
+    assert L.replay_gather_validate(ctypes.byref(rp), FAKE, 4, 1, FAKE + 64, None) == dq.DQN_EINVAL
+
+
+@fake_ptr_test
 def test_fill_argument_errors():
     L = dq.lib()
     rp = native._CReplay()

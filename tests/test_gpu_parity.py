@@ -52,6 +52,29 @@ def test_gather_bit_exact(dev, replay, batch):
     assert np.array_equal(host(a), ra) and np.array_equal(host(r), rr) and np.array_equal(host(t), rt)
 
 
+def test_gather_validate_counts_out_of_range_indices(dev, replay):
+    """replay_gather_validate counts exactly the indices outside [0, size-2]
+    (with s') or [0, size-1] (states only), over several workgroup-widths."""
+    import torch
+    _, rp = replay
+    rng = np.random.default_rng(17)
+    idx = rng.integers(0, rp.size - 1, 700).astype(np.int64)
+    idx[[3, 200, 699]] = [-1, rp.size - 1, rp.size + 5]      # out with s'; size-1 is fine without
+    idx[511] = np.iinfo(np.int64).min
+    bad = torch.full((1,), -7, dtype=torch.int32, device=dev)
+    say("[gather] validate 700 indices")
+    dq.replay_gather_validate(rp, dev_tensor(idx), bad, with_next=True)
+    torch.cuda.synchronize()
+    want = int(((idx < 0) | (idx > rp.size - 2)).sum())
+    assert want == 4 and int(bad.item()) == want
+    dq.replay_gather_validate(rp, dev_tensor(idx), bad, with_next=False)
+    torch.cuda.synchronize()
+    assert int(bad.item()) == 3
+    dq.replay_gather_validate(rp, dev_tensor(np.arange(rp.size - 1, dtype=np.int64)), bad)
+    torch.cuda.synchronize()
+    assert int(bad.item()) == 0
+
+
 def test_gather_states_only_reaches_last_record(dev, replay):
     import torch
     hr, rp = replay
