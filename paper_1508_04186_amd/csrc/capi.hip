@@ -302,6 +302,12 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // The bf16-input variant reads the network input with the byte-input
     // conv1 kernels, which need 16-byte aligned samples.
     if (ni.bf16 && (!conv_s12_fwd_aligned(s0) || !conv_s12_fwd_aligned(sn0))) return DQN_EINVAL;
+    // bf16-input variant of the large network from 128 samples: conv1's and
+    // conv2's outputs are stored as bfloat16 values.  Every reader rounds them
+    // to bfloat16 anyway (conv2's and conv3's forward and weight gradient) or
+    // takes only their sign (the ReLU masks of the input gradients), and all
+    // of those readers are the kernels that accept bfloat16 storage.
+    const bool a16 = ni.bf16 && L == 3 && B >= kRegWgradMinRows && 2 * B >= kFwdClMinRows;
 
     // Forward of s under theta (samples 0..B-1) and of s' under theta^-
     // (samples B..2B-1): one launch per layer, or both conv layers of the
@@ -320,13 +326,14 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             RUN(DQN_K_CONV1_FWD,
                 launch_conv1_u8_fwd(CONV_L1, s0, sn0, B, 2 * B, th + ni.w_off[0], th + ni.b_off[0],
                                     tt + ni.w_off[0], tt + ni.b_off[0], t.act[0],
-                                    src.replay ? &side : nullptr, ni.bf16, st));
+                                    src.replay ? &side : nullptr, ni.bf16, a16, st));
             continue;
         }
         if (l > 0 && igemm_fwd(ni.conv[l], 2 * B, ni.bf16)) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], t.act[l - 1], B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
-                                      tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], ni.bf16, st));
+                                      tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], ni.bf16, a16, a16 && l < 2,
+                                      st));
             continue;
         }
         if (ni.bf16) return DQN_EUNSUPPORTED;  // the per-layer kernels are fp32 only
@@ -416,7 +423,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             chunks_used[0] = conv1_u8_wgrad_slots(B);
         } else if (reg_wgrad(ni.conv[l], B, ni.bf16)) {
             RUN(DQN_K_CONV1_WGRAD + l,
-                launch_conv_wgrad_reg(ni.conv[l], t.act[l - 1], t.dconv[l], B, t.wpart[l], t.bpart[l], ni.bf16, st));
+                launch_conv_wgrad_reg(ni.conv[l], t.act[l - 1], t.dconv[l], B, t.wpart[l], t.bpart[l], ni.bf16,
+                                      a16, st));
             chunks_used[l] = conv_wgrad_reg_slots(ni.conv[l], B);
         } else if (igemm_wgrad(ni.conv[l], B, ni.bf16)) {
             RUN(DQN_K_CONV1_WGRAD + l,
@@ -432,9 +440,9 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
                 ni.conv[l] == CONV_L2
                     ? launch_conv2_dgrad_phase(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
-                                               ni.bf16, st)
+                                               ni.bf16, a16, st)
                     : launch_conv3_dgrad(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
-                                         ni.bf16, st));
+                                         ni.bf16, a16, st));
         else if (l > 0 && igemm_dgrad(ni.conv[l], B, ni.bf16))
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
                 launch_conv_igemm_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],
@@ -608,17 +616,20 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
             launch_conv_s12_fwd(in0, in0, batch, batch, th + ni.w_off[0], th + ni.b_off[0],
                                 th + ni.w_off[1], th + ni.b_off[1], th + ni.w_off[0], th + ni.b_off[0],
                                 th + ni.w_off[1], th + ni.b_off[1], f.act[0], f.act[1], nullptr, st));
+    // bfloat16 storage of conv1's and conv2's outputs, as in the TD step
+    const bool a16 = ni.bf16 && ni.n_conv == 3 && batch >= kFwdClMinRows;
     for (int l = 0; l < ni.n_conv && !fused_fwd; ++l) {
         if (l == 0 && conv1_u8(ni.conv[0], batch, ni.bf16) && conv_s12_fwd_aligned(in0)) {
             RUN(DQN_K_CONV1_FWD,
                 launch_conv1_u8_fwd(CONV_L1, in0, in0, batch, batch, th + ni.w_off[0], th + ni.b_off[0],
-                                    th + ni.w_off[0], th + ni.b_off[0], f.act[0], nullptr, ni.bf16, st));
+                                    th + ni.w_off[0], th + ni.b_off[0], f.act[0], nullptr, ni.bf16, a16, st));
             continue;
         }
         if (l > 0 && igemm_fwd(ni.conv[l], batch, ni.bf16)) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], f.act[l - 1], batch, batch, th + ni.w_off[l], th + ni.b_off[l],
-                                      th + ni.w_off[l], th + ni.b_off[l], f.act[l], ni.bf16, st));
+                                      th + ni.w_off[l], th + ni.b_off[l], f.act[l], ni.bf16, a16, a16 && l < 2,
+                                      st));
             continue;
         }
         if (ni.bf16) return DQN_EUNSUPPORTED;  // the per-layer kernels are fp32 only

@@ -182,11 +182,14 @@ hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float*
 // Forward of the fp32-input large-network layers (CONV_L2, CONV_L3) as one
 // implicit GEMM over all n samples (dense input [n][cin][ih][iw]; samples
 // below n_a use (w_a, b_a), the rest (w_b, b_b)); bias + ReLU; output
-// [n][cout][oh][ow].  Weights 16-byte aligned.
+// [n][cout][oh][ow].  Weights 16-byte aligned.  In the bf16-input variant
+// from kFwdClMinRows samples, the input (in16) and the output (out16) may be
+// held as bfloat16 values: the contraction rounds its input to bfloat16
+// anyway, so only the storage changes.
 bool conv_igemm_fwd_supported(ConvId id);
 hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, const float* w_a,
                                  const float* b_a, const float* w_b, const float* b_b, float* out,
-                                 bool bf16, hipStream_t st);
+                                 bool bf16, bool in16, bool out16, hipStream_t st);
 
 // The forward of CONV_L2 / CONV_L3 from kFwdClMinRows samples on, both
 // precisions: weights held in registers, each sample staged channels-last in
@@ -195,7 +198,8 @@ hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, con
 constexpr int kFwdClMinRows = 256;
 bool conv_fwd_cl_use(ConvId id, int n, bool bf16);
 hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const float* w_a, const float* b_a,
-                              const float* w_b, const float* b_b, float* out, bool bf16, hipStream_t st);
+                              const float* w_b, const float* b_b, float* out, bool bf16, bool in16, bool out16,
+                              hipStream_t st);
 
 // Input gradient of CONV_L2 / CONV_L3 for n samples as an implicit GEMM per
 // stride phase, masked by [h_in > 0] (as launch_conv_dgrad).
@@ -206,21 +210,22 @@ hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, c
 // [h_in > 0] (as launch_conv_dgrad), with each phase's weights held in
 // registers and dz staged in LDS with a zero border.
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
-                                    bool bf16, hipStream_t st);
+                                    bool bf16, bool h16, hipStream_t st);
 
 // Input gradient of CONV_L3 for n samples, masked by [h_in > 0], in the same
 // arrangement (weights in registers, zero-bordered dz in LDS, the sample's
 // gradient assembled in LDS).  h_in and din 16-byte aligned.
 hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
-                              hipStream_t st);
+                              bool h16, hipStream_t st);
 
 // Weight/bias gradient partial sums of CONV_L2 or CONV_L3 for n samples, one
 // workgroup per run of samples holding every output in registers:
 // conv_wgrad_reg_slots(id, n) slots of wpart [slots][64][cin*k*k] and bpart
-// [slots][64].  in: the layer input [n][cin][ih][iw] (floats).
+// [slots][64].  in: the layer input [n][cin][ih][iw] (floats, or bfloat16
+// values when in16).
 int conv_wgrad_reg_slots(ConvId id, int n);
 hipError_t launch_conv_wgrad_reg(ConvId id, const float* in, const float* dz, int n, float* wpart, float* bpart,
-                                 bool bf16, hipStream_t st);
+                                 bool bf16, bool in16, hipStream_t st);
 
 // Weight/bias gradient partial sums of a large-network layer for n samples as
 // an implicit GEMM over pixel chunks: conv_igemm_wgrad_chunks(id, n) slots of
@@ -237,7 +242,7 @@ hipError_t launch_conv_igemm_wgrad(ConvId id, const ConvIn& in, const float* dz,
 bool conv1_u8_fwd_supported(ConvId id);
 hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
                                const float* w_a, const float* b_a, const float* w_b, const float* b_b,
-                               float* out, const SideFields* side, bool bf16, hipStream_t st);
+                               float* out, const SideFields* side, bool bf16, bool out16, hipStream_t st);
 
 // conv1 weight/bias gradient on byte input (CONV_L1 or CONV_S1) for many
 // samples: conv1_u8_wgrad_slots(n) partial-sum slots of wpart

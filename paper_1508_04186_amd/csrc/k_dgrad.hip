@@ -47,10 +47,21 @@ static_assert(D2_IN % 4 == 0, "whole float4 rows");
 struct Dgrad2Params {
     const float* dz;    // [n][64][9][9]
     const float* w;     // [64][32][4][4]
-    const float* h_in;  // [n][32][20][20]
+    const float* h_in;  // [n][32][20][20] (bfloat16 values when h16)
     float* din;         // [n][32][20][20]
     int n, spg;         // samples, samples per workgroup
 };
+
+// Four consecutive values of the layer input h_in (the ReLU mask source) at
+// element offset off (a multiple of 4), as floats; H16: h_in holds bfloat16.
+template <bool H16>
+__device__ __forceinline__ f4 mask4(const Dgrad2Params& p, size_t off) {
+    if constexpr (H16) {
+        const bf16x4 h = *(const bf16x4*)((const __bf16*)p.h_in + off);
+        return f4{(float)h[0], (float)h[1], (float)h[2], (float)h[3]};
+    }
+    return *(const f4*)(p.h_in + off);
+}
 
 __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p) {
     __shared__ float s_dz[D2_STAGE];
@@ -125,7 +136,7 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p
 #pragma unroll
         for (int u = 0; u < D2_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
-            if (e4 < D2_IN / 4) mreg[u] = *(const f4*)(p.h_in + o0 + 4 * e4);
+            if (e4 < D2_IN / 4) mreg[u] = mask4<false>(p, o0 + 4 * e4);
         }
 
         f4 acc[D2_MT];
@@ -199,6 +210,7 @@ constexpr int D2C_PAIRS = D2_DZ / 2;           // (channel pair, pixel) items
 constexpr int D2C_PER = (D2C_PAIRS + D2_WG - 1) / D2_WG;
 static_assert(D2C_PSB % 16 == 0 && D2C_PSB >= 2 * D2_COUT, "slot size");
 
+template <bool H16>
 __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
     __shared__ __align__(16) unsigned char s_cl[D2C_SLOTS * D2C_PSB];
     __shared__ __align__(16) float s_din[D2_IN];
@@ -276,7 +288,7 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
 #pragma unroll
         for (int u = 0; u < D2_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
-            if (e4 < D2_IN / 4) mreg[u] = *(const f4*)(p.h_in + o0 + 4 * e4);
+            if (e4 < D2_IN / 4) mreg[u] = mask4<H16>(p, o0 + 4 * e4);
         }
 
         f4 acc[D2_MT];
@@ -422,7 +434,7 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
 #pragma unroll
         for (int u = 0; u < D3_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
-            if (e4 < D3_IN / 4) mreg[u] = *(const f4*)(p.h_in + o0 + 4 * e4);
+            if (e4 < D3_IN / 4) mreg[u] = mask4<false>(p, o0 + 4 * e4);
         }
 
         f4 acc[D3_TPW];
@@ -483,6 +495,7 @@ constexpr int D3C_PSB = 144;
 constexpr int D3C_PAIRS = D3_DZ / 2;
 constexpr int D3C_PER = (D3C_PAIRS + D2_WG - 1) / D2_WG;
 
+template <bool H16>
 __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
     __shared__ __align__(16) unsigned char s_cl[D3C_SLOTS * D3C_PSB];
     __shared__ __align__(16) float s_din[D3_IN];
@@ -554,7 +567,7 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
 #pragma unroll
         for (int u = 0; u < D3_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
-            if (e4 < D3_IN / 4) mreg[u] = *(const f4*)(p.h_in + o0 + 4 * e4);
+            if (e4 < D3_IN / 4) mreg[u] = mask4<H16>(p, o0 + 4 * e4);
         }
 
         f4 acc[D3_TPW];
@@ -607,27 +620,31 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
 }  // namespace
 
 hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
-                              hipStream_t st) {
-    if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15)) return hipErrorInvalidValue;
+                              bool h16, hipStream_t st) {
+    if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15) || (h16 && !bf16)) return hipErrorInvalidValue;
     const int spg = std::max(1, (n + 255) / 256);
     const int blocks = (n + spg - 1) / spg;
     const Dgrad2Params prm{dz, w, h_in, din, n, spg};
-    if (bf16)
-        hipLaunchKernelGGL(conv3_dgrad_cl_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    if (bf16 && h16)
+        hipLaunchKernelGGL(conv3_dgrad_cl_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    else if (bf16)
+        hipLaunchKernelGGL(conv3_dgrad_cl_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else
         hipLaunchKernelGGL(conv3_dgrad_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     return hipGetLastError();
 }
 
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
-                                    bool bf16, hipStream_t st) {
-    if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15)) return hipErrorInvalidValue;
+                                    bool bf16, bool h16, hipStream_t st) {
+    if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15) || (h16 && !bf16)) return hipErrorInvalidValue;
     // about one workgroup per CU, one sample per round
     const int spg = std::max(1, (n + 255) / 256);
     const int blocks = (n + spg - 1) / spg;
     const Dgrad2Params prm{dz, w, h_in, din, n, spg};
-    if (bf16)
-        hipLaunchKernelGGL(conv2_dgrad_cl_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    if (bf16 && h16)
+        hipLaunchKernelGGL(conv2_dgrad_cl_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    else if (bf16)
+        hipLaunchKernelGGL(conv2_dgrad_cl_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else
         hipLaunchKernelGGL(conv2_dgrad_phase_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     return hipGetLastError();

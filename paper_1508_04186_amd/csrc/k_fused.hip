@@ -671,11 +671,11 @@ struct U8FwdParams {
     ConvIn in_a, in_b;
     int n_a, n, spb, blocks_a;   // samples per workgroup; workgroups of set a
     const float *w_a, *b_a, *w_b, *b_b;
-    float* out;                  // [n][COUT][20][20]
+    float* out;                  // [n][COUT][20][20], bfloat16 values when out16
     SideFields side;
 };
 
-template <int COUT, int PARTS>
+template <int COUT, int PARTS, bool OUT16>
 __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
     constexpr int REC = C0 * H0 * H0;            // bytes per sample (28,224)
     constexpr int RV = REC / 16;                 // 16-byte units (1,764)
@@ -811,7 +811,14 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
                     f4 v;
 #pragma unroll
                     for (int r = 0; r < 4; ++r) v[r] = fmaxf(acc[i][nt][r] * inv255 + bo, 0.f);
-                    *(f4*)(oj + (size_t)o * H1 * H1 + pb) = v;
+                    if constexpr (OUT16) {
+                        bf16x4 h;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) h[r] = (__bf16)v[r];
+                        *(bf16x4*)((__bf16*)p.out + ((size_t)j * COUT + o) * H1 * H1 + pb) = h;
+                    } else {
+                        *(f4*)(oj + (size_t)o * H1 * H1 + pb) = v;
+                    }
                 }
             }
         }
@@ -825,9 +832,9 @@ bool conv1_u8_fwd_supported(ConvId id) { return id == CONV_L1 || id == CONV_S1; 
 
 hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b, int n_a, int n,
                                const float* w_a, const float* b_a, const float* w_b, const float* b_b,
-                               float* out, const SideFields* side, bool bf16, hipStream_t st) {
+                               float* out, const SideFields* side, bool bf16, bool out16, hipStream_t st) {
     if (n <= 0 || n_a < 0 || n_a > n || !conv_s12_fwd_aligned(in_a) || !conv_s12_fwd_aligned(in_b) ||
-        ((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15))
+        ((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15) || ((uintptr_t)out & 15) || (out16 && !bf16))
         return hipErrorInvalidValue;
     // about 512 workgroups (two per compute unit, so one's loads overlap the
     // other's MFMAs): a few samples each, so the weight split is amortized
@@ -841,8 +848,12 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
         hipLaunchKernelGGL(kern, grid, dim3(WG), lds, st, prm);
         return hipGetLastError();
     };
-    if (id == CONV_L1) return bf16 ? go(conv1_u8_fwd_kernel<32, 1>, 32, 1) : go(conv1_u8_fwd_kernel<32, 3>, 32, 3);
-    if (id == CONV_S1) return bf16 ? go(conv1_u8_fwd_kernel<16, 1>, 16, 1) : go(conv1_u8_fwd_kernel<16, 3>, 16, 3);
+    if (id == CONV_L1) {
+        if (out16) return go(conv1_u8_fwd_kernel<32, 1, true>, 32, 1);
+        return bf16 ? go(conv1_u8_fwd_kernel<32, 1, false>, 32, 1) : go(conv1_u8_fwd_kernel<32, 3, false>, 32, 3);
+    }
+    if (id == CONV_S1 && !out16)
+        return bf16 ? go(conv1_u8_fwd_kernel<16, 1, false>, 16, 1) : go(conv1_u8_fwd_kernel<16, 3, false>, 16, 3);
     return hipErrorInvalidValue;
 }
 

@@ -51,13 +51,13 @@ struct FwdClGeom {
 };
 
 struct FwdClParams {
-    const float* in;           // [n][cin][ih][ih]
-    float* out;                // [n][64][oh][oh]
+    const float* in;           // [n][cin][ih][ih] (bfloat16 values when in16)
+    float* out;                // [n][64][oh][oh] (bfloat16 values when out16)
     const float *w_a, *b_a, *w_b, *b_b;
     int n, n_a, g_a, spg;      // blocks [0, g_a) take samples [0, n_a), the rest [n_a, n); runs of spg
 };
 
-template <int CIN, int IH, int K, int S, int OH, int SPR>
+template <int CIN, int IH, int K, int S, int OH, int SPR, bool IN16, bool OUT16>
 __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
     using G = FwdClGeom<CIN, IH, K, S, OH, SPR>;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -86,13 +86,19 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
         for (int s = 0; s < SPR; ++s) {
             if (j + s >= j_hi) break;
             const float* x = p.in + (size_t)(j + s) * G::IN;
+            const __bf16* xh = (const __bf16*)p.in + (size_t)(j + s) * G::IN;
 #pragma unroll
             for (int u = 0; u < G::PER; ++u) {
                 const int q = t + u * FC_WG;
                 if (q < G::PAIRS) {
                     const int cp = q / G::IP, pix = q - cp * G::IP;
-                    va[s][u] = x[(2 * cp) * G::IP + pix];
-                    vb[s][u] = x[(2 * cp + 1) * G::IP + pix];
+                    if constexpr (IN16) {   // bf16 to float is exact; stage rounds it back unchanged
+                        va[s][u] = (float)xh[(2 * cp) * G::IP + pix];
+                        vb[s][u] = (float)xh[(2 * cp + 1) * G::IP + pix];
+                    } else {
+                        va[s][u] = x[(2 * cp) * G::IP + pix];
+                        vb[s][u] = x[(2 * cp + 1) * G::IP + pix];
+                    }
                 }
             }
         }
@@ -206,24 +212,37 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
                 }
         __syncthreads();
         const int ns = min(SPR, j_hi - j);
-        f4* dst = (f4*)(p.out + (size_t)j * G::OUTF);
-        for (int q = t; q < ns * G::OUTF / 4; q += FC_WG) dst[q] = ((const f4*)s_out)[q];
+        if constexpr (OUT16) {
+            bf16x4* dst = (bf16x4*)((__bf16*)p.out + (size_t)j * G::OUTF);
+            for (int q = t; q < ns * G::OUTF / 4; q += FC_WG) {
+                const f4 v = ((const f4*)s_out)[q];
+                dst[q] = bf16x4{(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+            }
+        } else {
+            f4* dst = (f4*)(p.out + (size_t)j * G::OUTF);
+            for (int q = t; q < ns * G::OUTF / 4; q += FC_WG) dst[q] = ((const f4*)s_out)[q];
+        }
     }
 }
 
 template <int CIN, int IH, int K, int S, int OH, int SPR>
 hipError_t fwd_cl_launch(const float* in, int n_a, int n, const float* w_a, const float* b_a, const float* w_b,
-                         const float* b_b, float* out, hipStream_t st) {
+                         const float* b_b, float* out, bool in16, bool out16, hipStream_t st) {
     using G = FwdClGeom<CIN, IH, K, S, OH, SPR>;
     if (n <= 0 || n_a < 0 || n_a > n) return hipErrorInvalidValue;
     if (((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15) || ((uintptr_t)out & 15)) return hipErrorInvalidValue;
     const int spg = std::max(1, (n + FC_TARGET_BLOCKS - 1) / FC_TARGET_BLOCKS);
     const int g_a = (n_a + spg - 1) / spg, g_b = (n - n_a + spg - 1) / spg;
     const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg};
-    auto kern = conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR>;
-    if (!allow_lds((const void*)kern, G::LDS)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(g_a + g_b)), dim3(FC_WG), G::LDS, st, prm);
-    return hipGetLastError();
+    auto go = [&](auto kern) -> hipError_t {
+        if (!allow_lds((const void*)kern, G::LDS)) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(kern, dim3((unsigned)(g_a + g_b)), dim3(FC_WG), G::LDS, st, prm);
+        return hipGetLastError();
+    };
+    if (in16 && out16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, true, true>);
+    if (in16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, true, false>);
+    if (out16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, false, true>);
+    return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, false, false>);
 }
 
 // The fp32 variant: v_mfma_f32_16x16x4_f32, weights held in registers as
@@ -380,13 +399,15 @@ bool conv_fwd_cl_use(ConvId id, int n, bool bf16) {
 }
 
 hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const float* w_a, const float* b_a,
-                              const float* w_b, const float* b_b, float* out, bool bf16, hipStream_t st) {
+                              const float* w_b, const float* b_b, float* out, bool bf16, bool in16, bool out16,
+                              hipStream_t st) {
+    if (!bf16 && (in16 || out16)) return hipErrorInvalidValue;   // bf16 activations: the bf16 variant only
     switch (id) {
         case CONV_L2:
-            return bf16 ? fwd_cl_launch<32, 20, 4, 2, 9, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, st)
+            return bf16 ? fwd_cl_launch<32, 20, 4, 2, 9, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, st)
                         : fwd_cl32_launch<32, 20, 4, 2, 9>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
         case CONV_L3:
-            return bf16 ? fwd_cl_launch<64, 9, 3, 1, 7, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, st)
+            return bf16 ? fwd_cl_launch<64, 9, 3, 1, 7, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, st)
                         : fwd_cl32_launch<64, 9, 3, 1, 7>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
         default: return hipErrorInvalidValue;
     }

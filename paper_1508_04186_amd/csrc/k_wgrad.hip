@@ -50,14 +50,14 @@ struct WgradGeom {
 };
 
 struct WgradRegParams {
-    const float* in;    // [n][cin][ih][ih]
+    const float* in;    // [n][cin][ih][ih] (bfloat16 values when in16)
     const float* dz;    // [n][64][oh][oh]
     float* wpart;       // [slots][64][cin*k*k]
     float* bpart;       // [slots][64]
     int n, spg;         // samples; samples per workgroup (slot)
 };
 
-template <int CIN, int IH, int K, int S, int OH, bool BF16, int MS>
+template <int CIN, int IH, int K, int S, int OH, bool BF16, int MS, bool IN16>
 __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p) {
     using G = WgradGeom<CIN, IH, K, S, OH>;
     static_assert(MS == 1 || MS == 2, "one or two workgroups per slot");
@@ -110,6 +110,7 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p)
     auto fetch = [&](int j) {
         const float* dzj = p.dz + (size_t)j * G::DZ;
         const float* inj = p.in + (size_t)j * G::IN;
+        const __bf16* inh = (const __bf16*)p.in + (size_t)j * G::IN;
 #pragma unroll
         for (int u = 0; u < G::PER_DZ; ++u) {
             const int e = t + u * WR_WG;
@@ -118,7 +119,8 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p)
 #pragma unroll
         for (int u = 0; u < G::PER_IN; ++u) {
             const int e = t + u * WR_WG;
-            vin[u] = e < G::IN ? inj[e] : 0.f;
+            if constexpr (IN16) vin[u] = e < G::IN ? (float)inh[e] : 0.f;
+            else vin[u] = e < G::IN ? inj[e] : 0.f;
         }
     };
     auto stage = [&]() {
@@ -214,11 +216,12 @@ int wgrad_reg_spg(int cin, int n) { return wgrad_reg_ms(cin, n) == 2 ? 2 : std::
 
 template <int CIN, int IH, int K, int S, int OH>
 hipError_t wgrad_reg_launch(const float* in, const float* dz, int n, float* wpart, float* bpart, bool bf16,
-                            hipStream_t st) {
+                            bool in16, hipStream_t st) {
     using G = WgradGeom<CIN, IH, K, S, OH>;
     if (n <= 0) return hipErrorInvalidValue;
     const int spg = wgrad_reg_spg(CIN, n), ms = wgrad_reg_ms(CIN, n);
     const int blocks = (n + spg - 1) / spg * ms;
+    if (in16 && !bf16) return hipErrorInvalidValue;
     const WgradRegParams prm{in, dz, wpart, bpart, n, spg};
     constexpr size_t lds = (size_t)G::LDS * 4;
     auto go = [&](auto kern) -> hipError_t {
@@ -226,11 +229,14 @@ hipError_t wgrad_reg_launch(const float* in, const float* dz, int n, float* wpar
         hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(WR_WG), lds, st, prm);
         return hipGetLastError();
     };
-    if (ms == 2)
-        return bf16 ? go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, true, 2>)
-                    : go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, false, 2>);
-    return bf16 ? go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, true, 1>)
-                : go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, false, 1>);
+    if (ms == 2) {
+        if (in16) return go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, true, 2, true>);
+        return bf16 ? go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, true, 2, false>)
+                    : go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, false, 2, false>);
+    }
+    if (in16) return go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, true, 1, true>);
+    return bf16 ? go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, true, 1, false>)
+                : go(conv_wgrad_reg_kernel<CIN, IH, K, S, OH, false, 1, false>);
 }
 
 }  // namespace
@@ -242,10 +248,10 @@ int conv_wgrad_reg_slots(ConvId id, int n) {
 }
 
 hipError_t launch_conv_wgrad_reg(ConvId id, const float* in, const float* dz, int n, float* wpart, float* bpart,
-                                 bool bf16, hipStream_t st) {
+                                 bool bf16, bool in16, hipStream_t st) {
     switch (id) {
-        case CONV_L2: return wgrad_reg_launch<32, 20, 4, 2, 9>(in, dz, n, wpart, bpart, bf16, st);
-        case CONV_L3: return wgrad_reg_launch<64, 9, 3, 1, 7>(in, dz, n, wpart, bpart, bf16, st);
+        case CONV_L2: return wgrad_reg_launch<32, 20, 4, 2, 9>(in, dz, n, wpart, bpart, bf16, in16, st);
+        case CONV_L3: return wgrad_reg_launch<64, 9, 3, 1, 7>(in, dz, n, wpart, bpart, bf16, in16, st);
         default: return hipErrorInvalidValue;
     }
 }
