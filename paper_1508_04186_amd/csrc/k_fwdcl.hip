@@ -79,9 +79,31 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
     const float* __restrict__ bias = second ? p.b_b : p.b_a;
 
     // SPR samples per round: sample j + s of the round is read into
-    // registers (va, vb) and staged into s_in buffer s.
-    float va[SPR][G::PER], vb[SPR][G::PER];
+    // registers (va, vb) and staged into s_in buffer s.  bfloat16 input with
+    // an even pixel count (conv2's) is read as 32-bit words of two pixels of
+    // one channel and restaged bit for bit, without conversions.
+    constexpr bool W32 = IN16 && G::IP % 2 == 0;
+    constexpr int PER2 = ((CIN / 2) * (G::IP / 2) + FC_WG - 1) / FC_WG;
+    float va[SPR][W32 ? 1 : G::PER], vb[SPR][W32 ? 1 : G::PER];
+    uint32_t wa[SPR][W32 ? PER2 : 1], wb[SPR][W32 ? PER2 : 1];
     auto fetch = [&](int j) {
+        if constexpr (W32) {
+#pragma unroll
+            for (int s = 0; s < SPR; ++s) {
+                if (j + s >= j_hi) break;
+                const uint32_t* x = (const uint32_t*)((const __bf16*)p.in + (size_t)(j + s) * G::IN);
+#pragma unroll
+                for (int u = 0; u < PER2; ++u) {
+                    const int q = t + u * FC_WG;
+                    if (q < (CIN / 2) * (G::IP / 2)) {
+                        const int cp = q / (G::IP / 2), w = q - cp * (G::IP / 2);
+                        wa[s][u] = x[(2 * cp) * (G::IP / 2) + w];       // channel 2cp, pixels 2w, 2w+1
+                        wb[s][u] = x[(2 * cp + 1) * (G::IP / 2) + w];   // channel 2cp+1
+                    }
+                }
+            }
+            return;
+        }
 #pragma unroll
         for (int s = 0; s < SPR; ++s) {
             if (j + s >= j_hi) break;
@@ -104,6 +126,24 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
         }
     };
     auto stage = [&](int j) {
+        if constexpr (W32) {
+#pragma unroll
+            for (int s = 0; s < SPR; ++s) {
+                if (j + s >= j_hi) break;
+#pragma unroll
+                for (int u = 0; u < PER2; ++u) {
+                    const int q = t + u * FC_WG;
+                    if (q < (CIN / 2) * (G::IP / 2)) {
+                        const int cp = q / (G::IP / 2), w = q - cp * (G::IP / 2);
+                        const uint32_t a = wa[s][u], b = wb[s][u];
+                        unsigned char* d = s_in + (s * G::IP + 2 * w) * G::PSB + 4 * cp;
+                        *(uint32_t*)d = (a & 0xffffu) | (b << 16);                       // pixel 2w
+                        *(uint32_t*)(d + G::PSB) = (a >> 16) | (b & 0xffff0000u);        // pixel 2w+1
+                    }
+                }
+            }
+            return;
+        }
 #pragma unroll
         for (int s = 0; s < SPR; ++s) {
             if (j + s >= j_hi) break;

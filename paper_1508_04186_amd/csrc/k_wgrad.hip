@@ -106,21 +106,32 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p)
         for (int i = 0; i < G::NPW; ++i) acc[m][i] = f4{0.f, 0.f, 0.f, 0.f};
     float bsum = 0.f;
 
-    float vdz[G::PER_DZ], vin[G::PER_IN];
+    // bfloat16 input (IN16) is read as 32-bit words of two values
+    static_assert(G::IN % 2 == 0, "whole words of bfloat16 input");
+    constexpr int PER_IN2 = (G::IN / 2 + WR_WG - 1) / WR_WG;
+    float vdz[G::PER_DZ], vin[IN16 ? 1 : G::PER_IN];
+    uint32_t vin2[IN16 ? PER_IN2 : 1];
     auto fetch = [&](int j) {
         const float* dzj = p.dz + (size_t)j * G::DZ;
         const float* inj = p.in + (size_t)j * G::IN;
-        const __bf16* inh = (const __bf16*)p.in + (size_t)j * G::IN;
+        const uint32_t* inw = (const uint32_t*)((const __bf16*)p.in + (size_t)j * G::IN);
 #pragma unroll
         for (int u = 0; u < G::PER_DZ; ++u) {
             const int e = t + u * WR_WG;
             vdz[u] = e < G::DZ ? dzj[e] : 0.f;
         }
+        if constexpr (IN16) {
 #pragma unroll
-        for (int u = 0; u < G::PER_IN; ++u) {
-            const int e = t + u * WR_WG;
-            if constexpr (IN16) vin[u] = e < G::IN ? (float)inh[e] : 0.f;
-            else vin[u] = e < G::IN ? inj[e] : 0.f;
+            for (int u = 0; u < PER_IN2; ++u) {
+                const int e = t + u * WR_WG;
+                vin2[u] = e < G::IN / 2 ? inw[e] : 0u;
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < G::PER_IN; ++u) {
+                const int e = t + u * WR_WG;
+                vin[u] = e < G::IN ? inj[e] : 0.f;
+            }
         }
     };
     auto stage = [&]() {
@@ -132,10 +143,21 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_reg_kernel(WgradRegParams p)
                 s_dz[o * G::DCS + e - o * G::P] = vdz[u];
             }
         }
+        if constexpr (IN16) {   // a bfloat16 is the top half of the float it stands for
 #pragma unroll
-        for (int u = 0; u < G::PER_IN; ++u) {
-            const int e = t + u * WR_WG;
-            if (e < G::IN) s_in[e] = vin[u];
+            for (int u = 0; u < PER_IN2; ++u) {
+                const int e = t + u * WR_WG;
+                if (e < G::IN / 2) {
+                    s_in[2 * e] = __builtin_bit_cast(float, vin2[u] << 16);
+                    s_in[2 * e + 1] = __builtin_bit_cast(float, vin2[u] & 0xffff0000u);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < G::PER_IN; ++u) {
+                const int e = t + u * WR_WG;
+                if (e < G::IN) s_in[e] = vin[u];
+            }
         }
     };
 
