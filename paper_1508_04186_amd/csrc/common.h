@@ -113,6 +113,41 @@ struct SideFields {
     int batch;
 };
 
+// The copy of SideFields split into stages, so that its two dependent
+// global round trips (the index, then the fields it selects) overlap the
+// caller's own loads and arithmetic: begin() loads thread t's index, fetch()
+// the fields, end() stores them and copies any transitions from nthreads on
+// with a plain loop.  on: the copying workgroup.
+struct SideCopy {
+    int64_t i = 0;
+    uint8_t a = 0, term = 0;
+    int8_t r = 0;
+    __device__ void begin(const SideFields& s, bool on, int t) {
+        if (on && t < s.batch) i = s.idx[t];
+    }
+    __device__ void fetch(const SideFields& s, bool on, int t) {
+        if (on && t < s.batch) {
+            a = s.action[i];
+            r = s.reward[i];
+            term = s.terminal[i];
+        }
+    }
+    __device__ void end(const SideFields& s, bool on, int t, int nthreads) {
+        if (!on) return;
+        if (t < s.batch) {
+            s.a_out[t] = a;
+            s.r_out[t] = (float)r;
+            s.t_out[t] = term;
+        }
+        for (int j = t + nthreads; j < s.batch; j += nthreads) {
+            const int64_t k = s.idx[j];
+            s.a_out[j] = s.action[k];
+            s.r_out[j] = (float)s.reward[k];
+            s.t_out[j] = s.terminal[k];
+        }
+    }
+};
+
 // ---- launchers (host side); every one returns hipGetLastError() ----------
 
 // Measurement hook (dqn_profile.h): the event pair of kernel id `kid` around

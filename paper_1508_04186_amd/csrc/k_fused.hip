@@ -93,14 +93,10 @@ __global__ __launch_bounds__(WG) void conv_s12_fwd_kernel(FusedFwdParams p) {
     const float* b2 = second ? p.b2_b : p.b2_a;
     const int t = threadIdx.x;
 
-    if (p.side.idx && blockIdx.x == 0) {
-        for (int j = t; j < p.side.batch; j += WG) {
-            const int64_t i = p.side.idx[j];
-            p.side.a_out[j] = p.side.action[i];
-            p.side.r_out[j] = (float)p.side.reward[i];
-            p.side.t_out[j] = p.side.terminal[i];
-        }
-    }
+    // side fields of the transitions (block 0), in stages around the work
+    const bool side_on = p.side.idx && blockIdx.x == 0;
+    SideCopy side;
+    side.begin(p.side, side_on, t);
 
     // ---- staging: every global load of the workgroup is issued before the
     // first LDS store.  Input rows [band*R2*S2*S1, +R0) of each channel are
@@ -180,6 +176,7 @@ __global__ __launch_bounds__(WG) void conv_s12_fwd_kernel(FusedFwdParams p) {
     }
     if (t < C1 + C2) s_b[t] = bias;
     __syncthreads();
+    side.fetch(p.side, side_on, t);   // in flight during conv1 (a barrier waits for loads)
 
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
@@ -331,6 +328,7 @@ __global__ __launch_bounds__(WG) void conv_s12_fwd_kernel(FusedFwdParams p) {
         }
         static_assert(MT2 * NT2 * 64 == WG, "one thread per output lane of the band");
     }
+    side.end(p.side, side_on, t, WG);
 }
 
 // ---------------------------------------------------------------------------
@@ -699,15 +697,16 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
     const float* bias = second ? p.b_b : p.b_a;
     const int t = threadIdx.x;
 
-    if (p.side.idx && blockIdx.x == 0) {
-        for (int j = t; j < p.side.batch; j += WG) {
-            const int64_t i = p.side.idx[j];
-            p.side.a_out[j] = p.side.action[i];
-            p.side.r_out[j] = (float)p.side.reward[i];
-            p.side.t_out[j] = p.side.terminal[i];
-        }
+    // side fields of the transitions (block 0, which always has samples),
+    // in stages around the work
+    const bool side_on = p.side.idx && blockIdx.x == 0;
+    SideCopy side;
+    side.begin(p.side, side_on, t);
+    if (j0 >= j1) {  // uniform
+        side.fetch(p.side, side_on, t);
+        side.end(p.side, side_on, t, WG);
+        return;
     }
-    if (j0 >= j1) return;  // uniform
 
     auto sample_src = [&](int j) -> const f4* {
         return (const f4*)(j < p.n_a ? sample_ptr(p.in_a, j) : sample_ptr(p.in_b, j - p.n_a));
@@ -750,6 +749,7 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
         }
     }
     if (t < COUT) s_b[t] = bias[t];
+    side.fetch(p.side, side_on, t);   // in flight during the first sample
 
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
@@ -824,6 +824,7 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
         }
         __syncthreads();  // all reads of s_in done before the next sample is stored
     }
+    side.end(p.side, side_on, t, WG);
 }
 
 }  // namespace

@@ -405,10 +405,16 @@ __global__ __launch_bounds__(256) void finalize_small_kernel(FinalizeArgs a, PsU
         const int k = (int)(i / a.H), h = (int)(i - (int64_t)k * a.H);
         const int q = threadIdx.x & 7;
         float s0 = 0.f, s1 = 0.f;
+        // every load issued before the action test that selects it (an index
+        // past the batch reads sample j and is not added)
+#pragma unroll 4
         for (int j = q; j < a.B; j += 16) {
-            const float t0 = clamp_action(a.action[j], a.A) == k ? a.delta[j] * a.h1s[(int64_t)j * a.H + h] : 0.f;
-            const float t1 = (j + 8 < a.B && clamp_action(a.action[j + 8], a.A) == k)
-                                 ? a.delta[j + 8] * a.h1s[(int64_t)(j + 8) * a.H + h] : 0.f;
+            const int jb = j + 8 < a.B ? j + 8 : j;
+            const int a0 = a.action[j], a1 = a.action[jb];
+            const float d0 = a.delta[j], d1 = a.delta[jb];
+            const float h0 = a.h1s[(int64_t)j * a.H + h], h1 = a.h1s[(int64_t)jb * a.H + h];
+            const float t0 = clamp_action(a0, a.A) == k ? d0 * h0 : 0.f;
+            const float t1 = (j + 8 < a.B && clamp_action(a1, a.A) == k) ? d1 * h1 : 0.f;
             s0 += t0;
             s1 += t1;
         }
@@ -423,7 +429,12 @@ __global__ __launch_bounds__(256) void finalize_small_kernel(FinalizeArgs a, PsU
     if (i < a.A) {
         const int q = threadIdx.x & 7;
         float s = 0.f;
-        for (int j = q; j < a.B; j += 8) s += clamp_action(a.action[j], a.A) == (int)i ? a.delta[j] : 0.f;
+#pragma unroll 4
+        for (int j = q; j < a.B; j += 8) {
+            const int aj = a.action[j];
+            const float dj = a.delta[j];
+            s += clamp_action(aj, a.A) == (int)i ? dj : 0.f;
+        }
         s += __shfl_xor(s, 1, 64);
         s += __shfl_xor(s, 2, 64);
         s += __shfl_xor(s, 4, 64);
