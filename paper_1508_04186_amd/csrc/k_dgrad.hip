@@ -53,15 +53,25 @@ struct Dgrad2Params {
 };
 
 // Four consecutive values of the layer input h_in (the ReLU mask source) at
-// element offset off (a multiple of 4), as floats; H16: h_in holds bfloat16.
+// element offset off (a multiple of 4): floats, or, with H16 (h_in holds
+// bfloat16), the raw 16-bit values, tested only where the mask is applied so
+// that nothing waits for the load before then.
 template <bool H16>
-__device__ __forceinline__ f4 mask4(const Dgrad2Params& p, size_t off) {
-    if constexpr (H16) {
-        const bf16x4 h = *(const bf16x4*)((const __bf16*)p.h_in + off);
-        return f4{(float)h[0], (float)h[1], (float)h[2], (float)h[3]};
+struct Mask4 {
+    f4 v;
+    __device__ void load(const Dgrad2Params& p, size_t off) { v = *(const f4*)(p.h_in + off); }
+    __device__ bool pos(int k) const { return v[k] > 0.f; }
+};
+template <>
+struct Mask4<true> {
+    uint2 v;
+    __device__ void load(const Dgrad2Params& p, size_t off) { v = *(const uint2*)((const __bf16*)p.h_in + off); }
+    __device__ bool pos(int k) const {   // > 0: sign clear, nonzero, not a NaN (bits 0x0001..0x7f80)
+        const uint32_t w = k < 2 ? v.x : v.y;
+        const uint32_t b = (w >> (16 * (k & 1))) & 0xffffu;
+        return b - 1u < 0x7f80u;
     }
-    return *(const f4*)(p.h_in + off);
-}
+};
 
 __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p) {
     __shared__ float s_dz[D2_STAGE];
@@ -132,11 +142,11 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p
         if (j + 1 < j_hi) fetch(j + 1);  // in flight during this sample's MFMAs
         // this sample's ReLU mask, for the write-out below
         const size_t o0 = (size_t)j * D2_IN;
-        f4 mreg[D2_OUT4];
+        Mask4<false> mreg[D2_OUT4];
 #pragma unroll
         for (int u = 0; u < D2_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
-            if (e4 < D2_IN / 4) mreg[u] = mask4<false>(p, o0 + 4 * e4);
+            if (e4 < D2_IN / 4) mreg[u].load(p, o0 + 4 * e4);
         }
 
         f4 acc[D2_MT];
@@ -184,11 +194,10 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p
         for (int u = 0; u < D2_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
             if (e4 < D2_IN / 4) {
-                const f4 h = mreg[u];
                 const f4 d = *(const f4*)(s_din + 4 * e4);
                 f4 o;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) o[k] = h[k] > 0.f ? d[k] : 0.f;
+                for (int k = 0; k < 4; ++k) o[k] = mreg[u].pos(k) ? d[k] : 0.f;
                 *(f4*)(p.din + o0 + 4 * e4) = o;
             }
         }
@@ -284,11 +293,11 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
         if (j + 1 < j_hi) fetch(j + 1);  // in flight during this sample's MFMAs
         // this sample's ReLU mask, for the write-out below
         const size_t o0 = (size_t)j * D2_IN;
-        f4 mreg[D2_OUT4];
+        Mask4<H16> mreg[D2_OUT4];
 #pragma unroll
         for (int u = 0; u < D2_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
-            if (e4 < D2_IN / 4) mreg[u] = mask4<H16>(p, o0 + 4 * e4);
+            if (e4 < D2_IN / 4) mreg[u].load(p, o0 + 4 * e4);
         }
 
         f4 acc[D2_MT];
@@ -330,11 +339,10 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
         for (int u = 0; u < D2_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
             if (e4 < D2_IN / 4) {
-                const f4 h = mreg[u];
                 const f4 d = *(const f4*)(s_din + 4 * e4);
                 f4 o;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) o[k] = h[k] > 0.f ? d[k] : 0.f;
+                for (int k = 0; k < 4; ++k) o[k] = mreg[u].pos(k) ? d[k] : 0.f;
                 *(f4*)(p.din + o0 + 4 * e4) = o;
             }
         }
@@ -430,11 +438,11 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
         if (j + 1 < j_hi) fetch(j + 1);
         // this sample's ReLU mask, for the write-out below
         const size_t o0 = (size_t)j * D3_IN;
-        f4 mreg[D3_OUT4];
+        Mask4<false> mreg[D3_OUT4];
 #pragma unroll
         for (int u = 0; u < D3_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
-            if (e4 < D3_IN / 4) mreg[u] = mask4<false>(p, o0 + 4 * e4);
+            if (e4 < D3_IN / 4) mreg[u].load(p, o0 + 4 * e4);
         }
 
         f4 acc[D3_TPW];
@@ -473,11 +481,10 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
         for (int u = 0; u < D3_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
             if (e4 < D3_IN / 4) {
-                const f4 h = mreg[u];
                 const f4 d = *(const f4*)(s_din + 4 * e4);
                 f4 o;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) o[k] = h[k] > 0.f ? d[k] : 0.f;
+                for (int k = 0; k < 4; ++k) o[k] = mreg[u].pos(k) ? d[k] : 0.f;
                 *(f4*)(p.din + o0 + 4 * e4) = o;
             }
         }
@@ -563,11 +570,11 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
         __syncthreads();
         if (j + 1 < j_hi) fetch(j + 1);
         const size_t o0 = (size_t)j * D3_IN;
-        f4 mreg[D3_OUT4];
+        Mask4<H16> mreg[D3_OUT4];
 #pragma unroll
         for (int u = 0; u < D3_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
-            if (e4 < D3_IN / 4) mreg[u] = mask4<H16>(p, o0 + 4 * e4);
+            if (e4 < D3_IN / 4) mreg[u].load(p, o0 + 4 * e4);
         }
 
         f4 acc[D3_TPW];
@@ -606,11 +613,10 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
         for (int u = 0; u < D3_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
             if (e4 < D3_IN / 4) {
-                const f4 h = mreg[u];
                 const f4 d = *(const f4*)(s_din + 4 * e4);
                 f4 o;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) o[q] = h[q] > 0.f ? d[q] : 0.f;
+                for (int q = 0; q < 4; ++q) o[q] = mreg[u].pos(q) ? d[q] : 0.f;
                 *(f4*)(p.din + o0 + 4 * e4) = o;
             }
         }
