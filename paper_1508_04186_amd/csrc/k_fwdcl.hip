@@ -83,9 +83,15 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
     // an even pixel count (conv2's) is read as 32-bit words of two pixels of
     // one channel and restaged bit for bit, without conversions.
     constexpr bool W32 = IN16 && G::IP % 2 == 0;
+    // bfloat16 input with an odd pixel count (conv3's): 32-bit words of the
+    // flat [channel][pixel] sample, each value stored into its place of the
+    // channels-last stage with a 16-bit LDS write
+    constexpr bool WFLAT = IN16 && !W32;
     constexpr int PER2 = ((CIN / 2) * (G::IP / 2) + FC_WG - 1) / FC_WG;
-    float va[SPR][W32 ? 1 : G::PER], vb[SPR][W32 ? 1 : G::PER];
-    uint32_t wa[SPR][W32 ? PER2 : 1], wb[SPR][W32 ? PER2 : 1];
+    constexpr int PERF = (G::IN / 2 + FC_WG - 1) / FC_WG;
+    static_assert(G::IN % 2 == 0, "whole words of bfloat16 input");
+    float va[SPR][IN16 ? 1 : G::PER], vb[SPR][IN16 ? 1 : G::PER];
+    uint32_t wa[SPR][W32 ? PER2 : (WFLAT ? PERF : 1)], wb[SPR][W32 ? PER2 : 1];
     auto fetch = [&](int j) {
         if constexpr (W32) {
 #pragma unroll
@@ -100,6 +106,19 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
                         wa[s][u] = x[(2 * cp) * (G::IP / 2) + w];       // channel 2cp, pixels 2w, 2w+1
                         wb[s][u] = x[(2 * cp + 1) * (G::IP / 2) + w];   // channel 2cp+1
                     }
+                }
+            }
+            return;
+        }
+        if constexpr (WFLAT) {
+#pragma unroll
+            for (int s = 0; s < SPR; ++s) {
+                if (j + s >= j_hi) break;
+                const uint32_t* x = (const uint32_t*)((const __bf16*)p.in + (size_t)(j + s) * G::IN);
+#pragma unroll
+                for (int u = 0; u < PERF; ++u) {
+                    const int q = t + u * FC_WG;
+                    if (q < G::IN / 2) wa[s][u] = x[q];
                 }
             }
             return;
@@ -139,6 +158,25 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
                         unsigned char* d = s_in + (s * G::IP + 2 * w) * G::PSB + 4 * cp;
                         *(uint32_t*)d = (a & 0xffffu) | (b << 16);                       // pixel 2w
                         *(uint32_t*)(d + G::PSB) = (a >> 16) | (b & 0xffff0000u);        // pixel 2w+1
+                    }
+                }
+            }
+            return;
+        }
+        if constexpr (WFLAT) {
+#pragma unroll
+            for (int s = 0; s < SPR; ++s) {
+                if (j + s >= j_hi) break;
+#pragma unroll
+                for (int u = 0; u < PERF; ++u) {
+                    const int q = t + u * FC_WG;
+                    if (q < G::IN / 2) {
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {   // flat element 2q + h = channel c, pixel pix
+                            const int e = 2 * q + h, c = e / G::IP, pix = e - c * G::IP;
+                            *(uint16_t*)(s_in + (s * G::IP + pix) * G::PSB + 2 * c) =
+                                (uint16_t)(wa[s][u] >> (16 * h));
+                        }
                     }
                 }
             }
