@@ -302,11 +302,12 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // The bf16-input variant reads the network input with the byte-input
     // conv1 kernels, which need 16-byte aligned samples.
     if (ni.bf16 && (!conv_s12_fwd_aligned(s0) || !conv_s12_fwd_aligned(sn0))) return DQN_EINVAL;
-    // bf16-input variant of the large network from 128 samples: conv1's and
-    // conv2's outputs are stored as bfloat16 values.  Every reader rounds them
-    // to bfloat16 anyway (conv2's and conv3's forward and weight gradient) or
-    // takes only their sign (the ReLU masks of the input gradients), and all
-    // of those readers are the kernels that accept bfloat16 storage.
+    // bf16-input variant of the large network from 128 samples: the conv
+    // layers' outputs are stored as bfloat16 values.  Every reader rounds them
+    // to bfloat16 anyway (the next layer's forward and weight gradient, the fc1
+    // contractions) or takes only their sign (the ReLU masks of the input
+    // gradients), and all of those readers are the kernels that accept
+    // bfloat16 storage.
     const bool a16 = ni.bf16 && L == 3 && B >= kRegWgradMinRows && 2 * B >= kFwdClMinRows;
 
     // Forward of s under theta (samples 0..B-1) and of s' under theta^-
@@ -332,8 +333,7 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
         if (l > 0 && igemm_fwd(ni.conv[l], 2 * B, ni.bf16)) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], t.act[l - 1], B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
-                                      tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], ni.bf16, a16, a16 && l < 2,
-                                      st));
+                                      tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], ni.bf16, a16, a16, st));
             continue;
         }
         if (ni.bf16) return DQN_EUNSUPPORTED;  // the per-layer kernels are fp32 only
@@ -346,16 +346,19 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
                             l == 0 && src.replay ? &side : nullptr, st));
     }
     const float* xlast = t.act[L - 1];
+    // s' rows of the last conv output (bfloat16 elements when a16)
+    const float* xlast_b = a16 ? (const float*)((const __bf16*)xlast + (int64_t)B * ni.flat)
+                               : xlast + (int64_t)B * ni.flat;
     const int64_t slice = (int64_t)2 * B * ni.H;
     if (tt == th) {
         RUN(DQN_K_FC1_FWD,
             launch_gemm(GEMM_NT, 2 * B, ni.H, ni.flat, xlast, ni.flat, th + ni.w_off[L], ni.flat,
-                        t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, ni.bf16, st));
+                        t.fc1p, ni.H, t.ks, t.kchunk, slice, nullptr, ni.bf16, a16, st));
     } else {
         RUN(DQN_K_FC1_FWD,
-            launch_gemm_fwd2(B, ni.H, ni.flat, xlast, th + ni.w_off[L], t.fc1p, xlast + (int64_t)B * ni.flat,
+            launch_gemm_fwd2(B, ni.H, ni.flat, xlast, th + ni.w_off[L], t.fc1p, xlast_b,
                              tt + ni.w_off[L], t.fc1p + (int64_t)B * ni.H, ni.flat, ni.flat, ni.H, t.ks,
-                             t.kchunk, slice, ni.bf16, st));
+                             t.kchunk, slice, ni.bf16, a16, st));
     }
     HeadTdArgs h{};
     h.fc1p = t.fc1p;
@@ -390,10 +393,10 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     } else {
         RUN(DQN_K_FC1_WGRAD,
             launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat,
-                        grad_out + ni.w_off[L], ni.flat, 1, (B + 31) / 32 * 32, 0, nullptr, ni.bf16, st));
+                        grad_out + ni.w_off[L], ni.flat, 1, (B + 31) / 32 * 32, 0, nullptr, ni.bf16, a16, st));
         RUN(DQN_K_FC1_DGRAD,
             launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
-                        t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, ni.bf16, st));
+                        t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, ni.bf16, a16, st));
     }
     // The small network's conv layers in one launch: conv2's weight gradient,
     // and conv2's input gradient with conv1's weight gradient per (sample,
@@ -616,7 +619,7 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
             launch_conv_s12_fwd(in0, in0, batch, batch, th + ni.w_off[0], th + ni.b_off[0],
                                 th + ni.w_off[1], th + ni.b_off[1], th + ni.w_off[0], th + ni.b_off[0],
                                 th + ni.w_off[1], th + ni.b_off[1], f.act[0], f.act[1], nullptr, st));
-    // bfloat16 storage of conv1's and conv2's outputs, as in the TD step
+    // bfloat16 storage of the conv layers' outputs, as in the TD step
     const bool a16 = ni.bf16 && ni.n_conv == 3 && batch >= kFwdClMinRows;
     for (int l = 0; l < ni.n_conv && !fused_fwd; ++l) {
         if (l == 0 && conv1_u8(ni.conv[0], batch, ni.bf16) && conv_s12_fwd_aligned(in0)) {
@@ -628,8 +631,7 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
         if (l > 0 && igemm_fwd(ni.conv[l], batch, ni.bf16)) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], f.act[l - 1], batch, batch, th + ni.w_off[l], th + ni.b_off[l],
-                                      th + ni.w_off[l], th + ni.b_off[l], f.act[l], ni.bf16, a16, a16 && l < 2,
-                                      st));
+                                      th + ni.w_off[l], th + ni.b_off[l], f.act[l], ni.bf16, a16, a16, st));
             continue;
         }
         if (ni.bf16) return DQN_EUNSUPPORTED;  // the per-layer kernels are fp32 only
@@ -643,7 +645,7 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
     const int L = ni.n_conv;
     RUN(DQN_K_FC1_FWD,
         launch_gemm(GEMM_NT, batch, ni.H, ni.flat, f.act[L - 1], ni.flat, th + ni.w_off[L], ni.flat,
-                    f.fc1p, ni.H, f.ks, f.kchunk, (int64_t)batch * ni.H, nullptr, ni.bf16, st));
+                    f.fc1p, ni.H, f.ks, f.kchunk, (int64_t)batch * ni.H, nullptr, ni.bf16, a16, st));
     HeadFwdArgs h{};
     h.fc1p = f.fc1p;
     h.ks = f.ks;

@@ -317,20 +317,22 @@ void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk);
 void gemm_fwd_split_bf16(int rows, int N, int K, int* ks, int* kchunk);
 // The bf16-input contractions of launch_gemm (same arguments; operands
 // rounded to bfloat16 as they are staged).
+// x16 (bf16 only): the activation operand -- A of GEMM_NT, B of GEMM_TN, the
+// mask of GEMM_NN -- holds bfloat16 values.
 hipError_t launch_gemm_bf16(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
                             float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
-                            hipStream_t st);
+                            bool x16, hipStream_t st);
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
-                       const float* mask, bool bf16, hipStream_t st);
+                       const float* mask, bool bf16, bool x16, hipStream_t st);
 // Two fc1 forward contractions of one shape in one launch (GEMM_NT, split-K
 // as above): C0 = A0 B0^T and C1 = A1 B1^T, each in its own k-slices.
 hipError_t launch_gemm_bf16_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0,
                                  const float* A1, const float* B1, float* C1, int lda, int ldb, int ldc,
-                                 int kslices, int kchunk, int64_t c_slice, hipStream_t st);
+                                 int kslices, int kchunk, int64_t c_slice, bool x16, hipStream_t st);
 hipError_t launch_gemm_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0, const float* A1,
                             const float* B1, float* C1, int lda, int ldb, int ldc, int kslices, int kchunk,
-                            int64_t c_slice, bool bf16, hipStream_t st);
+                            int64_t c_slice, bool bf16, bool x16, hipStream_t st);
 
 // fc1 backward for batch B: dW [H][F] = dz1^T x (x = first B rows of the last
 // conv output) and dx [B][F] = (dz1 W) masked by [x > 0], as one launch where

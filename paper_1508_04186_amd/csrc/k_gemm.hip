@@ -358,10 +358,10 @@ hipError_t launch_gemm_prec(GemmKind kind, int M, int N, int K, const float* A, 
 
 hipError_t launch_gemm_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0, const float* A1,
                             const float* B1, float* C1, int lda, int ldb, int ldc, int kslices, int kchunk,
-                            int64_t c_slice, bool bf16, hipStream_t st) {
-    if (kchunk % 32 != 0 || kslices <= 0) return hipErrorInvalidValue;
+                            int64_t c_slice, bool bf16, bool x16, hipStream_t st) {
+    if (kchunk % 32 != 0 || kslices <= 0 || (x16 && !bf16)) return hipErrorInvalidValue;
     if (bf16) return launch_gemm_bf16_fwd2(M, N, K, A0, B0, C0, A1, B1, C1, lda, ldb, ldc, kslices, kchunk,
-                                           c_slice, st);
+                                           c_slice, x16, st);
     const GemmParams p0{M, N, K, A0, lda, B0, ldb, C0, ldc, kchunk, c_slice, nullptr};
     const GemmParams p1{M, N, K, A1, lda, B1, ldb, C1, ldc, kchunk, c_slice, nullptr};
     const TileCfg c = fwd_tile(M, kchunk);
@@ -379,9 +379,9 @@ hipError_t launch_gemm_fwd2(int M, int N, int K, const float* A0, const float* B
 
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
-                       const float* mask, bool bf16, hipStream_t st) {
-    if (kchunk % 32 != 0) return hipErrorInvalidValue;
-    return bf16 ? launch_gemm_bf16(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st)
+                       const float* mask, bool bf16, bool x16, hipStream_t st) {
+    if (kchunk % 32 != 0 || (x16 && !bf16)) return hipErrorInvalidValue;
+    return bf16 ? launch_gemm_bf16(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, x16, st)
                 : launch_gemm_prec<false>(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
 }
 

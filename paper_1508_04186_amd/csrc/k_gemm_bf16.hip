@@ -17,6 +17,7 @@
 // launch still covers the chip.
 #include <algorithm>
 #include <initializer_list>
+#include <type_traits>
 
 #include "common.h"
 
@@ -43,24 +44,37 @@ __device__ __forceinline__ uint2 pack4(f4 v) {
     return uint2{a | (b << 16), c | (d << 16)};
 }
 
+// Element i (0..3) of four bfloat16 values packed in a uint2.
+__device__ __forceinline__ uint32_t half16(uint2 x, int i) { return ((i < 2 ? x.x : x.y) >> (16 * (i & 1))) & 0xffffu; }
+
 // One operand's stage: ROWS rows (m or n) x BK k, staged by NT threads.
 // KCONT: the operand is contiguous along k in memory (element (r, k) at
 // src[r*ld + k]); otherwise along r (element (r, k) at src[k*ld + r]).
-template <int ROWS, int BK, int NT, bool KCONT>
+// SRC16: the operand holds bfloat16 values (moved as they are) instead of
+// floats (rounded as they are staged).
+template <int ROWS, int BK, int NT, bool KCONT, bool SRC16 = false>
 struct Stage {
-    static constexpr int KQ = BK / 4;                 // float4s along k per row
-    static constexpr int NV = ROWS * BK / 4 / NT;     // float4s per thread
+    static constexpr int KQ = BK / 4;                 // four-value groups along k per row
+    static constexpr int NV = ROWS * BK / 4 / NT;     // four-value groups per thread
     static constexpr int RS = BK + 8;                 // LDS row stride (bf16)
     static_assert(NV * NT * 4 == ROWS * BK && (KCONT || NV % 4 == 0), "stage split");
-    f4 v[NV];
+    using V = std::conditional_t<SRC16, uint2, f4>;
+    V v[NV];
+    __device__ __forceinline__ static V zero() {
+        if constexpr (SRC16) return uint2{0u, 0u};
+        else return f4{0.f, 0.f, 0.f, 0.f};
+    }
+    __device__ __forceinline__ static V at(const float* __restrict__ src, size_t off) {
+        if constexpr (SRC16) return *(const uint2*)((const __bf16*)src + off);
+        else return *(const f4*)(src + off);
+    }
     __device__ __forceinline__ void load(const float* __restrict__ src, int ld, int r0, int rlim, int k0, int klim) {
         const int t = threadIdx.x;
         if constexpr (KCONT) {
 #pragma unroll
             for (int u = 0; u < NV; ++u) {
                 const int q = t + NT * u, r = q / KQ, k = k0 + 4 * (q % KQ);
-                v[u] = (r0 + r < rlim && k < klim) ? *(const f4*)(src + (size_t)(r0 + r) * ld + k)
-                                                   : f4{0.f, 0.f, 0.f, 0.f};
+                v[u] = (r0 + r < rlim && k < klim) ? at(src, (size_t)(r0 + r) * ld + k) : zero();
             }
         } else {
             // 4x4 block b: rows 4 (b % (ROWS/4)) .. +3, k-rows 4 (b / (ROWS/4)) .. +3
@@ -70,8 +84,7 @@ struct Stage {
                 const int r = r0 + 4 * (b % (ROWS / 4)), kb = k0 + 4 * (b / (ROWS / 4));
 #pragma unroll
                 for (int u = 0; u < 4; ++u)
-                    v[4 * w + u] = (kb + u < klim && r < rlim) ? *(const f4*)(src + (size_t)(kb + u) * ld + r)
-                                                               : f4{0.f, 0.f, 0.f, 0.f};
+                    v[4 * w + u] = (kb + u < klim && r < rlim) ? at(src, (size_t)(kb + u) * ld + r) : zero();
             }
         }
     }
@@ -81,7 +94,8 @@ struct Stage {
 #pragma unroll
             for (int u = 0; u < NV; ++u) {
                 const int q = t + NT * u, r = q / KQ, k = 4 * (q % KQ);
-                *(uint2*)&s[r * RS + k] = pack4(v[u]);
+                if constexpr (SRC16) *(uint2*)&s[r * RS + k] = v[u];
+                else *(uint2*)&s[r * RS + k] = pack4(v[u]);
             }
         } else {
 #pragma unroll
@@ -89,9 +103,15 @@ struct Stage {
                 const int b = t + NT * w;
                 const int r = 4 * (b % (ROWS / 4)), k = 4 * (b / (ROWS / 4));
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    *(uint2*)&s[(r + i) * RS + k] =
-                        pack4(f4{v[4 * w][i], v[4 * w + 1][i], v[4 * w + 2][i], v[4 * w + 3][i]});
+                for (int i = 0; i < 4; ++i) {
+                    if constexpr (SRC16)
+                        *(uint2*)&s[(r + i) * RS + k] =
+                            uint2{half16(v[4 * w], i) | (half16(v[4 * w + 1], i) << 16),
+                                  half16(v[4 * w + 2], i) | (half16(v[4 * w + 3], i) << 16)};
+                    else
+                        *(uint2*)&s[(r + i) * RS + k] =
+                            pack4(f4{v[4 * w][i], v[4 * w + 1][i], v[4 * w + 2][i], v[4 * w + 3][i]});
+                }
             }
         }
     }
@@ -100,7 +120,9 @@ struct Stage {
 // TA: A(m,k) = A[k*lda + m] else A[m*lda + k].
 // TB: B(k,n) = B[n*ldb + k] else B[k*ldb + n].
 // MASK: C(m,n) = 0 where mask[m*ldc + n] <= 0.
-template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
+// A16, B16, M16: A, B or the mask hold bfloat16 values.
+template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK, bool A16 = false, bool B16 = false,
+          bool M16 = false>
 __device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z) {
     constexpr int NT = 64 * WGM * WGN;
     constexpr int WTM = BM / WGM, WTN = BN / WGN;     // wave tile
@@ -115,8 +137,8 @@ __device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z) {
     const int li = lane & 15, g = lane >> 4;
     const int wm = (wave / WGN) * WTM, wn = (wave % WGN) * WTN;
 
-    Stage<BM, BK, NT, !TA> sa;
-    Stage<BN, BK, NT, TB> sb;
+    Stage<BM, BK, NT, !TA, A16> sa;
+    Stage<BN, BK, NT, TB, B16> sb;
     f4 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -162,43 +184,56 @@ __device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z) {
                 const int m = m0 + wm + 16 * i + 4 * g + r;
                 if (m < p.M && n < p.N) {
                     float v = acc[i][j][r];
-                    if constexpr (MASK) v = p.mask[(size_t)m * p.ldc + n] > 0.f ? v : 0.f;
+                    if constexpr (MASK && M16) v = (float)((const __bf16*)p.mask)[(size_t)m * p.ldc + n] > 0.f ? v : 0.f;
+                    else if constexpr (MASK) v = p.mask[(size_t)m * p.ldc + n] > 0.f ? v : 0.f;
                     Cz[(size_t)m * p.ldc + n] = v;
                 }
             }
         }
 }
 
-template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
+template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK, bool A16, bool B16, bool M16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Params p) {
-    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK>(p, blockIdx.z);
+    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, A16, B16, M16>(p, blockIdx.z);
 }
 
 // Two forward contractions of one shape (the online network on s, the
 // target network on s'): k-slices z < ks0 run p0, the rest p1.
-template <int BM, int BN, int BK, int WGM, int WGN>
+template <int BM, int BN, int BK, int WGM, int WGN, bool A16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_fwd2_kernel(GemmBf16Params p0, GemmBf16Params p1,
                                                                        int ks0) {
     const int z = blockIdx.z;
     if (z < ks0)
-        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false>(p0, z);
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p0, z);
     else
-        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false>(p1, z - ks0);
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p1, z - ks0);
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN>
-hipError_t gemm_bf16_fwd2_launch(const GemmBf16Params& p0, const GemmBf16Params& p1, int kslices, hipStream_t st) {
+hipError_t gemm_bf16_fwd2_launch(const GemmBf16Params& p0, const GemmBf16Params& p1, int kslices, bool a16,
+                                 hipStream_t st) {
     const dim3 grid((unsigned)((p0.M + BM - 1) / BM), (unsigned)((p0.N + BN - 1) / BN), (unsigned)(2 * kslices));
-    hipLaunchKernelGGL((gemm_bf16_fwd2_kernel<BM, BN, BK, WGM, WGN>), grid, dim3(64 * WGM * WGN), 0, st, p0, p1,
-                       kslices);
+    if (a16)
+        hipLaunchKernelGGL((gemm_bf16_fwd2_kernel<BM, BN, BK, WGM, WGN, true>), grid, dim3(64 * WGM * WGN), 0, st, p0,
+                           p1, kslices);
+    else
+        hipLaunchKernelGGL((gemm_bf16_fwd2_kernel<BM, BN, BK, WGM, WGN, false>), grid, dim3(64 * WGM * WGN), 0, st, p0,
+                           p1, kslices);
     return hipGetLastError();
 }
 
+// x16: the activation operand (A of the forward, B of the weight gradient,
+// the mask of the input gradient) holds bfloat16 values.
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
-hipError_t gemm_bf16_launch(const GemmBf16Params& prm, int kslices, hipStream_t st) {
+hipError_t gemm_bf16_launch(const GemmBf16Params& prm, int kslices, bool x16, hipStream_t st) {
     const dim3 grid((unsigned)((prm.M + BM - 1) / BM), (unsigned)((prm.N + BN - 1) / BN), (unsigned)kslices);
-    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, TA, TB, MASK>), grid, dim3(64 * WGM * WGN), 0, st,
-                       prm);
+    constexpr bool FWD = !TA && TB && !MASK, WGR = TA && !TB && !MASK;
+    if (x16)
+        hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, TA, TB, MASK, FWD, WGR, MASK>), grid,
+                           dim3(64 * WGM * WGN), 0, st, prm);
+    else
+        hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, TA, TB, MASK, false, false, false>), grid,
+                           dim3(64 * WGM * WGN), 0, st, prm);
     return hipGetLastError();
 }
 
@@ -221,35 +256,35 @@ void gemm_fwd_split_bf16(int rows, int N, int K, int* ks, int* kchunk) {
 
 hipError_t launch_gemm_bf16_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0,
                                  const float* A1, const float* B1, float* C1, int lda, int ldb, int ldc,
-                                 int kslices, int kchunk, int64_t c_slice, hipStream_t st) {
+                                 int kslices, int kchunk, int64_t c_slice, bool x16, hipStream_t st) {
     if (M <= 0 || N <= 0 || K <= 0 || kslices <= 0 || kchunk % 32 != 0 || K % 4) return hipErrorInvalidValue;
     for (const float* x : {A0, B0, A1, B1})
         if ((uintptr_t)x % 16) return hipErrorInvalidValue;
     if (lda % 4 || ldb % 4) return hipErrorInvalidValue;
     const GemmBf16Params p0{M, N, K, A0, lda, B0, ldb, C0, ldc, kchunk, c_slice, nullptr};
     const GemmBf16Params p1{M, N, K, A1, lda, B1, ldb, C1, ldc, kchunk, c_slice, nullptr};
-    if (M >= kBf16BigRows) return gemm_bf16_fwd2_launch<128, 256, 64, 2, 4>(p0, p1, kslices, st);
-    return gemm_bf16_fwd2_launch<64, 64, 128, 2, 2>(p0, p1, kslices, st);
+    if (M >= kBf16BigRows) return gemm_bf16_fwd2_launch<128, 256, 64, 2, 4>(p0, p1, kslices, x16, st);
+    return gemm_bf16_fwd2_launch<64, 64, 128, 2, 2>(p0, p1, kslices, x16, st);
 }
 
 hipError_t launch_gemm_bf16(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
                             float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
-                            hipStream_t st) {
+                            bool x16, hipStream_t st) {
     if (M <= 0 || N <= 0 || K <= 0 || kslices <= 0 || kchunk % 32 != 0) return hipErrorInvalidValue;
     if ((uintptr_t)A % 16 || (uintptr_t)B % 16 || lda % 4 || ldb % 4) return hipErrorInvalidValue;
     const GemmBf16Params prm{M, N, K, A, lda, B, ldb, C, ldc, kchunk, c_slice, mask};
     switch (kind) {
         case GEMM_NT:
             if (K % 4) return hipErrorInvalidValue;
-            if (M >= kBf16BigRows) return gemm_bf16_launch<128, 256, 64, 2, 4, false, true, false>(prm, kslices, st);
-            return gemm_bf16_launch<64, 64, 128, 2, 2, false, true, false>(prm, kslices, st);
+            if (M >= kBf16BigRows) return gemm_bf16_launch<128, 256, 64, 2, 4, false, true, false>(prm, kslices, x16, st);
+            return gemm_bf16_launch<64, 64, 128, 2, 2, false, true, false>(prm, kslices, x16, st);
         case GEMM_TN:
             if (M % 4 || N % 4) return hipErrorInvalidValue;
-            return gemm_bf16_launch<64, 64, 128, 2, 2, true, false, false>(prm, kslices, st);
+            return gemm_bf16_launch<64, 64, 128, 2, 2, true, false, false>(prm, kslices, x16, st);
         case GEMM_NN:
             if (!mask || K % 4 || N % 4) return hipErrorInvalidValue;
-            if (M >= kBf16BigRows) return gemm_bf16_launch<128, 128, 64, 2, 4, false, false, true>(prm, kslices, st);
-            return gemm_bf16_launch<64, 64, 128, 2, 2, false, false, true>(prm, kslices, st);
+            if (M >= kBf16BigRows) return gemm_bf16_launch<128, 128, 64, 2, 4, false, false, true>(prm, kslices, x16, st);
+            return gemm_bf16_launch<64, 64, 128, 2, 2, false, false, true>(prm, kslices, x16, st);
         default: return hipErrorInvalidValue;
     }
 }
