@@ -54,7 +54,8 @@ typedef enum {
     DQN_K_CONV12_BWD = 20,  /* conv2 weight + input gradient and conv1 weight gradient, small network */
     DQN_K_SNAKE_STEP = 21,  /* one move of every game with its replay write (dqn_actor.h) */
     DQN_K_OBSERVE = 22,     /* preprocessing of raw screens (dqn_preprocess, dqn_observe) */
-    DQN_K_COUNT = 23
+    DQN_K_DGRAD_REPACK = 23, /* conv2/conv3 weights in the per-lane order of the fp32 input gradients */
+    DQN_K_COUNT = 24
 } dqn_kernel;
 
 int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs, int32_t stride);

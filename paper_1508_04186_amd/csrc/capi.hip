@@ -140,6 +140,7 @@ struct TdLayout {
     int chunks[3];
     int ks, kchunk;
     float* spart;   // sample-sum chunk slots of the finalize (above 128 samples)
+    float *wpk2, *wpk3;   // repacked conv2/conv3 weights of the fp32 input gradients (large network)
     size_t bytes;
 };
 
@@ -174,6 +175,10 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
         t.bpart[l] = cv.take<float>(ws, slots * c.cout);
     }
     t.spart = cv.take<float>(ws, (int64_t)finalize_sample_chunks(B) * ((int64_t)ni.A * ni.H + ni.H + ni.A + 1));
+    if (ni.n_conv == 3) {
+        t.wpk2 = cv.take<float>(ws, dgrad_repack_floats(CONV_L2));
+        t.wpk3 = cv.take<float>(ws, dgrad_repack_floats(CONV_L3));
+    }
     t.bytes = cv.off;
     return t;
 }
@@ -385,6 +390,12 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // fc1: weight gradient and the masked gradient of the last conv output;
     // then the conv layers, last to first.  At small batch each layer's two
     // independent backward kernels share one launch.
+    // Up to 512 samples (one or two per input-gradient workgroup) the fp32
+    // input-gradient kernels load their weights from a copy in per-lane order
+    // instead of gathering 64 / 144 scattered words per lane.
+    const bool repack = !ni.bf16 && L == 3 && phase_dgrad(CONV_L2, B, false) && B <= 512;
+    if (repack)
+        RUN(DQN_K_DGRAD_REPACK, launch_dgrad_repack(th + ni.w_off[1], th + ni.w_off[2], t.wpk2, t.wpk3, st));
     const bool paired = B <= kPairMaxBatch;
     if (paired) {
         RUN(DQN_K_FC1_BWD,
@@ -443,9 +454,9 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
                 ni.conv[l] == CONV_L2
                     ? launch_conv2_dgrad_phase(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
-                                               ni.bf16, a16, st)
+                                               ni.bf16, a16, repack ? t.wpk2 : nullptr, st)
                     : launch_conv3_dgrad(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
-                                         ni.bf16, a16, st));
+                                         ni.bf16, a16, repack ? t.wpk3 : nullptr, st));
         else if (l > 0 && igemm_dgrad(ni.conv[l], B, ni.bf16))
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
                 launch_conv_igemm_dgrad(ni.conv[l], t.dconv[l], th + ni.w_off[l], t.act[l - 1],

@@ -244,14 +244,21 @@ hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, c
 // Input gradient of CONV_L2 for n samples by stride phase, masked by
 // [h_in > 0] (as launch_conv_dgrad), with each phase's weights held in
 // registers and dz staged in LDS with a zero border.
+// wpk (fp32 only; NULL: read W directly): the weights repacked by
+// launch_dgrad_repack, which the workgroups load coalesced.
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
-                                    bool bf16, bool h16, hipStream_t st);
+                                    bool bf16, bool h16, const float* wpk, hipStream_t st);
 
 // Input gradient of CONV_L3 for n samples, masked by [h_in > 0], in the same
 // arrangement (weights in registers, zero-bordered dz in LDS, the sample's
 // gradient assembled in LDS).  h_in and din 16-byte aligned.
 hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
-                              bool h16, hipStream_t st);
+                              bool h16, const float* wpk, hipStream_t st);
+// conv2's and conv3's weights in the per-lane order of the fp32
+// input-gradient kernels: dgrad_repack_floats(CONV_L2) floats into p2,
+// dgrad_repack_floats(CONV_L3) into p3.
+int64_t dgrad_repack_floats(ConvId id);
+hipError_t launch_dgrad_repack(const float* w2, const float* w3, float* p2, float* p3, hipStream_t st);
 
 // Weight/bias gradient partial sums of CONV_L2 or CONV_L3 for n samples, one
 // workgroup per run of samples holding every output in registers:

@@ -50,6 +50,7 @@ struct Dgrad2Params {
     const float* h_in;  // [n][32][20][20] (bfloat16 values when h16)
     float* din;         // [n][32][20][20]
     int n, spg;         // samples, samples per workgroup
+    const float* wpk;   // fp32 kernels: the weights in per-lane order (dgrad_repack), or NULL
 };
 
 // Four consecutive values of the layer input h_in (the ReLU mask source) at
@@ -73,6 +74,7 @@ struct Mask4<true> {
     }
 };
 
+template <bool PK>   // weights from p.wpk (dgrad_repack) instead of p.w
 __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p) {
     __shared__ float s_dz[D2_STAGE];
     __shared__ __align__(16) float s_din[D2_IN];
@@ -92,7 +94,10 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p
     const int c = nt * 16 + li;
     constexpr int KS = D2_KT / 4;
     float wreg[KS];
-    {
+    if constexpr (PK) {   // coalesced: lane-consecutive per k-step
+#pragma unroll
+        for (int s = 0; s < KS; ++s) wreg[s] = p.wpk[((size_t)wave * KS + s) * 64 + lane];
+    } else {
         const float* wc = p.w + (size_t)c * D2_K * D2_K + py * D2_K + px;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
@@ -377,6 +382,7 @@ constexpr int D3_OUT4 = (D3_IN / 4 + D2_WG - 1) / D2_WG;
 static_assert(D3_CS >= (D3_OH + 4) * D3_IH && D3_CS % 64 == 48, "channel stride: border and banks");
 static_assert(D3_MT % 2 == 0 && D3_IN % 4 == 0, "tile split and float4 rows");
 
+template <bool PK>   // weights from p.wpk (dgrad_repack) instead of p.w
 __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
     __shared__ float s_dz[D3_STAGE];
     __shared__ __align__(16) float s_din[D3_IN];
@@ -395,7 +401,10 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
     const int c = nt * 16 + li;
     constexpr int KS = D3_KT / 4;
     float wreg[KS];
-    {
+    if constexpr (PK) {   // coalesced: lane-consecutive per k-step (waves nt and nt + 4 share a slice)
+#pragma unroll
+        for (int s = 0; s < KS; ++s) wreg[s] = p.wpk[((size_t)nt * KS + s) * 64 + lane];
+    } else {
         const float* wc = p.w + (size_t)c * D3_K * D3_K;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
@@ -623,36 +632,73 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
     }
 }
 
+// The weights of conv2's and conv3's fp32 input-gradient kernels in the order
+// their lanes load them into registers: element ((w * KS + s) * 64 + lane)
+// is wave w's k-step s for that lane.  A lane's own gather reads 64 (conv2)
+// or 144 (conv3) scattered words from W; from this copy every load of a
+// wave is one contiguous 256-byte row.
+__global__ __launch_bounds__(256) void dgrad_repack_kernel(const float* __restrict__ w2, const float* __restrict__ w3,
+                                                           float* __restrict__ p2, float* __restrict__ p3) {
+    constexpr int KS2 = D2_KT / 4, N2 = 8 * KS2 * 64;
+    constexpr int KS3 = D3_KT / 4, N3 = 4 * KS3 * 64;
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e < N2) {
+        const int lane = e & 63, s = (e >> 6) % KS2, wave = (e >> 6) / KS2;
+        const int li = lane & 15, g = lane >> 4, ph = wave >> 1, nt = wave & 1;
+        const int py = ph >> 1, px = ph & 1, c = nt * 16 + li;
+        const int tap = s / 16, ty = tap >> 1, tx = tap & 1, o = 4 * (s % 16) + g;
+        p2[e] = w2[(size_t)o * D2_CIN * D2_K * D2_K + (size_t)c * D2_K * D2_K + (py + 2 * ty) * D2_K + px + 2 * tx];
+    } else if (e < N2 + N3) {
+        const int f = e - N2;
+        const int lane = f & 63, s = (f >> 6) % KS3, nt = (f >> 6) / KS3;
+        const int li = lane & 15, g = lane >> 4, c = nt * 16 + li;
+        const int tap = s / 16, o = 4 * (s % 16) + g;
+        p3[f] = w3[(size_t)o * D3_CIN * D3_K * D3_K + (size_t)c * D3_K * D3_K + tap];
+    }
+}
+
 }  // namespace
 
+int64_t dgrad_repack_floats(ConvId id) { return id == CONV_L2 ? 8 * (D2_KT / 4) * 64 : 4 * (D3_KT / 4) * 64; }
+
+hipError_t launch_dgrad_repack(const float* w2, const float* w3, float* p2, float* p3, hipStream_t st) {
+    const int64_t n = dgrad_repack_floats(CONV_L2) + dgrad_repack_floats(CONV_L3);
+    hipLaunchKernelGGL(dgrad_repack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, w2, w3, p2, p3);
+    return hipGetLastError();
+}
+
 hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
-                              bool h16, hipStream_t st) {
+                              bool h16, const float* wpk, hipStream_t st) {
     if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15) || (h16 && !bf16)) return hipErrorInvalidValue;
     const int spg = std::max(1, (n + 255) / 256);
     const int blocks = (n + spg - 1) / spg;
-    const Dgrad2Params prm{dz, w, h_in, din, n, spg};
+    const Dgrad2Params prm{dz, w, h_in, din, n, spg, bf16 ? nullptr : wpk};
     if (bf16 && h16)
         hipLaunchKernelGGL(conv3_dgrad_cl_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else if (bf16)
         hipLaunchKernelGGL(conv3_dgrad_cl_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    else if (prm.wpk)
+        hipLaunchKernelGGL(conv3_dgrad_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else
-        hipLaunchKernelGGL(conv3_dgrad_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+        hipLaunchKernelGGL(conv3_dgrad_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     return hipGetLastError();
 }
 
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
-                                    bool bf16, bool h16, hipStream_t st) {
+                                    bool bf16, bool h16, const float* wpk, hipStream_t st) {
     if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15) || (h16 && !bf16)) return hipErrorInvalidValue;
     // about one workgroup per CU, one sample per round
     const int spg = std::max(1, (n + 255) / 256);
     const int blocks = (n + spg - 1) / spg;
-    const Dgrad2Params prm{dz, w, h_in, din, n, spg};
+    const Dgrad2Params prm{dz, w, h_in, din, n, spg, bf16 ? nullptr : wpk};
     if (bf16 && h16)
         hipLaunchKernelGGL(conv2_dgrad_cl_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else if (bf16)
         hipLaunchKernelGGL(conv2_dgrad_cl_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    else if (prm.wpk)
+        hipLaunchKernelGGL(conv2_dgrad_phase_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else
-        hipLaunchKernelGGL(conv2_dgrad_phase_kernel, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+        hipLaunchKernelGGL(conv2_dgrad_phase_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     return hipGetLastError();
 }
 
