@@ -162,8 +162,8 @@ def kernel_work(shape, B, forward_only=False, rule="sgd"):
         for l in range(1, len(dims)):
             w[f"conv{l+1}_bwd"] = (w[f"conv{l+1}_wgrad"][0] + w[f"conv{l+1}_dgrad"][0], 0)
         w["gather"] = (0, 4 * B * rec)          # read s and s', write both
-        if len(dims) == 3:                      # conv2/conv3 weights into the input-gradient lane order
-            w["dgrad_repack"] = (0, 2 * 4 * (8 * 64 * 64 + 4 * 144 * 64))
+        if len(dims) == 3:                      # conv2/conv3 weights into the fp32 kernels' lane order
+            w["weight_repack"] = (0, 2 * 4 * 2 * (4 * 128 * 64 + 4 * 144 * 64) + 2 * 4 * (8 * 64 * 64 + 4 * 144 * 64))
         # SGD reads theta and g and writes theta; RMSProp and AdaGrad also
         # read and write their state
         ub = 12 * P if rule == "sgd" else 20 * P

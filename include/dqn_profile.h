@@ -54,7 +54,7 @@ typedef enum {
     DQN_K_CONV12_BWD = 20,  /* conv2 weight + input gradient and conv1 weight gradient, small network */
     DQN_K_SNAKE_STEP = 21,  /* one move of every game with its replay write (dqn_actor.h) */
     DQN_K_OBSERVE = 22,     /* preprocessing of raw screens (dqn_preprocess, dqn_observe) */
-    DQN_K_DGRAD_REPACK = 23, /* conv2/conv3 weights in the per-lane order of the fp32 input gradients */
+    DQN_K_WEIGHT_REPACK = 23, /* conv2/conv3 weights in the per-lane order of the fp32 kernels */
     DQN_K_COUNT = 24
 } dqn_kernel;
 

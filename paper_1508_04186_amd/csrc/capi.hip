@@ -141,6 +141,7 @@ struct TdLayout {
     int ks, kchunk;
     float* spart;   // sample-sum chunk slots of the finalize (above 128 samples)
     float *wpk2, *wpk3;   // repacked conv2/conv3 weights of the fp32 input gradients (large network)
+    float *fpk[2][2];     // ... of the fp32 forward: [layer conv2, conv3][set theta, theta^-]
     size_t bytes;
 };
 
@@ -176,8 +177,12 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
     }
     t.spart = cv.take<float>(ws, (int64_t)finalize_sample_chunks(B) * ((int64_t)ni.A * ni.H + ni.H + ni.A + 1));
     if (ni.n_conv == 3) {
-        t.wpk2 = cv.take<float>(ws, dgrad_repack_floats(CONV_L2));
-        t.wpk3 = cv.take<float>(ws, dgrad_repack_floats(CONV_L3));
+        t.wpk2 = cv.take<float>(ws, weight_repack_floats(CONV_L2));
+        t.wpk3 = cv.take<float>(ws, weight_repack_floats(CONV_L3));
+        for (int w = 0; w < 2; ++w) {
+            t.fpk[0][w] = cv.take<float>(ws, kFwdPack2);
+            t.fpk[1][w] = cv.take<float>(ws, kFwdPack3);
+        }
     }
     t.bytes = cv.off;
     return t;
@@ -315,6 +320,28 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // bfloat16 storage.
     const bool a16 = ni.bf16 && L == 3 && B >= kRegWgradMinRows && 2 * B >= kFwdClMinRows;
 
+    // Up to 512 samples (a few per workgroup) the large network's fp32 conv2
+    // and conv3 kernels -- forward (both weight sets) and input gradient --
+    // load their weights from copies in per-lane order, written by one
+    // launch, instead of gathering 64 to 144 scattered words per lane.
+    const bool repack_fwd = !ni.bf16 && L == 3 && conv_fwd_cl_use(CONV_L2, 2 * B, false) && B <= 512;
+    const bool repack = !ni.bf16 && L == 3 && phase_dgrad(CONV_L2, B, false) && B <= 512;
+    if (repack_fwd || repack) {
+        WeightRepack r{th + ni.w_off[1], th + ni.w_off[2], tt + ni.w_off[1], tt + ni.w_off[2],
+                       nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+        if (repack_fwd) {
+            r.f2a = t.fpk[0][0];
+            r.f3a = t.fpk[1][0];
+            r.f2b = t.fpk[0][1];
+            r.f3b = t.fpk[1][1];
+        }
+        if (repack) {
+            r.d2 = t.wpk2;
+            r.d3 = t.wpk3;
+        }
+        RUN(DQN_K_WEIGHT_REPACK, launch_weight_repack(r, st));
+    }
+
     // Forward of s under theta (samples 0..B-1) and of s' under theta^-
     // (samples B..2B-1): one launch per layer, or both conv layers of the
     // small network in one launch at small batch.
@@ -338,7 +365,9 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
         if (l > 0 && igemm_fwd(ni.conv[l], 2 * B, ni.bf16)) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], t.act[l - 1], B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
-                                      tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], ni.bf16, a16, a16, st));
+                                      tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], ni.bf16, a16, a16,
+                                      repack_fwd ? t.fpk[l - 1][0] : nullptr, repack_fwd ? t.fpk[l - 1][1] : nullptr,
+                                      st));
             continue;
         }
         if (ni.bf16) return DQN_EUNSUPPORTED;  // the per-layer kernels are fp32 only
@@ -393,9 +422,6 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // Up to 512 samples (one or two per input-gradient workgroup) the fp32
     // input-gradient kernels load their weights from a copy in per-lane order
     // instead of gathering 64 / 144 scattered words per lane.
-    const bool repack = !ni.bf16 && L == 3 && phase_dgrad(CONV_L2, B, false) && B <= 512;
-    if (repack)
-        RUN(DQN_K_DGRAD_REPACK, launch_dgrad_repack(th + ni.w_off[1], th + ni.w_off[2], t.wpk2, t.wpk3, st));
     const bool paired = B <= kPairMaxBatch;
     if (paired) {
         RUN(DQN_K_FC1_BWD,
@@ -642,7 +668,8 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
         if (l > 0 && igemm_fwd(ni.conv[l], batch, ni.bf16)) {
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], f.act[l - 1], batch, batch, th + ni.w_off[l], th + ni.b_off[l],
-                                      th + ni.w_off[l], th + ni.b_off[l], f.act[l], ni.bf16, a16, a16, st));
+                                      th + ni.w_off[l], th + ni.b_off[l], f.act[l], ni.bf16, a16, a16, nullptr,
+                                      nullptr, st));
             continue;
         }
         if (ni.bf16) return DQN_EUNSUPPORTED;  // the per-layer kernels are fp32 only

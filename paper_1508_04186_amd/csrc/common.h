@@ -224,7 +224,8 @@ hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float*
 bool conv_igemm_fwd_supported(ConvId id);
 hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, const float* w_a,
                                  const float* b_a, const float* w_b, const float* b_b, float* out,
-                                 bool bf16, bool in16, bool out16, hipStream_t st);
+                                 bool bf16, bool in16, bool out16, const float* pk_a, const float* pk_b,
+                                 hipStream_t st);
 
 // The forward of CONV_L2 / CONV_L3 from kFwdClMinRows samples on, both
 // precisions: weights held in registers, each sample staged channels-last in
@@ -232,9 +233,11 @@ hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, con
 // it).
 constexpr int kFwdClMinRows = 256;
 bool conv_fwd_cl_use(ConvId id, int n, bool bf16);
+// pk_a, pk_b (fp32 only; both or neither): w_a, w_b repacked by
+// launch_weight_repack.
 hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const float* w_a, const float* b_a,
                               const float* w_b, const float* b_b, float* out, bool bf16, bool in16, bool out16,
-                              hipStream_t st);
+                              const float* pk_a, const float* pk_b, hipStream_t st);
 
 // Input gradient of CONV_L2 / CONV_L3 for n samples as an implicit GEMM per
 // stride phase, masked by [h_in > 0] (as launch_conv_dgrad).
@@ -245,7 +248,7 @@ hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, c
 // [h_in > 0] (as launch_conv_dgrad), with each phase's weights held in
 // registers and dz staged in LDS with a zero border.
 // wpk (fp32 only; NULL: read W directly): the weights repacked by
-// launch_dgrad_repack, which the workgroups load coalesced.
+// launch_weight_repack, which the workgroups load coalesced.
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
                                     bool bf16, bool h16, const float* wpk, hipStream_t st);
 
@@ -254,11 +257,18 @@ hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float
 // gradient assembled in LDS).  h_in and din 16-byte aligned.
 hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
                               bool h16, const float* wpk, hipStream_t st);
-// conv2's and conv3's weights in the per-lane order of the fp32
-// input-gradient kernels: dgrad_repack_floats(CONV_L2) floats into p2,
-// dgrad_repack_floats(CONV_L3) into p3.
-int64_t dgrad_repack_floats(ConvId id);
-hipError_t launch_dgrad_repack(const float* w2, const float* w3, float* p2, float* p3, hipStream_t st);
+// conv2's and conv3's weights in the per-lane order of the large network's
+// fp32 kernels, one launch: forward copies of two weight sets (a: theta, b:
+// theta^-; 4 * 128 * 64 and 4 * 144 * 64 floats) and input-gradient copies
+// of set a (weight_repack_floats(CONV_L2 / CONV_L3) floats).  NULL outputs
+// are skipped.
+struct WeightRepack {
+    const float *w2a, *w3a, *w2b, *w3b;
+    float *f2a, *f3a, *f2b, *f3b, *d2, *d3;
+};
+constexpr int64_t kFwdPack2 = 4 * 128 * 64, kFwdPack3 = 4 * 144 * 64;
+int64_t weight_repack_floats(ConvId id);
+hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st);
 
 // Weight/bias gradient partial sums of CONV_L2 or CONV_L3 for n samples, one
 // workgroup per run of samples holding every output in registers:

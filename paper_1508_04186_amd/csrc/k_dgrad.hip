@@ -50,7 +50,7 @@ struct Dgrad2Params {
     const float* h_in;  // [n][32][20][20] (bfloat16 values when h16)
     float* din;         // [n][32][20][20]
     int n, spg;         // samples, samples per workgroup
-    const float* wpk;   // fp32 kernels: the weights in per-lane order (dgrad_repack), or NULL
+    const float* wpk;   // fp32 kernels: the weights in per-lane order (weight_repack), or NULL
 };
 
 // Four consecutive values of the layer input h_in (the ReLU mask source) at
@@ -74,7 +74,7 @@ struct Mask4<true> {
     }
 };
 
-template <bool PK>   // weights from p.wpk (dgrad_repack) instead of p.w
+template <bool PK>   // weights from p.wpk (weight_repack) instead of p.w
 __global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p) {
     __shared__ float s_dz[D2_STAGE];
     __shared__ __align__(16) float s_din[D2_IN];
@@ -382,7 +382,7 @@ constexpr int D3_OUT4 = (D3_IN / 4 + D2_WG - 1) / D2_WG;
 static_assert(D3_CS >= (D3_OH + 4) * D3_IH && D3_CS % 64 == 48, "channel stride: border and banks");
 static_assert(D3_MT % 2 == 0 && D3_IN % 4 == 0, "tile split and float4 rows");
 
-template <bool PK>   // weights from p.wpk (dgrad_repack) instead of p.w
+template <bool PK>   // weights from p.wpk (weight_repack) instead of p.w
 __global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
     __shared__ float s_dz[D3_STAGE];
     __shared__ __align__(16) float s_din[D3_IN];
@@ -632,38 +632,61 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
     }
 }
 
-// The weights of conv2's and conv3's fp32 input-gradient kernels in the order
-// their lanes load them into registers: element ((w * KS + s) * 64 + lane)
-// is wave w's k-step s for that lane.  A lane's own gather reads 64 (conv2)
-// or 144 (conv3) scattered words from W; from this copy every load of a
-// wave is one contiguous 256-byte row.
-__global__ __launch_bounds__(256) void dgrad_repack_kernel(const float* __restrict__ w2, const float* __restrict__ w3,
-                                                           float* __restrict__ p2, float* __restrict__ p3) {
-    constexpr int KS2 = D2_KT / 4, N2 = 8 * KS2 * 64;
-    constexpr int KS3 = D3_KT / 4, N3 = 4 * KS3 * 64;
+// The weights of the large network's fp32 conv2/conv3 kernels in the order
+// their lanes load them into registers, so that every load of a wave is one
+// contiguous 256-byte row instead of a gather of scattered words:
+//  - input gradients (this file): element ((w KS + s) 64 + lane) is wave w's
+//    k-step s, w over the 8 (phase, N-tile) waves of conv2 (KS = 64) and the
+//    4 N-tiles of conv3 (KS = 144); values W[o][c][tap] as the kernels read;
+//  - forward (conv_fwd_cl32_kernel, k_fwdcl.hip): element ((nt KS + s) 64 +
+//    lane) holds W[16nt + li][16b + 4g + i][tap] for k-step s = (tap CB + b)
+//    4 + i, CB = cin / 16 (KS = 128 for conv2, 144 for conv3).
+// Job j of the launch (blockIdx.y) writes one copy; a NULL output skips it.
+__device__ __forceinline__ float fwd_pack_value(const float* __restrict__ w, int cin, int kk, int e) {
+    const int ks = kk * (cin / 16) * 4, cb = cin / 16;
+    const int lane = e & 63, s = (e >> 6) % ks, nt = (e >> 6) / ks;
+    const int li = lane & 15, g = lane >> 4;
+    const int tap = s / (cb * 4), b = (s / 4) % cb, i = s % 4;
+    return w[(size_t)(16 * nt + li) * cin * kk + (size_t)(16 * b + 4 * g + i) * kk + tap];
+}
+
+__global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
     const int e = blockIdx.x * 256 + threadIdx.x;
-    if (e < N2) {
-        const int lane = e & 63, s = (e >> 6) % KS2, wave = (e >> 6) / KS2;
-        const int li = lane & 15, g = lane >> 4, ph = wave >> 1, nt = wave & 1;
-        const int py = ph >> 1, px = ph & 1, c = nt * 16 + li;
-        const int tap = s / 16, ty = tap >> 1, tx = tap & 1, o = 4 * (s % 16) + g;
-        p2[e] = w2[(size_t)o * D2_CIN * D2_K * D2_K + (size_t)c * D2_K * D2_K + (py + 2 * ty) * D2_K + px + 2 * tx];
-    } else if (e < N2 + N3) {
-        const int f = e - N2;
-        const int lane = f & 63, s = (f >> 6) % KS3, nt = (f >> 6) / KS3;
-        const int li = lane & 15, g = lane >> 4, c = nt * 16 + li;
-        const int tap = s / 16, o = 4 * (s % 16) + g;
-        p3[f] = w3[(size_t)o * D3_CIN * D3_K * D3_K + (size_t)c * D3_K * D3_K + tap];
+    const int job = blockIdx.y;
+    if (job < 4) {   // forward copies: conv2 a, conv3 a, conv2 b, conv3 b
+        const bool l3 = job & 1;
+        const float* w = job == 0 ? r.w2a : job == 1 ? r.w3a : job == 2 ? r.w2b : r.w3b;
+        float* out = job == 0 ? r.f2a : job == 1 ? r.f3a : job == 2 ? r.f2b : r.f3b;
+        const int cin = l3 ? 64 : 32, kk = l3 ? 9 : 16;
+        if (out && e < 4 * kk * (cin / 16) * 4 * 64) out[e] = fwd_pack_value(w, cin, kk, e);
+    } else if (job == 4) {   // conv2 input gradient
+        constexpr int KS2 = D2_KT / 4;
+        if (r.d2 && e < 8 * KS2 * 64) {
+            const int lane = e & 63, s = (e >> 6) % KS2, wave = (e >> 6) / KS2;
+            const int li = lane & 15, g = lane >> 4, ph = wave >> 1, nt = wave & 1;
+            const int py = ph >> 1, px = ph & 1, c = nt * 16 + li;
+            const int tap = s / 16, ty = tap >> 1, tx = tap & 1, o = 4 * (s % 16) + g;
+            r.d2[e] = r.w2a[(size_t)o * D2_CIN * D2_K * D2_K + (size_t)c * D2_K * D2_K + (py + 2 * ty) * D2_K + px +
+                            2 * tx];
+        }
+    } else {   // conv3 input gradient
+        constexpr int KS3 = D3_KT / 4;
+        if (r.d3 && e < 4 * KS3 * 64) {
+            const int lane = e & 63, s = (e >> 6) % KS3, nt = (e >> 6) / KS3;
+            const int li = lane & 15, g = lane >> 4, c = nt * 16 + li;
+            const int tap = s / 16, o = 4 * (s % 16) + g;
+            r.d3[e] = r.w3a[(size_t)o * D3_CIN * D3_K * D3_K + (size_t)c * D3_K * D3_K + tap];
+        }
     }
 }
 
 }  // namespace
 
-int64_t dgrad_repack_floats(ConvId id) { return id == CONV_L2 ? 8 * (D2_KT / 4) * 64 : 4 * (D3_KT / 4) * 64; }
+int64_t weight_repack_floats(ConvId id) { return id == CONV_L2 ? 8 * (D2_KT / 4) * 64 : 4 * (D3_KT / 4) * 64; }
 
-hipError_t launch_dgrad_repack(const float* w2, const float* w3, float* p2, float* p3, hipStream_t st) {
-    const int64_t n = dgrad_repack_floats(CONV_L2) + dgrad_repack_floats(CONV_L3);
-    hipLaunchKernelGGL(dgrad_repack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, w2, w3, p2, p3);
+hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st) {
+    // every copy has at most 4 * 144 * 64 = 36,864 elements
+    hipLaunchKernelGGL(weight_repack_kernel, dim3(36864 / 256, 6), dim3(256), 0, st, r);
     return hipGetLastError();
 }
 

@@ -55,6 +55,7 @@ struct FwdClParams {
     float* out;                // [n][64][oh][oh] (bfloat16 values when out16)
     const float *w_a, *b_a, *w_b, *b_b;
     int n, n_a, g_a, spg;      // blocks [0, g_a) take samples [0, n_a), the rest [n_a, n); runs of spg
+    const float *wpk_a, *wpk_b;  // fp32 kernel: w_a, w_b in per-lane order (weight_repack), or NULL
 };
 
 template <int CIN, int IH, int K, int S, int OH, int SPR, bool IN16, bool OUT16>
@@ -311,7 +312,7 @@ hipError_t fwd_cl_launch(const float* in, int n_a, int n, const float* w_a, cons
     if (((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15) || ((uintptr_t)out & 15)) return hipErrorInvalidValue;
     const int spg = std::max(1, (n + FC_TARGET_BLOCKS - 1) / FC_TARGET_BLOCKS);
     const int g_a = (n_a + spg - 1) / spg, g_b = (n - n_a + spg - 1) / spg;
-    const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg};
+    const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg, nullptr, nullptr};
     auto go = [&](auto kern) -> hipError_t {
         if (!allow_lds((const void*)kern, G::LDS)) return hipErrorInvalidValue;
         hipLaunchKernelGGL(kern, dim3((unsigned)(g_a + g_b)), dim3(FC_WG), G::LDS, st, prm);
@@ -349,7 +350,7 @@ struct FwdCl32Geom {
     static_assert(MT % 2 == 0 && CIN % 16 == 0 && (PSF * 4) % 16 == 0 && OUTF % 4 == 0, "geometry");
 };
 
-template <int CIN, int IH, int K, int S, int OH>
+template <int CIN, int IH, int K, int S, int OH, bool PK>   // PK: weights from wpk_a / wpk_b
 __global__ __launch_bounds__(FC_WG) void conv_fwd_cl32_kernel(FwdClParams p) {
     using G = FwdCl32Geom<CIN, IH, K, S, OH>;
     extern __shared__ __align__(16) float smem32[];
@@ -392,7 +393,11 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl32_kernel(FwdClParams p) {
 
     // k-step s = (tap, block b, i): lane (li, g) holds W[16nt + li][16b + 4g + i][tap]
     float wv[G::KS];
-    {
+    if constexpr (PK) {   // wave nt's k-step s for this lane at ((nt KS + s) 64 + lane)
+        const float* wp = second ? p.wpk_b : p.wpk_a;
+#pragma unroll
+        for (int s = 0; s < G::KS; ++s) wv[s] = wp[((size_t)nt * G::KS + s) * 64 + lane];
+    } else {
         const float* wr = W + (size_t)(16 * nt + li) * CIN * G::KK;
 #pragma unroll
         for (int tap = 0; tap < G::KK; ++tap)
@@ -458,16 +463,18 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl32_kernel(FwdClParams p) {
 
 template <int CIN, int IH, int K, int S, int OH>
 hipError_t fwd_cl32_launch(const float* in, int n_a, int n, const float* w_a, const float* b_a, const float* w_b,
-                           const float* b_b, float* out, hipStream_t st) {
+                           const float* b_b, float* out, const float* pk_a, const float* pk_b, hipStream_t st) {
     using G = FwdCl32Geom<CIN, IH, K, S, OH>;
-    if (n <= 0 || n_a < 0 || n_a > n || ((uintptr_t)out & 15)) return hipErrorInvalidValue;
+    if (n <= 0 || n_a < 0 || n_a > n || ((uintptr_t)out & 15) || (!pk_a != !pk_b)) return hipErrorInvalidValue;
     const int spg = std::max(1, (n + FC_TARGET_BLOCKS - 1) / FC_TARGET_BLOCKS);
     const int g_a = (n_a + spg - 1) / spg, g_b = (n - n_a + spg - 1) / spg;
-    const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg};
-    auto kern = conv_fwd_cl32_kernel<CIN, IH, K, S, OH>;
-    if (!allow_lds((const void*)kern, G::LDS)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(g_a + g_b)), dim3(FC_WG), G::LDS, st, prm);
-    return hipGetLastError();
+    const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg, pk_a, pk_b};
+    auto go = [&](auto kern) -> hipError_t {
+        if (!allow_lds((const void*)kern, G::LDS)) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(kern, dim3((unsigned)(g_a + g_b)), dim3(FC_WG), G::LDS, st, prm);
+        return hipGetLastError();
+    };
+    return pk_a ? go(conv_fwd_cl32_kernel<CIN, IH, K, S, OH, true>) : go(conv_fwd_cl32_kernel<CIN, IH, K, S, OH, false>);
 }
 
 }  // namespace
@@ -478,15 +485,15 @@ bool conv_fwd_cl_use(ConvId id, int n, bool bf16) {
 
 hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const float* w_a, const float* b_a,
                               const float* w_b, const float* b_b, float* out, bool bf16, bool in16, bool out16,
-                              hipStream_t st) {
+                              const float* pk_a, const float* pk_b, hipStream_t st) {
     if (!bf16 && (in16 || out16)) return hipErrorInvalidValue;   // bf16 activations: the bf16 variant only
     switch (id) {
         case CONV_L2:
             return bf16 ? fwd_cl_launch<32, 20, 4, 2, 9, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, st)
-                        : fwd_cl32_launch<32, 20, 4, 2, 9>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
+                        : fwd_cl32_launch<32, 20, 4, 2, 9>(in, n_a, n, w_a, b_a, w_b, b_b, out, pk_a, pk_b, st);
         case CONV_L3:
             return bf16 ? fwd_cl_launch<64, 9, 3, 1, 7, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, st)
-                        : fwd_cl32_launch<64, 9, 3, 1, 7>(in, n_a, n, w_a, b_a, w_b, b_b, out, st);
+                        : fwd_cl32_launch<64, 9, 3, 1, 7>(in, n_a, n, w_a, b_a, w_b, b_b, out, pk_a, pk_b, st);
         default: return hipErrorInvalidValue;
     }
 }

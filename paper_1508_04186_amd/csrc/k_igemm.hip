@@ -461,10 +461,11 @@ bool conv_igemm_fwd_supported(ConvId id) { return id == CONV_L2 || id == CONV_L3
 
 hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, const float* w_a,
                                  const float* b_a, const float* w_b, const float* b_b, float* out,
-                                 bool bf16, bool in16, bool out16, hipStream_t st) {
+                                 bool bf16, bool in16, bool out16, const float* pk_a, const float* pk_b,
+                                 hipStream_t st) {
     if (conv_fwd_cl_use(id, n, bf16))
-        return launch_conv_fwd_cl(id, in, n_a, n, w_a, b_a, w_b, b_b, out, bf16, in16, out16, st);
-    if (in16 || out16) return hipErrorInvalidValue;   // bf16 activations only through the kernel above
+        return launch_conv_fwd_cl(id, in, n_a, n, w_a, b_a, w_b, b_b, out, bf16, in16, out16, pk_a, pk_b, st);
+    if (in16 || out16 || pk_a || pk_b) return hipErrorInvalidValue;   // only through the kernel above
     switch (id) {
         case CONV_L2:
             return bf16 ? igemm_launch<32, 20, 20, 64, 4, 2, 9, 9, true>(in, n_a, n, w_a, b_a, w_b, b_b, out, st)

@@ -473,7 +473,7 @@ def dqn_train_replicas(net, theta_ring, opt_state, rule, lr, decay, eps, gamma, 
 KERNEL_NAMES = ["gather", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head", "fc1_wgrad",
                 "fc1_dgrad", "conv1_wgrad", "conv2_wgrad", "conv3_wgrad", "conv2_dgrad",
                 "conv3_dgrad", "finalize", "apply", "fc1_bwd", "conv2_bwd", "conv3_bwd",
-                "finalize_apply", "conv12_fwd", "conv12_bwd", "snake_step", "observe", "dgrad_repack"]
+                "finalize_apply", "conv12_fwd", "conv12_bwd", "snake_step", "observe", "weight_repack"]
 _ATTACHED = {}
 
 
