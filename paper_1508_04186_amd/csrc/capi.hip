@@ -325,17 +325,20 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // load their weights from copies in per-lane order, written by one
     // launch, instead of gathering 64 to 144 scattered words per lane.
     const bool repack_fwd = !ni.bf16 && L == 3 && conv_fwd_cl_use(CONV_L2, 2 * B, false) && B <= 512;
-    const bool repack = !ni.bf16 && L == 3 && phase_dgrad(CONV_L2, B, false) && B <= 512;
+    const bool repack = L == 3 && phase_dgrad(CONV_L2, B, ni.bf16) && B <= 512;
     if (repack_fwd || repack) {
         WeightRepack r{th + ni.w_off[1], th + ni.w_off[2], tt + ni.w_off[1], tt + ni.w_off[2],
-                       nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+                       nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
         if (repack_fwd) {
             r.f2a = t.fpk[0][0];
             r.f3a = t.fpk[1][0];
             r.f2b = t.fpk[0][1];
             r.f3b = t.fpk[1][1];
         }
-        if (repack) {
+        if (repack && ni.bf16) {
+            r.h2 = t.wpk2;
+            r.h3 = t.wpk3;
+        } else if (repack) {
             r.d2 = t.wpk2;
             r.d3 = t.wpk3;
         }

@@ -247,8 +247,8 @@ hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, c
 // Input gradient of CONV_L2 for n samples by stride phase, masked by
 // [h_in > 0] (as launch_conv_dgrad), with each phase's weights held in
 // registers and dz staged in LDS with a zero border.
-// wpk (fp32 only; NULL: read W directly): the weights repacked by
-// launch_weight_repack, which the workgroups load coalesced.
+// wpk (NULL: read W directly): the weights repacked by launch_weight_repack
+// (d2/d3 for fp32, h2/h3 for bf16), which the workgroups load coalesced.
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
                                     bool bf16, bool h16, const float* wpk, hipStream_t st);
 
@@ -265,6 +265,7 @@ hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in
 struct WeightRepack {
     const float *w2a, *w3a, *w2b, *w3b;
     float *f2a, *f3a, *f2b, *f3b, *d2, *d3;
+    void *h2, *h3;   // bf16 input-gradient operands of set a (half the floats of d2, d3)
 };
 constexpr int64_t kFwdPack2 = 4 * 128 * 64, kFwdPack3 = 4 * 144 * 64;
 int64_t weight_repack_floats(ConvId id);

@@ -224,7 +224,7 @@ constexpr int D2C_PAIRS = D2_DZ / 2;           // (channel pair, pixel) items
 constexpr int D2C_PER = (D2C_PAIRS + D2_WG - 1) / D2_WG;
 static_assert(D2C_PSB % 16 == 0 && D2C_PSB >= 2 * D2_COUT, "slot size");
 
-template <bool H16>
+template <bool H16, bool PK>   // PK: bf16 weight operands from p.wpk (weight_repack)
 __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
     __shared__ __align__(16) unsigned char s_cl[D2C_SLOTS * D2C_PSB];
     __shared__ __align__(16) float s_din[D2_IN];
@@ -243,7 +243,10 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
     constexpr int KS = D2_KT / 32;
     const int c = nt * 16 + li;
     bf16x8 wreg[KS];
-    {
+    if constexpr (PK) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) wreg[s] = ((const bf16x8*)p.wpk)[((size_t)wave * KS + s) * 64 + lane];
+    } else {
         const float* wc = p.w + (size_t)c * D2_K * D2_K + py * D2_K + px;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
@@ -511,7 +514,7 @@ constexpr int D3C_PSB = 144;
 constexpr int D3C_PAIRS = D3_DZ / 2;
 constexpr int D3C_PER = (D3C_PAIRS + D2_WG - 1) / D2_WG;
 
-template <bool H16>
+template <bool H16, bool PK>   // PK: bf16 weight operands from p.wpk (weight_repack)
 __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
     __shared__ __align__(16) unsigned char s_cl[D3C_SLOTS * D3C_PSB];
     __shared__ __align__(16) float s_din[D3_IN];
@@ -529,7 +532,10 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
     constexpr int KS = D3_KT / 32;
     const int c = nt * 16 + li;
     bf16x8 wreg[KS];
-    {
+    if constexpr (PK) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) wreg[s] = ((const bf16x8*)p.wpk)[((size_t)nt * KS + s) * 64 + lane];
+    } else {
         const float* wc = p.w + (size_t)c * D3_K * D3_K;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
@@ -669,6 +675,36 @@ __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
             r.d2[e] = r.w2a[(size_t)o * D2_CIN * D2_K * D2_K + (size_t)c * D2_K * D2_K + (py + 2 * ty) * D2_K + px +
                             2 * tx];
         }
+    } else if (job == 6) {   // conv2 input gradient, bf16 operands: one 8-value vector per thread
+        constexpr int KS2 = D2_KT / 32;
+        if (r.h2 && e < 8 * KS2 * 64) {
+            const int lane = e & 63, s = (e >> 6) % KS2, wave = (e >> 6) / KS2;
+            const int li = lane & 15, g = lane >> 4, ph = wave >> 1, nt = wave & 1;
+            const int py = ph >> 1, px = ph & 1, c = nt * 16 + li;
+            const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
+            bf16x8 v;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int o = 32 * (s % 2) + 8 * g + q;
+                v[q] = (__bf16)r.w2a[(size_t)o * D2_CIN * D2_K * D2_K + (size_t)c * D2_K * D2_K +
+                                     (py + 2 * ty) * D2_K + px + 2 * tx];
+            }
+            ((bf16x8*)r.h2)[e] = v;
+        }
+    } else if (job == 7) {   // conv3 input gradient, bf16 operands
+        constexpr int KS3 = D3_KT / 32;
+        if (r.h3 && e < 4 * KS3 * 64) {
+            const int lane = e & 63, s = (e >> 6) % KS3, nt = (e >> 6) / KS3;
+            const int li = lane & 15, g = lane >> 4, c = nt * 16 + li;
+            const int tap = s / 2;
+            bf16x8 v;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int o = 32 * (s % 2) + 8 * g + q;
+                v[q] = (__bf16)r.w3a[(size_t)o * D3_CIN * D3_K * D3_K + (size_t)c * D3_K * D3_K + tap];
+            }
+            ((bf16x8*)r.h3)[e] = v;
+        }
     } else {   // conv3 input gradient
         constexpr int KS3 = D3_KT / 4;
         if (r.d3 && e < 4 * KS3 * 64) {
@@ -686,7 +722,7 @@ int64_t weight_repack_floats(ConvId id) { return id == CONV_L2 ? 8 * (D2_KT / 4)
 
 hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st) {
     // every copy has at most 4 * 144 * 64 = 36,864 elements
-    hipLaunchKernelGGL(weight_repack_kernel, dim3(36864 / 256, 6), dim3(256), 0, st, r);
+    hipLaunchKernelGGL(weight_repack_kernel, dim3(36864 / 256, 8), dim3(256), 0, st, r);
     return hipGetLastError();
 }
 
@@ -695,11 +731,12 @@ hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in
     if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15) || (h16 && !bf16)) return hipErrorInvalidValue;
     const int spg = std::max(1, (n + 255) / 256);
     const int blocks = (n + spg - 1) / spg;
-    const Dgrad2Params prm{dz, w, h_in, din, n, spg, bf16 ? nullptr : wpk};
-    if (bf16 && h16)
-        hipLaunchKernelGGL(conv3_dgrad_cl_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
-    else if (bf16)
-        hipLaunchKernelGGL(conv3_dgrad_cl_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    const Dgrad2Params prm{dz, w, h_in, din, n, spg, wpk};
+    const dim3 grid((unsigned)blocks), blk(D2_WG);
+    if (bf16 && h16 && wpk) hipLaunchKernelGGL((conv3_dgrad_cl_kernel<true, true>), grid, blk, 0, st, prm);
+    else if (bf16 && h16) hipLaunchKernelGGL((conv3_dgrad_cl_kernel<true, false>), grid, blk, 0, st, prm);
+    else if (bf16 && wpk) hipLaunchKernelGGL((conv3_dgrad_cl_kernel<false, true>), grid, blk, 0, st, prm);
+    else if (bf16) hipLaunchKernelGGL((conv3_dgrad_cl_kernel<false, false>), grid, blk, 0, st, prm);
     else if (prm.wpk)
         hipLaunchKernelGGL(conv3_dgrad_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else
@@ -713,11 +750,12 @@ hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float
     // about one workgroup per CU, one sample per round
     const int spg = std::max(1, (n + 255) / 256);
     const int blocks = (n + spg - 1) / spg;
-    const Dgrad2Params prm{dz, w, h_in, din, n, spg, bf16 ? nullptr : wpk};
-    if (bf16 && h16)
-        hipLaunchKernelGGL(conv2_dgrad_cl_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
-    else if (bf16)
-        hipLaunchKernelGGL(conv2_dgrad_cl_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    const Dgrad2Params prm{dz, w, h_in, din, n, spg, wpk};
+    const dim3 grid((unsigned)blocks), blk(D2_WG);
+    if (bf16 && h16 && wpk) hipLaunchKernelGGL((conv2_dgrad_cl_kernel<true, true>), grid, blk, 0, st, prm);
+    else if (bf16 && h16) hipLaunchKernelGGL((conv2_dgrad_cl_kernel<true, false>), grid, blk, 0, st, prm);
+    else if (bf16 && wpk) hipLaunchKernelGGL((conv2_dgrad_cl_kernel<false, true>), grid, blk, 0, st, prm);
+    else if (bf16) hipLaunchKernelGGL((conv2_dgrad_cl_kernel<false, false>), grid, blk, 0, st, prm);
     else if (prm.wpk)
         hipLaunchKernelGGL(conv2_dgrad_phase_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
     else
