@@ -330,7 +330,7 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (workers and "
+        print("bench.py measures one GPU only: this implementation has no multi-GPU path (workers and "
               "their parameter server run on one device); run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
