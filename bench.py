@@ -2,10 +2,11 @@
 """Throughput of the DQN TD-gradient + parameter-server update hot path on one
 MI355X (arXiv 1508.04186, Alg. 1 and Alg. 2), on seeded synthetic inputs.
 
-Configurations (--config; the default line is config 1):
+Configurations (--config; the default line is config 4b, the largest
+single-GPU workload):
   0   small Q-network (conv 16@8x8/4, conv 32@4x4/2, fc 256, fc 6), one
       batch of 32 uniform random states: TD gradient + SGD step, repeated.
-  1   small Q-network, 100,000-transition replay in device memory, 2,000
+  1   small Q-network, 100,000-transition replay in device memory,
       sequential steps of gather (batch 32) -> TD gradient -> SGD.
   2   small Q-network, 16 worker replicas on 16 streams + a server stream
       applying AdaGrad (lr 0.01, eps 1e-8) in order, gradients at most 4
@@ -20,7 +21,6 @@ Configurations (--config; the default line is config 1):
       (epsilon-greedy, annealed epsilon), store into a replay pooled over
       the games, and one TD gradient + SGD step follows on a minibatch of 32
       drawn from it (a step = one such iteration).
-
   observe  preprocessing phi on the device: 1,024 games each hand over a
       raw 176 x 176 RGB screen per step; phi (gray, crop, 2 x 2 mean) goes
       into each game's 4-frame state and the state into a replay keeping
@@ -32,27 +32,32 @@ Configurations (--config; the default line is config 1):
 
 A step is one pass of the whole hot path over one batch (config 2: one
 update; config 4a: one forward pass over 8,192 states).  Inputs are resident
-in device memory before the timed region; the timed region is bracketed by
-device synchronizations and HIP events on the work's stream(s).
+in device memory before the timed region.  After warm-up, --repeats timed
+runs of --steps consecutive steps each are bracketed by device
+synchronizations and events, with nothing attached to the library's
+measurement hook; `value` is their median and `timed_runs_ms` lists them.
 
 The JSON line adds:
+  step_tflops   the step's algorithmic FLOP (Alg. 1: forward of s and s',
+                every weight and input gradient) times steps/s;
   roofline      the dominant kernel (largest time per step, from an
                 event-bracketed breakdown pass before timing): its
                 algorithmic FLOP (or bytes) per launch divided by its average
-                launch time, measured with HIP event pairs around the launches
-                of that kernel inside the timed region (every launch for the
-                large-batch configs, every tenth for configs 0 to 2), less
-                what a pair adds around a one-element fill kernel compared
-                with that kernel's per-launch time in a dependent chain (so
-                the figure includes the kernel's dispatch and drain, as a
-                rocprofv3 kernel duration does);
+                launch time, measured in a separate pass over the steps that
+                follow the timed runs, with a HIP event pair on the kernel's
+                stream around every launch, less what a pair adds around a
+                one-element fill kernel compared with that kernel's
+                per-launch time in a chain (so the figure includes the
+                kernel's dispatch and drain, as a rocprofv3 kernel duration
+                does);
                 `traffic` is the HBM bytes per launch from the committed
                 rocprofv3 PMC summary (profiles/) while the kernel's source
                 is unchanged;
   cpu_baseline  the CPU oracle (fp64, direct loops) timed on this host on a
-                bounded sample of the same workload;
+                bounded sample of the same workload, on all its threads and
+                (`single_thread`) on one;
   breakdown     per-kernel average times (us) and the paper's T (worker
-                gradient time) and tau (server update time).
+                gradient time) and tau (server update time) on the GPU clock.
 """
 from __future__ import annotations
 
@@ -73,17 +78,12 @@ METRIC = "DQN TD-gradient+update steps/sec (transitions/sec); % MFMA peak and HB
 PEAK_FP32_MFMA = 157.3e12   # MI355X dense fp32 matrix FLOP/s
 PEAK_HBM = 8.0e12           # MI355X HBM3E bytes/s
 PEAK_BF16_MFMA = 2.5e15     # MI355X dense bf16 matrix FLOP/s
-# In the timed region, one launch of the dominant kernel in `stride` is
-# bracketed by events: a pair idles the GPU for a few microseconds around
-# the launch it brackets (a few per cent of a large-network step at batch
-# 256 when every launch was bracketed), so about 40 launches of a run are.
-SAMPLE_STRIDE = 50
-
-
-def sample_stride(steps):
-    """Stride of the bracketed launches: SAMPLE_STRIDE, or smaller for short
-    runs so that at least 40 launches are timed."""
-    return max(1, min(SAMPLE_STRIDE, steps // 40))
+# Timed runs per configuration; `value` is their median.
+REPEATS = 5
+# Steps of the separate pass, after the timed runs, that times the dominant
+# kernel with an event pair around each of its launches (the first launches
+# of a short run read a few per cent slow).
+KERNEL_PASS_STEPS = 200
 F32 = np.float32
 
 
@@ -173,6 +173,29 @@ def kernel_work(shape, B, forward_only=False, rule="sgd"):
     return w
 
 
+def step_flop(shape, B, forward_only=False):
+    """Algorithmic FLOP of one step: 2 x multiply-adds of the forward pass of
+    s through every layer (and of s' under theta^-, whose activations are
+    not kept), and of every layer's weight gradient and every input gradient
+    below the output layer except the first conv layer's (the input is
+    data), plus the output layer's backward, which is sparse in the taken
+    action (one row of B x hidden per gradient).  Forward only: the forward
+    pass of B states."""
+    dims = shape.conv_dims()
+    H, A, F = shape.fc_hidden, shape.n_actions, shape.flat()
+    nf = B if forward_only else 2 * B
+    f = 0
+    for l, (cin, ih, iw, cout, k, s, oh, ow) in enumerate(dims):
+        macs = oh * ow * cout * cin * k * k
+        f += 2 * nf * macs
+        if not forward_only:
+            f += 2 * B * macs * (2 if l > 0 else 1)
+    f += 2 * nf * (H * F + A * H)
+    if not forward_only:
+        f += 4 * B * H * F + 4 * B * H
+    return f
+
+
 # Kernels whose roofline is reported (dense contractions and the
 # memory-bound gather); the head and finalize are latency-bound reductions.
 ROOFLINE_KERNELS = ("conv1_fwd", "conv2_fwd", "conv3_fwd", "conv12_fwd", "conv12_bwd", "fc1_fwd", "fc1_wgrad", "fc1_dgrad",
@@ -181,20 +204,40 @@ ROOFLINE_KERNELS = ("conv1_fwd", "conv2_fwd", "conv3_fwd", "conv12_fwd", "conv12
 
 
 class Profiler:
-    """Event-bracketed timing of the library's kernels via dqn_profile.h."""
+    """Event-bracketed timing of the library's kernels via dqn_profile.h.
+
+    Nothing is attached while a run that sets `value` is timed.  Kernel times
+    come from separate passes in which an event pair brackets every launch of
+    the kernel; a pair adds a fixed time to what it brackets, measured here
+    and subtracted (`overhead`)."""
 
     def __init__(self, hip):
+        import torch
         import paper_1508_04186_amd as dq
         self.dq, self.hip = dq, hip
         self._overhead = None
+        self._busy_out = torch.empty(2048, device="cuda")
+        rec = hip.L.hipEventRecord
+        rec.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        rec.restype = ctypes.c_int
+        self.rec = rec
+
+    def busy(self, ms=15.0):
+        """Enqueue a matrix-core loop of about `ms` milliseconds on the current
+        stream, so that the host enqueues what follows before the GPU reaches
+        it (the spans measured after it hold no host time)."""
+        iters = max(1, int(ms * 1e-3 * 1.2e14 / (2048 * 4 * 4 * 2048)))
+        self.dq.profile_mfma_peak(self.dq.DQN_PEAK_FP32, 2048, iters, self._busy_out)
 
     def overhead(self):
-        """Event-bracket overhead in microseconds (measured once)."""
+        """Event-pair overhead in microseconds (measured once)."""
         if self._overhead is None:
             self._overhead = self.empty_pair_us()
         return self._overhead
 
     def breakdown(self, run, n, kernels):
+        """{kernel: (us per launch, launches)} over `run()`, every launch of
+        every listed kernel bracketed (an untimed pass)."""
         dq = self.dq
         evs = {}
         for name in kernels:
@@ -214,44 +257,123 @@ class Profiler:
             self.hip.destroy(ev)
         return out
 
-    def attach(self, name, launches, stride=1):
-        kid = self.dq.KERNEL_NAMES.index(name)
+    def kernel_pass(self, name, run, launches):
+        """Average launch time (us) of kernel `name` over a pass `run()` (the
+        same steps as a timed run) with an event pair around every launch:
+        (time less the pair overhead, raw pair time, launches bracketed)."""
+        import torch
+        dq = self.dq
+        kid = dq.KERNEL_NAMES.index(name)
         ev = self.hip.create(2 * launches)
-        self.dq.profile_attach(kid, ev, stride)
-        return kid, ev
-
-    def collect(self, kid, ev):
-        used = self.dq.profile_used(kid)
-        self.dq.profile_attach(kid, None)
-        us = 1e3 * sum(self.hip.ms(ev[2 * j], ev[2 * j + 1]) for j in range(used)) / max(used, 1)
+        dq.profile_attach(kid, ev, 1)
+        torch.cuda.synchronize()
+        run()
+        torch.cuda.synchronize()
+        used = dq.profile_used(kid)
+        dq.profile_attach(kid, None)
+        raw = 1e3 * sum(self.hip.ms(ev[2 * j], ev[2 * j + 1]) for j in range(used)) / max(used, 1)
         self.hip.destroy(ev)
-        return us, used
+        return raw - self.overhead(), raw, used
+
+    def spans_us(self, fn, n):
+        """Median GPU time (us) of one call fn(i), over n calls each bracketed
+        by an event pair on the current stream and queued behind `busy`, less
+        the pair overhead."""
+        import torch
+        stream = torch.cuda.current_stream().cuda_stream
+        ev = self.hip.create(2 * n)
+        torch.cuda.synchronize()
+        self.busy()
+        for i in range(n):
+            self.rec(ev[2 * i], stream)
+            fn(i)
+            self.rec(ev[2 * i + 1], stream)
+        torch.cuda.synchronize()
+        us = [1e3 * self.hip.ms(ev[2 * i], ev[2 * i + 1]) for i in range(n)]
+        self.hip.destroy(ev)
+        return float(np.median(us)) - self.overhead()
 
     def empty_pair_us(self, n=200):
         """What an event pair adds to the time of the launch it brackets: the
         mean bracketed time of a one-element fill kernel, less that kernel's
-        per-launch time in a chain of n dependent launches (which, like a
-        rocprofv3 kernel duration, includes its dispatch and drain).  Both
-        are measured here on the current stream."""
+        per-launch time in a chain of n launches (which, like a rocprofv3
+        kernel duration, includes its dispatch and drain).  Both are queued
+        behind `busy` on the current stream, so neither holds host time."""
         import torch
         stream = torch.cuda.current_stream().cuda_stream
         x = torch.zeros(1, device="cuda")
-        rec = self.hip.L.hipEventRecord
-        rec.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
-        rec.restype = ctypes.c_int
         for _ in range(20):
             x.fill_(1.0)
-        chain_ms = time_region(torch.cuda.synchronize, lambda: [x.fill_(1.0) for _ in range(n)])
-        ev = self.hip.create(2 * n)
+        ev = self.hip.create(2 * n + 2)
         torch.cuda.synchronize()
-        for j in range(n):
-            rec(ev[2 * j], stream)
+        self.busy()
+        self.rec(ev[2 * n], stream)
+        for _ in range(n):
             x.fill_(1.0)
-            rec(ev[2 * j + 1], stream)
+        self.rec(ev[2 * n + 1], stream)
+        for j in range(n):
+            self.rec(ev[2 * j], stream)
+            x.fill_(1.0)
+            self.rec(ev[2 * j + 1], stream)
         torch.cuda.synchronize()
+        chain_us = 1e3 * self.hip.ms(ev[2 * n], ev[2 * n + 1]) / n
         us = 1e3 * sum(self.hip.ms(ev[2 * j], ev[2 * j + 1]) for j in range(n)) / n
         self.hip.destroy(ev)
-        return us - 1e3 * chain_ms / n
+        return us - chain_us
+
+
+def timed_runs(run, lo, K, R):
+    """R timed runs of the K consecutive steps run(lo, lo + K), then the next
+    K, ...; nothing is attached to the measurement hook.  Returns (median ms,
+    every run's ms, the first step after them)."""
+    import torch
+    ms = []
+    for _ in range(R):
+        ms.append(time_region(torch.cuda.synchronize, lambda a=lo: run(a, a + K)))
+        lo += K
+    return float(np.median(ms)), ms, lo
+
+
+def worker_server_times(prof, grad_one, update_one, n=50):
+    """The paper's T (one worker gradient: the minibatch read from the replay
+    and the TD gradient) and tau (one server update: the apply kernel), on
+    the GPU clock (Sec. IV.D.1)."""
+    grad_one(0)
+    update_one(0)
+    T = prof.spans_us(grad_one, n)
+    tau = prof.spans_us(update_one, n)
+    return {"T_us": round(T, 2), "tau_us": round(tau, 2), "T_over_tau": round(T / tau, 2),
+            "server_bound_updates_per_s": round(1e6 / tau, 1),
+            "method": "median over 50 calls of the GPU time between event pairs on the stream, queued "
+                      "behind a matrix-core loop so that no host time is in them, less the pair overhead"}
+
+
+def single_thread_baseline(grad_fn, update_fn, B, b, budget_s=3.0):
+    """The oracle on one thread: grad_fn(b) computes the gradient (or the
+    forward pass) of b of a step's B transitions and update_fn() the step's
+    update (None: no update); the gradient is repeated for about budget_s and
+    scaled by B / b, the update is timed once."""
+    import oracle
+    n0 = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        n, c0 = 0, time.perf_counter()
+        while True:
+            grad_fn(b)
+            n += 1
+            el = time.perf_counter() - c0
+            if el >= budget_s:
+                break
+        c1 = time.perf_counter()
+        if update_fn is not None:
+            update_fn()
+        upd = time.perf_counter() - c1
+    finally:
+        oracle.set_num_threads(n0)
+    step_s = el / n * B / b + upd
+    return {"value": round(1.0 / step_s, 5), "unit": "steps/s", "cores": 1,
+            "sample": f"{n} x {b} of the {B} transitions of the first step ({el:.1f}s wall), scaled by "
+                      f"{B}/{b}" + (f", plus one update ({upd * 1e3:.1f} ms)" if update_fn is not None else "")}
 
 
 def measured_traffic(config, name):
@@ -310,8 +432,10 @@ def time_region(stream_sync, fn):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--config", default="1", choices=["0", "1", "2", "3", "4a", "4b", "actor", "observe"])
-    ap.add_argument("--steps", type=int, default=None, help="timed steps (default per config)")
+    ap.add_argument("--config", default="4b", choices=["0", "1", "2", "3", "4a", "4b", "actor", "observe"])
+    ap.add_argument("--steps", type=int, default=None, help="timed steps per run (default per config)")
+    ap.add_argument("--repeats", type=int, default=REPEATS,
+                    help="timed runs of --steps steps each; value is their median")
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--breakdown-steps", type=int, default=50)
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -444,20 +568,22 @@ def bench_single(args):
     steps(W)
     work = kernel_work(shape, B)
     work.pop("gather")
-    saved = theta.clone()
-    bd = prof.breakdown(lambda: steps(args.breakdown_steps), args.breakdown_steps, list(work))
-    theta.copy_(saved)
+    nb = min(args.breakdown_steps, K)
+    bd = prof.breakdown(lambda: steps(nb), nb, list(work))
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
-    kid, ev = prof.attach(dom, K * 4 // sample_stride(K) + 4, sample_stride(K))
-    ms = time_region(torch.cuda.synchronize, lambda: steps(K))
-    raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.overhead()
+    R = args.repeats
+    ms, runs, _ = timed_runs(lambda lo, hi: steps(hi - lo), 0, K, R)
+    kp = KERNEL_PASS_STEPS
+    dom_us, raw_us, used = prof.kernel_pass(dom, lambda: steps(kp), kp)
     rec = base_record(K, W, ms)
-    rec["config"] = {"workload": "config 0: small Q-network, one batch of 32 uniform random "
-                                 "states, TD gradient + SGD step (lr 2.5e-4) repeated",
+    rec["timed_runs_ms"] = [round(x, 3) for x in runs]
+    rec["config"] = {"workload": f"config 0: small Q-network, one batch of 32 uniform random "
+                                 f"states, TD gradient + SGD step (lr 2.5e-4) repeated {K} times "
+                                 f"(median of {R} timed runs)",
                      "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "batch": B, "update": "sgd",
                      "gamma": GAMMA, "target": "theta"}
     rec["transitions_per_s"] = round(rec["value"] * B, 1)
+    rec["step_tflops"] = round(step_flop(shape, B) * rec["value"] / 1e12, 4)
     rec["roofline"] = roofline(work, dom, dom_us, used, 1, raw_us, "0")
     rec["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()}}
     if not args.no_cpu_baseline:
@@ -475,6 +601,10 @@ def bench_single(args):
                                "cores": oracle.num_threads(), "kind": "oracle",
                                "sample": f"{n} repetitions of the same step (fp64 TD gradient + "
                                          f"SGD), {el:.1f}s wall"}
+        rec["cpu_baseline"]["single_thread"] = single_thread_baseline(
+            lambda b: oracle.td_gradient(shape, th0, None, s_h[:b], sn_h[:b], a_h[:b], r_h[:b], t_h[:b],
+                                         float(F32(GAMMA))),
+            lambda: oracle.apply_update("sgd", th0, None, res["grad"], float(F32(LR))), B, B)
     return rec
 
 
@@ -490,7 +620,6 @@ def bench_sequential(args):
     B, SIZE, SEED, LR, GAMMA = 32, 100_000, 1001, 2.5e-4, 0.99
     K = args.steps or 2000
     W = args.warmup if args.warmup is not None else 50
-    total = K + W
     t0 = time.time()
     log(f"replay: generating {SIZE} transitions (seed {SEED})")
     hr = di.host_replay(SIZE, shape.n_actions, SEED)
@@ -498,6 +627,10 @@ def bench_sequential(args):
     rec = rp.frames
     log(f"replay ready in {time.time() - t0:.1f}s ({rec.numel() / 2**30:.2f} GiB on device)")
     th0 = di.xavier_theta(shape, SEED)
+    R = args.repeats
+    nb = min(args.breakdown_steps, K)
+    kp = KERNEL_PASS_STEPS
+    total = W + nb + R * K + kp
     idx_host = di.index_stream(total, B, SIZE, SEED)
     idx = torch.from_numpy(idx_host).to(dev)
     theta = torch.from_numpy(th0).to(dev)
@@ -511,56 +644,35 @@ def bench_sequential(args):
     run(0, W)
     torch.cuda.synchronize()
     work = kernel_work(shape, B)
-    saved = theta.clone()
-    nb = min(args.breakdown_steps, K)
     bd = prof.breakdown(lambda: run(W, W + nb), nb, list(work))
-    theta.copy_(saved)
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
-    kid, ev = prof.attach(dom, K * 4 // sample_stride(K) + 4, sample_stride(K))
-    ms = time_region(torch.cuda.synchronize, lambda: run(W, total))
-    raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.overhead()
-    final_loss = float(losses[total - 1].item())
-    log(f"timed {K} steps in {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
+    ms, runs, lo = timed_runs(run, W + nb, K, R)
+    final_loss = float(losses[lo - 1].item())
+    dom_us, raw_us, used = prof.kernel_pass(dom, lambda: run(lo, lo + kp), kp)
+    log(f"timed {R} x {K} steps, median {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
 
-    # the paper's T (worker gradient) and tau (server update), timed separately
-    s = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
-    sn = torch.empty_like(s)
-    a = torch.empty(B, dtype=torch.int32, device=dev)
-    r = torch.empty(B, dtype=torch.float32, device=dev)
-    t = torch.empty(B, dtype=torch.uint8, device=dev)
+    # the paper's T (worker gradient) and tau (server update) on the GPU clock
     g = torch.empty(dq.dqn_param_count(net), dtype=torch.float32, device=dev)
     loss = torch.empty(1, dtype=torch.float32, device=dev)
     tws = dq.workspace(net, B, dq.DQN_OP_TD_GRADIENT, dev)
-
-    def grad_only(n):
-        for i in range(n):
-            dq.replay_gather(rp, idx[i], s, sn, a, r, t)
-            dq.dqn_td_gradient(net, theta, theta, s, sn, a, r, t, GAMMA, g, loss, ws=tws)
-
     th_copy = theta.clone()
-
-    def update_only(n):
-        for _ in range(n):
-            dq.ps_apply_update(dq.PS_SGD, th_copy, th_copy, None, g, LR)
-    nT = min(200, idx.shape[0])
-    T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(nT)) / nT
-    tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(nT)) / nT
+    Tt = worker_server_times(
+        prof, lambda i: dq.dqn_td_gradient_replay(net, th_copy, th_copy, rp, idx[i], GAMMA, g, loss, ws=tws),
+        lambda i: dq.ps_apply_update(dq.PS_SGD, th_copy, th_copy, None, g, LR))
 
     rec_ = base_record(K, W, ms)
+    rec_["timed_runs_ms"] = [round(x, 3) for x in runs]
     rec_["config"] = {
-        "workload": "config 1: small Q-network, batch 32, 100,000-transition device replay, "
-                    "2,000 sequential gather + TD-gradient + SGD steps",
+        "workload": f"config 1: small Q-network, batch 32, 100,000-transition device replay, "
+                    f"{K} sequential gather + TD-gradient + SGD steps (median of {R} timed runs)",
         "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "batch": B, "replay_transitions": SIZE,
         "update": "sgd", "lr": LR, "gamma": GAMMA, "target": "theta",
         "parallelism": "one worker + server on one GPU"}
     rec_["transitions_per_s"] = round(rec_["value"] * B, 1)
-    rec_["step_tflops"] = round(sum(v[0] for v in work.values()) * rec_["value"] / 1e12, 4)
+    rec_["step_tflops"] = round(step_flop(shape, B) * rec_["value"] / 1e12, 4)
     rec_["final_loss"] = final_loss
     rec_["roofline"] = roofline(work, dom, dom_us, used, 1, raw_us, "1")
-    rec_["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
-                         "T_us": round(T_us, 2), "tau_us": round(tau_us, 2),
-                         "T_over_tau": round(T_us / tau_us, 2)}
+    rec_["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()}, **Tt}
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle steps for about {args.cpu_seconds:.0f}s")
         th = th0.copy()
@@ -578,6 +690,11 @@ def bench_sequential(args):
             "kind": "oracle",
             "sample": f"first {n} steps of the same run (batch 32, same replay and index stream), "
                       f"gather + fp64 TD gradient + SGD, {el:.1f}s wall"}
+        si, sni, ai, ri, ti = oracle.gather_from_host_replay(hr, idx_host[0])
+        rec_["cpu_baseline"]["single_thread"] = single_thread_baseline(
+            lambda b: oracle.td_gradient(shape, th0, None, si[:b], sni[:b], ai[:b], ri[:b], ti[:b],
+                                         float(F32(GAMMA))),
+            lambda: oracle.apply_update("sgd", th0, None, res["grad"], float(F32(LR))), B, B)
     return rec_
 
 
@@ -602,7 +719,10 @@ def bench_actor(args):
     FILL = 64
     K = args.steps or 2000
     W = args.warmup if args.warmup is not None else 50
-    total = FILL + W + K
+    R = args.repeats
+    nb = min(args.breakdown_steps, K, 50)
+    kp = KERNEL_PASS_STEPS
+    total = FILL + W + nb + R * K + kp
     th0 = di.xavier_theta(shape, SEED)
     theta = torch.from_numpy(th0).to(dev)
     tgt = torch.empty_like(theta)
@@ -644,27 +764,25 @@ def bench_actor(args):
     # the acting forward shares conv12_fwd, fc1_fwd and head with the TD step, so the roofline is
     # taken over kernels that only one of them launches
     cands = ("conv12_bwd", "fc1_bwd", "finalize_apply", "snake_step")
-    nb = min(args.breakdown_steps, K, 50)
     bd = prof.breakdown(lambda: run(FILL + W, FILL + W + nb), nb, [k for k in work if k in cands] +
                         ["conv12_fwd", "fc1_fwd", "head"])
     # the games and the learner go on from where the breakdown left them
     dom = max((k for k in bd if k in cands), key=lambda k: bd[k][0] * bd[k][1])
-    kid, ev = prof.attach(dom, K // sample_stride(K) + 4, sample_stride(K))
-    lo = FILL + W + nb
-    Kt = K - nb
-    ms = time_region(torch.cuda.synchronize, lambda: run(lo, lo + Kt))
-    raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.overhead()
-    out = base_record(Kt, W, ms)
+    ms, runs, lo = timed_runs(run, FILL + W + nb, K, R)
+    final_loss = float(losses[lo - 1].item())
+    dom_us, raw_us, used = prof.kernel_pass(dom, lambda: run(lo, lo + kp), kp)
+    out = base_record(K, W, ms)
+    out["timed_runs_ms"] = [round(x, 3) for x in runs]
     out["config"] = {
         "workload": f"Alg. 1 closed: {E} Snake games (12x12 board, 84x84 frames) act epsilon-greedily with "
                     f"annealed epsilon and store into a {E * N:,}-experience replay pooled over the games, then "
-                    f"one TD gradient + SGD step on a minibatch of {B}; target refreshed every {C}",
+                    f"one TD gradient + SGD step on a minibatch of {B}; target refreshed every {C}; "
+                    f"{K} iterations (median of {R} timed runs)",
         "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "games": E, "batch": B, "replay_states": E * N,
         "update": "sgd", "lr": LR, "gamma": GAMMA, "epsilon": f"{EMAX} -> {EMIN} over {NMAX} iterations"}
     out["env_steps_per_s"] = round(out["value"] * E, 1)
     out["transitions_per_s"] = round(out["value"] * B, 1)
-    out["final_loss"] = float(losses[lo + Kt - 1].item())
+    out["final_loss"] = final_loss
     out["roofline"] = roofline(work, dom, dom_us, used, 1, raw_us, None)
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
                         "launches_per_step": {k: v[1] / nb for k, v in bd.items()}}
@@ -712,7 +830,9 @@ def bench_observe(args):
     E, N, H, Wd, TOP, LEFT, F, POOL, SEED = 1024, 64, 176, 176, 4, 4, 2, 8, 1006
     K = args.steps or 2000
     W = args.warmup if args.warmup is not None else 50
-    total = W + K
+    R = args.repeats
+    kp = KERNEL_PASS_STEPS
+    total = W + R * K + kp
     log(f"observe: generating {POOL} sets of {E} screens {H}x{Wd}")
     screens_host = [di.rgb_screens(E, SEED * 100 + i, H, Wd) for i in range(POOL)]
     screens = [torch.from_numpy(x).to(dev) for x in screens_host]
@@ -733,28 +853,27 @@ def bench_observe(args):
     torch.cuda.synchronize()
     hip = HipEvents()
     prof = Profiler(hip)
-    kid, ev = prof.attach("observe", K // sample_stride(K) + 4, sample_stride(K))
-    ms = time_region(torch.cuda.synchronize, lambda: run(W, W + K))
-    raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.overhead()
+    ms, runs, lo = timed_runs(run, W, K, R)
+    dom_us, raw_us, used = prof.kernel_pass("observe", lambda: run(lo, lo + kp), kp)
     # algorithmic bytes per launch, averaged over the timed steps: the 168 x 168 x 3 window of
     # every screen, the three kept frames of the games that go on, the 4-frame state and its
     # replay record (twice when the record lands in slot 0, which slot N repeats), the side
     # fields (read 4 + 1 + 1 bytes, write 3)
     FB = 84 * 84
     win = (84 * F) ** 2 * 3
-    steps = np.arange(W, W + K)
-    kept = 3 * FB * (1 - term_h[W:W + K]).sum(axis=1)
+    steps = np.arange(lo, lo + kp)
+    kept = 3 * FB * (1 - term_h[lo:lo + kp]).sum(axis=1)
     mirror = ((steps + 1) % N == 0) * E * 4 * FB
     per = E * (win + 2 * 4 * FB + 9) + kept + mirror
     work = {"observe": (0, int(round(per.mean())))}
     out = base_record(K, W, ms)
+    out["timed_runs_ms"] = [round(x, 3) for x in runs]
     out["metric"] = "observe steps/sec (raw RGB screens -> phi -> 4-frame states + replay); HBM GB/s"
     out["dtype"] = "u8"
     out["config"] = {
         "workload": f"phi of {E} raw {H}x{Wd} RGB screens per step (BT.601 gray, {84 * F}x{84 * F} crop at "
                     f"({TOP},{LEFT}), {F}x{F} mean) into {E} 4-frame states and a replay of {N} states per game; "
-                    f"10% of the games restart per step",
+                    f"10% of the games restart per step; {K} steps (median of {R} timed runs)",
         "games": E, "screen": [H, Wd, 3], "factor": F, "replay_states": E * N}
     out["screens_per_s"] = round(out["value"] * E, 1)
     out["roofline"] = roofline(work, "observe", dom_us, used, 1, raw_us, "observe")
@@ -801,33 +920,20 @@ def bench_replica_sweep(args):
     th0 = torch.from_numpy(di.xavier_theta(shape, SEED)).to(dev)
     P = dq.dqn_param_count(net)
     RS = dq.dqn_train_ring_stride(net)
+    prof = Profiler(HipEvents())
     rows = []
     for B in (32, 128, 512):
         idx = torch.from_numpy(di.index_stream(U, B, SIZE, SEED + B)).to(dev)
         # T and tau alone
-        s = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
-        sn = torch.empty_like(s)
-        a = torch.empty(B, dtype=torch.int32, device=dev)
-        r = torch.empty(B, dtype=torch.float32, device=dev)
-        t = torch.empty(B, dtype=torch.uint8, device=dev)
         g = torch.empty(P, dtype=torch.float32, device=dev)
         loss = torch.empty(1, dtype=torch.float32, device=dev)
         G = torch.zeros(P, dtype=torch.float32, device=dev)
         tws = dq.workspace(net, B, dq.DQN_OP_TD_GRADIENT, dev)
         th = th0.clone()
-
-        def grad_only(n):
-            for i in range(n):
-                dq.dqn_td_gradient_replay(net, th, th, rp, idx[i], GAMMA, g, loss, ws=tws)
-
-        def update_only(n):
-            for _ in range(n):
-                dq.ps_apply_update(dq.PS_ADAGRAD, th, th, G, g, LR, 0.0, EPS)
-        grad_only(20)
-        update_only(20)
-        nT = min(200, idx.shape[0])
-        T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(nT)) / nT
-        tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(nT)) / nT
+        Tt = worker_server_times(
+            prof, lambda i: dq.dqn_td_gradient_replay(net, th, th, rp, idx[i], GAMMA, g, loss, ws=tws),
+            lambda i: dq.ps_apply_update(dq.PS_ADAGRAD, th, th, G, g, LR, 0.0, EPS))
+        T_us, tau_us = Tt["T_us"], Tt["tau_us"]
         del tws
         for R in (1, 2, 4, 8, 16, 32):
             S = min(4, R - 1)
@@ -873,7 +979,7 @@ def bench_replicas(args):
     import paper_1508_04186_amd as dq
     dev = torch.device("cuda:0")
     net, shape = _small_setup(dev)
-    B, SIZE, SEED, LR, EPS, GAMMA, R, S = 32, 100_000, 1002, 0.01, 1e-8, 0.99, 16, 4
+    B, SIZE, SEED, LR, EPS, GAMMA, R_, S = 32, 100_000, 1002, 0.01, 1e-8, 0.99, 16, 4
     U = args.steps or 5000
     W = args.warmup if args.warmup is not None else 100
     log(f"replay: generating {SIZE} transitions (seed {SEED})")
@@ -887,14 +993,14 @@ def bench_replicas(args):
     ring = torch.empty((S + 1) * RS, dtype=torch.float32, device=dev)
     G = torch.zeros(P, dtype=torch.float32, device=dev)
     losses = torch.empty(U, dtype=torch.float32, device=dev)
-    ws = torch.empty(dq.dqn_train_workspace_bytes(net, B, R), dtype=torch.uint8, device=dev)
-    hs = dq.HipStreams(R + 1)
+    ws = torch.empty(dq.dqn_train_workspace_bytes(net, B, R_), dtype=torch.uint8, device=dev)
+    hs = dq.HipStreams(R_ + 1)
 
     def run(n):
         ring[:P].copy_(torch.from_numpy(th0).to(dev))
         G.zero_()
         torch.cuda.synchronize()
-        dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA, rp, idx[:n], R, S,
+        dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA, rp, idx[:n], R_, S,
                               hs.handles, losses_out=losses[:n], ws=ws)
 
     run(W)
@@ -905,63 +1011,55 @@ def bench_replicas(args):
     nb = min(args.breakdown_steps, U)
     bd = prof.breakdown(lambda: run(nb), nb, list(work))
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
-    # timed: all U updates from the initial parameters (the setup copies
-    # above are outside the region)
+    # timed: all U updates from the initial parameters, R times (the setup
+    # copies are outside the timed regions)
+    R = args.repeats
+    runs = []
+    for _ in range(R):
+        ring[:P].copy_(torch.from_numpy(th0).to(dev))
+        G.zero_()
+        runs.append(time_region(torch.cuda.synchronize,
+                                lambda: dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA,
+                                                              rp, idx, R_, S, hs.handles, losses_out=losses,
+                                                              ws=ws)))
+    ms = float(np.median(runs))
+    final_loss = float(losses[U - 1].item())
+    # the dominant kernel's launch time over a separate run of the first updates
+    kp = min(U, KERNEL_PASS_STEPS)
     ring[:P].copy_(torch.from_numpy(th0).to(dev))
     G.zero_()
-    kid, ev = prof.attach(dom, U * 4 // sample_stride(U) + 4, sample_stride(U))
-    e0 = time.perf_counter()
-    ms = time_region(torch.cuda.synchronize,
-                     lambda: dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA,
-                                                   rp, idx, R, S, hs.handles, losses_out=losses,
-                                                   ws=ws))
-    host_s = time.perf_counter() - e0
-    raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.overhead()
-    final_loss = float(losses[U - 1].item())
+    dom_us, raw_us, used = prof.kernel_pass(
+        dom, lambda: dq.dqn_train_replicas(net, ring, G, dq.PS_ADAGRAD, LR, 0.0, EPS, GAMMA, rp, idx[:kp], R_, S,
+                                           hs.handles, ws=ws), kp * max(1, round(bd[dom][1] / nb)))
     hs.close()
-    log(f"timed {U} updates in {ms:.1f} ms (host enqueue+wait {host_s * 1e3:.1f} ms)")
+    log(f"timed {R} x {U} updates, median {ms:.1f} ms")
     # T and tau (paper Sec. IV.D.1): one worker gradient, one server update
-    s = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
-    sn = torch.empty_like(s)
-    a = torch.empty(B, dtype=torch.int32, device=dev)
-    r = torch.empty(B, dtype=torch.float32, device=dev)
-    t = torch.empty(B, dtype=torch.uint8, device=dev)
     g = torch.empty(P, dtype=torch.float32, device=dev)
     loss = torch.empty(1, dtype=torch.float32, device=dev)
     tws = dq.workspace(net, B, dq.DQN_OP_TD_GRADIENT, dev)
     th = ring[:P].clone()
-
-    def grad_only(n):
-        for i in range(n):
-            dq.replay_gather(rp, idx[i], s, sn, a, r, t)
-            dq.dqn_td_gradient(net, th, th, s, sn, a, r, t, GAMMA, g, loss, ws=tws)
-
-    def update_only(n):
-        for _ in range(n):
-            dq.ps_apply_update(dq.PS_ADAGRAD, th, th, G, g, LR, 0.0, EPS)
-    nT = min(200, idx.shape[0])
-    T_us = 1e3 * time_region(torch.cuda.synchronize, lambda: grad_only(nT)) / nT
-    tau_us = 1e3 * time_region(torch.cuda.synchronize, lambda: update_only(nT)) / nT
+    G2 = G.clone()
+    Tt = worker_server_times(
+        prof, lambda i: dq.dqn_td_gradient_replay(net, th, th, rp, idx[i], GAMMA, g, loss, ws=tws),
+        lambda i: dq.ps_apply_update(dq.PS_ADAGRAD, th, th, G2, g, LR, 0.0, EPS))
 
     out = base_record(U, W, ms)
     out["config"] = {
         "workload": "config 2: 16 small-Q-network worker replicas on 16 streams + server stream, "
-                    "AdaGrad (lr 0.01, eps 1e-8), staleness <= 4, 5,000 updates of batch 32, "
-                    "100,000-transition device replay",
-        "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "batch": B, "replicas": R, "staleness": S,
+                    f"AdaGrad (lr 0.01, eps 1e-8), staleness <= 4, {U} updates of batch 32, "
+                    f"100,000-transition device replay (median of {R} timed runs)",
+        "net": "conv16@8x8/4-conv32@4x4/2-fc256-fc6", "batch": B, "replicas": R_, "staleness": S,
         "replay_transitions": SIZE, "update": "adagrad", "lr": LR, "gamma": GAMMA,
         "parallelism": "16 replicas + 1 server on one GPU (streams)"}
     out["transitions_per_s"] = round(out["value"] * B, 1)
+    out["step_tflops"] = round(step_flop(shape, B) * out["value"] / 1e12, 4)
     out["final_loss"] = final_loss
     out["roofline"] = roofline(work, dom, dom_us, used, 1, raw_us, "2")
     out["roofline"]["note"] = ("kernels of up to five updates run concurrently on the replica "
-                               "streams, so the event-bracketed launch time includes sharing "
-                               "the GPU with them")
-    out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
-                        "T_us": round(T_us, 2), "tau_us": round(tau_us, 2),
-                        "T_over_tau": round(T_us / tau_us, 2),
-                        "server_bound_updates_per_s": round(1e6 / tau_us, 1)}
+                               "streams, so the event-bracketed launch time (a separate run of the "
+                               "first updates) includes sharing the GPU with them")
+    out["timed_runs_ms"] = [round(x, 3) for x in runs]
+    out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()}, **Tt}
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle stale-schedule updates for about {args.cpu_seconds:.0f}s")
         n_try = 8
@@ -977,6 +1075,14 @@ def bench_replicas(args):
         out["cpu_baseline"] = {"value": round(n / el, 3), "unit": "steps/s",
                                "cores": oracle.num_threads(), "kind": "oracle",
                                "sample": f"first {n} updates of the same schedule, {el:.1f}s wall"}
+        si, sni, ai, ri, ti = oracle.gather_from_host_replay(hr, idx_host[0])
+        res = oracle.td_gradient(shape, th0, None, si, sni, ai, ri, ti, float(F32(GAMMA)))
+        G0 = np.zeros_like(th0)
+        out["cpu_baseline"]["single_thread"] = single_thread_baseline(
+            lambda b: oracle.td_gradient(shape, th0, None, si[:b], sni[:b], ai[:b], ri[:b], ti[:b],
+                                         float(F32(GAMMA))),
+            lambda: oracle.apply_update("adagrad", th0, G0, res["grad"], float(F32(LR)), eps=float(F32(EPS))),
+            B, B)
     return out
 
 
@@ -1028,7 +1134,10 @@ def bench_large(args):
         B, C = 2048, 0
         K = args.steps or 100
         W = args.warmup if args.warmup is not None else 5
-    total = K + W
+    R = args.repeats
+    nb = min(args.breakdown_steps, K, 20)
+    kp = KERNEL_PASS_STEPS
+    total = W + nb + R * K + kp
     rp = _large_replay(dev, SIZE, SEED)
     th0 = di.xavier_theta(shape, SEED)
     idx_host = di.index_stream(total, B, SIZE, SEED)
@@ -1045,27 +1154,27 @@ def bench_large(args):
     run(0, W)
     torch.cuda.synchronize()
     work = kernel_work(shape, B)
-    saved = theta.clone()
-    saved_t = None if tgt is None else tgt.clone()
-    nb = min(args.breakdown_steps, K, 20)
     bd = prof.breakdown(lambda: run(W, W + nb), nb, list(work))
-    theta.copy_(saved)
-    if tgt is not None:
-        tgt.copy_(saved_t)
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
     lps = max(1, round(bd[dom][1] / nb))          # launches of the kernel per step
-    stride = sample_stride(K)
-    kid, ev = prof.attach(dom, K * lps // stride + 4, stride)
-    ms = time_region(torch.cuda.synchronize, lambda: run(W, total))
-    raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.overhead()
-    final_loss = float(losses[total - 1].item())
-    log(f"timed {K} steps in {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
+    ms, runs, lo = timed_runs(run, W + nb, K, R)
+    final_loss = float(losses[lo - 1].item())
+    dom_us, raw_us, used = prof.kernel_pass(dom, lambda: run(lo, lo + kp), kp * lps)
+    log(f"timed {R} x {K} steps, median {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
+    # the paper's T (worker gradient) and tau (server update) on the GPU clock
+    g = torch.empty(dq.dqn_param_count(net), dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    tws = dq.workspace(net, B, dq.DQN_OP_TD_GRADIENT, dev)
+    th_copy = theta.clone()
+    Tt = worker_server_times(
+        prof, lambda i: dq.dqn_td_gradient_replay(net, th_copy, th_copy, rp, idx[i], GAMMA, g, loss, ws=tws),
+        lambda i: dq.ps_apply_update(dq.PS_SGD, th_copy, th_copy, None, g, LR), n=20)
+    del tws
     out = base_record(K, W, ms)
     name = "config 3" if args.config == "3" else "config 4b"
     out["config"] = {
         "workload": f"{name}: large Q-network, batch {B}, 1,000,000-transition device replay, "
-                    f"{K} sequential gather + TD-gradient + SGD steps"
+                    f"{K} sequential gather + TD-gradient + SGD steps (median of {R} timed runs)"
                     + (f", target network refreshed every {C} steps" if C else "")
                     + (", bf16-input MFMA contractions with fp32 accumulation" if bf16 else ""),
         "net": "conv32@8x8/4-conv64@4x4/2-conv64@3x3/1-fc512-fc18", "batch": B,
@@ -1074,15 +1183,16 @@ def bench_large(args):
     if bf16:
         out["dtype"] = "bf16"
         out["config"]["accumulate"] = "f32"
+    out["timed_runs_ms"] = [round(x, 3) for x in runs]
     out["transitions_per_s"] = round(out["value"] * B, 1)
-    out["step_tflops"] = round(sum(v[0] for v in work.values()) * out["value"] / 1e12, 4)
+    out["step_tflops"] = round(step_flop(shape, B) * out["value"] / 1e12, 4)
     out["final_loss"] = final_loss
     out["roofline"] = roofline(work, dom, dom_us, used, lps, raw_us,
                                args.config + (" bf16" if bf16 else ""),
                                PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
                         "per_layer_tflops": {k: round(work[k][0] / (v[0] * (v[1] / nb) * 1e-6) / 1e12, 3)
-                                             for k, v in bd.items() if work[k][0] > 0}}
+                                             for k, v in bd.items() if work[k][0] > 0}, **Tt}
     if not args.no_cpu_baseline:
         log(f"cpu baseline: oracle steps for about {args.cpu_seconds:.0f}s")
         th = th0.copy()
@@ -1100,6 +1210,11 @@ def bench_large(args):
                                "sample": f"first {n} step(s) of the same run (batch {B}), fp64 TD "
                                          f"gradient{' (bf16-input variant)' if bf16 else ''} + SGD, "
                                          f"{el:.1f}s wall"}
+        s, sn, a, r, t = di.transitions_at(SEED, idx_host[0][:32], shape.n_actions, SIZE)
+        out["cpu_baseline"]["single_thread"] = single_thread_baseline(
+            lambda b: oracle.td_gradient(shape, th0, None, s[:b], sn[:b], a[:b], r[:b], t[:b],
+                                         float(F32(GAMMA)), bf16=bf16),
+            lambda: oracle.apply_update("sgd", th0, None, res["grad"], float(F32(LR))), B, 32)
     return out
 
 
@@ -1116,10 +1231,14 @@ def bench_forward(args):
     SIZE, SEED, B, EPS = 1_000_000, 1004, 8192, F32(0.05)
     K = args.steps or 200
     W = args.warmup if args.warmup is not None else 10
+    R = args.repeats
+    nb = min(args.breakdown_steps, K, 20)
+    kp = KERNEL_PASS_STEPS
+    total = W + nb + R * K + kp
     rp = _large_replay(dev, SIZE, SEED)
     th0 = di.xavier_theta(shape, SEED)
     rng = np.random.default_rng(SEED)
-    idx_host = rng.integers(0, SIZE, size=(K + W, B), dtype=np.int64)
+    idx_host = rng.integers(0, SIZE, size=(total, B), dtype=np.int64)
     idx = torch.from_numpy(idx_host).to(dev)
     draws = torch.from_numpy(di.egreedy_draws(B, SEED)).to(dev)
     theta = torch.from_numpy(th0).to(dev)
@@ -1136,28 +1255,26 @@ def bench_forward(args):
     run(0, W)
     torch.cuda.synchronize()
     work = kernel_work(shape, B, forward_only=True)
-    nb = min(args.breakdown_steps, K, 20)
     bd = prof.breakdown(lambda: run(W, W + nb), nb, list(work))
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
     lps = max(1, round(bd[dom][1] / nb))
-    stride = sample_stride(K)
-    kid, ev = prof.attach(dom, K * lps // stride + 4, stride)
-    ms = time_region(torch.cuda.synchronize, lambda: run(W, K + W))
-    raw_us, used = prof.collect(kid, ev)
-    dom_us = raw_us - prof.overhead()
-    log(f"timed {K} forward passes in {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
+    ms, runs, lo = timed_runs(run, W + nb, K, R)
+    dom_us, raw_us, used = prof.kernel_pass(dom, lambda: run(lo, lo + kp), kp * lps)
+    log(f"timed {R} x {K} forward passes, median {ms:.1f} ms; dominant kernel {dom} {dom_us:.2f} us/launch")
     out = base_record(K, W, ms)
     out["config"] = {
-        "workload": "config 4a: large Q-network, epsilon-greedy (eps 0.05) forward pass over 8,192 "
-                    "states gathered from a 1,000,000-transition device replay"
+        "workload": f"config 4a: large Q-network, epsilon-greedy (eps 0.05) forward pass over 8,192 "
+                    f"states gathered from a 1,000,000-transition device replay, {K} passes "
+                    f"(median of {R} timed runs)"
                     + (", bf16-input MFMA contractions with fp32 accumulation" if bf16 else ""),
         "net": "conv32@8x8/4-conv64@4x4/2-conv64@3x3/1-fc512-fc18", "batch": B,
         "replay_transitions": SIZE, "epsilon": float(EPS)}
     if bf16:
         out["dtype"] = "bf16"
         out["config"]["accumulate"] = "f32"
+    out["timed_runs_ms"] = [round(x, 3) for x in runs]
     out["states_per_s"] = round(out["value"] * B, 1)
-    out["step_tflops"] = round(sum(v[0] for v in work.values()) * out["value"] / 1e12, 4)
+    out["step_tflops"] = round(step_flop(shape, B, forward_only=True) * out["value"] / 1e12, 4)
     out["roofline"] = roofline(work, dom, dom_us, used, lps, raw_us, "4a" + (" bf16" if bf16 else ""),
                                PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
@@ -1174,6 +1291,8 @@ def bench_forward(args):
                                "cores": oracle.num_threads(), "kind": "oracle",
                                "sample": f"fp64 forward + epsilon-greedy choice on {n} of the "
                                          f"8,192 states ({el:.1f}s wall), scaled to 8,192"}
+        out["cpu_baseline"]["single_thread"] = single_thread_baseline(
+            lambda b: oracle.forward_q(shape, th0, s[:b], bf16=bf16), None, B, 32)
     return out
 
 

@@ -18,6 +18,11 @@
  *    enqueued.  DQN_EHIP reports a failed kernel launch.  Faults inside a
  *    kernel surface at the caller's next synchronization.
  *  - Calls on different streams that write different buffers may overlap.
+ *  - Thread safety: the entry points keep no mutable process-wide state, so
+ *    they may be called concurrently from several host threads (on their
+ *    own streams and buffers).  The only process-wide state is the
+ *    measurement hook of dqn_profile.h: while a kernel is attached there,
+ *    calls must not race with attach/detach or with each other.
  *
  * Networks (Sec. III.A; Appendix A's figure is not available, so the two
  * supported shapes are fixed here): input 4x84x84 bytes scaled by 1/255,

@@ -58,6 +58,8 @@ def _lib():
         lib = ctypes.CDLL(lib_path())
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
+        lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+        lib.oracle_set_num_threads.restype = ctypes.c_int
         lib.oracle_param_count.argtypes = [ctypes.POINTER(_Net)]
         lib.oracle_param_count.restype = ctypes.c_int64
         lib.oracle_param_offset.argtypes = [ctypes.POINTER(_Net), ctypes.c_int32, ctypes.c_int32]
@@ -117,6 +119,12 @@ def _check(rc, what):
 
 def num_threads() -> int:
     return int(_lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (the results do not
+    depend on the count)."""
+    _check(_lib().oracle_set_num_threads(int(n)), "oracle_set_num_threads")
 
 
 def param_count(net) -> int:

@@ -125,8 +125,14 @@ int oracle_bf16_round(const double* in, int64_t n, double* out) {
     return ORACLE_OK;
 }
 
-/* Threads the oracle's parallel loops use. */
+/* Threads the oracle's parallel loops use, and a way to set that count (the
+ * results do not depend on it: every reduction runs in sample order). */
 int oracle_num_threads(void) { return omp_get_max_threads(); }
+int oracle_set_num_threads(int n) {
+    if (n < 1) return ORACLE_EINVAL;
+    omp_set_num_threads(n);
+    return ORACLE_OK;
+}
 
 int64_t oracle_param_count(const oracle_net* net) {
     shapes_t sh;

@@ -1,6 +1,7 @@
 // C ABI of libdqn.so (declared in include/dqn.h): argument checks, the
 // workspace layout and the kernel sequence of each entry point.
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstddef>
 
@@ -84,7 +85,8 @@ constexpr int kPairMaxBatch = 64;
 // run as one fused launch (measured faster at every batch up to 1024
 // samples per launch, and by 2x at 64).
 constexpr int kFuseMaxRows = 1 << 20;
-bool g_fusion = true;  // dqn_profile_set_fusion
+// dqn_profile_set_fusion (a measurement switch; read once per call)
+std::atomic<bool> g_fusion{true};
 // Samples per forward launch from which the large network's fp32 conv layers
 // run as one implicit GEMM over all samples (2-3x the per-layer kernel from
 // 256 samples; slower at 64).
@@ -224,8 +226,13 @@ struct ProfSlot {
     bool open = false;
 };
 ProfSlot g_prof[DQN_K_COUNT];
+// Number of attached slots.  While it is zero the launches touch no slot, so
+// the entry points read and write no process-wide state and concurrent calls
+// from several host threads do not interact.
+std::atomic<int> g_prof_attached{0};
 
 inline void prof_begin(int k, hipStream_t st) {
+    if (g_prof_attached.load(std::memory_order_relaxed) == 0) return;
     ProfSlot& p = g_prof[k];
     if (p.ev && p.used < p.n && p.seen % p.stride == 0) {
         (void)hipEventRecord(p.ev[2 * p.used], st);
@@ -234,6 +241,7 @@ inline void prof_begin(int k, hipStream_t st) {
     ++p.seen;
 }
 inline void prof_end(int k, hipStream_t st) {
+    if (g_prof_attached.load(std::memory_order_relaxed) == 0) return;
     ProfSlot& p = g_prof[k];
     if (p.open) {
         (void)hipEventRecord(p.ev[2 * p.used + 1], st);
@@ -350,7 +358,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // Forward of s under theta (samples 0..B-1) and of s' under theta^-
     // (samples B..2B-1): one launch per layer, or both conv layers of the
     // small network in one launch at small batch.
-    const bool fused_fwd = g_fusion && L == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
+    const bool fusion = g_fusion.load(std::memory_order_relaxed);
+    const bool fused_fwd = fusion && L == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
                            2 * B <= kFuseMaxRows && conv_s12_fwd_aligned(s0) && conv_s12_fwd_aligned(sn0);
     if (fused_fwd)
         RUN(DQN_K_CONV12_FWD,
@@ -443,7 +452,7 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // The small network's conv layers in one launch: conv2's weight gradient,
     // and conv2's input gradient with conv1's weight gradient per (sample,
     // band of conv1 rows).
-    const bool fused_bwd = g_fusion && L == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
+    const bool fused_bwd = fusion && L == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
                            B <= kFuseMaxRows && conv_s12_fwd_aligned(s0);
     int chunks_used[3] = {t.chunks[0], t.chunks[1], t.chunks[2]};
     int& chunks0 = chunks_used[0];
@@ -654,7 +663,7 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
     hipStream_t st = (hipStream_t)stream;
     const float* th = theta;
     const ConvIn in0{states, nullptr, (int64_t)net->in_c * net->in_h * net->in_w, 0};
-    const bool fused_fwd = g_fusion && ni.n_conv == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
+    const bool fused_fwd = g_fusion.load(std::memory_order_relaxed) && ni.n_conv == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
                            batch <= kFuseMaxRows && conv_s12_fwd_aligned(in0);
     if (fused_fwd)
         RUN(DQN_K_CONV12_FWD,
@@ -757,17 +766,20 @@ int ps_apply_update(int32_t rule, const float* theta_in, float* theta_out, float
 int dqn_profile_attach(int32_t kernel, void** events, int32_t n_pairs, int32_t stride) {
     if (kernel < 0 || kernel >= DQN_K_COUNT || n_pairs < 0 || stride < 1) return DQN_EINVAL;
     ProfSlot& p = g_prof[kernel];
+    const bool was = p.ev != nullptr;
     p.ev = (events && n_pairs > 0) ? (hipEvent_t*)events : nullptr;
     p.n = p.ev ? n_pairs : 0;
     p.used = 0;
     p.stride = stride;
     p.seen = 0;
     p.open = false;
+    if (p.ev && !was) g_prof_attached.fetch_add(1, std::memory_order_relaxed);
+    if (!p.ev && was) g_prof_attached.fetch_sub(1, std::memory_order_relaxed);
     return DQN_OK;
 }
 
 int dqn_profile_set_fusion(int32_t enabled) {
-    g_fusion = enabled != 0;
+    g_fusion.store(enabled != 0, std::memory_order_relaxed);
     return DQN_OK;
 }
 

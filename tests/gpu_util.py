@@ -1,5 +1,6 @@
 """Helpers shared by the GPU parity tests: device copies, per-tensor error
-norms against the oracle, and the action-choice comparison rule."""
+bounds against the oracle (normwise and element by element), and the
+action-choice comparison rule."""
 import sys
 
 import numpy as np
@@ -30,6 +31,33 @@ def rel_l2(x, ref):
     return num / den
 
 
+def max_elem_err(x, ref, slack=None):
+    """Largest elementwise error relative to the tensor's largest magnitude:
+    max (|x - ref| - slack) / max |ref| (0 when both are zero).  slack: an
+    elementwise allowance (e.g. one float32 ulp of a stored result)."""
+    x = np.asarray(x, np.float64).ravel()
+    ref = np.asarray(ref, np.float64).ravel()
+    if x.size == 0:
+        return 0.0
+    d = np.abs(x - ref)
+    if slack is not None:
+        d = np.maximum(d - np.asarray(slack, np.float64).ravel(), 0.0)
+    num = d.max()
+    den = np.abs(ref).max()
+    if den == 0.0:
+        return 0.0 if num == 0.0 else np.inf
+    return num / den
+
+
+def assert_close(x, ref, tol=FP32_TOL, what="value"):
+    """Per tensor: the relative L2 error is at most tol, and so is every
+    element's error relative to the tensor's largest magnitude
+    (|x_i - ref_i| <= tol * max |ref|).  Returns (normwise, elementwise)."""
+    n, e = rel_l2(x, ref), max_elem_err(x, ref)
+    assert n <= tol and e <= tol, f"{what}: relative L2 {n:.3e}, max elementwise {e:.3e} (bound {tol})"
+    return n, e
+
+
 def grad_errors(net_shape, g, ref):
     """{tensor name: relative L2 error} over the flat parameter layout."""
     out = {}
@@ -39,10 +67,33 @@ def grad_errors(net_shape, g, ref):
     return out
 
 
-def assert_grad_close(net_shape, g, ref, tol=FP32_TOL, what="grad"):
+def grad_elem_errors(net_shape, g, ref, slack=None):
+    """{tensor name: max elementwise error / max |ref|} over the flat layout."""
+    out = {}
+    for name, (off, shape) in net_shape.slices().items():
+        n = int(np.prod(shape))
+        out[name] = max_elem_err(g[off:off + n], ref[off:off + n],
+                                 None if slack is None else slack[off:off + n])
+    return out
+
+
+def assert_grad_close(net_shape, g, ref, tol=FP32_TOL, what="grad", slack=None):
+    """Every tensor of the flat layout (each W and b separately) within tol,
+    normwise and element by element (assert_close's bounds).  slack: an
+    elementwise allowance added to the elementwise bound, for differences of
+    float32-stored values (a parameter change theta_new - theta carries one
+    ulp of the stored theta_new, whatever computed it).  The largest
+    elementwise error is printed as a diagnostic.  Returns the normwise
+    errors."""
     errs = grad_errors(net_shape, g, ref)
+    elem = grad_elem_errors(net_shape, g, ref, slack)
+    worst = max(elem, key=elem.get)
+    say(f"{what}: max elementwise error {elem[worst]:.2e} ({worst}), max relative L2 "
+        f"{max(errs.values()):.2e}")
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, f"{what}: per-tensor relative L2 errors above {tol}: {bad} (all: {errs})"
+    bad = {k: v for k, v in elem.items() if not v <= tol}
+    assert not bad, f"{what}: per-tensor max elementwise errors above {tol} x max|ref|: {bad} (all: {elem})"
     return errs
 
 

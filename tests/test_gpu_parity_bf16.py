@@ -1,20 +1,23 @@
 """GPU parity of the bf16-input variant of the large Q-network (every conv
-and fc1 contraction operand rounded to bfloat16, fp32 accumulation) against
-the oracle's bf16-input variant, which computes the same definition with
-exact (double) sums.  Tolerance: 3e-2 relative L2 per tensor.
+and fc1 contraction operand rounded to bfloat16, fp32 accumulation).
 
-The unrounded float64 oracle is not the reference here: on these workloads
-an exact bf16-input computation itself differs from it by several percent in
-the gradients (the TD residual Q - y is small next to Q, so the bf16-sized
-error of Q is amplified in dQ), which the oracle shows on its own.  Q values
-stay within the tolerance of the float64 oracle too, and that is checked."""
+Two references, both per tensor (each W and b separately):
+  - the oracle's bf16-input variant, which computes the same definition with
+    exact (double) sums: within 3e-2, normwise and element by element;
+  - the unrounded float64 oracle: Q within 3e-2; the gradients within the
+    error of the exact bf16-input computation itself plus 3e-2, i.e.
+    |g_gpu - g64| / |g64| <= |g_bf16 - g64| / |g64| + 3e-2.  On these
+    workloads an exact bf16-input computation already differs from the
+    float64 gradients by several percent (the TD residual Q - y is small next
+    to Q, so the bf16-sized error of Q is amplified in dQ), so 3e-2 alone
+    is not met against the float64 oracle by any bf16-input computation."""
 import numpy as np
 import pytest
 
 import dqn_inputs as di
 import oracle
 import paper_1508_04186_amd as dq
-from gpu_util import assert_grad_close, check_actions, dev_tensor, grad_errors, host, rel_l2, say
+from gpu_util import assert_close, assert_grad_close, check_actions, dev_tensor, grad_errors, host, rel_l2, say
 
 pytestmark = pytest.mark.gpu
 F32 = np.float32
@@ -55,17 +58,20 @@ def test_bf16_td_gradient_matches_oracle(dev, B, held):
     g, loss, q, y = _run_td(dev, th, tt, s, sn, a, r, t)
     say(f"[bf16-td] batch={B}: oracle (bf16-input variant)")
     ref = oracle.td_gradient(SHAPE, th, tt, s, sn, a, r, t, float(F32(0.99)), bf16=True)
-    assert rel_l2(q, ref["q"]) <= BF16_TOL
-    assert rel_l2(y, ref["y"]) <= BF16_TOL
+    assert_close(q, ref["q"], BF16_TOL, "q")
+    assert_close(y, ref["y"], BF16_TOL, "y")
     assert abs(loss - ref["loss"]) <= BF16_TOL * abs(ref["loss"])
     errs = assert_grad_close(SHAPE, g, ref["grad"], tol=BF16_TOL, what="bf16 grad")
     say(f"[bf16-td] batch={B}: worst per-tensor error vs the bf16-input oracle {max(errs.values()):.2e}")
-    if B <= 256:
-        ref64 = oracle.td_gradient(SHAPE, th, tt, s, sn, a, r, t, float(F32(0.99)))
-        assert rel_l2(q, ref64["q"]) <= BF16_TOL
-        e64 = grad_errors(SHAPE, g, ref64["grad"])
-        say(f"[bf16-td] batch={B}: (diagnostic) worst per-tensor error vs the float64 oracle "
-            f"{max(e64.values()):.2e}")
+    say(f"[bf16-td] batch={B}: oracle (float64)")
+    ref64 = oracle.td_gradient(SHAPE, th, tt, s, sn, a, r, t, float(F32(0.99)))
+    assert_close(q, ref64["q"], BF16_TOL, "q against the float64 oracle")
+    e64 = grad_errors(SHAPE, g, ref64["grad"])
+    b64 = grad_errors(SHAPE, ref["grad"], ref64["grad"])
+    for k in e64:
+        say(f"[bf16-td] batch={B} {k}: GPU vs float64 {e64[k]:.3e}; exact bf16-input vs float64 {b64[k]:.3e}")
+    bad = {k: (e64[k], b64[k]) for k in e64 if not e64[k] <= b64[k] + BF16_TOL}
+    assert not bad, f"bf16 gradients against the float64 oracle: {bad}"
 
 
 def test_bf16_td_gradient_is_deterministic_and_differs_from_fp32(dev):
@@ -93,7 +99,7 @@ def test_bf16_forward_matches_oracle(dev, B):
     dq.dqn_forward(NET, dev_tensor(th), dev_tensor(st), 0.0, None, q, act)
     torch.cuda.synchronize()
     q_ref = oracle.forward_q(SHAPE, th, st, bf16=True)
-    assert rel_l2(host(q), q_ref) <= BF16_TOL
+    assert_close(host(q), q_ref, BF16_TOL, "host(q)")
     act_ref = oracle.select_actions(q_ref, 0.0)
     check_actions(host(act), host(q), q_ref, act_ref, np.zeros(B, bool), tol=BF16_TOL)
 
@@ -113,7 +119,7 @@ def test_bf16_forward_8192_states_egreedy(dev):
     say("[bf16-fwd] oracle (bf16-input variant) on 512 sampled states")
     q_ref = oracle.forward_q(SHAPE, th, st[sample], bf16=True)
     qg = host(q)[sample]
-    assert rel_l2(qg, q_ref) <= BF16_TOL
+    assert_close(qg, q_ref, BF16_TOL, "qg")
     act_ref = oracle.select_actions(q_ref, float(F32(0.05)), draws[sample])
     explore = (draws[sample] >> np.uint64(32)) < np.uint64(214748368)
     check_actions(host(act)[sample], qg, q_ref, act_ref, explore, tol=BF16_TOL)

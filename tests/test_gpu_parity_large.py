@@ -13,7 +13,7 @@ import pytest
 import dqn_inputs as di
 import oracle
 import paper_1508_04186_amd as dq
-from gpu_util import (FP32_TOL, assert_grad_close, check_actions, dev_tensor, host, rel_l2, say,
+from gpu_util import (FP32_TOL, assert_close, assert_grad_close, check_actions, dev_tensor, host, rel_l2, say,
                       split_by_margin)
 
 pytestmark = pytest.mark.gpu
@@ -61,8 +61,8 @@ def test_td_gradient_full_size(dev, name, B, target):
     g, loss, q, y = _run_td(dev, net, th, tt, s, sn, a, r, t, 0.99)
     say(f"[td-large] net={name} batch={B}: oracle")
     ref = oracle.td_gradient(shape, th, tt, s, sn, a, r, t, float(F32(0.99)))
-    assert rel_l2(q, ref["q"]) <= FP32_TOL
-    assert rel_l2(y, ref["y"]) <= FP32_TOL
+    assert_close(q, ref["q"], FP32_TOL, "q")
+    assert_close(y, ref["y"], FP32_TOL, "y")
     assert abs(loss - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
     assert_grad_close(shape, g, ref["grad"])
 
@@ -91,7 +91,7 @@ def test_forward_8192_states_egreedy(dev):
     say("[fwd-large] oracle on 1,024 sampled states")
     q_ref = oracle.forward_q(shape, th, states.reshape(-1, 4, 84, 84))
     qg = host(q)[sample]
-    assert rel_l2(qg, q_ref) <= FP32_TOL
+    assert_close(qg, q_ref, FP32_TOL, "qg")
     act_ref = oracle.select_actions(q_ref, float(F32(0.05)), draws[sample])
     explore = (draws[sample] >> np.uint64(32)) < np.uint64(214748368)
     check_actions(host(act)[sample], qg, q_ref, act_ref, explore)
@@ -124,6 +124,6 @@ def test_td_precision_ambiguous_transitions(dev):
     g2, l2, _, _ = _run_td(dev, net, th, None, s, sn, a, r, t, 0.99)
     assert np.array_equal(g1, g2) and l1 == l2 and np.all(np.isfinite(g1))
     ref = oracle.td_gradient(shape, th, None, s, sn, a, r, t, float(F32(0.99)))
-    assert rel_l2(q, ref["q"]) <= FP32_TOL
-    assert rel_l2(y, ref["y"]) <= FP32_TOL
+    assert_close(q, ref["q"], FP32_TOL, "q")
+    assert_close(y, ref["y"], FP32_TOL, "y")
     assert abs(l1 - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
