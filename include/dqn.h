@@ -194,6 +194,27 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
                     float* grad_out, float* loss_out, float* q_out, float* y_out,
                     void* ws, size_t ws_bytes, void* stream);
 
+/* dqn_td_gradient for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving or training loops, harnesses that forbid
+ * hipMalloc): the same arguments without a workspace, the same kernels and
+ * bitwise the same outputs.  The workspace is the library's own static
+ * device array of 64 MiB, one per GPU, held from the library's load on that
+ * GPU until the process ends; the call allocates and frees nothing.
+ * The batch is limited by that size: when dqn_workspace_bytes(net, batch,
+ * DQN_OP_TD_GRADIENT) exceeds 64 MiB the call returns DQN_EWORKSPACE and
+ * enqueues nothing.  Every batch up to 289 samples fits for the small
+ * network, and every batch up to 94 for the large one (either precision).  The array needs no clearing between calls (every call writes
+ * what it reads).  Every call on one GPU shares that GPU's array: calls that
+ * overlap on one GPU (concurrent streams or host threads) race, so serialize
+ * them.  The stream must belong to the current device (else DQN_EINVAL).
+ * The first call on a device looks up the array's address there
+ * (hipGetSymbolAddress); make that first call outside graph capture. */
+int dqn_td_gradient_noalloc(const dqn_net* net, const float* theta, const float* theta_target,
+                            const uint8_t* s, const uint8_t* s_next, const int32_t* action,
+                            const float* reward, const uint8_t* terminal, int32_t batch, float gamma,
+                            float* grad_out, float* loss_out, float* q_out, float* y_out,
+                            void* stream);
+
 /* The same gradient with the minibatch drawn from the replay memory in the
  * same call (Alg. 1: "uniformly sample minibatch X from D_k", then the
  * gradient): transition j is idx[j] of `replay`, exactly as replay_gather

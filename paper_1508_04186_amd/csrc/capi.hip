@@ -4,12 +4,22 @@
 #include <atomic>
 #include <cmath>
 #include <cstddef>
+#include <mutex>
 
 #include "common.h"
 #include "dqn.h"
 #include "dqn_profile.h"
 
 using namespace dqn;
+
+// Scratch of dqn_td_gradient_noalloc: the workspace of the TD step in the
+// library's own device memory, one copy per GPU (the loader places it when
+// the library's code is loaded on a device; it is held until the process
+// ends).  In host code `scratch` is only a stand-in for the symbol: its
+// device address comes from hipGetSymbolAddress, looked up once per device
+// with that device current, and only that address is handed to kernels.
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
 
 namespace {
 
@@ -581,6 +591,39 @@ int td_step_replay(const dqn_net* net, const float* theta_target, const dqn_repl
 
 }  // namespace dqn
 
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_dev[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// The scratch address on the current device (looked up on the first call on
+// that device).  The stream must belong to the current device.
+int scratch_on_current_device(hipStream_t st, void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return DQN_EHIP;
+    if (dev < 0 || dev >= kMaxDevices) return DQN_EUNSUPPORTED;
+    if (st) {
+        hipDevice_t sdev = -1;
+        if (hipStreamGetDevice(st, &sdev) != hipSuccess) return DQN_EHIP;
+        if (sdev != dev) return DQN_EINVAL;
+    }
+    void* p = g_scratch_dev[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_dev[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return DQN_EHIP;
+            if ((uintptr_t)p % 256 != 0) return DQN_EHIP;
+            g_scratch_dev[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return DQN_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* dqn_status_string(int status) {
@@ -726,6 +769,27 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
     TdSource src{s, s_next, action, reward, terminal, nullptr, nullptr};
     return td_gradient_impl(net, ni, theta, theta_target, src, batch, gamma, grad_out, loss_out,
                             q_out, y_out, ws, ws_bytes, (hipStream_t)stream);
+}
+
+int dqn_td_gradient_noalloc(const dqn_net* net, const float* theta, const float* theta_target,
+                            const uint8_t* s, const uint8_t* s_next, const int32_t* action,
+                            const float* reward, const uint8_t* terminal, int32_t batch, float gamma,
+                            float* grad_out, float* loss_out, float* q_out, float* y_out, void* stream) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (!s || !s_next || !action || !reward || !terminal) return DQN_EINVAL;
+    if (!aligned(s, 16) || !aligned(s_next, 16)) return DQN_EINVAL;
+    if (batch <= 0) return DQN_EINVAL;
+    // Reject a batch whose workspace exceeds the scratch before touching it.
+    if (td_layout(ni, batch, nullptr).bytes > kNoAllocScratchBytes) return DQN_EWORKSPACE;
+    const hipStream_t st = (hipStream_t)stream;
+    void* ws = nullptr;
+    rc = scratch_on_current_device(st, &ws);
+    if (rc != DQN_OK) return rc;
+    TdSource src{s, s_next, action, reward, terminal, nullptr, nullptr};
+    return td_gradient_impl(net, ni, theta, theta_target, src, batch, gamma, grad_out, loss_out,
+                            q_out, y_out, ws, kNoAllocScratchBytes, st);
 }
 
 int dqn_td_gradient_replay(const dqn_net* net, const float* theta, const float* theta_target,

@@ -111,6 +111,9 @@ def lib():
                                              _P, ctypes.c_int32, ctypes.c_float, _P, _P, _P, _P,
                                              _P, ctypes.c_size_t, _P]
         L.dqn_td_gradient_replay.restype = ctypes.c_int
+        L.dqn_td_gradient_noalloc.argtypes = [ctypes.POINTER(_CNet), _P, _P, _P, _P, _P, _P, _P,
+                                              ctypes.c_int32, ctypes.c_float, _P, _P, _P, _P, _P]
+        L.dqn_td_gradient_noalloc.restype = ctypes.c_int
         L.ps_apply_update.argtypes = [ctypes.c_int32, _P, _P, _P, _P, ctypes.c_int64,
                                       ctypes.c_float, ctypes.c_float, ctypes.c_float, _P]
         for f in ("replay_gather", "dqn_forward", "dqn_td_gradient", "ps_apply_update"):
@@ -321,6 +324,33 @@ def dqn_td_gradient(net, theta, theta_target, s, s_next, action, reward, termina
                                _ptr(q_out, torch.float32, "q_out"), _ptr(y_out, torch.float32, "y_out"),
                                _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream))
     _check(rc, "dqn_td_gradient")
+
+
+def dqn_td_gradient_noalloc(net, theta, theta_target, s, s_next, action, reward, terminal, gamma,
+                            grad_out, loss_out, q_out=None, y_out=None, stream=None):
+    """dqn_td_gradient on the library's static per-GPU scratch instead of a
+    caller workspace (include/dqn.h dqn_td_gradient_noalloc)."""
+    import torch
+    B = s.shape[0]
+    P = dqn_param_count(net)
+    for name, t, n in (("theta", theta, P), ("theta_target", theta_target, P),
+                       ("grad_out", grad_out, P), ("s_next", s_next, s.numel()),
+                       ("action", action, B), ("reward", reward, B), ("terminal", terminal, B),
+                       ("loss_out", loss_out, 1), ("q_out", q_out, B * net.n_actions),
+                       ("y_out", y_out, B)):
+        if t is not None and t.numel() < n:
+            raise ValueError(f"{name} too small")
+    rc = lib().dqn_td_gradient_noalloc(ctypes.byref(_cnet(net)), _ptr(theta, torch.float32, "theta"),
+                                       _ptr(theta_target, torch.float32, "theta_target"),
+                                       _ptr(s, torch.uint8, "s"), _ptr(s_next, torch.uint8, "s_next"),
+                                       _ptr(action, torch.int32, "action"),
+                                       _ptr(reward, torch.float32, "reward"),
+                                       _ptr(terminal, torch.uint8, "terminal"), B, float(gamma),
+                                       _ptr(grad_out, torch.float32, "grad_out"),
+                                       _ptr(loss_out, torch.float32, "loss_out"),
+                                       _ptr(q_out, torch.float32, "q_out"), _ptr(y_out, torch.float32, "y_out"),
+                                       _stream(stream))
+    _check(rc, "dqn_td_gradient_noalloc")
 
 
 def dqn_td_gradient_replay(net, theta, theta_target, replay: Replay, idx, gamma, grad_out, loss_out,
