@@ -275,33 +275,34 @@ class Profiler:
         self.hip.destroy(ev)
         return raw - self.overhead(), raw, used
 
-    def spans_us(self, fn, n):
-        """Median GPU time (us) of one call fn(i), over n calls each bracketed
-        by an event pair on the current stream and queued behind `busy`, less
-        the pair overhead."""
+    def chain_us(self, fn, n):
+        """GPU time (us) per call of n back-to-back calls fn(0..n-1) on the
+        current stream, between one event before the first and one after the
+        last, queued behind `busy` (so no host time is in it)."""
         import torch
         stream = torch.cuda.current_stream().cuda_stream
-        ev = self.hip.create(2 * n)
+        ev = self.hip.create(2)
         torch.cuda.synchronize()
         self.busy()
+        self.rec(ev[0], stream)
         for i in range(n):
-            self.rec(ev[2 * i], stream)
             fn(i)
-            self.rec(ev[2 * i + 1], stream)
+        self.rec(ev[1], stream)
         torch.cuda.synchronize()
-        us = [1e3 * self.hip.ms(ev[2 * i], ev[2 * i + 1]) for i in range(n)]
+        us = 1e3 * self.hip.ms(ev[0], ev[1]) / n
         self.hip.destroy(ev)
-        return float(np.median(us)) - self.overhead()
+        return us
 
-    def empty_pair_us(self, n=200):
+    def empty_pair_us(self, n=100):
         """What an event pair adds to the time of the launch it brackets: the
-        mean bracketed time of a one-element fill kernel, less that kernel's
+        mean bracketed time of a 16 MiB fill kernel, less that kernel's
         per-launch time in a chain of n launches (which, like a rocprofv3
-        kernel duration, includes its dispatch and drain).  Both are queued
-        behind `busy` on the current stream, so neither holds host time."""
+        kernel duration, includes its dispatch and drain; a kernel this size
+        leaves the chain no launch latency to hide).  Both are queued behind
+        `busy` on the current stream, so neither holds host time."""
         import torch
         stream = torch.cuda.current_stream().cuda_stream
-        x = torch.zeros(1, device="cuda")
+        x = torch.zeros(1 << 22, device="cuda")
         for _ in range(20):
             x.fill_(1.0)
         ev = self.hip.create(2 * n + 2)
@@ -336,16 +337,18 @@ def timed_runs(run, lo, K, R):
 
 def worker_server_times(prof, grad_one, update_one, n=50):
     """The paper's T (one worker gradient: the minibatch read from the replay
-    and the TD gradient) and tau (one server update: the apply kernel), on
-    the GPU clock (Sec. IV.D.1)."""
+    and the TD gradient) and tau (one server update: the apply kernel) on the
+    GPU clock (Sec. IV.D.1): the time per call of n back-to-back calls, so
+    1/tau is the update rate the server sustains and T the time a worker
+    takes per gradient."""
     grad_one(0)
     update_one(0)
-    T = prof.spans_us(grad_one, n)
-    tau = prof.spans_us(update_one, n)
+    T = prof.chain_us(grad_one, n)
+    tau = prof.chain_us(update_one, n)
     return {"T_us": round(T, 2), "tau_us": round(tau, 2), "T_over_tau": round(T / tau, 2),
             "server_bound_updates_per_s": round(1e6 / tau, 1),
-            "method": "median over 50 calls of the GPU time between event pairs on the stream, queued "
-                      "behind a matrix-core loop so that no host time is in them, less the pair overhead"}
+            "method": f"GPU time per call over {n} back-to-back calls on one stream, between events queued "
+                      f"behind a matrix-core loop so that no host time is in them"}
 
 
 def single_thread_baseline(grad_fn, update_fn, B, b, budget_s=3.0):
@@ -397,16 +400,24 @@ def measured_traffic(config, name):
     return None
 
 
+# Large-network float32 kernels that run their contraction on bf16 MFMA with
+# exact three-term bf16 splits of float32 operands: the number of bf16
+# products per float32 product (both operands split: 6 of the 9 pairs; one
+# operand exact in bf16, the input bytes: 3).  Their matrix ceiling is the
+# bf16 dense peak divided by that count.
+SPLIT_PRODUCTS = {"conv1_fwd": 3, "conv1_wgrad": 3, "conv2_fwd": 6, "conv3_fwd": 6}
+
+
 def roofline(work, name, avg_us, launches, per_step_launches, raw_us=None, config=None,
-             peak_flops=PEAK_FP32_MFMA):
+             peak_flops=PEAK_FP32_MFMA, products=1):
     flop, byts = work[name]           # per step: per launch when a step launches the kernel several times
     if per_step_launches > 1:
         flop, byts = flop // per_step_launches, byts // per_step_launches
     if flop > 0:
-        achieved, peak, unit, bound = flop / (avg_us * 1e-6) / 1e12, peak_flops / 1e12, "TFLOP/s", "mfma"
+        achieved, peak, unit, bound = flop / (avg_us * 1e-6) / 1e12, peak_flops / 1e12 / products, "TFLOP/s", "mfma"
     else:
         achieved, peak, unit, bound = byts / (avg_us * 1e-6) / 1e9, PEAK_HBM / 1e9, "GB/s", "hbm"
-    out = {"kernel": name, "bound": bound, "achieved": round(achieved, 4), "peak": peak,
+    out = {"kernel": name, "bound": bound, "achieved": round(achieved, 4), "peak": round(peak, 4),
            "unit": unit, "frac": round(achieved / peak, 6),
            "traffic": measured_traffic(config, name) if config is not None else None,
            "per_launch": {"flop": flop, "bytes": byts, "avg_us": round(avg_us, 3),
@@ -414,6 +425,10 @@ def roofline(work, name, avg_us, launches, per_step_launches, raw_us=None, confi
     if raw_us is not None:
         out["per_launch"]["event_pair_us"] = round(raw_us, 3)
         out["per_launch"]["event_overhead_us"] = round(raw_us - avg_us, 3)
+    if products > 1:
+        out["peak_basis"] = (f"float32 contraction on bf16 MFMA, {products} bf16 products per float32 product "
+                             f"(exact three-term splits): bf16 dense {PEAK_BF16_MFMA / 1e12:.0f} TFLOP/s / {products}")
+        out["frac_of_fp32_matrix_peak"] = round(achieved / (PEAK_FP32_MFMA / 1e12), 6)
     return out
 
 
@@ -1189,7 +1204,8 @@ def bench_large(args):
     out["final_loss"] = final_loss
     out["roofline"] = roofline(work, dom, dom_us, used, lps, raw_us,
                                args.config + (" bf16" if bf16 else ""),
-                               PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
+                               PEAK_BF16_MFMA if bf16 else PEAK_BF16_MFMA if dom in SPLIT_PRODUCTS else PEAK_FP32_MFMA,
+                               1 if bf16 else SPLIT_PRODUCTS.get(dom, 1))
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
                         "per_layer_tflops": {k: round(work[k][0] / (v[0] * (v[1] / nb) * 1e-6) / 1e12, 3)
                                              for k, v in bd.items() if work[k][0] > 0}, **Tt}
@@ -1276,7 +1292,8 @@ def bench_forward(args):
     out["states_per_s"] = round(out["value"] * B, 1)
     out["step_tflops"] = round(step_flop(shape, B, forward_only=True) * out["value"] / 1e12, 4)
     out["roofline"] = roofline(work, dom, dom_us, used, lps, raw_us, "4a" + (" bf16" if bf16 else ""),
-                               PEAK_BF16_MFMA if bf16 else PEAK_FP32_MFMA)
+                               PEAK_BF16_MFMA if bf16 else PEAK_BF16_MFMA if dom in SPLIT_PRODUCTS else PEAK_FP32_MFMA,
+                               1 if bf16 else SPLIT_PRODUCTS.get(dom, 1))
     out["breakdown"] = {"us_per_launch": {k: round(v[0], 2) for k, v in bd.items()},
                         "per_layer_tflops": {k: round(work[k][0] / (v[0] * (v[1] / nb) * 1e-6) / 1e12, 3)
                                              for k, v in bd.items() if work[k][0] > 0}}

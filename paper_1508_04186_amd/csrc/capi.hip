@@ -152,8 +152,8 @@ struct TdLayout {
     int chunks[3];
     int ks, kchunk;
     float* spart;   // sample-sum chunk slots of the finalize (above 128 samples)
-    float *wpk2, *wpk3;   // repacked conv2/conv3 weights of the fp32 input gradients (large network)
-    float *fpk[2][2];     // ... of the fp32 forward: [layer conv2, conv3][set theta, theta^-]
+    float *wpk2, *wpk3;   // repacked conv2/conv3 weights of the input gradients (large network)
+    float *fpk[2][2];     // ... the fp32 forward's bf16 planes: [layer conv2, conv3][set theta, theta^-]
     size_t bytes;
 };
 
@@ -192,8 +192,8 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
         t.wpk2 = cv.take<float>(ws, weight_repack_floats(CONV_L2));
         t.wpk3 = cv.take<float>(ws, weight_repack_floats(CONV_L3));
         for (int w = 0; w < 2; ++w) {
-            t.fpk[0][w] = cv.take<float>(ws, kFwdPack2);
-            t.fpk[1][w] = cv.take<float>(ws, kFwdPack3);
+            t.fpk[0][w] = cv.take<float>(ws, fwd_x6_pack_floats(CONV_L2));
+            t.fpk[1][w] = cv.take<float>(ws, fwd_x6_pack_floats(CONV_L3));
         }
     }
     t.bytes = cv.off;
@@ -278,6 +278,18 @@ namespace {
         prof_end((kid), st);                            \
     } while (0)
 
+// The per-lane weight copies of a large-network TD step: the input
+// gradients' (r, when set) and the fp32 forward's planes (fwd).
+hipError_t repack_weights(const WeightRepack* r, bool fwd, const float* w2a, const float* w3a, const float* w2b,
+                          const float* w3b, float* const fpk[2][2], hipStream_t st) {
+    if (r) {
+        const hipError_t e = launch_weight_repack(*r, st);
+        if (e != hipSuccess) return e;
+    }
+    if (fwd) return launch_fwd_x6_pack(w2a, w3a, w2b, w3b, fpk[0][0], fpk[1][0], fpk[0][1], fpk[1][1], st);
+    return hipSuccess;
+}
+
 // Where a TD step's transitions come from: dense device buffers, or replay
 // records and side arrays addressed by an index array.
 struct TdSource {
@@ -339,22 +351,16 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     const bool a16 = ni.bf16 && L == 3 && B >= kRegWgradMinRows && 2 * B >= kFwdClMinRows;
 
     // The large network's conv2 and conv3 kernels that hold their weights in
-    // registers -- the fp32 forward (both weight sets) and the input gradients
-    // of both precisions -- load them from copies in per-lane order, written
-    // by one launch, instead of gathering 64 to 144 scattered words per lane
-    // (the gather dominated a workgroup's first sample: batch 256, conv2's
-    // fp32 input gradient 33 -> 21 us, bf16 23 -> 9 us).
+    // registers load them from copies in per-lane order, written at the start
+    // of the step: the fp32 forward's three bf16 planes of both weight sets,
+    // and the input gradients' weights of both precisions (instead of
+    // gathering 64 to 144 scattered words per lane; the gather dominated a
+    // workgroup's first sample: batch 256, conv2's fp32 input gradient 33 ->
+    // 21 us, bf16 23 -> 9 us).
     const bool repack_fwd = !ni.bf16 && L == 3 && conv_fwd_cl_use(CONV_L2, 2 * B, false);
     const bool repack = L == 3 && phase_dgrad(CONV_L2, B, ni.bf16);
     if (repack_fwd || repack) {
-        WeightRepack r{th + ni.w_off[1], th + ni.w_off[2], tt + ni.w_off[1], tt + ni.w_off[2],
-                       nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
-        if (repack_fwd) {
-            r.f2a = t.fpk[0][0];
-            r.f3a = t.fpk[1][0];
-            r.f2b = t.fpk[0][1];
-            r.f3b = t.fpk[1][1];
-        }
+        WeightRepack r{th + ni.w_off[1], th + ni.w_off[2], nullptr, nullptr, nullptr, nullptr};
         if (repack && ni.bf16) {
             r.h2 = t.wpk2;
             r.h3 = t.wpk3;
@@ -362,7 +368,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             r.d2 = t.wpk2;
             r.d3 = t.wpk3;
         }
-        RUN(DQN_K_WEIGHT_REPACK, launch_weight_repack(r, st));
+        RUN(DQN_K_WEIGHT_REPACK, repack_weights(repack ? &r : nullptr, repack_fwd, th + ni.w_off[1],
+                                                th + ni.w_off[2], tt + ni.w_off[1], tt + ni.w_off[2], t.fpk, st));
     }
 
     // Forward of s under theta (samples 0..B-1) and of s' under theta^-

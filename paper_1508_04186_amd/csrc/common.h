@@ -28,6 +28,17 @@ __device__ __forceinline__ f4 mfma16x16x32bf16(bf16x8 a, bf16x8 b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// Exact split of a float32 value into three bfloat16 terms, w = hi + mid +
+// lo: each remainder is exactly representable in float32, and after two
+// terms at most 8 significand bits remain (values below about 2^-110, whose
+// low terms underflow, lose them).
+__device__ __forceinline__ void split3(float w, __bf16& hi, __bf16& mid, __bf16& lo) {
+    hi = (__bf16)w;
+    const float r1 = w - (float)hi;
+    mid = (__bf16)r1;
+    lo = (__bf16)(r1 - (float)mid);
+}
+
 // Operand of the bf16-input contraction step over 32 k-values staged in
 // fp32: element e holds the value at k = 4e + g for lane group g (the
 // contraction is a sum over k, so any assignment of k to (g, e) that both
@@ -233,8 +244,8 @@ hipError_t launch_conv_igemm_fwd(ConvId id, const float* in, int n_a, int n, con
 // it).
 constexpr int kFwdClMinRows = 256;
 bool conv_fwd_cl_use(ConvId id, int n, bool bf16);
-// pk_a, pk_b (fp32 only; both or neither): w_a, w_b repacked by
-// launch_weight_repack.
+// pk_a, pk_b (fp32 only; both or neither): the three bf16 planes of w_a,
+// w_b written by launch_fwd_x6_pack (NULL: the kernel splits W itself).
 hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const float* w_a, const float* b_a,
                               const float* w_b, const float* b_b, float* out, bool bf16, bool in16, bool out16,
                               const float* pk_a, const float* pk_b, hipStream_t st);
@@ -257,19 +268,24 @@ hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float
 // gradient assembled in LDS).  h_in and din 16-byte aligned.
 hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
                               bool h16, const float* wpk, hipStream_t st);
-// conv2's and conv3's weights in the per-lane order of the large network's
-// fp32 kernels, one launch: forward copies of two weight sets (a: theta, b:
-// theta^-; 4 * 128 * 64 and 4 * 144 * 64 floats) and input-gradient copies
-// of set a (weight_repack_floats(CONV_L2 / CONV_L3) floats).  NULL outputs
-// are skipped.
+// conv2's and conv3's weights of set a (theta) in the per-lane order of the
+// large network's input-gradient kernels, one launch
+// (weight_repack_floats(CONV_L2 / CONV_L3) floats each).  NULL outputs are
+// skipped.
 struct WeightRepack {
-    const float *w2a, *w3a, *w2b, *w3b;
-    float *f2a, *f3a, *f2b, *f3b, *d2, *d3;
+    const float *w2a, *w3a;
+    float *d2, *d3;
     void *h2, *h3;   // bf16 input-gradient operands of set a (half the floats of d2, d3)
 };
-constexpr int64_t kFwdPack2 = 4 * 128 * 64, kFwdPack3 = 4 * 144 * 64;
 int64_t weight_repack_floats(ConvId id);
 hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st);
+// The float32 forward's weights of conv2 and conv3 for two weight sets (a:
+// theta, b: theta^-) as the three exact bf16 planes in the per-lane order of
+// the forward kernel (fwd_x6_pack_floats(id) floats each, 16-byte aligned);
+// NULL outputs are skipped.
+int64_t fwd_x6_pack_floats(ConvId id);
+hipError_t launch_fwd_x6_pack(const float* w2a, const float* w3a, const float* w2b, const float* w3b, float* x2a,
+                              float* x3a, float* x2b, float* x3b, hipStream_t st);
 
 // Weight/bias gradient partial sums of CONV_L2 or CONV_L3 for n samples, one
 // workgroup per run of samples holding every output in registers:

@@ -638,34 +638,18 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
     }
 }
 
-// The weights of the large network's fp32 conv2/conv3 kernels in the order
-// their lanes load them into registers, so that every load of a wave is one
-// contiguous 256-byte row instead of a gather of scattered words:
-//  - input gradients (this file): element ((w KS + s) 64 + lane) is wave w's
-//    k-step s, w over the 8 (phase, N-tile) waves of conv2 (KS = 64) and the
-//    4 N-tiles of conv3 (KS = 144); values W[o][c][tap] as the kernels read;
-//  - forward (conv_fwd_cl32_kernel, k_fwdcl.hip): element ((nt KS + s) 64 +
-//    lane) holds W[16nt + li][16b + 4g + i][tap] for k-step s = (tap CB + b)
-//    4 + i, CB = cin / 16 (KS = 128 for conv2, 144 for conv3).
-// Job j of the launch (blockIdx.y) writes one copy; a NULL output skips it.
-__device__ __forceinline__ float fwd_pack_value(const float* __restrict__ w, int cin, int kk, int e) {
-    const int ks = kk * (cin / 16) * 4, cb = cin / 16;
-    const int lane = e & 63, s = (e >> 6) % ks, nt = (e >> 6) / ks;
-    const int li = lane & 15, g = lane >> 4;
-    const int tap = s / (cb * 4), b = (s / 4) % cb, i = s % 4;
-    return w[(size_t)(16 * nt + li) * cin * kk + (size_t)(16 * b + 4 * g + i) * kk + tap];
-}
-
+// The weights of the large network's conv2/conv3 input-gradient kernels in
+// the order their lanes load them into registers, so that every load of a
+// wave is one contiguous 256-byte row instead of a gather of scattered
+// words: element ((w KS + s) 64 + lane) is wave w's k-step s, w over the 8
+// (phase, N-tile) waves of conv2 (KS = 64) and the 4 N-tiles of conv3
+// (KS = 144); values W[o][c][tap] as the kernels read (bf16 copies: one
+// 8-value vector per element).  Job j of the launch (blockIdx.y) writes one
+// copy; a NULL output skips it.
 __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
     const int e = blockIdx.x * 256 + threadIdx.x;
     const int job = blockIdx.y;
-    if (job < 4) {   // forward copies: conv2 a, conv3 a, conv2 b, conv3 b
-        const bool l3 = job & 1;
-        const float* w = job == 0 ? r.w2a : job == 1 ? r.w3a : job == 2 ? r.w2b : r.w3b;
-        float* out = job == 0 ? r.f2a : job == 1 ? r.f3a : job == 2 ? r.f2b : r.f3b;
-        const int cin = l3 ? 64 : 32, kk = l3 ? 9 : 16;
-        if (out && e < 4 * kk * (cin / 16) * 4 * 64) out[e] = fwd_pack_value(w, cin, kk, e);
-    } else if (job == 4) {   // conv2 input gradient
+    if (job == 0) {   // conv2 input gradient
         constexpr int KS2 = D2_KT / 4;
         if (r.d2 && e < 8 * KS2 * 64) {
             const int lane = e & 63, s = (e >> 6) % KS2, wave = (e >> 6) / KS2;
@@ -675,7 +659,7 @@ __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
             r.d2[e] = r.w2a[(size_t)o * D2_CIN * D2_K * D2_K + (size_t)c * D2_K * D2_K + (py + 2 * ty) * D2_K + px +
                             2 * tx];
         }
-    } else if (job == 6) {   // conv2 input gradient, bf16 operands: one 8-value vector per thread
+    } else if (job == 2) {   // conv2 input gradient, bf16 operands: one 8-value vector per thread
         constexpr int KS2 = D2_KT / 32;
         if (r.h2 && e < 8 * KS2 * 64) {
             const int lane = e & 63, s = (e >> 6) % KS2, wave = (e >> 6) / KS2;
@@ -691,7 +675,7 @@ __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
             }
             ((bf16x8*)r.h2)[e] = v;
         }
-    } else if (job == 7) {   // conv3 input gradient, bf16 operands
+    } else if (job == 3) {   // conv3 input gradient, bf16 operands
         constexpr int KS3 = D3_KT / 32;
         if (r.h3 && e < 4 * KS3 * 64) {
             const int lane = e & 63, s = (e >> 6) % KS3, nt = (e >> 6) / KS3;
@@ -705,7 +689,7 @@ __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
             }
             ((bf16x8*)r.h3)[e] = v;
         }
-    } else {   // conv3 input gradient
+    } else {   // job 1: conv3 input gradient
         constexpr int KS3 = D3_KT / 4;
         if (r.d3 && e < 4 * KS3 * 64) {
             const int lane = e & 63, s = (e >> 6) % KS3, nt = (e >> 6) / KS3;
@@ -722,7 +706,7 @@ int64_t weight_repack_floats(ConvId id) { return id == CONV_L2 ? 8 * (D2_KT / 4)
 
 hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st) {
     // every copy has at most 4 * 144 * 64 = 36,864 elements
-    hipLaunchKernelGGL(weight_repack_kernel, dim3(36864 / 256, 8), dim3(256), 0, st, r);
+    hipLaunchKernelGGL(weight_repack_kernel, dim3(36864 / 256, 4), dim3(256), 0, st, r);
     return hipGetLastError();
 }
 

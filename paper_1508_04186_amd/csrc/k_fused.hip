@@ -55,16 +55,6 @@ constexpr int LDS_BYTES = OFF_B + (C1 + C2) * 4;
 static_assert(OFF_W1 % 16 == 0 && OFF_A1 % 16 == 0 && OFF_W2 % 16 == 0 && OFF_B % 16 == 0, "alignment");
 
 
-// Exact split of an fp32 value into three bf16 terms, w = hi + mid + lo: each
-// remainder is exactly representable in fp32, and after two terms at most 8
-// significand bits remain.
-__device__ __forceinline__ void split3(float w, __bf16& hi, __bf16& mid, __bf16& lo) {
-    hi = (__bf16)w;
-    const float r1 = w - (float)hi;
-    mid = (__bf16)r1;
-    lo = (__bf16)(r1 - (float)mid);
-}
-
 struct FusedFwdParams {
     ConvIn in_a, in_b;
     int n_a, n;
@@ -861,15 +851,38 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
 }  // namespace dqn
 
 // ---------------------------------------------------------------------------
-// conv1 weight/bias gradient on byte input for many samples: a workgroup owns
-// all COUT x 256 outputs for a run of samples (one partial-sum slot).  Per
-// sample it stages the input bytes and dz, then each wave contracts the 400
-// pixels for 2 M-tiles (output channels) x NTW N-tiles (weight columns),
-// every accumulator chain independent; lane group g takes pixel 4*st + g.
-// The bf16-input variant rounds dz to bfloat16 (the bytes are exact) and
-// contracts 32 pixels per step, pixel 32*st + 4*e + g in element e.
+// conv1 weight/bias gradient on byte input for many samples:
+//   dW[o][c][ky][kx] = (1/255) sum over samples and pixels (y, x) of
+//                      dz[o][y][x] * byte[c][4y + ky][4x + kx],  db[o] = sum dz.
+// One workgroup of eight waves per compute unit owns all COUT x 256 outputs
+// for a run of samples (one partial-sum slot).  The contraction over pixels
+// runs on v_mfma_f32_16x16x32_bf16: the bytes are exact in bfloat16, and dz
+// is split exactly into three bfloat16 planes (hi + mid + lo; PARTS = 3), so
+// the three products per step are those of the float32 dz; the bf16-input
+// variant rounds dz to one plane (PARTS = 1).  Per sample, dz is staged as
+// the planes [part][o][pixel] and the bytes as phases
+// [c][row][kx][i] = byte[c][row][4i + kx] (i < 20), so that four pixels
+// (y, x..x+3) of one row are 8 contiguous bytes of a plane and one 4-byte
+// word of a phase row.  Lane group g of k-step st takes pixels 32 st + 8 g + e
+// (e < 8), two groups of four within rows; pixels 400..415 of the last step
+// are zero in the planes.  Wave w owns N-tiles (weight columns) 2w, 2w+1 and
+// every M-tile (output channel block); the next sample's dz and bytes are
+// read into registers during the current sample's MFMAs.
 namespace dqn {
 namespace {
+
+constexpr int UW_WG = 512;                      // eight waves
+constexpr int UW_TARGET_BLOCKS = 256;           // one workgroup per compute unit
+constexpr int UW_P = H1 * H1;                   // 400 pixels
+constexpr int UW_LDZ = 424;                     // bf16 plane row stride (848 B: 16-byte reads conflict-free)
+constexpr int UW_STEPS = (UW_P + 31) / 32;      // 13 k-steps of 32 pixels
+constexpr int UW_PHROW = 8 * H1;                // phase bytes per (channel, row): 8 kx x 20
+constexpr int UW_PH = C0 * H0 * UW_PHROW;       // 53,760 bytes
+constexpr int UW_ITEMS = C0 * H0 * 5;           // (channel, row, 16-byte column block) items
+constexpr int UW_IPER = (UW_ITEMS + UW_WG - 1) / UW_WG;
+static_assert(32 * UW_STEPS <= UW_LDZ && UW_P % 4 == 0 && H1 % 4 == 0, "pixel groups of four within rows");
+
+constexpr size_t uw_lds(int cout, int parts) { return (size_t)parts * cout * UW_LDZ * 2 + UW_PH; }
 
 struct U8WgradParams {
     ConvIn in;            // network input (bytes)
@@ -880,153 +893,189 @@ struct U8WgradParams {
     float in_scale;
 };
 
-template <int COUT, bool BF16>
-__global__ __launch_bounds__(WG) void conv1_u8_wgrad_kernel(U8WgradParams p) {
-    constexpr int REC = C0 * H0 * H0;
-    constexpr int RV = REC / 16, RPER = (RV + WG - 1) / WG;
-    constexpr int P1 = H1 * H1;                        // 400 pixels
-    constexpr int DV = COUT * P1 / 4, DPER = (DV + WG - 1) / WG;
+template <int COUT, int PARTS>
+__global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) {
     constexpr int MT = COUT / 16;
-    constexpr int NTW = KW1 / 16 / 4;                  // N-tiles per wave (4)
-    constexpr int LDZ = P1 + 4;                        // dz row stride (= 20 mod 64: conflict-free)
+    constexpr int RPW = COUT / 8;                      // dz rows staged per wave
+    constexpr int CPR = UW_P / 4;                      // f4 chunks per dz row (100)
+    static_assert(PARTS == 1 || PARTS == 3, "exact split or bf16 rounding");
+    static_assert(KW1 == 16 * 16 && COUT % 16 == 0, "16 N-tiles of weight columns, 2 per wave");
     extern __shared__ __align__(16) unsigned char smem[];
-    unsigned char* s_in = smem;                        // u8 [REC]
-    float* s_dz = (float*)(smem + REC);                // f32 [COUT][LDZ]
-    static_assert(REC % 16 == 0, "alignment");
+    __bf16* s_dz = (__bf16*)smem;                                   // [PARTS][COUT][UW_LDZ]
+    unsigned char* s_ph = smem + (size_t)PARTS * COUT * UW_LDZ * 2;  // [C0][H0][8][20]
 
     const int j0 = blockIdx.x * p.spb, j1 = min(p.n, j0 + p.spb);
-    const int t = threadIdx.x;
-    const int lane = t & 63, wave = t >> 6;
+    if (j0 >= j1) return;  // whole workgroup
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
-    int koff[NTW];
-#pragma unroll
-    for (int i = 0; i < NTW; ++i) {
-        const int col = (wave * NTW + i) * 16 + li;
-        const int c = col / (K1 * K1), ky = (col / K1) % K1, kx = col % K1;
-        koff[i] = (c * H0 + ky) * H0 + kx;
+
+    // pixels 400 .. UW_LDZ-1 of every plane row stay zero
+    for (int e = t; e < PARTS * COUT * (UW_LDZ - UW_P); e += UW_WG) {
+        const int row = e / (UW_LDZ - UW_P), q = e - row * (UW_LDZ - UW_P);
+        s_dz[row * UW_LDZ + UW_P + q] = (__bf16)0.f;
     }
-    f4 acc[MT][NTW];
+
+    // next sample in registers: dz rows wave*RPW .. +RPW-1 (chunks lane, lane + 64),
+    // and the 20-byte column blocks of the phase items
+    f4 vdz[RPW][2];
+    uint32_t vb[UW_IPER][5];
+    auto load = [&](int j) {
+        const float* dzj = p.dz + (size_t)j * COUT * UW_P;
+#pragma unroll
+        for (int q = 0; q < RPW; ++q)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int ch = lane + 64 * h;
+                if (ch < CPR) vdz[q][h] = *(const f4*)(dzj + (wave * RPW + q) * UW_P + 4 * ch);
+            }
+        const unsigned char* src = sample_ptr(p.in, j);
+#pragma unroll
+        for (int u = 0; u < UW_IPER; ++u) {
+            const int it = t + u * UW_WG;
+            if (it < UW_ITEMS) {
+                const int row = it / 5, qb = it - row * 5;   // row = c * H0 + r
+                const uint32_t* w = (const uint32_t*)(src + row * H0 + 16 * qb);
+#pragma unroll
+                for (int d = 0; d < 5; ++d) vb[u][d] = w[d];
+            }
+        }
+    };
+    float bs[RPW];
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) bs[q] = 0.f;
+    auto stage = [&]() {
+#pragma unroll
+        for (int q = 0; q < RPW; ++q) {
+            const int o = wave * RPW + q;
+            float part = 0.f;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int ch = lane + 64 * h;
+                if (ch < CPR) {
+                    const f4 v = vdz[q][h];
+                    part += (v[0] + v[1]) + (v[2] + v[3]);
+                    bf16x4 hv, mv, lv;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        __bf16 hi, mid, lo;
+                        split3(v[i], hi, mid, lo);
+                        hv[i] = hi;
+                        mv[i] = mid;
+                        lv[i] = lo;
+                    }
+                    *(bf16x4*)(s_dz + (0 * COUT + o) * UW_LDZ + 4 * ch) = hv;
+                    if constexpr (PARTS == 3) {
+                        *(bf16x4*)(s_dz + (1 * COUT + o) * UW_LDZ + 4 * ch) = mv;
+                        *(bf16x4*)(s_dz + (2 * COUT + o) * UW_LDZ + 4 * ch) = lv;
+                    }
+                }
+            }
+            bs[q] += wave_sum(part);
+        }
+        // phase word (row, kx, block qb) = bytes 16 qb + 4e + kx, e < 4, of the row
+#pragma unroll
+        for (int u = 0; u < UW_IPER; ++u) {
+            const int it = t + u * UW_WG;
+            if (it < UW_ITEMS) {
+                const int row = it / 5, qb = it - row * 5;
+#pragma unroll
+                for (int kx = 0; kx < 8; ++kx) {
+                    const int m = kx & 3, d = kx >> 2;
+                    const uint32_t sel = (uint32_t)m | ((uint32_t)(4 + m) << 8) | 0x0c0c0000u;
+                    const uint32_t lo2 = __builtin_amdgcn_perm(vb[u][d + 1], vb[u][d], sel);
+                    const uint32_t hi2 = __builtin_amdgcn_perm(vb[u][d + 3], vb[u][d + 2], sel);
+                    *(uint32_t*)(s_ph + (row * 8 + kx) * H1 + 4 * qb) = __builtin_amdgcn_perm(hi2, lo2, 0x05040100u);
+                }
+            }
+        }
+    };
+
+    // weight column (c, ky, kx) of this lane in each of its two N-tiles
+    int cb[2];
+#pragma unroll
+    for (int n = 0; n < 2; ++n) {
+        const int col = (2 * wave + n) * 16 + li;
+        const int c = col / (K1 * K1), ky = (col / K1) % K1, kx = col % K1;
+        cb[n] = ((c * H0 + ky) * 8 + kx) * H1;
+    }
+    f4 acc[MT][2];
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
-        for (int i = 0; i < NTW; ++i) acc[m][i] = f4{0.f, 0.f, 0.f, 0.f};
-    float bsum = 0.f;
+        for (int n = 0; n < 2; ++n) acc[m][n] = f4{0.f, 0.f, 0.f, 0.f};
 
+    load(j0);
     for (int j = j0; j < j1; ++j) {
-        f4 vin[RPER], vdz[DPER];
-        const f4* src = (const f4*)sample_ptr(p.in, j);
-        const f4* dzj = (const f4*)(p.dz + (size_t)j * COUT * P1);
-#pragma unroll
-        for (int u = 0; u < RPER; ++u) {
-            const int e = t + u * WG;
-            if (e < RV) vin[u] = src[e];
-        }
-#pragma unroll
-        for (int u = 0; u < DPER; ++u) {
-            const int e = t + u * WG;
-            if (e < DV) vdz[u] = dzj[e];
-        }
         __syncthreads();  // the previous sample's reads are done
-#pragma unroll
-        for (int u = 0; u < RPER; ++u) {
-            const int e = t + u * WG;
-            if (e < RV) *(f4*)(s_in + 16 * e) = vin[u];
-        }
-#pragma unroll
-        for (int u = 0; u < DPER; ++u) {
-            const int e = t + u * WG;
-            if (e < DV) {
-                const int o = (4 * e) / P1, q = (4 * e) % P1;
-                *(f4*)(s_dz + o * LDZ + q) = vdz[u];
-            }
-        }
+        stage();
         __syncthreads();
-        if (t < COUT) {
-            const float* row = s_dz + t * LDZ;
-            float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-            for (int q = 0; q < P1; q += 4) {
-                s0 += row[q];
-                s1 += row[q + 1];
-                s2 += row[q + 2];
-                s3 += row[q + 3];
+        if (j + 1 < j1) load(j + 1);
+        for (int st = 0; st < UW_STEPS; ++st) {
+            const int p0 = 32 * st + 8 * g;
+            // phase offsets of the two pixel groups (pixels past 400 read row 0: their dz is zero)
+            int po[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int pp = p0 + 4 * h;
+                const int y = pp < UW_P ? pp / H1 : 0, x = pp < UW_P ? pp - (pp / H1) * H1 : 0;
+                po[h] = S1 * y * 8 * H1 + x;
             }
-            bsum += (s0 + s1) + (s2 + s3);
-        }
-        if constexpr (BF16) {
-            // pixel q = 32*st + 4*e + g; the 4 lane groups stay in one row
-            // (20 is a multiple of 4); the last step covers pixels 384..399
-            constexpr int STEPS = (P1 + 31) / 32;
-            for (int st = 0; st < STEPS; ++st) {
-                bf16x8 a[MT], b[NTW];
+            bf16x8 b[2];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const bool v = 32 * st + 4 * e < P1;     // uniform across the wave
-                    const int q0 = v ? 32 * st + 4 * e : 0;    // no address past the tile
-                    const int y = q0 / H1, x = q0 % H1 + g;
-                    const int po = S1 * y * H0 + S1 * x;
+            for (int n = 0; n < 2; ++n) {
 #pragma unroll
-                    for (int m = 0; m < MT; ++m)
-                        a[m][e] = v ? (__bf16)s_dz[(m * 16 + li) * LDZ + q0 + g] : (__bf16)0.f;
+                for (int h = 0; h < 2; ++h) {
+                    const uint32_t w = *(const uint32_t*)(s_ph + cb[n] + po[h]);
 #pragma unroll
-                    for (int i = 0; i < NTW; ++i) b[i][e] = v ? (__bf16)(float)s_in[koff[i] + po] : (__bf16)0.f;
+                    for (int e = 0; e < 4; ++e) b[n][4 * h + e] = (__bf16)(float)((w >> (8 * e)) & 0xffu);
                 }
-#pragma unroll
-                for (int m = 0; m < MT; ++m)
-#pragma unroll
-                    for (int i = 0; i < NTW; ++i) acc[m][i] = mfma16x16x32bf16(a[m], b[i], acc[m][i]);
             }
-        } else {
-            // pixel q = 4*st + g: row q/20, column q%20 (a step stays in one row)
-#pragma unroll 2
-            for (int st = 0; st < P1 / 4; ++st) {
-                const int q = 4 * st + g;
-                const int y = (4 * st) / H1, x = (4 * st) % H1 + g;
-                const int po = S1 * y * H0 + S1 * x;
-                float a[MT], b[NTW];
 #pragma unroll
-                for (int m = 0; m < MT; ++m) a[m] = s_dz[(m * 16 + li) * LDZ + q];
+            for (int m = 0; m < MT; ++m)
 #pragma unroll
-                for (int i = 0; i < NTW; ++i) b[i] = (float)s_in[koff[i] + po];
+                for (int part = 0; part < PARTS; ++part) {
+                    const bf16x8 a = *(const bf16x8*)(s_dz + (part * COUT + m * 16 + li) * UW_LDZ + p0);
 #pragma unroll
-                for (int m = 0; m < MT; ++m)
-#pragma unroll
-                    for (int i = 0; i < NTW; ++i) acc[m][i] = mfma16x16x4(a[m], b[i], acc[m][i]);
-            }
+                    for (int n = 0; n < 2; ++n) acc[m][n] = mfma16x16x32bf16(a, b[n], acc[m][n]);
+                }
         }
     }
-    // D[4g + r][li] of tile (m, i): channel m*16 + 4g + r, column (wave*NTW + i)*16 + li
+    // D[4g + r][li] of tile (m, n): channel m*16 + 4g + r, column (2 wave + n)*16 + li
     float* wp = p.wpart + (size_t)blockIdx.x * COUT * KW1;
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
-        for (int i = 0; i < NTW; ++i)
+        for (int n = 0; n < 2; ++n)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-                wp[(size_t)(m * 16 + 4 * g + r) * KW1 + (wave * NTW + i) * 16 + li] = acc[m][i][r] * p.in_scale;
-    if (t < COUT) p.bpart[(size_t)blockIdx.x * COUT + t] = bsum;
+                wp[(size_t)(m * 16 + 4 * g + r) * KW1 + (2 * wave + n) * 16 + li] = acc[m][n][r] * p.in_scale;
+    if (lane == 0) {
+#pragma unroll
+        for (int q = 0; q < RPW; ++q) p.bpart[(size_t)blockIdx.x * COUT + wave * RPW + q] = bs[q];
+    }
 }
 
 }  // namespace
 
 int conv1_u8_wgrad_slots(int n) {
-    const int spb = std::max(1, (n + 511) / 512);
+    const int spb = std::max(1, (n + UW_TARGET_BLOCKS - 1) / UW_TARGET_BLOCKS);
     return (n + spb - 1) / spb;
 }
 
 hipError_t launch_conv1_u8_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
                                  float* bpart, float in_scale, bool bf16, hipStream_t st) {
     if (n <= 0 || !conv_s12_fwd_aligned(in) || in.off != 0 || ((uintptr_t)dz & 15)) return hipErrorInvalidValue;
-    const int spb = std::max(1, (n + 511) / 512);
+    const int spb = std::max(1, (n + UW_TARGET_BLOCKS - 1) / UW_TARGET_BLOCKS);
     const int blocks = (n + spb - 1) / spb;
     const U8WgradParams prm{in, dz, n, spb, wpart, bpart, in_scale};
-    auto go = [&](auto kern, int cout) -> hipError_t {
-        const size_t lds = (size_t)C0 * H0 * H0 + (size_t)cout * (H1 * H1 + 4) * 4;
+    auto go = [&](auto kern, int cout, int parts) -> hipError_t {
+        const size_t lds = uw_lds(cout, parts);
         if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(WG), lds, st, prm);
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(UW_WG), lds, st, prm);
         return hipGetLastError();
     };
-    if (id == CONV_L1) return bf16 ? go(conv1_u8_wgrad_kernel<32, true>, 32) : go(conv1_u8_wgrad_kernel<32, false>, 32);
-    if (id == CONV_S1) return bf16 ? go(conv1_u8_wgrad_kernel<16, true>, 16) : go(conv1_u8_wgrad_kernel<16, false>, 16);
+    if (id == CONV_L1) return bf16 ? go(conv1_u8_wgrad_kernel<32, 1>, 32, 1) : go(conv1_u8_wgrad_kernel<32, 3>, 32, 3);
+    if (id == CONV_S1) return bf16 ? go(conv1_u8_wgrad_kernel<16, 1>, 16, 1) : go(conv1_u8_wgrad_kernel<16, 3>, 16, 3);
     return hipErrorInvalidValue;
 }
 

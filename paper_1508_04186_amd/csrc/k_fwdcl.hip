@@ -16,6 +16,8 @@
 // LDS: coalesced loads, converted to bf16 and stored in the order the lanes
 // read them.
 #include <algorithm>
+#include <initializer_list>
+#include <type_traits>
 
 #include "common.h"
 
@@ -324,41 +326,63 @@ hipError_t fwd_cl_launch(const float* in, int n_a, int n, const float* w_a, cons
     return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, false, false>);
 }
 
-// The fp32 variant: v_mfma_f32_16x16x4_f32, weights held in registers as
-// fp32 (wave (nt, mh): 16 output channels, KT/4 registers), each sample's
-// input staged in LDS as fp32, channels-last (pixel stride CIN + 4 floats).
-// Per tap the channels go in blocks of 16, four k-steps per block: at k-step
-// i of block b lane group g supplies channel 16b + 4g + i, so one 16-byte
-// LDS read gives a lane its A values for four consecutive k-steps.  Weights
-// are read straight from global memory into registers (each lane's channels
-// are runs of k*k consecutive taps).
+// The float32 variant on bf16 MFMA: every float32 operand is split exactly
+// into three bfloat16 terms, x = hi + mid + lo (8 significand bits each), and
+// a k-step multiplies the six pairs whose product is at least 2^-16 of
+// hi*hi: hi*hi, hi*mid, mid*hi, hi*lo, mid*mid, lo*hi.  The products of 8-bit
+// significands are exact and accumulate in float32; the two dropped pairs
+// are below 2^-23 of the product, the size of a float32 rounding, so the
+// sums keep float32 accuracy at six v_mfma_f32_16x16x32_bf16 per 32 k-values
+// (2.7x the matrix rate of eight v_mfma_f32_16x16x4_f32).
+//
+// Eight waves per workgroup, one workgroup per compute unit: wave (nt, kh)
+// owns output channels 16nt .. 16nt+15 and half kh of the k-steps (k order
+// (tap, 32 channels), as the bf16 variant), holding those weights' three
+// planes in registers (96 or 108), for every M-tile of the sample.  Each
+// sample's input is split into three bf16 planes staged channels-last in LDS
+// (one 16-byte read per operand and plane); the two halves' sums meet in LDS
+// at the end of the sample, where bias and ReLU are applied and the output
+// map is assembled and written as 16-byte vectors.  The next sample's input
+// is read into registers during the MFMAs.
 template <int CIN, int IH, int K, int S, int OH>
-struct FwdCl32Geom {
+struct FwdX6Geom {
     static constexpr int COUT = 64;
     static constexpr int P = OH * OH;
-    static constexpr int MT = (P + 15) / 16;
-    static constexpr int MPW = MT / 2;
+    static constexpr int MT = (P + 15) / 16;            // M-tiles per sample (all in every wave)
     static constexpr int KK = K * K;
-    static constexpr int CB = CIN / 16;                 // channel blocks per tap
-    static constexpr int KS = KK * CB * 4;              // fp32 k-steps
+    static constexpr int CH = CIN / 32;                 // k-steps per tap
+    static constexpr int KS = KK * CH;                  // k-steps
+    static constexpr int KSH = KS / 2;                  // per half
     static constexpr int IP = IH * IH;
-    static constexpr int PSF = CIN + 4;                 // LDS floats per staged pixel
+    static constexpr int PSB = CIN * 2 + 16;            // bytes per staged pixel and plane
+    static constexpr int PLANE = IP * PSB;
     static constexpr int IN = CIN * IP;
-    static constexpr int PER = (IN + FC_WG - 1) / FC_WG;
+    static constexpr int ITEMS = (CIN / 8) * IP;        // (8-channel group, pixel) items
+    static constexpr int IPER = (ITEMS + FC_WG - 1) / FC_WG;
     static constexpr int OUTF = COUT * P;
-    static constexpr int LDS = IP * PSF * 4 + OUTF * 4;
-    static_assert(MT % 2 == 0 && CIN % 16 == 0 && (PSF * 4) % 16 == 0 && OUTF % 4 == 0, "geometry");
+    static constexpr int PART = 4 * MT * 64 * 16;       // half-sums of the kh = 1 waves (bytes)
+    static constexpr int LDS = 3 * PLANE;
+    static constexpr int PACK = 3 * 4 * KS * 64;        // bf16x8 vectors of the repacked planes
+    static_assert(KS % 2 == 0 && CIN % 32 == 0 && PSB % 16 == 0 && OUTF % 4 == 0, "geometry");
+    static_assert(PART + OUTF * 4 <= LDS, "half-sums and output map fit in the input planes");
 };
 
-template <int CIN, int IH, int K, int S, int OH, bool PK>   // PK: weights from wpk_a / wpk_b
-__global__ __launch_bounds__(FC_WG) void conv_fwd_cl32_kernel(FwdClParams p) {
-    using G = FwdCl32Geom<CIN, IH, K, S, OH>;
-    extern __shared__ __align__(16) float smem32[];
-    float* s_in = smem32;                                  // [IP][PSF]
-    float* s_out = smem32 + G::IP * G::PSF;                // [64][P]
+template <int CIN, int IH, int K, int S, int OH>
+__device__ __forceinline__ int x6_pack_index(int p, int nt, int kh, int s, int lane) {
+    using G = FwdX6Geom<CIN, IH, K, S, OH>;
+    return (((p * 4 + nt) * 2 + kh) * G::KSH + s) * 64 + lane;
+}
+
+template <int CIN, int IH, int K, int S, int OH, bool PK>   // PK: weight planes from wpk_a / wpk_b
+__global__ __launch_bounds__(FC_WG) void conv_fwd_x6_kernel(FwdClParams p) {
+    using G = FwdX6Geom<CIN, IH, K, S, OH>;
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* s_in = smem;                                     // [3][IP][PSB] bf16 planes
+    f4* s_part = (f4*)smem;                                         // [4][MT][64] (after the MFMAs)
+    float* s_out = (float*)(smem + G::PART);                        // [64][P]     (after the MFMAs)
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
-    const int nt = wave & 3, mh = wave >> 2;
+    const int nt = wave & 3, kh = wave >> 2;
 
     const bool second = (int)blockIdx.x >= p.g_a;
     const int blk = second ? (int)blockIdx.x - p.g_a : (int)blockIdx.x;
@@ -367,94 +391,143 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl32_kernel(FwdClParams p) {
     const int j_lo = first + blk * p.spg;
     const int j_hi = min(end, j_lo + p.spg);
     if (j_lo >= j_hi) return;  // whole workgroup
-    const float* __restrict__ W = second ? p.w_b : p.w_a;
     const float* __restrict__ bias = second ? p.b_b : p.b_a;
 
-    float v[G::PER];
+    // input items (8 channels at one pixel) of the next sample, in registers
+    float v[G::IPER][8];
     auto fetch = [&](int j) {
         const float* x = p.in + (size_t)j * G::IN;
 #pragma unroll
-        for (int u = 0; u < G::PER; ++u) {
-            const int e = t + u * FC_WG;
-            if (e < G::IN) v[u] = x[e];
+        for (int u = 0; u < G::IPER; ++u) {
+            const int q = t + u * FC_WG;
+            if (q < G::ITEMS) {
+                const int cg = q / G::IP, pix = q - cg * G::IP;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[u][e] = x[(8 * cg + e) * G::IP + pix];
+            }
         }
     };
     auto stage = [&]() {
 #pragma unroll
-        for (int u = 0; u < G::PER; ++u) {
-            const int e = t + u * FC_WG;
-            if (e < G::IN) {
-                const int c = e / G::IP, pix = e - c * G::IP;
-                s_in[pix * G::PSF + c] = v[u];
+        for (int u = 0; u < G::IPER; ++u) {
+            const int q = t + u * FC_WG;
+            if (q < G::ITEMS) {
+                const int cg = q / G::IP, pix = q - cg * G::IP;
+                bf16x8 h, m, l;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    __bf16 a, b, c;
+                    split3(v[u][e], a, b, c);
+                    h[e] = a;
+                    m[e] = b;
+                    l[e] = c;
+                }
+                unsigned char* d = s_in + pix * G::PSB + 16 * cg;
+                *(bf16x8*)d = h;
+                *(bf16x8*)(d + G::PLANE) = m;
+                *(bf16x8*)(d + 2 * G::PLANE) = l;
             }
         }
     };
     fetch(j_lo);
 
-    // k-step s = (tap, block b, i): lane (li, g) holds W[16nt + li][16b + 4g + i][tap]
-    float wv[G::KS];
-    if constexpr (PK) {   // wave nt's k-step s for this lane at ((nt KS + s) 64 + lane)
-        const float* wp = second ? p.wpk_b : p.wpk_a;
+    // weights: lane (li, g) of wave (nt, kh) at its k-step s holds, in plane
+    // pl, W[16nt + li][32 cb + 8g + e][tap] split, with ks = kh KSH + s,
+    // tap = ks / CH, cb = ks % CH
+    bf16x8 wv[3][G::KSH];
+    if constexpr (PK) {
+        const bf16x8* wp = (const bf16x8*)(second ? p.wpk_b : p.wpk_a);
 #pragma unroll
-        for (int s = 0; s < G::KS; ++s) wv[s] = wp[((size_t)nt * G::KS + s) * 64 + lane];
+        for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+            for (int s = 0; s < G::KSH; ++s) wv[pl][s] = wp[x6_pack_index<CIN, IH, K, S, OH>(pl, nt, kh, s, lane)];
     } else {
+        const float* __restrict__ W = second ? p.w_b : p.w_a;
         const float* wr = W + (size_t)(16 * nt + li) * CIN * G::KK;
 #pragma unroll
-        for (int tap = 0; tap < G::KK; ++tap)
+        for (int s = 0; s < G::KSH; ++s) {
+            const int ks = kh * G::KSH + s, tap = ks / G::CH, cb = ks % G::CH;
 #pragma unroll
-            for (int b = 0; b < G::CB; ++b)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    wv[(tap * G::CB + b) * 4 + i] = wr[(16 * b + 4 * g + i) * G::KK + tap];
+            for (int e = 0; e < 8; ++e) {
+                __bf16 a, b, c;
+                split3(wr[(32 * cb + 8 * g + e) * G::KK + tap], a, b, c);
+                wv[0][s][e] = a;
+                wv[1][s][e] = b;
+                wv[2][s][e] = c;
+            }
+        }
     }
     const float bo = bias[16 * nt + li];
 
-    // float offset in s_in of the lane's first pixel for each M-tile, plus its channel group
-    int pb[G::MPW];
+    // byte offset in a plane of the lane's first input pixel for each M-tile
+    // (rows past the map read pixel 0; their results are dropped)
+    int pb[G::MT];
 #pragma unroll
-    for (int i = 0; i < G::MPW; ++i) {
-        const int pp = 16 * (mh * G::MPW + i) + li;
+    for (int i = 0; i < G::MT; ++i) {
+        const int pp = 16 * i + li;
         const int pc = pp < G::P ? pp : 0;
         const int oy = pc / OH, ox = pc - oy * OH;
-        pb[i] = ((S * oy) * IH + S * ox) * G::PSF + 4 * g;
+        pb[i] = ((S * oy) * IH + S * ox) * G::PSB + 16 * g;
     }
 
+    // the k-steps of half KH: per step, the three planes of every M-tile's A
+    // operand, then the six products, each over all M-tiles (independent chains)
+    auto half = [&](auto khc, f4* acc) {
+        constexpr int KH = decltype(khc)::value;
+#pragma unroll
+        for (int s = 0; s < G::KSH; ++s) {
+            const int ks = KH * G::KSH + s, tap = ks / G::CH, cb = ks % G::CH;
+            const int off = ((tap / K) * IH + tap % K) * G::PSB + 64 * cb;
+            bf16x8 a[3][G::MT];
+#pragma unroll
+            for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+                for (int i = 0; i < G::MT; ++i) a[pl][i] = *(const bf16x8*)(s_in + pl * G::PLANE + pb[i] + off);
+#pragma unroll
+            for (int i = 0; i < G::MT; ++i) acc[i] = mfma16x16x32bf16(a[2][i], wv[0][s], acc[i]);   // lo*hi
+#pragma unroll
+            for (int i = 0; i < G::MT; ++i) acc[i] = mfma16x16x32bf16(a[1][i], wv[1][s], acc[i]);   // mid*mid
+#pragma unroll
+            for (int i = 0; i < G::MT; ++i) acc[i] = mfma16x16x32bf16(a[0][i], wv[2][s], acc[i]);   // hi*lo
+#pragma unroll
+            for (int i = 0; i < G::MT; ++i) acc[i] = mfma16x16x32bf16(a[1][i], wv[0][s], acc[i]);   // mid*hi
+#pragma unroll
+            for (int i = 0; i < G::MT; ++i) acc[i] = mfma16x16x32bf16(a[0][i], wv[1][s], acc[i]);   // hi*mid
+#pragma unroll
+            for (int i = 0; i < G::MT; ++i) acc[i] = mfma16x16x32bf16(a[0][i], wv[0][s], acc[i]);   // hi*hi
+        }
+    };
+
     for (int j = j_lo; j < j_hi; ++j) {
-        __syncthreads();  // the previous sample's reads of s_in / s_out are done
+        __syncthreads();  // the previous sample's reads of s_out are done
         stage();
         __syncthreads();
         if (j + 1 < j_hi) fetch(j + 1);
-        f4 acc[G::MPW];
+        f4 acc[G::MT];
 #pragma unroll
-        for (int i = 0; i < G::MPW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
-        // one 16-byte read per (tap, block) and M-tile, a (tap, block) ahead
-        constexpr int NB = G::KK * G::CB;
-        auto a_at = [&](int q, int i) {
-            const int tap = q / G::CB, b = q % G::CB;
-            return *(const f4*)(s_in + pb[i] + ((tap / K) * IH + tap % K) * G::PSF + 16 * b);
-        };
-        f4 abuf[2][G::MPW];
+        for (int i = 0; i < G::MT; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        if (kh == 0)
+            half(std::integral_constant<int, 0>{}, acc);
+        else
+            half(std::integral_constant<int, 1>{}, acc);
+        __syncthreads();  // every wave's reads of the planes are done
+        if (kh == 1) {
 #pragma unroll
-        for (int i = 0; i < G::MPW; ++i) abuf[0][i] = a_at(0, i);
-#pragma unroll
-        for (int q = 0; q < NB; ++q) {
-            if (q + 1 < NB) {
-#pragma unroll
-                for (int i = 0; i < G::MPW; ++i) abuf[(q + 1) & 1][i] = a_at(q + 1, i);
-            }
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-#pragma unroll
-                for (int i = 0; i < G::MPW; ++i) acc[i] = mfma16x16x4(abuf[q & 1][i][k], wv[q * 4 + k], acc[i]);
-            __builtin_amdgcn_sched_barrier(0);
+            for (int i = 0; i < G::MT; ++i) s_part[(nt * G::MT + i) * 64 + lane] = acc[i];
         }
+        __syncthreads();
+        if (kh == 0) {
+            // D[4g + r][li] of M-tile i: pixel 16 i + 4g + r, channel 16nt + li
 #pragma unroll
-        for (int i = 0; i < G::MPW; ++i)
+            for (int i = 0; i < G::MT; ++i) {
+                const f4 o = s_part[(nt * G::MT + i) * 64 + lane];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int pp = 16 * (mh * G::MPW + i) + 4 * g + r;
-                if (pp < G::P) s_out[(16 * nt + li) * G::P + pp] = fmaxf(acc[i][r] + bo, 0.f);
+                for (int r = 0; r < 4; ++r) {
+                    const int pp = 16 * i + 4 * g + r;
+                    if (pp < G::P) s_out[(16 * nt + li) * G::P + pp] = fmaxf((acc[i][r] + o[r]) + bo, 0.f);
+                }
             }
+        }
         __syncthreads();
         f4* dst = (f4*)(p.out + (size_t)j * G::OUTF);
         for (int q = t; q < G::OUTF / 4; q += FC_WG) dst[q] = ((const f4*)s_out)[q];
@@ -462,10 +535,11 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl32_kernel(FwdClParams p) {
 }
 
 template <int CIN, int IH, int K, int S, int OH>
-hipError_t fwd_cl32_launch(const float* in, int n_a, int n, const float* w_a, const float* b_a, const float* w_b,
-                           const float* b_b, float* out, const float* pk_a, const float* pk_b, hipStream_t st) {
-    using G = FwdCl32Geom<CIN, IH, K, S, OH>;
+hipError_t fwd_x6_launch(const float* in, int n_a, int n, const float* w_a, const float* b_a, const float* w_b,
+                         const float* b_b, float* out, const float* pk_a, const float* pk_b, hipStream_t st) {
+    using G = FwdX6Geom<CIN, IH, K, S, OH>;
     if (n <= 0 || n_a < 0 || n_a > n || ((uintptr_t)out & 15) || (!pk_a != !pk_b)) return hipErrorInvalidValue;
+    if (pk_a && (((uintptr_t)pk_a & 15) || ((uintptr_t)pk_b & 15))) return hipErrorInvalidValue;
     const int spg = std::max(1, (n + FC_TARGET_BLOCKS - 1) / FC_TARGET_BLOCKS);
     const int g_a = (n_a + spg - 1) / spg, g_b = (n - n_a + spg - 1) / spg;
     const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg, pk_a, pk_b};
@@ -474,7 +548,27 @@ hipError_t fwd_cl32_launch(const float* in, int n_a, int n, const float* w_a, co
         hipLaunchKernelGGL(kern, dim3((unsigned)(g_a + g_b)), dim3(FC_WG), G::LDS, st, prm);
         return hipGetLastError();
     };
-    return pk_a ? go(conv_fwd_cl32_kernel<CIN, IH, K, S, OH, true>) : go(conv_fwd_cl32_kernel<CIN, IH, K, S, OH, false>);
+    return pk_a ? go(conv_fwd_x6_kernel<CIN, IH, K, S, OH, true>) : go(conv_fwd_x6_kernel<CIN, IH, K, S, OH, false>);
+}
+
+// The repacked weight planes of the float32 forward (job jb of the repack
+// launch: one bf16x8 vector per thread e, e < 3 * 4 * KS * 64).
+template <int CIN, int IH, int K, int S, int OH>
+__device__ __forceinline__ void x6_pack_job(const float* __restrict__ w, bf16x8* out, int e) {
+    using G = FwdX6Geom<CIN, IH, K, S, OH>;
+    if (e >= G::PACK) return;
+    const int lane = e & 63, r = e >> 6;
+    const int s = r % G::KSH, kh = (r / G::KSH) & 1, nt = (r / (2 * G::KSH)) & 3, pl = r / (8 * G::KSH);
+    const int li = lane & 15, g = lane >> 4;
+    const int ks = kh * G::KSH + s, tap = ks / G::CH, cb = ks % G::CH;
+    bf16x8 o;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        __bf16 a, b, c;
+        split3(w[(size_t)(16 * nt + li) * CIN * G::KK + (size_t)(32 * cb + 8 * g + q) * G::KK + tap], a, b, c);
+        o[q] = pl == 0 ? a : pl == 1 ? b : c;
+    }
+    out[e] = o;
 }
 
 }  // namespace
@@ -490,12 +584,39 @@ hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const 
     switch (id) {
         case CONV_L2:
             return bf16 ? fwd_cl_launch<32, 20, 4, 2, 9, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, st)
-                        : fwd_cl32_launch<32, 20, 4, 2, 9>(in, n_a, n, w_a, b_a, w_b, b_b, out, pk_a, pk_b, st);
+                        : fwd_x6_launch<32, 20, 4, 2, 9>(in, n_a, n, w_a, b_a, w_b, b_b, out, pk_a, pk_b, st);
         case CONV_L3:
             return bf16 ? fwd_cl_launch<64, 9, 3, 1, 7, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, st)
-                        : fwd_cl32_launch<64, 9, 3, 1, 7>(in, n_a, n, w_a, b_a, w_b, b_b, out, pk_a, pk_b, st);
+                        : fwd_x6_launch<64, 9, 3, 1, 7>(in, n_a, n, w_a, b_a, w_b, b_b, out, pk_a, pk_b, st);
         default: return hipErrorInvalidValue;
     }
+}
+
+__global__ __launch_bounds__(256) void fwd_x6_pack_kernel(const float* w2a, const float* w3a, const float* w2b,
+                                                          const float* w3b, void* x2a, void* x3a, void* x2b,
+                                                          void* x3b) {
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    switch (blockIdx.y) {
+        case 0: if (x2a) x6_pack_job<32, 20, 4, 2, 9>(w2a, (bf16x8*)x2a, e); break;
+        case 1: if (x3a) x6_pack_job<64, 9, 3, 1, 7>(w3a, (bf16x8*)x3a, e); break;
+        case 2: if (x2b) x6_pack_job<32, 20, 4, 2, 9>(w2b, (bf16x8*)x2b, e); break;
+        default: if (x3b) x6_pack_job<64, 9, 3, 1, 7>(w3b, (bf16x8*)x3b, e); break;
+    }
+}
+
+int64_t fwd_x6_pack_floats(ConvId id) {
+    // bf16x8 vectors (4 floats each) of the three planes
+    return id == CONV_L2 ? 4 * FwdX6Geom<32, 20, 4, 2, 9>::PACK : 4 * FwdX6Geom<64, 9, 3, 1, 7>::PACK;
+}
+
+hipError_t launch_fwd_x6_pack(const float* w2a, const float* w3a, const float* w2b, const float* w3b, float* x2a,
+                              float* x3a, float* x2b, float* x3b, hipStream_t st) {
+    for (const float* q : {(const float*)x2a, (const float*)x3a, (const float*)x2b, (const float*)x3b})
+        if ((uintptr_t)q & 15) return hipErrorInvalidValue;
+    constexpr int MAXV = FwdX6Geom<64, 9, 3, 1, 7>::PACK;   // the larger of the two layers
+    hipLaunchKernelGGL(fwd_x6_pack_kernel, dim3((MAXV + 255) / 256, 4), dim3(256), 0, st, w2a, w3a, w2b, w3b, x2a, x3a,
+                       x2b, x3b);
+    return hipGetLastError();
 }
 
 }  // namespace dqn
