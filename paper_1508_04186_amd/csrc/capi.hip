@@ -365,8 +365,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             r.h2 = t.wpk2;
             r.h3 = t.wpk3;
         } else if (repack) {
-            r.d2 = t.wpk2;
-            r.d3 = t.wpk3;
+            r.x2 = t.wpk2;
+            r.x3 = t.wpk3;
         }
         RUN(DQN_K_WEIGHT_REPACK, repack_weights(repack ? &r : nullptr, repack_fwd, th + ni.w_off[1],
                                                 th + ni.w_off[2], tt + ni.w_off[1], tt + ni.w_off[2], t.fpk, st));

@@ -269,13 +269,13 @@ hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float
 hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in, float* din, int n, bool bf16,
                               bool h16, const float* wpk, hipStream_t st);
 // conv2's and conv3's weights of set a (theta) in the per-lane order of the
-// large network's input-gradient kernels, one launch
-// (weight_repack_floats(CONV_L2 / CONV_L3) floats each).  NULL outputs are
-// skipped.
+// large network's input-gradient kernels, one launch (at most
+// weight_repack_floats(CONV_L2 / CONV_L3) floats each, 16-byte aligned).
+// NULL outputs are skipped.
 struct WeightRepack {
     const float *w2a, *w3a;
-    float *d2, *d3;
-    void *h2, *h3;   // bf16 input-gradient operands of set a (half the floats of d2, d3)
+    void *h2, *h3;   // bf16 input-gradient operands (the bf16-input variant)
+    void *x2, *x3;   // the three exact bf16 planes of the float32 input gradients
 };
 int64_t weight_repack_floats(ConvId id);
 hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st);

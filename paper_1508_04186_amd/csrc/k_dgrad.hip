@@ -1,25 +1,27 @@
-// Input gradient of the large network's second convolution (32 -> 64
-// channels, 4x4 stride 2, 20x20 -> 9x9) at large batch, by stride phase
+// Input gradients of the large network's second and third convolutions at
+// large batch, masked by the ReLU mask of the layer below.
+//
+// conv2 (32 -> 64 channels, 4x4 stride 2, 20x20 -> 9x9) by stride phase
 // (py, px): input pixel (2qy + py, 2qx + px), qy, qx in [0, 10), receives
 //   din = [h_in > 0] * sum_{o, ty, tx} W[o][c][py + 2ty][px + 2tx] * dz[o][qy - ty][qx - tx]
 // with dz = 0 outside the 9x9 map, so no product multiplies a structural
-// zero of the strided kernel.
+// zero of the strided kernel.  conv3 (64 -> 64, 3x3 stride 1, 9x9 -> 7x7):
+//   din[c][y][x] = [h_in > 0] * sum_{o, ky, kx} W[o][c][ky][kx] * dz[o][y - ky][x - kx].
 //
-// A workgroup walks a group of samples, one per round; its eight waves are
-// (phase, N-tile of 16 input channels) pairs, and each wave holds its 16 x 256
-// slice of the weights (c x (tap, o)) in registers for the whole launch: the
-// B operand of every k-step.  A sample's dz is staged in LDS with a zero
-// border (row -1, row 9, column 9 and two spare slots per channel), so the A
-// operand of pixel m and tap (ty, tx) sits at a per-lane base plus a
-// compile-time offset and needs no bounds test: channel stride 112 floats
-// (= 48 mod 64) and 16 consecutive pixels contiguous, so a wave's 64 reads
-// hit 64 banks.  A phase has 100 pixels: 7 M-tiles of 16, the last one
-// partly unused.  The four phases' results are assembled into the sample's
-// whole input gradient in LDS, then written with 16-byte stores, masked by
-// the ReLU mask read into registers at the start of the sample's round.  The
-// next sample's dz is read into registers while the current one is
-// computed.  fp32 MFMA; the bf16-input variant is conv2_dgrad_cl_kernel.
+// A workgroup walks a group of samples, one per round, its eight waves
+// holding slices of the weights in registers for the whole launch (the B
+// operand of every k-step).  A sample's dz is staged in LDS channels-last
+// with a zero border, so the A operand of a pixel and tap sits at a per-lane
+// base plus a compile-time offset and needs no bounds test; the sample's
+// whole input gradient is assembled in LDS and written with 16-byte stores,
+// masked by the ReLU mask read into registers at the start of the round, and
+// the next sample's dz is read into registers while the current one is
+// computed.  The bf16-input variant rounds operands to bf16
+// (conv2_dgrad_cl_kernel, conv3_dgrad_cl_kernel); the float32 kernels split
+// them exactly into three bf16 terms (conv2_dgrad_x6_kernel,
+// conv3_dgrad_x6_kernel).
 #include <algorithm>
+#include <initializer_list>
 #include <type_traits>
 
 #include "common.h"
@@ -32,16 +34,10 @@ constexpr int D2_CIN = 32, D2_IH = 20, D2_COUT = 64, D2_OH = 9, D2_K = 4;
 constexpr int D2_Q = 10;                       // phase grid side
 constexpr int D2_QP = D2_Q * D2_Q;             // phase pixels per sample
 constexpr int D2_MT = (D2_QP + 15) / 16;       // M-tiles per phase (7)
-constexpr int D2_CS = 112;                     // staged floats per dz channel
-constexpr int D2_LEAD = 16;                    // zeros before the stage (offset -1 reads)
-constexpr int D2_TAIL = 32;                    // slack after it (rows of the unused pixels)
-constexpr int D2_STAGE = D2_LEAD + D2_COUT * D2_CS + D2_TAIL;
 constexpr int D2_DZ = D2_COUT * D2_OH * D2_OH; // dz floats per sample (5,184)
 constexpr int D2_IN = D2_CIN * D2_IH * D2_IH;  // input-gradient floats per sample (12,800)
 constexpr int D2_KT = D2_COUT * 4;             // contraction length (o, tap): 256
-constexpr int D2_PER = (D2_DZ + D2_WG - 1) / D2_WG;       // dz floats per thread (11)
 constexpr int D2_OUT4 = (D2_IN / 4 + D2_WG - 1) / D2_WG;  // float4 of din per thread (7)
-static_assert(D2_CS >= (D2_OH + 2) * D2_Q && D2_CS % 64 == 48, "channel stride: border and banks");
 static_assert(D2_IN % 4 == 0, "whole float4 rows");
 
 struct Dgrad2Params {
@@ -50,7 +46,7 @@ struct Dgrad2Params {
     const float* h_in;  // [n][32][20][20] (bfloat16 values when h16)
     float* din;         // [n][32][20][20]
     int n, spg;         // samples, samples per workgroup
-    const float* wpk;   // fp32 kernels: the weights in per-lane order (weight_repack), or NULL
+    const float* wpk;   // the weights in per-lane order (weight_repack), or NULL
 };
 
 // Four consecutive values of the layer input h_in (the ReLU mask source) at
@@ -74,142 +70,7 @@ struct Mask4<true> {
     }
 };
 
-template <bool PK>   // weights from p.wpk (weight_repack) instead of p.w
-__global__ __launch_bounds__(D2_WG) void conv2_dgrad_phase_kernel(Dgrad2Params p) {
-    __shared__ float s_dz[D2_STAGE];
-    __shared__ __align__(16) float s_din[D2_IN];
-    const int t = threadIdx.x;
-    const int lane = t & 63, wave = t >> 6;
-    const int li = lane & 15, g = lane >> 4;
-    const int ph = wave >> 1, nt = wave & 1;   // phase; N-tile
-    const int py = ph >> 1, px = ph & 1;
-
-    for (int e = t; e < D2_STAGE; e += D2_WG) s_dz[e] = 0.f;
-
-    const int j_lo = blockIdx.x * p.spg;
-    const int j_hi = min(p.n, j_lo + p.spg);
-    if (j_lo >= j_hi) return;  // uniform
-
-    // B operands of this lane for every k-step: k = tap * 64 + o, tap = 2ty + tx.
-    const int c = nt * 16 + li;
-    constexpr int KS = D2_KT / 4;
-    float wreg[KS];
-    if constexpr (PK) {   // coalesced: lane-consecutive per k-step
-#pragma unroll
-        for (int s = 0; s < KS; ++s) wreg[s] = p.wpk[((size_t)wave * KS + s) * 64 + lane];
-    } else {
-        const float* wc = p.w + (size_t)c * D2_K * D2_K + py * D2_K + px;
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-            // k-step s: tap s / 16, o = 4 * (s % 16) + g
-            const int tap = s / 16, ty = tap >> 1, tx = tap & 1;
-            const int o = 4 * (s % 16) + g;
-            wreg[s] = wc[(size_t)o * D2_CIN * D2_K * D2_K + 2 * ty * D2_K + 2 * tx];
-        }
-    }
-
-    // Per-lane LDS base of each M-tile: pixel m = 16 mt + li, channel g, row
-    // shifted by one (the zero row above the map).  The A operand of tap
-    // (ty, tx) and channel o0 + g is then at base + o0*D2_CS - 10ty - tx, a
-    // compile-time offset.
-    int base[D2_MT];
-#pragma unroll
-    for (int i = 0; i < D2_MT; ++i) base[i] = D2_LEAD + g * D2_CS + i * 16 + li + D2_Q;
-
-    // A sample's dz in registers (thread t holds flat elements t + u*D2_WG),
-    // then into LDS at channel e / 81, row oy + 1, column ox: offset q + q/9
-    // past the row shift.
-    float v[D2_PER];
-    auto fetch = [&](int j) {
-        const float* src = p.dz + (size_t)j * D2_DZ;
-#pragma unroll
-        for (int u = 0; u < D2_PER; ++u) {
-            const int e = t + u * D2_WG;
-            v[u] = e < D2_DZ ? src[e] : 0.f;
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int u = 0; u < D2_PER; ++u) {
-            const int e = t + u * D2_WG;
-            if (e < D2_DZ) {
-                const int row = e / (D2_OH * D2_OH), q = e - row * (D2_OH * D2_OH);
-                s_dz[D2_LEAD + D2_Q + row * D2_CS + q + q / D2_OH] = v[u];
-            }
-        }
-    };
-
-    fetch(j_lo);
-    for (int j = j_lo; j < j_hi; ++j) {
-        __syncthreads();  // the zero fill, or the previous round's LDS reads, are done
-        stage();
-        __syncthreads();
-        if (j + 1 < j_hi) fetch(j + 1);  // in flight during this sample's MFMAs
-        // this sample's ReLU mask, for the write-out below
-        const size_t o0 = (size_t)j * D2_IN;
-        Mask4<false> mreg[D2_OUT4];
-#pragma unroll
-        for (int u = 0; u < D2_OUT4; ++u) {
-            const int e4 = t + u * D2_WG;
-            if (e4 < D2_IN / 4) mreg[u].load(p, o0 + 4 * e4);
-        }
-
-        f4 acc[D2_MT];
-#pragma unroll
-        for (int i = 0; i < D2_MT; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
-        // The k-steps run in order with the next step's A operands read
-        // before the current step's MFMAs issue (scheduling groups), and a
-        // barrier per step keeps the compiler from hoisting every LDS read.
-        {
-            auto load = [&](int s, float (&a)[D2_MT]) {
-                const int tap = s / 16, ty = tap >> 1, tx = tap & 1;
-                const int off = 4 * (s % 16) * D2_CS - D2_Q * ty - tx;
-#pragma unroll
-                for (int i = 0; i < D2_MT; ++i) a[i] = s_dz[base[i] + off];
-            };
-            float a[2][D2_MT];
-            load(0, a[0]);
-#pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                if (s + 1 < KS) load(s + 1, a[(s + 1) & 1]);
-#pragma unroll
-                for (int i = 0; i < D2_MT; ++i) acc[i] = mfma16x16x4(a[s & 1][i], wreg[s], acc[i]);
-                if (s + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x100, D2_MT, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, D2_MT, 0);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-
-        // D[4g + r][li] of tile i: phase pixel m = 16 i + 4g + r, channel c,
-        // into the sample's gradient in LDS (the previous sample's write-out
-        // finished before this round's second barrier).
-#pragma unroll
-        for (int i = 0; i < D2_MT; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = i * 16 + 4 * g + r;
-                if (m < D2_QP) {
-                    const int qy = m / D2_Q, qx = m - qy * D2_Q;
-                    s_din[c * D2_IH * D2_IH + (2 * qy + py) * D2_IH + 2 * qx + px] = acc[i][r];
-                }
-            }
-        __syncthreads();
-        // masked write-out with 16-byte accesses
-#pragma unroll
-        for (int u = 0; u < D2_OUT4; ++u) {
-            const int e4 = t + u * D2_WG;
-            if (e4 < D2_IN / 4) {
-                const f4 d = *(const f4*)(s_din + 4 * e4);
-                f4 o;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) o[k] = mreg[u].pos(k) ? d[k] : 0.f;
-                *(f4*)(p.din + o0 + 4 * e4) = o;
-            }
-        }
-    }
-}
-
-// The bf16-input variant of the same computation with dz staged as bf16,
+// conv2 with dz staged as bf16 (the bf16-input variant),
 // channels-last: slot sigma(y, x) = 10 (y + 1) + x + 1 of the zero-bordered
 // 10-wide map (rows -1 .. 10; a row's column 9 is the next row's column -1)
 // holds dz[o][y][x] for the 64 channels o, 144 bytes per slot.  The eight
@@ -358,153 +219,19 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
 }
 
 // ---------------------------------------------------------------------------
-// Input gradient of the large network's third convolution (64 -> 64
-// channels, 3x3 stride 1, 9x9 -> 7x7):
-//   din[c][y][x] = [h_in > 0] * sum_{o, ky, kx} W[o][c][ky][kx] * dz[o][y - ky][x - kx]
-// with dz = 0 outside the 7x7 map, in the same arrangement: a workgroup walks
-// samples; its eight waves are (N-tile of 16 input channels, half of the six
-// M-tiles of the 81 pixels) pairs, each holding its 16 x 576 weight slice in
-// registers.  dz is staged with two zero rows above and below and two zero
-// columns on the right of each 7-wide row, at a row stride of 9, so pixel m
-// = 9y + x reads tap (ky, kx) at m + 18 - 9ky - kx past its channel's base:
-// 16 consecutive pixels are contiguous and reads that leave a row land on
-// zeros.
+// conv3 geometry.
 constexpr int D3_CIN = 64, D3_IH = 9, D3_COUT = 64, D3_OH = 7, D3_K = 3;
 constexpr int D3_P = D3_IH * D3_IH;            // input pixels per sample (81)
 constexpr int D3_MT = (D3_P + 15) / 16;        // M-tiles (6)
 constexpr int D3_TPW = D3_MT / 2;              // M-tiles per wave (3)
-constexpr int D3_CS = 112;                     // staged floats per dz channel
-constexpr int D3_ROW0 = 2 * D3_IH;             // two zero rows
-constexpr int D3_LEAD = 16, D3_TAIL = 32;
-constexpr int D3_STAGE = D3_LEAD + D3_COUT * D3_CS + D3_TAIL;
 constexpr int D3_DZ = D3_COUT * D3_OH * D3_OH; // dz floats per sample (3,136)
 constexpr int D3_IN = D3_CIN * D3_P;           // input-gradient floats per sample (5,184)
 constexpr int D3_KT = D3_COUT * D3_K * D3_K;   // contraction length (tap, o): 576
-constexpr int D3_PER = (D3_DZ + D2_WG - 1) / D2_WG;
 constexpr int D3_OUT4 = (D3_IN / 4 + D2_WG - 1) / D2_WG;
-static_assert(D3_CS >= (D3_OH + 4) * D3_IH && D3_CS % 64 == 48, "channel stride: border and banks");
 static_assert(D3_MT % 2 == 0 && D3_IN % 4 == 0, "tile split and float4 rows");
 
-template <bool PK>   // weights from p.wpk (weight_repack) instead of p.w
-__global__ __launch_bounds__(D2_WG) void conv3_dgrad_kernel(Dgrad2Params p) {
-    __shared__ float s_dz[D3_STAGE];
-    __shared__ __align__(16) float s_din[D3_IN];
-    const int t = threadIdx.x;
-    const int lane = t & 63, wave = t >> 6;
-    const int li = lane & 15, g = lane >> 4;
-    const int nt = wave & 3, mh = wave >> 2;   // N-tile; half of the M-tiles
-
-    for (int e = t; e < D3_STAGE; e += D2_WG) s_dz[e] = 0.f;
-
-    const int j_lo = blockIdx.x * p.spg;
-    const int j_hi = min(p.n, j_lo + p.spg);
-    if (j_lo >= j_hi) return;  // uniform
-
-    // B operands for every k-step: k = tap * 64 + o, tap = 3ky + kx.
-    const int c = nt * 16 + li;
-    constexpr int KS = D3_KT / 4;
-    float wreg[KS];
-    if constexpr (PK) {   // coalesced: lane-consecutive per k-step (waves nt and nt + 4 share a slice)
-#pragma unroll
-        for (int s = 0; s < KS; ++s) wreg[s] = p.wpk[((size_t)nt * KS + s) * 64 + lane];
-    } else {
-        const float* wc = p.w + (size_t)c * D3_K * D3_K;
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-            const int tap = s / 16, o = 4 * (s % 16) + g;
-            wreg[s] = wc[(size_t)o * D3_CIN * D3_K * D3_K + tap];
-        }
-    }
-
-    int base[D3_TPW];
-#pragma unroll
-    for (int i = 0; i < D3_TPW; ++i)
-        base[i] = D3_LEAD + g * D3_CS + (mh * D3_TPW + i) * 16 + li + D3_ROW0;
-
-    float v[D3_PER];
-    auto fetch = [&](int j) {
-        const float* src = p.dz + (size_t)j * D3_DZ;
-#pragma unroll
-        for (int u = 0; u < D3_PER; ++u) {
-            const int e = t + u * D2_WG;
-            v[u] = e < D3_DZ ? src[e] : 0.f;
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int u = 0; u < D3_PER; ++u) {
-            const int e = t + u * D2_WG;
-            if (e < D3_DZ) {
-                const int o = e / (D3_OH * D3_OH), q = e - o * (D3_OH * D3_OH);
-                // row oy + 2 at stride 9: offset 18 + q + 2 * (q / 7)
-                s_dz[D3_LEAD + o * D3_CS + D3_ROW0 + q + 2 * (q / D3_OH)] = v[u];
-            }
-        }
-    };
-
-    fetch(j_lo);
-    for (int j = j_lo; j < j_hi; ++j) {
-        __syncthreads();
-        stage();
-        __syncthreads();
-        if (j + 1 < j_hi) fetch(j + 1);
-        // this sample's ReLU mask, for the write-out below
-        const size_t o0 = (size_t)j * D3_IN;
-        Mask4<false> mreg[D3_OUT4];
-#pragma unroll
-        for (int u = 0; u < D3_OUT4; ++u) {
-            const int e4 = t + u * D2_WG;
-            if (e4 < D3_IN / 4) mreg[u].load(p, o0 + 4 * e4);
-        }
-
-        f4 acc[D3_TPW];
-#pragma unroll
-        for (int i = 0; i < D3_TPW; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
-        {
-            auto load = [&](int s, float (&a)[D3_TPW]) {
-                const int tap = s / 16, ky = tap / 3, kx = tap % 3;
-                const int off = 4 * (s % 16) * D3_CS - D3_IH * ky - kx;
-#pragma unroll
-                for (int i = 0; i < D3_TPW; ++i) a[i] = s_dz[base[i] + off];
-            };
-            float a[2][D3_TPW];
-            load(0, a[0]);
-#pragma unroll
-            for (int s = 0; s < KS; ++s) {
-                if (s + 1 < KS) load(s + 1, a[(s + 1) & 1]);
-#pragma unroll
-                for (int i = 0; i < D3_TPW; ++i) acc[i] = mfma16x16x4(a[s & 1][i], wreg[s], acc[i]);
-                if (s + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x100, D3_TPW, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, D3_TPW, 0);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-
-        // D[4g + r][li] of tile i: pixel m, channel c
-#pragma unroll
-        for (int i = 0; i < D3_TPW; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = (mh * D3_TPW + i) * 16 + 4 * g + r;
-                if (m < D3_P) s_din[c * D3_P + m] = acc[i][r];
-            }
-        __syncthreads();
-#pragma unroll
-        for (int u = 0; u < D3_OUT4; ++u) {
-            const int e4 = t + u * D2_WG;
-            if (e4 < D3_IN / 4) {
-                const f4 d = *(const f4*)(s_din + 4 * e4);
-                f4 o;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) o[k] = mreg[u].pos(k) ? d[k] : 0.f;
-                *(f4*)(p.din + o0 + 4 * e4) = o;
-            }
-        }
-    }
-}
-
-
-// The bf16-input variant with dz staged channels-last as bf16: slot
+// conv3 with dz staged channels-last as bf16 (the bf16-input variant; eight
+// waves of (N-tile, half of the six M-tiles)): slot
 // sigma = 9 (y + 2) + x + 2 of the zero-bordered map (two zero rows above
 // and below, columns 7 and 8 of a row zero, two lead slots) holds dz[o][y][x]
 // for the 64 channels, 144 bytes per slot; pixel m reads tap (ky, kx) at
@@ -638,28 +365,352 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// The float32 input gradients on bf16 MFMA with exact three-term splits (the
+// arithmetic of the float32 forward, conv_fwd_x6_kernel: six products per 32
+// k-values, float32 accuracy): dz is split into three bf16 planes staged in
+// the slot layouts of the bf16 kernels above, the weights' three planes sit
+// in registers, loaded in per-lane order from the step's repack (or split
+// in the kernel).  Plane pl of the packed weights: element
+// ((pl W + w) KS + s) 64 + lane for wave (or N-tile) w and k-step s, in the
+// bf16 kernels' k order.
+//
+// conv2: waves are (phase, N-tile) pairs as in conv2_dgrad_cl_kernel (8
+// k-steps of 32: 96 registers of weights); the seven M-tiles of a phase run
+// in two groups (4, then 3) to bound the operand registers.
+constexpr int X2_KS = D2_KT / 32;              // 8
+constexpr int X3_KS = D3_KT / 32;              // 18 (9 per half)
+constexpr int X2_LDS = 3 * D2C_SLOTS * D2C_PSB;
+constexpr int X3_LDS = 3 * D3C_SLOTS * D3C_PSB;
+
+template <bool PK>
+__global__ __launch_bounds__(D2_WG) void conv2_dgrad_x6_kernel(Dgrad2Params p) {
+    __shared__ __align__(16) unsigned char s_cl[X2_LDS];     // [3][slots][144]
+    __shared__ __align__(16) float s_din[D2_IN];
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int ph = wave >> 1, nt = wave & 1;
+    const int py = ph >> 1, px = ph & 1;
+    constexpr int PL = D2C_SLOTS * D2C_PSB;
+
+    for (int e = t; e < X2_LDS / 16; e += D2_WG) ((uint4*)s_cl)[e] = uint4{0u, 0u, 0u, 0u};
+
+    const int j_lo = blockIdx.x * p.spg;
+    const int j_hi = min(p.n, j_lo + p.spg);
+    if (j_lo >= j_hi) return;  // uniform
+
+    const int c = nt * 16 + li;
+    bf16x8 wreg[3][X2_KS];
+    if constexpr (PK) {
+#pragma unroll
+        for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+            for (int s = 0; s < X2_KS; ++s)
+                wreg[pl][s] = ((const bf16x8*)p.wpk)[((size_t)(pl * 8 + wave) * X2_KS + s) * 64 + lane];
+    } else {
+        const float* wc = p.w + (size_t)c * D2_K * D2_K + py * D2_K + px;
+#pragma unroll
+        for (int s = 0; s < X2_KS; ++s) {
+            const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int o = 32 * (s % 2) + 8 * g + e;
+                __bf16 a, b, d;
+                split3(wc[(size_t)o * D2_CIN * D2_K * D2_K + 2 * ty * D2_K + 2 * tx], a, b, d);
+                wreg[0][s][e] = a;
+                wreg[1][s][e] = b;
+                wreg[2][s][e] = d;
+            }
+        }
+    }
+    int base[D2_MT];
+#pragma unroll
+    for (int i = 0; i < D2_MT; ++i) {
+        const int m = i * 16 + li, qy = m / D2_Q, qx = m - qy * D2_Q;
+        base[i] = (D2_Q * (qy + 1) + qx + 1) * D2C_PSB + 16 * g;
+    }
+
+    float va[D2C_PER], vb[D2C_PER];
+    auto fetch = [&](int j) {
+        const float* src = p.dz + (size_t)j * D2_DZ;
+#pragma unroll
+        for (int u = 0; u < D2C_PER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < D2C_PAIRS) {
+                const int op = q2 / (D2_OH * D2_OH), q = q2 - op * (D2_OH * D2_OH);
+                va[u] = src[(2 * op) * D2_OH * D2_OH + q];
+                vb[u] = src[(2 * op + 1) * D2_OH * D2_OH + q];
+            }
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < D2C_PER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < D2C_PAIRS) {
+                const int op = q2 / (D2_OH * D2_OH), q = q2 - op * (D2_OH * D2_OH);
+                const int oy = q / D2_OH, ox = q - oy * D2_OH;
+                __bf16 a0, a1, a2, b0, b1, b2;
+                split3(va[u], a0, a1, a2);
+                split3(vb[u], b0, b1, b2);
+                unsigned char* d = s_cl + (D2_Q * (oy + 1) + ox + 1) * D2C_PSB + 4 * op;
+                auto word = [](__bf16 lo, __bf16 hi) {
+                    return (uint32_t)__builtin_bit_cast(unsigned short, lo) |
+                           ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
+                };
+                *(uint32_t*)d = word(a0, b0);
+                *(uint32_t*)(d + PL) = word(a1, b1);
+                *(uint32_t*)(d + 2 * PL) = word(a2, b2);
+            }
+        }
+    };
+
+    // M-tiles [I0, I0 + NI): per k-step the three planes of their A operands,
+    // then the six products, each over the group's tiles
+    auto group = [&](auto i0c, auto nic, f4* acc) {
+        constexpr int I0 = decltype(i0c)::value, NI = decltype(nic)::value;
+#pragma unroll
+        for (int s = 0; s < X2_KS; ++s) {
+            const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
+            const int off = -(D2_Q * ty + tx) * D2C_PSB + 64 * (s % 2);
+            bf16x8 a[3][NI];
+#pragma unroll
+            for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+                for (int i = 0; i < NI; ++i) a[pl][i] = *(const bf16x8*)(s_cl + pl * PL + base[I0 + i] + off);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) acc[I0 + i] = mfma16x16x32bf16(a[2][i], wreg[0][s], acc[I0 + i]);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) acc[I0 + i] = mfma16x16x32bf16(a[1][i], wreg[1][s], acc[I0 + i]);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) acc[I0 + i] = mfma16x16x32bf16(a[0][i], wreg[2][s], acc[I0 + i]);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) acc[I0 + i] = mfma16x16x32bf16(a[1][i], wreg[0][s], acc[I0 + i]);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) acc[I0 + i] = mfma16x16x32bf16(a[0][i], wreg[1][s], acc[I0 + i]);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) acc[I0 + i] = mfma16x16x32bf16(a[0][i], wreg[0][s], acc[I0 + i]);
+        }
+    };
+
+    fetch(j_lo);
+    for (int j = j_lo; j < j_hi; ++j) {
+        __syncthreads();  // the zero fill, or the previous round's LDS reads, are done
+        stage();
+        __syncthreads();
+        if (j + 1 < j_hi) fetch(j + 1);  // in flight during this sample's MFMAs
+        const size_t o0 = (size_t)j * D2_IN;
+        Mask4<false> mreg[D2_OUT4];
+#pragma unroll
+        for (int u = 0; u < D2_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D2_IN / 4) mreg[u].load(p, o0 + 4 * e4);
+        }
+        f4 acc[D2_MT];
+#pragma unroll
+        for (int i = 0; i < D2_MT; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        group(std::integral_constant<int, 0>{}, std::integral_constant<int, 4>{}, acc);
+        group(std::integral_constant<int, 4>{}, std::integral_constant<int, D2_MT - 4>{}, acc);
+#pragma unroll
+        for (int i = 0; i < D2_MT; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = i * 16 + 4 * g + r;
+                if (m < D2_QP) {
+                    const int qy = m / D2_Q, qx = m - qy * D2_Q;
+                    s_din[c * D2_IH * D2_IH + (2 * qy + py) * D2_IH + 2 * qx + px] = acc[i][r];
+                }
+            }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < D2_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D2_IN / 4) {
+                const f4 d = *(const f4*)(s_din + 4 * e4);
+                f4 o;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) o[k] = mreg[u].pos(k) ? d[k] : 0.f;
+                *(f4*)(p.din + o0 + 4 * e4) = o;
+            }
+        }
+    }
+}
+
+// conv3: waves are (N-tile, half of the 18 k-steps) pairs (108 registers of
+// weights) over all six M-tiles; the second half's sums reach the first
+// half's waves through LDS.
+template <bool PK>
+__global__ __launch_bounds__(D2_WG) void conv3_dgrad_x6_kernel(Dgrad2Params p) {
+    __shared__ __align__(16) unsigned char s_cl[X3_LDS];     // [3][slots][144]
+    __shared__ __align__(16) float s_din[D3_IN];
+    __shared__ f4 s_part[4 * D3_MT * 64];                     // the k-half 1 waves' sums
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int nt = wave & 3, kh = wave >> 2;
+    constexpr int PL = D3C_SLOTS * D3C_PSB;
+    constexpr int KSH = X3_KS / 2;
+
+    for (int e = t; e < X3_LDS / 16; e += D2_WG) ((uint4*)s_cl)[e] = uint4{0u, 0u, 0u, 0u};
+
+    const int j_lo = blockIdx.x * p.spg;
+    const int j_hi = min(p.n, j_lo + p.spg);
+    if (j_lo >= j_hi) return;  // uniform
+
+    const int c = nt * 16 + li;
+    bf16x8 wreg[3][KSH];
+    if constexpr (PK) {
+#pragma unroll
+        for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+            for (int s = 0; s < KSH; ++s)
+                wreg[pl][s] = ((const bf16x8*)p.wpk)[((size_t)(pl * 4 + nt) * X3_KS + kh * KSH + s) * 64 + lane];
+    } else {
+        const float* wc = p.w + (size_t)c * D3_K * D3_K;
+#pragma unroll
+        for (int s = 0; s < KSH; ++s) {
+            const int ks = kh * KSH + s, tap = ks / 2;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int o = 32 * (ks % 2) + 8 * g + e;
+                __bf16 a, b, d;
+                split3(wc[(size_t)o * D3_CIN * D3_K * D3_K + tap], a, b, d);
+                wreg[0][s][e] = a;
+                wreg[1][s][e] = b;
+                wreg[2][s][e] = d;
+            }
+        }
+    }
+    int base[D3_MT];
+#pragma unroll
+    for (int i = 0; i < D3_MT; ++i) base[i] = (i * 16 + li + 20) * D3C_PSB + 16 * g;
+
+    float va[D3C_PER], vb[D3C_PER];
+    auto fetch = [&](int j) {
+        const float* src = p.dz + (size_t)j * D3_DZ;
+#pragma unroll
+        for (int u = 0; u < D3C_PER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < D3C_PAIRS) {
+                const int op = q2 / (D3_OH * D3_OH), q = q2 - op * (D3_OH * D3_OH);
+                va[u] = src[(2 * op) * D3_OH * D3_OH + q];
+                vb[u] = src[(2 * op + 1) * D3_OH * D3_OH + q];
+            }
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < D3C_PER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < D3C_PAIRS) {
+                const int op = q2 / (D3_OH * D3_OH), q = q2 - op * (D3_OH * D3_OH);
+                const int oy = q / D3_OH, ox = q - oy * D3_OH;
+                __bf16 a0, a1, a2, b0, b1, b2;
+                split3(va[u], a0, a1, a2);
+                split3(vb[u], b0, b1, b2);
+                unsigned char* d = s_cl + (D3_IH * (oy + 2) + ox + 2) * D3C_PSB + 4 * op;
+                auto word = [](__bf16 lo, __bf16 hi) {
+                    return (uint32_t)__builtin_bit_cast(unsigned short, lo) |
+                           ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
+                };
+                *(uint32_t*)d = word(a0, b0);
+                *(uint32_t*)(d + PL) = word(a1, b1);
+                *(uint32_t*)(d + 2 * PL) = word(a2, b2);
+            }
+        }
+    };
+    auto half = [&](auto khc, f4* acc) {
+        constexpr int KH = decltype(khc)::value;
+#pragma unroll
+        for (int s = 0; s < KSH; ++s) {
+            const int ks = KH * KSH + s, tap = ks / 2, ky = tap / 3, kx = tap % 3;
+            const int off = -(D3_IH * ky + kx) * D3C_PSB + 64 * (ks % 2);
+            bf16x8 a[3][D3_MT];
+#pragma unroll
+            for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+                for (int i = 0; i < D3_MT; ++i) a[pl][i] = *(const bf16x8*)(s_cl + pl * PL + base[i] + off);
+#pragma unroll
+            for (int i = 0; i < D3_MT; ++i) acc[i] = mfma16x16x32bf16(a[2][i], wreg[0][s], acc[i]);
+#pragma unroll
+            for (int i = 0; i < D3_MT; ++i) acc[i] = mfma16x16x32bf16(a[1][i], wreg[1][s], acc[i]);
+#pragma unroll
+            for (int i = 0; i < D3_MT; ++i) acc[i] = mfma16x16x32bf16(a[0][i], wreg[2][s], acc[i]);
+#pragma unroll
+            for (int i = 0; i < D3_MT; ++i) acc[i] = mfma16x16x32bf16(a[1][i], wreg[0][s], acc[i]);
+#pragma unroll
+            for (int i = 0; i < D3_MT; ++i) acc[i] = mfma16x16x32bf16(a[0][i], wreg[1][s], acc[i]);
+#pragma unroll
+            for (int i = 0; i < D3_MT; ++i) acc[i] = mfma16x16x32bf16(a[0][i], wreg[0][s], acc[i]);
+        }
+    };
+
+    fetch(j_lo);
+    for (int j = j_lo; j < j_hi; ++j) {
+        __syncthreads();  // the zero fill, or the previous round's LDS reads, are done
+        stage();
+        __syncthreads();
+        if (j + 1 < j_hi) fetch(j + 1);
+        const size_t o0 = (size_t)j * D3_IN;
+        Mask4<false> mreg[D3_OUT4];
+#pragma unroll
+        for (int u = 0; u < D3_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D3_IN / 4) mreg[u].load(p, o0 + 4 * e4);
+        }
+        f4 acc[D3_MT];
+#pragma unroll
+        for (int i = 0; i < D3_MT; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+        if (kh == 0)
+            half(std::integral_constant<int, 0>{}, acc);
+        else
+            half(std::integral_constant<int, 1>{}, acc);
+        if (kh == 1) {
+#pragma unroll
+            for (int i = 0; i < D3_MT; ++i) s_part[(nt * D3_MT + i) * 64 + lane] = acc[i];
+        }
+        __syncthreads();
+        if (kh == 0) {
+            // D[4g + r][li] of tile i: pixel m, channel c
+#pragma unroll
+            for (int i = 0; i < D3_MT; ++i) {
+                const f4 o = s_part[(nt * D3_MT + i) * 64 + lane];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int m = i * 16 + 4 * g + r;
+                    if (m < D3_P) s_din[c * D3_P + m] = acc[i][r] + o[r];
+                }
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < D3_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D3_IN / 4) {
+                const f4 d = *(const f4*)(s_din + 4 * e4);
+                f4 o;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) o[q] = mreg[u].pos(q) ? d[q] : 0.f;
+                *(f4*)(p.din + o0 + 4 * e4) = o;
+            }
+        }
+    }
+}
+
 // The weights of the large network's conv2/conv3 input-gradient kernels in
 // the order their lanes load them into registers, so that every load of a
-// wave is one contiguous 256-byte row instead of a gather of scattered
-// words: element ((w KS + s) 64 + lane) is wave w's k-step s, w over the 8
-// (phase, N-tile) waves of conv2 (KS = 64) and the 4 N-tiles of conv3
-// (KS = 144); values W[o][c][tap] as the kernels read (bf16 copies: one
-// 8-value vector per element).  Job j of the launch (blockIdx.y) writes one
-// copy; a NULL output skips it.
+// wave is one contiguous row instead of a gather of scattered words: one
+// 8-value bf16 vector per element, element ((w KS + s) 64 + lane) holding
+// wave w's k-step s, w over the 8 (phase, N-tile) waves of conv2 (KS = 8) or
+// the 4 N-tiles of conv3 (KS = 18), values W[o][c][tap] as the kernels read;
+// the float32 kernels' copies hold the three planes of the exact split one
+// after another.  Job j of the launch (blockIdx.y) writes one copy; a NULL
+// output skips it.
 __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
     const int e = blockIdx.x * 256 + threadIdx.x;
     const int job = blockIdx.y;
-    if (job == 0) {   // conv2 input gradient
-        constexpr int KS2 = D2_KT / 4;
-        if (r.d2 && e < 8 * KS2 * 64) {
-            const int lane = e & 63, s = (e >> 6) % KS2, wave = (e >> 6) / KS2;
-            const int li = lane & 15, g = lane >> 4, ph = wave >> 1, nt = wave & 1;
-            const int py = ph >> 1, px = ph & 1, c = nt * 16 + li;
-            const int tap = s / 16, ty = tap >> 1, tx = tap & 1, o = 4 * (s % 16) + g;
-            r.d2[e] = r.w2a[(size_t)o * D2_CIN * D2_K * D2_K + (size_t)c * D2_K * D2_K + (py + 2 * ty) * D2_K + px +
-                            2 * tx];
-        }
-    } else if (job == 2) {   // conv2 input gradient, bf16 operands: one 8-value vector per thread
+    if (job == 0) {   // conv2 input gradient, bf16 operands: one 8-value vector per thread
         constexpr int KS2 = D2_KT / 32;
         if (r.h2 && e < 8 * KS2 * 64) {
             const int lane = e & 63, s = (e >> 6) % KS2, wave = (e >> 6) / KS2;
@@ -675,7 +726,7 @@ __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
             }
             ((bf16x8*)r.h2)[e] = v;
         }
-    } else if (job == 3) {   // conv3 input gradient, bf16 operands
+    } else if (job == 1) {   // conv3 input gradient, bf16 operands
         constexpr int KS3 = D3_KT / 32;
         if (r.h3 && e < 4 * KS3 * 64) {
             const int lane = e & 63, s = (e >> 6) % KS3, nt = (e >> 6) / KS3;
@@ -689,24 +740,51 @@ __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
             }
             ((bf16x8*)r.h3)[e] = v;
         }
-    } else {   // job 1: conv3 input gradient
-        constexpr int KS3 = D3_KT / 4;
-        if (r.d3 && e < 4 * KS3 * 64) {
-            const int lane = e & 63, s = (e >> 6) % KS3, nt = (e >> 6) / KS3;
+    } else if (job == 2) {   // conv2 float32 input gradient: plane pl of the split, as job 0
+        if (r.x2 && e < 3 * 8 * X2_KS * 64) {
+            const int lane = e & 63, s = (e >> 6) % X2_KS, wave = ((e >> 6) / X2_KS) % 8, pl = (e >> 6) / (8 * X2_KS);
+            const int li = lane & 15, g = lane >> 4, ph = wave >> 1, nt = wave & 1;
+            const int py = ph >> 1, px = ph & 1, c = nt * 16 + li;
+            const int tap = s / 2, ty = tap >> 1, tx = tap & 1;
+            bf16x8 v;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int o = 32 * (s % 2) + 8 * g + q;
+                __bf16 a, b, d;
+                split3(r.w2a[(size_t)o * D2_CIN * D2_K * D2_K + (size_t)c * D2_K * D2_K + (py + 2 * ty) * D2_K + px +
+                             2 * tx], a, b, d);
+                v[q] = pl == 0 ? a : pl == 1 ? b : d;
+            }
+            ((bf16x8*)r.x2)[e] = v;
+        }
+    } else {   // job 3: conv3 float32 input gradient, as job 1
+        if (r.x3 && e < 3 * 4 * X3_KS * 64) {
+            const int lane = e & 63, s = (e >> 6) % X3_KS, nt = ((e >> 6) / X3_KS) % 4, pl = (e >> 6) / (4 * X3_KS);
             const int li = lane & 15, g = lane >> 4, c = nt * 16 + li;
-            const int tap = s / 16, o = 4 * (s % 16) + g;
-            r.d3[e] = r.w3a[(size_t)o * D3_CIN * D3_K * D3_K + (size_t)c * D3_K * D3_K + tap];
+            const int tap = s / 2;
+            bf16x8 v;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int o = 32 * (s % 2) + 8 * g + q;
+                __bf16 a, b, d;
+                split3(r.w3a[(size_t)o * D3_CIN * D3_K * D3_K + (size_t)c * D3_K * D3_K + tap], a, b, d);
+                v[q] = pl == 0 ? a : pl == 1 ? b : d;
+            }
+            ((bf16x8*)r.x3)[e] = v;
         }
     }
 }
 
 }  // namespace
 
-int64_t weight_repack_floats(ConvId id) { return id == CONV_L2 ? 8 * (D2_KT / 4) * 64 : 4 * (D3_KT / 4) * 64; }
+// floats of the larger copy of a layer (the float32 planes: 4 floats per bf16x8)
+int64_t weight_repack_floats(ConvId id) { return id == CONV_L2 ? 4 * 3 * 8 * X2_KS * 64 : 4 * 3 * 4 * X3_KS * 64; }
 
 hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st) {
-    // every copy has at most 4 * 144 * 64 = 36,864 elements
-    hipLaunchKernelGGL(weight_repack_kernel, dim3(36864 / 256, 4), dim3(256), 0, st, r);
+    for (const void* q : {r.h2, r.h3, r.x2, r.x3})
+        if ((uintptr_t)q & 15) return hipErrorInvalidValue;
+    // every copy has at most 3 * 4 * 18 * 64 = 13,824 vectors
+    hipLaunchKernelGGL(weight_repack_kernel, dim3(13824 / 256, 4), dim3(256), 0, st, r);
     return hipGetLastError();
 }
 
@@ -721,10 +799,8 @@ hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in
     else if (bf16 && h16) hipLaunchKernelGGL((conv3_dgrad_cl_kernel<true, false>), grid, blk, 0, st, prm);
     else if (bf16 && wpk) hipLaunchKernelGGL((conv3_dgrad_cl_kernel<false, true>), grid, blk, 0, st, prm);
     else if (bf16) hipLaunchKernelGGL((conv3_dgrad_cl_kernel<false, false>), grid, blk, 0, st, prm);
-    else if (prm.wpk)
-        hipLaunchKernelGGL(conv3_dgrad_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
-    else
-        hipLaunchKernelGGL(conv3_dgrad_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    else if (prm.wpk) hipLaunchKernelGGL(conv3_dgrad_x6_kernel<true>, grid, blk, 0, st, prm);
+    else hipLaunchKernelGGL(conv3_dgrad_x6_kernel<false>, grid, blk, 0, st, prm);
     return hipGetLastError();
 }
 
@@ -740,10 +816,8 @@ hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float
     else if (bf16 && h16) hipLaunchKernelGGL((conv2_dgrad_cl_kernel<true, false>), grid, blk, 0, st, prm);
     else if (bf16 && wpk) hipLaunchKernelGGL((conv2_dgrad_cl_kernel<false, true>), grid, blk, 0, st, prm);
     else if (bf16) hipLaunchKernelGGL((conv2_dgrad_cl_kernel<false, false>), grid, blk, 0, st, prm);
-    else if (prm.wpk)
-        hipLaunchKernelGGL(conv2_dgrad_phase_kernel<true>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
-    else
-        hipLaunchKernelGGL(conv2_dgrad_phase_kernel<false>, dim3((unsigned)blocks), dim3(D2_WG), 0, st, prm);
+    else if (prm.wpk) hipLaunchKernelGGL(conv2_dgrad_x6_kernel<true>, grid, blk, 0, st, prm);
+    else hipLaunchKernelGGL(conv2_dgrad_x6_kernel<false>, grid, blk, 0, st, prm);
     return hipGetLastError();
 }
 
