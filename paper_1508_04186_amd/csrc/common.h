@@ -347,6 +347,22 @@ enum GemmKind { GEMM_NT = 0, GEMM_TN = 1, GEMM_NN = 2 };
 // k-slicing of the fc1 forward GEMM for `rows` output rows: ks slices of
 // kchunk (a multiple of 64, the last one possibly shorter).
 void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk);
+// From kGemmX6MinRows rows the float32 fc1 forward (GEMM_NT: both operands
+// contiguous along k) runs on bf16 MFMA with the exact three-plane split
+// (launch_gemm_x6: GEMM_NT only; same arguments as launch_gemm, kchunk a
+// multiple of 32).
+// The weight and input gradients, whose operands are contiguous along m or
+// n, stay on fp32 MFMA: transposing and splitting them as they are staged
+// cost more than the six products saved (batch 2,048: 80 -> 128 us and
+// 76 -> 87 us), and so did the forward's split below 1,024 rows.
+constexpr int kGemmX6MinRows = 1024;
+void gemm_fwd_split_x6(int rows, int N, int K, int* ks, int* kchunk);
+hipError_t launch_gemm_x6(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
+                          float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
+                          hipStream_t st);
+hipError_t launch_gemm_x6_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0, const float* A1,
+                               const float* B1, float* C1, int lda, int ldb, int ldc, int kslices, int kchunk,
+                               int64_t c_slice, hipStream_t st);
 // The same for the bf16-input variant's forward GEMM (its own tiles).
 void gemm_fwd_split_bf16(int rows, int N, int K, int* ks, int* kchunk);
 // The bf16-input contractions of launch_gemm (same arguments; operands

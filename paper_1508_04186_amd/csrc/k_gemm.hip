@@ -309,6 +309,7 @@ hipError_t pair_tn_nnmask(const GemmParams& w, const GemmParams& d, hipStream_t 
 }  // namespace
 
 void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk) {
+    if (rows >= kGemmX6MinRows) return gemm_fwd_split_x6(rows, N, K, ks, kchunk);
     // Enough k-slices that the launch has several hundred workgroups; the
     // head kernel sums the slices.  Past 256 output tiles the launch fills
     // the chip without splitting, and every slice would cost the head a
@@ -362,6 +363,9 @@ hipError_t launch_gemm_fwd2(int M, int N, int K, const float* A0, const float* B
     if (kchunk % 32 != 0 || kslices <= 0 || (x16 && !bf16)) return hipErrorInvalidValue;
     if (bf16) return launch_gemm_bf16_fwd2(M, N, K, A0, B0, C0, A1, B1, C1, lda, ldb, ldc, kslices, kchunk,
                                            c_slice, x16, st);
+    // (the split was chosen for the 2M rows of both sets: gemm_fwd_split)
+    if (2 * M >= kGemmX6MinRows)
+        return launch_gemm_x6_fwd2(M, N, K, A0, B0, C0, A1, B1, C1, lda, ldb, ldc, kslices, kchunk, c_slice, st);
     const GemmParams p0{M, N, K, A0, lda, B0, ldb, C0, ldc, kchunk, c_slice, nullptr};
     const GemmParams p1{M, N, K, A1, lda, B1, ldb, C1, ldc, kchunk, c_slice, nullptr};
     const TileCfg c = fwd_tile(M, kchunk);
@@ -381,8 +385,10 @@ hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int l
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
                        const float* mask, bool bf16, bool x16, hipStream_t st) {
     if (kchunk % 32 != 0 || (x16 && !bf16)) return hipErrorInvalidValue;
-    return bf16 ? launch_gemm_bf16(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, x16, st)
-                : launch_gemm_prec<false>(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+    if (bf16) return launch_gemm_bf16(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, x16, st);
+    if (kind == GEMM_NT && M >= kGemmX6MinRows)
+        return launch_gemm_x6(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
+    return launch_gemm_prec<false>(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
 }
 
 }  // namespace dqn

@@ -1,7 +1,13 @@
-// The fully connected layer contractions of the bf16-input variant (fc1
-// forward with split-K partial sums, fc1 weight gradient, fc1 input gradient
-// with the ReLU mask of the last conv layer): both operands rounded to
-// bfloat16 (nearest-even) as they are staged, fp32 accumulation.
+// The fully connected layer contractions on bf16 MFMA (fc1 forward with
+// split-K partial sums, fc1 weight gradient, fc1 input gradient with the
+// ReLU mask of the last conv layer), fp32 accumulation, in two arithmetics:
+//  - the bf16-input variant: both operands rounded to bfloat16
+//    (nearest-even) as they are staged (PARTS = 1);
+//  - float32: both operands split exactly into three bfloat16 planes
+//    (hi + mid + lo, as the float32 convolutions) as they are staged, and
+//    six products per 32 k-values (hi*hi, hi*mid, mid*hi, hi*lo, mid*mid,
+//    lo*hi; the dropped pairs are below 2^-23 of the product), which keeps
+//    float32 accuracy (PARTS = 3).
 //
 // BMxBN output tiles on WGM x WGN waves, each wave a block of 16x16
 // v_mfma_f32_16x16x32_bf16 tiles, k-stages of BK.  Each operand is staged
@@ -44,6 +50,22 @@ __device__ __forceinline__ uint2 pack4(f4 v) {
     return uint2{a | (b << 16), c | (d << 16)};
 }
 
+// The three exact bf16 planes of four floats, packed as pack4 does.
+__device__ __forceinline__ void split4(f4 v, uint2& h, uint2& m, uint2& l) {
+    uint32_t hh[4], mm[4], ll[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        __bf16 a, b, c;
+        split3(v[i], a, b, c);
+        hh[i] = __builtin_bit_cast(unsigned short, a);
+        mm[i] = __builtin_bit_cast(unsigned short, b);
+        ll[i] = __builtin_bit_cast(unsigned short, c);
+    }
+    h = uint2{hh[0] | (hh[1] << 16), hh[2] | (hh[3] << 16)};
+    m = uint2{mm[0] | (mm[1] << 16), mm[2] | (mm[3] << 16)};
+    l = uint2{ll[0] | (ll[1] << 16), ll[2] | (ll[3] << 16)};
+}
+
 // Element i (0..3) of four bfloat16 values packed in a uint2.
 __device__ __forceinline__ uint32_t half16(uint2 x, int i) { return ((i < 2 ? x.x : x.y) >> (16 * (i & 1))) & 0xffffu; }
 
@@ -51,8 +73,9 @@ __device__ __forceinline__ uint32_t half16(uint2 x, int i) { return ((i < 2 ? x.
 // KCONT: the operand is contiguous along k in memory (element (r, k) at
 // src[r*ld + k]); otherwise along r (element (r, k) at src[k*ld + r]).
 // SRC16: the operand holds bfloat16 values (moved as they are) instead of
-// floats (rounded as they are staged).
-template <int ROWS, int BK, int NT, bool KCONT, bool SRC16 = false>
+// floats (rounded as they are staged).  PARTS = 3: floats split into three
+// planes, plane pl at s + pl * ROWS * RS.
+template <int ROWS, int BK, int NT, bool KCONT, bool SRC16 = false, int PARTS = 1>
 struct Stage {
     static constexpr int KQ = BK / 4;                 // four-value groups along k per row
     static constexpr int NV = ROWS * BK / 4 / NT;     // four-value groups per thread
@@ -88,14 +111,27 @@ struct Stage {
             }
         }
     }
+    // the four values x at row r, k-values k..k+3 of every plane
+    __device__ __forceinline__ static void put(__bf16* s, int off, f4 x) {
+        if constexpr (PARTS == 3) {
+            uint2 h, m, l;
+            split4(x, h, m, l);
+            *(uint2*)&s[off] = h;
+            *(uint2*)&s[off + ROWS * RS] = m;
+            *(uint2*)&s[off + 2 * ROWS * RS] = l;
+        } else {
+            *(uint2*)&s[off] = pack4(x);
+        }
+    }
     __device__ __forceinline__ void store(__bf16* s) const {
         const int t = threadIdx.x;
+        static_assert(PARTS == 1 || !SRC16, "the exact split takes float input");
         if constexpr (KCONT) {
 #pragma unroll
             for (int u = 0; u < NV; ++u) {
                 const int q = t + NT * u, r = q / KQ, k = 4 * (q % KQ);
                 if constexpr (SRC16) *(uint2*)&s[r * RS + k] = v[u];
-                else *(uint2*)&s[r * RS + k] = pack4(v[u]);
+                else put(s, r * RS + k, v[u]);
             }
         } else {
 #pragma unroll
@@ -109,8 +145,7 @@ struct Stage {
                             uint2{half16(v[4 * w], i) | (half16(v[4 * w + 1], i) << 16),
                                   half16(v[4 * w + 2], i) | (half16(v[4 * w + 3], i) << 16)};
                     else
-                        *(uint2*)&s[(r + i) * RS + k] =
-                            pack4(f4{v[4 * w][i], v[4 * w + 1][i], v[4 * w + 2][i], v[4 * w + 3][i]});
+                        put(s, (r + i) * RS + k, f4{v[4 * w][i], v[4 * w + 1][i], v[4 * w + 2][i], v[4 * w + 3][i]});
                 }
             }
         }
@@ -121,24 +156,24 @@ struct Stage {
 // TB: B(k,n) = B[n*ldb + k] else B[k*ldb + n].
 // MASK: C(m,n) = 0 where mask[m*ldc + n] <= 0.
 // A16, B16, M16: A, B or the mask hold bfloat16 values.
+// PARTS: 1 (operands rounded) or 3 (exact split, six products); the stages
+// live at As, Bs (PARTS planes each).
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK, bool A16 = false, bool B16 = false,
-          bool M16 = false>
-__device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z) {
+          bool M16 = false, int PARTS = 1>
+__device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z, __bf16* As, __bf16* Bs) {
     constexpr int NT = 64 * WGM * WGN;
     constexpr int WTM = BM / WGM, WTN = BN / WGN;     // wave tile
     constexpr int TM = WTM / 16, TN = WTN / 16;       // MFMA tiles per wave
     constexpr int RS = BK + 8;
     static_assert(BK % 32 == 0 && WTM % 16 == 0 && WTN % 16 == 0, "tile shape");
-    __shared__ __align__(16) __bf16 As[BM * RS];
-    __shared__ __align__(16) __bf16 Bs[BN * RS];
     const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
     const int kbeg = z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
     const int wm = (wave / WGN) * WTM, wn = (wave % WGN) * WTN;
 
-    Stage<BM, BK, NT, !TA, A16> sa;
-    Stage<BN, BK, NT, TB, B16> sb;
+    Stage<BM, BK, NT, !TA, A16, PARTS> sa;
+    Stage<BN, BK, NT, TB, B16, PARTS> sb;
     f4 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -159,15 +194,32 @@ __device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z) {
         }
 #pragma unroll
         for (int kb = 0; kb < BK / 32; ++kb) {
-            bf16x8 a[TM], b[TN];
+            bf16x8 a[PARTS][TM], b[PARTS][TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) a[i] = *(const bf16x8*)&As[(wm + 16 * i + li) * RS + 32 * kb + 8 * g];
+            for (int pl = 0; pl < PARTS; ++pl) {
 #pragma unroll
-            for (int j = 0; j < TN; ++j) b[j] = *(const bf16x8*)&Bs[(wn + 16 * j + li) * RS + 32 * kb + 8 * g];
+                for (int i = 0; i < TM; ++i)
+                    a[pl][i] = *(const bf16x8*)&As[pl * BM * RS + (wm + 16 * i + li) * RS + 32 * kb + 8 * g];
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+                for (int j = 0; j < TN; ++j)
+                    b[pl][j] = *(const bf16x8*)&Bs[pl * BN * RS + (wn + 16 * j + li) * RS + 32 * kb + 8 * g];
+            }
+            if constexpr (PARTS == 1) {
 #pragma unroll
-                for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x32bf16(a[i], b[j], acc[i][j]);
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x32bf16(a[0][i], b[0][j], acc[i][j]);
+            } else {
+                // the six plane pairs (pa, pb), smallest first; each over all tiles
+                constexpr int PA[6] = {2, 1, 0, 1, 0, 0}, PB[6] = {0, 1, 2, 0, 1, 0};
+#pragma unroll
+                for (int q = 0; q < 6; ++q)
+#pragma unroll
+                    for (int i = 0; i < TM; ++i)
+#pragma unroll
+                        for (int j = 0; j < TN; ++j)
+                            acc[i][j] = mfma16x16x32bf16(a[PA[q]][i], b[PB[q]][j], acc[i][j]);
+            }
         }
         __syncthreads();
     }
@@ -192,9 +244,22 @@ __device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z) {
         }
 }
 
+template <int BM, int BN, int BK>
+constexpr int gemm_lds_bf16(int parts) { return parts * (BM + BN) * (BK + 8); }   // bf16 elements
+
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK, bool A16, bool B16, bool M16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Params p) {
-    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, A16, B16, M16>(p, blockIdx.z);
+    __shared__ __align__(16) __bf16 As[BM * (BK + 8)];
+    __shared__ __align__(16) __bf16 Bs[BN * (BK + 8)];
+    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, A16, B16, M16>(p, blockIdx.z, As, Bs);
+}
+
+// float32 operands, exact three-plane split (stages in dynamic LDS)
+template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_x6_kernel(GemmBf16Params p) {
+    extern __shared__ __align__(16) __bf16 smem_x6[];
+    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, false, false, false, 3>(p, blockIdx.z, smem_x6,
+                                                                              smem_x6 + 3 * BM * (BK + 8));
 }
 
 // Two forward contractions of one shape (the online network on s, the
@@ -202,11 +267,44 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Param
 template <int BM, int BN, int BK, int WGM, int WGN, bool A16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_fwd2_kernel(GemmBf16Params p0, GemmBf16Params p1,
                                                                        int ks0) {
+    __shared__ __align__(16) __bf16 As[BM * (BK + 8)];
+    __shared__ __align__(16) __bf16 Bs[BN * (BK + 8)];
     const int z = blockIdx.z;
     if (z < ks0)
-        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p0, z);
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p0, z, As, Bs);
     else
-        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p1, z - ks0);
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p1, z - ks0, As, Bs);
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_x6_fwd2_kernel(GemmBf16Params p0, GemmBf16Params p1, int ks0) {
+    extern __shared__ __align__(16) __bf16 smem_x6[];
+    __bf16* Bs = smem_x6 + 3 * BM * (BK + 8);
+    const int z = blockIdx.z;
+    if (z < ks0)
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, false, false, false, 3>(p0, z, smem_x6, Bs);
+    else
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, false, false, false, 3>(p1, z - ks0, smem_x6, Bs);
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
+hipError_t gemm_x6_launch(const GemmBf16Params& prm, int kslices, hipStream_t st) {
+    const dim3 grid((unsigned)((prm.M + BM - 1) / BM), (unsigned)((prm.N + BN - 1) / BN), (unsigned)kslices);
+    auto kern = gemm_x6_kernel<BM, BN, BK, WGM, WGN, TA, TB, MASK>;
+    const size_t lds = (size_t)gemm_lds_bf16<BM, BN, BK>(3) * 2;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, grid, dim3(64 * WGM * WGN), lds, st, prm);
+    return hipGetLastError();
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN>
+hipError_t gemm_x6_fwd2_launch(const GemmBf16Params& p0, const GemmBf16Params& p1, int kslices, hipStream_t st) {
+    const dim3 grid((unsigned)((p0.M + BM - 1) / BM), (unsigned)((p0.N + BN - 1) / BN), (unsigned)(2 * kslices));
+    auto kern = gemm_x6_fwd2_kernel<BM, BN, BK, WGM, WGN>;
+    const size_t lds = (size_t)gemm_lds_bf16<BM, BN, BK>(3) * 2;
+    if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, grid, dim3(64 * WGM * WGN), lds, st, p0, p1, kslices);
+    return hipGetLastError();
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN>
@@ -252,6 +350,43 @@ void gemm_fwd_split_bf16(int rows, int N, int K, int* ks, int* kchunk) {
     const int want = (int)std::min<long>(steps, std::max<long>(1, (target + tiles - 1) / tiles));
     *kchunk = (steps + want - 1) / want * 64;
     *ks = (K + *kchunk - 1) / *kchunk;
+}
+
+// The float32 forward's split (from kGemmX6MinRows rows): 128x256 tiles
+// from kBf16BigRows rows, else 64x64, and enough k-slices (of a multiple of
+// 64) for about 256 workgroups (the head sums the slices).
+void gemm_fwd_split_x6(int rows, int N, int K, int* ks, int* kchunk) {
+    const bool big = rows >= kBf16BigRows;
+    const int bm = big ? 128 : 64, bn = big ? 256 : 64;
+    const long tiles = (long)((rows + bm - 1) / bm) * ((N + bn - 1) / bn);
+    const int steps = (K + 63) / 64;
+    const int want = (int)std::min<long>(steps, std::max<long>(1, (256 + tiles - 1) / tiles));
+    *kchunk = (steps + want - 1) / want * 64;
+    *ks = (K + *kchunk - 1) / *kchunk;
+}
+
+hipError_t launch_gemm_x6_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0, const float* A1,
+                               const float* B1, float* C1, int lda, int ldb, int ldc, int kslices, int kchunk,
+                               int64_t c_slice, hipStream_t st) {
+    if (M <= 0 || N <= 0 || K <= 0 || kslices <= 0 || kchunk % 32 != 0 || K % 4) return hipErrorInvalidValue;
+    for (const float* x : {A0, B0, A1, B1})
+        if ((uintptr_t)x % 16) return hipErrorInvalidValue;
+    if (lda % 4 || ldb % 4) return hipErrorInvalidValue;
+    const GemmBf16Params p0{M, N, K, A0, lda, B0, ldb, C0, ldc, kchunk, c_slice, nullptr};
+    const GemmBf16Params p1{M, N, K, A1, lda, B1, ldb, C1, ldc, kchunk, c_slice, nullptr};
+    if (M >= kBf16BigRows) return gemm_x6_fwd2_launch<128, 256, 32, 2, 4>(p0, p1, kslices, st);
+    return gemm_x6_fwd2_launch<64, 64, 64, 2, 2>(p0, p1, kslices, st);
+}
+
+hipError_t launch_gemm_x6(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
+                          float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
+                          hipStream_t st) {
+    if (M <= 0 || N <= 0 || K <= 0 || kslices <= 0 || kchunk % 32 != 0) return hipErrorInvalidValue;
+    if ((uintptr_t)A % 16 || (uintptr_t)B % 16 || lda % 4 || ldb % 4) return hipErrorInvalidValue;
+    if (kind != GEMM_NT || mask || K % 4) return hipErrorInvalidValue;   // the forward only
+    const GemmBf16Params prm{M, N, K, A, lda, B, ldb, C, ldc, kchunk, c_slice, nullptr};
+    if (M >= kBf16BigRows) return gemm_x6_launch<128, 256, 32, 2, 4, false, true, false>(prm, kslices, st);
+    return gemm_x6_launch<64, 64, 64, 2, 2, false, true, false>(prm, kslices, st);
 }
 
 hipError_t launch_gemm_bf16_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0,
