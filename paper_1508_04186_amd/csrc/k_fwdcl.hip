@@ -340,7 +340,8 @@ hipError_t fwd_cl_launch(const float* in, int n_a, int n, const float* w_a, cons
 // (tap, 32 channels), as the bf16 variant), holding those weights' three
 // planes in registers (96 or 108), for every M-tile of the sample.  Each
 // sample's input is split into three bf16 planes staged channels-last in LDS
-// (one 16-byte read per operand and plane); the two halves' sums meet in LDS
+// (one 16-byte read per operand and plane, free of bank conflicts: see
+// FwdX6Geom::slot); the two halves' sums meet in LDS
 // at the end of the sample, where bias and ReLU are applied and the output
 // map is assembled and written as 16-byte vectors.  The next sample's input
 // is read into registers during the MFMAs.
@@ -355,7 +356,15 @@ struct FwdX6Geom {
     static constexpr int KSH = KS / 2;                  // per half
     static constexpr int IP = IH * IH;
     static constexpr int PSB = CIN * 2 + 16;            // bytes per staged pixel and plane
-    static constexpr int PLANE = IP * PSB;
+    // Staged pixel order: stride 2 splits rows and columns by parity, so the
+    // input pixels of consecutive output pixels are consecutive slots; rows
+    // at a pitch of RP slots, RP = OH (mod 16), so the slots of any 16
+    // consecutive output pixels are 16 consecutive values mod 16, and with
+    // PSB / 16 odd a lane group's 16-byte reads hit 16 distinct groups of
+    // four banks.
+    static constexpr int RP = OH + 16;
+    static constexpr int SLOTS = IH * RP;
+    static constexpr int PLANE = SLOTS * PSB;
     static constexpr int IN = CIN * IP;
     static constexpr int ITEMS = (CIN / 8) * IP;        // (8-channel group, pixel) items
     static constexpr int IPER = (ITEMS + FC_WG - 1) / FC_WG;
@@ -363,8 +372,14 @@ struct FwdX6Geom {
     static constexpr int PART = 4 * MT * 64 * 16;       // half-sums of the kh = 1 waves (bytes)
     static constexpr int LDS = 3 * PLANE;
     static constexpr int PACK = 3 * 4 * KS * 64;        // bf16x8 vectors of the repacked planes
-    static_assert(KS % 2 == 0 && CIN % 32 == 0 && PSB % 16 == 0 && OUTF % 4 == 0, "geometry");
+    static_assert(KS % 2 == 0 && CIN % 32 == 0 && PSB % 16 == 0 && (PSB / 16) % 2 == 1 && OUTF % 4 == 0, "geometry");
+    static_assert(S == 1 || (S == 2 && IH % 2 == 0 && IH / 2 <= RP), "stride-phase layout");
+    static_assert(RP >= IH && (RP - OH) % 16 == 0, "row pitch");
     static_assert(PART + OUTF * 4 <= LDS, "half-sums and output map fit in the input planes");
+    // slot of input pixel (y, x); slot(S oy + ky, S ox + kx) = slot(ky, kx) + oy RP + ox
+    __host__ __device__ static constexpr int slot(int y, int x) {
+        return S == 2 ? ((y & 1) * (IH / 2) + (y >> 1)) * RP + (x & 1) * (IH / 2) + (x >> 1) : y * RP + x;
+    }
 };
 
 template <int CIN, int IH, int K, int S, int OH>
@@ -413,6 +428,7 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_x6_kernel(FwdClParams p) {
             const int q = t + u * FC_WG;
             if (q < G::ITEMS) {
                 const int cg = q / G::IP, pix = q - cg * G::IP;
+                const int y = pix / IH, x = pix - y * IH;
                 bf16x8 h, m, l;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
@@ -422,7 +438,7 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_x6_kernel(FwdClParams p) {
                     m[e] = b;
                     l[e] = c;
                 }
-                unsigned char* d = s_in + pix * G::PSB + 16 * cg;
+                unsigned char* d = s_in + G::slot(y, x) * G::PSB + 16 * cg;
                 *(bf16x8*)d = h;
                 *(bf16x8*)(d + G::PLANE) = m;
                 *(bf16x8*)(d + 2 * G::PLANE) = l;
@@ -467,7 +483,7 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_x6_kernel(FwdClParams p) {
         const int pp = 16 * i + li;
         const int pc = pp < G::P ? pp : 0;
         const int oy = pc / OH, ox = pc - oy * OH;
-        pb[i] = ((S * oy) * IH + S * ox) * G::PSB + 16 * g;
+        pb[i] = (oy * G::RP + ox) * G::PSB + 16 * g;
     }
 
     // the k-steps of half KH: per step, the three planes of every M-tile's A
@@ -477,7 +493,7 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_x6_kernel(FwdClParams p) {
 #pragma unroll
         for (int s = 0; s < G::KSH; ++s) {
             const int ks = KH * G::KSH + s, tap = ks / G::CH, cb = ks % G::CH;
-            const int off = ((tap / K) * IH + tap % K) * G::PSB + 64 * cb;
+            const int off = G::slot(tap / K, tap % K) * G::PSB + 64 * cb;
             bf16x8 a[3][G::MT];
 #pragma unroll
             for (int pl = 0; pl < 3; ++pl)
