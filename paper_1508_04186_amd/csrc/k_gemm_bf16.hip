@@ -11,16 +11,20 @@
 //
 // BMxBN output tiles on WGM x WGN waves, each wave a block of 16x16
 // v_mfma_f32_16x16x32_bf16 tiles, k-stages of BK.  Each operand is staged
-// in LDS as bf16 rows of k-values, [mn][BK + 8], so that the eight k-values
-// a lane feeds one MFMA are one 16-byte read; the padded row stride puts
-// the 16 rows a lane group reads in 16 distinct groups of four banks.  An
-// operand contiguous along k in memory is loaded as float4s along k; one
-// contiguous along m or n as 4x4 blocks (four k-rows of four values)
-// transposed in registers, so every LDS store is 8 bytes.  The next stage's
-// global loads are in flight during the current stage's MFMAs.  The tiles
-// are large where the batch is (each operand is re-read once per tile of
-// the other dimension, from L2), and the forward pass splits K so that the
-// launch still covers the chip.
+// in LDS as bf16 rows of BK k-values, so that the eight k-values a lane
+// feeds one MFMA are one 16-byte read.  The 16-byte chunks of a row are
+// permuted by an XOR with a function of the row (lds_off): the 16 rows a
+// lane group reads land in 16 distinct groups of four banks, and so do the
+// rows of the 8-byte stores of a transposed stage (below), which with a
+// padded row stride instead hit four banks sixteen times.  An operand
+// contiguous along k in memory is loaded as float4s along k; one contiguous
+// along m or n as 4x4 blocks (four k-rows of four values) transposed in
+// registers (v_perm_b32 for bf16 values), so every LDS store is 8 bytes.
+// A stage wholly inside the operands is loaded without per-value bounds
+// tests.  The next stage's global loads are in flight during the current
+// stage's MFMAs.  The tiles are large where the batch is (each operand is
+// re-read once per tile of the other dimension, from L2), and the forward
+// pass splits K so that the launch still covers the chip.
 #include <algorithm>
 #include <initializer_list>
 #include <type_traits>
@@ -66,8 +70,18 @@ __device__ __forceinline__ void split4(f4 v, uint2& h, uint2& m, uint2& l) {
     l = uint2{ll[0] | (ll[1] << 16), ll[2] | (ll[3] << 16)};
 }
 
-// Element i (0..3) of four bfloat16 values packed in a uint2.
-__device__ __forceinline__ uint32_t half16(uint2 x, int i) { return ((i < 2 ? x.x : x.y) >> (16 * (i & 1))) & 0xffffu; }
+// Offset (bf16 elements) of k-value k of row `row` in a stage of BK
+// k-values per row: 16-byte chunk k/8 of the row is stored at chunk
+// (k/8) xor f(row).  f takes the row's position within a 256-byte bank line
+// (128/BK rows share one when BK < 128) and the row's block of 16, so that
+// rows 16a..16a+15 (one MFMA operand read) and rows 4l+i, l = 0..15 (one
+// transposed store) each cover distinct chunks of the bank line.
+template <int BK>
+__device__ __forceinline__ int lds_off(int row, int k) {
+    constexpr int CH = BK / 8, RPL = BK >= 128 ? 1 : 128 / BK, FM = (CH < 16 ? CH : 16) - 1;
+    const int f = ((row / RPL) ^ (row >> 4)) & FM;
+    return row * BK + (((k >> 3) ^ f) << 3) + (k & 7);
+}
 
 // One operand's stage: ROWS rows (m or n) x BK k, staged by NT threads.
 // KCONT: the operand is contiguous along k in memory (element (r, k) at
@@ -79,7 +93,7 @@ template <int ROWS, int BK, int NT, bool KCONT, bool SRC16 = false, int PARTS = 
 struct Stage {
     static constexpr int KQ = BK / 4;                 // four-value groups along k per row
     static constexpr int NV = ROWS * BK / 4 / NT;     // four-value groups per thread
-    static constexpr int RS = BK + 8;                 // LDS row stride (bf16)
+    static constexpr int RS = BK;                     // LDS row stride (bf16)
     static_assert(NV * NT * 4 == ROWS * BK && (KCONT || NV % 4 == 0), "stage split");
     using V = std::conditional_t<SRC16, uint2, f4>;
     V v[NV];
@@ -92,23 +106,43 @@ struct Stage {
         else return *(const f4*)(src + off);
     }
     __device__ __forceinline__ void load(const float* __restrict__ src, int ld, int r0, int rlim, int k0, int klim) {
+        if (r0 + ROWS <= rlim && k0 + BK <= klim) load_body<false>(src, ld, r0, rlim, k0, klim);
+        else load_body<true>(src, ld, r0, rlim, k0, klim);
+    }
+    // GUARD: values outside rows < rlim, k < klim read as zero
+    template <bool GUARD>
+    __device__ __forceinline__ void load_body(const float* __restrict__ src, int ld, int r0, int rlim, int k0,
+                                              int klim) {
         const int t = threadIdx.x;
         if constexpr (KCONT) {
+            // value group u: row rt + RP u, k-values kt .. kt+3
+            static_assert(NT % KQ == 0, "rows per pass");
+            constexpr int RP = NT / KQ;
+            const int rt = t / KQ, kt = 4 * (t % KQ);
+            const size_t off0 = (size_t)(r0 + rt) * ld + k0 + kt;
 #pragma unroll
             for (int u = 0; u < NV; ++u) {
-                const int q = t + NT * u, r = q / KQ, k = k0 + 4 * (q % KQ);
-                v[u] = (r0 + r < rlim && k < klim) ? at(src, (size_t)(r0 + r) * ld + k) : zero();
+                if (!GUARD || (r0 + rt + RP * u < rlim && k0 + kt < klim))
+                    v[u] = at(src, off0 + (size_t)(RP * u) * ld);
+                else
+                    v[u] = zero();
             }
         } else {
-            // 4x4 block b: rows 4 (b % (ROWS/4)) .. +3, k-rows 4 (b / (ROWS/4)) .. +3
+            // 4x4 block w: rows rt .. rt+3, k-rows kt + 4 RK w .. +3
+            constexpr int RQ = ROWS / 4;
+            static_assert(NT % RQ == 0, "blocks per pass");
+            constexpr int RK = NT / RQ;
+            const int rt = 4 * (t % RQ), kt = 4 * (t / RQ);
+            const size_t off0 = (size_t)(k0 + kt) * ld + r0 + rt;
 #pragma unroll
-            for (int w = 0; w < NV / 4; ++w) {
-                const int b = t + NT * w;
-                const int r = r0 + 4 * (b % (ROWS / 4)), kb = k0 + 4 * (b / (ROWS / 4));
+            for (int w = 0; w < NV / 4; ++w)
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    v[4 * w + u] = (kb + u < klim && r < rlim) ? at(src, (size_t)(kb + u) * ld + r) : zero();
-            }
+                for (int u = 0; u < 4; ++u) {
+                    if (!GUARD || (k0 + kt + 4 * RK * w + u < klim && r0 + rt < rlim))
+                        v[4 * w + u] = at(src, off0 + (size_t)(4 * RK * w + u) * ld);
+                    else
+                        v[4 * w + u] = zero();
+                }
         }
     }
     // the four values x at row r, k-values k..k+3 of every plane
@@ -130,8 +164,8 @@ struct Stage {
 #pragma unroll
             for (int u = 0; u < NV; ++u) {
                 const int q = t + NT * u, r = q / KQ, k = 4 * (q % KQ);
-                if constexpr (SRC16) *(uint2*)&s[r * RS + k] = v[u];
-                else put(s, r * RS + k, v[u]);
+                if constexpr (SRC16) *(uint2*)&s[lds_off<BK>(r, k)] = v[u];
+                else put(s, lds_off<BK>(r, k), v[u]);
             }
         } else {
 #pragma unroll
@@ -140,12 +174,16 @@ struct Stage {
                 const int r = 4 * (b % (ROWS / 4)), k = 4 * (b / (ROWS / 4));
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    if constexpr (SRC16)
-                        *(uint2*)&s[(r + i) * RS + k] =
-                            uint2{half16(v[4 * w], i) | (half16(v[4 * w + 1], i) << 16),
-                                  half16(v[4 * w + 2], i) | (half16(v[4 * w + 3], i) << 16)};
-                    else
-                        put(s, (r + i) * RS + k, f4{v[4 * w][i], v[4 * w + 1][i], v[4 * w + 2][i], v[4 * w + 3][i]});
+                    if constexpr (SRC16) {
+                        // bf16 value i of four k-rows: halves of packed words picked by v_perm_b32
+                        const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;
+                        const uint2 a = v[4 * w], b = v[4 * w + 1], c = v[4 * w + 2], d = v[4 * w + 3];
+                        *(uint2*)&s[lds_off<BK>(r + i, k)] =
+                            uint2{__builtin_amdgcn_perm(i < 2 ? b.x : b.y, i < 2 ? a.x : a.y, sel),
+                                  __builtin_amdgcn_perm(i < 2 ? d.x : d.y, i < 2 ? c.x : c.y, sel)};
+                    } else {
+                        put(s, lds_off<BK>(r + i, k), f4{v[4 * w][i], v[4 * w + 1][i], v[4 * w + 2][i], v[4 * w + 3][i]});
+                    }
                 }
             }
         }
@@ -164,7 +202,7 @@ __device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z, _
     constexpr int NT = 64 * WGM * WGN;
     constexpr int WTM = BM / WGM, WTN = BN / WGN;     // wave tile
     constexpr int TM = WTM / 16, TN = WTN / 16;       // MFMA tiles per wave
-    constexpr int RS = BK + 8;
+    constexpr int RS = BK;
     static_assert(BK % 32 == 0 && WTM % 16 == 0 && WTN % 16 == 0, "tile shape");
     const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
     const int kbeg = z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
@@ -199,10 +237,10 @@ __device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z, _
             for (int pl = 0; pl < PARTS; ++pl) {
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
-                    a[pl][i] = *(const bf16x8*)&As[pl * BM * RS + (wm + 16 * i + li) * RS + 32 * kb + 8 * g];
+                    a[pl][i] = *(const bf16x8*)&As[pl * BM * RS + lds_off<BK>(wm + 16 * i + li, 32 * kb + 8 * g)];
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    b[pl][j] = *(const bf16x8*)&Bs[pl * BN * RS + (wn + 16 * j + li) * RS + 32 * kb + 8 * g];
+                    b[pl][j] = *(const bf16x8*)&Bs[pl * BN * RS + lds_off<BK>(wn + 16 * j + li, 32 * kb + 8 * g)];
             }
             if constexpr (PARTS == 1) {
 #pragma unroll
@@ -245,12 +283,12 @@ __device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z, _
 }
 
 template <int BM, int BN, int BK>
-constexpr int gemm_lds_bf16(int parts) { return parts * (BM + BN) * (BK + 8); }   // bf16 elements
+constexpr int gemm_lds_bf16(int parts) { return parts * (BM + BN) * BK; }   // bf16 elements
 
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK, bool A16, bool B16, bool M16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Params p) {
-    __shared__ __align__(16) __bf16 As[BM * (BK + 8)];
-    __shared__ __align__(16) __bf16 Bs[BN * (BK + 8)];
+    __shared__ __align__(16) __bf16 As[BM * BK];
+    __shared__ __align__(16) __bf16 Bs[BN * BK];
     gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, A16, B16, M16>(p, blockIdx.z, As, Bs);
 }
 
@@ -259,7 +297,7 @@ template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_x6_kernel(GemmBf16Params p) {
     extern __shared__ __align__(16) __bf16 smem_x6[];
     gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, false, false, false, 3>(p, blockIdx.z, smem_x6,
-                                                                              smem_x6 + 3 * BM * (BK + 8));
+                                                                              smem_x6 + 3 * BM * BK);
 }
 
 // Two forward contractions of one shape (the online network on s, the
@@ -267,8 +305,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_x6_kernel(GemmBf16Params 
 template <int BM, int BN, int BK, int WGM, int WGN, bool A16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_fwd2_kernel(GemmBf16Params p0, GemmBf16Params p1,
                                                                        int ks0) {
-    __shared__ __align__(16) __bf16 As[BM * (BK + 8)];
-    __shared__ __align__(16) __bf16 Bs[BN * (BK + 8)];
+    __shared__ __align__(16) __bf16 As[BM * BK];
+    __shared__ __align__(16) __bf16 Bs[BN * BK];
     const int z = blockIdx.z;
     if (z < ks0)
         gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p0, z, As, Bs);
@@ -279,7 +317,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_fwd2_kernel(GemmBf16
 template <int BM, int BN, int BK, int WGM, int WGN>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_x6_fwd2_kernel(GemmBf16Params p0, GemmBf16Params p1, int ks0) {
     extern __shared__ __align__(16) __bf16 smem_x6[];
-    __bf16* Bs = smem_x6 + 3 * BM * (BK + 8);
+    __bf16* Bs = smem_x6 + 3 * BM * BK;
     const int z = blockIdx.z;
     if (z < ks0)
         gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, false, false, false, 3>(p0, z, smem_x6, Bs);
