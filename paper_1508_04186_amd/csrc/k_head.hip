@@ -175,97 +175,169 @@ __global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
     }
 }
 
-// The TD head for large batches: a workgroup stages both fc2 weight sets in
-// LDS once and its four waves take whole samples (wave w: samples j_lo + w,
-// j_lo + w + 4, ...), lane l owning hidden units l + 64e.  The fc1 slices
-// are summed in slice order, the fc2 outputs with one wave reduction each;
-// no workgroup barrier after the staging.  Same arithmetic per sample as
-// head_td_kernel, in a different association of the hidden-unit sums.
+// Sums over the 64 lanes of a wave of N values per lane, by halving: at
+// the step with lane mask M every lane keeps half of its current list (the
+// lower half if its bit M is clear, else the upper half, padded with zeros)
+// and adds the partner lane's copy of that half.  Each value is summed over
+// the lanes in the same butterfly order as wave_sum (xor 32, 16, ..., 1),
+// with at most N + 6 shuffles in all instead of 6N.  Lane l ends with the sum of
+// value halving_index<N>(l), or of padding where that is -1.
+template <int N, int M>
+__device__ __forceinline__ float halving_step(const float* v, int lane) {
+    if constexpr (M == 0) {
+        return v[0];
+    } else {
+        constexpr int H = (N + 1) / 2;
+        const bool up = (lane & M) != 0;
+        float w[H];
+#pragma unroll
+        for (int i = 0; i < H; ++i) {
+            const float lo = v[i];
+            const float hi = H + i < N ? v[H + i] : 0.f;
+            w[i] = (up ? hi : lo) + __shfl_xor(up ? lo : hi, M, 64);
+        }
+        return halving_step<H, M / 2>(w, lane);
+    }
+}
+
+template <int N>
+__device__ __forceinline__ int halving_index(int lane) {
+    int n = N, base = 0, real = N;
+    for (int m = 32; m >= 1; m >>= 1) {
+        const int h = (n + 1) / 2;
+        if (lane & m) {
+            base += h;
+            real = real > h ? real - h : 0;
+        } else {
+            real = real < h ? real : h;
+        }
+        n = h;
+    }
+    return real > 0 ? base : -1;
+}
+
+// The TD head for large batches: one wave per sample, lane l owning the
+// hidden units 4l + 256e .. +3 (float4 loads and stores).  A workgroup first
+// issues the loads of its first samples' fc1 slices, then stages both fc2
+// weight sets in LDS, so the two are in flight together; slices are summed
+// in slice order, KG of them loaded at once.  The 2A fc2 outputs of a sample are
+// summed over the wave with halving_step; the maximum over a' and Q(s, a)
+// are then read across lanes.  Same arithmetic per sample as head_td_kernel
+// up to the association of the hidden-unit sums.
+constexpr int kHeadWideWaves = 4;
 template <int H, int A>
-__global__ __launch_bounds__(256) void head_td_wide_kernel(HeadTdArgs p, int spg) {
-    constexpr int E = H / 64;
-    extern __shared__ float s_w2[];   // [2][A][H]: W2, then W2t
+__global__ __launch_bounds__(64 * kHeadWideWaves) void head_td_wide_kernel(HeadTdArgs p) {
+    constexpr int E = H / 256, KG = 4;
+    static_assert(H % 256 == 0 && 2 * A <= 64, "head shape");
+    extern __shared__ __align__(16) float s_w2[];   // [2][A][H]: W2, then W2t
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    for (int i = threadIdx.x; i < A * H / 4; i += 256) {
+    const int B = p.B;
+    const int64_t slice = (int64_t)2 * B * H;
+    const int stride = gridDim.x * kHeadWideWaves;
+    int j = blockIdx.x * kHeadWideWaves + w;
+    f4 a[KG][E], b[KG][E];
+    auto load_group = [&](int jj, int z0) {
+#pragma unroll
+        for (int g = 0; g < KG; ++g)
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const bool ok = z0 + g < p.ks;
+                const float* sl = p.fc1p + (int64_t)(z0 + g) * slice + 4 * lane + 256 * e;
+                a[g][e] = ok ? *(const f4*)(sl + (int64_t)jj * H) : f4{0.f, 0.f, 0.f, 0.f};
+                b[g][e] = ok ? *(const f4*)(sl + (int64_t)(B + jj) * H) : f4{0.f, 0.f, 0.f, 0.f};
+            }
+    };
+    if (j < B) load_group(j, 0);
+    for (int i = threadIdx.x; i < A * H / 4; i += 64 * kHeadWideWaves) {
         ((f4*)s_w2)[i] = ((const f4*)p.W2)[i];
         ((f4*)s_w2)[A * H / 4 + i] = ((const f4*)p.W2t)[i];
     }
-    float b1v[E], b1tv[E];
+    f4 b1v[E], b1tv[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        b1v[e] = p.b1[lane + 64 * e];
-        b1tv[e] = p.b1t[lane + 64 * e];
+        b1v[e] = *(const f4*)(p.b1 + 4 * lane + 256 * e);
+        b1tv[e] = *(const f4*)(p.b1t + 4 * lane + 256 * e);
     }
+    const int my = halving_index<2 * A>(lane);
+    const float b2my = my >= 0 && my < A ? p.b2[my] : 0.f;
+    const float b2tmy = my >= A ? p.b2t[my - A] : 0.f;
     __syncthreads();
     const float* W2 = s_w2;
     const float* W2t = s_w2 + A * H;
-    const int B = p.B;
-    const int64_t slice = (int64_t)2 * B * H;
-    const int j_lo = blockIdx.x * spg, j_hi = min(B, j_lo + spg);
-    for (int j = j_lo + w; j < j_hi; j += 4) {
+    for (; j < B; j += stride) {
+        if (j != blockIdx.x * kHeadWideWaves + w) load_group(j, 0);   // (beyond the first pass)
+        f4 zs[E], zn[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) zs[e] = zn[e] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int z0 = 0;;) {
+#pragma unroll
+            for (int g = 0; g < KG; ++g)
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    zs[e] += a[g][e];
+                    zn[e] += b[g][e];
+                }
+            z0 += KG;
+            if (z0 >= p.ks) break;
+            load_group(j, z0);
+        }
         const int act = min(max(p.action[j], 0), A - 1);
         const float r = p.reward[j];
         const bool term = p.terminal[j] != 0;
-        float zs[E], zn[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e) zs[e] = zn[e] = 0.f;
-        for (int z = 0; z < p.ks; ++z) {
-            const float* sl = p.fc1p + (int64_t)z * slice;
-            float a[E], b[E];
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                a[e] = sl[(int64_t)j * H + lane + 64 * e];
-                b[e] = sl[(int64_t)(B + j) * H + lane + 64 * e];
-            }
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                zs[e] += a[e];
-                zn[e] += b[e];
-            }
-        }
-        float hs[E], v[2 * A];
+        f4 hs[E];
+        float v[2 * A];
 #pragma unroll
         for (int k = 0; k < 2 * A; ++k) v[k] = 0.f;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const int h = lane + 64 * e;
+            const int h = 4 * lane + 256 * e;
             zs[e] += b1v[e];
-            hs[e] = fmaxf(zs[e], 0.f);
-            const float hn = fmaxf(zn[e] + b1tv[e], 0.f);
+            f4 hn;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                hs[e][c] = fmaxf(zs[e][c], 0.f);
+                hn[c] = fmaxf(zn[e][c] + b1tv[e][c], 0.f);
+            }
 #pragma unroll
             for (int k = 0; k < A; ++k) {
-                v[k] = fmaf(W2[k * H + h], hs[e], v[k]);
-                v[A + k] = fmaf(W2t[k * H + h], hn, v[A + k]);
+                const f4 wk = *(const f4*)&W2[k * H + h];
+                const f4 wt = *(const f4*)&W2t[k * H + h];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    v[k] = fmaf(wk[c], hs[e][c], v[k]);
+                    v[A + k] = fmaf(wt[c], hn[c], v[A + k]);
+                }
+                // (keeps the compiler from hoisting every weight read at once)
+                if (k % 4 == 3) __builtin_amdgcn_sched_barrier(0);
             }
         }
+        const float sum = halving_step<2 * A, 32>(v, lane);
+        // max over a' of Q(s', a'; theta^-): the lanes holding values A..2A-1
+        float m = my >= A ? sum + b2tmy : -INFINITY;
 #pragma unroll
-        for (int k = 0; k < 2 * A; ++k) v[k] = wave_sum(v[k]);
-        float m = v[A] + p.b2t[0];
-#pragma unroll
-        for (int k = 1; k < A; ++k) m = fmaxf(m, v[A + k] + p.b2t[k]);
+        for (int msk = 32; msk >= 1; msk >>= 1) m = fmaxf(m, __shfl_xor(m, msk, 64));
+        // Q(s, a): read from the lane holding value act
+        const uint64_t at = __ballot(my == act);
+        const float qa = __shfl(sum, __ffsll((unsigned long long)at) - 1, 64) + p.b2[act];
         const float y = term ? r : fmaf(p.gamma, m, r);
-        float qa = v[0] + p.b2[0];
-#pragma unroll
-        for (int k = 1; k < A; ++k) qa = (k == act) ? v[k] + p.b2[k] : qa;
         const float diff = qa - y;
         const float delta = diff / (float)B;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            const int h = lane + 64 * e;
-            p.h1s[(int64_t)j * H + h] = hs[e];
-            p.dz1[(int64_t)j * H + h] = zs[e] > 0.f ? delta * W2[act * H + h] : 0.f;
+            const int h = 4 * lane + 256 * e;
+            const f4 wa = *(const f4*)&W2[act * H + h];
+            f4 d;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) d[c] = zs[e][c] > 0.f ? delta * wa[c] : 0.f;
+            *(f4*)&p.h1s[(int64_t)j * H + h] = hs[e];
+            *(f4*)&p.dz1[(int64_t)j * H + h] = d;
         }
         if (lane == 0) {
             p.delta[j] = delta;
             p.lossj[j] = 0.5f * diff * diff / (float)B;
             if (p.y_out) p.y_out[j] = y;
         }
-        if (p.q_out && lane < A) {
-            float q = v[0];
-#pragma unroll
-            for (int k = 1; k < A; ++k) q = (k == lane) ? v[k] : q;
-            p.q_out[(int64_t)j * A + lane] = q + p.b2[lane];
-        }
+        if (p.q_out && my >= 0 && my < A) p.q_out[(int64_t)j * A + my] = sum + b2my;
     }
 }
 
@@ -581,13 +653,14 @@ constexpr int kHeadWideRows = 1024;
 template <int H, int A>
 hipError_t td_launch(const HeadTdArgs& a, hipStream_t st) {
     if (a.B >= kHeadWideRows) {
-        if (((uintptr_t)a.W2 & 15) || ((uintptr_t)a.W2t & 15)) return hipErrorInvalidValue;
-        const int blocks = std::min(256, (a.B + 3) / 4);
-        const int spg = (a.B + blocks - 1) / blocks;
+        for (const float* x : {a.fc1p, a.b1, a.b1t, a.W2, a.W2t, (const float*)a.h1s, (const float*)a.dz1})
+            if ((uintptr_t)x & 15) return hipErrorInvalidValue;
+        // one sample per wave; beyond 1024 workgroups the waves loop
+        const int blocks = std::min(1024, (a.B + kHeadWideWaves - 1) / kHeadWideWaves);
         constexpr size_t lds = (size_t)2 * A * H * 4;
         auto kern = head_td_wide_kernel<H, A>;
         if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(kern, dim3((unsigned)((a.B + spg - 1) / spg)), dim3(256), lds, st, a, spg);
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * kHeadWideWaves), lds, st, a);
         return hipGetLastError();
     }
     hipLaunchKernelGGL((head_td_kernel<H, A>), dim3((unsigned)a.B), dim3(HT), 0, st, a);
