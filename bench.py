@@ -15,7 +15,8 @@ single-GPU workload):
       batch 256, 1,000,000-transition replay (28 GB), target network
       refreshed every 1,000 steps, SGD.
   4a  large Q-network, epsilon-greedy forward pass (eps 0.05) over 8,192
-      states gathered from the 1,000,000-transition replay.
+      states drawn from the 1,000,000-transition replay (read in place by
+      the first convolution, dqn_forward_replay).
   4b  large Q-network, TD gradient + SGD at batch 2,048 from that replay.
   actor  Alg. 1 closed: 32 Snake games act with the small network
       (epsilon-greedy, annealed epsilon), store into a replay pooled over
@@ -1258,19 +1259,18 @@ def bench_forward(args):
     idx = torch.from_numpy(idx_host).to(dev)
     draws = torch.from_numpy(di.egreedy_draws(B, SEED)).to(dev)
     theta = torch.from_numpy(th0).to(dev)
-    st = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
     q = torch.empty((B, net.n_actions), dtype=torch.float32, device=dev)
     act = torch.empty(B, dtype=torch.int32, device=dev)
     ws = dq.workspace(net, B, dq.DQN_OP_FORWARD, dev)
 
     def run(lo, hi):
         for i in range(lo, hi):
-            dq.replay_gather(rp, idx[i], st)
-            dq.dqn_forward(net, theta, st, float(EPS), draws, q, act, ws=ws)
+            dq.dqn_forward_replay(net, theta, rp, idx[i], float(EPS), draws, q, act, ws=ws)
 
     run(0, W)
     torch.cuda.synchronize()
     work = kernel_work(shape, B, forward_only=True)
+    work.pop("gather")
     bd = prof.breakdown(lambda: run(W, W + nb), nb, list(work))
     dom = max((k for k in bd if k in ROOFLINE_KERNELS), key=lambda k: bd[k][0] * bd[k][1])
     lps = max(1, round(bd[dom][1] / nb))
@@ -1280,7 +1280,7 @@ def bench_forward(args):
     out = base_record(K, W, ms)
     out["config"] = {
         "workload": f"config 4a: large Q-network, epsilon-greedy (eps 0.05) forward pass over 8,192 "
-                    f"states gathered from a 1,000,000-transition device replay, {K} passes "
+                    f"states read in place from a 1,000,000-transition device replay, {K} passes "
                     f"(median of {R} timed runs)"
                     + (", bf16-input MFMA contractions with fp32 accumulation" if bf16 else ""),
         "net": "conv32@8x8/4-conv64@4x4/2-conv64@3x3/1-fc512-fc18", "batch": B,

@@ -171,6 +171,18 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
                 float epsilon, const uint64_t* draws, float* q_out, int32_t* action_out,
                 void* ws, size_t ws_bytes, void* stream);
 
+/* The same forward pass and action choice on states read in place from the
+ * replay memory: state j is phi_i of record i = idx[j], the bytes
+ * replay_gather would copy to s_out[j], read by the first convolution
+ * instead of being copied first.  idx: device int64 [batch] with values in
+ * [0, size-1] (not checked on the device; an out-of-range value reads out of
+ * bounds; replay_gather_validate checks them).  The replay record shape must
+ * equal the network input.  Outputs, epsilon, draws, workspace
+ * (DQN_OP_FORWARD) and errors as dqn_forward. */
+int dqn_forward_replay(const dqn_net* net, const float* theta, const dqn_replay* replay,
+                       const int64_t* idx, int32_t batch, float epsilon, const uint64_t* draws,
+                       float* q_out, int32_t* action_out, void* ws, size_t ws_bytes, void* stream);
+
 /* Worker minibatch gradient (Alg. 1; Eq. (1)):
  *   y_j = r_j                                          if terminal_j,
  *   y_j = r_j + gamma * max_a' Q(s_next_j, a'; theta_target)   otherwise;

@@ -1,7 +1,7 @@
 """MI355X (gfx950) hot path of distributed deep Q-learning (arXiv 1508.04186).
 
 Thin Python binding over libdqn.so: the same entry points as the C ABI in
-include/dqn.h (replay_gather, dqn_forward, dqn_td_gradient, ps_apply_update
+include/dqn.h (replay_gather, dqn_forward, dqn_forward_replay, dqn_td_gradient, ps_apply_update
 and the layout/workspace queries) and include/dqn_train.h (the worker and
 parameter-server loops dqn_train_steps and dqn_train_replicas), with torch
 tensors for device memory and streams.  All arithmetic runs in the library's HIP kernels; there is no CPU
@@ -12,7 +12,7 @@ from .native import (  # noqa: F401
     PS_SGD, PS_RMSPROP, PS_ADAGRAD, DQN_OP_FORWARD, DQN_OP_TD_GRADIENT,
     DqnError, Net, NET_SMALL, NET_LARGE, NET_LARGE_BF16, DQN_FP32, DQN_BF16, Replay,
     lib, lib_path, dqn_param_count, dqn_param_offset, dqn_workspace_bytes,
-    replay_gather, dqn_forward, dqn_td_gradient, dqn_td_gradient_replay, dqn_td_gradient_noalloc,
+    replay_gather, dqn_forward, dqn_forward_replay, dqn_td_gradient, dqn_td_gradient_replay, dqn_td_gradient_noalloc,
     ps_apply_update,
     dqn_status_string,
     workspace, profile_attach, profile_used, profile_set_fusion, KERNEL_NAMES,

@@ -695,24 +695,24 @@ int replay_gather_validate(const dqn_replay* rp, const int64_t* idx, int32_t bat
     return DQN_OK;
 }
 
-int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, int32_t batch,
-                float epsilon, const uint64_t* draws, float* q_out, int32_t* action_out, void* ws,
-                size_t ws_bytes, void* stream) {
-    NetInfo ni;
-    int rc = identify(net, &ni);
-    if (rc != DQN_OK) return rc;
-    if (!theta || !states || batch <= 0 || !ws) return DQN_EINVAL;
+}  // extern "C"
+
+namespace {
+
+// The forward pass of dqn_forward / dqn_forward_replay on layer-0 input in0.
+int forward_impl(const dqn_net* net, const NetInfo& ni, const float* theta, const ConvIn& in0, int32_t batch,
+                 float epsilon, const uint64_t* draws, float* q_out, int32_t* action_out, void* ws,
+                 size_t ws_bytes, hipStream_t st) {
+    if (!theta || batch <= 0 || !ws) return DQN_EINVAL;
     if (!(epsilon >= 0.f && epsilon <= 1.f)) return DQN_EINVAL;
     const double te = std::floor((double)epsilon * 4294967296.0);
     const uint64_t thresh = te >= 4294967296.0 ? 4294967296ull : (uint64_t)te;
     if (thresh > 0 && !draws) return DQN_EINVAL;
-    if (!aligned(ws, 256) || !aligned(theta, 16) || !aligned(states, 16)) return DQN_EINVAL;
+    if (!aligned(ws, 256) || !aligned(theta, 16)) return DQN_EINVAL;
     FwdLayout f = fwd_layout(ni, batch, nullptr);
     if (ws_bytes < f.bytes) return DQN_EWORKSPACE;
     f = fwd_layout(ni, batch, ws);
-    hipStream_t st = (hipStream_t)stream;
     const float* th = theta;
-    const ConvIn in0{states, nullptr, (int64_t)net->in_c * net->in_h * net->in_w, 0};
     const bool fused_fwd = g_fusion.load(std::memory_order_relaxed) && ni.n_conv == 2 && conv_s12_fwd_supported(ni.conv[0], ni.conv[1]) &&
                            batch <= kFuseMaxRows && conv_s12_fwd_aligned(in0);
     if (fused_fwd)
@@ -761,6 +761,37 @@ int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, i
     h.action_out = action_out;
     RUN(DQN_K_HEAD, launch_head_fwd(ni.H, ni.A, h, st));
     return DQN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dqn_forward(const dqn_net* net, const float* theta, const uint8_t* states, int32_t batch,
+                float epsilon, const uint64_t* draws, float* q_out, int32_t* action_out, void* ws,
+                size_t ws_bytes, void* stream) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    if (!states || !aligned(states, 16)) return DQN_EINVAL;
+    const ConvIn in0{states, nullptr, (int64_t)net->in_c * net->in_h * net->in_w, 0};
+    return forward_impl(net, ni, theta, in0, batch, epsilon, draws, q_out, action_out, ws, ws_bytes,
+                        (hipStream_t)stream);
+}
+
+int dqn_forward_replay(const dqn_net* net, const float* theta, const dqn_replay* replay, const int64_t* idx,
+                       int32_t batch, float epsilon, const uint64_t* draws, float* q_out, int32_t* action_out,
+                       void* ws, size_t ws_bytes, void* stream) {
+    NetInfo ni;
+    int rc = identify(net, &ni);
+    if (rc != DQN_OK) return rc;
+    rc = check_replay(replay, false);
+    if (rc != DQN_OK) return rc;
+    if (!idx) return DQN_EINVAL;
+    if (replay->c != net->in_c || replay->h != net->in_h || replay->w != net->in_w) return DQN_EINVAL;
+    const ConvIn in0{replay->frames, idx, replay->record_stride, 0};
+    return forward_impl(net, ni, theta, in0, batch, epsilon, draws, q_out, action_out, ws, ws_bytes,
+                        (hipStream_t)stream);
 }
 
 int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_target,

@@ -386,6 +386,92 @@ __global__ __launch_bounds__(HT) void head_fwd_kernel(HeadFwdArgs p) {
     }
 }
 
+// The forward head for large batches, laid out as head_td_wide_kernel: one
+// wave per state, the A outputs summed over the wave by halving, then the
+// greedy action (lowest index of the maximum, for finite Q) by a wave
+// reduction over (value, index) pairs, replaced by the caller-drawn action
+// where the state explores.
+template <int H, int A>
+__global__ __launch_bounds__(64 * kHeadWideWaves) void head_fwd_wide_kernel(HeadFwdArgs p) {
+    constexpr int E = H / 256, KG = 4;
+    static_assert(H % 256 == 0 && A <= 64, "head shape");
+    extern __shared__ __align__(16) float s_w2[];   // [A][H]
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int B = p.B;
+    const int64_t slice = (int64_t)B * H;
+    const int stride = gridDim.x * kHeadWideWaves;
+    const int j0 = blockIdx.x * kHeadWideWaves + w;
+    f4 a[KG][E];
+    auto load_group = [&](int jj, int z0) {
+#pragma unroll
+        for (int g = 0; g < KG; ++g)
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const float* sl = p.fc1p + (int64_t)(z0 + g) * slice + (int64_t)jj * H + 4 * lane + 256 * e;
+                a[g][e] = z0 + g < p.ks ? *(const f4*)sl : f4{0.f, 0.f, 0.f, 0.f};
+            }
+    };
+    if (j0 < B) load_group(j0, 0);
+    for (int i = threadIdx.x; i < A * H / 4; i += 64 * kHeadWideWaves) ((f4*)s_w2)[i] = ((const f4*)p.W2)[i];
+    f4 b1v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) b1v[e] = *(const f4*)(p.b1 + 4 * lane + 256 * e);
+    const int my = halving_index<A>(lane);
+    const float b2my = my >= 0 ? p.b2[my] : 0.f;
+    __syncthreads();
+    for (int j = j0; j < B; j += stride) {
+        if (j != j0) load_group(j, 0);   // (beyond the first pass)
+        f4 zs[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) zs[e] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int z0 = 0;;) {
+#pragma unroll
+            for (int g = 0; g < KG; ++g)
+#pragma unroll
+                for (int e = 0; e < E; ++e) zs[e] += a[g][e];
+            z0 += KG;
+            if (z0 >= p.ks) break;
+            load_group(j, z0);
+        }
+        float v[A];
+#pragma unroll
+        for (int k = 0; k < A; ++k) v[k] = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int h = 4 * lane + 256 * e;
+            f4 hs;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) hs[c] = fmaxf(zs[e][c] + b1v[e][c], 0.f);
+#pragma unroll
+            for (int k = 0; k < A; ++k) {
+                const f4 wk = *(const f4*)&s_w2[k * H + h];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) v[k] = fmaf(wk[c], hs[c], v[k]);
+                if (k % 8 == 7) __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        const float q = halving_step<A, 32>(v, lane) + b2my;
+        float bq = my >= 0 ? q : -INFINITY;
+        int bi = my >= 0 ? my : A;
+#pragma unroll
+        for (int msk = 32; msk >= 1; msk >>= 1) {
+            const float ov = __shfl_xor(bq, msk, 64);
+            const int oi = __shfl_xor(bi, msk, 64);
+            if (ov > bq || (ov == bq && oi < bi)) {
+                bq = ov;
+                bi = oi;
+            }
+        }
+        int best = bi;
+        if (p.thresh > 0) {
+            const uint64_t d = p.draws[j];
+            if ((d >> 32) < p.thresh) best = (int)(((d & 0xffffffffull) * (uint64_t)A) >> 32);
+        }
+        if (lane == 0 && p.action_out) p.action_out[j] = best;
+        if (p.q_out && my >= 0) p.q_out[(int64_t)j * A + my] = q;
+    }
+}
+
 // Each output's terms are summed in a fixed association, without atomics.
 // Up to 128 samples, finalize_small_kernel below.  Above, two launches:
 //  - sample_partials_kernel: for chunks of 32 samples, the chunk's sums of
@@ -647,9 +733,9 @@ __global__ __launch_bounds__(256) void finalize_wide_kernel(FinalizeArgs a, PsUp
     else emit<MODE>(a, u, dst, s);
 }
 
-// From kHeadWideRows samples on, the wide head on up to 256 workgroups
-// (below, one workgroup per sample is faster).
-constexpr int kHeadWideRows = 1024;
+// From kHeadWideRows samples on, the wide heads (one wave per sample);
+// below, one workgroup per sample is faster.
+constexpr int kHeadWideRows = 128;
 template <int H, int A>
 hipError_t td_launch(const HeadTdArgs& a, hipStream_t st) {
     if (a.B >= kHeadWideRows) {
@@ -669,6 +755,16 @@ hipError_t td_launch(const HeadTdArgs& a, hipStream_t st) {
 
 template <int H, int A>
 hipError_t fwd_launch(const HeadFwdArgs& a, hipStream_t st) {
+    if (a.B >= kHeadWideRows) {
+        for (const float* x : {a.fc1p, a.b1, a.W2})
+            if ((uintptr_t)x & 15) return hipErrorInvalidValue;
+        const int blocks = std::min(1024, (a.B + kHeadWideWaves - 1) / kHeadWideWaves);
+        constexpr size_t lds = (size_t)A * H * 4;
+        auto kern = head_fwd_wide_kernel<H, A>;
+        if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(64 * kHeadWideWaves), lds, st, a);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL((head_fwd_kernel<H, A>), dim3((unsigned)a.B), dim3(HT), 0, st, a);
     return hipGetLastError();
 }

@@ -107,6 +107,10 @@ def lib():
         L.dqn_td_gradient.argtypes = [ctypes.POINTER(_CNet), _P, _P, _P, _P, _P, _P, _P,
                                       ctypes.c_int32, ctypes.c_float, _P, _P, _P, _P, _P,
                                       ctypes.c_size_t, _P]
+        L.dqn_forward_replay.argtypes = [ctypes.POINTER(_CNet), _P, ctypes.POINTER(_CReplay), _P,
+                                         ctypes.c_int32, ctypes.c_float, _P, _P, _P, _P, ctypes.c_size_t,
+                                         _P]
+        L.dqn_forward_replay.restype = ctypes.c_int
         L.dqn_td_gradient_replay.argtypes = [ctypes.POINTER(_CNet), _P, _P, ctypes.POINTER(_CReplay),
                                              _P, ctypes.c_int32, ctypes.c_float, _P, _P, _P, _P,
                                              _P, ctypes.c_size_t, _P]
@@ -297,6 +301,29 @@ def dqn_forward(net, theta, states, epsilon=0.0, draws=None, q_out=None, action_
                            _ptr(action_out, torch.int32, "action_out"),
                            _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream))
     _check(rc, "dqn_forward")
+
+
+def dqn_forward_replay(net, theta, replay: Replay, idx, epsilon=0.0, draws=None, q_out=None,
+                       action_out=None, ws=None, stream=None):
+    """dqn_forward on the states idx (device int64 [B]) read in place from the
+    replay (include/dqn.h dqn_forward_replay)."""
+    import torch
+    B = idx.shape[0]
+    if ws is None:
+        ws = workspace(net, B, DQN_OP_FORWARD, theta.device)
+    if q_out is not None and q_out.numel() < B * net.n_actions:
+        raise ValueError("q_out too small")
+    if action_out is not None and action_out.numel() < B:
+        raise ValueError("action_out too small")
+    if draws is not None and draws.numel() < B:
+        raise ValueError("draws too small")
+    rc = lib().dqn_forward_replay(ctypes.byref(_cnet(net)), _ptr(theta, torch.float32, "theta"),
+                                  ctypes.byref(_creplay(replay)), _ptr(idx, torch.int64, "idx"), B,
+                                  float(epsilon), _ptr(draws, torch.uint64, "draws"),
+                                  _ptr(q_out, torch.float32, "q_out"),
+                                  _ptr(action_out, torch.int32, "action_out"),
+                                  _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream))
+    _check(rc, "dqn_forward_replay")
 
 
 def dqn_td_gradient(net, theta, theta_target, s, s_next, action, reward, terminal, gamma,

@@ -25,7 +25,7 @@ def header_functions(names=None):
 
 def test_header_declares_the_four_calls():
     fns = header_functions(["dqn.h"])
-    for f in ("replay_gather", "dqn_forward", "dqn_td_gradient", "dqn_td_gradient_replay",
+    for f in ("replay_gather", "dqn_forward", "dqn_forward_replay", "dqn_td_gradient", "dqn_td_gradient_replay",
               "ps_apply_update", "dqn_param_count", "dqn_param_offset", "dqn_workspace_bytes", "dqn_status_string"):
         assert f in fns
 
@@ -367,3 +367,32 @@ def test_td_gradient_replay_argument_errors():
     rp.record_stride = 28224
     rp.action = None
     assert call() == dq.DQN_EINVAL                     # side arrays required
+
+
+@fake_ptr_test
+def test_forward_replay_argument_errors():
+    L = dq.lib()
+    n = dq.NET_LARGE
+    ws = dq.dqn_workspace_bytes(n, 8, dq.DQN_OP_FORWARD)
+    rp = native._CReplay()
+    rp.frames, rp.action, rp.reward, rp.terminal = FAKE, None, None, None
+    rp.record_stride, rp.size, rp.c, rp.h, rp.w = 28224, 100, 4, 84, 84
+
+    def call(idx=FAKE, B=8, eps=0.0, draws=None, wsb=ws, **kw):
+        for k, v in kw.items():
+            setattr(rp, k, v)
+        return L.dqn_forward_replay(_cnet(n), FAKE, ctypes.byref(rp), idx, B, ctypes.c_float(eps), draws,
+                                    None, None, FAKE + 2**34, wsb, None)
+    assert call(idx=None) == dq.DQN_EINVAL
+    assert call(B=0) == dq.DQN_EINVAL
+    assert call(wsb=ws - 1) == dq.DQN_EWORKSPACE
+    assert call(eps=1.5) == dq.DQN_EINVAL
+    assert call(eps=0.05) == dq.DQN_EINVAL             # exploring needs draws
+    assert call(c=2) == dq.DQN_EINVAL                  # record shape differs from the input
+    rp.c = 4
+    assert call(size=0) == dq.DQN_EINVAL
+    rp.size = 1                                        # one record is a valid state
+    assert call(record_stride=28230) == dq.DQN_EINVAL
+    rp.record_stride = 28224
+    assert L.dqn_forward_replay(_cnet(n), FAKE, None, FAKE, 8, ctypes.c_float(0.0), None, None, None,
+                                FAKE + 2**34, ws, None) == dq.DQN_EINVAL

@@ -133,8 +133,10 @@ def test_apply_matches_oracle(dev, rule, n):
 # ---------------------------------------------------------------------------
 # dqn_forward
 
-# large 200: the fp32 implicit-GEMM forward of conv2/conv3 (128 to 255 rows)
-@pytest.mark.parametrize("name,batch", [("small", 1), ("small", 45), ("large", 3), ("large", 70), ("large", 200)])
+# large 200: the fp32 implicit-GEMM forward of conv2/conv3 (128 to 255 rows);
+# small 1030: the one-wave-per-state head (from 1,024 states)
+@pytest.mark.parametrize("name,batch", [("small", 1), ("small", 45), ("large", 3), ("large", 70), ("large", 200),
+                                        ("small", 1030)])
 def test_forward_q_and_greedy_actions(dev, name, batch):
     import torch
     net, shape = NETS[name]
@@ -175,6 +177,33 @@ def test_forward_epsilon_greedy(dev, name):
     dq.dqn_forward(net, dev_tensor(th), dev_tensor(st), 1.0, dev_tensor(draws), None, act)
     torch.cuda.synchronize()
     assert np.array_equal(host(act), oracle.select_actions(q_ref, 1.0, draws))
+
+
+@pytest.mark.parametrize("name,B", [("small", 1030), ("large", 77)])
+def test_forward_replay_equals_gather_then_forward(dev, replay, name, B):
+    """Reading the states in place from the replay gives bit-for-bit the
+    Q values and actions of replay_gather followed by dqn_forward."""
+    import torch
+    _, rp = replay
+    net, shape = NETS[name]
+    th = dev_tensor(di.xavier_theta(shape, 120 + B, bias_scale=0.05))
+    idx = np.random.default_rng(B + 1).integers(0, rp.size, B).astype(np.int64)
+    idx[-1] = rp.size - 1   # the last record is a valid state
+    idx = dev_tensor(idx)
+    draws = dev_tensor(di.egreedy_draws(B, 121))
+    eps = float(F32(0.05))
+    say(f"[fwd-replay] net={name} batch={B}: gather + forward")
+    s = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
+    dq.replay_gather(rp, idx, s)
+    q1 = torch.empty((B, net.n_actions), dtype=torch.float32, device=dev)
+    a1 = torch.empty(B, dtype=torch.int32, device=dev)
+    dq.dqn_forward(net, th, s, eps, draws, q1, a1)
+    say(f"[fwd-replay] net={name} batch={B}: in place")
+    q2 = torch.empty_like(q1)
+    a2 = torch.empty_like(a1)
+    dq.dqn_forward_replay(net, th, rp, idx, eps, draws, q2, a2)
+    torch.cuda.synchronize()
+    assert torch.equal(q1, q2) and torch.equal(a1, a2)
 
 
 def test_forward_exact_ties_take_action_zero(dev):
