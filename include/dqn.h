@@ -215,7 +215,8 @@ int dqn_td_gradient(const dqn_net* net, const float* theta, const float* theta_t
  * The batch is limited by that size: when dqn_workspace_bytes(net, batch,
  * DQN_OP_TD_GRADIENT) exceeds 64 MiB the call returns DQN_EWORKSPACE and
  * enqueues nothing.  Every batch up to 289 samples fits for the small
- * network, and every batch up to 94 for the large one (either precision).  The array needs no clearing between calls (every call writes
+ * network, up to 100 for the large one and up to 93 for its bf16-input
+ * variant.  The array needs no clearing between calls (every call writes
  * what it reads).  Every call on one GPU shares that GPU's array: calls that
  * overlap on one GPU (concurrent streams or host threads) race, so serialize
  * them.  The stream must belong to the current device (else DQN_EINVAL).

@@ -152,6 +152,7 @@ struct TdLayout {
     int chunks[3];
     int ks, kchunk;
     float* spart;   // sample-sum chunk slots of the finalize (above 128 samples)
+    __bf16* dz1h;         // dz1 in bfloat16 (bf16-input variant from 128 samples), else null
     float *wpk2, *wpk3;   // repacked conv2/conv3 weights of the input gradients (large network)
     float *fpk[2][2];     // ... the fp32 forward's bf16 planes: [layer conv2, conv3][set theta, theta^-]
     size_t bytes;
@@ -196,6 +197,9 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
             t.fpk[1][w] = cv.take<float>(ws, fwd_x6_pack_floats(CONV_L3));
         }
     }
+    // (from 128 samples, where the fc1 gradients are separate launches; kept
+    // out of smaller workspaces)
+    if (ni.bf16 && B >= 128) t.dz1h = cv.take<__bf16>(ws, (int64_t)B * ni.H);
     t.bytes = cv.off;
     return t;
 }
@@ -445,6 +449,7 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     h.lossj = t.lossj;
     h.q_out = q_out;
     h.y_out = y_out;
+    h.dz1h = t.dz1h;
     RUN(DQN_K_HEAD, launch_head_td(ni.H, ni.A, h, st));
 
     // fc1: weight gradient and the masked gradient of the last conv output;
@@ -459,12 +464,15 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             launch_gemm_wgrad_dgrad(ni.H, ni.flat, B, t.dz1, xlast, grad_out + ni.w_off[L],
                                     th + ni.w_off[L], t.dconv[L - 1], ni.bf16, st));
     } else {
+        // the bf16-input variant reads the head's bfloat16 copy of dz1 (the
+        // same rounding the staging would apply)
+        const float* dzA = t.dz1h ? (const float*)t.dz1h : t.dz1;
         RUN(DQN_K_FC1_WGRAD,
-            launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat,
-                        grad_out + ni.w_off[L], ni.flat, 1, (B + 31) / 32 * 32, 0, nullptr, ni.bf16, a16, st));
+            launch_gemm(GEMM_TN, ni.H, ni.flat, B, dzA, ni.H, xlast, ni.flat, grad_out + ni.w_off[L], ni.flat, 1,
+                        (B + 31) / 32 * 32, 0, nullptr, ni.bf16, a16, st, t.dz1h != nullptr));
         RUN(DQN_K_FC1_DGRAD,
-            launch_gemm(GEMM_NN, B, ni.flat, ni.H, t.dz1, ni.H, th + ni.w_off[L], ni.flat,
-                        t.dconv[L - 1], ni.flat, 1, (ni.H + 31) / 32 * 32, 0, xlast, ni.bf16, a16, st));
+            launch_gemm(GEMM_NN, B, ni.flat, ni.H, dzA, ni.H, th + ni.w_off[L], ni.flat, t.dconv[L - 1], ni.flat, 1,
+                        (ni.H + 31) / 32 * 32, 0, xlast, ni.bf16, a16, st, t.dz1h != nullptr));
     }
     // The small network's conv layers in one launch: conv2's weight gradient,
     // and conv2's input gradient with conv1's weight gradient per (sample,

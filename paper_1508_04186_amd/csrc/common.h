@@ -368,13 +368,14 @@ void gemm_fwd_split_bf16(int rows, int N, int K, int* ks, int* kchunk);
 // The bf16-input contractions of launch_gemm (same arguments; operands
 // rounded to bfloat16 as they are staged).
 // x16 (bf16 only): the activation operand -- A of GEMM_NT, B of GEMM_TN, the
-// mask of GEMM_NN -- holds bfloat16 values.
+// mask of GEMM_NN -- holds bfloat16 values.  a16 (bf16 only, GEMM_TN and
+// GEMM_NN): so does A, the pre-activation gradient.
 hipError_t launch_gemm_bf16(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
                             float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
-                            bool x16, hipStream_t st);
+                            bool x16, hipStream_t st, bool a16 = false);
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
-                       const float* mask, bool bf16, bool x16, hipStream_t st);
+                       const float* mask, bool bf16, bool x16, hipStream_t st, bool a16 = false);
 // Two fc1 forward contractions of one shape in one launch (GEMM_NT, split-K
 // as above): C0 = A0 B0^T and C1 = A1 B1^T, each in its own k-slices.
 hipError_t launch_gemm_bf16_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0,
@@ -399,6 +400,7 @@ struct HeadTdArgs {
     const uint8_t* terminal;
     float gamma;
     float *h1s, *dz1, *delta, *lossj, *q_out, *y_out;
+    __bf16* dz1h;        // when set, dz1 rounded to bfloat16 (nearest even) as well
 };
 hipError_t launch_head_td(int H, int A, const HeadTdArgs& a, hipStream_t st);
 

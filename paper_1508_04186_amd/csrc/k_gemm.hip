@@ -383,9 +383,10 @@ hipError_t launch_gemm_fwd2(int M, int N, int K, const float* A0, const float* B
 
 hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B,
                        int ldb, float* C, int ldc, int kslices, int kchunk, int64_t c_slice,
-                       const float* mask, bool bf16, bool x16, hipStream_t st) {
-    if (kchunk % 32 != 0 || (x16 && !bf16)) return hipErrorInvalidValue;
-    if (bf16) return launch_gemm_bf16(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, x16, st);
+                       const float* mask, bool bf16, bool x16, hipStream_t st, bool a16) {
+    if (kchunk % 32 != 0 || ((x16 || a16) && !bf16)) return hipErrorInvalidValue;
+    if (bf16)
+        return launch_gemm_bf16(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, x16, st, a16);
     if (kind == GEMM_NT && M >= kGemmX6MinRows)
         return launch_gemm_x6(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
     return launch_gemm_prec<false>(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);

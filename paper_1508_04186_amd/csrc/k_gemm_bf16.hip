@@ -359,11 +359,26 @@ hipError_t gemm_bf16_fwd2_launch(const GemmBf16Params& p0, const GemmBf16Params&
 }
 
 // x16: the activation operand (A of the forward, B of the weight gradient,
-// the mask of the input gradient) holds bfloat16 values.
+// the mask of the input gradient) holds bfloat16 values.  a16: A of the
+// weight or input gradient (the pre-activation gradient) holds bfloat16
+// values.
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
-hipError_t gemm_bf16_launch(const GemmBf16Params& prm, int kslices, bool x16, hipStream_t st) {
+hipError_t gemm_bf16_launch(const GemmBf16Params& prm, int kslices, bool x16, hipStream_t st, bool a16 = false) {
     const dim3 grid((unsigned)((prm.M + BM - 1) / BM), (unsigned)((prm.N + BN - 1) / BN), (unsigned)kslices);
     constexpr bool FWD = !TA && TB && !MASK, WGR = TA && !TB && !MASK;
+    if (a16) {
+        if constexpr (WGR || MASK) {
+            if (x16)
+                hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, TA, TB, MASK, true, WGR, MASK>), grid,
+                                   dim3(64 * WGM * WGN), 0, st, prm);
+            else
+                hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, TA, TB, MASK, true, false, false>), grid,
+                                   dim3(64 * WGM * WGN), 0, st, prm);
+            return hipGetLastError();
+        } else {
+            return hipErrorInvalidValue;
+        }
+    }
     if (x16)
         hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WGM, WGN, TA, TB, MASK, FWD, WGR, MASK>), grid,
                            dim3(64 * WGM * WGN), 0, st, prm);
@@ -442,10 +457,11 @@ hipError_t launch_gemm_bf16_fwd2(int M, int N, int K, const float* A0, const flo
 
 hipError_t launch_gemm_bf16(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
                             float* C, int ldc, int kslices, int kchunk, int64_t c_slice, const float* mask,
-                            bool x16, hipStream_t st) {
+                            bool x16, hipStream_t st, bool a16) {
     if (M <= 0 || N <= 0 || K <= 0 || kslices <= 0 || kchunk % 32 != 0) return hipErrorInvalidValue;
     if ((uintptr_t)A % 16 || (uintptr_t)B % 16 || lda % 4 || ldb % 4) return hipErrorInvalidValue;
     const GemmBf16Params prm{M, N, K, A, lda, B, ldb, C, ldc, kchunk, c_slice, mask};
+    if (a16 && kind == GEMM_NT) return hipErrorInvalidValue;
     switch (kind) {
         case GEMM_NT:
             if (K % 4) return hipErrorInvalidValue;
@@ -453,11 +469,12 @@ hipError_t launch_gemm_bf16(GemmKind kind, int M, int N, int K, const float* A, 
             return gemm_bf16_launch<64, 64, 128, 2, 2, false, true, false>(prm, kslices, x16, st);
         case GEMM_TN:
             if (M % 4 || N % 4) return hipErrorInvalidValue;
-            return gemm_bf16_launch<64, 64, 128, 2, 2, true, false, false>(prm, kslices, x16, st);
+            return gemm_bf16_launch<64, 64, 128, 2, 2, true, false, false>(prm, kslices, x16, st, a16);
         case GEMM_NN:
             if (!mask || K % 4 || N % 4) return hipErrorInvalidValue;
-            if (M >= kBf16BigRows) return gemm_bf16_launch<128, 128, 64, 2, 4, false, false, true>(prm, kslices, x16, st);
-            return gemm_bf16_launch<64, 64, 128, 2, 2, false, false, true>(prm, kslices, x16, st);
+            if (M >= kBf16BigRows)
+                return gemm_bf16_launch<128, 128, 64, 2, 4, false, false, true>(prm, kslices, x16, st, a16);
+            return gemm_bf16_launch<64, 64, 128, 2, 2, false, false, true>(prm, kslices, x16, st, a16);
         default: return hipErrorInvalidValue;
     }
 }

@@ -159,8 +159,10 @@ __global__ __launch_bounds__(HT) void head_td_kernel(HeadTdArgs p) {
         float wa = w2[0][e];
 #pragma unroll
         for (int k = 1; k < A; ++k) wa = (k == act) ? w2[k][e] : wa;
+        const float d = zs[e] > 0.f ? delta * wa : 0.f;
         p.h1s[(int64_t)j * H + h] = hs[e];
-        p.dz1[(int64_t)j * H + h] = zs[e] > 0.f ? delta * wa : 0.f;
+        p.dz1[(int64_t)j * H + h] = d;
+        if (p.dz1h) p.dz1h[(int64_t)j * H + h] = (__bf16)d;
     }
     if (threadIdx.x == 0) {
         p.delta[j] = delta;
@@ -331,6 +333,12 @@ __global__ __launch_bounds__(64 * kHeadWideWaves) void head_td_wide_kernel(HeadT
             for (int c = 0; c < 4; ++c) d[c] = zs[e][c] > 0.f ? delta * wa[c] : 0.f;
             *(f4*)&p.h1s[(int64_t)j * H + h] = hs[e];
             *(f4*)&p.dz1[(int64_t)j * H + h] = d;
+            if (p.dz1h) {
+                uint32_t u[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) u[c] = __builtin_bit_cast(unsigned short, (__bf16)d[c]);
+                *(uint2*)&p.dz1h[(int64_t)j * H + h] = uint2{u[0] | (u[1] << 16), u[2] | (u[3] << 16)};
+            }
         }
         if (lane == 0) {
             p.delta[j] = delta;

@@ -396,3 +396,13 @@ def test_forward_replay_argument_errors():
     rp.record_stride = 28224
     assert L.dqn_forward_replay(_cnet(n), FAKE, None, FAKE, 8, ctypes.c_float(0.0), None, None, None,
                                 FAKE + 2**34, ws, None) == dq.DQN_EINVAL
+
+
+@pytest.mark.parametrize("net,limit", [(dq.NET_SMALL, 289), (dq.NET_LARGE, 100), (dq.NET_LARGE_BF16, 93)])
+def test_noalloc_batch_limits_match_the_header(net, limit):
+    """dqn_td_gradient_noalloc runs in a 64 MiB static workspace: every batch
+    up to the limit that include/dqn.h states fits it, the next does not."""
+    cap = 64 * 2**20
+    sizes = [dq.dqn_workspace_bytes(net, b, dq.DQN_OP_TD_GRADIENT) for b in range(1, limit + 2)]
+    assert all(0 < s <= cap for s in sizes[:limit])
+    assert sizes[limit] > cap
