@@ -487,6 +487,13 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
                                 t.wpart[0], t.bpart[0], st));
         chunks0 = conv_s12_bwd_slots(B);
     }
+    // The bf16-input variant of the large network carries conv1's output
+    // gradient in bfloat16 (the rounding its weight gradient applies anyway);
+    // conv2's input-gradient kernel then also sums conv1's bias gradient
+    // from the float32 values, in the same per-workgroup slots.
+    const bool dz16_0 = !fused_bwd && ni.bf16 && a16 && L == 3 && conv1_u8(ni.conv[0], B, true) &&
+                        conv_s12_fwd_aligned(s0) && phase_dgrad(ni.conv[1], B, true) &&
+                        conv2_dgrad_phase_blocks(B) == conv1_u8_wgrad_slots(B);
     for (int l = L - 1; l >= 0 && !fused_bwd; --l) {
         const ConvIn in = l == 0 ? s0 : ConvIn{t.act[l - 1], nullptr, act_elems(ni.d[l - 1]) * 4, 0};
         const float scale = l == 0 ? (float)(1.0 / 255.0) : 1.f;
@@ -498,7 +505,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
         }
         if (l == 0 && conv1_u8(ni.conv[0], B, ni.bf16) && conv_s12_fwd_aligned(s0)) {
             RUN(DQN_K_CONV1_WGRAD,
-                launch_conv1_u8_wgrad(CONV_L1, s0, t.dconv[0], B, t.wpart[0], t.bpart[0], scale, ni.bf16, st));
+                launch_conv1_u8_wgrad(CONV_L1, s0, t.dconv[0], B, t.wpart[0], t.bpart[0], scale, ni.bf16, st,
+                                      dz16_0));
             chunks_used[0] = conv1_u8_wgrad_slots(B);
         } else if (reg_wgrad(ni.conv[l], B, ni.bf16)) {
             RUN(DQN_K_CONV1_WGRAD + l,
@@ -519,7 +527,9 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             RUN(DQN_K_CONV2_DGRAD + (l - 1),
                 ni.conv[l] == CONV_L2
                     ? launch_conv2_dgrad_phase(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
-                                               ni.bf16, a16, repack ? t.wpk2 : nullptr, st)
+                                               ni.bf16, a16, repack ? t.wpk2 : nullptr, st,
+                                               dz16_0 ? (__bf16*)t.dconv[0] : nullptr,
+                                               dz16_0 ? t.bpart[0] : nullptr)
                     : launch_conv3_dgrad(t.dconv[l], th + ni.w_off[l], t.act[l - 1], t.dconv[l - 1], B,
                                          ni.bf16, a16, repack ? t.wpk3 : nullptr, st));
         else if (l > 0 && igemm_dgrad(ni.conv[l], B, ni.bf16))

@@ -260,8 +260,15 @@ hipError_t launch_conv_igemm_dgrad(ConvId id, const float* dz, const float* w, c
 // registers and dz staged in LDS with a zero border.
 // wpk (NULL: read W directly): the weights repacked by launch_weight_repack
 // (d2/d3 for fp32, h2/h3 for bf16), which the workgroups load coalesced.
+// din16 (bf16 only; then din is unused): the input gradient is written
+// rounded to bfloat16 there, and workgroup b's per-channel sums of the
+// float32 values (conv1's bias-gradient partials) to bpart[b][32], for
+// conv2_dgrad_phase_blocks(n) workgroups, each a run of consecutive samples
+// as conv1_u8_wgrad_slots.
+int conv2_dgrad_phase_blocks(int n);
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
-                                    bool bf16, bool h16, const float* wpk, hipStream_t st);
+                                    bool bf16, bool h16, const float* wpk, hipStream_t st,
+                                    __bf16* din16 = nullptr, float* bpart = nullptr);
 
 // Input gradient of CONV_L3 for n samples, masked by [h_in > 0], in the same
 // arrangement (weights in registers, zero-bordered dz in LDS, the sample's
@@ -317,9 +324,11 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
 // samples: conv1_u8_wgrad_slots(n) partial-sum slots of wpart
 // [slots][cout][256] and bpart [slots][cout]; input 16-byte aligned, dz
 // [n][cout][20][20].
+// dz16 (bf16 only): dz holds bfloat16 values, and the bias partial sums are
+// left to the producer of dz (bpart is not written).
 int conv1_u8_wgrad_slots(int n);
 hipError_t launch_conv1_u8_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
-                                 float* bpart, float in_scale, bool bf16, hipStream_t st);
+                                 float* bpart, float in_scale, bool bf16, hipStream_t st, bool dz16 = false);
 
 // Weight and bias gradient partial sums over sample chunks:
 // wpart [chunks][cout][cin*k*k], bpart [chunks][cout].

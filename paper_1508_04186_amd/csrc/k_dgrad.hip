@@ -47,6 +47,8 @@ struct Dgrad2Params {
     float* din;         // [n][32][20][20]
     int n, spg;         // samples, samples per workgroup
     const float* wpk;   // the weights in per-lane order (weight_repack), or NULL
+    __bf16* din16;      // conv2 bf16 kernel: when set, din is written here rounded to bfloat16 instead,
+    float* bpart;       // ... and the workgroup's per-channel sums of the float32 din to bpart[block][32]
 };
 
 // Four consecutive values of the layer input h_in (the ReLU mask source) at
@@ -154,6 +156,9 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
         }
     };
 
+    float bsum[D2_OUT4];
+#pragma unroll
+    for (int u = 0; u < D2_OUT4; ++u) bsum[u] = 0.f;
     fetch(j_lo);
     for (int j = j_lo; j < j_hi; ++j) {
         __syncthreads();  // the zero fill, or the previous round's LDS reads, are done
@@ -212,8 +217,38 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
                 f4 o;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) o[k] = mreg[u].pos(k) ? d[k] : 0.f;
-                *(f4*)(p.din + o0 + 4 * e4) = o;
+                if (p.din16) {
+                    bsum[u] += (o[0] + o[1]) + (o[2] + o[3]);
+                    uint32_t hb[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) hb[k] = __builtin_bit_cast(unsigned short, (__bf16)o[k]);
+                    *(uint2*)(p.din16 + o0 + 4 * e4) = uint2{hb[0] | (hb[1] << 16), hb[2] | (hb[3] << 16)};
+                } else {
+                    *(f4*)(p.din + o0 + 4 * e4) = o;
+                }
             }
+        }
+    }
+    if (p.din16) {
+        // channel c's sum over its 100 float4 groups (400 pixels), each
+        // summed over this workgroup's samples in sample order: four lanes
+        // take 25 consecutive groups each, then ((l0 + l1) + (l2 + l3))
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < D2_OUT4; ++u) {
+            const int e4 = t + u * D2_WG;
+            if (e4 < D2_IN / 4) s_din[e4] = bsum[u];
+        }
+        __syncthreads();
+        constexpr int G = D2_IH * D2_IH / 4, GL = G / 4;
+        static_assert(G % 4 == 0 && 4 * D2_CIN <= D2_WG, "four lanes per channel");
+        if (t < 4 * D2_CIN) {
+            const float* src = s_din + (t >> 2) * G + (t & 3) * GL;
+            float sum = 0.f;
+            for (int q = 0; q < GL; ++q) sum += src[q];
+            sum += __shfl_xor(sum, 1, 64);
+            sum += __shfl_xor(sum, 2, 64);
+            if ((t & 3) == 0) p.bpart[(size_t)blockIdx.x * D2_CIN + (t >> 2)] = sum;
         }
     }
 }
@@ -804,13 +839,20 @@ hipError_t launch_conv3_dgrad(const float* dz, const float* w, const float* h_in
     return hipGetLastError();
 }
 
+int conv2_dgrad_phase_blocks(int n) {
+    const int spg = std::max(1, (n + 255) / 256);
+    return (n + spg - 1) / spg;
+}
+
 hipError_t launch_conv2_dgrad_phase(const float* dz, const float* w, const float* h_in, float* din, int n,
-                                    bool bf16, bool h16, const float* wpk, hipStream_t st) {
-    if (n <= 0 || ((uintptr_t)h_in & 15) || ((uintptr_t)din & 15) || (h16 && !bf16)) return hipErrorInvalidValue;
+                                    bool bf16, bool h16, const float* wpk, hipStream_t st, __bf16* din16,
+                                    float* bpart) {
+    if (n <= 0 || ((uintptr_t)h_in & 15) || (h16 && !bf16)) return hipErrorInvalidValue;
+    if (din16 ? (!bf16 || !bpart || ((uintptr_t)din16 & 15)) : ((uintptr_t)din & 15)) return hipErrorInvalidValue;
     // about one workgroup per CU, one sample per round
     const int spg = std::max(1, (n + 255) / 256);
     const int blocks = (n + spg - 1) / spg;
-    const Dgrad2Params prm{dz, w, h_in, din, n, spg, wpk};
+    const Dgrad2Params prm{dz, w, h_in, din, n, spg, wpk, din16, bpart};
     const dim3 grid((unsigned)blocks), blk(D2_WG);
     if (bf16 && h16 && wpk) hipLaunchKernelGGL((conv2_dgrad_cl_kernel<true, true>), grid, blk, 0, st, prm);
     else if (bf16 && h16) hipLaunchKernelGGL((conv2_dgrad_cl_kernel<true, false>), grid, blk, 0, st, prm);

@@ -886,19 +886,22 @@ constexpr size_t uw_lds(int cout, int parts) { return (size_t)parts * cout * UW_
 
 struct U8WgradParams {
     ConvIn in;            // network input (bytes)
-    const float* dz;      // [n][COUT][20][20]
+    const float* dz;      // [n][COUT][20][20] (bfloat16 values with DZ16)
     int n, spb;
     float* wpart;         // [blocks][COUT][256]
     float* bpart;         // [blocks][COUT]
     float in_scale;
 };
 
-template <int COUT, int PARTS>
+// DZ16: dz arrives rounded to bfloat16 (bf16-input variant) and is staged as
+// it is; the bias partial sums then come from dz's producer.
+template <int COUT, int PARTS, bool DZ16 = false>
 __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) {
     constexpr int MT = COUT / 16;
     constexpr int RPW = COUT / 8;                      // dz rows staged per wave
-    constexpr int CPR = UW_P / 4;                      // f4 chunks per dz row (100)
+    constexpr int CPR = UW_P / 4;                      // four-value chunks per dz row (100)
     static_assert(PARTS == 1 || PARTS == 3, "exact split or bf16 rounding");
+    static_assert(!DZ16 || PARTS == 1, "bfloat16 dz is one plane");
     static_assert(KW1 == 16 * 16 && COUT % 16 == 0, "16 N-tiles of weight columns, 2 per wave");
     extern __shared__ __align__(16) unsigned char smem[];
     __bf16* s_dz = (__bf16*)smem;                                   // [PARTS][COUT][UW_LDZ]
@@ -917,16 +920,21 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
 
     // next sample in registers: dz rows wave*RPW .. +RPW-1 (chunks lane, lane + 64),
     // and the 20-byte column blocks of the phase items
-    f4 vdz[RPW][2];
+    std::conditional_t<DZ16, uint2, f4> vdz[RPW][2];
     uint32_t vb[UW_IPER][5];
     auto load = [&](int j) {
-        const float* dzj = p.dz + (size_t)j * COUT * UW_P;
+        const size_t dzj = (size_t)j * COUT * UW_P;
 #pragma unroll
         for (int q = 0; q < RPW; ++q)
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int ch = lane + 64 * h;
-                if (ch < CPR) vdz[q][h] = *(const f4*)(dzj + (wave * RPW + q) * UW_P + 4 * ch);
+                const size_t off = dzj + (wave * RPW + q) * UW_P + 4 * ch;
+                if constexpr (DZ16) {
+                    if (ch < CPR) vdz[q][h] = *(const uint2*)((const __bf16*)p.dz + off);
+                } else {
+                    if (ch < CPR) vdz[q][h] = *(const f4*)(p.dz + off);
+                }
             }
         const unsigned char* src = sample_ptr(p.in, j);
 #pragma unroll
@@ -951,7 +959,10 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int ch = lane + 64 * h;
-                if (ch < CPR) {
+                if constexpr (DZ16) {
+                    if (ch < CPR) *(uint2*)(s_dz + o * UW_LDZ + 4 * ch) = vdz[q][h];
+                    continue;
+                } else if (ch < CPR) {
                     const f4 v = vdz[q][h];
                     part += (v[0] + v[1]) + (v[2] + v[3]);
                     bf16x4 hv, mv, lv;
@@ -970,7 +981,7 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
                     }
                 }
             }
-            bs[q] += wave_sum(part);
+            if constexpr (!DZ16) bs[q] += wave_sum(part);
         }
         // phase word (row, kx, block qb) = bytes 16 qb + 4e + kx, e < 4, of the row
 #pragma unroll
@@ -1049,7 +1060,7 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
 #pragma unroll
             for (int r = 0; r < 4; ++r)
                 wp[(size_t)(m * 16 + 4 * g + r) * KW1 + (2 * wave + n) * 16 + li] = acc[m][n][r] * p.in_scale;
-    if (lane == 0) {
+    if (!DZ16 && lane == 0) {
 #pragma unroll
         for (int q = 0; q < RPW; ++q) p.bpart[(size_t)blockIdx.x * COUT + wave * RPW + q] = bs[q];
     }
@@ -1063,8 +1074,9 @@ int conv1_u8_wgrad_slots(int n) {
 }
 
 hipError_t launch_conv1_u8_wgrad(ConvId id, const ConvIn& in, const float* dz, int n, float* wpart,
-                                 float* bpart, float in_scale, bool bf16, hipStream_t st) {
+                                 float* bpart, float in_scale, bool bf16, hipStream_t st, bool dz16) {
     if (n <= 0 || !conv_s12_fwd_aligned(in) || in.off != 0 || ((uintptr_t)dz & 15)) return hipErrorInvalidValue;
+    if (dz16 && (!bf16 || id != CONV_L1)) return hipErrorInvalidValue;
     const int spb = std::max(1, (n + UW_TARGET_BLOCKS - 1) / UW_TARGET_BLOCKS);
     const int blocks = (n + spb - 1) / spb;
     const U8WgradParams prm{in, dz, n, spb, wpart, bpart, in_scale};
@@ -1074,6 +1086,7 @@ hipError_t launch_conv1_u8_wgrad(ConvId id, const ConvIn& in, const float* dz, i
         hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(UW_WG), lds, st, prm);
         return hipGetLastError();
     };
+    if (id == CONV_L1 && dz16) return go(conv1_u8_wgrad_kernel<32, 1, true>, 32, 1);
     if (id == CONV_L1) return bf16 ? go(conv1_u8_wgrad_kernel<32, 1>, 32, 1) : go(conv1_u8_wgrad_kernel<32, 3>, 32, 3);
     if (id == CONV_S1) return bf16 ? go(conv1_u8_wgrad_kernel<16, 1>, 16, 1) : go(conv1_u8_wgrad_kernel<16, 3>, 16, 3);
     return hipErrorInvalidValue;
