@@ -649,11 +649,18 @@ hipError_t launch_conv_s12_bwd(const ConvIn& in, const float* act1, const float*
 // many samples: a workgroup splits its weights into three bf16 planes once
 // (exact, as above; PARTS = 3), or rounds them to one bf16 plane (the
 // bf16-input variant; PARTS = 1), then walks its samples with the next
-// sample's bytes loaded into registers while the current one is computed.  Each wave runs
-// its M-tiles (16 pixels) for every N-tile as independent accumulator
-// chains; the A operand is converted from the staged bytes as it is built.
+// sample's bytes loaded into registers while the current one is computed.
+// Each sample is staged in LDS already converted to bfloat16 (exact for
+// bytes), once per byte, so an A operand (eight consecutive bytes of one
+// input row) is two 8-byte LDS reads; converting in the MFMA loop had
+// converted every byte four times (the 8x8 windows at stride 4 overlap) and
+// left the loop bound by that VALU work.  Eight waves, one workgroup per
+// compute unit; M-tile (16 pixels) m goes to wave m mod 8, and each wave runs
+// its M-tiles for every N-tile as independent accumulator chains.
 namespace dqn {
 namespace {
+
+constexpr int U8F_WG = 512;
 
 struct U8FwdParams {
     ConvIn in_a, in_b;
@@ -663,19 +670,24 @@ struct U8FwdParams {
     SideFields side;
 };
 
+constexpr size_t u8f_lds(int cout, int parts) {
+    return (size_t)C0 * H0 * H0 * 2 + (size_t)parts * cout * RS1 * 2 + (size_t)cout * 4;
+}
+
 template <int COUT, int PARTS, bool OUT16>
-__global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
+__global__ __launch_bounds__(U8F_WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
     constexpr int REC = C0 * H0 * H0;            // bytes per sample (28,224)
     constexpr int RV = REC / 16;                 // 16-byte units (1,764)
-    constexpr int RPER = (RV + WG - 1) / WG;     // per thread (7)
+    constexpr int RPER = (RV + U8F_WG - 1) / U8F_WG;   // per thread (4)
     constexpr int NT = COUT / 16;
     constexpr int MT = H1 * H1 / 16;             // 25 M-tiles per sample
-    constexpr int MPW = (MT + 3) / 4;            // M-tiles per wave, at most (7)
+    constexpr int NW = U8F_WG / 64;              // waves (8)
+    constexpr int MPW = (MT + NW - 1) / NW;      // M-tiles per wave, at most (4)
     constexpr int PL = COUT * RS1;               // bf16 per weight plane
-    static_assert(REC % 16 == 0 && (H1 * H1) % 16 == 0, "whole tiles");
+    static_assert(REC % 16 == 0 && (H1 * H1) % 16 == 0 && (H0 * 2) % 8 == 0, "whole tiles, 8-byte rows");
     extern __shared__ __align__(16) unsigned char smem[];
-    unsigned char* s_in = smem;                  // u8 [REC]
-    __bf16* s_w = (__bf16*)(smem + ((REC + 15) / 16) * 16);  // bf16 [PARTS][COUT][RS1]
+    __bf16* s_in = (__bf16*)smem;                // bf16 [REC]
+    __bf16* s_w = s_in + REC;                    // bf16 [PARTS][COUT][RS1]
     float* s_b = (float*)(s_w + PARTS * PL);
     static_assert(PARTS == 1 || PARTS == 3, "exact split or bf16 rounding");
 
@@ -694,33 +706,49 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
     side.begin(p.side, side_on, t);
     if (j0 >= j1) {  // uniform
         side.fetch(p.side, side_on, t);
-        side.end(p.side, side_on, t, WG);
+        side.end(p.side, side_on, t, U8F_WG);
         return;
     }
 
     auto sample_src = [&](int j) -> const f4* {
         return (const f4*)(j < p.n_a ? sample_ptr(p.in_a, j) : sample_ptr(p.in_b, j - p.n_a));
     };
-    f4 vin[RPER];
+    uint4 vin[RPER];
     auto load_in = [&](int j) {
-        const f4* src = sample_src(j);
+        const uint4* src = (const uint4*)sample_src(j);
 #pragma unroll
         for (int u = 0; u < RPER; ++u) {
-            const int e = t + u * WG;
+            const int e = t + u * U8F_WG;
             if (e < RV) vin[u] = src[e];
         }
     };
+    // sixteen bytes -> sixteen bf16 (the upper halves of the exact floats)
     auto store_in = [&]() {
 #pragma unroll
         for (int u = 0; u < RPER; ++u) {
-            const int e = t + u * WG;
-            if (e < RV) *(f4*)(s_in + 16 * e) = vin[u];
+            const int e = t + u * U8F_WG;
+            if (e < RV) {
+                const uint32_t w[4] = {vin[u].x, vin[u].y, vin[u].z, vin[u].w};
+                uint32_t h[8];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t f0 = __builtin_bit_cast(uint32_t, (float)(w[q] & 0xffu));
+                    const uint32_t f1 = __builtin_bit_cast(uint32_t, (float)((w[q] >> 8) & 0xffu));
+                    const uint32_t f2 = __builtin_bit_cast(uint32_t, (float)((w[q] >> 16) & 0xffu));
+                    const uint32_t f3 = __builtin_bit_cast(uint32_t, (float)(w[q] >> 24));
+                    h[2 * q] = __builtin_amdgcn_perm(f1, f0, 0x07060302u);
+                    h[2 * q + 1] = __builtin_amdgcn_perm(f3, f2, 0x07060302u);
+                }
+                uint4* d = (uint4*)(s_in + 16 * e);
+                d[0] = uint4{h[0], h[1], h[2], h[3]};
+                d[1] = uint4{h[4], h[5], h[6], h[7]};
+            }
         }
     };
 
     // weights -> PARTS bf16 planes [part][o][k] (exact split, or rounding); bias
     load_in(j0);
-    for (int e = t; e < COUT * KW1 / 4; e += WG) {
+    for (int e = t; e < COUT * KW1 / 4; e += U8F_WG) {
         const f4 w = ((const f4*)W)[e];
         const int o = (4 * e) / KW1, k = (4 * e) % KW1;
         bf16x4 h, m, l;
@@ -743,11 +771,11 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
 
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
-    const int ntile = (MT - wave + 3) / 4;       // this wave's M-tiles (uniform)
+    const int ntile = (MT - wave + NW - 1) / NW;  // this wave's M-tiles (uniform)
     int abase[MPW];
 #pragma unroll
     for (int i = 0; i < MPW; ++i) {
-        const int mt = wave + 4 * min(i, ntile - 1);
+        const int mt = wave + NW * min(i, ntile - 1);
         const int pa = mt * 16 + li;
         const int ra = pa / H1, xa = pa - ra * H1;
         abase[i] = S1 * ra * H0 + S1 * xa;
@@ -774,18 +802,16 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
                     b[nt][part] = *(const bf16x8*)(s_w + part * PL + (nt * 16 + li) * RS1 + kb * 32 + 8 * g);
 #pragma unroll
             for (int i = 0; i < MPW; ++i) {
-                const unsigned char* ap = s_in + (c * H0 + ky) * H0 + abase[i];
-                const uint32_t w0 = *(const uint32_t*)ap, w1 = *(const uint32_t*)(ap + 4);
-                bf16x8 a;
+                if (i < ntile) {
+                    // bytes (c, 4 ra + ky, 4 xa .. 4 xa + 7) as bf16: two 8-byte reads
+                    const __bf16* ap = s_in + (c * H0 + ky) * H0 + abase[i];
+                    const uint2 lo = *(const uint2*)ap, hi = *(const uint2*)(ap + 4);
+                    const bf16x8 a = __builtin_bit_cast(bf16x8, uint4{lo.x, lo.y, hi.x, hi.y});
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    a[q] = (__bf16)(float)((w0 >> (8 * q)) & 0xffu);
-                    a[4 + q] = (__bf16)(float)((w1 >> (8 * q)) & 0xffu);
+                    for (int part = 0; part < PARTS; ++part)
+#pragma unroll
+                        for (int nt = 0; nt < NT; ++nt) acc[i][nt] = mfma16x16x32bf16(a, b[nt][part], acc[i][nt]);
                 }
-#pragma unroll
-                for (int part = 0; part < PARTS; ++part)
-#pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) acc[i][nt] = mfma16x16x32bf16(a, b[nt][part], acc[i][nt]);
             }
         }
         // lane holds pixels 16*mt + 4g + r of channel nt*16 + li
@@ -793,7 +819,7 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
 #pragma unroll
         for (int i = 0; i < MPW; ++i) {
             if (i < ntile) {
-                const int pb = (wave + 4 * i) * 16 + 4 * g;
+                const int pb = (wave + NW * i) * 16 + 4 * g;
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt) {
                     const int o = nt * 16 + li;
@@ -814,7 +840,7 @@ __global__ __launch_bounds__(WG) void conv1_u8_fwd_kernel(U8FwdParams p) {
         }
         __syncthreads();  // all reads of s_in done before the next sample is stored
     }
-    side.end(p.side, side_on, t, WG);
+    side.end(p.side, side_on, t, U8F_WG);
 }
 
 }  // namespace
@@ -827,16 +853,16 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
     if (n <= 0 || n_a < 0 || n_a > n || !conv_s12_fwd_aligned(in_a) || !conv_s12_fwd_aligned(in_b) ||
         ((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15) || ((uintptr_t)out & 15) || (out16 && !bf16))
         return hipErrorInvalidValue;
-    // about 512 workgroups (two per compute unit, so one's loads overlap the
-    // other's MFMAs): a few samples each, so the weight split is amortized
-    const int spb = std::max(1, (n + 511) / 512);
+    // about 256 workgroups (one per compute unit): a run of samples each, so
+    // the weight split is amortized
+    const int spb = std::max(1, (n + 255) / 256);
     const int blocks_a = (n_a + spb - 1) / spb, blocks_b = (n - n_a + spb - 1) / spb;
     U8FwdParams prm{in_a, in_b, n_a, n, spb, blocks_a, w_a, b_a, w_b, b_b, out, side ? *side : SideFields{}};
     const dim3 grid((unsigned)std::max(1, blocks_a + blocks_b));
     auto go = [&](auto kern, int cout, int parts) -> hipError_t {
-        const size_t lds = ((C0 * H0 * H0 + 15) / 16) * 16 + (size_t)parts * cout * RS1 * 2 + (size_t)cout * 4;
+        const size_t lds = u8f_lds(cout, parts);
         if (!allow_lds((const void*)kern, lds)) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(kern, grid, dim3(WG), lds, st, prm);
+        hipLaunchKernelGGL(kern, grid, dim3(U8F_WG), lds, st, prm);
         return hipGetLastError();
     };
     if (id == CONV_L1) {
