@@ -74,6 +74,38 @@ __device__ __forceinline__ void ps_update(float& th, float& st, float g, float l
     }
 }
 
+// Output tile (x, y, z) of workgroup (blockIdx) in a grid of gx x gy x gz
+// tiles, ordered so that each of the eight XCDs (each with its own L2) runs
+// a contiguous range of tiles: workgroups are dealt to the XCDs round-robin
+// by linear id, so XCD c runs ids c, c + 8, ...; its r-th one takes tile
+// first(c) + r, first(c) being the number of ids dealt to XCDs before c.
+// Within a k-slice z, ROWS_SHARE orders the tiles x-major (runs that share
+// a row block of the row operand), otherwise y-major (runs that share a
+// column block of the column operand).
+struct TileXYZ {
+    int x, y, z;
+};
+template <bool ROWS_SHARE>
+__device__ __forceinline__ TileXYZ xcd_tile() {
+    const int gx = gridDim.x, gy = gridDim.y, gz = gridDim.z;
+    const int tiles = gx * gy * gz;
+    const int id = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+    const int c = id & 7, q = tiles >> 3, rem = tiles & 7;
+    const int t = c * q + min(c, rem) + (id >> 3);
+    const int z = t / (gx * gy), u = t - z * (gx * gy);
+    if constexpr (ROWS_SHARE) return TileXYZ{u / gy, u % gy, z};
+    else return TileXYZ{u % gx, u / gx, z};
+}
+// The forward contractions (split-K): the XCD-contiguous order when every
+// XCD's range spans at least two k-slices.  With fewer, whole XCDs would
+// hold one slice each, and a shorter last slice leaves its XCDs idle; the
+// launch order then already keeps each row block on one XCD (gx a multiple
+// of 8), the weights being fetched once per XCD.
+__device__ __forceinline__ TileXYZ fwd_tile_order() {
+    if (gridDim.z >= 16) return xcd_tile<true>();   // (gx*gy*gz / 8 >= 2*gx*gy)
+    return TileXYZ{(int)blockIdx.x, (int)blockIdx.y, (int)blockIdx.z};
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
@@ -356,14 +388,14 @@ enum GemmKind { GEMM_NT = 0, GEMM_TN = 1, GEMM_NN = 2 };
 // k-slicing of the fc1 forward GEMM for `rows` output rows: ks slices of
 // kchunk (a multiple of 64, the last one possibly shorter).
 void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk);
-// From kGemmX6MinRows rows the float32 fc1 forward (GEMM_NT: both operands
-// contiguous along k) runs on bf16 MFMA with the exact three-plane split
-// (launch_gemm_x6: GEMM_NT only; same arguments as launch_gemm, kchunk a
-// multiple of 32).
-// The weight and input gradients, whose operands are contiguous along m or
-// n, stay on fp32 MFMA: transposing and splitting them as they are staged
-// cost more than the six products saved (batch 2,048: 80 -> 128 us and
-// 76 -> 87 us), and so did the forward's split below 1,024 rows.
+// From a batch of kGemmX6MinRows (M of the forward and of the input
+// gradient, K of the weight gradient) the float32 fc1 contractions run on
+// bf16 MFMA with the exact three-plane split (launch_gemm_x6: same arguments
+// as launch_gemm, kchunk a multiple of 32): the forward on 128x256 tiles,
+// the weight and input gradients (operands contiguous along m or n,
+// transposed as they are staged) on 64x64 tiles, batch 2,048: 80 -> 77 us
+// and 77 -> 68 us.  Below that batch the split cost more than the six
+// products saved.
 constexpr int kGemmX6MinRows = 1024;
 void gemm_fwd_split_x6(int rows, int N, int K, int* ks, int* kchunk);
 hipError_t launch_gemm_x6(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,

@@ -6,7 +6,10 @@
 // global loads issued before the current step's MFMAs; four waves in a 2x2
 // arrangement.  The bf16-input variant rounds both staged operands to
 // bfloat16 as it reads them and runs one v_mfma_f32_16x16x32_bf16 per 32
-// k-values instead of eight fp32 steps.
+// k-values instead of eight fp32 steps.  The weight and input gradients
+// take their output tiles in the XCD-contiguous order of xcd_tile (tiles
+// sharing the column operand run on one XCD, so it is fetched into that
+// XCD's L2 once), and so does the forward when its k-slices are many.
 #include <algorithm>
 
 #include "common.h"
@@ -194,7 +197,8 @@ __device__ __forceinline__ void gemm_body(const GemmParams& p, int bx, int by, i
 template <int BM, int BN, int BK, bool TA, bool TB, bool MASK, bool BF16>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
     extern __shared__ __align__(16) float smem[];
-    gemm_body<BM, BN, BK, TA, TB, MASK, BF16>(p, blockIdx.x, blockIdx.y, blockIdx.z, smem);
+    const TileXYZ tile = !TA && TB ? fwd_tile_order() : xcd_tile<false>();
+    gemm_body<BM, BN, BK, TA, TB, MASK, BF16>(p, tile.x, tile.y, tile.z, smem);
 }
 
 // Two forward GEMMs of one shape in one launch (the online network on s and
@@ -202,11 +206,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p) {
 template <int BM, int BN, int BK, bool BF16>
 __global__ __launch_bounds__(256) void gemm_fwd2_kernel(GemmParams p0, GemmParams p1, int ks0) {
     extern __shared__ __align__(16) float smem[];
-    const int z = blockIdx.z;
+    const TileXYZ tile = fwd_tile_order();
+    const int z = tile.z;
     if (z < ks0)
-        gemm_body<BM, BN, BK, false, true, false, BF16>(p0, blockIdx.x, blockIdx.y, z, smem);
+        gemm_body<BM, BN, BK, false, true, false, BF16>(p0, tile.x, tile.y, z, smem);
     else
-        gemm_body<BM, BN, BK, false, true, false, BF16>(p1, blockIdx.x, blockIdx.y, z - ks0, smem);
+        gemm_body<BM, BN, BK, false, true, false, BF16>(p1, tile.x, tile.y, z - ks0, smem);
 }
 
 template <int BM, int BN, int BK>
@@ -387,7 +392,8 @@ hipError_t launch_gemm(GemmKind kind, int M, int N, int K, const float* A, int l
     if (kchunk % 32 != 0 || ((x16 || a16) && !bf16)) return hipErrorInvalidValue;
     if (bf16)
         return launch_gemm_bf16(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, x16, st, a16);
-    if (kind == GEMM_NT && M >= kGemmX6MinRows)
+    // the batch is M of the forward and the input gradient, K of the weight gradient
+    if ((kind == GEMM_TN ? K : M) >= kGemmX6MinRows)
         return launch_gemm_x6(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
     return launch_gemm_prec<false>(kind, M, N, K, A, lda, B, ldb, C, ldc, kslices, kchunk, c_slice, mask, st);
 }

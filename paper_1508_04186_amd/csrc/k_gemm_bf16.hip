@@ -24,7 +24,12 @@
 // tests.  The next stage's global loads are in flight during the current
 // stage's MFMAs.  The tiles are large where the batch is (each operand is
 // re-read once per tile of the other dimension, from L2), and the forward
-// pass splits K so that the launch still covers the chip.
+// pass splits K so that the launch still covers the chip.  The weight and
+// input gradients take their tiles in the XCD-contiguous order of xcd_tile,
+// so that the tiles of one XCD share the column operand (the activations of
+// the weight gradient, the weight columns of the input gradient), which is
+// then fetched into each L2 once instead of once per XCD; the forward does
+// so when its k-slices are many (fwd_tile_order).
 #include <algorithm>
 #include <initializer_list>
 #include <type_traits>
@@ -198,13 +203,14 @@ struct Stage {
 // live at As, Bs (PARTS planes each).
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK, bool A16 = false, bool B16 = false,
           bool M16 = false, int PARTS = 1>
-__device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, int z, __bf16* As, __bf16* Bs) {
+__device__ __forceinline__ void gemm_bf16_body(const GemmBf16Params& p, TileXYZ tile, int z, __bf16* As,
+                                               __bf16* Bs) {
     constexpr int NT = 64 * WGM * WGN;
     constexpr int WTM = BM / WGM, WTN = BN / WGN;     // wave tile
     constexpr int TM = WTM / 16, TN = WTN / 16;       // MFMA tiles per wave
     constexpr int RS = BK;
     static_assert(BK % 32 == 0 && WTM % 16 == 0 && WTN % 16 == 0, "tile shape");
-    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+    const int m0 = tile.x * BM, n0 = tile.y * BN;
     const int kbeg = z * p.kchunk, kend = min(p.K, kbeg + p.kchunk);
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
@@ -289,14 +295,16 @@ template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK,
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_kernel(GemmBf16Params p) {
     __shared__ __align__(16) __bf16 As[BM * BK];
     __shared__ __align__(16) __bf16 Bs[BN * BK];
-    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, A16, B16, M16>(p, blockIdx.z, As, Bs);
+    const TileXYZ tile = !TA && TB ? fwd_tile_order() : xcd_tile<false>();
+    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, A16, B16, M16>(p, tile, tile.z, As, Bs);
 }
 
 // float32 operands, exact three-plane split (stages in dynamic LDS)
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_x6_kernel(GemmBf16Params p) {
     extern __shared__ __align__(16) __bf16 smem_x6[];
-    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, false, false, false, 3>(p, blockIdx.z, smem_x6,
+    const TileXYZ tile = !TA && TB ? fwd_tile_order() : xcd_tile<false>();
+    gemm_bf16_body<BM, BN, BK, WGM, WGN, TA, TB, MASK, false, false, false, 3>(p, tile, tile.z, smem_x6,
                                                                               smem_x6 + 3 * BM * BK);
 }
 
@@ -307,22 +315,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_bf16_fwd2_kernel(GemmBf16
                                                                        int ks0) {
     __shared__ __align__(16) __bf16 As[BM * BK];
     __shared__ __align__(16) __bf16 Bs[BN * BK];
-    const int z = blockIdx.z;
+    const TileXYZ tile = fwd_tile_order();
+    const int z = tile.z;
     if (z < ks0)
-        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p0, z, As, Bs);
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p0, tile, z, As, Bs);
     else
-        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p1, z - ks0, As, Bs);
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, A16>(p1, tile, z - ks0, As, Bs);
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_x6_fwd2_kernel(GemmBf16Params p0, GemmBf16Params p1, int ks0) {
     extern __shared__ __align__(16) __bf16 smem_x6[];
     __bf16* Bs = smem_x6 + 3 * BM * BK;
-    const int z = blockIdx.z;
+    const TileXYZ tile = fwd_tile_order();
+    const int z = tile.z;
     if (z < ks0)
-        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, false, false, false, 3>(p0, z, smem_x6, Bs);
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, false, false, false, 3>(p0, tile, z, smem_x6, Bs);
     else
-        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, false, false, false, 3>(p1, z - ks0, smem_x6, Bs);
+        gemm_bf16_body<BM, BN, BK, WGM, WGN, false, true, false, false, false, false, 3>(p1, tile, z - ks0, smem_x6,
+                                                                                         Bs);
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN, bool TA, bool TB, bool MASK>
@@ -436,10 +447,20 @@ hipError_t launch_gemm_x6(GemmKind kind, int M, int N, int K, const float* A, in
                           hipStream_t st) {
     if (M <= 0 || N <= 0 || K <= 0 || kslices <= 0 || kchunk % 32 != 0) return hipErrorInvalidValue;
     if ((uintptr_t)A % 16 || (uintptr_t)B % 16 || lda % 4 || ldb % 4) return hipErrorInvalidValue;
-    if (kind != GEMM_NT || mask || K % 4) return hipErrorInvalidValue;   // the forward only
-    const GemmBf16Params prm{M, N, K, A, lda, B, ldb, C, ldc, kchunk, c_slice, nullptr};
-    if (M >= kBf16BigRows) return gemm_x6_launch<128, 256, 32, 2, 4, false, true, false>(prm, kslices, st);
-    return gemm_x6_launch<64, 64, 64, 2, 2, false, true, false>(prm, kslices, st);
+    const GemmBf16Params prm{M, N, K, A, lda, B, ldb, C, ldc, kchunk, c_slice, mask};
+    switch (kind) {
+        case GEMM_NT:
+            if (mask || K % 4) return hipErrorInvalidValue;
+            if (M >= kBf16BigRows) return gemm_x6_launch<128, 256, 32, 2, 4, false, true, false>(prm, kslices, st);
+            return gemm_x6_launch<64, 64, 64, 2, 2, false, true, false>(prm, kslices, st);
+        case GEMM_TN:   // (64x64 tiles: the output is hidden x flat, only a few row blocks)
+            if (mask || M % 4 || N % 4) return hipErrorInvalidValue;
+            return gemm_x6_launch<64, 64, 64, 2, 2, true, false, false>(prm, kslices, st);
+        case GEMM_NN:
+            if (!mask || K % 4 || N % 4) return hipErrorInvalidValue;
+            return gemm_x6_launch<64, 64, 64, 2, 2, false, false, true>(prm, kslices, st);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_gemm_bf16_fwd2(int M, int N, int K, const float* A0, const float* B0, float* C0,
