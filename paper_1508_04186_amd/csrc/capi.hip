@@ -361,10 +361,15 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     // gathering 64 to 144 scattered words per lane; the gather dominated a
     // workgroup's first sample: batch 256, conv2's fp32 input gradient 33 ->
     // 21 us, bf16 23 -> 9 us).
+    // (the bf16-input variant's forward copies, for its bf16 activations,
+    // are jobs of the input gradients' repack launch: batch 2,048, conv2 and
+    // conv3 forward 44.6 -> 42.4 and 37.2 -> 31.7 us)
     const bool repack_fwd = !ni.bf16 && L == 3 && conv_fwd_cl_use(CONV_L2, 2 * B, false);
+    const bool fwd16 = a16 && conv_fwd_cl_use(CONV_L2, 2 * B, true) && conv_fwd_cl_use(CONV_L3, 2 * B, true);
     const bool repack = L == 3 && phase_dgrad(CONV_L2, B, ni.bf16);
-    if (repack_fwd || repack) {
-        WeightRepack r{th + ni.w_off[1], th + ni.w_off[2], nullptr, nullptr, nullptr, nullptr};
+    if (repack_fwd || repack || fwd16) {
+        WeightRepack r{th + ni.w_off[1], th + ni.w_off[2], nullptr, nullptr, nullptr, nullptr,
+                       tt + ni.w_off[1], tt + ni.w_off[2], nullptr, nullptr, nullptr, nullptr};
         if (repack && ni.bf16) {
             r.h2 = t.wpk2;
             r.h3 = t.wpk3;
@@ -372,7 +377,13 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             r.x2 = t.wpk2;
             r.x3 = t.wpk3;
         }
-        RUN(DQN_K_WEIGHT_REPACK, repack_weights(repack ? &r : nullptr, repack_fwd, th + ni.w_off[1],
+        if (fwd16) {
+            r.f2a = t.fpk[0][0];
+            r.f3a = t.fpk[1][0];
+            r.f2b = t.fpk[0][1];
+            r.f3b = t.fpk[1][1];
+        }
+        RUN(DQN_K_WEIGHT_REPACK, repack_weights(repack || fwd16 ? &r : nullptr, repack_fwd, th + ni.w_off[1],
                                                 th + ni.w_off[2], tt + ni.w_off[1], tt + ni.w_off[2], t.fpk, st));
     }
 
@@ -401,7 +412,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             RUN(DQN_K_CONV1_FWD + l,
                 launch_conv_igemm_fwd(ni.conv[l], t.act[l - 1], B, 2 * B, th + ni.w_off[l], th + ni.b_off[l],
                                       tt + ni.w_off[l], tt + ni.b_off[l], t.act[l], ni.bf16, a16, a16,
-                                      repack_fwd ? t.fpk[l - 1][0] : nullptr, repack_fwd ? t.fpk[l - 1][1] : nullptr,
+                                      repack_fwd || fwd16 ? t.fpk[l - 1][0] : nullptr,
+                                      repack_fwd || fwd16 ? t.fpk[l - 1][1] : nullptr,
                                       st));
             continue;
         }

@@ -315,6 +315,11 @@ struct WeightRepack {
     const float *w2a, *w3a;
     void *h2, *h3;   // bf16 input-gradient operands (the bf16-input variant)
     void *x2, *x3;   // the three exact bf16 planes of the float32 input gradients
+    // The bf16-input variant's forward weights of both sets (a: w2a, w3a;
+    // b: w2b, w3b) rounded to bf16 in the per-lane order of its forward
+    // kernel: the first plane of the float32 forward's copies (same layout).
+    const float *w2b, *w3b;
+    void *f2a, *f3a, *f2b, *f3b;
 };
 int64_t weight_repack_floats(ConvId id);
 hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st);

@@ -80,17 +80,86 @@ struct Mask4<true> {
 // consecutive channels at one slot: one 16-byte read at a per-lane base and
 // a compile-time tap offset, issued two k-steps ahead of its MFMA.  k-step
 // s: tap s / 2, channels 32 (s % 2) + 8g + e in element e of lane group g
-// (the weights in registers follow the same order).
+// (the weights in registers follow the same order).  The input gradient is
+// assembled in LDS channel by channel at a row stride of D2_CS = 402 floats:
+// a stride of 400 (16 mod 32 banks) put the 16 channels of one store on two
+// banks (16-way conflicts), 402 spreads them (at most 4-way); rows then start
+// 8-byte aligned and the read-out takes a float4 as two 8-byte reads.
 constexpr int D2C_SLOTS = 132;                 // sigma of every read: 0 .. 122
 constexpr int D2C_PSB = 144;                   // bytes per slot: 64 bf16 + 16
-constexpr int D2C_PAIRS = D2_DZ / 2;           // (channel pair, pixel) items
-constexpr int D2C_PER = (D2C_PAIRS + D2_WG - 1) / D2_WG;
-static_assert(D2C_PSB % 16 == 0 && D2C_PSB >= 2 * D2_COUT, "slot size");
+static_assert(D2C_PSB % 16 == 0 && D2C_PSB >= 2 * D2_COUT && (D2C_PSB / 16) % 2 == 1, "slot size");
+constexpr int D2_CS = D2_IH * D2_IH + 2;       // LDS row stride of the assembled input gradient (floats)
+
+// A sample's dz [64][OH][OH] staged channels-last (144-byte slots, slot
+// RW (oy + R0) + ox + C0 for pixel (oy, ox)) as items of CPI channels at
+// one pixel: one 2*CPI-byte store per item and plane, consecutive lanes at
+// consecutive slots (9 chunks of 16 bytes apart).  Items of eight channels
+// store without bank conflicts and of four with at most two-way ones, where
+// 4-byte stores of channel pairs at that stride conflicted four to eight
+// ways; four channels keep fewer values in registers (for the float32 conv2
+// kernel's budget).  PLANES = 1: rounded to bf16; 3: the exact split, plane
+// pl at + pl * plane bytes.
+template <int OH, int RW, int R0, int C0, int PLANES, int CPI = 8>
+struct DzStage {
+    static_assert(CPI == 4 || CPI == 8, "item width");
+    static constexpr int P = OH * OH, ITEMS = (D2_COUT / CPI) * P, IPER = (ITEMS + D2_WG - 1) / D2_WG;
+    using V = std::conditional_t<CPI == 8, bf16x8, bf16x4>;
+    float v[IPER][CPI];
+    __device__ __forceinline__ void fetch(const float* src, int t) {
+#pragma unroll
+        for (int u = 0; u < IPER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < ITEMS) {
+                const int og = q2 / P, q = q2 - og * P;
+#pragma unroll
+                for (int e = 0; e < CPI; ++e) v[u][e] = src[(CPI * og + e) * P + q];
+            }
+        }
+    }
+    __device__ __forceinline__ void stage(unsigned char* s_cl, int t, int plane_bytes) const {
+#pragma unroll
+        for (int u = 0; u < IPER; ++u) {
+            const int q2 = t + u * D2_WG;
+            if (q2 < ITEMS) {
+                const int og = q2 / P, q = q2 - og * P, oy = q / OH, ox = q - oy * OH;
+                unsigned char* d = s_cl + (RW * (oy + R0) + ox + C0) * 144 + 2 * CPI * og;
+                V h, m, l;
+#pragma unroll
+                for (int e = 0; e < CPI; ++e) {
+                    if constexpr (PLANES == 3) {
+                        __bf16 a, b, c;
+                        split3(v[u][e], a, b, c);
+                        h[e] = a;
+                        m[e] = b;
+                        l[e] = c;
+                    } else {
+                        h[e] = (__bf16)v[u][e];
+                    }
+                }
+                *(V*)d = h;
+                if constexpr (PLANES == 3) {
+                    *(V*)(d + plane_bytes) = m;
+                    *(V*)(d + 2 * plane_bytes) = l;
+                }
+            }
+        }
+    }
+};
+
+// Float4 e4 of the input gradient (pixels 4k .. 4k+3 of channel c) from the
+// LDS assembly above (rows at a stride of D2_CS floats, 8-byte aligned).
+__device__ __forceinline__ f4 d2_din4(const float* s_din, int e4) {
+    constexpr int CP = D2_IH * D2_IH;
+    const int ch = e4 / (CP / 4);
+    const float* r = s_din + ch * D2_CS + (4 * e4 - ch * CP);
+    const float2 a = *(const float2*)r, b = *(const float2*)(r + 2);
+    return f4{a.x, a.y, b.x, b.y};
+}
 
 template <bool H16, bool PK>   // PK: bf16 weight operands from p.wpk (weight_repack)
 __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
     __shared__ __align__(16) unsigned char s_cl[D2C_SLOTS * D2C_PSB];
-    __shared__ __align__(16) float s_din[D2_IN];
+    __shared__ __align__(16) float s_din[D2_CIN * D2_CS];
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
@@ -129,32 +198,9 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
         base[i] = (D2_Q * (qy + 1) + qx + 1) * D2C_PSB + 16 * g;
     }
 
-    float va[D2C_PER], vb[D2C_PER];
-    auto fetch = [&](int j) {
-        const float* src = p.dz + (size_t)j * D2_DZ;
-#pragma unroll
-        for (int u = 0; u < D2C_PER; ++u) {
-            const int q2 = t + u * D2_WG;
-            if (q2 < D2C_PAIRS) {
-                const int op = q2 / (D2_OH * D2_OH), q = q2 - op * (D2_OH * D2_OH);
-                va[u] = src[(2 * op) * D2_OH * D2_OH + q];
-                vb[u] = src[(2 * op + 1) * D2_OH * D2_OH + q];
-            }
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int u = 0; u < D2C_PER; ++u) {
-            const int q2 = t + u * D2_WG;
-            if (q2 < D2C_PAIRS) {
-                const int op = q2 / (D2_OH * D2_OH), q = q2 - op * (D2_OH * D2_OH);
-                const int oy = q / D2_OH, ox = q - oy * D2_OH;
-                const uint32_t lo = __builtin_bit_cast(unsigned short, (__bf16)va[u]);
-                const uint32_t hi = __builtin_bit_cast(unsigned short, (__bf16)vb[u]);
-                *(uint32_t*)(s_cl + (D2_Q * (oy + 1) + ox + 1) * D2C_PSB + 4 * op) = lo | (hi << 16);
-            }
-        }
-    };
+    DzStage<D2_OH, D2_Q, 1, 1, 1> dzs;
+    auto fetch = [&](int j) { dzs.fetch(p.dz + (size_t)j * D2_DZ, t); };
+    auto stage = [&]() { dzs.stage(s_cl, t, 0); };
 
     float bsum[D2_OUT4];
 #pragma unroll
@@ -205,7 +251,7 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
                 const int m = i * 16 + 4 * g + r;
                 if (m < D2_QP) {
                     const int qy = m / D2_Q, qx = m - qy * D2_Q;
-                    s_din[c * D2_IH * D2_IH + (2 * qy + py) * D2_IH + 2 * qx + px] = acc[i][r];
+                    s_din[c * D2_CS + (2 * qy + py) * D2_IH + 2 * qx + px] = acc[i][r];
                 }
             }
         __syncthreads();
@@ -213,7 +259,7 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_cl_kernel(Dgrad2Params p) {
         for (int u = 0; u < D2_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
             if (e4 < D2_IN / 4) {
-                const f4 d = *(const f4*)(s_din + 4 * e4);
+                const f4 d = d2_din4(s_din, e4);
                 f4 o;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) o[k] = mreg[u].pos(k) ? d[k] : 0.f;
@@ -273,8 +319,6 @@ static_assert(D3_MT % 2 == 0 && D3_IN % 4 == 0, "tile split and float4 rows");
 // slot m + 20 - 9ky - kx.  k-step s: tap s / 2, channels 32 (s % 2) + 8g + e.
 constexpr int D3C_SLOTS = 120;                 // every read: slot 0 .. 115
 constexpr int D3C_PSB = 144;
-constexpr int D3C_PAIRS = D3_DZ / 2;
-constexpr int D3C_PER = (D3C_PAIRS + D2_WG - 1) / D2_WG;
 
 template <bool H16, bool PK>   // PK: bf16 weight operands from p.wpk (weight_repack)
 __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
@@ -313,32 +357,9 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_cl_kernel(Dgrad2Params p) {
 #pragma unroll
     for (int i = 0; i < D3_TPW; ++i) base[i] = ((mh * D3_TPW + i) * 16 + li + 20) * D3C_PSB + 16 * g;
 
-    float va[D3C_PER], vb[D3C_PER];
-    auto fetch = [&](int j) {
-        const float* src = p.dz + (size_t)j * D3_DZ;
-#pragma unroll
-        for (int u = 0; u < D3C_PER; ++u) {
-            const int q2 = t + u * D2_WG;
-            if (q2 < D3C_PAIRS) {
-                const int op = q2 / (D3_OH * D3_OH), q = q2 - op * (D3_OH * D3_OH);
-                va[u] = src[(2 * op) * D3_OH * D3_OH + q];
-                vb[u] = src[(2 * op + 1) * D3_OH * D3_OH + q];
-            }
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int u = 0; u < D3C_PER; ++u) {
-            const int q2 = t + u * D2_WG;
-            if (q2 < D3C_PAIRS) {
-                const int op = q2 / (D3_OH * D3_OH), q = q2 - op * (D3_OH * D3_OH);
-                const int oy = q / D3_OH, ox = q - oy * D3_OH;
-                const uint32_t lo = __builtin_bit_cast(unsigned short, (__bf16)va[u]);
-                const uint32_t hi = __builtin_bit_cast(unsigned short, (__bf16)vb[u]);
-                *(uint32_t*)(s_cl + (D3_IH * (oy + 2) + ox + 2) * D3C_PSB + 4 * op) = lo | (hi << 16);
-            }
-        }
-    };
+    DzStage<D3_OH, D3_IH, 2, 2, 1> dzs;
+    auto fetch = [&](int j) { dzs.fetch(p.dz + (size_t)j * D3_DZ, t); };
+    auto stage = [&]() { dzs.stage(s_cl, t, 0); };
 
     fetch(j_lo);
     for (int j = j_lo; j < j_hi; ++j) {
@@ -421,7 +442,7 @@ constexpr int X3_LDS = 3 * D3C_SLOTS * D3C_PSB;
 template <bool PK>
 __global__ __launch_bounds__(D2_WG) void conv2_dgrad_x6_kernel(Dgrad2Params p) {
     __shared__ __align__(16) unsigned char s_cl[X2_LDS];     // [3][slots][144]
-    __shared__ __align__(16) float s_din[D2_IN];
+    __shared__ __align__(16) float s_din[D2_CIN * D2_CS];
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
@@ -466,40 +487,9 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_x6_kernel(Dgrad2Params p) {
         base[i] = (D2_Q * (qy + 1) + qx + 1) * D2C_PSB + 16 * g;
     }
 
-    float va[D2C_PER], vb[D2C_PER];
-    auto fetch = [&](int j) {
-        const float* src = p.dz + (size_t)j * D2_DZ;
-#pragma unroll
-        for (int u = 0; u < D2C_PER; ++u) {
-            const int q2 = t + u * D2_WG;
-            if (q2 < D2C_PAIRS) {
-                const int op = q2 / (D2_OH * D2_OH), q = q2 - op * (D2_OH * D2_OH);
-                va[u] = src[(2 * op) * D2_OH * D2_OH + q];
-                vb[u] = src[(2 * op + 1) * D2_OH * D2_OH + q];
-            }
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int u = 0; u < D2C_PER; ++u) {
-            const int q2 = t + u * D2_WG;
-            if (q2 < D2C_PAIRS) {
-                const int op = q2 / (D2_OH * D2_OH), q = q2 - op * (D2_OH * D2_OH);
-                const int oy = q / D2_OH, ox = q - oy * D2_OH;
-                __bf16 a0, a1, a2, b0, b1, b2;
-                split3(va[u], a0, a1, a2);
-                split3(vb[u], b0, b1, b2);
-                unsigned char* d = s_cl + (D2_Q * (oy + 1) + ox + 1) * D2C_PSB + 4 * op;
-                auto word = [](__bf16 lo, __bf16 hi) {
-                    return (uint32_t)__builtin_bit_cast(unsigned short, lo) |
-                           ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
-                };
-                *(uint32_t*)d = word(a0, b0);
-                *(uint32_t*)(d + PL) = word(a1, b1);
-                *(uint32_t*)(d + 2 * PL) = word(a2, b2);
-            }
-        }
-    };
+    DzStage<D2_OH, D2_Q, 1, 1, 3, 4> dzs;   // (four channels an item: the register budget)
+    auto fetch = [&](int j) { dzs.fetch(p.dz + (size_t)j * D2_DZ, t); };
+    auto stage = [&]() { dzs.stage(s_cl, t, PL); };
 
     // M-tiles [I0, I0 + NI): per k-step the three planes of their A operands,
     // then the six products, each over the group's tiles
@@ -554,7 +544,7 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_x6_kernel(Dgrad2Params p) {
                 const int m = i * 16 + 4 * g + r;
                 if (m < D2_QP) {
                     const int qy = m / D2_Q, qx = m - qy * D2_Q;
-                    s_din[c * D2_IH * D2_IH + (2 * qy + py) * D2_IH + 2 * qx + px] = acc[i][r];
+                    s_din[c * D2_CS + (2 * qy + py) * D2_IH + 2 * qx + px] = acc[i][r];
                 }
             }
         __syncthreads();
@@ -562,7 +552,7 @@ __global__ __launch_bounds__(D2_WG) void conv2_dgrad_x6_kernel(Dgrad2Params p) {
         for (int u = 0; u < D2_OUT4; ++u) {
             const int e4 = t + u * D2_WG;
             if (e4 < D2_IN / 4) {
-                const f4 d = *(const f4*)(s_din + 4 * e4);
+                const f4 d = d2_din4(s_din, e4);
                 f4 o;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) o[k] = mreg[u].pos(k) ? d[k] : 0.f;
@@ -621,40 +611,9 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_x6_kernel(Dgrad2Params p) {
 #pragma unroll
     for (int i = 0; i < D3_MT; ++i) base[i] = (i * 16 + li + 20) * D3C_PSB + 16 * g;
 
-    float va[D3C_PER], vb[D3C_PER];
-    auto fetch = [&](int j) {
-        const float* src = p.dz + (size_t)j * D3_DZ;
-#pragma unroll
-        for (int u = 0; u < D3C_PER; ++u) {
-            const int q2 = t + u * D2_WG;
-            if (q2 < D3C_PAIRS) {
-                const int op = q2 / (D3_OH * D3_OH), q = q2 - op * (D3_OH * D3_OH);
-                va[u] = src[(2 * op) * D3_OH * D3_OH + q];
-                vb[u] = src[(2 * op + 1) * D3_OH * D3_OH + q];
-            }
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int u = 0; u < D3C_PER; ++u) {
-            const int q2 = t + u * D2_WG;
-            if (q2 < D3C_PAIRS) {
-                const int op = q2 / (D3_OH * D3_OH), q = q2 - op * (D3_OH * D3_OH);
-                const int oy = q / D3_OH, ox = q - oy * D3_OH;
-                __bf16 a0, a1, a2, b0, b1, b2;
-                split3(va[u], a0, a1, a2);
-                split3(vb[u], b0, b1, b2);
-                unsigned char* d = s_cl + (D3_IH * (oy + 2) + ox + 2) * D3C_PSB + 4 * op;
-                auto word = [](__bf16 lo, __bf16 hi) {
-                    return (uint32_t)__builtin_bit_cast(unsigned short, lo) |
-                           ((uint32_t)__builtin_bit_cast(unsigned short, hi) << 16);
-                };
-                *(uint32_t*)d = word(a0, b0);
-                *(uint32_t*)(d + PL) = word(a1, b1);
-                *(uint32_t*)(d + 2 * PL) = word(a2, b2);
-            }
-        }
-    };
+    DzStage<D3_OH, D3_IH, 2, 2, 3> dzs;
+    auto fetch = [&](int j) { dzs.fetch(p.dz + (size_t)j * D3_DZ, t); };
+    auto stage = [&]() { dzs.stage(s_cl, t, PL); };
     auto half = [&](auto khc, f4* acc) {
         constexpr int KH = decltype(khc)::value;
 #pragma unroll
@@ -741,10 +700,35 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_x6_kernel(Dgrad2Params p) {
 // the 4 N-tiles of conv3 (KS = 18), values W[o][c][tap] as the kernels read;
 // the float32 kernels' copies hold the three planes of the exact split one
 // after another.  Job j of the launch (blockIdx.y) writes one copy; a NULL
-// output skips it.
+// output skips it.  Jobs 4 to 7: the bf16-input forward's weights of
+// conv2 and conv3 for both weight sets, vector (nt KS + ks) 64 + lane
+// holding W[16nt + li][32 (ks % CH) + 8g + q][ks / CH] rounded (CH = cin /
+// 32, KS = taps * CH), as its kernel reads them.
+template <int CIN, int KK>
+__device__ __forceinline__ void fwd_bf16_pack_job(const float* w, void* out, int e) {
+    constexpr int CH = CIN / 32, KS = KK * CH;
+    if (!out || e >= 4 * KS * 64) return;
+    const int lane = e & 63, ks = (e >> 6) % KS, nt = (e >> 6) / KS;
+    const int li = lane & 15, g = lane >> 4, tap = ks / CH, cb = ks % CH;
+    const float* wr = w + (size_t)(16 * nt + li) * CIN * KK;
+    bf16x8 v;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = (__bf16)wr[(32 * cb + 8 * g + q) * KK + tap];
+    ((bf16x8*)out)[e] = v;
+}
+
 __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
     const int e = blockIdx.x * 256 + threadIdx.x;
     const int job = blockIdx.y;
+    if (job >= 4) {
+        switch (job) {
+            case 4: fwd_bf16_pack_job<D2_CIN, D2_K * D2_K>(r.w2a, r.f2a, e); break;
+            case 5: fwd_bf16_pack_job<D3_CIN, D3_K * D3_K>(r.w3a, r.f3a, e); break;
+            case 6: fwd_bf16_pack_job<D2_CIN, D2_K * D2_K>(r.w2b, r.f2b, e); break;
+            default: fwd_bf16_pack_job<D3_CIN, D3_K * D3_K>(r.w3b, r.f3b, e); break;
+        }
+        return;
+    }
     if (job == 0) {   // conv2 input gradient, bf16 operands: one 8-value vector per thread
         constexpr int KS2 = D2_KT / 32;
         if (r.h2 && e < 8 * KS2 * 64) {
@@ -816,10 +800,13 @@ __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
 int64_t weight_repack_floats(ConvId id) { return id == CONV_L2 ? 4 * 3 * 8 * X2_KS * 64 : 4 * 3 * 4 * X3_KS * 64; }
 
 hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st) {
-    for (const void* q : {r.h2, r.h3, r.x2, r.x3})
+    for (const void* q : {r.h2, r.h3, r.x2, r.x3, r.f2a, r.f3a, r.f2b, r.f3b})
         if ((uintptr_t)q & 15) return hipErrorInvalidValue;
-    // every copy has at most 3 * 4 * 18 * 64 = 13,824 vectors
-    hipLaunchKernelGGL(weight_repack_kernel, dim3(13824 / 256, 4), dim3(256), 0, st, r);
+    if ((r.f2b && !r.w2b) || (r.f3b && !r.w3b)) return hipErrorInvalidValue;
+    // every copy has at most 3 * 4 * 18 * 64 = 13,824 vectors; the forward's
+    // jobs only when one of their outputs is set
+    const bool fwd = r.f2a || r.f3a || r.f2b || r.f3b;
+    hipLaunchKernelGGL(weight_repack_kernel, dim3(13824 / 256, fwd ? 8 : 4), dim3(256), 0, st, r);
     return hipGetLastError();
 }
 

@@ -9,7 +9,12 @@
 // in LDS as bf16, channels-last, so that the eight k-values a lane feeds one
 // v_mfma_f32_16x16x32_bf16 (eight consecutive input channels at one pixel of
 // one filter tap) are one 16-byte LDS read, issued two k-steps ahead of its
-// MFMA.  The k order of a step is (tap, 32 channels).  A round takes SPR
+// MFMA.  The k order of a step is (tap, 32 channels).  The staged pixels are
+// laid out as the float32 kernel's (FwdX6Geom::slot: stride-2 rows and
+// columns split by parity, rows at a pitch of OH + 16 slots, an odd number
+// of 16-byte chunks per pixel), so that the reads of 16 consecutive output
+// pixels hit 16 distinct groups of four banks; a sample is staged as items
+// of eight channels at one pixel, one 16-byte store each.  A round takes SPR
 // samples; the next round's input is read from HBM into registers during
 // the current round's MFMAs, and the output maps are assembled in LDS and
 // written as whole 16-byte vectors.  Weights reach the registers through
@@ -39,17 +44,23 @@ struct FwdClGeom {
     static constexpr int KT = CIN * KK;                 // contraction length
     static constexpr int IP = IH * IH;                  // input pixels
     static constexpr int PSB = CIN * 2 + 16;            // LDS bytes per staged pixel (16-byte multiple)
+    static constexpr int RP = OH + 16;                  // row pitch (slots): RP = OH (mod 16)
+    static constexpr int SLOTS = IH * RP;
     static constexpr int IN = CIN * IP;                 // input floats per sample
-    static constexpr int PAIRS = IN / 2;                // (channel pair, pixel) items
-    static constexpr int PER = (PAIRS + FC_WG - 1) / FC_WG;
     static constexpr int OUTF = COUT * P;               // output floats per sample
-    static constexpr int LDS_MAIN = SPR * (IP * PSB + OUTF * 4);
+    static constexpr int LDS_MAIN = SPR * (SLOTS * PSB + OUTF * 4);
     static constexpr int LDS_W = COUT * KT * 2;         // all weights as bf16 operands
     static constexpr int WPER = COUT * KT / 4 / FC_WG;  // weight float4s per thread
     static_assert(COUT * KT % (4 * FC_WG) == 0, "whole weight float4s per thread");
     static constexpr int LDS = LDS_MAIN > LDS_W ? LDS_MAIN : LDS_W;
     static_assert(MT % 2 == 0 && CIN % 32 == 0, "geometry");
-    static_assert(OUTF % 4 == 0 && KT % 4 == 0 && PSB % 16 == 0, "vector widths");
+    static_assert(OUTF % 4 == 0 && KT % 4 == 0 && PSB % 16 == 0 && (PSB / 16) % 2 == 1, "vector widths");
+    static_assert(S == 1 || (S == 2 && IH % 2 == 0 && IH / 2 <= RP), "stride-phase layout");
+    static_assert(RP >= IH, "row pitch");
+    // slot of input pixel (y, x); slot(S oy + ky, S ox + kx) = slot(ky, kx) + oy RP + ox
+    __host__ __device__ static constexpr int slot(int y, int x) {
+        return S == 2 ? ((y & 1) * (IH / 2) + (y >> 1)) * RP + (x & 1) * (IH / 2) + (x >> 1) : y * RP + x;
+    }
 };
 
 struct FwdClParams {
@@ -57,15 +68,16 @@ struct FwdClParams {
     float* out;                // [n][64][oh][oh] (bfloat16 values when out16)
     const float *w_a, *b_a, *w_b, *b_b;
     int n, n_a, g_a, spg;      // blocks [0, g_a) take samples [0, n_a), the rest [n_a, n); runs of spg
-    const float *wpk_a, *wpk_b;  // fp32 kernel: w_a, w_b in per-lane order (weight_repack), or NULL
+    const float *wpk_a, *wpk_b;  // w_a, w_b in per-lane order (fwd_x6_pack, or weight_repack's bf16 jobs), or NULL
 };
 
-template <int CIN, int IH, int K, int S, int OH, int SPR, bool IN16, bool OUT16>
+// PK: the weights from wpk_a / wpk_b (weight_repack: per-lane order, rounded)
+template <int CIN, int IH, int K, int S, int OH, int SPR, bool IN16, bool OUT16, bool PK>
 __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
     using G = FwdClGeom<CIN, IH, K, S, OH, SPR>;
     extern __shared__ __align__(16) unsigned char smem[];
-    unsigned char* s_in = smem;                                  // [SPR][IP][PSB] bf16, channels-last
-    float* s_out = (float*)(smem + SPR * G::IP * G::PSB);        // [SPR][64][P]
+    unsigned char* s_in = smem;                                  // [SPR][SLOTS][PSB] bf16, channels-last
+    float* s_out = (float*)(smem + SPR * G::SLOTS * G::PSB);     // [SPR][64][P]
     __bf16* s_w = (__bf16*)smem;                                 // [4][KS][64][8] bf16 (weights, before the samples)
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int li = lane & 15, g = lane >> 4;
@@ -82,132 +94,97 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
     const float* __restrict__ bias = second ? p.b_b : p.b_a;
 
     // SPR samples per round: sample j + s of the round is read into
-    // registers (va, vb) and staged into s_in buffer s.  bfloat16 input with
-    // an even pixel count (conv2's) is read as 32-bit words of two pixels of
-    // one channel and restaged bit for bit, without conversions.
-    constexpr bool W32 = IN16 && G::IP % 2 == 0;
-    // bfloat16 input with an odd pixel count (conv3's): 32-bit words of the
-    // flat [channel][pixel] sample, each value stored into its place of the
-    // channels-last stage with a 16-bit LDS write
-    constexpr bool WFLAT = IN16 && !W32;
-    constexpr int PER2 = ((CIN / 2) * (G::IP / 2) + FC_WG - 1) / FC_WG;
-    constexpr int PERF = (G::IN / 2 + FC_WG - 1) / FC_WG;
-    static_assert(G::IN % 2 == 0, "whole words of bfloat16 input");
-    float va[SPR][IN16 ? 1 : G::PER], vb[SPR][IN16 ? 1 : G::PER];
-    uint32_t wa[SPR][W32 ? PER2 : (WFLAT ? PERF : 1)], wb[SPR][W32 ? PER2 : 1];
+    // registers (hv) and staged into s_in buffer s, as items of eight
+    // channels 8cg .. 8cg+7: bfloat16 input with an even pixel count
+    // (conv2's) is read as 32-bit words of two pixels of one channel, an item
+    // covering pixels 2w, 2w+1 (split by v_perm_b32, moved bit for bit);
+    // otherwise an item is one pixel, its eight values read one by one
+    // (bfloat16 moved as they are, floats rounded as they are staged).
+    constexpr bool PAIRS16 = IN16 && G::IP % 2 == 0;
+    constexpr int NPIX = PAIRS16 ? G::IP / 2 : G::IP;   // items per channel group
+    constexpr int ITEMS = (CIN / 8) * NPIX;
+    constexpr int IPER = (ITEMS + FC_WG - 1) / FC_WG;
+    uint32_t hv[SPR][IPER][8];
     auto fetch = [&](int j) {
-        if constexpr (W32) {
-#pragma unroll
-            for (int s = 0; s < SPR; ++s) {
-                if (j + s >= j_hi) break;
-                const uint32_t* x = (const uint32_t*)((const __bf16*)p.in + (size_t)(j + s) * G::IN);
-#pragma unroll
-                for (int u = 0; u < PER2; ++u) {
-                    const int q = t + u * FC_WG;
-                    if (q < (CIN / 2) * (G::IP / 2)) {
-                        const int cp = q / (G::IP / 2), w = q - cp * (G::IP / 2);
-                        wa[s][u] = x[(2 * cp) * (G::IP / 2) + w];       // channel 2cp, pixels 2w, 2w+1
-                        wb[s][u] = x[(2 * cp + 1) * (G::IP / 2) + w];   // channel 2cp+1
-                    }
-                }
-            }
-            return;
-        }
-        if constexpr (WFLAT) {
-#pragma unroll
-            for (int s = 0; s < SPR; ++s) {
-                if (j + s >= j_hi) break;
-                const uint32_t* x = (const uint32_t*)((const __bf16*)p.in + (size_t)(j + s) * G::IN);
-#pragma unroll
-                for (int u = 0; u < PERF; ++u) {
-                    const int q = t + u * FC_WG;
-                    if (q < G::IN / 2) wa[s][u] = x[q];
-                }
-            }
-            return;
-        }
 #pragma unroll
         for (int s = 0; s < SPR; ++s) {
             if (j + s >= j_hi) break;
             const float* x = p.in + (size_t)(j + s) * G::IN;
-            const __bf16* xh = (const __bf16*)p.in + (size_t)(j + s) * G::IN;
+            const unsigned short* xh = (const unsigned short*)p.in + (size_t)(j + s) * G::IN;
 #pragma unroll
-            for (int u = 0; u < G::PER; ++u) {
+            for (int u = 0; u < IPER; ++u) {
                 const int q = t + u * FC_WG;
-                if (q < G::PAIRS) {
-                    const int cp = q / G::IP, pix = q - cp * G::IP;
-                    if constexpr (IN16) {   // bf16 to float is exact; stage rounds it back unchanged
-                        va[s][u] = (float)xh[(2 * cp) * G::IP + pix];
-                        vb[s][u] = (float)xh[(2 * cp + 1) * G::IP + pix];
-                    } else {
-                        va[s][u] = x[(2 * cp) * G::IP + pix];
-                        vb[s][u] = x[(2 * cp + 1) * G::IP + pix];
+                if (q < ITEMS) {
+                    const int cg = q / NPIX, w = q - cg * NPIX;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        if constexpr (PAIRS16) hv[s][u][e] = ((const uint32_t*)xh)[(8 * cg + e) * (G::IP / 2) + w];
+                        else if constexpr (IN16) hv[s][u][e] = xh[(8 * cg + e) * G::IP + w];
+                        else hv[s][u][e] = __builtin_bit_cast(uint32_t, x[(8 * cg + e) * G::IP + w]);
                     }
                 }
             }
         }
     };
     auto stage = [&](int j) {
-        if constexpr (W32) {
-#pragma unroll
-            for (int s = 0; s < SPR; ++s) {
-                if (j + s >= j_hi) break;
-#pragma unroll
-                for (int u = 0; u < PER2; ++u) {
-                    const int q = t + u * FC_WG;
-                    if (q < (CIN / 2) * (G::IP / 2)) {
-                        const int cp = q / (G::IP / 2), w = q - cp * (G::IP / 2);
-                        const uint32_t a = wa[s][u], b = wb[s][u];
-                        unsigned char* d = s_in + (s * G::IP + 2 * w) * G::PSB + 4 * cp;
-                        *(uint32_t*)d = (a & 0xffffu) | (b << 16);                       // pixel 2w
-                        *(uint32_t*)(d + G::PSB) = (a >> 16) | (b & 0xffff0000u);        // pixel 2w+1
-                    }
-                }
-            }
-            return;
-        }
-        if constexpr (WFLAT) {
-#pragma unroll
-            for (int s = 0; s < SPR; ++s) {
-                if (j + s >= j_hi) break;
-#pragma unroll
-                for (int u = 0; u < PERF; ++u) {
-                    const int q = t + u * FC_WG;
-                    if (q < G::IN / 2) {
-#pragma unroll
-                        for (int h = 0; h < 2; ++h) {   // flat element 2q + h = channel c, pixel pix
-                            const int e = 2 * q + h, c = e / G::IP, pix = e - c * G::IP;
-                            *(uint16_t*)(s_in + (s * G::IP + pix) * G::PSB + 2 * c) =
-                                (uint16_t)(wa[s][u] >> (16 * h));
-                        }
-                    }
-                }
-            }
-            return;
-        }
 #pragma unroll
         for (int s = 0; s < SPR; ++s) {
             if (j + s >= j_hi) break;
 #pragma unroll
-            for (int u = 0; u < G::PER; ++u) {
+            for (int u = 0; u < IPER; ++u) {
                 const int q = t + u * FC_WG;
-                if (q < G::PAIRS) {
-                    const int cp = q / G::IP, pix = q - cp * G::IP;
-                    const uint32_t lo = __builtin_bit_cast(unsigned short, (__bf16)va[s][u]);
-                    const uint32_t hi = __builtin_bit_cast(unsigned short, (__bf16)vb[s][u]);
-                    *(uint32_t*)(s_in + (s * G::IP + pix) * G::PSB + 4 * cp) = lo | (hi << 16);
+                if (q < ITEMS) {
+                    const int cg = q / NPIX, w = q - cg * NPIX;
+                    const uint32_t* h = hv[s][u];
+                    unsigned char* base = s_in + s * G::SLOTS * G::PSB + 16 * cg;
+                    if constexpr (PAIRS16) {
+                        const int pix = 2 * w, y = pix / IH, x = pix - y * IH;   // x even: x + 1 on the same row
+                        uint4 a, b;
+                        a.x = __builtin_amdgcn_perm(h[1], h[0], 0x05040100u);
+                        a.y = __builtin_amdgcn_perm(h[3], h[2], 0x05040100u);
+                        a.z = __builtin_amdgcn_perm(h[5], h[4], 0x05040100u);
+                        a.w = __builtin_amdgcn_perm(h[7], h[6], 0x05040100u);
+                        b.x = __builtin_amdgcn_perm(h[1], h[0], 0x07060302u);
+                        b.y = __builtin_amdgcn_perm(h[3], h[2], 0x07060302u);
+                        b.z = __builtin_amdgcn_perm(h[5], h[4], 0x07060302u);
+                        b.w = __builtin_amdgcn_perm(h[7], h[6], 0x07060302u);
+                        *(uint4*)(base + G::slot(y, x) * G::PSB) = a;
+                        *(uint4*)(base + G::slot(y, x + 1) * G::PSB) = b;
+                    } else {
+                        const int y = w / IH, x = w - y * IH;
+                        uint32_t k[4];
+#pragma unroll
+                        for (int e2 = 0; e2 < 4; ++e2) {
+                            uint32_t lo, hi;
+                            if constexpr (IN16) {
+                                lo = h[2 * e2];
+                                hi = h[2 * e2 + 1];
+                            } else {
+                                lo = __builtin_bit_cast(unsigned short, (__bf16)__builtin_bit_cast(float, h[2 * e2]));
+                                hi = __builtin_bit_cast(unsigned short, (__bf16)__builtin_bit_cast(float, h[2 * e2 + 1]));
+                            }
+                            k[e2] = lo | (hi << 16);
+                        }
+                        *(uint4*)(base + G::slot(y, x) * G::PSB) = uint4{k[0], k[1], k[2], k[3]};
+                    }
                 }
             }
         }
     };
     fetch(j_lo);  // in flight while the weights are loaded
 
-    // Weights: every thread converts its share of W (coalesced float4s) to
-    // bf16 and stores each value where the lane that feeds it to the MFMAs
-    // reads it: lane (li, g) of the wave owning N-tile nt holds, at k-step
-    // ks, W[o][c][tap] for o = 16nt + li, tap = ks / CH, c = 32 (ks % CH) +
-    // 8g + e in element e, at s_w[((nt KS + ks) 64 + lane) 8 + e].
-    {
+    // Weights: from the per-lane copy (PK), or every thread converts its
+    // share of W (coalesced float4s) to bf16 and stores each value where the
+    // lane that feeds it to the MFMAs reads it: lane (li, g) of the wave
+    // owning N-tile nt holds, at k-step ks, W[o][c][tap] for o = 16nt + li,
+    // tap = ks / CH, c = 32 (ks % CH) + 8g + e in element e, at
+    // s_w[((nt KS + ks) 64 + lane) 8 + e].
+    bf16x8 wv[G::KS];
+    if constexpr (PK) {
+        const bf16x8* wp = (const bf16x8*)(second ? p.wpk_b : p.wpk_a);
+#pragma unroll
+        for (int ks = 0; ks < G::KS; ++ks) wv[ks] = wp[(nt * G::KS + ks) * 64 + lane];
+    } else {
         f4 wr[G::WPER];
 #pragma unroll
         for (int u = 0; u < G::WPER; ++u) wr[u] = ((const f4*)W)[t + u * FC_WG];
@@ -222,11 +199,10 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
                 s_w[(((o >> 4) * G::KS + ks) * 64 + ln) * 8 + (c & 7)] = (__bf16)wr[u][v];
             }
         }
-    }
-    __syncthreads();
-    bf16x8 wv[G::KS];
+        __syncthreads();
 #pragma unroll
-    for (int ks = 0; ks < G::KS; ++ks) wv[ks] = *(const bf16x8*)&s_w[((nt * G::KS + ks) * 64 + lane) * 8];
+        for (int ks = 0; ks < G::KS; ++ks) wv[ks] = *(const bf16x8*)&s_w[((nt * G::KS + ks) * 64 + lane) * 8];
+    }
     const float bo = bias[16 * nt + li];
 
     // byte offset in s_in of the lane's first input pixel for each of its
@@ -237,7 +213,7 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
         const int pp = 16 * (mh * G::MPW + i) + li;
         const int pc = pp < G::P ? pp : 0;
         const int oy = pc / OH, ox = pc - oy * OH;
-        pb[i] = ((S * oy) * IH + S * ox) * G::PSB + 16 * g;
+        pb[i] = (oy * G::RP + ox) * G::PSB + 16 * g;
     }
 
     for (int j = j_lo; j < j_hi; j += SPR) {
@@ -256,7 +232,7 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
         constexpr int AHEAD = 2;
         auto a_addr = [&](int ks, int s, int i) {
             const int tap = ks / G::CH;
-            return s_in + s * G::IP * G::PSB + pb[i] + ((tap / K) * IH + tap % K) * G::PSB + 64 * (ks % G::CH);
+            return s_in + s * G::SLOTS * G::PSB + pb[i] + G::slot(tap / K, tap % K) * G::PSB + 64 * (ks % G::CH);
         };
         bf16x8 abuf[AHEAD + 1][SPR][G::MPW];
 #pragma unroll
@@ -308,22 +284,30 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_cl_kernel(FwdClParams p) {
 
 template <int CIN, int IH, int K, int S, int OH, int SPR>
 hipError_t fwd_cl_launch(const float* in, int n_a, int n, const float* w_a, const float* b_a, const float* w_b,
-                         const float* b_b, float* out, bool in16, bool out16, hipStream_t st) {
+                         const float* b_b, float* out, bool in16, bool out16, const float* pk_a, const float* pk_b,
+                         hipStream_t st) {
     using G = FwdClGeom<CIN, IH, K, S, OH, SPR>;
     if (n <= 0 || n_a < 0 || n_a > n) return hipErrorInvalidValue;
     if (((uintptr_t)w_a & 15) || ((uintptr_t)w_b & 15) || ((uintptr_t)out & 15)) return hipErrorInvalidValue;
+    // the packed weights: both sets or neither, 16-byte aligned
+    if (!pk_a != !pk_b || ((uintptr_t)pk_a & 15) || ((uintptr_t)pk_b & 15)) return hipErrorInvalidValue;
     const int spg = std::max(1, (n + FC_TARGET_BLOCKS - 1) / FC_TARGET_BLOCKS);
     const int g_a = (n_a + spg - 1) / spg, g_b = (n - n_a + spg - 1) / spg;
-    const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg, nullptr, nullptr};
+    const FwdClParams prm{in, out, w_a, b_a, w_b, b_b, n, n_a, g_a, spg, pk_a, pk_b};
     auto go = [&](auto kern) -> hipError_t {
         if (!allow_lds((const void*)kern, G::LDS)) return hipErrorInvalidValue;
         hipLaunchKernelGGL(kern, dim3((unsigned)(g_a + g_b)), dim3(FC_WG), G::LDS, st, prm);
         return hipGetLastError();
     };
-    if (in16 && out16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, true, true>);
-    if (in16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, true, false>);
-    if (out16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, false, true>);
-    return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, false, false>);
+    if (pk_a) {   // (the TD step's bf16 activations)
+        if (in16 && out16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, true, true, true>);
+        if (in16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, true, false, true>);
+        return hipErrorInvalidValue;
+    }
+    if (in16 && out16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, true, true, false>);
+    if (in16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, true, false, false>);
+    if (out16) return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, false, true, false>);
+    return go(conv_fwd_cl_kernel<CIN, IH, K, S, OH, SPR, false, false, false>);
 }
 
 // The float32 variant on bf16 MFMA: every float32 operand is split exactly
@@ -599,10 +583,12 @@ hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const 
     if (!bf16 && (in16 || out16)) return hipErrorInvalidValue;   // bf16 activations: the bf16 variant only
     switch (id) {
         case CONV_L2:
-            return bf16 ? fwd_cl_launch<32, 20, 4, 2, 9, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, st)
+            return bf16 ? fwd_cl_launch<32, 20, 4, 2, 9, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, pk_a, pk_b,
+                                                            st)
                         : fwd_x6_launch<32, 20, 4, 2, 9>(in, n_a, n, w_a, b_a, w_b, b_b, out, pk_a, pk_b, st);
         case CONV_L3:
-            return bf16 ? fwd_cl_launch<64, 9, 3, 1, 7, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, st)
+            return bf16 ? fwd_cl_launch<64, 9, 3, 1, 7, 1>(in, n_a, n, w_a, b_a, w_b, b_b, out, in16, out16, pk_a, pk_b,
+                                                           st)
                         : fwd_x6_launch<64, 9, 3, 1, 7>(in, n_a, n, w_a, b_a, w_b, b_b, out, pk_a, pk_b, st);
         default: return hipErrorInvalidValue;
     }
