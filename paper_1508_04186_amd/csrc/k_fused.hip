@@ -893,7 +893,12 @@ hipError_t launch_conv1_u8_fwd(ConvId id, const ConvIn& in_a, const ConvIn& in_b
 // (e < 8), two groups of four within rows; pixels 400..415 of the last step
 // are zero in the planes.  Wave w owns N-tiles (weight columns) 2w, 2w+1 and
 // every M-tile (output channel block); the next sample's dz and bytes are
-// read into registers during the current sample's MFMAs.
+// read into registers during the current sample's MFMAs.  With one dz plane
+// (the bf16-input variant) the phases are staged already converted to
+// bfloat16 (two bytes an entry, 105 KB), so a B operand is two 8-byte reads;
+// with three the LDS holds only the bytes, converted as they are read.  The
+// pixel-group offsets of a lane are formed once, and each k-step's operands
+// are read while the previous step multiplies.
 namespace dqn {
 namespace {
 
@@ -908,7 +913,8 @@ constexpr int UW_ITEMS = C0 * H0 * 5;           // (channel, row, 16-byte column
 constexpr int UW_IPER = (UW_ITEMS + UW_WG - 1) / UW_WG;
 static_assert(32 * UW_STEPS <= UW_LDZ && UW_P % 4 == 0 && H1 % 4 == 0, "pixel groups of four within rows");
 
-constexpr size_t uw_lds(int cout, int parts) { return (size_t)parts * cout * UW_LDZ * 2 + UW_PH; }
+// (phase entries of two bytes with one plane: bfloat16)
+constexpr size_t uw_lds(int cout, int parts) { return (size_t)parts * cout * UW_LDZ * 2 + (size_t)UW_PH * (parts == 1 ? 2 : 1); }
 
 struct U8WgradParams {
     ConvIn in;            // network input (bytes)
@@ -929,6 +935,8 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
     static_assert(PARTS == 1 || PARTS == 3, "exact split or bf16 rounding");
     static_assert(!DZ16 || PARTS == 1, "bfloat16 dz is one plane");
     static_assert(KW1 == 16 * 16 && COUT % 16 == 0, "16 N-tiles of weight columns, 2 per wave");
+    constexpr bool PH16 = PARTS == 1;      // phases staged as bfloat16
+    constexpr int PHB = PH16 ? 2 : 1;      // bytes per phase entry
     extern __shared__ __align__(16) unsigned char smem[];
     __bf16* s_dz = (__bf16*)smem;                                   // [PARTS][COUT][UW_LDZ]
     unsigned char* s_ph = smem + (size_t)PARTS * COUT * UW_LDZ * 2;  // [C0][H0][8][20]
@@ -1021,25 +1029,70 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
                     const uint32_t sel = (uint32_t)m | ((uint32_t)(4 + m) << 8) | 0x0c0c0000u;
                     const uint32_t lo2 = __builtin_amdgcn_perm(vb[u][d + 1], vb[u][d], sel);
                     const uint32_t hi2 = __builtin_amdgcn_perm(vb[u][d + 3], vb[u][d + 2], sel);
-                    *(uint32_t*)(s_ph + (row * 8 + kx) * H1 + 4 * qb) = __builtin_amdgcn_perm(hi2, lo2, 0x05040100u);
+                    const uint32_t w = __builtin_amdgcn_perm(hi2, lo2, 0x05040100u);
+                    if constexpr (PH16) {   // the four bytes as bfloat16 (exact)
+                        bf16x4 h;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) h[e] = (__bf16)(float)((w >> (8 * e)) & 0xffu);
+                        *(bf16x4*)(s_ph + ((row * 8 + kx) * H1 + 4 * qb) * 2) = h;
+                    } else {
+                        *(uint32_t*)(s_ph + (row * 8 + kx) * H1 + 4 * qb) = w;
+                    }
                 }
             }
         }
     };
 
-    // weight column (c, ky, kx) of this lane in each of its two N-tiles
+    // weight column (c, ky, kx) of this lane in each of its two N-tiles (byte offsets)
     int cb[2];
 #pragma unroll
     for (int n = 0; n < 2; ++n) {
         const int col = (2 * wave + n) * 16 + li;
         const int c = col / (K1 * K1), ky = (col / K1) % K1, kx = col % K1;
-        cb[n] = ((c * H0 + ky) * 8 + kx) * H1;
+        cb[n] = ((c * H0 + ky) * 8 + kx) * H1 * PHB;
     }
+    // phase byte offsets of the lane's pixel groups 32 st + 8 g + 4 h (pixels
+    // past 400 read row 0: their dz is zero)
+    int po[UW_STEPS][2];
+#pragma unroll
+    for (int st = 0; st < UW_STEPS; ++st)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int pp = 32 * st + 8 * g + 4 * h;
+            const int y = pp < UW_P ? pp / H1 : 0, x = pp < UW_P ? pp - (pp / H1) * H1 : 0;
+            po[st][h] = (S1 * y * 8 * H1 + x) * PHB;
+        }
     f4 acc[MT][2];
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
         for (int n = 0; n < 2; ++n) acc[m][n] = f4{0.f, 0.f, 0.f, 0.f};
+
+    // operands of k-step st into buffer slot
+    bf16x8 bb[2][2], aa[2][MT][PARTS];
+    auto operands = [&](int st, int slot) {
+#pragma unroll
+        for (int n = 0; n < 2; ++n) {
+            if constexpr (PH16) {
+                const uint2 w0 = *(const uint2*)(s_ph + cb[n] + po[st][0]);
+                const uint2 w1 = *(const uint2*)(s_ph + cb[n] + po[st][1]);
+                bb[slot][n] = __builtin_bit_cast(bf16x8, uint4{w0.x, w0.y, w1.x, w1.y});
+            } else {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const uint32_t w = *(const uint32_t*)(s_ph + cb[n] + po[st][h]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) bb[slot][n][4 * h + e] = (__bf16)(float)((w >> (8 * e)) & 0xffu);
+                }
+            }
+        }
+        const int p0 = 32 * st + 8 * g;
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int part = 0; part < PARTS; ++part)
+                aa[slot][m][part] = *(const bf16x8*)(s_dz + (part * COUT + m * 16 + li) * UW_LDZ + p0);
+    };
 
     load(j0);
     for (int j = j0; j < j1; ++j) {
@@ -1047,34 +1100,17 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
         stage();
         __syncthreads();
         if (j + 1 < j1) load(j + 1);
+        operands(0, 0);
+#pragma unroll
         for (int st = 0; st < UW_STEPS; ++st) {
-            const int p0 = 32 * st + 8 * g;
-            // phase offsets of the two pixel groups (pixels past 400 read row 0: their dz is zero)
-            int po[2];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int pp = p0 + 4 * h;
-                const int y = pp < UW_P ? pp / H1 : 0, x = pp < UW_P ? pp - (pp / H1) * H1 : 0;
-                po[h] = S1 * y * 8 * H1 + x;
-            }
-            bf16x8 b[2];
-#pragma unroll
-            for (int n = 0; n < 2; ++n) {
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const uint32_t w = *(const uint32_t*)(s_ph + cb[n] + po[h]);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) b[n][4 * h + e] = (__bf16)(float)((w >> (8 * e)) & 0xffu);
-                }
-            }
+            if (st + 1 < UW_STEPS) operands(st + 1, (st + 1) & 1);   // read while step st multiplies
+            const int sl = st & 1;
 #pragma unroll
             for (int m = 0; m < MT; ++m)
 #pragma unroll
-                for (int part = 0; part < PARTS; ++part) {
-                    const bf16x8 a = *(const bf16x8*)(s_dz + (part * COUT + m * 16 + li) * UW_LDZ + p0);
+                for (int part = 0; part < PARTS; ++part)
 #pragma unroll
-                    for (int n = 0; n < 2; ++n) acc[m][n] = mfma16x16x32bf16(a, b[n], acc[m][n]);
-                }
+                    for (int n = 0; n < 2; ++n) acc[m][n] = mfma16x16x32bf16(aa[sl][m][part], bb[sl][n], acc[m][n]);
         }
     }
     // D[4g + r][li] of tile (m, n): channel m*16 + 4g + r, column (2 wave + n)*16 + li
