@@ -155,8 +155,14 @@ struct TdLayout {
     __bf16* dz1h;         // dz1 in bfloat16 (bf16-input variant from 128 samples), else null
     float *wpk2, *wpk3;   // repacked conv2/conv3 weights of the input gradients (large network)
     float *fpk[2][2];     // ... the fp32 forward's bf16 planes: [layer conv2, conv3][set theta, theta^-]
+    float* fc1w_part;     // the float32 fc1 weight gradient's k-slices (large batch, wide layer), else null
     size_t bytes;
 };
+
+// The float32 fc1 weight gradient of a large batch and a 512-wide hidden
+// layer is computed as kGemmX6WgradSlices k-slices of partial sums (larger
+// tiles), which the finalize adds.
+bool fc1w_split(const NetInfo& ni, int B) { return !ni.bf16 && B >= kGemmX6MinRows && ni.H >= 512; }
 
 TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
     TdLayout t{};
@@ -200,6 +206,7 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
     // (from 128 samples, where the fc1 gradients are separate launches; kept
     // out of smaller workspaces)
     if (ni.bf16 && B >= 128) t.dz1h = cv.take<__bf16>(ws, (int64_t)B * ni.H);
+    if (fc1w_split(ni, B)) t.fc1w_part = cv.take<float>(ws, (int64_t)kGemmX6WgradSlices * ni.H * ni.flat);
     t.bytes = cv.off;
     return t;
 }
@@ -479,9 +486,16 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
         // the bf16-input variant reads the head's bfloat16 copy of dz1 (the
         // same rounding the staging would apply)
         const float* dzA = t.dz1h ? (const float*)t.dz1h : t.dz1;
-        RUN(DQN_K_FC1_WGRAD,
-            launch_gemm(GEMM_TN, ni.H, ni.flat, B, dzA, ni.H, xlast, ni.flat, grad_out + ni.w_off[L], ni.flat, 1,
-                        (B + 31) / 32 * 32, 0, nullptr, ni.bf16, a16, st, t.dz1h != nullptr));
+        if (t.fc1w_part) {   // k-slices of ceil(B / 128) * 64 samples (the last one at most that)
+            constexpr int S = kGemmX6WgradSlices;
+            RUN(DQN_K_FC1_WGRAD,
+                launch_gemm(GEMM_TN, ni.H, ni.flat, B, t.dz1, ni.H, xlast, ni.flat, t.fc1w_part, ni.flat, S,
+                            (B + 64 * S - 1) / (64 * S) * 64, (int64_t)ni.H * ni.flat, nullptr, false, false, st));
+        } else {
+            RUN(DQN_K_FC1_WGRAD,
+                launch_gemm(GEMM_TN, ni.H, ni.flat, B, dzA, ni.H, xlast, ni.flat, grad_out + ni.w_off[L], ni.flat, 1,
+                            (B + 31) / 32 * 32, 0, nullptr, ni.bf16, a16, st, t.dz1h != nullptr));
+        }
         RUN(DQN_K_FC1_DGRAD,
             launch_gemm(GEMM_NN, B, ni.flat, ni.H, dzA, ni.H, th + ni.w_off[L], ni.flat, t.dconv[L - 1], ni.flat, 1,
                         (ni.H + 31) / 32 * 32, 0, xlast, ni.bf16, a16, st, t.dz1h != nullptr));
@@ -580,6 +594,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     fa.grad_base = grad_out;
     fa.fc1w_off = ni.w_off[L];
     fa.fc1w_count = (int64_t)ni.H * ni.flat;
+    fa.fc1w_part = t.fc1w_part;
+    fa.fc1w_slices = t.fc1w_part ? kGemmX6WgradSlices : 0;
     fa.spart = t.spart;
     fa.schunks = finalize_sample_chunks(B);
     if (upd)

@@ -397,10 +397,14 @@ void gemm_fwd_split(int rows, int N, int K, int* ks, int* kchunk);
 // gradient, K of the weight gradient) the float32 fc1 contractions run on
 // bf16 MFMA with the exact three-plane split (launch_gemm_x6: same arguments
 // as launch_gemm, kchunk a multiple of 32): the forward on 128x256 tiles,
-// the weight and input gradients (operands contiguous along m or n,
-// transposed as they are staged) on 64x64 tiles, batch 2,048: 80 -> 77 us
-// and 77 -> 68 us.  Below that batch the split cost more than the six
-// products saved.
+// the input gradient (B contiguous along n, transposed as it is staged) on
+// 64x64 tiles, batch 2,048: 77 -> 68 us; the weight gradient (both operands
+// transposed) on 64x64 tiles, or, split into kGemmX6WgradSlices k-slices of
+// partial sums, on 128x128 tiles with 64-wide k-stages (each staged operand
+// value then serves twice the products; batch 2,048: 77 -> 63 us, the
+// finalize adding the slices).  Below that batch the split cost more than
+// the six products saved.
+constexpr int kGemmX6WgradSlices = 2;
 constexpr int kGemmX6MinRows = 1024;
 void gemm_fwd_split_x6(int rows, int N, int K, int* ks, int* kchunk);
 hipError_t launch_gemm_x6(GemmKind kind, int M, int N, int K, const float* A, int lda, const float* B, int ldb,
@@ -475,9 +479,13 @@ struct FinalizeArgs {
     int B, H, A;
     float *g_b1, *g_W2, *g_b2, *loss_out;
     // Gradient vector the gw/gb/g_* pointers point into, and the range of it
-    // (the fc1 weights) that an earlier kernel wrote in full.
+    // (the fc1 weights) that an earlier kernel wrote in full, or, with
+    // fc1w_part set, wrote as fc1w_slices partial sums fc1w_part[z][i] (k
+    // split into slices) that the finalize adds in slice order.
     const float* grad_base;
     int64_t fc1w_off, fc1w_count;
+    const float* fc1w_part;
+    int fc1w_slices;
     // Above 128 samples: sample-sum partial slots, one per chunk of 32
     // samples, each A*H + H + A + 1 floats (workspace).
     float* spart;

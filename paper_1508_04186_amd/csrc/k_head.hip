@@ -510,12 +510,26 @@ __device__ __forceinline__ void emit(const FinalizeArgs& a, const PsUpdate& u, f
     }
 }
 
+// The fc1 weights, four per thread: the gradient stored (MODE < 0, only
+// with slices to add) or applied; with fc1w_part, the slices' sum in slice
+// order.
 template <int MODE>
 __device__ __forceinline__ void apply_fc1w(const FinalizeArgs& a, const PsUpdate& u, int64_t i4) {
     if (i4 >= a.fc1w_count / 4) return;
     const int64_t off = a.fc1w_off + 4 * i4;
+    f4 gv;
+    if (a.fc1w_part) {
+        gv = *(const f4*)(a.fc1w_part + 4 * i4);
+        for (int z = 1; z < a.fc1w_slices; ++z) gv += *(const f4*)(a.fc1w_part + (int64_t)z * a.fc1w_count + 4 * i4);
+        if constexpr (MODE < 0) {
+            *(f4*)(const_cast<float*>(a.grad_base) + off) = gv;
+            return;
+        }
+    } else {
+        gv = *(const f4*)(a.grad_base + off);
+    }
+    if constexpr (MODE < 0) return;   // (no slices: the gradient is already in place)
     f4 th = *(const f4*)(u.theta + off);
-    const f4 gv = *(const f4*)(a.grad_base + off);
     f4 sv = f4{0.f, 0.f, 0.f, 0.f};
     if constexpr (MODE != 0) sv = *(const f4*)(u.state + off);
 #pragma unroll
@@ -539,11 +553,9 @@ __device__ __forceinline__ int clamp_action(int a, int A) { return min(max(a, 0)
 // batch 32 (6.6 against 7.1 us under rocprofv3).
 template <int MODE>
 __global__ __launch_bounds__(256) void finalize_small_kernel(FinalizeArgs a, PsUpdate u, int n_fin) {
-    if constexpr (MODE >= 0) {
-        if ((int)blockIdx.x >= n_fin) {
-            apply_fc1w<MODE>(a, u, (int64_t)(blockIdx.x - n_fin) * 256 + threadIdx.x);
-            return;
-        }
+    if ((int)blockIdx.x >= n_fin) {   // (launched for MODE < 0 only with slices to add)
+        apply_fc1w<MODE>(a, u, (int64_t)(blockIdx.x - n_fin) * 256 + threadIdx.x);
+        return;
     }
     int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 3;
     const bool lead = (threadIdx.x & 7) == 0;
@@ -687,11 +699,9 @@ constexpr int FW_U = 32;   // slots in flight per lane
 constexpr int FW_L = 4;    // lanes per output
 template <int MODE>
 __global__ __launch_bounds__(256) void finalize_wide_kernel(FinalizeArgs a, PsUpdate u, int n_fin) {
-    if constexpr (MODE >= 0) {
-        if ((int)blockIdx.x >= n_fin) {
-            apply_fc1w<MODE>(a, u, (int64_t)(blockIdx.x - n_fin) * 256 + threadIdx.x);
-            return;
-        }
+    if ((int)blockIdx.x >= n_fin) {   // (launched for MODE < 0 only with slices to add)
+        apply_fc1w<MODE>(a, u, (int64_t)(blockIdx.x - n_fin) * 256 + threadIdx.x);
+        return;
     }
     // FW_L consecutive lanes share an output (a group exits or stays as one)
     const int ql = threadIdx.x & (FW_L - 1);
@@ -800,12 +810,14 @@ hipError_t finalize_wide_launch(const FinalizeArgs& a, const PsUpdate* upd, hipS
     int64_t total = (int64_t)A * a.H + a.H + A + 1;
     for (int l = 0; l < a.n_conv; ++l) total += a.wcount[l] + a.cout[l];
     const int n_fin = (int)((total * FW_L + 255) / 256);
+    if ((upd || a.fc1w_part) && (a.fc1w_off % 4 != 0 || a.fc1w_count % 4 != 0 || !a.grad_base))
+        return hipErrorInvalidValue;
+    const int n_w = upd || a.fc1w_part ? (int)((a.fc1w_count / 4 + 255) / 256) : 0;
+    const dim3 grid((unsigned)(n_fin + n_w));
     if (!upd) {
-        hipLaunchKernelGGL(finalize_wide_kernel<-1>, dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{}, n_fin);
+        hipLaunchKernelGGL(finalize_wide_kernel<-1>, grid, dim3(256), 0, st, a, PsUpdate{}, n_fin);
         return hipGetLastError();
     }
-    if (a.fc1w_off % 4 != 0 || a.fc1w_count % 4 != 0 || !a.grad_base) return hipErrorInvalidValue;
-    const dim3 grid((unsigned)(n_fin + (a.fc1w_count / 4 + 255) / 256));
     switch (upd->rule) {
         case 0: hipLaunchKernelGGL(finalize_wide_kernel<0>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
         case 1: hipLaunchKernelGGL(finalize_wide_kernel<1>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
@@ -819,12 +831,14 @@ hipError_t finalize_small_launch(const FinalizeArgs& a, const PsUpdate* upd, hip
     int64_t total = a.H + (int64_t)a.A * a.H + a.A + 1;
     for (int l = 0; l < a.n_conv; ++l) total += a.wcount[l] + a.cout[l];
     const int n_fin = (int)((total * 8 + 255) / 256);
+    if ((upd || a.fc1w_part) && (a.fc1w_off % 4 != 0 || a.fc1w_count % 4 != 0 || !a.grad_base))
+        return hipErrorInvalidValue;
+    const int n_w = upd || a.fc1w_part ? (int)((a.fc1w_count / 4 + 255) / 256) : 0;
+    const dim3 grid((unsigned)(n_fin + n_w));
     if (!upd) {
-        hipLaunchKernelGGL(finalize_small_kernel<-1>, dim3((unsigned)n_fin), dim3(256), 0, st, a, PsUpdate{}, n_fin);
+        hipLaunchKernelGGL(finalize_small_kernel<-1>, grid, dim3(256), 0, st, a, PsUpdate{}, n_fin);
         return hipGetLastError();
     }
-    if (a.fc1w_off % 4 != 0 || a.fc1w_count % 4 != 0 || !a.grad_base) return hipErrorInvalidValue;
-    const dim3 grid((unsigned)(n_fin + (a.fc1w_count / 4 + 255) / 256));
     switch (upd->rule) {
         case 0: hipLaunchKernelGGL(finalize_small_kernel<0>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
         case 1: hipLaunchKernelGGL(finalize_small_kernel<1>, grid, dim3(256), 0, st, a, *upd, n_fin); break;
