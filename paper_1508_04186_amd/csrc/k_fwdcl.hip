@@ -17,8 +17,7 @@
 // of eight channels at one pixel, one 16-byte store each.  A round takes SPR
 // samples; the next round's input is read from HBM into registers during
 // the current round's MFMAs, and the output maps are assembled in LDS and
-// written as whole 16-byte vectors.  Weights reach the registers as 16-byte
-// vectors from the repack launch's per-lane copies (the TD step), or through
+// written as whole 16-byte vectors.  Weights reach the registers through
 // LDS: coalesced loads, converted to bf16 and stored in the order the lanes
 // read them.
 #include <algorithm>
