@@ -189,7 +189,8 @@ TdLayout td_layout(const NetInfo& ni, int B, void* ws) {
             slots = std::max<int64_t>(slots, conv_s12_bwd_slots(B));
         if (igemm_wgrad(ni.conv[l], B, ni.bf16))
             slots = std::max<int64_t>(slots, conv_igemm_wgrad_chunks(ni.conv[l], B));
-        if (reg_wgrad(ni.conv[l], B, ni.bf16)) slots = std::max<int64_t>(slots, conv_wgrad_reg_slots(ni.conv[l], B));
+        if (reg_wgrad(ni.conv[l], B, ni.bf16))
+            slots = std::max<int64_t>(slots, conv_wgrad_reg_slots(ni.conv[l], B, ni.bf16));
         if (l == 0 && conv1_u8(ni.conv[0], B, ni.bf16)) slots = std::max<int64_t>(slots, conv1_u8_wgrad_slots(B));
         t.wpart[l] = cv.take<float>(ws, slots * c.cout * c.cin * c.k * c.k);
         t.bpart[l] = cv.take<float>(ws, slots * c.cout);
@@ -538,7 +539,7 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             RUN(DQN_K_CONV1_WGRAD + l,
                 launch_conv_wgrad_reg(ni.conv[l], t.act[l - 1], t.dconv[l], B, t.wpart[l], t.bpart[l], ni.bf16,
                                       a16, st));
-            chunks_used[l] = conv_wgrad_reg_slots(ni.conv[l], B);
+            chunks_used[l] = conv_wgrad_reg_slots(ni.conv[l], B, ni.bf16);
         } else if (igemm_wgrad(ni.conv[l], B, ni.bf16)) {
             RUN(DQN_K_CONV1_WGRAD + l,
                 launch_conv_igemm_wgrad(ni.conv[l], in, t.dconv[l], B, t.wpart[l], t.bpart[l], scale,

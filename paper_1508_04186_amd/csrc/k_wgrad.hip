@@ -20,6 +20,10 @@
 // vanish.  B operand in[c][S*oy + ky][S*ox + kx]: a per-lane column base
 // plus a per-step pixel base.  Both precisions: fp32 MFMA (pixel 4s + g in
 // step s), or the bf16-input variant (pixel 32s + 4e + g in element e).
+// Below, the kernels that stage row segments (every MFMA operand one
+// 16-byte LDS read): the bf16-input variant's with bfloat16 activations, and
+// the float32 one from 512 samples on bf16 MFMA with the exact three-plane
+// split (batch 2,048: conv2 108.6 -> 96.2 us, conv3 73.0 -> 49.3 us).
 #include <algorithm>
 #include <type_traits>
 
@@ -456,6 +460,261 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_seg_kernel(WgradRegParams p)
     if (t < G::COUT) p.bpart[(size_t)slot * G::COUT + t] = bsum;
 }
 
+// The float32 weight gradient on bf16 MFMA (from kWgradX6MinRows samples):
+// dz and the layer input split exactly into three bfloat16 planes as they
+// are staged (split3, hi + mid + lo), each plane in the segment layout of
+// conv_wgrad_seg_kernel, and per k-step the six products of planes whose
+// product is at least 2^-16 of hi*hi (as the float32 forward), which keeps
+// float32 accuracy.  The fp32-MFMA kernel above is bound by the fp32 matrix
+// rate (87-90% of its cycles busy at batch 2,048); six bf16 products take
+// half that time at the measured rates.  Three planes of conv2's row
+// segments do not fit in LDS with all 32 input channels: its workgroups
+// take NSPLIT = 2 halves of them, two workgroups per slot (each staging the
+// whole dz), which also halves the slots for the finalize to read.  The
+// bias sums come from the float32 dz, as in the kernel above.
+template <int CIN, int IH, int K, int S, int OH, int NSPLIT>
+struct SegX6Geom {
+    static constexpr int COUT = 64, P = OH * OH, KK = K * K;
+    static constexpr int CW = CIN / NSPLIT;                // input channels per workgroup
+    static constexpr int KT = CW * KK, KTF = CIN * KK;     // weight columns: the workgroup's, the layer's
+    static constexpr int NTT = KT / 16, NPW = NTT / 4;
+    static constexpr bool COL9 = OH > 8;
+    static constexpr int NROW = OH;
+    static constexpr int NSEG = COL9 ? OH + 2 : OH;
+    static constexpr int STEPS = (NSEG + 3) / 4;
+    static constexpr int DZS = 4 * STEPS * 8 + 8;           // dz row stride (bf16; an odd number of 16-byte chunks)
+    static constexpr int RSEG = CW * IH * K * 8;           // [c][y][kx][8]
+    static constexpr int CSEG = COL9 ? CW * KK * 8 : 0;    // [c][ky][kx][8]: rows 0..7, and row 8 (element 0)
+    static constexpr int O_CSEG = RSEG, O_CSEG2 = O_CSEG + CSEG, O_ZERO = O_CSEG2 + CSEG, O_DZ = O_ZERO + 8;
+    static constexpr int PLANE = O_DZ + COUT * DZS;        // bf16 elements per plane
+    static constexpr int LDS = 3 * PLANE * 2 + COUT * OH * 4;   // bytes, with the dz row sums
+    static constexpr int DZ_ITEMS = COUT * OH, IN_ITEMS = CW * IH;   // (o, output row), (c, input row)
+    static constexpr int DZ_PER = (DZ_ITEMS + WR_WG - 1) / WR_WG, IN_PER = (IN_ITEMS + WR_WG - 1) / WR_WG;
+    static_assert(CIN % NSPLIT == 0 && NTT % 4 == 0 && (DZS / 8) % 2 == 1 && PLANE % 8 == 0 && OH <= 9 &&
+                      (S == 1 || (S == 2 && IH == 20 && K == 4 && OH == 9)) && (S == 2 || (IH == 9 && K == 3 && OH == 7)),
+                  "the large network's conv2 and conv3");
+};
+
+template <int CIN, int IH, int K, int S, int OH, int NSPLIT>
+__global__ __launch_bounds__(WR_WG) void conv_wgrad_seg_x6_kernel(WgradRegParams p) {
+    using G = SegX6Geom<CIN, IH, K, S, OH, NSPLIT>;
+    extern __shared__ __align__(16) float smem[];
+    __bf16* s16 = (__bf16*)smem;                        // three planes of PLANE elements
+    float* s_bs = smem + 3 * G::PLANE / 2;              // [64][OH] row sums of dz
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int li = lane & 15, g = lane >> 4;
+    const int mh = wave >> 2, ng = wave & 3;
+    const int slot = blockIdx.x / NSPLIT, part = blockIdx.x % NSPLIT;
+    const int c0 = part * G::CW;                        // the workgroup's first input channel
+
+    // zero segments, and the dz slots no pixel writes, stay zero in every plane
+#pragma unroll
+    for (int pl = 0; pl < 3; ++pl)
+        for (int e = t; e < (G::PLANE - G::O_CSEG2) / 8; e += WR_WG)
+            *(uint4*)(s16 + pl * G::PLANE + G::O_CSEG2 + 8 * e) = uint4{0u, 0u, 0u, 0u};
+
+    const int j_lo = slot * p.spg, j_hi = min(p.n, j_lo + p.spg);
+
+    // B operand bases of the lane's column (of the workgroup's columns) in each N-tile
+    int rbase[G::NPW], cbase[G::NPW];
+#pragma unroll
+    for (int i = 0; i < G::NPW; ++i) {
+        const int n = (ng * G::NPW + i) * 16 + li;
+        const int c = n / G::KK, r = n - c * G::KK, ky = r / K, kx = r - ky * K;
+        rbase[i] = ((c * IH + ky) * K + kx) * 8;
+        cbase[i] = G::O_CSEG + ((c * K + ky) * K + kx) * 8;
+    }
+    auto boff = [&](int sg, int i) -> int {
+        if (sg < G::NROW) return rbase[i] + S * sg * K * 8;
+        if (G::COL9 && sg == G::NROW) return cbase[i];
+        if (G::COL9 && sg == G::NROW + 1) return cbase[i] + G::CSEG;
+        return G::O_ZERO;
+    };
+    int arow[2];
+#pragma unroll
+    for (int m = 0; m < 2; ++m) arow[m] = G::O_DZ + ((2 * mh + m) * 16 + li) * G::DZS + 8 * g;
+
+    f4 acc[2][G::NPW];
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int i = 0; i < G::NPW; ++i) acc[m][i] = f4{0.f, 0.f, 0.f, 0.f};
+    float bsum = 0.f;
+
+    // next sample in registers: dz rows (o, oy) and the workgroup's input rows (c, y)
+    float vdz[G::DZ_PER][OH];
+    float vin[G::IN_PER][IH];
+    auto fetch = [&](int j) {
+        const float* dzj = p.dz + (size_t)j * G::COUT * G::P;
+        const float* inj = p.in + ((size_t)j * CIN + c0) * IH * IH;
+#pragma unroll
+        for (int u = 0; u < G::DZ_PER; ++u) {
+            const int q = t + u * WR_WG;
+            if (q < G::DZ_ITEMS) {
+#pragma unroll
+                for (int x = 0; x < OH; ++x) vdz[u][x] = dzj[q * OH + x];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < G::IN_PER; ++u) {
+            const int q = t + u * WR_WG;
+            if (q < G::IN_ITEMS) {
+                if constexpr (IH % 4 == 0) {   // 16-byte aligned rows
+                    const f4* w = (const f4*)(inj + q * IH);
+#pragma unroll
+                    for (int d = 0; d < IH / 4; ++d) {
+                        const f4 v = w[d];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) vin[u][4 * d + e] = v[e];
+                    }
+                } else {
+#pragma unroll
+                    for (int x = 0; x < IH; ++x) vin[u][x] = inj[q * IH + x];
+                }
+            }
+        }
+    };
+    // the three planes' bits of a value
+    auto split_bits = [](float f, uint32_t (&b)[3]) {
+        __bf16 h, m, l;
+        split3(f, h, m, l);
+        b[0] = __builtin_bit_cast(unsigned short, h);
+        b[1] = __builtin_bit_cast(unsigned short, m);
+        b[2] = __builtin_bit_cast(unsigned short, l);
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < G::DZ_PER; ++u) {
+            const int q = t + u * WR_WG;
+            if (q < G::DZ_ITEMS) {
+                const int o = q / OH, oy = q - o * OH;
+                uint32_t hb[OH][3];
+#pragma unroll
+                for (int x = 0; x < OH; ++x) split_bits(vdz[u][x], hb[x]);
+#pragma unroll
+                for (int pl = 0; pl < 3; ++pl) {
+                    uint32_t w[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const uint32_t lo = 2 * k < OH ? hb[2 * k][pl] : 0u;
+                        const uint32_t hi = 2 * k + 1 < OH ? hb[2 * k + 1][pl] : 0u;
+                        w[k] = lo | (hi << 16);
+                    }
+                    __bf16* row = s16 + pl * G::PLANE + G::O_DZ + o * G::DZS;
+                    *(uint4*)(row + 8 * oy) = uint4{w[0], w[1], w[2], w[3]};
+                    if constexpr (G::COL9)   // ox = 8: segment NROW (rows 0..7) or NROW + 1 (row 8)
+                        *(unsigned short*)(row + (oy < 8 ? 8 * G::NROW + oy : 8 * (G::NROW + 1))) =
+                            (unsigned short)hb[8][pl];
+                }
+                float rs = 0.f;
+#pragma unroll
+                for (int x = 0; x < OH; ++x) rs += vdz[u][x];
+                s_bs[q] = rs;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < G::IN_PER; ++u) {
+            const int q = t + u * WR_WG;
+            if (q < G::IN_ITEMS) {
+                const int c = q / IH, y = q - c * IH;
+                uint32_t hb[IH][3];
+#pragma unroll
+                for (int x = 0; x < IH; ++x) split_bits(vin[u][x], hb[x]);
+#pragma unroll
+                for (int pl = 0; pl < 3; ++pl) {
+                    __bf16* seg = s16 + pl * G::PLANE + (c * IH + y) * K * 8;
+                    if constexpr (G::COL9) {
+                        // words w_i = (x_2i, x_2i+1); kx even: x_{2e + kx} = lo(w_{e + kx/2}), odd: hi(...)
+                        uint32_t w[IH / 2];
+#pragma unroll
+                        for (int d = 0; d < IH / 2; ++d) w[d] = hb[2 * d][pl] | (hb[2 * d + 1][pl] << 16);
+#pragma unroll
+                        for (int kx = 0; kx < 4; ++kx) {
+                            const int d = kx >> 1;
+                            const uint32_t sel = (kx & 1) ? 0x07060302u : 0x05040100u;
+                            uint4 v;
+                            v.x = __builtin_amdgcn_perm(w[d + 1], w[d + 0], sel);
+                            v.y = __builtin_amdgcn_perm(w[d + 3], w[d + 2], sel);
+                            v.z = __builtin_amdgcn_perm(w[d + 5], w[d + 4], sel);
+                            v.w = __builtin_amdgcn_perm(w[d + 7], w[d + 6], sel);
+                            *(uint4*)(seg + kx * 8) = v;
+                        }
+                        // ninth column: x_{16 + kx} to segment (c, ky, kx) element (y - ky) / 2 for ky of y's parity
+#pragma unroll
+                        for (int kx = 0; kx < 4; ++kx) {
+                            const unsigned short v = (unsigned short)hb[16 + kx][pl];
+#pragma unroll
+                            for (int kp = 0; kp < 2; ++kp) {
+                                const int ky = (y & 1) + 2 * kp, e2 = y - ky;
+                                if (e2 >= 0 && e2 <= 16) {
+                                    const int e = e2 / 2;
+                                    __bf16* cs = s16 + pl * G::PLANE + G::O_CSEG + ((c * K + ky) * K + kx) * 8;
+                                    *(unsigned short*)(e < 8 ? cs + e : cs + G::CSEG) = v;
+                                }
+                            }
+                        }
+                    } else {
+#pragma unroll
+                        for (int kx = 0; kx < K; ++kx) {
+                            uint32_t v[4];
+#pragma unroll
+                            for (int k = 0; k < 4; ++k) {
+                                const int x0 = 2 * k + kx, x1 = x0 + 1;
+                                v[k] = (x0 < IH ? hb[x0][pl] : 0u) | ((x1 < IH ? hb[x1][pl] : 0u) << 16);
+                            }
+                            *(uint4*)(seg + kx * 8) = uint4{v[0], v[1], v[2], v[3]};
+                        }
+                    }
+                }
+            }
+        }
+    };
+
+    if (j_lo < j_hi) fetch(j_lo);
+    for (int j = j_lo; j < j_hi; ++j) {
+        __syncthreads();  // the zero fill, or the previous sample's reads, are done
+        stage();
+        __syncthreads();
+        if (j + 1 < j_hi) fetch(j + 1);
+        if (part == 0 && t < G::COUT) {
+#pragma unroll
+            for (int oy = 0; oy < OH; ++oy) bsum += s_bs[t * OH + oy];
+        }
+#pragma unroll
+        for (int st = 0; st < G::STEPS; ++st) {
+            bf16x8 a[3][2];
+#pragma unroll
+            for (int pl = 0; pl < 3; ++pl)
+#pragma unroll
+                for (int m = 0; m < 2; ++m) a[pl][m] = *(const bf16x8*)(s16 + pl * G::PLANE + arow[m] + 32 * st);
+#pragma unroll
+            for (int i = 0; i < G::NPW; ++i) {
+                bf16x8 b[3];
+#pragma unroll
+                for (int pl = 0; pl < 3; ++pl) b[pl] = *(const bf16x8*)(s16 + pl * G::PLANE + boff(4 * st + g, i));
+                // the six plane pairs (dz plane, input plane), smallest first
+                constexpr int PA[6] = {2, 1, 0, 1, 0, 0}, PB[6] = {0, 1, 2, 0, 1, 0};
+#pragma unroll
+                for (int q = 0; q < 6; ++q)
+#pragma unroll
+                    for (int m = 0; m < 2; ++m) acc[m][i] = mfma16x16x32bf16(a[PA[q]][m], b[PB[q]], acc[m][i]);
+            }
+        }
+    }
+
+    // D[4g + r][li] of tile (m, i): channel (2mh + m)*16 + 4g + r, column c0*KK + (ng*NPW + i)*16 + li
+    if (j_lo >= j_hi) return;  // uniform; padding slot of nothing
+    float* wp = p.wpart + (size_t)slot * G::COUT * G::KTF + c0 * G::KK;
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int i = 0; i < G::NPW; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                wp[(size_t)((2 * mh + m) * 16 + 4 * g + r) * G::KTF + (ng * G::NPW + i) * 16 + li] = acc[m][i][r];
+    if (part == 0 && t < G::COUT) p.bpart[(size_t)slot * G::COUT + t] = bsum;
+}
+
 // Up to 256 samples: two samples per slot, a slot's two workgroups taking
 // half of the output channels each; above, one workgroup per slot and
 // enough samples per slot that there are at most 256 slots.
@@ -463,14 +722,32 @@ constexpr bool kSplitConv2 = false, kSplitConv3 = true;   // layers whose slots 
 int wgrad_reg_ms(int cin, int n) { return n <= 256 && (cin == 32 ? kSplitConv2 : kSplitConv3) ? 2 : 1; }
 int wgrad_reg_spg(int cin, int n) { return wgrad_reg_ms(cin, n) == 2 ? 2 : std::max(1, (n + 255) / 256); }
 
+// The float32 six-product kernel: from kWgradX6MinRows samples; conv2's
+// slots of two workgroups; enough samples per slot for about 256
+// workgroups.
+constexpr int kWgradX6MinRows = 512;
+bool wgrad_x6(bool bf16, int n) { return !bf16 && n >= kWgradX6MinRows; }
+int wgrad_x6_nsplit(int cin) { return cin == 32 ? 2 : 1; }
+int wgrad_x6_spg(int cin, int n) { return std::max(1, (n * wgrad_x6_nsplit(cin) + 255) / 256); }
+
 template <int CIN, int IH, int K, int S, int OH>
 hipError_t wgrad_reg_launch(const float* in, const float* dz, int n, float* wpart, float* bpart, bool bf16,
                             bool in16, hipStream_t st) {
     using G = WgradGeom<CIN, IH, K, S, OH>;
     if (n <= 0) return hipErrorInvalidValue;
+    if (in16 && !bf16) return hipErrorInvalidValue;
+    if (wgrad_x6(bf16, n)) {
+        constexpr int NS = CIN == 32 ? 2 : 1;
+        using XG = SegX6Geom<CIN, IH, K, S, OH, NS>;
+        const int spg = wgrad_x6_spg(CIN, n);
+        const WgradRegParams prm{in, dz, wpart, bpart, n, spg};
+        auto kern = conv_wgrad_seg_x6_kernel<CIN, IH, K, S, OH, NS>;
+        if (!allow_lds((const void*)kern, XG::LDS)) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(kern, dim3((unsigned)((n + spg - 1) / spg * NS)), dim3(WR_WG), XG::LDS, st, prm);
+        return hipGetLastError();
+    }
     const int spg = wgrad_reg_spg(CIN, n), ms = wgrad_reg_ms(CIN, n);
     const int blocks = (n + spg - 1) / spg * ms;
-    if (in16 && !bf16) return hipErrorInvalidValue;
     const WgradRegParams prm{in, dz, wpart, bpart, n, spg};
     constexpr size_t lds = (size_t)G::LDS * 4;
     auto go = [&](auto kern) -> hipError_t {
@@ -496,9 +773,10 @@ hipError_t wgrad_reg_launch(const float* in, const float* dz, int n, float* wpar
 
 }  // namespace
 
-int conv_wgrad_reg_slots(ConvId id, int n) {
+int conv_wgrad_reg_slots(ConvId id, int n, bool bf16) {
     if (id != CONV_L2 && id != CONV_L3) return -1;
-    const int spg = wgrad_reg_spg(id == CONV_L2 ? 32 : 64, n);
+    const int cin = id == CONV_L2 ? 32 : 64;
+    const int spg = wgrad_x6(bf16, n) ? wgrad_x6_spg(cin, n) : wgrad_reg_spg(cin, n);
     return (n + spg - 1) / spg;
 }
 
