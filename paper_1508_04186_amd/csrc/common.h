@@ -333,7 +333,7 @@ hipError_t launch_fwd_x6_pack(const float* w2a, const float* w3a, const float* w
 
 // Weight/bias gradient partial sums of CONV_L2 or CONV_L3 for n samples, one
 // workgroup per run of samples holding its outputs in registers (in float32
-// from 512 samples, two workgroups per conv2 slot, each over half of the
+// from 256 samples, two workgroups per conv2 slot, each over half of the
 // input channels): conv_wgrad_reg_slots(id, n, bf16) slots of wpart
 // [slots][64][cin*k*k] and bpart [slots][64].  in: the layer input
 // [n][cin][ih][iw] (floats, or bfloat16 values when in16).

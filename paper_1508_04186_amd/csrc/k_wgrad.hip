@@ -22,8 +22,8 @@
 // step s), or the bf16-input variant (pixel 32s + 4e + g in element e).
 // Below, the kernels that stage row segments (every MFMA operand one
 // 16-byte LDS read): the bf16-input variant's with bfloat16 activations, and
-// the float32 one from 512 samples on bf16 MFMA with the exact three-plane
-// split (batch 2,048: conv2 108.6 -> 96.2 us, conv3 73.0 -> 49.3 us).
+// the float32 one from 256 samples on bf16 MFMA with the exact three-plane
+// split (batch 2,048: conv2 108.6 -> 90.6 us, conv3 73.0 -> 49.3 us).
 #include <algorithm>
 #include <type_traits>
 
@@ -687,17 +687,37 @@ __global__ __launch_bounds__(WR_WG) void conv_wgrad_seg_x6_kernel(WgradRegParams
             for (int pl = 0; pl < 3; ++pl)
 #pragma unroll
                 for (int m = 0; m < 2; ++m) a[pl][m] = *(const bf16x8*)(s16 + pl * G::PLANE + arow[m] + 32 * st);
+            // the six plane pairs (dz plane, input plane), smallest first
+            constexpr int PA[6] = {2, 1, 0, 1, 0, 0}, PB[6] = {0, 1, 2, 0, 1, 0};
+            if constexpr (G::NPW <= 4) {
+                // each pair over every tile: 2 NPW independent chains between dependent MFMAs
+                // (conv2, batch 2,048: 94.8 -> 90.6 us; conv3's nine N-tiles so took 256
+                // VGPRs and 48.8 -> 50.0 us)
+                bf16x8 b[3][G::NPW];
 #pragma unroll
-            for (int i = 0; i < G::NPW; ++i) {
-                bf16x8 b[3];
+                for (int pl = 0; pl < 3; ++pl)
 #pragma unroll
-                for (int pl = 0; pl < 3; ++pl) b[pl] = *(const bf16x8*)(s16 + pl * G::PLANE + boff(4 * st + g, i));
-                // the six plane pairs (dz plane, input plane), smallest first
-                constexpr int PA[6] = {2, 1, 0, 1, 0, 0}, PB[6] = {0, 1, 2, 0, 1, 0};
+                    for (int i = 0; i < G::NPW; ++i)
+                        b[pl][i] = *(const bf16x8*)(s16 + pl * G::PLANE + boff(4 * st + g, i));
 #pragma unroll
                 for (int q = 0; q < 6; ++q)
 #pragma unroll
-                    for (int m = 0; m < 2; ++m) acc[m][i] = mfma16x16x32bf16(a[PA[q]][m], b[PB[q]], acc[m][i]);
+                    for (int i = 0; i < G::NPW; ++i)
+#pragma unroll
+                        for (int m = 0; m < 2; ++m)
+                            acc[m][i] = mfma16x16x32bf16(a[PA[q]][m], b[PB[q]][i], acc[m][i]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < G::NPW; ++i) {
+                    bf16x8 b[3];
+#pragma unroll
+                    for (int pl = 0; pl < 3; ++pl)
+                        b[pl] = *(const bf16x8*)(s16 + pl * G::PLANE + boff(4 * st + g, i));
+#pragma unroll
+                    for (int q = 0; q < 6; ++q)
+#pragma unroll
+                        for (int m = 0; m < 2; ++m) acc[m][i] = mfma16x16x32bf16(a[PA[q]][m], b[PB[q]], acc[m][i]);
+                }
             }
         }
     }
@@ -724,8 +744,9 @@ int wgrad_reg_spg(int cin, int n) { return wgrad_reg_ms(cin, n) == 2 ? 2 : std::
 
 // The float32 six-product kernel: from kWgradX6MinRows samples; conv2's
 // slots of two workgroups; enough samples per slot for about 256
-// workgroups.
-constexpr int kWgradX6MinRows = 512;
+// workgroups.  (At batch 256: conv2 19.6 -> 15.1 us, conv3 14.7 -> 12.1 us,
+// the finalize +1.8 us for conv3's 256 slots instead of 128.)
+constexpr int kWgradX6MinRows = 256;
 bool wgrad_x6(bool bf16, int n) { return !bf16 && n >= kWgradX6MinRows; }
 int wgrad_x6_nsplit(int cin) { return cin == 32 ? 2 : 1; }
 int wgrad_x6_spg(int cin, int n) { return std::max(1, (n * wgrad_x6_nsplit(cin) + 255) / 256); }

@@ -1,6 +1,6 @@
-"""GPU parity at the full workload sizes: the large Q-network at batch 256
-and 2,048 (TD gradient), the small one at batch 700 (its large-batch launch
-shapes), and an 8,192-state epsilon-greedy forward pass whose Q values and
+"""GPU parity at the full workload sizes: the large Q-network at batch 256,
+517 and 2,048 (TD gradient), the small one at batch 700 (its large-batch
+launch shapes), and an 8,192-state epsilon-greedy forward pass whose Q values and
 actions are compared with the oracle on a 1,024-state sample.
 
 TD batches are drawn from transitions whose forward pass keeps every ReLU
@@ -36,9 +36,11 @@ def _run_td(dev, net, th, tt, s, sn, a, r, t, gamma):
     return host(g), float(host(loss)[0]), host(q), host(y)
 
 
+# large 517: ragged weight-gradient slots (the float32 six-product kernels:
+# conv2 slots of 5 samples, the last of 2; conv3 slots of 3, the last of 1)
 @pytest.mark.parametrize("name,B,target", [("small", 700, "same"), ("small", 1024, "held"),
                                            ("large", 131, "held"), ("large", 256, "held"),
-                                           ("large", 2048, "same")])
+                                           ("large", 517, "held"), ("large", 2048, "same")])
 def test_td_gradient_full_size(dev, name, B, target):
     net, shape = (dq.NET_SMALL, di.NET_S) if name == "small" else (dq.NET_LARGE, di.NET_L)
     size = 4 * B + 10
