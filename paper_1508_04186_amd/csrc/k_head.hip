@@ -680,18 +680,21 @@ __global__ __launch_bounds__(256) void sample_partials_kernel(FinalizeArgs a) {
             slot[(k < A ? (int64_t)k * a.H : (int64_t)A * a.H) + h] = v;
         }
     } else if (w == 1 && blockIdx.x == 0) {
+        // the A fc2 bias sums and the loss (slot entries A*H + H + i, i <= A)
+        // by halving over the wave: the same butterfly order per value as
+        // A + 1 wave sums, in 22 shuffles instead of 114 (batch 256: this
+        // kernel 7.9 us, most of it the chain of wave sums)
         const int j = j0 + lane;
         const bool v = lane < SP_CHUNK && j < j1;
         const int act = v ? clamp_action(a.action[j], A) : -1;
         const float d = v ? a.delta[j] : 0.f;
-        const float l = v ? a.lossj[j] : 0.f;
+        float vals[A + 1];
 #pragma unroll
-        for (int k = 0; k < A; ++k) {
-            const float t = wave_sum(act == k ? d : 0.f);
-            if (lane == 0) slot[(int64_t)A * a.H + a.H + k] = t;
-        }
-        const float t = wave_sum(l);
-        if (lane == 0) slot[count - 1] = t;
+        for (int k = 0; k < A; ++k) vals[k] = act == k ? d : 0.f;
+        vals[A] = v ? a.lossj[j] : 0.f;
+        const float t = halving_step<A + 1, 32>(vals, lane);
+        const int i = halving_index<A + 1>(lane);
+        if (i >= 0) slot[(int64_t)A * a.H + a.H + i] = t;
     }
 }
 
