@@ -982,14 +982,16 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
             }
         }
     };
-    float bs[RPW];
-#pragma unroll
-    for (int q = 0; q < RPW; ++q) bs[q] = 0.f;
+    // bias sum of row wave * RPW + halving_index<RPW>(lane) (where that is >= 0):
+    // the RPW rows' wave sums by halving, in each value's wave_sum order
+    float bs = 0.f;
     auto stage = [&]() {
+        float parts[RPW];
 #pragma unroll
         for (int q = 0; q < RPW; ++q) {
             const int o = wave * RPW + q;
-            float part = 0.f;
+            float& part = parts[q];
+            part = 0.f;
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int ch = lane + 64 * h;
@@ -1015,8 +1017,8 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
                     }
                 }
             }
-            if constexpr (!DZ16) bs[q] += wave_sum(part);
         }
+        if constexpr (!DZ16) bs += halving_step<RPW, 32>(parts, lane);
         // phase word (row, kx, block qb) = bytes 16 qb + 4e + kx, e < 4, of the row
 #pragma unroll
         for (int u = 0; u < UW_IPER; ++u) {
@@ -1122,9 +1124,9 @@ __global__ __launch_bounds__(UW_WG) void conv1_u8_wgrad_kernel(U8WgradParams p) 
 #pragma unroll
             for (int r = 0; r < 4; ++r)
                 wp[(size_t)(m * 16 + 4 * g + r) * KW1 + (2 * wave + n) * 16 + li] = acc[m][n][r] * p.in_scale;
-    if (!DZ16 && lane == 0) {
-#pragma unroll
-        for (int q = 0; q < RPW; ++q) p.bpart[(size_t)blockIdx.x * COUT + wave * RPW + q] = bs[q];
+    if constexpr (!DZ16) {
+        const int bi = halving_index<RPW>(lane);
+        if (bi >= 0) p.bpart[(size_t)blockIdx.x * COUT + wave * RPW + bi] = bs;
     }
 }
 

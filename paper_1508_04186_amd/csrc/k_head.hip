@@ -38,47 +38,6 @@ __device__ __forceinline__ float sum_strided_x8(const float* __restrict__ x, int
     return t;
 }
 
-// Sums over the 64 lanes of a wave of N values per lane, by halving: at
-// the step with lane mask M every lane keeps half of its current list (the
-// lower half if its bit M is clear, else the upper half, padded with zeros)
-// and adds the partner lane's copy of that half.  Each value is summed over
-// the lanes in the same butterfly order as wave_sum (xor 32, 16, ..., 1),
-// with at most N + 6 shuffles in all instead of 6N.  Lane l ends with the sum of
-// value halving_index<N>(l), or of padding where that is -1.
-template <int N, int M>
-__device__ __forceinline__ float halving_step(const float* v, int lane) {
-    if constexpr (M == 0) {
-        return v[0];
-    } else {
-        constexpr int H = (N + 1) / 2;
-        const bool up = (lane & M) != 0;
-        float w[H];
-#pragma unroll
-        for (int i = 0; i < H; ++i) {
-            const float lo = v[i];
-            const float hi = H + i < N ? v[H + i] : 0.f;
-            w[i] = (up ? hi : lo) + __shfl_xor(up ? lo : hi, M, 64);
-        }
-        return halving_step<H, M / 2>(w, lane);
-    }
-}
-
-template <int N>
-__device__ __forceinline__ int halving_index(int lane) {
-    int n = N, base = 0, real = N;
-    for (int m = 32; m >= 1; m >>= 1) {
-        const int h = (n + 1) / 2;
-        if (lane & m) {
-            base += h;
-            real = real > h ? real - h : 0;
-        } else {
-            real = real < h ? real : h;
-        }
-        n = h;
-    }
-    return real > 0 ? base : -1;
-}
-
 // Block-wide sums of NV per-thread values; every thread gets the results.
 // Wave sums first (by halving: per value the butterfly order of wave_sum,
 // NV + 6 shuffles instead of 6 NV; batch 32, head 6.8 us, most of it the
