@@ -290,17 +290,6 @@ namespace {
         prof_end((kid), st);                            \
     } while (0)
 
-// The per-lane weight copies of a large-network TD step: the input
-// gradients' (r, when set) and the fp32 forward's planes (fwd).
-hipError_t repack_weights(const WeightRepack* r, bool fwd, const float* w2a, const float* w3a, const float* w2b,
-                          const float* w3b, float* const fpk[2][2], hipStream_t st) {
-    if (r) {
-        const hipError_t e = launch_weight_repack(*r, st);
-        if (e != hipSuccess) return e;
-    }
-    if (fwd) return launch_fwd_x6_pack(w2a, w3a, w2b, w3b, fpk[0][0], fpk[1][0], fpk[0][1], fpk[1][1], st);
-    return hipSuccess;
-}
 
 // Where a TD step's transitions come from: dense device buffers, or replay
 // records and side arrays addressed by an index array.
@@ -377,7 +366,8 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
     const bool repack = L == 3 && phase_dgrad(CONV_L2, B, ni.bf16);
     if (repack_fwd || repack || fwd16) {
         WeightRepack r{th + ni.w_off[1], th + ni.w_off[2], nullptr, nullptr, nullptr, nullptr,
-                       tt + ni.w_off[1], tt + ni.w_off[2], nullptr, nullptr, nullptr, nullptr};
+                       tt + ni.w_off[1], tt + ni.w_off[2], nullptr, nullptr, nullptr, nullptr,
+                       nullptr, nullptr, nullptr, nullptr};
         if (repack && ni.bf16) {
             r.h2 = t.wpk2;
             r.h3 = t.wpk3;
@@ -391,8 +381,13 @@ int td_gradient_impl(const dqn_net* net, const NetInfo& ni, const float* theta,
             r.f2b = t.fpk[0][1];
             r.f3b = t.fpk[1][1];
         }
-        RUN(DQN_K_WEIGHT_REPACK, repack_weights(repack || fwd16 ? &r : nullptr, repack_fwd, th + ni.w_off[1],
-                                                th + ni.w_off[2], tt + ni.w_off[1], tt + ni.w_off[2], t.fpk, st));
+        if (repack_fwd) {
+            r.p2a = t.fpk[0][0];
+            r.p3a = t.fpk[1][0];
+            r.p2b = t.fpk[0][1];
+            r.p3b = t.fpk[1][1];
+        }
+        RUN(DQN_K_WEIGHT_REPACK, launch_weight_repack(r, st));   // (every copy in one launch)
     }
 
     // Forward of s under theta (samples 0..B-1) and of s' under theta^-

@@ -361,16 +361,49 @@ struct WeightRepack {
     // kernel: the first plane of the float32 forward's copies (same layout).
     const float *w2b, *w3b;
     void *f2a, *f3a, *f2b, *f3b;
+    // The float32 forward's weights of both sets as the three exact bf16
+    // planes in the per-lane order of its kernel (X6FwdPack below;
+    // fwd_x6_pack_floats(id) floats each), or NULL.
+    void *p2a, *p3a, *p2b, *p3b;
 };
 int64_t weight_repack_floats(ConvId id);
+// One launch writes every copy whose output is set (16-byte aligned).
 hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st);
-// The float32 forward's weights of conv2 and conv3 for two weight sets (a:
-// theta, b: theta^-) as the three exact bf16 planes in the per-lane order of
-// the forward kernel (fwd_x6_pack_floats(id) floats each, 16-byte aligned);
-// NULL outputs are skipped.
 int64_t fwd_x6_pack_floats(ConvId id);
-hipError_t launch_fwd_x6_pack(const float* w2a, const float* w3a, const float* w2b, const float* w3b, float* x2a,
-                              float* x3a, float* x2b, float* x3b, hipStream_t st);
+
+// The float32 forward's conv2/conv3 weights as the three exact bf16 planes,
+// in the order that forward's lanes load them: vector
+// index(pl, nt, kh, s, lane) of plane pl holds, for lane (li, g) of the wave
+// owning output channels 16 nt .. 16 nt + 15 and k-step ks = kh KSH + s
+// (tap ks / CH, input channels from 32 (ks % CH)), the values
+// W[16 nt + li][32 (ks % CH) + 8 g + q][tap], q = 0..7 (CH = cin / 32,
+// KSH = taps * CH / 2).
+template <int CIN, int KK>
+struct X6FwdPack {
+    static constexpr int CH = CIN / 32, KS = KK * CH, KSH = KS / 2;
+    static constexpr int VECS = 3 * 4 * KS * 64;   // bf16x8 vectors of the three planes
+    __host__ __device__ static constexpr int index(int pl, int nt, int kh, int s, int lane) {
+        return (((pl * 4 + nt) * 2 + kh) * KSH + s) * 64 + lane;
+    }
+};
+// Vector e of that layout from W[cout][cin][taps] (nothing when out is NULL).
+template <int CIN, int KK>
+__device__ __forceinline__ void x6_fwd_pack_job(const float* __restrict__ w, void* out, int e) {
+    using X = X6FwdPack<CIN, KK>;
+    if (!out || e >= X::VECS) return;
+    const int lane = e & 63, r = e >> 6;
+    const int s = r % X::KSH, kh = (r / X::KSH) & 1, nt = (r / (2 * X::KSH)) & 3, pl = r / (8 * X::KSH);
+    const int li = lane & 15, g = lane >> 4;
+    const int ks = kh * X::KSH + s, tap = ks / X::CH, cb = ks % X::CH;
+    bf16x8 o;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        __bf16 a, b, d;
+        split3(w[(size_t)(16 * nt + li) * CIN * KK + (size_t)(32 * cb + 8 * g + q) * KK + tap], a, b, d);
+        o[q] = pl == 0 ? a : pl == 1 ? b : d;
+    }
+    ((bf16x8*)out)[e] = o;
+}
 
 // Weight/bias gradient partial sums of CONV_L2 or CONV_L3 for n samples, one
 // workgroup per run of samples holding its outputs in registers (in float32

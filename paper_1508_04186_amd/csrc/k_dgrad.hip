@@ -703,7 +703,9 @@ __global__ __launch_bounds__(D2_WG) void conv3_dgrad_x6_kernel(Dgrad2Params p) {
 // output skips it.  Jobs 4 to 7: the bf16-input forward's weights of
 // conv2 and conv3 for both weight sets, vector (nt KS + ks) 64 + lane
 // holding W[16nt + li][32 (ks % CH) + 8g + q][ks / CH] rounded (CH = cin /
-// 32, KS = taps * CH), as its kernel reads them.
+// 32, KS = taps * CH), as its kernel reads them.  Jobs 8 to 11: the float32
+// forward's three planes of the same weights (X6FwdPack), in the same
+// launch (a launch of its own had cost 4.4 us at batch 2,048).
 template <int CIN, int KK>
 __device__ __forceinline__ void fwd_bf16_pack_job(const float* w, void* out, int e) {
     constexpr int CH = CIN / 32, KS = KK * CH;
@@ -725,7 +727,11 @@ __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
             case 4: fwd_bf16_pack_job<D2_CIN, D2_K * D2_K>(r.w2a, r.f2a, e); break;
             case 5: fwd_bf16_pack_job<D3_CIN, D3_K * D3_K>(r.w3a, r.f3a, e); break;
             case 6: fwd_bf16_pack_job<D2_CIN, D2_K * D2_K>(r.w2b, r.f2b, e); break;
-            default: fwd_bf16_pack_job<D3_CIN, D3_K * D3_K>(r.w3b, r.f3b, e); break;
+            case 7: fwd_bf16_pack_job<D3_CIN, D3_K * D3_K>(r.w3b, r.f3b, e); break;
+            case 8: x6_fwd_pack_job<D2_CIN, D2_K * D2_K>(r.w2a, r.p2a, e); break;
+            case 9: x6_fwd_pack_job<D3_CIN, D3_K * D3_K>(r.w3a, r.p3a, e); break;
+            case 10: x6_fwd_pack_job<D2_CIN, D2_K * D2_K>(r.w2b, r.p2b, e); break;
+            default: x6_fwd_pack_job<D3_CIN, D3_K * D3_K>(r.w3b, r.p3b, e); break;
         }
         return;
     }
@@ -800,13 +806,17 @@ __global__ __launch_bounds__(256) void weight_repack_kernel(WeightRepack r) {
 int64_t weight_repack_floats(ConvId id) { return id == CONV_L2 ? 4 * 3 * 8 * X2_KS * 64 : 4 * 3 * 4 * X3_KS * 64; }
 
 hipError_t launch_weight_repack(const WeightRepack& r, hipStream_t st) {
-    for (const void* q : {r.h2, r.h3, r.x2, r.x3, r.f2a, r.f3a, r.f2b, r.f3b})
+    for (const void* q : {r.h2, r.h3, r.x2, r.x3, r.f2a, r.f3a, r.f2b, r.f3b, r.p2a, r.p3a, r.p2b, r.p3b})
         if ((uintptr_t)q & 15) return hipErrorInvalidValue;
-    if ((r.f2b && !r.w2b) || (r.f3b && !r.w3b)) return hipErrorInvalidValue;
+    if ((r.f2b && !r.w2b) || (r.f3b && !r.w3b) || (r.p2b && !r.w2b) || (r.p3b && !r.w3b)) return hipErrorInvalidValue;
     // every copy has at most 3 * 4 * 18 * 64 = 13,824 vectors; the forward's
     // jobs only when one of their outputs is set
+    static_assert(X6FwdPack<D2_CIN, D2_K * D2_K>::VECS <= 13824 && X6FwdPack<D3_CIN, D3_K * D3_K>::VECS <= 13824 &&
+                      3 * 8 * X2_KS * 64 <= 13824 && 3 * 4 * X3_KS * 64 <= 13824,
+                  "copies within the grid");
+    const bool x6 = r.p2a || r.p3a || r.p2b || r.p3b;
     const bool fwd = r.f2a || r.f3a || r.f2b || r.f3b;
-    hipLaunchKernelGGL(weight_repack_kernel, dim3(13824 / 256, fwd ? 8 : 4), dim3(256), 0, st, r);
+    hipLaunchKernelGGL(weight_repack_kernel, dim3(13824 / 256, x6 ? 12 : fwd ? 8 : 4), dim3(256), 0, st, r);
     return hipGetLastError();
 }
 

@@ -68,7 +68,7 @@ struct FwdClParams {
     float* out;                // [n][64][oh][oh] (bfloat16 values when out16)
     const float *w_a, *b_a, *w_b, *b_b;
     int n, n_a, g_a, spg;      // blocks [0, g_a) take samples [0, n_a), the rest [n_a, n); runs of spg
-    const float *wpk_a, *wpk_b;  // w_a, w_b in per-lane order (fwd_x6_pack, or weight_repack's bf16 jobs), or NULL
+    const float *wpk_a, *wpk_b;  // w_a, w_b in per-lane order (weight_repack's forward jobs), or NULL
 };
 
 // PK: the weights from wpk_a / wpk_b (weight_repack: per-lane order, rounded)
@@ -355,7 +355,6 @@ struct FwdX6Geom {
     static constexpr int OUTF = COUT * P;
     static constexpr int PART = 4 * MT * 64 * 16;       // half-sums of the kh = 1 waves (bytes)
     static constexpr int LDS = 3 * PLANE;
-    static constexpr int PACK = 3 * 4 * KS * 64;        // bf16x8 vectors of the repacked planes
     static_assert(KS % 2 == 0 && CIN % 32 == 0 && PSB % 16 == 0 && (PSB / 16) % 2 == 1 && OUTF % 4 == 0, "geometry");
     static_assert(S == 1 || (S == 2 && IH % 2 == 0 && IH / 2 <= RP), "stride-phase layout");
     static_assert(RP >= IH && (RP - OH) % 16 == 0, "row pitch");
@@ -366,11 +365,6 @@ struct FwdX6Geom {
     }
 };
 
-template <int CIN, int IH, int K, int S, int OH>
-__device__ __forceinline__ int x6_pack_index(int p, int nt, int kh, int s, int lane) {
-    using G = FwdX6Geom<CIN, IH, K, S, OH>;
-    return (((p * 4 + nt) * 2 + kh) * G::KSH + s) * 64 + lane;
-}
 
 template <int CIN, int IH, int K, int S, int OH, bool PK>   // PK: weight planes from wpk_a / wpk_b
 __global__ __launch_bounds__(FC_WG) void conv_fwd_x6_kernel(FwdClParams p) {
@@ -440,7 +434,7 @@ __global__ __launch_bounds__(FC_WG) void conv_fwd_x6_kernel(FwdClParams p) {
 #pragma unroll
         for (int pl = 0; pl < 3; ++pl)
 #pragma unroll
-            for (int s = 0; s < G::KSH; ++s) wv[pl][s] = wp[x6_pack_index<CIN, IH, K, S, OH>(pl, nt, kh, s, lane)];
+            for (int s = 0; s < G::KSH; ++s) wv[pl][s] = wp[X6FwdPack<CIN, G::KK>::index(pl, nt, kh, s, lane)];
     } else {
         const float* __restrict__ W = second ? p.w_b : p.w_a;
         const float* wr = W + (size_t)(16 * nt + li) * CIN * G::KK;
@@ -551,26 +545,6 @@ hipError_t fwd_x6_launch(const float* in, int n_a, int n, const float* w_a, cons
     return pk_a ? go(conv_fwd_x6_kernel<CIN, IH, K, S, OH, true>) : go(conv_fwd_x6_kernel<CIN, IH, K, S, OH, false>);
 }
 
-// The repacked weight planes of the float32 forward (job jb of the repack
-// launch: one bf16x8 vector per thread e, e < 3 * 4 * KS * 64).
-template <int CIN, int IH, int K, int S, int OH>
-__device__ __forceinline__ void x6_pack_job(const float* __restrict__ w, bf16x8* out, int e) {
-    using G = FwdX6Geom<CIN, IH, K, S, OH>;
-    if (e >= G::PACK) return;
-    const int lane = e & 63, r = e >> 6;
-    const int s = r % G::KSH, kh = (r / G::KSH) & 1, nt = (r / (2 * G::KSH)) & 3, pl = r / (8 * G::KSH);
-    const int li = lane & 15, g = lane >> 4;
-    const int ks = kh * G::KSH + s, tap = ks / G::CH, cb = ks % G::CH;
-    bf16x8 o;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        __bf16 a, b, c;
-        split3(w[(size_t)(16 * nt + li) * CIN * G::KK + (size_t)(32 * cb + 8 * g + q) * G::KK + tap], a, b, c);
-        o[q] = pl == 0 ? a : pl == 1 ? b : c;
-    }
-    out[e] = o;
-}
-
 }  // namespace
 
 bool conv_fwd_cl_use(ConvId id, int n, bool bf16) {
@@ -594,31 +568,10 @@ hipError_t launch_conv_fwd_cl(ConvId id, const float* in, int n_a, int n, const 
     }
 }
 
-__global__ __launch_bounds__(256) void fwd_x6_pack_kernel(const float* w2a, const float* w3a, const float* w2b,
-                                                          const float* w3b, void* x2a, void* x3a, void* x2b,
-                                                          void* x3b) {
-    const int e = blockIdx.x * 256 + threadIdx.x;
-    switch (blockIdx.y) {
-        case 0: if (x2a) x6_pack_job<32, 20, 4, 2, 9>(w2a, (bf16x8*)x2a, e); break;
-        case 1: if (x3a) x6_pack_job<64, 9, 3, 1, 7>(w3a, (bf16x8*)x3a, e); break;
-        case 2: if (x2b) x6_pack_job<32, 20, 4, 2, 9>(w2b, (bf16x8*)x2b, e); break;
-        default: if (x3b) x6_pack_job<64, 9, 3, 1, 7>(w3b, (bf16x8*)x3b, e); break;
-    }
-}
-
 int64_t fwd_x6_pack_floats(ConvId id) {
     // bf16x8 vectors (4 floats each) of the three planes
-    return id == CONV_L2 ? 4 * FwdX6Geom<32, 20, 4, 2, 9>::PACK : 4 * FwdX6Geom<64, 9, 3, 1, 7>::PACK;
+    return id == CONV_L2 ? 4 * X6FwdPack<32, 16>::VECS : 4 * X6FwdPack<64, 9>::VECS;
 }
 
-hipError_t launch_fwd_x6_pack(const float* w2a, const float* w3a, const float* w2b, const float* w3b, float* x2a,
-                              float* x3a, float* x2b, float* x3b, hipStream_t st) {
-    for (const float* q : {(const float*)x2a, (const float*)x3a, (const float*)x2b, (const float*)x3b})
-        if ((uintptr_t)q & 15) return hipErrorInvalidValue;
-    constexpr int MAXV = FwdX6Geom<64, 9, 3, 1, 7>::PACK;   // the larger of the two layers
-    hipLaunchKernelGGL(fwd_x6_pack_kernel, dim3((MAXV + 255) / 256, 4), dim3(256), 0, st, w2a, w3a, w2b, w3b, x2a, x3a,
-                       x2b, x3b);
-    return hipGetLastError();
-}
 
 }  // namespace dqn
